@@ -1,0 +1,244 @@
+/*
+ * CPU oracle for the tied-trit-plane integer dot pass (Grella, "Tied Trit-Planes",
+ * 2026). TEST INFRASTRUCTURE ONLY: this file exists so that tests, the smoke check and
+ * the benchmark's CPU-baseline leg can check the HIP path against a plain, slow,
+ * obviously correct definition. No product code may link or call it, and it shares no
+ * code with the HIP library (no headers, helpers, tables or constants).
+ *
+ * Arithmetic rules:
+ *  - integer work (fold, unfold, block dots) is exact, accumulated in int64;
+ *  - the activation quantizer decides integer codes in IEEE fp32 (the precision the
+ *    kernels decide them in; the paper fixes none): correctly rounded division and
+ *    multiplication, round-half-to-even, no fused multiply-add (build with
+ *    -ffp-contract=off);
+ *  - the scale combine is evaluated in fp64.
+ *
+ * Pins (tests/oracle_pins.py; every function below has at least one, none re-derives
+ * the function's own formula, and tests/test_oracle_mutants.py checks that planted
+ * mistakes in each function are caught):
+ *   orc_fold/orc_unfold ..... the paper's fold table (golden fixture), bijection onto
+ *                             -4..4, round trip, equality with the tied two-plane model
+ *   orc_two_plane_dequant ... the paper's level sets for ratios 1, 2, 3, 1/3, -3, 1.7
+ *   orc_f16_to_f64/dequant .. numpy's binary16 decode
+ *   orc_quantize ............ closed forms (amax 127 -> rne(x), amax 254 -> rne(x/2)),
+ *                             amax element -> +-127, error bound, odd symmetry, block
+ *                             independence, pure-Python fp32 brute force
+ *   orc_dot_i8 .............. exhaustive 9^4 four-element code vectors, bound extremes
+ *   orc_gemv ................ trit-plane identity 3(T1.q)+(T2.q), offset form, exact
+ *                             integer products at unit scales, power-of-two scaling,
+ *                             dequantized-matmul error bound, exact rational brute force
+ *   orc_splitmix64_word ..... SplitMix64's published seed-0 outputs
+ *   orc_synth_matrix ........ the written recipe (pure-Python), trit/code/scale
+ *                             distributions
+ * No function here is "parity unpinned". The activation quantizer's block size, scale
+ * rule and rounding are this oracle's reading of a passage that fixes none of them;
+ * the pins fix the reading, not the paper.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+
+#define ORC_OK 0
+#define ORC_BAD_INPUT (-1)
+
+/* ------------------------------------------------------------------------------ */
+/* Fold and unfold (Sec. 2.1, the tied composite equation; Sec. 2.2).              */
+/* With scales tied at alpha = (3s, s), the two trit planes combine into a single    */
+/* code c = 3*t1 + t2, which takes the nine values -4..4.                            */
+/* ------------------------------------------------------------------------------ */
+
+int orc_fold(const int8_t* t1, const int8_t* t2, int64_t n, int8_t* c) {
+  for (int64_t i = 0; i < n; ++i) {
+    if (t1[i] < -1 || t1[i] > 1 || t2[i] < -1 || t2[i] > 1) return ORC_BAD_INPUT;
+    c[i] = (int8_t)(3 * t1[i] + t2[i]);
+  }
+  return ORC_OK;
+}
+
+/* Inverse of the fold: balanced-ternary digits of c in -4..4.
+ * t1 = floor((c + 4) / 3) - 1 and t2 = c - 3*t1. */
+int orc_unfold(const int8_t* c, int64_t n, int8_t* t1, int8_t* t2) {
+  for (int64_t i = 0; i < n; ++i) {
+    int v = c[i];
+    if (v < -4 || v > 4) return ORC_BAD_INPUT;
+    int a = (v + 4) / 3 - 1; /* v + 4 >= 0, so C division is floor */
+    t1[i] = (int8_t)a;
+    t2[i] = (int8_t)(v - 3 * a);
+  }
+  return ORC_OK;
+}
+
+/* PTQTP's two-plane reconstruction alpha1*T1 + alpha2*T2 (Sec. 2.1, first
+ * paragraph), in fp64, for the free-scale model the tie constrains. */
+int orc_two_plane_dequant(const int8_t* t1, const int8_t* t2, int64_t n, double alpha1,
+                          double alpha2, double* w) {
+  for (int64_t i = 0; i < n; ++i) {
+    if (t1[i] < -1 || t1[i] > 1 || t2[i] < -1 || t2[i] > 1) return ORC_BAD_INPUT;
+    w[i] = alpha1 * (double)t1[i] + alpha2 * (double)t2[i];
+  }
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------------ */
+/* IEEE 754 binary16 decode. The tied scale s is serialized as f16 (Sec. 2.1,     */
+/* "scales serialize to f16"; Sec. 2.2, four f16 column scales per block).          */
+/* 1 sign bit, 5 exponent bits (bias 15), 10 fraction bits.                         */
+/* ------------------------------------------------------------------------------ */
+
+double orc_f16_to_f64(uint16_t h) {
+  int sign = (h >> 15) & 1;
+  int e = (h >> 10) & 0x1F;
+  int f = h & 0x3FF;
+  double v;
+  if (e == 0) {
+    v = ldexp((double)f, -24); /* subnormal: f * 2^-14 / 2^10 */
+  } else if (e == 31) {
+    v = (f == 0) ? INFINITY : NAN;
+  } else {
+    v = ldexp((double)(1024 + f), e - 25); /* (1 + f/1024) * 2^(e-15) */
+  }
+  return sign ? -v : v;
+}
+
+/* Dequantized tied weight W_hat = s * c (Sec. 2.1), row-major [n][k], one scale per
+ * (row, 256-column block). */
+int orc_dequant(const int8_t* c, const uint16_t* s, int64_t n, int64_t k, double* w) {
+  if (k % 256 != 0) return ORC_BAD_INPUT;
+  int64_t kb = k / 256;
+  for (int64_t r = 0; r < n; ++r)
+    for (int64_t i = 0; i < k; ++i)
+      w[r * k + i] = orc_f16_to_f64(s[r * kb + i / 256]) * (double)c[r * k + i];
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------------ */
+/* Block activation quantization (Sec. 2.2: the codes are dotted "against block-    */
+/* quantized activations"). The paper fixes neither block size, scale rule nor      */
+/* rounding; the reading implemented here: blocks of 256 along k (the weight block), */
+/* symmetric absmax scale d = amax/127, codes q = clamp(rne(x * (127/amax)), +-127)  */
+/* in fp32, d kept in fp32, bsum = sum of the block's codes; an all-zero block gives */
+/* d = 0 and q = 0.                                                                  */
+/* ------------------------------------------------------------------------------ */
+
+static int quantize_block(const float* x, int64_t len, int8_t* q, float* d, int32_t* bsum) {
+  float amax = 0.0f;
+  for (int64_t i = 0; i < len; ++i) {
+    if (!isfinite(x[i])) return ORC_BAD_INPUT;
+    float a = fabsf(x[i]);
+    if (a > amax) amax = a;
+  }
+  if (amax == 0.0f) {
+    for (int64_t i = 0; i < len; ++i) q[i] = 0;
+    *d = 0.0f;
+    *bsum = 0;
+    return ORC_OK;
+  }
+  float inv = 127.0f / amax;
+  *d = amax / 127.0f;
+  int32_t s = 0;
+  for (int64_t i = 0; i < len; ++i) {
+    float y = x[i] * inv;       /* one fp32 multiply, rounded to nearest even */
+    float r = rintf(y);         /* round half to even (default rounding mode) */
+    if (r > 127.0f) r = 127.0f;
+    if (r < -127.0f) r = -127.0f;
+    q[i] = (int8_t)r;
+    s += (int32_t)r;
+  }
+  *bsum = s;
+  return ORC_OK;
+}
+
+/* x [t][k] fp32 -> q [t][k] int8, d [t][k/blk] fp32, bsum [t][k/blk] int32. */
+int orc_quantize(const float* x, int64_t t, int64_t k, int64_t blk, int8_t* q, float* d,
+                 int32_t* bsum) {
+  if (blk <= 0 || k % blk != 0) return ORC_BAD_INPUT;
+  int64_t nb = k / blk;
+  for (int64_t tt = 0; tt < t; ++tt)
+    for (int64_t b = 0; b < nb; ++b) {
+      int rc = quantize_block(x + tt * k + b * blk, blk, q + tt * k + b * blk, d + tt * nb + b,
+                              bsum + tt * nb + b);
+      if (rc != ORC_OK) return rc;
+    }
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------------ */
+/* Integer dot (Sec. 2.2: codes dot against the int8 activations with integer SIMD). */
+/* ------------------------------------------------------------------------------ */
+
+int64_t orc_dot_i8(const int8_t* a, const int8_t* b, int64_t n) {
+  int64_t s = 0;
+  for (int64_t i = 0; i < n; ++i) s += (int64_t)a[i] * (int64_t)b[i];
+  return s;
+}
+
+/* ------------------------------------------------------------------------------ */
+/* The serving dot pass (Sec. 2.2): for every token t, output channel r and        */
+/* 256-block b, the exact integer block sum isum = sum_i c[r][256b+i] * q[t][256b+i], */
+/* then one scale multiply-add per block: y[t][r] = sum_b s[r][b] * d[t][b] * isum.  */
+/* Evaluated in fp64 in ascending b; absref[t][r] = sum_b |term| bounds cancellation. */
+/* c: logical codes [n][k] in -4..4; s: f16 bits [n][k/256]; q [t][k]; d [t][k/256].  */
+/* isum (nullable): [t][n][k/256].                                                    */
+/* ------------------------------------------------------------------------------ */
+
+int orc_gemv(const int8_t* c, const uint16_t* s, int64_t n, int64_t k, const int8_t* q,
+             const float* d, int64_t t, double* y, double* absref, int32_t* isum) {
+  if (k % 256 != 0) return ORC_BAD_INPUT;
+  int64_t kb = k / 256;
+  for (int64_t tt = 0; tt < t; ++tt)
+    for (int64_t r = 0; r < n; ++r) {
+      double acc = 0.0, aacc = 0.0;
+      for (int64_t b = 0; b < kb; ++b) {
+        int64_t v = orc_dot_i8(c + r * k + b * 256, q + tt * k + b * 256, 256);
+        if (v > INT32_MAX || v < INT32_MIN) return ORC_BAD_INPUT;
+        if (isum) isum[(tt * n + r) * kb + b] = (int32_t)v;
+        double term = orc_f16_to_f64(s[r * kb + b]) * (double)d[tt * kb + b] * (double)v;
+        acc += term;
+        aacc += fabs(term);
+      }
+      y[tt * n + r] = acc;
+      if (absref) absref[tt * n + r] = aacc;
+    }
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------------ */
+/* Synthetic weight stream (input generation, not the method): SplitMix64 as a     */
+/* counter-based generator (Steele, Lea & Flood 2014), trits by 16-bit multiply-     */
+/* shift, scales uniform over the fp16 patterns in [1e-3, 1e-1]. Written here from    */
+/* the published definition; the HIP side carries its own implementation.            */
+/* ------------------------------------------------------------------------------ */
+
+static uint64_t sm64_word(uint64_t key, uint64_t i) {
+  uint64_t z = key + (i + 1) * 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+uint64_t orc_splitmix64_word(uint64_t key, uint64_t i) { return sm64_word(key, i); }
+
+static int8_t trit16(uint64_t f) { return (int8_t)((int)((f * 3u) >> 16) - 1); }
+
+/* Trit planes and f16 scales of rows [row0, row0 + rows) of an n x k matrix. */
+int orc_synth_matrix(uint64_t key, int64_t n, int64_t k, int64_t row0, int64_t rows,
+                     int8_t* t1, int8_t* t2, uint16_t* s) {
+  if (k % 256 != 0 || row0 < 0 || row0 + rows > n) return ORC_BAD_INPUT;
+  const uint64_t lo = 0x1419, span = 0x2E66 - 0x1419 + 1;
+  int64_t kb = k / 256;
+  for (int64_t r = 0; r < rows; ++r) {
+    for (int64_t col = 0; col < k; ++col) {
+      uint64_t e = (uint64_t)((row0 + r) * k + col);
+      uint64_t w = sm64_word(key, e >> 1);
+      int sh = (e & 1) ? 32 : 0;
+      t1[r * k + col] = trit16((w >> sh) & 0xFFFF);
+      t2[r * k + col] = trit16((w >> (sh + 16)) & 0xFFFF);
+    }
+    for (int64_t b = 0; b < kb; ++b) {
+      uint64_t j = (uint64_t)((row0 + r) * kb + b);
+      uint64_t w = sm64_word(key, (uint64_t)(n * k / 2) + j);
+      s[r * kb + b] = (uint16_t)(lo + (((w >> 32) * span) >> 32));
+    }
+  }
+  return ORC_OK;
+}

@@ -1,0 +1,87 @@
+"""Plant plausible mistakes in copies of the CPU oracle and check the pins catch each.
+
+Every mutant is built from a patched copy of ``oracle/tq_oracle.c`` in a temporary
+directory (or is a Python subclass of the oracle); the committed oracle is untouched.
+A mutant that no pin rejects would mean the pins leave that part of the oracle
+unchecked.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import oracle as oracle_pkg
+from oracle import build as obuild
+from oracle_pins import PINS
+
+SRC = open(obuild.SRC).read()
+
+C_MUTANTS = {
+    "fold_planes_transposed": ("c[i] = (int8_t)(3 * t1[i] + t2[i]);", "c[i] = (int8_t)(t1[i] + 3 * t2[i]);"),
+    "unfold_off_by_one": ("int a = (v + 4) / 3 - 1;", "int a = (v + 3) / 3 - 1;"),
+    "two_plane_alpha_swapped": ("w[i] = alpha1 * (double)t1[i] + alpha2 * (double)t2[i];", "w[i] = alpha2 * (double)t1[i] + alpha1 * (double)t2[i];"),
+    "f16_exponent_bias": ("ldexp((double)(1024 + f), e - 25)", "ldexp((double)(1024 + f), e - 24)"),
+    "f16_subnormal_scale": ("v = ldexp((double)f, -24);", "v = ldexp((double)f, -25);"),
+    "f16_sign_dropped": ("return sign ? -v : v;", "return v;"),
+    "quant_round_half_away": ("float r = rintf(y);", "float r = roundf(y);"),
+    "quant_scale_128": ("float inv = 127.0f / amax;", "float inv = 128.0f / amax;"),
+    "quant_d_128": ("*d = amax / 127.0f;", "*d = amax / 128.0f;"),
+    "quant_signed_max": ("float a = fabsf(x[i]);", "float a = x[i];"),
+    "quant_bsum_sign": ("s += (int32_t)r;", "s -= (int32_t)r;"),
+    "quant_truncate": ("float r = rintf(y);", "float r = truncf(y);"),
+    "quant_block_stride": ("d + tt * nb + b,", "d + b,"),
+    "dot_int8_wrap": ("s += (int64_t)a[i] * (int64_t)b[i];", "s += (int8_t)(a[i] * b[i]);"),
+    "gemv_token_index_dropped": ("q + tt * k + b * 256, 256)", "q + b * 256, 256)"),
+    "gemv_row_index_dropped": ("orc_dot_i8(c + r * k + b * 256,", "orc_dot_i8(c + b * 256,"),
+    "gemv_scale_transposed": ("orc_f16_to_f64(s[r * kb + b])", "orc_f16_to_f64(s[b * n + r])"),
+    "gemv_act_scale_dropped": ("* (double)d[tt * kb + b] * (double)v;", "* (double)v;"),
+    "gemv_block_offset": ("q + tt * k + b * 256, 256)", "q + tt * k + b * 255, 256)"),
+    "gemv_absref_signed": ("aacc += fabs(term);", "aacc += term;"),
+    "synth_field_swap": ("int sh = (e & 1) ? 32 : 0;", "int sh = (e & 1) ? 0 : 32;"),
+    "synth_trit_shift": ("((f * 3u) >> 16) - 1", "((f * 3u) >> 15) - 1"),
+    "synth_scale_counter": ("sm64_word(key, (uint64_t)(n * k / 2) + j)", "sm64_word(key, j)"),
+    "synth_gamma": ("z = key + (i + 1) * 0x9E3779B97F4A7C15ull;", "z = key + i * 0x9E3779B97F4A7C15ull;"),
+}
+
+
+def _first_failure(o):
+    for p in PINS:
+        try:
+            p(o)
+        except Exception as e:  # noqa: BLE001 - any failure kills the mutant
+            return f"{p.__name__}: {type(e).__name__}"
+    return None
+
+
+@pytest.mark.parametrize("name", sorted(C_MUTANTS))
+def test_c_mutant_is_caught(name, tmp_path):
+    old, new = C_MUTANTS[name]
+    assert SRC.count(old) == 1, f"mutation anchor for {name} not unique"
+    src = tmp_path / "mut.c"
+    src.write_text(SRC.replace(old, new))
+    lib = obuild.build(str(src), str(tmp_path / "libmut.so"), werror=False)
+    killed = _first_failure(oracle_pkg.Oracle(lib))
+    assert killed is not None, f"mutant {name} survived every pin"
+
+
+class _SwapGateUp(oracle_pkg.Oracle):
+    def expert_slot(self, ex, x_row):
+        return super().expert_slot({"gate": ex["up"], "up": ex["gate"], "down": ex["down"]}, x_row)
+
+
+class _SiluSign(oracle_pkg.Oracle):
+    @staticmethod
+    def silu(z):
+        z = np.asarray(z, dtype=np.float64)
+        return z / (1.0 + np.exp(z))
+
+
+class _FirstWeightOnly(oracle_pkg.Oracle):
+    def moe(self, x, idx, w, get_expert, tokens=None):
+        w = np.repeat(np.asarray(w)[:, :1], w.shape[1], axis=1)
+        return super().moe(x, idx, w, get_expert, tokens)
+
+
+@pytest.mark.parametrize("cls", [_SwapGateUp, _SiluSign, _FirstWeightOnly], ids=lambda c: c.__name__)
+def test_python_mutant_is_caught(cls):
+    assert _first_failure(cls(oracle_pkg.oracle.DEFAULT_LIB)) is not None
