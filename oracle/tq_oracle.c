@@ -116,8 +116,9 @@ int orc_dequant(const int8_t* c, const uint16_t* s, int64_t n, int64_t k, double
 /* quantized activations"). The paper fixes neither block size, scale rule nor      */
 /* rounding; the reading implemented here: blocks of 256 along k (the weight block), */
 /* symmetric absmax scale d = amax/127, codes q = clamp(rne(x * (127/amax)), +-127)  */
-/* in fp32, d kept in fp32, bsum = sum of the block's codes; an all-zero block gives */
-/* d = 0 and q = 0.                                                                  */
+/* in fp32, d kept in fp32, bsum = sum of the block's codes. A block whose amax is    */
+/* below 2^-100 (an all-zero block in particular) gives d = 0 and q = 0: below that   */
+/* 127/amax would overflow fp32 or amax/127 turn subnormal.                          */
 /* ------------------------------------------------------------------------------ */
 
 static int quantize_block(const float* x, int64_t len, int8_t* q, float* d, int32_t* bsum) {
@@ -127,7 +128,7 @@ static int quantize_block(const float* x, int64_t len, int8_t* q, float* d, int3
     float a = fabsf(x[i]);
     if (a > amax) amax = a;
   }
-  if (amax == 0.0f) {
+  if (amax < 0x1p-100f) {
     for (int64_t i = 0; i < len; ++i) q[i] = 0;
     *d = 0.0f;
     *bsum = 0;

@@ -190,6 +190,13 @@ def quantize_blocks_are_independent_and_zero_block(o):
     x[0, 256:512] = 0.0
     q, d, b = o.quantize(x)
     assert d[0, 1] == 0 and b[0, 1] == 0 and not q[0, 256:512].any()
+    # below 2^-100 a block quantizes to zeros; at 2^-100 it does not
+    tiny = np.zeros((1, 512), np.float32)
+    tiny[0, :256] = np.float32(2.0 ** -101) * np.linspace(-1, 1, 256, dtype=np.float32)
+    tiny[0, 256:] = np.float32(2.0 ** -100) * np.linspace(-1, 1, 256, dtype=np.float32)
+    qt, dt, _ = o.quantize(tiny)
+    assert dt[0, 0] == 0 and not qt[0, :256].any()
+    assert dt[0, 1] > 0 and qt[0, 256] == -127 and qt[0, 511] == 127
     # a large value at index 255 changes block 0 only; at index 256 block 1 only
     y = x.copy(); y[0, 255] = 1000.0
     qy, dy, _ = o.quantize(y)

@@ -30,6 +30,7 @@ C_MUTANTS = {
     "quant_bsum_sign": ("s += (int32_t)r;", "s -= (int32_t)r;"),
     "quant_truncate": ("float r = rintf(y);", "float r = truncf(y);"),
     "quant_block_stride": ("d + tt * nb + b,", "d + b,"),
+    "quant_tiny_threshold": ("if (amax < 0x1p-100f) {", "if (amax == 0.0f) {"),
     "dot_int8_wrap": ("s += (int64_t)a[i] * (int64_t)b[i];", "s += (int8_t)(a[i] * b[i]);"),
     "gemv_token_index_dropped": ("q + tt * k + b * 256, 256)", "q + b * 256, 256)"),
     "gemv_row_index_dropped": ("orc_dot_i8(c + r * k + b * 256,", "orc_dot_i8(c + b * 256,"),
