@@ -1,0 +1,197 @@
+/*
+ * tq.h - C ABI of the MI355X (gfx950) tied-trit-plane expert dot pass.
+ *
+ * The method (M. Grella, "Tied Trit-Planes", 2026):
+ *  - Sec. 2.1: with the two PTQTP plane scales tied at alpha = (3s, s), the trit planes
+ *    T1, T2 in {-1,0,1} fold into one code c = 3*t1 + t2 in {-4,...,4}; W_hat = s*c with
+ *    one f16 scale s per group.
+ *  - Sec. 2.2: the folded code plane is the persistent serving representation (4.0625
+ *    bits/weight: 4-bit codes plus one f16 scale per 256 weights of an output channel).
+ *    Serving is one pass: the codes decode to -4..4 by arithmetic, an integer dot runs
+ *    against block-quantized int8 activations, and each block costs one float
+ *    multiply-add.
+ *
+ * Persistent layout of one matrix with n output channels (rows) and k inputs
+ * (k % 256 == 0, kb = k/256 blocks per row):
+ *   codes  [n][kb][128] bytes, 128-byte aligned. Block (r, b) holds the 256 codes of
+ *          row r, columns 256b .. 256b+255, as unsigned nibbles u = c + 4 (0..8; the
+ *          values 9..15 never occur). Byte 16j + i (j = 0..7, i = 0..15) holds column
+ *          256b + 32j + i in its low nibble and column 256b + 32j + 16 + i in its high
+ *          nibble, so that the 16 bytes of chunk j unpack to 32 int8 codes whose
+ *          activations are 32 contiguous bytes.
+ *   scales [n][kb] IEEE binary16 bit patterns (s of row r, block b).
+ *   Bytes: 128 + 2 per 256 weights = 4.0625 bits/weight, the paper's figure.
+ * Quantized activations of t tokens over k inputs:
+ *   q [t][k] int8 (-127..127), d [t][kb] fp32 block scale, bsum [t][kb] int32 = sum of the
+ *   block's q. The codes and d are this library's reading of "block-quantized
+ *   activations" (Sec. 2.2 fixes no rule): blocks of 256, amax = max|x| over the block,
+ *   d = amax/127 and q = rne(x * (127/amax)) in IEEE fp32 (correctly rounded division,
+ *   round half to even); a block with amax < 2^-100 (an all-zero block in particular) has
+ *   d = 0 and q = 0.
+ * Block integer sum and combine (Sec. 2.2):
+ *   isum[t][r][b] = sum_i c[r][256b+i] * q[t][256b+i] (exact int32; computed as
+ *   sum u*q - 4*bsum), y[t][r] = sum_b f32(s[r][b]) * d[t][b] * isum[t][r][b] in fp32
+ *   (block order unspecified).
+ *
+ * Conventions for every entry point:
+ *  - Pointers are device pointers unless marked "host". The caller owns every buffer; the
+ *    library allocates and frees no memory and never synchronizes a stream, except
+ *    tq_moe_status, which synchronizes the stream it is given.
+ *  - Device work is enqueued on the caller's HIP stream, passed as `void* stream`
+ *    (a hipStream_t; NULL means the default stream). Calls are asynchronous.
+ *  - Arguments are validated on the host before any launch. A failed check returns a
+ *    negative status with no side effects; tq_last_error() then describes it (the
+ *    message is thread-local and valid until the calling thread's next call).
+ *  - TQ_ERR_DEVICE reports a launch failure (the HIP error string is in tq_last_error).
+ *  - Preconditions not checked (documented): activations are finite; codes hold only
+ *    nibbles 0..8; buffers are at least as large as their stated shapes.
+ *  - Thread-safe: no state besides the thread-local error message.
+ */
+#ifndef TQ_H_
+#define TQ_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t tq_status;
+#define TQ_OK 0
+#define TQ_ERR_INVALID (-1)   /* bad shape, null pointer or out-of-range argument */
+#define TQ_ERR_ALIGN (-2)     /* a pointer misses its required alignment */
+#define TQ_ERR_WORKSPACE (-3) /* workspace smaller than tq_moe_workspace_bytes */
+#define TQ_ERR_DEVICE (-4)    /* a HIP launch or runtime call failed */
+
+#define TQ_BLOCK 256       /* weights (and activations) per block */
+#define TQ_BLOCK_BYTES 128 /* packed code bytes per block */
+
+/* One tq matrix in the persistent layout above. codes: 128-byte aligned; scales:
+ * 2-byte aligned. n >= 1; 256 <= k <= 16384, k % 256 == 0. */
+typedef struct {
+  int32_t n;
+  int32_t k;
+  const uint8_t* codes;
+  const uint16_t* scales;
+} tq_mat;
+
+/* The routed experts of one MoE layer. Expert e's gate and up matrices are
+ * [inter][hidden] and its down matrix [hidden][inter], each in the persistent layout,
+ * at gate_codes + e * stride_codes[0] (bytes), gate_scales + e * stride_scales[0]
+ * (f16 elements), and likewise for up [1] and down [2]. hidden and inter are multiples
+ * of 256 in [256, 16384]; every codes pointer and byte stride is a multiple of 128. */
+typedef struct {
+  int32_t n_experts;
+  int32_t hidden;
+  int32_t inter;
+  const uint8_t* gate_codes;
+  const uint16_t* gate_scales;
+  const uint8_t* up_codes;
+  const uint16_t* up_scales;
+  const uint8_t* down_codes;
+  const uint16_t* down_scales;
+  int64_t stride_codes[3];
+  int64_t stride_scales[3];
+} tq_experts;
+
+/* Bytes of the codes plane (n * k / 2) and of the scales plane (2 * n * k / 256) of an
+ * n x k matrix; 0 if k % 256 != 0 or n < 0. Sec. 2.2: 4.0625 bits/weight in total. */
+size_t tq_codes_bytes(int32_t n, int32_t k);
+size_t tq_scales_bytes(int32_t n, int32_t k);
+
+/* Fold and pack on the host (Sec. 2.1 fold, Sec. 2.2 persistent format).
+ * t1, t2: host [n][k] trits in {-1,0,1}; codes_out: host, tq_codes_bytes(n, k) bytes.
+ * Writes c = 3*t1 + t2 as u = c + 4 nibbles in the layout above. TQ_ERR_INVALID if a
+ * trit is out of range (codes_out is then unspecified). */
+tq_status tq_fold_pack_host(const int8_t* t1, const int8_t* t2, int32_t n, int32_t k,
+                            uint8_t* codes_out);
+
+/* Inverse of the packing on the host: codes (host, layout above) -> c_out (host [n][k]
+ * int8 in -4..4). TQ_ERR_INVALID if a nibble exceeds 8. */
+tq_status tq_unpack_host(const uint8_t* codes, int32_t n, int32_t k, int8_t* c_out);
+
+/* Synthetic matrix generated on the device, folded and packed in place: trits and
+ * scales follow the SplitMix64 counter recipe keyed by `key` (word(key, i) is the i-th
+ * SplitMix64 output from state `key`; element e = r*k + col takes t1, t2 from the 16-bit
+ * fields (0,1) of word(key, e/2) if e is even and (2,3) if odd, trit = ((f*3)>>16) - 1;
+ * scale j = r*kb + b is 0x1419 + ((hi32(word(key, n*k/2 + j)) * 0x1A4E) >> 32) as f16
+ * bits, i.e. uniform over the f16 values in [1e-3, 1e-1]). For benchmark and test
+ * workloads too large to draw on the host; the fold and pack are those of
+ * tq_fold_pack_host. codes: 128-byte aligned, tq_codes_bytes(n, k); scales: n * kb. */
+tq_status tq_synth_weights(uint64_t key, int32_t n, int32_t k, uint8_t* codes,
+                           uint16_t* scales, void* stream);
+
+/* Activation quantizer (Sec. 2.2 block-quantized activations; rule stated above).
+ * x [t][k] fp32 (16-byte aligned) -> q [t][k] int8 (16-byte aligned), d [t][kb] fp32,
+ * bsum [t][kb] int32. t >= 0 (t = 0 is a no-op); k % 256 == 0, k <= 16384. */
+tq_status tq_quantize_act(const float* x, int64_t t, int32_t k, int8_t* q, float* d,
+                          int32_t* bsum, void* stream);
+
+/* The serving dot pass for one matrix and t tokens (Sec. 2.2): y[t][n] fp32 =
+ * sum_b f32(s[r][b]) * d[t][b] * isum[t][r][b]. q, d, bsum as from tq_quantize_act
+ * (q 16-byte aligned). isum_dbg: NULL, or a [t][n][kb] int32 buffer that receives the
+ * exact block sums (debug and parity; same kernel, one extra store per block).
+ * t >= 0 (t = 0 is a no-op). */
+tq_status tq_gemv(const tq_mat* w, const int8_t* q, const float* d, const int32_t* bsum,
+                  int64_t t, float* y, int32_t* isum_dbg, void* stream);
+
+/* Routed-expert MoE layer over the folded experts (Sec. 2.2 dot pass applied to every
+ * routed gate/up/down projection; the paper's layers are 43 x 3 projections x 256
+ * experts, Sec. 2.1). For every token t and slot j < topk with e = topk_idx[t][j]:
+ *   xq = quantize(x[t]);  g = W_gate[e] xq;  u = W_up[e] xq  (dot pass, fp32)
+ *   h = SiLU(g) * u  (fp32, SiLU(z) = z / (1 + exp(-z)));  hq = quantize(h)
+ *   y[t][j] = W_down[e] hq;   out[t] = sum_j topk_w[t][j] * y[t][j]  (ascending j)
+ * A slot whose expert id lies outside [0, n_experts) contributes nothing and sets a
+ * device flag that tq_moe_status reports. Duplicate ids in a token's list are separate
+ * slots. x: [t][hidden] fp32 (16-byte aligned); topk_idx, topk_w: [t][topk];
+ * out: [t][hidden] fp32, overwritten. 1 <= topk <= 64, topk <= n_experts.
+ * ws: device workspace of at least tq_moe_workspace_bytes(ex, t, topk) bytes, 256-byte
+ * aligned; its contents on entry are ignored, and on return it holds the stage buffers
+ * described by tq_moe_workspace_layout (for staged parity checks).
+ * flags: 0 (automatic path choice), or TQ_MOE_FORCE_VALU / TQ_MOE_FORCE_MFMA to pin
+ * the per-expert path (VALU dot4 for few tokens per expert, int8 MFMA for many). */
+#define TQ_MOE_FORCE_VALU 1
+#define TQ_MOE_FORCE_MFMA 2
+size_t tq_moe_workspace_bytes(const tq_experts* ex, int64_t t, int32_t topk);
+tq_status tq_moe_grouped(const tq_experts* ex, const float* x, int64_t t,
+                         const int32_t* topk_idx, const float* topk_w, int32_t topk,
+                         float* out, void* ws, size_t ws_bytes, int32_t flags, void* stream);
+
+/* Byte offsets, inside the workspace, of the stage buffers tq_moe_grouped leaves behind
+ * (S = t * topk slots, slot s = t * topk + j):
+ *   xq [t][hidden] int8, xd [t][hidden/256] fp32, xb [t][hidden/256] int32;
+ *   h [S][inter] fp32; hq [S][inter] int8, hd [S][inter/256] fp32, hb [S][inter/256] int32;
+ *   yd [S][hidden] fp32 (per-slot down output, before the routing weight);
+ *   flags: int32, bit 0 set if an expert id was out of range. */
+typedef struct {
+  size_t xq, xd, xb, h, hq, hd, hb, yd, flags;
+  size_t total;
+} tq_moe_layout;
+tq_status tq_moe_workspace_layout(const tq_experts* ex, int64_t t, int32_t topk,
+                                  tq_moe_layout* out);
+
+/* As tq_moe_grouped, and also records host-created HIP events (hipEvent_t, passed as
+ * void*) on the stream at the stage boundaries: events[i] before stage i and
+ * events[tq_moe_stage_count()] after the last stage. For per-stage timing in
+ * benchmarks; events may not be NULL. */
+int32_t tq_moe_stage_count(void);
+const char* tq_moe_stage_name(int32_t i);
+tq_status tq_moe_grouped_timed(const tq_experts* ex, const float* x, int64_t t,
+                               const int32_t* topk_idx, const float* topk_w, int32_t topk,
+                               float* out, void* ws, size_t ws_bytes, int32_t flags,
+                               void* stream, void* const* events);
+
+/* Synchronizes `stream`, then copies the workspace's device flags word to *flags_out
+ * (host). Returns TQ_OK, or TQ_ERR_DEVICE if the stream reports an error. */
+tq_status tq_moe_status(const void* ws, const tq_experts* ex, int64_t t, int32_t topk,
+                        int32_t* flags_out, void* stream);
+
+/* Thread-local description of the last failed call on this thread ("" if none). */
+const char* tq_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TQ_H_ */

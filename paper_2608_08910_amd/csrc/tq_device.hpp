@@ -1,0 +1,118 @@
+// Device-side building blocks of the tied-trit-plane dot pass on gfx950 (CDNA4, wave64).
+//
+// Lane geometry shared by every kernel here: a 256-weight block is 128 bytes of
+// nibble codes = 8 chunks of 16 bytes, and 8 consecutive lanes ("a group") cover one
+// block, lane (l & 7) holding chunk (l & 7). A wave's 16-byte load therefore covers 8
+// consecutive blocks (1 KB, fully coalesced). Chunk j's 16 bytes unpack to 32 int8
+// codes: low nibbles are columns 32j..32j+15, high nibbles columns 32j+16..32j+31, so
+// the matching activations are 32 contiguous int8 bytes.
+#pragma once
+
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tq {
+
+// DPP control words (GCN/CDNA encoding of the dpp_ctrl field).
+constexpr int kDppXor1 = 0xb1;        // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4e;        // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141; // lane i <- lane 7-i within each 8-lane half row
+constexpr int kDppRowRor8 = 0x128;    // lane i <- lane (i+8) mod 16 within each 16-lane row
+// ds_swizzle bit-mode offset: lane ^ 16 within each 32-lane half (and 0x1f, xor 0x10).
+constexpr int kSwizzleXor16 = 0x401f;
+
+constexpr uint32_t kLowNibbles = 0x0F0F0F0Fu;
+
+// Sum over the 8 lanes of a group; every lane of the group receives the sum.
+__device__ __forceinline__ int group_sum_i32(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, kDppXor1, 0xf, 0xf, false);
+  v += __builtin_amdgcn_update_dpp(0, v, kDppXor2, 0xf, 0xf, false);
+  v += __builtin_amdgcn_update_dpp(0, v, kDppHalfMirror, 0xf, 0xf, false);
+  return v;
+}
+
+__device__ __forceinline__ float group_max_f32(float v) {
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), kDppXor1, 0xf, 0xf, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), kDppXor2, 0xf, 0xf, false)));
+  v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), kDppHalfMirror, 0xf, 0xf, false)));
+  return v;
+}
+
+// Sum of one representative per group (lanes l, l^8, ..., l^56) over the whole wave;
+// the result is wave-uniform. Fixed order, so deterministic.
+__device__ __forceinline__ float wave_sum_groups_f32(float v) {
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), kDppRowRor8, 0xf, 0xf, false));
+  v += __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), kSwizzleXor16));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)) +
+         __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+}
+
+__device__ __forceinline__ float f16_bits_to_f32(uint16_t h) {
+  return __half2float(__ushort_as_half(h));
+}
+
+// Integer dot of one 16-byte code chunk (32 unsigned nibbles u = c + 4) with the
+// chunk's 32 int8 activations a[0..7] (dwords: a[m] = columns 4m..4m+3 of the low
+// half, a[4+m] = columns 16+4m..16+4m+3).
+__device__ __forceinline__ int dot_chunk_u(const uint4 w, const int (&a)[8]) {
+  int acc = 0;
+  acc = __builtin_amdgcn_sdot4(int(w.x & kLowNibbles), a[0], acc, false);
+  acc = __builtin_amdgcn_sdot4(int((w.x >> 4) & kLowNibbles), a[4], acc, false);
+  acc = __builtin_amdgcn_sdot4(int(w.y & kLowNibbles), a[1], acc, false);
+  acc = __builtin_amdgcn_sdot4(int((w.y >> 4) & kLowNibbles), a[5], acc, false);
+  acc = __builtin_amdgcn_sdot4(int(w.z & kLowNibbles), a[2], acc, false);
+  acc = __builtin_amdgcn_sdot4(int((w.z >> 4) & kLowNibbles), a[6], acc, false);
+  acc = __builtin_amdgcn_sdot4(int(w.w & kLowNibbles), a[3], acc, false);
+  acc = __builtin_amdgcn_sdot4(int((w.w >> 4) & kLowNibbles), a[7], acc, false);
+  return acc;
+}
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte streaming load (nontemporal: expert weights are read once per step).
+__device__ __forceinline__ uint4 ldg16(const void* p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+
+// Block quantizer on a group: each of the 8 lanes holds 32 consecutive values of one
+// 256-block (lane (l & 7) holds columns 32*(l&7) ..). Produces the lane's 32 int8 codes
+// packed into 8 dwords, and the block's fp32 scale d and code sum (group-uniform).
+// Rule: amax = max|x| (exact), d = amax/127 and inv = 127/amax (IEEE division, correctly
+// rounded: this library is built without fast-math), q = rne(x * inv) with the multiply
+// rounded on its own; amax < 2^-100 (all-zero blocks included) gives d = 0, q = 0.
+__device__ __forceinline__ void quantize_group32(const float (&x)[32], int (&qw)[8], float& d, int& bsum) {
+  float a = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 32; ++i) a = fmaxf(a, fabsf(x[i]));
+  const float amax = group_max_f32(a);
+  if (amax < 0x1p-100f) {
+#pragma unroll
+    for (int m = 0; m < 8; ++m) qw[m] = 0;
+    d = 0.0f;
+    bsum = 0;
+    return;
+  }
+  const float inv = 127.0f / amax;
+  d = amax / 127.0f;
+  int s = 0;
+#pragma unroll
+  for (int m = 0; m < 8; ++m) {
+    uint32_t packed = 0;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      float r = rintf(__fmul_rn(x[4 * m + b], inv));
+      r = fminf(fmaxf(r, -127.0f), 127.0f);
+      const int qi = (int)r;
+      s += qi;
+      packed |= (uint32_t(qi) & 0xFFu) << (8 * b);
+    }
+    qw[m] = int(packed);
+  }
+  bsum = group_sum_i32(s);
+}
+
+}  // namespace tq

@@ -1,0 +1,612 @@
+// Routed-expert MoE layer over folded tq experts: the dot pass of Sec. 2.2 applied to the
+// gate, up and down projections of every routed expert (the paper's model has 43 such
+// layers x 3 projections x 256 experts, Sec. 2.1). The glue around the projections
+// (SiLU(gate) * up, the requantized hidden, the softmax-weighted sum after down) is the
+// workload's definition, stated in tq.h.
+//
+// Stages (one kernel each, all on the caller's stream; no host synchronization):
+//   prologue  quantize x per 256-block, and (one extra workgroup) dispatch the routing:
+//             per-expert slot counts, the active-expert list, slot lists grouped by
+//             expert, task counts; zero the work tickets.
+//   gate_up   dynamic work queue over (active expert, row tile): a wave loads RPW rows of
+//             gate and of up (each byte read once per step), walks the expert's tokens NT
+//             at a time, and writes h = SiLU(g) * u per slot.
+//   requant   quantize h per 256-block (same quantizer as x).
+//   down      dynamic work queue over (active expert, row tile) of the down projection,
+//             writing y[slot][row].
+//   combine   out[t] = sum_j w[t][j] * y[t*topk + j] in ascending j (fixed order: no
+//             floating-point atomics, bitwise reproducible).
+#include <algorithm>
+
+#include "tq_device.hpp"
+#include "tq_internal.hpp"
+
+namespace tq {
+
+constexpr int kMaxExperts = 4096;
+constexpr int kMaxTopk = 64;
+constexpr int kNumStages = 5;
+static const char* const kStageNames[kNumStages] = {"prologue", "gate_up", "requant", "down", "combine"};
+
+// Control words at the start of the workspace.
+enum Ctrl { kFlags = 0, kNActive = 1, kTasksGU = 2, kTasksDn = 3, kTicketGU = 4, kTicketDn = 5, kNValid = 6, kCtrlWords = 64 };
+
+struct Layout {
+  size_t ctrl, active, act_off, slot_list, xq, xd, xb, h, hq, hd, hb, yd, total;
+};
+
+static size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+static Layout make_layout(int n_experts, int hidden, int inter, int64_t t, int topk) {
+  Layout L{};
+  const size_t S = (size_t)t * topk;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o = align_up(o + bytes, 256);
+    return at;
+  };
+  L.ctrl = take(kCtrlWords * 4);
+  L.active = take((size_t)n_experts * 4);
+  L.act_off = take(((size_t)n_experts + 1) * 4);
+  L.slot_list = take(S * 4);
+  L.xq = take((size_t)t * hidden);
+  L.xd = take((size_t)t * (hidden / 256) * 4);
+  L.xb = take((size_t)t * (hidden / 256) * 4);
+  L.h = take(S * inter * 4);
+  L.hq = take(S * inter);
+  L.hd = take(S * (inter / 256) * 4);
+  L.hb = take(S * (inter / 256) * 4);
+  L.yd = take(S * hidden * 4);
+  L.total = o;
+  return L;
+}
+
+// ---------------------------------------------------------------------------------
+// Shared pieces
+// ---------------------------------------------------------------------------------
+
+// Quantize 8 consecutive 256-blocks per wave of the flattened block grid.
+__device__ __forceinline__ void quantize_wave_blocks(const float* __restrict__ x, int64_t nblocks, int64_t wave_id,
+                                                     int8_t* __restrict__ q, float* __restrict__ d,
+                                                     int32_t* __restrict__ bsum) {
+  const int lane = threadIdx.x & 63;
+  const int64_t blk = wave_id * 8 + (lane >> 3);
+  if (blk >= nblocks) return;
+  const int cp = lane & 7;
+  const float4* xp = reinterpret_cast<const float4*>(x + blk * 256 + cp * 32);
+  float v[32];
+#pragma unroll
+  for (int m = 0; m < 8; ++m) {
+    const float4 f = xp[m];
+    v[4 * m + 0] = f.x;
+    v[4 * m + 1] = f.y;
+    v[4 * m + 2] = f.z;
+    v[4 * m + 3] = f.w;
+  }
+  int qw[8];
+  float dd;
+  int bs;
+  quantize_group32(v, qw, dd, bs);
+  int4* qp = reinterpret_cast<int4*>(q + blk * 256 + cp * 32);
+  qp[0] = make_int4(qw[0], qw[1], qw[2], qw[3]);
+  qp[1] = make_int4(qw[4], qw[5], qw[6], qw[7]);
+  if (cp == 0) {
+    d[blk] = dd;
+    bsum[blk] = bs;
+  }
+}
+
+// The lane's activation slice of one token: for load i, block 8i + g, chunk cp.
+template <int NL>
+__device__ __forceinline__ void load_acts(const int8_t* __restrict__ qrow, const float* __restrict__ drow,
+                                          const int32_t* __restrict__ brow, int kb, int g, int cp, bool ok,
+                                          int (&qa)[NL][8], float (&dd)[NL], int (&bb)[NL]) {
+#pragma unroll
+  for (int i = 0; i < NL; ++i) {
+    const int b = 8 * i + g;
+    if (ok && b < kb) {
+      const int4* p = reinterpret_cast<const int4*>(qrow + b * 256 + cp * 32);
+      const int4 lo = p[0], hi = p[1];
+      qa[i][0] = lo.x; qa[i][1] = lo.y; qa[i][2] = lo.z; qa[i][3] = lo.w;
+      qa[i][4] = hi.x; qa[i][5] = hi.y; qa[i][6] = hi.z; qa[i][7] = hi.w;
+      dd[i] = drow[b];
+      bb[i] = brow[b];
+    } else {
+#pragma unroll
+      for (int m = 0; m < 8; ++m) qa[i][m] = 0;
+      dd[i] = 0.0f;
+      bb[i] = 0;
+    }
+  }
+}
+
+template <int NL>
+__device__ __forceinline__ void load_row(const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
+                                         int64_t row, int kb, int g, int cp, bool ok, uint4 (&w)[NL], float (&s)[NL]) {
+#pragma unroll
+  for (int i = 0; i < NL; ++i) {
+    const int b = 8 * i + g;
+    const bool v = ok && b < kb;
+    w[i] = v ? ldg16(codes + (row * kb + b) * 128 + cp * 16) : make_uint4(0, 0, 0, 0);
+    s[i] = v ? f16_bits_to_f32(scales[row * kb + b]) : 0.0f;
+  }
+}
+
+// One row against one token: exact block sums, one multiply-add per block, wave total.
+template <int NL>
+__device__ __forceinline__ float row_dot(const uint4 (&w)[NL], const float (&s)[NL], const int (&qa)[NL][8],
+                                         const float (&dd)[NL], const int (&bb)[NL]) {
+  float acc = 0.0f;
+#pragma unroll
+  for (int i = 0; i < NL; ++i) {
+    const int is = group_sum_i32(dot_chunk_u(w[i], qa[i])) - 4 * bb[i];
+    acc = fmaf(s[i] * dd[i], (float)is, acc);
+  }
+  return wave_sum_groups_f32(acc);
+}
+
+__device__ __forceinline__ float silu_f32(float z) { return z / (1.0f + expf(-z)); }
+
+struct MoeArgs {
+  int n_experts, hidden, inter, topk;
+  int64_t t;
+  const uint8_t* codes[3];
+  const uint16_t* scales[3];
+  int64_t stride_codes[3], stride_scales[3];
+  const int32_t* topk_idx;
+  const float* topk_w;
+  int32_t* ctrl;
+  int32_t* active;
+  int32_t* act_off;
+  int32_t* slot_list;
+  int8_t* xq;
+  float* xd;
+  int32_t* xb;
+  float* h;
+  int8_t* hq;
+  float* hd;
+  int32_t* hb;
+  float* yd;
+  int tiles_gu, tiles_dn;
+};
+
+// ---------------------------------------------------------------------------------
+// prologue: quantize x (workgroups 0 .. nq-1) + dispatch (last workgroup)
+// ---------------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ x, MoeArgs A, int nq) {
+  if ((int)blockIdx.x < nq) {
+    const int64_t nblocks = A.t * (A.hidden / 256);
+    quantize_wave_blocks(x, nblocks, (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6), A.xq, A.xd, A.xb);
+    return;
+  }
+  __shared__ int s_cnt[kMaxExperts];
+  __shared__ int s_base[kMaxExperts];
+  __shared__ int s_scan_a[256], s_scan_s[256];
+  __shared__ int s_bad;
+  const int tid = threadIdx.x, E = A.n_experts;
+  const int64_t S = A.t * A.topk;
+  for (int e = tid; e < E; e += 256) s_cnt[e] = 0;
+  if (tid == 0) s_bad = 0;
+  __syncthreads();
+  for (int64_t s = tid; s < S; s += 256) {
+    const int e = A.topk_idx[s];
+    if (e >= 0 && e < E) atomicAdd(&s_cnt[e], 1);
+    else s_bad = 1;
+  }
+  __syncthreads();
+  // exclusive scan of (active experts, slots) over contiguous expert ranges per thread
+  const int per = (E + 255) / 256;
+  const int e0 = min(E, tid * per), e1 = min(E, e0 + per);
+  int na = 0, ns = 0;
+  for (int e = e0; e < e1; ++e) {
+    na += s_cnt[e] > 0;
+    ns += s_cnt[e];
+  }
+  s_scan_a[tid] = na;
+  s_scan_s[tid] = ns;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    const int va = tid >= off ? s_scan_a[tid - off] : 0;
+    const int vs = tid >= off ? s_scan_s[tid - off] : 0;
+    __syncthreads();
+    s_scan_a[tid] += va;
+    s_scan_s[tid] += vs;
+    __syncthreads();
+  }
+  int a = s_scan_a[tid] - na, pos = s_scan_s[tid] - ns;
+  for (int e = e0; e < e1; ++e) {
+    const int c = s_cnt[e];
+    if (c > 0) {
+      A.active[a] = e;
+      A.act_off[a] = pos;
+      s_base[e] = pos;
+      ++a;
+      pos += c;
+    }
+  }
+  if (tid == 255) {
+    const int n_active = s_scan_a[255], n_valid = s_scan_s[255];
+    A.act_off[n_active] = n_valid;
+    A.ctrl[kNActive] = n_active;
+    A.ctrl[kNValid] = n_valid;
+    A.ctrl[kTasksGU] = n_active * A.tiles_gu;
+    A.ctrl[kTasksDn] = n_active * A.tiles_dn;
+    A.ctrl[kTicketGU] = 0;
+    A.ctrl[kTicketDn] = 0;
+    A.ctrl[kFlags] = s_bad ? 1 : 0;
+  }
+  __syncthreads();
+  for (int64_t s = tid; s < S; s += 256) {
+    const int e = A.topk_idx[s];
+    if (e >= 0 && e < E) {
+      const int p = atomicAdd(&s_base[e], 1);
+      A.slot_list[p] = (int)s;
+    } else {
+      // an unrouted slot: its hidden row is defined (zero) so the requant stage reads
+      // finite values; the combine skips the slot.
+      float4* hp = reinterpret_cast<float4*>(A.h + s * A.inter);
+      for (int c = 0; c < A.inter / 4; ++c) hp[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------
+// gate_up: h[slot][row] = SiLU(Wg[e] xq) * (Wu[e] xq)
+// ---------------------------------------------------------------------------------
+
+template <int NL, int NT, int RPW>
+__global__ __launch_bounds__(256) void k_moe_gateup(MoeArgs A) {
+  __shared__ int s_task;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int g = lane >> 3, cp = lane & 7;
+  const int kb = A.hidden / 256, I = A.inter;
+  for (;;) {
+    if (threadIdx.x == 0) s_task = atomicAdd(&A.ctrl[kTicketGU], 1);
+    __syncthreads();
+    const int task = s_task;
+    __syncthreads();
+    if (task >= A.ctrl[kTasksGU]) return;
+    const int a = task / A.tiles_gu, tile = task - a * A.tiles_gu;
+    const int64_t e = A.active[a];
+    const int off = A.act_off[a], cnt = A.act_off[a + 1] - off;
+    const int row0 = (tile * 4 + wv) * RPW;
+    if (row0 >= I) continue;
+    const uint8_t* gc = A.codes[0] + e * A.stride_codes[0];
+    const uint8_t* uc = A.codes[1] + e * A.stride_codes[1];
+    const uint16_t* gs = A.scales[0] + e * A.stride_scales[0];
+    const uint16_t* us = A.scales[1] + e * A.stride_scales[1];
+    uint4 wg[RPW][NL], wu[RPW][NL];
+    float sg[RPW][NL], su[RPW][NL];
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) {
+      load_row<NL>(gc, gs, row0 + r, kb, g, cp, row0 + r < I, wg[r], sg[r]);
+      load_row<NL>(uc, us, row0 + r, kb, g, cp, row0 + r < I, wu[r], su[r]);
+    }
+    for (int c0 = 0; c0 < cnt; c0 += NT) {
+      int qa[NT][NL][8];
+      float dd[NT][NL];
+      int bb[NT][NL];
+      int slot[NT];
+#pragma unroll
+      for (int tt = 0; tt < NT; ++tt) {
+        const bool ok = c0 + tt < cnt;
+        slot[tt] = ok ? A.slot_list[off + c0 + tt] : 0;
+        const int64_t tok = slot[tt] / A.topk;
+        load_acts<NL>(A.xq + tok * A.hidden, A.xd + tok * kb, A.xb + tok * kb, kb, g, cp, ok, qa[tt], dd[tt], bb[tt]);
+      }
+#pragma unroll
+      for (int r = 0; r < RPW; ++r) {
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt) {
+          const float gv = row_dot<NL>(wg[r], sg[r], qa[tt], dd[tt], bb[tt]);
+          const float uv = row_dot<NL>(wu[r], su[r], qa[tt], dd[tt], bb[tt]);
+          if (lane == 0 && c0 + tt < cnt && row0 + r < I) A.h[(int64_t)slot[tt] * I + row0 + r] = silu_f32(gv) * uv;
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------
+// down: yd[slot][row] = Wd[e] hq[slot]
+// ---------------------------------------------------------------------------------
+
+template <int NL, int NT, int RPW>
+__global__ __launch_bounds__(256) void k_moe_down(MoeArgs A) {
+  __shared__ int s_task;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int g = lane >> 3, cp = lane & 7;
+  const int kb = A.inter / 256, H = A.hidden;
+  for (;;) {
+    if (threadIdx.x == 0) s_task = atomicAdd(&A.ctrl[kTicketDn], 1);
+    __syncthreads();
+    const int task = s_task;
+    __syncthreads();
+    if (task >= A.ctrl[kTasksDn]) return;
+    const int a = task / A.tiles_dn, tile = task - a * A.tiles_dn;
+    const int64_t e = A.active[a];
+    const int off = A.act_off[a], cnt = A.act_off[a + 1] - off;
+    const int row0 = (tile * 4 + wv) * RPW;
+    if (row0 >= H) continue;
+    const uint8_t* dc = A.codes[2] + e * A.stride_codes[2];
+    const uint16_t* ds = A.scales[2] + e * A.stride_scales[2];
+    uint4 w[RPW][NL];
+    float s[RPW][NL];
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) load_row<NL>(dc, ds, row0 + r, kb, g, cp, row0 + r < H, w[r], s[r]);
+    for (int c0 = 0; c0 < cnt; c0 += NT) {
+      int qa[NT][NL][8];
+      float dd[NT][NL];
+      int bb[NT][NL];
+      int slot[NT];
+#pragma unroll
+      for (int tt = 0; tt < NT; ++tt) {
+        const bool ok = c0 + tt < cnt;
+        slot[tt] = ok ? A.slot_list[off + c0 + tt] : 0;
+        const int64_t sl = slot[tt];
+        load_acts<NL>(A.hq + sl * A.inter, A.hd + sl * kb, A.hb + sl * kb, kb, g, cp, ok, qa[tt], dd[tt], bb[tt]);
+      }
+#pragma unroll
+      for (int r = 0; r < RPW; ++r) {
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt) {
+          const float v = row_dot<NL>(w[r], s[r], qa[tt], dd[tt], bb[tt]);
+          if (lane == 0 && c0 + tt < cnt && row0 + r < H) A.yd[(int64_t)slot[tt] * H + row0 + r] = v;
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------
+// requant and combine
+// ---------------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void k_moe_requant(MoeArgs A, int64_t nblocks) {
+  quantize_wave_blocks(A.h, nblocks, (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6), A.hq, A.hd, A.hb);
+}
+
+__global__ __launch_bounds__(256) void k_moe_combine(MoeArgs A, float* __restrict__ out) {
+  const int64_t H4 = A.hidden / 4;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= A.t * H4) return;
+  const int64_t tok = i / H4, c4 = i - tok * H4;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int j = 0; j < A.topk; ++j) {
+    const int64_t s = tok * A.topk + j;
+    const int e = A.topk_idx[s];
+    if (e < 0 || e >= A.n_experts) continue;
+    const float wj = A.topk_w[s];
+    const float4 v = reinterpret_cast<const float4*>(A.yd + s * A.hidden)[c4];
+    acc.x = fmaf(wj, v.x, acc.x);
+    acc.y = fmaf(wj, v.y, acc.y);
+    acc.z = fmaf(wj, v.z, acc.z);
+    acc.w = fmaf(wj, v.w, acc.w);
+  }
+  reinterpret_cast<float4*>(out)[i] = acc;
+}
+
+// ---------------------------------------------------------------------------------
+// host side
+// ---------------------------------------------------------------------------------
+
+using moe_fn = void (*)(MoeArgs);
+
+template <int NL, int RPW>
+static moe_fn pick_gu_nt(int nt) {
+  return nt == 1 ? k_moe_gateup<NL, 1, RPW> : k_moe_gateup<NL, 4, RPW>;
+}
+template <int NL, int RPW>
+static moe_fn pick_dn_nt(int nt) {
+  return nt == 1 ? k_moe_down<NL, 1, RPW> : k_moe_down<NL, 4, RPW>;
+}
+
+// gate/up: RPW = 4 (NL <= 2), 2 (NL <= 4), 1 otherwise; down: twice that (one matrix).
+static int rpw_gu(int nl) { return nl <= 2 ? 4 : (nl <= 4 ? 2 : 1); }
+static int rpw_dn(int nl) { return nl == 1 ? 8 : (nl <= 2 ? 4 : (nl <= 4 ? 2 : 1)); }
+
+static moe_fn pick_gateup(int nl, int nt) {
+  switch (nl) {
+    case 1: return pick_gu_nt<1, 4>(nt);
+    case 2: return pick_gu_nt<2, 4>(nt);
+    case 3: return pick_gu_nt<3, 2>(nt);
+    case 4: return pick_gu_nt<4, 2>(nt);
+    case 5: return pick_gu_nt<5, 1>(nt);
+    case 6: return pick_gu_nt<6, 1>(nt);
+    case 7: return pick_gu_nt<7, 1>(nt);
+    default: return pick_gu_nt<8, 1>(nt);
+  }
+}
+static moe_fn pick_down(int nl, int nt) {
+  switch (nl) {
+    case 1: return pick_dn_nt<1, 8>(nt);
+    case 2: return pick_dn_nt<2, 4>(nt);
+    case 3: return pick_dn_nt<3, 2>(nt);
+    case 4: return pick_dn_nt<4, 2>(nt);
+    case 5: return pick_dn_nt<5, 1>(nt);
+    case 6: return pick_dn_nt<6, 1>(nt);
+    case 7: return pick_dn_nt<7, 1>(nt);
+    default: return pick_dn_nt<8, 1>(nt);
+  }
+}
+
+static tq_status validate_experts(const tq_experts* ex, const char* fn) {
+  if (!ex) return fail(TQ_ERR_INVALID, "%s: null experts descriptor", fn);
+  if (ex->n_experts < 1 || ex->n_experts > kMaxExperts)
+    return fail(TQ_ERR_INVALID, "%s: n_experts = %d outside [1, %d]", fn, ex->n_experts, kMaxExperts);
+  for (int v : {ex->hidden, ex->inter})
+    if (v <= 0 || v % 256 != 0 || v > kMaxK)
+      return fail(TQ_ERR_INVALID, "%s: hidden = %d and inter = %d must be multiples of 256 in [256, %d]", fn, ex->hidden,
+                  ex->inter, kMaxK);
+  const uint8_t* cs[3] = {ex->gate_codes, ex->up_codes, ex->down_codes};
+  const uint16_t* ss[3] = {ex->gate_scales, ex->up_scales, ex->down_scales};
+  for (int p = 0; p < 3; ++p) {
+    if (!cs[p] || !ss[p]) return fail(TQ_ERR_INVALID, "%s: null expert codes or scales", fn);
+    if (!aligned(cs[p], 128) || ex->stride_codes[p] % 128 != 0)
+      return fail(TQ_ERR_ALIGN, "%s: expert codes pointers and byte strides must be multiples of 128", fn);
+    if (!aligned(ss[p], 2)) return fail(TQ_ERR_ALIGN, "%s: expert scales must be 2-byte aligned", fn);
+    if (ex->n_experts > 1 && (ex->stride_codes[p] <= 0 || ex->stride_scales[p] <= 0))
+      return fail(TQ_ERR_INVALID, "%s: expert strides must be positive", fn);
+  }
+  return TQ_OK;
+}
+
+static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const int32_t* topk_idx,
+                         const float* topk_w, int32_t topk, float* out, void* ws, size_t ws_bytes, int32_t flags,
+                         void* stream, void* const* events, const char* fn) {
+  clear_error();
+  tq_status st = validate_experts(ex, fn);
+  if (st != TQ_OK) return st;
+  if (t < 0 || t > (1 << 20)) return fail(TQ_ERR_INVALID, "%s: t = %lld outside [0, 2^20]", fn, (long long)t);
+  if (topk < 1 || topk > kMaxTopk || topk > ex->n_experts)
+    return fail(TQ_ERR_INVALID, "%s: topk = %d outside [1, min(%d, n_experts)]", fn, topk, kMaxTopk);
+  if (flags & ~(TQ_MOE_FORCE_VALU | TQ_MOE_FORCE_MFMA) || flags == (TQ_MOE_FORCE_VALU | TQ_MOE_FORCE_MFMA))
+    return fail(TQ_ERR_INVALID, "%s: bad flags 0x%x", fn, flags);
+  if (flags & TQ_MOE_FORCE_MFMA) return fail(TQ_ERR_INVALID, "%s: the MFMA expert path is not available", fn);
+  if (t == 0) {
+    if (events) {
+      for (int i = 0; i <= kNumStages; ++i)
+        if (hipEventRecord((hipEvent_t)events[i], (hipStream_t)stream) != hipSuccess)
+          return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
+    }
+    return TQ_OK;
+  }
+  if (!x || !topk_idx || !topk_w || !out || !ws) return fail(TQ_ERR_INVALID, "%s: null pointer", fn);
+  if (!aligned(x, 16) || !aligned(out, 16) || !aligned(ws, 256) || !aligned(topk_idx, 4) || !aligned(topk_w, 4))
+    return fail(TQ_ERR_ALIGN, "%s: x and out must be 16-byte aligned, ws 256-byte aligned", fn);
+  const Layout L = make_layout(ex->n_experts, ex->hidden, ex->inter, t, topk);
+  if (ws_bytes < L.total)
+    return fail(TQ_ERR_WORKSPACE, "%s: workspace %zu bytes < required %zu", fn, ws_bytes, L.total);
+
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  MoeArgs A{};
+  A.n_experts = ex->n_experts;
+  A.hidden = ex->hidden;
+  A.inter = ex->inter;
+  A.topk = topk;
+  A.t = t;
+  A.codes[0] = ex->gate_codes;
+  A.codes[1] = ex->up_codes;
+  A.codes[2] = ex->down_codes;
+  A.scales[0] = ex->gate_scales;
+  A.scales[1] = ex->up_scales;
+  A.scales[2] = ex->down_scales;
+  for (int p = 0; p < 3; ++p) {
+    A.stride_codes[p] = ex->stride_codes[p];
+    A.stride_scales[p] = ex->stride_scales[p];
+  }
+  A.topk_idx = topk_idx;
+  A.topk_w = topk_w;
+  A.ctrl = reinterpret_cast<int32_t*>(base + L.ctrl);
+  A.active = reinterpret_cast<int32_t*>(base + L.active);
+  A.act_off = reinterpret_cast<int32_t*>(base + L.act_off);
+  A.slot_list = reinterpret_cast<int32_t*>(base + L.slot_list);
+  A.xq = reinterpret_cast<int8_t*>(base + L.xq);
+  A.xd = reinterpret_cast<float*>(base + L.xd);
+  A.xb = reinterpret_cast<int32_t*>(base + L.xb);
+  A.h = reinterpret_cast<float*>(base + L.h);
+  A.hq = reinterpret_cast<int8_t*>(base + L.hq);
+  A.hd = reinterpret_cast<float*>(base + L.hd);
+  A.hb = reinterpret_cast<int32_t*>(base + L.hb);
+  A.yd = reinterpret_cast<float*>(base + L.yd);
+
+  const int nl_gu = (ex->hidden / 256 + 7) / 8, nl_dn = (ex->inter / 256 + 7) / 8;
+  const int nt = t == 1 ? 1 : 4;
+  A.tiles_gu = (ex->inter + 4 * rpw_gu(nl_gu) - 1) / (4 * rpw_gu(nl_gu));
+  A.tiles_dn = (ex->hidden + 4 * rpw_dn(nl_dn) - 1) / (4 * rpw_dn(nl_dn));
+  const int64_t S = t * topk;
+  const int64_t max_active = std::min<int64_t>(S, ex->n_experts);
+  const int64_t cap = 256 * 8;  // enough resident workgroups to fill 256 CUs
+  const unsigned g_gu = (unsigned)std::min<int64_t>(max_active * A.tiles_gu, cap);
+  const unsigned g_dn = (unsigned)std::min<int64_t>(max_active * A.tiles_dn, cap);
+  const int64_t xblocks = t * (ex->hidden / 256), hblocks = S * (ex->inter / 256);
+  const int nq = (int)((xblocks + 31) / 32);
+  hipStream_t stm = (hipStream_t)stream;
+
+  (void)hipGetLastError();
+  auto rec = [&](int i) -> bool { return !events || hipEventRecord((hipEvent_t)events[i], stm) == hipSuccess; };
+  if (!rec(0)) return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
+  hipLaunchKernelGGL(k_moe_prologue, dim3(nq + 1), dim3(256), 0, stm, x, A, nq);
+  if ((st = check_launch(fn)) != TQ_OK) return st;
+  if (!rec(1)) return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
+  hipLaunchKernelGGL(pick_gateup(nl_gu, nt), dim3(g_gu), dim3(256), 0, stm, A);
+  if ((st = check_launch(fn)) != TQ_OK) return st;
+  if (!rec(2)) return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
+  hipLaunchKernelGGL(k_moe_requant, dim3((unsigned)((hblocks + 31) / 32)), dim3(256), 0, stm, A, hblocks);
+  if ((st = check_launch(fn)) != TQ_OK) return st;
+  if (!rec(3)) return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
+  hipLaunchKernelGGL(pick_down(nl_dn, nt), dim3(g_dn), dim3(256), 0, stm, A);
+  if ((st = check_launch(fn)) != TQ_OK) return st;
+  if (!rec(4)) return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
+  const int64_t nout = t * (ex->hidden / 4);
+  hipLaunchKernelGGL(k_moe_combine, dim3((unsigned)((nout + 255) / 256)), dim3(256), 0, stm, A, out);
+  if ((st = check_launch(fn)) != TQ_OK) return st;
+  if (!rec(5)) return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
+  return TQ_OK;
+}
+
+}  // namespace tq
+
+extern "C" size_t tq_moe_workspace_bytes(const tq_experts* ex, int64_t t, int32_t topk) {
+  if (!ex || ex->n_experts < 1 || ex->hidden <= 0 || ex->inter <= 0 || t < 0 || topk < 1) return 0;
+  return tq::make_layout(ex->n_experts, ex->hidden, ex->inter, t, topk).total;
+}
+
+extern "C" tq_status tq_moe_workspace_layout(const tq_experts* ex, int64_t t, int32_t topk, tq_moe_layout* out) {
+  using namespace tq;
+  clear_error();
+  tq_status st = validate_experts(ex, "tq_moe_workspace_layout");
+  if (st != TQ_OK) return st;
+  if (!out || t < 0 || topk < 1) return fail(TQ_ERR_INVALID, "tq_moe_workspace_layout: bad arguments");
+  const Layout L = make_layout(ex->n_experts, ex->hidden, ex->inter, t, topk);
+  out->xq = L.xq;
+  out->xd = L.xd;
+  out->xb = L.xb;
+  out->h = L.h;
+  out->hq = L.hq;
+  out->hd = L.hd;
+  out->hb = L.hb;
+  out->yd = L.yd;
+  out->flags = L.ctrl + 4 * kFlags;
+  out->total = L.total;
+  return TQ_OK;
+}
+
+extern "C" tq_status tq_moe_grouped(const tq_experts* ex, const float* x, int64_t t, const int32_t* topk_idx,
+                                    const float* topk_w, int32_t topk, float* out, void* ws, size_t ws_bytes,
+                                    int32_t flags, void* stream) {
+  return tq::moe_run(ex, x, t, topk_idx, topk_w, topk, out, ws, ws_bytes, flags, stream, nullptr, "tq_moe_grouped");
+}
+
+extern "C" int32_t tq_moe_stage_count(void) { return tq::kNumStages; }
+
+extern "C" const char* tq_moe_stage_name(int32_t i) {
+  return (i >= 0 && i < tq::kNumStages) ? tq::kStageNames[i] : "";
+}
+
+extern "C" tq_status tq_moe_grouped_timed(const tq_experts* ex, const float* x, int64_t t, const int32_t* topk_idx,
+                                          const float* topk_w, int32_t topk, float* out, void* ws, size_t ws_bytes,
+                                          int32_t flags, void* stream, void* const* events) {
+  if (!events) return tq::fail(TQ_ERR_INVALID, "tq_moe_grouped_timed: events may not be NULL");
+  for (int i = 0; i <= tq::kNumStages; ++i)
+    if (!events[i]) return tq::fail(TQ_ERR_INVALID, "tq_moe_grouped_timed: null event %d", i);
+  return tq::moe_run(ex, x, t, topk_idx, topk_w, topk, out, ws, ws_bytes, flags, stream, events,
+                     "tq_moe_grouped_timed");
+}
+
+extern "C" tq_status tq_moe_status(const void* ws, const tq_experts* ex, int64_t t, int32_t topk, int32_t* flags_out,
+                                   void* stream) {
+  using namespace tq;
+  clear_error();
+  if (!ws || !flags_out) return fail(TQ_ERR_INVALID, "tq_moe_status: null pointer");
+  tq_status st = validate_experts(ex, "tq_moe_status");
+  if (st != TQ_OK) return st;
+  const Layout L = make_layout(ex->n_experts, ex->hidden, ex->inter, t, topk);
+  hipError_t e = hipStreamSynchronize((hipStream_t)stream);
+  if (e != hipSuccess) return fail(TQ_ERR_DEVICE, "tq_moe_status: stream error: %s", hipGetErrorString(e));
+  e = hipMemcpy(flags_out, static_cast<const uint8_t*>(ws) + L.ctrl + 4 * kFlags, 4, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return fail(TQ_ERR_DEVICE, "tq_moe_status: copy failed: %s", hipGetErrorString(e));
+  return TQ_OK;
+}

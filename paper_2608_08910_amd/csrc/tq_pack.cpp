@@ -1,0 +1,65 @@
+// Persistent-format sizes, and fold + pack / unpack on the host (Sec. 2.1 fold
+// c = 3*t1 + t2; Sec. 2.2 the folded code plane is the stored form).
+#include <cstring>
+
+#include "tq_internal.hpp"
+
+extern "C" size_t tq_codes_bytes(int32_t n, int32_t k) {
+  if (n < 0 || k <= 0 || k % 256 != 0) return 0;
+  return (size_t)n * (size_t)k / 2;
+}
+
+extern "C" size_t tq_scales_bytes(int32_t n, int32_t k) {
+  if (n < 0 || k <= 0 || k % 256 != 0) return 0;
+  return (size_t)n * (size_t)(k / 256) * 2;
+}
+
+extern "C" tq_status tq_fold_pack_host(const int8_t* t1, const int8_t* t2, int32_t n, int32_t k,
+                                       uint8_t* codes_out) {
+  using namespace tq;
+  clear_error();
+  if (n < 0 || k <= 0 || k % 256 != 0)
+    return fail(TQ_ERR_INVALID, "tq_fold_pack_host: bad shape n=%d k=%d (k must be a multiple of 256)", n, k);
+  if (n == 0) return TQ_OK;
+  if (!t1 || !t2 || !codes_out) return fail(TQ_ERR_INVALID, "tq_fold_pack_host: null pointer");
+  const int64_t kb = k / 256;
+  for (int64_t r = 0; r < n; ++r)
+    for (int64_t b = 0; b < kb; ++b) {
+      const int64_t col0 = r * k + b * 256;
+      uint8_t* blk = codes_out + (r * kb + b) * 128;
+      for (int j = 0; j < 8; ++j)
+        for (int i = 0; i < 16; ++i) {
+          const int64_t lo = col0 + 32 * j + i, hi = lo + 16;
+          const int a1 = t1[lo], a2 = t2[lo], b1 = t1[hi], b2 = t2[hi];
+          if (a1 < -1 || a1 > 1 || a2 < -1 || a2 > 1 || b1 < -1 || b1 > 1 || b2 < -1 || b2 > 1)
+            return fail(TQ_ERR_INVALID, "tq_fold_pack_host: trit out of range near element %lld", (long long)lo);
+          const int ulo = 3 * a1 + a2 + 4, uhi = 3 * b1 + b2 + 4;
+          blk[16 * j + i] = (uint8_t)(ulo | (uhi << 4));
+        }
+    }
+  return TQ_OK;
+}
+
+extern "C" tq_status tq_unpack_host(const uint8_t* codes, int32_t n, int32_t k, int8_t* c_out) {
+  using namespace tq;
+  clear_error();
+  if (n < 0 || k <= 0 || k % 256 != 0)
+    return fail(TQ_ERR_INVALID, "tq_unpack_host: bad shape n=%d k=%d (k must be a multiple of 256)", n, k);
+  if (n == 0) return TQ_OK;
+  if (!codes || !c_out) return fail(TQ_ERR_INVALID, "tq_unpack_host: null pointer");
+  const int64_t kb = k / 256;
+  for (int64_t r = 0; r < n; ++r)
+    for (int64_t b = 0; b < kb; ++b) {
+      const int64_t col0 = r * k + b * 256;
+      const uint8_t* blk = codes + (r * kb + b) * 128;
+      for (int j = 0; j < 8; ++j)
+        for (int i = 0; i < 16; ++i) {
+          const int ulo = blk[16 * j + i] & 0xF, uhi = blk[16 * j + i] >> 4;
+          if (ulo > 8 || uhi > 8)
+            return fail(TQ_ERR_INVALID, "tq_unpack_host: nibble > 8 in block (%lld, %lld)", (long long)r, (long long)b);
+          c_out[col0 + 32 * j + i] = (int8_t)(ulo - 4);
+          c_out[col0 + 32 * j + 16 + i] = (int8_t)(uhi - 4);
+        }
+    }
+  return TQ_OK;
+}

@@ -1,0 +1,271 @@
+"""Python binding of libtq (include/tq.h): argument marshalling only.
+
+Every function here has the name of the C entry point it calls and does no compute of
+its own: it checks dtypes, shapes, devices and contiguity, passes raw pointers and the
+caller's HIP stream, and raises ``TqError`` on a non-zero status. PyTorch provides
+device memory and streams. If ``libtq.so`` has not been built the import fails; there
+is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtq.so")
+
+TQ_OK = 0
+TQ_ERR_INVALID = -1
+TQ_ERR_ALIGN = -2
+TQ_ERR_WORKSPACE = -3
+TQ_ERR_DEVICE = -4
+TQ_MOE_FORCE_VALU = 1
+TQ_MOE_FORCE_MFMA = 2
+
+
+class TqError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{msg} (status {status})")
+        self.status = status
+
+
+class tq_mat(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("k", ctypes.c_int32), ("codes", ctypes.c_void_p), ("scales", ctypes.c_void_p)]
+
+
+class tq_experts(ctypes.Structure):
+    _fields_ = [
+        ("n_experts", ctypes.c_int32), ("hidden", ctypes.c_int32), ("inter", ctypes.c_int32),
+        ("gate_codes", ctypes.c_void_p), ("gate_scales", ctypes.c_void_p),
+        ("up_codes", ctypes.c_void_p), ("up_scales", ctypes.c_void_p),
+        ("down_codes", ctypes.c_void_p), ("down_scales", ctypes.c_void_p),
+        ("stride_codes", ctypes.c_int64 * 3), ("stride_scales", ctypes.c_int64 * 3),
+    ]
+
+
+class tq_moe_layout(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_size_t) for n in ("xq", "xd", "xb", "h", "hq", "hd", "hb", "yd", "flags", "total")]
+
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2608_08910_amd.build` (hipcc, gfx950)")
+
+_L = ctypes.CDLL(LIB_PATH)
+_vp, _i32, _i64, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+_P = ctypes.POINTER
+for _name, _args, _res in [
+    ("tq_codes_bytes", [_i32, _i32], _sz),
+    ("tq_scales_bytes", [_i32, _i32], _sz),
+    ("tq_fold_pack_host", [_vp, _vp, _i32, _i32, _vp], _i32),
+    ("tq_unpack_host", [_vp, _i32, _i32, _vp], _i32),
+    ("tq_synth_weights", [ctypes.c_uint64, _i32, _i32, _vp, _vp, _vp], _i32),
+    ("tq_quantize_act", [_vp, _i64, _i32, _vp, _vp, _vp, _vp], _i32),
+    ("tq_gemv", [_P(tq_mat), _vp, _vp, _vp, _i64, _vp, _vp, _vp], _i32),
+    ("tq_moe_workspace_bytes", [_P(tq_experts), _i64, _i32], _sz),
+    ("tq_moe_workspace_layout", [_P(tq_experts), _i64, _i32, _P(tq_moe_layout)], _i32),
+    ("tq_moe_grouped", [_P(tq_experts), _vp, _i64, _vp, _vp, _i32, _vp, _vp, _sz, _i32, _vp], _i32),
+    ("tq_moe_grouped_timed", [_P(tq_experts), _vp, _i64, _vp, _vp, _i32, _vp, _vp, _sz, _i32, _vp, _P(_vp)], _i32),
+    ("tq_moe_stage_count", [], _i32),
+    ("tq_moe_stage_name", [_i32], ctypes.c_char_p),
+    ("tq_moe_status", [_vp, _P(tq_experts), _i64, _i32, _P(_i32), _vp], _i32),
+    ("tq_last_error", [], ctypes.c_char_p),
+]:
+    _f = getattr(_L, _name)
+    _f.argtypes = _args
+    _f.restype = _res
+
+
+def tq_last_error() -> str:
+    return _L.tq_last_error().decode()
+
+
+def _ok(st: int):
+    if st != TQ_OK:
+        raise TqError(st, tq_last_error())
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _dev(t: torch.Tensor, dtype: torch.dtype, name: str, shape=None) -> int:
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name}: expected a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name}: expected dtype {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: expected shape {tuple(shape)}, got {tuple(t.shape)}")
+    return t.data_ptr()
+
+
+def _host(a: np.ndarray, dtype, name: str, shape=None) -> int:
+    if not isinstance(a, np.ndarray) or a.dtype != dtype or not a.flags["C_CONTIGUOUS"]:
+        raise TypeError(f"{name}: expected a C-contiguous numpy array of {np.dtype(dtype)}")
+    if shape is not None and a.shape != tuple(shape):
+        raise ValueError(f"{name}: expected shape {tuple(shape)}, got {a.shape}")
+    return a.ctypes.data
+
+
+# -- persistent format ------------------------------------------------------------------
+
+def tq_codes_bytes(n: int, k: int) -> int:
+    return int(_L.tq_codes_bytes(n, k))
+
+
+def tq_scales_bytes(n: int, k: int) -> int:
+    return int(_L.tq_scales_bytes(n, k))
+
+
+def tq_fold_pack_host(t1: np.ndarray, t2: np.ndarray) -> np.ndarray:
+    """Host fold + pack of trit planes [n][k] into codes [n][k/256][128] (uint8)."""
+    n, k = t1.shape
+    out = np.empty((n, k // 256, 128), dtype=np.uint8)
+    _ok(_L.tq_fold_pack_host(_host(t1, np.int8, "t1"), _host(t2, np.int8, "t2", (n, k)), n, k, _host(out, np.uint8, "codes")))
+    return out
+
+
+def tq_unpack_host(codes: np.ndarray, n: int, k: int) -> np.ndarray:
+    out = np.empty((n, k), dtype=np.int8)
+    _ok(_L.tq_unpack_host(_host(codes, np.uint8, "codes"), n, k, _host(out, np.int8, "c_out")))
+    return out
+
+
+@dataclass
+class TqMatrix:
+    """One matrix in the persistent layout: codes [n][kb][128] uint8, scales [n][kb] int16
+    (f16 bit patterns; torch has no uint16 arithmetic we need, int16 carries the bits)."""
+    n: int
+    k: int
+    codes: torch.Tensor
+    scales: torch.Tensor
+
+    @staticmethod
+    def empty(n: int, k: int, device="cuda") -> "TqMatrix":
+        return TqMatrix(n, k, torch.empty((n, k // 256, 128), dtype=torch.uint8, device=device),
+                        torch.empty((n, k // 256), dtype=torch.int16, device=device))
+
+    def desc(self) -> tq_mat:
+        _dev(self.codes, torch.uint8, "codes", (self.n, self.k // 256, 128))
+        _dev(self.scales, torch.int16, "scales", (self.n, self.k // 256))
+        return tq_mat(self.n, self.k, self.codes.data_ptr(), self.scales.data_ptr())
+
+
+def tq_synth_weights(key: int, m: TqMatrix, stream=None):
+    _ok(_L.tq_synth_weights(key & (2**64 - 1), m.n, m.k, _dev(m.codes, torch.uint8, "codes", (m.n, m.k // 256, 128)),
+                            _dev(m.scales, torch.int16, "scales", (m.n, m.k // 256)), _stream(stream)))
+
+
+# -- dot pass -----------------------------------------------------------------------------
+
+def tq_quantize_act(x: torch.Tensor, q: torch.Tensor, d: torch.Tensor, bsum: torch.Tensor, stream=None):
+    t, k = x.shape
+    _ok(_L.tq_quantize_act(_dev(x, torch.float32, "x"), t, k, _dev(q, torch.int8, "q", (t, k)),
+                           _dev(d, torch.float32, "d", (t, k // 256)), _dev(bsum, torch.int32, "bsum", (t, k // 256)),
+                           _stream(stream)))
+
+
+def tq_gemv(m: TqMatrix, q: torch.Tensor, d: torch.Tensor, bsum: torch.Tensor, y: torch.Tensor,
+            isum_dbg: torch.Tensor | None = None, stream=None):
+    t = q.shape[0]
+    desc = m.desc()
+    dbg = None if isum_dbg is None else _dev(isum_dbg, torch.int32, "isum_dbg", (t, m.n, m.k // 256))
+    _ok(_L.tq_gemv(ctypes.byref(desc), _dev(q, torch.int8, "q", (t, m.k)), _dev(d, torch.float32, "d", (t, m.k // 256)),
+                   _dev(bsum, torch.int32, "bsum", (t, m.k // 256)), t, _dev(y, torch.float32, "y", (t, m.n)), dbg,
+                   _stream(stream)))
+
+
+# -- routed-expert MoE layer ----------------------------------------------------------------
+
+@dataclass
+class TqExperts:
+    """Routed experts of one layer, stacked: gate/up codes [E][inter][hidden/256][128],
+    down codes [E][hidden][inter/256][128], scales likewise [E][rows][kb] (f16 bits)."""
+    n_experts: int
+    hidden: int
+    inter: int
+    codes: tuple  # (gate, up, down) uint8 tensors
+    scales: tuple  # (gate, up, down) int16 tensors
+
+    @staticmethod
+    def empty(n_experts: int, hidden: int, inter: int, device="cuda") -> "TqExperts":
+        shapes = [(inter, hidden), (inter, hidden), (hidden, inter)]
+        codes = tuple(torch.empty((n_experts, n, k // 256, 128), dtype=torch.uint8, device=device) for n, k in shapes)
+        scales = tuple(torch.empty((n_experts, n, k // 256), dtype=torch.int16, device=device) for n, k in shapes)
+        return TqExperts(n_experts, hidden, inter, codes, scales)
+
+    def shape(self, proj: int):
+        return [(self.inter, self.hidden), (self.inter, self.hidden), (self.hidden, self.inter)][proj]
+
+    def matrix(self, e: int, proj: int) -> TqMatrix:
+        n, k = self.shape(proj)
+        return TqMatrix(n, k, self.codes[proj][e], self.scales[proj][e])
+
+    def desc(self) -> tq_experts:
+        d = tq_experts()
+        d.n_experts, d.hidden, d.inter = self.n_experts, self.hidden, self.inter
+        for p, (cn, sn) in enumerate((("gate_codes", "gate_scales"), ("up_codes", "up_scales"), ("down_codes", "down_scales"))):
+            n, k = self.shape(p)
+            _dev(self.codes[p], torch.uint8, cn, (self.n_experts, n, k // 256, 128))
+            _dev(self.scales[p], torch.int16, sn, (self.n_experts, n, k // 256))
+            setattr(d, cn, self.codes[p].data_ptr())
+            setattr(d, sn, self.scales[p].data_ptr())
+            d.stride_codes[p] = n * (k // 256) * 128
+            d.stride_scales[p] = n * (k // 256)
+        return d
+
+
+def tq_moe_workspace_bytes(ex: TqExperts, t: int, topk: int) -> int:
+    return int(_L.tq_moe_workspace_bytes(ctypes.byref(ex.desc()), t, topk))
+
+
+def tq_moe_workspace_layout(ex: TqExperts, t: int, topk: int) -> dict:
+    lay = tq_moe_layout()
+    _ok(_L.tq_moe_workspace_layout(ctypes.byref(ex.desc()), t, topk, ctypes.byref(lay)))
+    return {n: int(getattr(lay, n)) for n, _ in tq_moe_layout._fields_}
+
+
+def _moe_args(ex, x, topk_idx, topk_w, out, ws):
+    t, h = x.shape
+    topk = topk_idx.shape[1]
+    if h != ex.hidden:
+        raise ValueError(f"x: hidden {h} != experts' hidden {ex.hidden}")
+    return (ctypes.byref(ex.desc()), _dev(x, torch.float32, "x"), t, _dev(topk_idx, torch.int32, "topk_idx", (t, topk)),
+            _dev(topk_w, torch.float32, "topk_w", (t, topk)), topk, _dev(out, torch.float32, "out", (t, h)),
+            _dev(ws, torch.uint8, "ws"), ws.numel())
+
+
+def tq_moe_grouped(ex: TqExperts, x, topk_idx, topk_w, out, ws, flags: int = 0, stream=None):
+    _ok(_L.tq_moe_grouped(*_moe_args(ex, x, topk_idx, topk_w, out, ws), flags, _stream(stream)))
+
+
+def tq_moe_stage_count() -> int:
+    return int(_L.tq_moe_stage_count())
+
+
+def tq_moe_stage_name(i: int) -> str:
+    return _L.tq_moe_stage_name(i).decode()
+
+
+def tq_moe_grouped_timed(ex: TqExperts, x, topk_idx, topk_w, out, ws, events, flags: int = 0, stream=None):
+    """events: tq_moe_stage_count() + 1 torch.cuda.Event(enable_timing=True) objects."""
+    n = tq_moe_stage_count() + 1
+    if len(events) != n:
+        raise ValueError(f"need {n} events")
+    arr = (_vp * n)(*[ev.cuda_event for ev in events])
+    _ok(_L.tq_moe_grouped_timed(*_moe_args(ex, x, topk_idx, topk_w, out, ws), flags, _stream(stream), arr))
+
+
+def tq_moe_status(ws, ex: TqExperts, t: int, topk: int, stream=None) -> int:
+    v = ctypes.c_int32(0)
+    _ok(_L.tq_moe_status(_dev(ws, torch.uint8, "ws"), ctypes.byref(ex.desc()), t, topk, ctypes.byref(v), _stream(stream)))
+    return v.value

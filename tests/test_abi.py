@@ -1,0 +1,170 @@
+"""Host-side checks of the C-ABI library (no GPU needed): exports, persistent-format
+arithmetic, host fold/pack against the oracle's fold, and argument validation."""
+import ctypes
+import json
+import os
+import re
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2608_08910_amd import tq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = open(os.path.join(ROOT, "include", "tq.h")).read()
+GOLDEN = json.load(open(os.path.join(ROOT, "tests", "golden", "paper_facts.json")))
+
+no_gpu_only = pytest.mark.skipif(torch.cuda.is_available(),
+                                 reason="feeds fake device pointers to validation paths; host-only")
+
+
+def declared_functions():
+    body = re.sub(r"/\*.*?\*/", "", HEADER, flags=re.S)
+    return sorted(set(re.findall(r"\b(tq_[a-z0-9_]+)\s*\(", body)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 15
+    lib = ctypes.CDLL(tq.LIB_PATH)
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_format_size_is_paper_bits_per_weight():
+    bpw = GOLDEN["bits_per_weight"]
+    assert bpw["tq2_0_fx4_block_bytes"] * 8 / bpw["tq2_0_fx4_block_weights"] == bpw["tq2_0_fx4"]
+    for n, k in ((2048, 4096), (4096, 2048), (2048, 7168), (1, 256)):
+        total = tq.tq_codes_bytes(n, k) + tq.tq_scales_bytes(n, k)
+        assert total * 8 / (n * k) == bpw["tq2_0_fx4"]
+    assert tq.tq_codes_bytes(4, 300) == 0 and tq.tq_scales_bytes(-1, 256) == 0
+
+
+def test_pack_layout_bytes_hand_built():
+    # one row, one block: column i holds code c_i; byte 16j+i must be
+    # (c[32j+i]+4) | (c[32j+16+i]+4) << 4
+    cols = np.arange(256)
+    c = ((cols * 7) % 9 - 4).astype(np.int8)
+    t1 = np.floor_divide(c.astype(int) + 4, 3) - 1
+    t2 = c.astype(int) - 3 * t1
+    codes = tq.tq_fold_pack_host(t1.astype(np.int8)[None], t2.astype(np.int8)[None])
+    for j in range(8):
+        for i in range(16):
+            want = (int(c[32 * j + i]) + 4) | ((int(c[32 * j + 16 + i]) + 4) << 4)
+            assert codes[0, 0, 16 * j + i] == want
+
+
+def test_fold_pack_unpack_matches_oracle_fold(oracle):
+    rng = np.random.default_rng(1)
+    for n, k in ((3, 256), (5, 768), (2, 7168)):
+        t1 = rng.integers(-1, 2, (n, k)).astype(np.int8)
+        t2 = rng.integers(-1, 2, (n, k)).astype(np.int8)
+        codes = tq.tq_fold_pack_host(t1, t2)
+        assert codes.shape == (n, k // 256, 128)
+        assert np.array_equal(tq.tq_unpack_host(codes, n, k), oracle.fold(t1, t2))
+        assert ((codes & 0xF) <= 8).all() and ((codes >> 4) <= 8).all()
+
+
+def test_fold_pack_rejects_bad_trits_and_unpack_bad_nibbles():
+    t = np.zeros((1, 256), np.int8)
+    bad = t.copy(); bad[0, 17] = 2
+    with pytest.raises(tq.TqError) as e:
+        tq.tq_fold_pack_host(bad, t)
+    assert e.value.status == tq.TQ_ERR_INVALID and "trit" in str(e.value)
+    codes = tq.tq_fold_pack_host(t, t)
+    codes[0, 0, 5] = 0x94  # high nibble 9
+    with pytest.raises(tq.TqError):
+        tq.tq_unpack_host(codes, 1, 256)
+
+
+FAKE = 0x7F0000000000  # 256-byte aligned, never dereferenced: every call below is invalid
+
+
+@no_gpu_only
+def test_gemv_validation_errors_before_launch():
+    L = tq._L
+    cases = [
+        (tq.tq_mat(0, 4096, FAKE, FAKE), 1, tq.TQ_ERR_INVALID),       # n < 1
+        (tq.tq_mat(16, 300, FAKE, FAKE), 1, tq.TQ_ERR_INVALID),       # k % 256
+        (tq.tq_mat(16, 32768, FAKE, FAKE), 1, tq.TQ_ERR_INVALID),     # k too large
+        (tq.tq_mat(16, 4096, FAKE + 16, FAKE), 1, tq.TQ_ERR_ALIGN),   # codes alignment
+        (tq.tq_mat(16, 4096, None, FAKE), 1, tq.TQ_ERR_INVALID),      # null codes
+        (tq.tq_mat(16, 4096, FAKE, FAKE), -1, tq.TQ_ERR_INVALID),     # t < 0
+    ]
+    for m, t, want in cases:
+        st = L.tq_gemv(ctypes.byref(m), FAKE, FAKE, FAKE, t, FAKE, None, None)
+        assert st == want, (m.n, m.k, t, st, tq.tq_last_error())
+        assert tq.tq_last_error()
+    st = L.tq_gemv(ctypes.byref(tq.tq_mat(16, 4096, FAKE, FAKE)), FAKE + 4, FAKE, FAKE, 1, FAKE, None, None)
+    assert st == tq.TQ_ERR_ALIGN  # q must be 16-byte aligned
+    # t == 0 is a no-op that touches nothing
+    assert L.tq_gemv(ctypes.byref(tq.tq_mat(16, 4096, FAKE, FAKE)), FAKE, FAKE, FAKE, 0, FAKE, None, None) == tq.TQ_OK
+
+
+@no_gpu_only
+def test_quantize_validation_errors_before_launch():
+    L = tq._L
+    assert L.tq_quantize_act(FAKE, 1, 300, FAKE, FAKE, FAKE, None) == tq.TQ_ERR_INVALID
+    assert L.tq_quantize_act(FAKE, -1, 256, FAKE, FAKE, FAKE, None) == tq.TQ_ERR_INVALID
+    assert L.tq_quantize_act(FAKE + 4, 1, 256, FAKE, FAKE, FAKE, None) == tq.TQ_ERR_ALIGN
+    assert L.tq_quantize_act(None, 1, 256, FAKE, FAKE, FAKE, None) == tq.TQ_ERR_INVALID
+    assert L.tq_quantize_act(FAKE, 0, 256, FAKE, FAKE, FAKE, None) == tq.TQ_OK
+
+
+def _experts_desc(E=8, H=512, I=256):
+    d = tq.tq_experts()
+    d.n_experts, d.hidden, d.inter = E, H, I
+    for name in ("gate_codes", "gate_scales", "up_codes", "up_scales", "down_codes", "down_scales"):
+        setattr(d, name, FAKE)
+    for p, (n, k) in enumerate(((I, H), (I, H), (H, I))):
+        d.stride_codes[p] = n * k // 2
+        d.stride_scales[p] = n * k // 256
+    return d
+
+
+@no_gpu_only
+def test_moe_validation_errors_before_launch():
+    L = tq._L
+
+    def call(d, t=2, topk=2, ws_bytes=None, flags=0, x=FAKE, out=FAKE, ws=FAKE):
+        if ws_bytes is None:
+            ws_bytes = L.tq_moe_workspace_bytes(ctypes.byref(d), t, topk)
+        return L.tq_moe_grouped(ctypes.byref(d), x, t, FAKE, FAKE, topk, out, ws, ws_bytes, flags, None)
+
+    d = _experts_desc()
+    need = L.tq_moe_workspace_bytes(ctypes.byref(d), 2, 2)
+    assert need > 0
+    assert call(d, ws_bytes=need - 1) == tq.TQ_ERR_WORKSPACE
+    assert call(d, topk=9) == tq.TQ_ERR_INVALID          # topk > n_experts
+    assert call(d, topk=0) == tq.TQ_ERR_INVALID
+    assert call(d, t=-1) == tq.TQ_ERR_INVALID
+    assert call(d, flags=3) == tq.TQ_ERR_INVALID
+    assert call(d, flags=8) == tq.TQ_ERR_INVALID
+    assert call(d, x=FAKE + 4) == tq.TQ_ERR_ALIGN
+    assert call(d, ws=FAKE + 128) == tq.TQ_ERR_ALIGN
+    assert call(d, x=None) == tq.TQ_ERR_INVALID
+    bad = _experts_desc(H=300)
+    assert call(bad) == tq.TQ_ERR_INVALID
+    bad = _experts_desc(); bad.stride_codes[1] = 100
+    assert call(bad) == tq.TQ_ERR_ALIGN
+    bad = _experts_desc(E=0)
+    assert call(bad) == tq.TQ_ERR_INVALID
+    bad = _experts_desc(); bad.down_scales = None
+    assert call(bad) == tq.TQ_ERR_INVALID
+    assert call(d, t=0) == tq.TQ_OK                      # no-op
+
+
+def test_moe_workspace_layout_is_consistent():
+    d = _experts_desc(E=256, H=4096, I=2048)
+    lay = tq.tq_moe_layout()
+    assert tq._L.tq_moe_workspace_layout(ctypes.byref(d), 32, 8, ctypes.byref(lay)) == tq.TQ_OK
+    S = 32 * 8
+    offs = sorted((getattr(lay, n), n) for n in ("xq", "xd", "xb", "h", "hq", "hd", "hb", "yd"))
+    sizes = {"xq": 32 * 4096, "xd": 32 * 16 * 4, "xb": 32 * 16 * 4, "h": S * 2048 * 4, "hq": S * 2048,
+             "hd": S * 8 * 4, "hb": S * 8 * 4, "yd": S * 4096 * 4}
+    for (o1, n1), (o2, _) in zip(offs, offs[1:]):
+        assert o1 % 256 == 0 and o1 + sizes[n1] <= o2
+    assert offs[-1][0] + sizes[offs[-1][1]] <= lay.total
+    assert lay.total == tq._L.tq_moe_workspace_bytes(ctypes.byref(d), 32, 8)
+    assert lay.flags < offs[0][0]

@@ -1,0 +1,190 @@
+"""GPU parity of the routed-expert MoE layer (tq_moe_grouped) against the CPU oracle.
+
+Staged parity, each GPU stage checked against the oracle applied to the GPU's previous
+stage (so every integer decision is compared on identical inputs):
+  xq, xd, xb  == oracle.quantize(x)                              (bit-exact)
+  h           ~= oracle SiLU(g) * u                               (bound from 1e-5 on g, u)
+  hq, hd, hb  == oracle.quantize(GPU h)                          (bit-exact)
+  yd          ~= oracle dot pass of W_down on GPU (hq, hd)       (1e-5 of abs terms)
+  out         ~= sum_j w_j * GPU yd_j in ascending j             (1e-5 of abs terms)
+End to end, the fully independent oracle output is compared for every token whose
+requantized hidden codes agree with the oracle's own; where a fp32 ulp in g or u moves
+an h value across a rounding boundary, one code differs by 1 (the rate is asserted to
+be tiny and each such token is covered by the staged check)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as oracle_pkg
+from gpu_util import announce, assert_close, device, host_experts, synth_experts, ws_views
+from synth import gen
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def tq():
+    device()
+    from paper_2608_08910_amd import tq as _tq
+    return _tq
+
+
+@pytest.fixture(scope="module")
+def experts_h4096(tq):
+    """The 256 routed experts (hidden 4096, inter 2048) of the decode workloads, seed 0."""
+    announce("synth 256 experts h4096 i2048")
+    ex = synth_experts(tq, gen.SEED, 0, 256, 4096, 2048)
+    torch.cuda.synchronize()
+    return ex
+
+
+def run_moe(tq, ex, x, idx, w, flags=0):
+    t, topk = idx.shape
+    xd = torch.from_numpy(np.ascontiguousarray(x)).cuda()
+    idd = torch.from_numpy(np.ascontiguousarray(idx)).cuda()
+    wd = torch.from_numpy(np.ascontiguousarray(w)).cuda()
+    out = torch.empty((t, ex.hidden), dtype=torch.float32, device="cuda")
+    ws = torch.empty(tq.tq_moe_workspace_bytes(ex, t, topk), dtype=torch.uint8, device="cuda")
+    tq.tq_moe_grouped(ex, xd, idd, wd, out, ws, flags)
+    torch.cuda.synchronize()
+    return out, ws
+
+
+def check_moe(tq, o, ex, get_expert, x, idx, w, out, ws, tokens):
+    """Staged + end-to-end parity on the listed tokens."""
+    t, topk = idx.shape
+    V = {k: v.cpu().numpy() for k, v in ws_views(tq, ex, ws, t, topk).items()}
+    out = out.cpu().numpy()
+    oq, od, ob = o.quantize(x[tokens])
+    assert np.array_equal(V["xq"][tokens], oq)
+    assert np.array_equal(V["xd"][tokens].view(np.uint32), od.view(np.uint32))
+    assert np.array_equal(V["xb"][tokens], ob)
+    ref_out, ref_abs, stages = o.moe(x, idx, w, get_expert, tokens=tokens)
+    flips = 0
+    codes = 0
+    flipped_tokens = set()
+    by_expert = {}
+    for tk in tokens:
+        for j in range(topk):
+            by_expert.setdefault(int(idx[tk, j]), []).append((tk, j))
+    for e in sorted(by_expert):
+        down = get_expert(e)["down"]
+        for tk, j in by_expert[e]:
+            s = tk * topk + j
+            st = stages[(tk, j)]
+            g, u, ga, ua = st["g"], st["u"], st["g_abs"], st["u_abs"]
+            tol_h = 1e-5 * (1.1 * ga * np.abs(u) + np.abs(o.silu(g)) * ua) + 2e-6 * np.abs(st["h"]) + 1e-30
+            err = np.abs(V["h"][s].astype(np.float64) - st["h"])
+            assert (err <= tol_h).all(), f"h slot {s}: worst {(err / tol_h).max()}"
+            hq, hd, hb = o.quantize(V["h"][s])
+            assert np.array_equal(V["hq"][s], hq[0]) and np.array_equal(V["hd"][s].view(np.uint32), hd[0].view(np.uint32))
+            assert np.array_equal(V["hb"][s], hb[0])
+            yr, ya = o.gemv(*down, V["hq"][s], V["hd"][s])
+            assert_close(V["yd"][s], yr[0], ya[0], what=f"yd slot {s}")
+            diff = int((V["hq"][s] != st["qh"]).sum())
+            codes += V["hq"][s].size
+            if diff:
+                flipped_tokens.add(tk)
+                flips += diff
+                assert np.abs(V["hq"][s].astype(int) - st["qh"].astype(int)).max() <= 1
+    for n_t, tk in enumerate(tokens):
+        yd = V["yd"][tk * topk:(tk + 1) * topk].astype(np.float64)
+        wt = w[tk].astype(np.float64)[:, None]
+        staged = np.zeros(ex.hidden)
+        for j in range(topk):  # ascending j, as the layer defines the sum
+            staged += wt[j] * yd[j]
+        staged_abs = (np.abs(wt) * np.abs(yd)).sum(0)
+        assert_close(out[tk], staged, staged_abs + 1e-30, rtol=1e-5, what=f"out token {tk} (staged)")
+        if tk not in flipped_tokens:
+            assert_close(out[tk], ref_out[n_t], ref_abs[n_t] + 1e-30, rtol=1e-5, what=f"out token {tk}")
+    assert flips <= max(2, 1e-3 * codes), f"{flips} requantized codes differ from the oracle's"
+    return flips
+
+
+def test_moe_small_host_packed(tq, oracle):
+    E, H, I, T, topk = 6, 512, 768, 7, 3
+    ex, logical = host_experts(tq, oracle, E, H, I, seed=5)
+    rng = np.random.default_rng(6)
+    x = (rng.standard_normal((T, H)) * 2).astype(np.float32)
+    idx = np.stack([rng.choice(E, topk, replace=False) for _ in range(T)]).astype(np.int32)
+    idx[3] = [2, 2, 5]  # a duplicated expert in one token's list: two separate slots
+    w = rng.uniform(0.1, 1.0, (T, topk)).astype(np.float32)
+    announce("moe small host-packed")
+    out, ws = run_moe(tq, ex, x, idx, w)
+    check_moe(tq, oracle, ex, lambda e: logical[e], x, idx, w, out, ws, list(range(T)))
+    assert tq.tq_moe_status(ws, ex, T, topk) == 0
+
+
+def test_moe_invalid_expert_ids_flagged_and_skipped(tq, oracle):
+    E, H, I, T, topk = 4, 256, 256, 3, 2
+    ex, logical = host_experts(tq, oracle, E, H, I, seed=8)
+    rng = np.random.default_rng(9)
+    x = rng.standard_normal((T, H)).astype(np.float32)
+    idx = np.array([[0, 1], [-1, 2], [3, E]], np.int32)
+    w = np.full((T, topk), 0.5, np.float32)
+    announce("moe invalid ids")
+    out, ws = run_moe(tq, ex, x, idx, w)
+    assert tq.tq_moe_status(ws, ex, T, topk) & 1
+    # valid slots only: the same as routing token 1 to expert 2 alone, token 2 to expert 3
+    ref, ref_abs, _ = oracle.moe(x, np.array([[0, 1], [2, 2], [3, 3]], np.int32),
+                                 np.array([[0.5, 0.5], [0.5, 0.0], [0.5, 0.0]], np.float32), lambda e: logical[e])
+    assert_close(out.cpu().numpy(), ref, ref_abs + 1e-30, what="out with invalid slots")
+
+
+def test_moe_zero_tokens_and_top1(tq, oracle):
+    E, H, I = 3, 256, 512
+    ex, logical = host_experts(tq, oracle, E, H, I, seed=11)
+    x = np.zeros((0, H), np.float32)
+    run_moe(tq, ex, x, np.zeros((0, 1), np.int32), np.zeros((0, 1), np.float32))
+    rng = np.random.default_rng(12)
+    x = rng.standard_normal((2, H)).astype(np.float32)
+    idx = np.array([[1], [2]], np.int32)
+    w = np.ones((2, 1), np.float32)
+    announce("moe top-1")
+    out, ws = run_moe(tq, ex, x, idx, w)
+    check_moe(tq, oracle, ex, lambda e: logical[e], x, idx, w, out, ws, [0, 1])
+
+
+def test_moe_decode_batch1_uniform(tq, oracle, experts_h4096):
+    """One MoE layer at decode, batch 1: 256 experts, hidden 4096, inter 2048, top-8
+    uniform without replacement, softmax weights over N(0,1) logits, seed 0."""
+    c = gen.CONFIGS[1]
+    x = gen.activations(gen.SEED, 0, c["tokens"], c["hidden"])
+    idx, w = gen.routing(gen.SEED, 0, c["tokens"], c["experts"], c["topk"], c["routing"])
+    announce("moe decode t=1 top-8 uniform")
+    out, ws = run_moe(tq, experts_h4096, x, idx, w)
+    get = oracle_pkg.expert_getter(gen.SEED, 0, c["hidden"], c["inter"], oracle)
+    check_moe(tq, oracle, experts_h4096, get, x, idx, w, out, ws, [0])
+    out2, _ = run_moe(tq, experts_h4096, x, idx, w)
+    assert torch.equal(out, out2)  # bitwise reproducible
+
+
+def test_moe_decode_batch32_zipf(tq, oracle, experts_h4096):
+    """Batched decode: 32 tokens, top-8 with Zipf(1.1) expert popularity, seed 0."""
+    c = gen.CONFIGS[2]
+    x = gen.activations(gen.SEED, 0, c["tokens"], c["hidden"])
+    idx, w = gen.routing(gen.SEED, 0, c["tokens"], c["experts"], c["topk"], c["routing"])
+    announce("moe decode t=32 top-8 zipf")
+    out, ws = run_moe(tq, experts_h4096, x, idx, w)
+    get = oracle_pkg.expert_getter(gen.SEED, 0, c["hidden"], c["inter"], oracle)
+    check_moe(tq, oracle, experts_h4096, get, x, idx, w, out, ws, list(range(c["tokens"])))
+
+
+def test_moe_prefill_2048_sampled(tq, oracle, experts_h4096):
+    """Prefill: 2048 tokens, Zipf top-8, activations scaled per token by a log-uniform
+    factor in [0.1, 10]. The whole layer runs on the GPU; the oracle checks a sample of
+    tokens (all their slots and stages) plus every token's quantized input."""
+    c = gen.CONFIGS[3]
+    x = gen.activations(gen.SEED, 0, c["tokens"], c["hidden"]) * gen.token_factors(gen.SEED, c["tokens"])[:, None]
+    idx, w = gen.routing(gen.SEED, 0, c["tokens"], c["experts"], c["topk"], c["routing"])
+    announce("moe prefill t=2048")
+    out, ws = run_moe(tq, experts_h4096, x, idx, w)
+    V = ws_views(tq, experts_h4096, ws, c["tokens"], c["topk"])
+    oq, od, _ = oracle.quantize(x)
+    assert np.array_equal(V["xq"].cpu().numpy(), oq)
+    # tokens routed to the hottest expert, the coldest used one, and a spread
+    counts = np.bincount(idx.ravel(), minlength=c["experts"])
+    cold = int(np.where(counts > 0)[0][np.argmin(counts[counts > 0])])
+    tokens = sorted(set([int(np.where((idx == 0).any(1))[0][0]), int(np.where((idx == cold).any(1))[0][0]), 0, 777, 2047]))
+    get = oracle_pkg.expert_getter(gen.SEED, 0, c["hidden"], c["inter"], oracle)
+    check_moe(tq, oracle, experts_h4096, get, x, idx, w, out, ws, tokens)
