@@ -28,17 +28,26 @@ __global__ __launch_bounds__(256) void k_gemv(const uint8_t* __restrict__ codes,
   if (row0 >= n) return;
   const int64_t k = (int64_t)kb * 256;
 
+  // Loads are unconditional from clamped addresses; invalid lanes are zeroed by a select
+  // (a predicated load becomes a branch that serializes the loads).
   uint4 w[RPW][NL];
   float s[RPW][NL];
 #pragma unroll
-  for (int r = 0; r < RPW; ++r)
+  for (int r = 0; r < RPW; ++r) {
+    const int64_t rc = min(row0 + r, n - 1);
+    const uint8_t* rowcodes = codes + rc * kb * 128;
+    const uint16_t* rowscales = scales + rc * kb;
 #pragma unroll
     for (int i = 0; i < NL; ++i) {
-      const int b = 8 * i + g, row = row0 + r;
-      const bool ok = b < kb && row < n;
-      w[r][i] = ok ? ldg16(codes + ((int64_t)row * kb + b) * 128 + cp * 16) : make_uint4(0, 0, 0, 0);
-      s[r][i] = ok ? f16_bits_to_f32(scales[(int64_t)row * kb + b]) : 0.0f;
+      const int b = 8 * i + g;
+      const bool ok = b < kb && row0 + r < n;
+      const int bc = b < kb ? b : kb - 1;
+      const uint4 raw = ldg16(rowcodes + bc * 128 + cp * 16);
+      const float sv = f16_bits_to_f32(rowscales[bc]);
+      w[r][i] = ok ? raw : make_uint4(0, 0, 0, 0);
+      s[r][i] = ok ? sv : 0.0f;
     }
+  }
 
   for (int t0 = 0; t0 < t; t0 += NT) {
     int qa[NT][NL][8];
@@ -49,19 +58,18 @@ __global__ __launch_bounds__(256) void k_gemv(const uint8_t* __restrict__ codes,
 #pragma unroll
       for (int i = 0; i < NL; ++i) {
         const int tok = t0 + tt, b = 8 * i + g;
-        if (tok < t && b < kb) {
-          const int4* p = reinterpret_cast<const int4*>(q + tok * k + b * 256 + cp * 32);
-          const int4 lo = p[0], hi = p[1];
-          qa[tt][i][0] = lo.x; qa[tt][i][1] = lo.y; qa[tt][i][2] = lo.z; qa[tt][i][3] = lo.w;
-          qa[tt][i][4] = hi.x; qa[tt][i][5] = hi.y; qa[tt][i][6] = hi.z; qa[tt][i][7] = hi.w;
-          dd[tt][i] = d[(int64_t)tok * kb + b];
-          bb[tt][i] = bsum[(int64_t)tok * kb + b];
-        } else {
-#pragma unroll
-          for (int m = 0; m < 8; ++m) qa[tt][i][m] = 0;
-          dd[tt][i] = 0.0f;
-          bb[tt][i] = 0;
-        }
+        const bool ok = tok < t && b < kb;
+        const int64_t tc = min(tok, t - 1);
+        const int bc = b < kb ? b : kb - 1;
+        const int4* p = reinterpret_cast<const int4*>(q + tc * k + bc * 256 + cp * 32);
+        const int4 lo = p[0], hi = p[1];
+        const float dv = d[tc * kb + bc];
+        const int bv = bsum[tc * kb + bc];
+        qa[tt][i][0] = ok ? lo.x : 0; qa[tt][i][1] = ok ? lo.y : 0; qa[tt][i][2] = ok ? lo.z : 0;
+        qa[tt][i][3] = ok ? lo.w : 0; qa[tt][i][4] = ok ? hi.x : 0; qa[tt][i][5] = ok ? hi.y : 0;
+        qa[tt][i][6] = ok ? hi.z : 0; qa[tt][i][7] = ok ? hi.w : 0;
+        dd[tt][i] = ok ? dv : 0.0f;
+        bb[tt][i] = ok ? bv : 0;
       }
 #pragma unroll
     for (int r = 0; r < RPW; ++r) {

@@ -6,13 +6,15 @@
 //
 // Stages (one kernel each, all on the caller's stream; no host synchronization):
 //   prologue  quantize x per 256-block, and (one extra workgroup) dispatch the routing:
-//             per-expert slot counts, the active-expert list, slot lists grouped by
-//             expert, task counts; zero the work tickets.
-//   gate_up   dynamic work queue over (active expert, row tile): a wave loads RPW rows of
+//             per-expert slot counts, the active-expert list (hottest first when a step
+//             has several tokens), slot lists grouped by expert, task counts.
+//   gate_up   static work queue over (active expert, row tile), tasks in rank order
+//             strided over the grid (no atomics: a device-scope counter serializes
+//             at one address across the 8 XCDs): a wave loads RPW rows of
 //             gate and of up (each byte read once per step), walks the expert's tokens NT
 //             at a time, and writes h = SiLU(g) * u per slot.
 //   requant   quantize h per 256-block (same quantizer as x).
-//   down      dynamic work queue over (active expert, row tile) of the down projection,
+//   down      the same queue over (active expert, row tile) of the down projection,
 //             writing y[slot][row].
 //   combine   out[t] = sum_j w[t][j] * y[t*topk + j] in ascending j (fixed order: no
 //             floating-point atomics, bitwise reproducible).
@@ -29,7 +31,7 @@ constexpr int kNumStages = 5;
 static const char* const kStageNames[kNumStages] = {"prologue", "gate_up", "requant", "down", "combine"};
 
 // Control words at the start of the workspace.
-enum Ctrl { kFlags = 0, kNActive = 1, kTasksGU = 2, kTasksDn = 3, kTicketGU = 4, kTicketDn = 5, kNValid = 6, kCtrlWords = 64 };
+enum Ctrl { kFlags = 0, kNActive = 1, kTasksGU = 2, kTasksDn = 3, kNValid = 4, kCtrlWords = 64 };
 
 struct Layout {
   size_t ctrl, active, act_off, slot_list, xq, xd, xb, h, hq, hd, hb, yd, total;
@@ -97,7 +99,12 @@ __device__ __forceinline__ void quantize_wave_blocks(const float* __restrict__ x
   }
 }
 
-// The lane's activation slice of one token: for load i, block 8i + g, chunk cp.
+// Loads are issued unconditionally from clamped (always valid) addresses and invalid
+// lanes are zeroed with a select afterwards: a predicated load becomes a branch, and the
+// compiler then waits for each load before issuing the next.
+
+// The lane's activation slice of one token: for load i, block 8i + g, chunk cp. The row
+// pointers are those of a valid token; `ok` zeroes the slice.
 template <int NL>
 __device__ __forceinline__ void load_acts(const int8_t* __restrict__ qrow, const float* __restrict__ drow,
                                           const int32_t* __restrict__ brow, int kb, int g, int cp, bool ok,
@@ -105,31 +112,32 @@ __device__ __forceinline__ void load_acts(const int8_t* __restrict__ qrow, const
 #pragma unroll
   for (int i = 0; i < NL; ++i) {
     const int b = 8 * i + g;
-    if (ok && b < kb) {
-      const int4* p = reinterpret_cast<const int4*>(qrow + b * 256 + cp * 32);
-      const int4 lo = p[0], hi = p[1];
-      qa[i][0] = lo.x; qa[i][1] = lo.y; qa[i][2] = lo.z; qa[i][3] = lo.w;
-      qa[i][4] = hi.x; qa[i][5] = hi.y; qa[i][6] = hi.z; qa[i][7] = hi.w;
-      dd[i] = drow[b];
-      bb[i] = brow[b];
-    } else {
-#pragma unroll
-      for (int m = 0; m < 8; ++m) qa[i][m] = 0;
-      dd[i] = 0.0f;
-      bb[i] = 0;
-    }
+    const bool v = ok && b < kb;
+    const int bc = b < kb ? b : kb - 1;
+    const int4* p = reinterpret_cast<const int4*>(qrow + bc * 256 + cp * 32);
+    const int4 lo = p[0], hi = p[1];
+    const float dv = drow[bc];
+    const int bv = brow[bc];
+    qa[i][0] = v ? lo.x : 0; qa[i][1] = v ? lo.y : 0; qa[i][2] = v ? lo.z : 0; qa[i][3] = v ? lo.w : 0;
+    qa[i][4] = v ? hi.x : 0; qa[i][5] = v ? hi.y : 0; qa[i][6] = v ? hi.z : 0; qa[i][7] = v ? hi.w : 0;
+    dd[i] = v ? dv : 0.0f;
+    bb[i] = v ? bv : 0;
   }
 }
 
+// One row's lane slice of codes and scales; rowcodes/rowscales point at a valid row.
 template <int NL>
-__device__ __forceinline__ void load_row(const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
-                                         int64_t row, int kb, int g, int cp, bool ok, uint4 (&w)[NL], float (&s)[NL]) {
+__device__ __forceinline__ void load_row(const uint8_t* __restrict__ rowcodes, const uint16_t* __restrict__ rowscales,
+                                         int kb, int g, int cp, bool ok, uint4 (&w)[NL], float (&s)[NL]) {
 #pragma unroll
   for (int i = 0; i < NL; ++i) {
     const int b = 8 * i + g;
     const bool v = ok && b < kb;
-    w[i] = v ? ldg16(codes + (row * kb + b) * 128 + cp * 16) : make_uint4(0, 0, 0, 0);
-    s[i] = v ? f16_bits_to_f32(scales[row * kb + b]) : 0.0f;
+    const int bc = b < kb ? b : kb - 1;
+    const uint4 raw = ldg16(rowcodes + bc * 128 + cp * 16);
+    const float sv = f16_bits_to_f32(rowscales[bc]);
+    w[i] = v ? raw : make_uint4(0, 0, 0, 0);
+    s[i] = v ? sv : 0.0f;
   }
 }
 
@@ -181,14 +189,18 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
     quantize_wave_blocks(x, nblocks, (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6), A.xq, A.xd, A.xb);
     return;
   }
-  __shared__ int s_cnt[kMaxExperts];
-  __shared__ int s_base[kMaxExperts];
-  __shared__ int s_scan_a[256], s_scan_s[256];
-  __shared__ int s_bad;
+  __shared__ int s_cnt[kMaxExperts];   // slots per expert
+  __shared__ int s_base[kMaxExperts];  // rank of an active expert, then its slot cursor
+  __shared__ int s_ebr[kMaxExperts];   // expert of each rank
+  __shared__ int s_scan[256];
+  __shared__ int s_nact, s_bad;
   const int tid = threadIdx.x, E = A.n_experts;
   const int64_t S = A.t * A.topk;
   for (int e = tid; e < E; e += 256) s_cnt[e] = 0;
-  if (tid == 0) s_bad = 0;
+  if (tid == 0) {
+    s_bad = 0;
+    s_nact = 0;
+  }
   __syncthreads();
   for (int64_t s = tid; s < S; s += 256) {
     const int e = A.topk_idx[s];
@@ -196,45 +208,58 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
     else s_bad = 1;
   }
   __syncthreads();
-  // exclusive scan of (active experts, slots) over contiguous expert ranges per thread
-  const int per = (E + 255) / 256;
-  const int e0 = min(E, tid * per), e1 = min(E, e0 + per);
-  int na = 0, ns = 0;
-  for (int e = e0; e < e1; ++e) {
-    na += s_cnt[e] > 0;
-    ns += s_cnt[e];
+  // Rank the active experts. With more than one token per step, hottest first (count
+  // descending, id ascending): the work queues below hand out tasks in rank order, so
+  // the longest tasks start first, one per workgroup. One token: id order.
+  const bool by_count = A.t > 1 && E <= 1024;
+  for (int e = tid; e < E; e += 256) {
+    const int c = s_cnt[e];
+    int r = -1;
+    if (c > 0) {
+      r = 0;
+      if (by_count) {
+        for (int e2 = 0; e2 < E; ++e2) {
+          const int c2 = s_cnt[e2];
+          r += (c2 > c) | ((c2 == c) & (e2 < e));
+        }
+      } else {
+        for (int e2 = 0; e2 < e; ++e2) r += s_cnt[e2] > 0;
+      }
+      s_ebr[r] = e;
+      atomicAdd(&s_nact, 1);
+    }
+    s_base[e] = r;
   }
-  s_scan_a[tid] = na;
-  s_scan_s[tid] = ns;
+  __syncthreads();
+  const int n_active = s_nact;
+  // exclusive scan of the slot counts in rank order, contiguous ranks per thread
+  const int per = (n_active + 255) / 256;
+  const int r0 = min(n_active, tid * per), r1 = min(n_active, r0 + per);
+  int ns = 0;
+  for (int r = r0; r < r1; ++r) ns += s_cnt[s_ebr[r]];
+  s_scan[tid] = ns;
   __syncthreads();
   for (int off = 1; off < 256; off <<= 1) {
-    const int va = tid >= off ? s_scan_a[tid - off] : 0;
-    const int vs = tid >= off ? s_scan_s[tid - off] : 0;
+    const int v = tid >= off ? s_scan[tid - off] : 0;
     __syncthreads();
-    s_scan_a[tid] += va;
-    s_scan_s[tid] += vs;
+    s_scan[tid] += v;
     __syncthreads();
   }
-  int a = s_scan_a[tid] - na, pos = s_scan_s[tid] - ns;
-  for (int e = e0; e < e1; ++e) {
-    const int c = s_cnt[e];
-    if (c > 0) {
-      A.active[a] = e;
-      A.act_off[a] = pos;
-      s_base[e] = pos;
-      ++a;
-      pos += c;
-    }
+  int pos = s_scan[tid] - ns;
+  for (int r = r0; r < r1; ++r) {
+    const int e = s_ebr[r];
+    A.active[r] = e;
+    A.act_off[r] = pos;
+    s_base[e] = pos;  // rank no longer needed: becomes the expert's slot cursor
+    pos += s_cnt[e];
   }
   if (tid == 255) {
-    const int n_active = s_scan_a[255], n_valid = s_scan_s[255];
+    const int n_valid = s_scan[255];
     A.act_off[n_active] = n_valid;
     A.ctrl[kNActive] = n_active;
     A.ctrl[kNValid] = n_valid;
     A.ctrl[kTasksGU] = n_active * A.tiles_gu;
     A.ctrl[kTasksDn] = n_active * A.tiles_dn;
-    A.ctrl[kTicketGU] = 0;
-    A.ctrl[kTicketDn] = 0;
     A.ctrl[kFlags] = s_bad ? 1 : 0;
   }
   __syncthreads();
@@ -258,16 +283,11 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
 
 template <int NL, int NT, int RPW>
 __global__ __launch_bounds__(256) void k_moe_gateup(MoeArgs A) {
-  __shared__ int s_task;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int g = lane >> 3, cp = lane & 7;
   const int kb = A.hidden / 256, I = A.inter;
-  for (;;) {
-    if (threadIdx.x == 0) s_task = atomicAdd(&A.ctrl[kTicketGU], 1);
-    __syncthreads();
-    const int task = s_task;
-    __syncthreads();
-    if (task >= A.ctrl[kTasksGU]) return;
+  const int n_tasks = A.ctrl[kTasksGU];
+  for (int task = blockIdx.x; task < n_tasks; task += gridDim.x) {
     const int a = task / A.tiles_gu, tile = task - a * A.tiles_gu;
     const int64_t e = A.active[a];
     const int off = A.act_off[a], cnt = A.act_off[a + 1] - off;
@@ -281,8 +301,9 @@ __global__ __launch_bounds__(256) void k_moe_gateup(MoeArgs A) {
     float sg[RPW][NL], su[RPW][NL];
 #pragma unroll
     for (int r = 0; r < RPW; ++r) {
-      load_row<NL>(gc, gs, row0 + r, kb, g, cp, row0 + r < I, wg[r], sg[r]);
-      load_row<NL>(uc, us, row0 + r, kb, g, cp, row0 + r < I, wu[r], su[r]);
+      const int64_t row = min(row0 + r, I - 1);
+      load_row<NL>(gc + row * kb * 128, gs + row * kb, kb, g, cp, row0 + r < I, wg[r], sg[r]);
+      load_row<NL>(uc + row * kb * 128, us + row * kb, kb, g, cp, row0 + r < I, wu[r], su[r]);
     }
     for (int c0 = 0; c0 < cnt; c0 += NT) {
       int qa[NT][NL][8];
@@ -292,7 +313,7 @@ __global__ __launch_bounds__(256) void k_moe_gateup(MoeArgs A) {
 #pragma unroll
       for (int tt = 0; tt < NT; ++tt) {
         const bool ok = c0 + tt < cnt;
-        slot[tt] = ok ? A.slot_list[off + c0 + tt] : 0;
+        slot[tt] = A.slot_list[off + min(c0 + tt, cnt - 1)];
         const int64_t tok = slot[tt] / A.topk;
         load_acts<NL>(A.xq + tok * A.hidden, A.xd + tok * kb, A.xb + tok * kb, kb, g, cp, ok, qa[tt], dd[tt], bb[tt]);
       }
@@ -315,16 +336,11 @@ __global__ __launch_bounds__(256) void k_moe_gateup(MoeArgs A) {
 
 template <int NL, int NT, int RPW>
 __global__ __launch_bounds__(256) void k_moe_down(MoeArgs A) {
-  __shared__ int s_task;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int g = lane >> 3, cp = lane & 7;
   const int kb = A.inter / 256, H = A.hidden;
-  for (;;) {
-    if (threadIdx.x == 0) s_task = atomicAdd(&A.ctrl[kTicketDn], 1);
-    __syncthreads();
-    const int task = s_task;
-    __syncthreads();
-    if (task >= A.ctrl[kTasksDn]) return;
+  const int n_tasks = A.ctrl[kTasksDn];
+  for (int task = blockIdx.x; task < n_tasks; task += gridDim.x) {
     const int a = task / A.tiles_dn, tile = task - a * A.tiles_dn;
     const int64_t e = A.active[a];
     const int off = A.act_off[a], cnt = A.act_off[a + 1] - off;
@@ -335,7 +351,10 @@ __global__ __launch_bounds__(256) void k_moe_down(MoeArgs A) {
     uint4 w[RPW][NL];
     float s[RPW][NL];
 #pragma unroll
-    for (int r = 0; r < RPW; ++r) load_row<NL>(dc, ds, row0 + r, kb, g, cp, row0 + r < H, w[r], s[r]);
+    for (int r = 0; r < RPW; ++r) {
+      const int64_t row = min(row0 + r, H - 1);
+      load_row<NL>(dc + row * kb * 128, ds + row * kb, kb, g, cp, row0 + r < H, w[r], s[r]);
+    }
     for (int c0 = 0; c0 < cnt; c0 += NT) {
       int qa[NT][NL][8];
       float dd[NT][NL];
@@ -344,7 +363,7 @@ __global__ __launch_bounds__(256) void k_moe_down(MoeArgs A) {
 #pragma unroll
       for (int tt = 0; tt < NT; ++tt) {
         const bool ok = c0 + tt < cnt;
-        slot[tt] = ok ? A.slot_list[off + c0 + tt] : 0;
+        slot[tt] = A.slot_list[off + min(c0 + tt, cnt - 1)];
         const int64_t sl = slot[tt];
         load_acts<NL>(A.hq + sl * A.inter, A.hd + sl * kb, A.hb + sl * kb, kb, g, cp, ok, qa[tt], dd[tt], bb[tt]);
       }
@@ -518,7 +537,7 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   A.tiles_dn = (ex->hidden + 4 * rpw_dn(nl_dn) - 1) / (4 * rpw_dn(nl_dn));
   const int64_t S = t * topk;
   const int64_t max_active = std::min<int64_t>(S, ex->n_experts);
-  const int64_t cap = 256 * 8;  // enough resident workgroups to fill 256 CUs
+  const int64_t cap = 256 * 16;  // workgroups per launch; the rest are strided over them
   const unsigned g_gu = (unsigned)std::min<int64_t>(max_active * A.tiles_gu, cap);
   const unsigned g_dn = (unsigned)std::min<int64_t>(max_active * A.tiles_dn, cap);
   const int64_t xblocks = t * (ex->hidden / 256), hblocks = S * (ex->inter / 256);

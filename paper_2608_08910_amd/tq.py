@@ -261,6 +261,9 @@ def tq_moe_grouped_timed(ex: TqExperts, x, topk_idx, topk_w, out, ws, events, fl
     n = tq_moe_stage_count() + 1
     if len(events) != n:
         raise ValueError(f"need {n} events")
+    for ev in events:  # torch creates the HIP event on its first record
+        if ev.cuda_event == 0:
+            ev.record()
     arr = (_vp * n)(*[ev.cuda_event for ev in events])
     _ok(_L.tq_moe_grouped_timed(*_moe_args(ex, x, topk_idx, topk_w, out, ws), flags, _stream(stream), arr))
 
