@@ -151,18 +151,21 @@ def main():
     # kernel so the GPU runs the stages back to back
     nst = tq.tq_moe_stage_count()
     names = [tq.tq_moe_stage_name(i) for i in range(nst)]
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nst + 1)] for _ in range(P)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * nst)] for _ in range(P)]
     torch.cuda.synchronize()
     torch.cuda._sleep(int(2.4e9 * 0.05))  # ~50 ms of queue head-room
     for j in range(P):
         i = W + (j % K)
         tq.tq_moe_grouped_timed(ex, x_all[i], idx_all[i], w_all[i], out, ws, evs[j])
     torch.cuda.synchronize()
-    stage_ms = {n: float(np.mean([evs[j][si].elapsed_time(evs[j][si + 1]) for j in range(P)])) for si, n in enumerate(names)}
+    stage_ms = {n: float(np.mean([evs[j][2 * si].elapsed_time(evs[j][2 * si + 1]) for j in range(P)]))
+                for si, n in enumerate(names)}
     gu = names.index("gate_up")
     gu_ms = stage_ms["gate_up"]
+    # gate_up moves the routed experts' gate and up codes + scales, reads x (fp32) and
+    # writes h (fp32, one row per slot)
     gu_bytes = float(np.mean([len(np.unique(sched[W + (j % K)][0])) for j in range(P)])) * 2 * matrix_bytes(I, H) \
-        + T * H + T * (H // 256) * 8 + T * topk * I * 4
+        + T * H * 4 + T * topk * I * 4
     achieved = gu_bytes / (gu_ms * 1e-3) / 1e9
 
     res = {

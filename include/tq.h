@@ -171,10 +171,13 @@ typedef struct {
 tq_status tq_moe_workspace_layout(const tq_experts* ex, int64_t t, int32_t topk,
                                   tq_moe_layout* out);
 
-/* As tq_moe_grouped, and also records host-created HIP events (hipEvent_t, passed as
- * void*) on the stream at the stage boundaries: events[i] before stage i and
- * events[tq_moe_stage_count()] after the last stage. For per-stage timing in
- * benchmarks; events may not be NULL. */
+/* As tq_moe_grouped, and also times each stage with host-created HIP events
+ * (hipEvent_t, passed as void*): events[2*i] and events[2*i + 1] bracket stage i, for
+ * i < tq_moe_stage_count(). A stage's kernel is launched with hipExtLaunchKernelGGL, so
+ * its pair carries that kernel's own start and stop timestamps; a stage with no kernel
+ * on the path taken (a single-token step fuses the prologue, requant and combine into
+ * its two kernels) has its pair recorded back to back. For per-stage timing in
+ * benchmarks; no event may be NULL. */
 int32_t tq_moe_stage_count(void);
 const char* tq_moe_stage_name(int32_t i);
 tq_status tq_moe_grouped_timed(const tq_experts* ex, const float* x, int64_t t,

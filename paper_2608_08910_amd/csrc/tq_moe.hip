@@ -18,6 +18,8 @@
 //             writing y[slot][row].
 //   combine   out[t] = sum_j w[t][j] * y[t*topk + j] in ascending j (fixed order: no
 //             floating-point atomics, bitwise reproducible).
+#include <hip/hip_ext.h>
+
 #include <algorithm>
 
 #include "tq_device.hpp"
@@ -408,6 +410,192 @@ __global__ __launch_bounds__(256) void k_moe_combine(MoeArgs A, float* __restric
 }
 
 // ---------------------------------------------------------------------------------
+// Single-token step (t == 1, topk <= 8): two kernels and no dispatch pass. Each slot
+// is its own task (a duplicated expert is simply computed twice), so the expert comes
+// straight from topk_idx; x is quantized once per workgroup into LDS while the weight
+// loads are in flight; the down kernel requantizes every slot's h into LDS once per
+// workgroup and folds the weighted combine into registers, in ascending slot order
+// (the same fmaf chain as k_moe_combine, so both paths give identical bits).
+// ---------------------------------------------------------------------------------
+
+constexpr int kT1MaxTopk = 8;
+constexpr int kT1MaxHq = 16384;  // topk * inter bytes of requantized hidden held in LDS
+
+// Quantize 256-block `blk` of src into LDS (one block per 8-lane group). The caller has
+// already loaded the lane's 32 values (v), ahead of its weight loads.
+// `store` is group-uniform; the quantization itself runs regardless, so that the loads
+// of v are not sunk into a branch behind the weight loads.
+__device__ __forceinline__ void quantize_to_lds(const float (&v)[32], int blk, int cp, int8_t* s_q, float* s_d,
+                                                int* s_b, bool store = true) {
+  int qw[8];
+  float dd;
+  int bs;
+  quantize_group32(v, qw, dd, bs);
+  if (!store) return;
+  int4* qp = reinterpret_cast<int4*>(s_q + blk * 256 + cp * 32);
+  qp[0] = make_int4(qw[0], qw[1], qw[2], qw[3]);
+  qp[1] = make_int4(qw[4], qw[5], qw[6], qw[7]);
+  if (cp == 0) {
+    s_d[blk] = dd;
+    s_b[blk] = bs;
+  }
+}
+
+__device__ __forceinline__ void load32(const float* p, float (&v)[32]) {
+  const float4* q = reinterpret_cast<const float4*>(p);
+#pragma unroll
+  for (int m = 0; m < 8; ++m) {
+    const float4 f = q[m];
+    v[4 * m + 0] = f.x;
+    v[4 * m + 1] = f.y;
+    v[4 * m + 2] = f.z;
+    v[4 * m + 3] = f.w;
+  }
+}
+
+// WAVES waves per workgroup; each wave owns RPW rows of gate and of up of one slot.
+template <int NL, int RPW, int WAVES>
+__global__ __launch_bounds__(WAVES * 64) void k_t1_gateup(const float* __restrict__ x, MoeArgs A) {
+  __shared__ __attribute__((aligned(16))) int8_t s_q[kMaxK];
+  __shared__ float s_d[kMaxK / 256];
+  __shared__ int s_b[kMaxK / 256];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int g = lane >> 3, cp = lane & 7, gid = wv * 8 + g;
+  const int kb = A.hidden / 256, I = A.inter;
+  const int j = blockIdx.x / A.tiles_gu, tile = blockIdx.x - j * A.tiles_gu;
+  const int e = A.topk_idx[j];
+  const bool valid = e >= 0 && e < A.n_experts;
+  const int64_t ec = valid ? e : 0;
+  const int row0 = (tile * WAVES + wv) * RPW;
+
+  // x first (its wait must not queue behind the weights), then every weight load
+  float v[32];
+  load32(x + min(gid, kb - 1) * 256 + cp * 32, v);
+  __builtin_amdgcn_sched_barrier(0);  // keep these loads ahead of the weights'
+  uint4 wg[RPW][NL], wu[RPW][NL];
+  float sg[RPW][NL], su[RPW][NL];
+  {
+    const uint8_t* gc = A.codes[0] + ec * A.stride_codes[0];
+    const uint8_t* uc = A.codes[1] + ec * A.stride_codes[1];
+    const uint16_t* gs = A.scales[0] + ec * A.stride_scales[0];
+    const uint16_t* us = A.scales[1] + ec * A.stride_scales[1];
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) {
+      const int64_t row = min(row0 + r, I - 1);
+      load_row<NL>(gc + row * kb * 128, gs + row * kb, kb, g, cp, row0 + r < I, wg[r], sg[r]);
+      load_row<NL>(uc + row * kb * 128, us + row * kb, kb, g, cp, row0 + r < I, wu[r], su[r]);
+    }
+  }
+  quantize_to_lds(v, min(gid, kb - 1), cp, s_q, s_d, s_b, gid < kb);
+  for (int blk = gid + WAVES * 8; blk < kb; blk += WAVES * 8) {
+    load32(x + blk * 256 + cp * 32, v);
+    quantize_to_lds(v, blk, cp, s_q, s_d, s_b);
+  }
+  __syncthreads();
+  if (blockIdx.x == 0) {  // stage buffers and the status word, once per call
+    for (int i = threadIdx.x; i < kb * 64; i += WAVES * 64)
+      reinterpret_cast<int*>(A.xq)[i] = reinterpret_cast<const int*>(s_q)[i];
+    for (int i = threadIdx.x; i < kb; i += WAVES * 64) {
+      A.xd[i] = s_d[i];
+      A.xb[i] = s_b[i];
+    }
+    if (threadIdx.x == 0) {
+      int bad = 0;
+      for (int jj = 0; jj < A.topk; ++jj) bad |= (A.topk_idx[jj] < 0) | (A.topk_idx[jj] >= A.n_experts);
+      A.ctrl[kFlags] = bad;
+    }
+  }
+  if (!valid || row0 >= I) return;
+  int qa[NL][8];
+  float dd[NL];
+  int bb[NL];
+  load_acts<NL>(s_q, s_d, s_b, kb, g, cp, true, qa, dd, bb);
+#pragma unroll
+  for (int r = 0; r < RPW; ++r) {
+    const float gv = row_dot<NL>(wg[r], sg[r], qa, dd, bb);
+    const float uv = row_dot<NL>(wu[r], su[r], qa, dd, bb);
+    if (lane == 0 && row0 + r < I) A.h[(int64_t)j * I + row0 + r] = silu_f32(gv) * uv;
+  }
+}
+
+// WAVES waves per workgroup; each wave owns RPW rows of down for every slot.
+template <int NL, int RPW, int TOPK, int WAVES>
+__global__ __launch_bounds__(WAVES * 64) void k_t1_down(MoeArgs A, float* __restrict__ out) {
+  __shared__ __attribute__((aligned(16))) int8_t s_hq[kT1MaxHq];
+  __shared__ float s_hd[kT1MaxHq / 256];
+  __shared__ int s_hb[kT1MaxHq / 256];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int g = lane >> 3, cp = lane & 7, gid = wv * 8 + g;
+  const int kb = A.inter / 256, H = A.hidden, I = A.inter;
+  const int nblk = TOPK * kb;
+  const int row0 = (blockIdx.x * WAVES + wv) * RPW;
+  int64_t ej[TOPK];
+  unsigned vmask = 0;
+#pragma unroll
+  for (int j = 0; j < TOPK; ++j) {
+    const int e = A.topk_idx[j];
+    const bool v = e >= 0 && e < A.n_experts;
+    vmask |= (unsigned)v << j;
+    ej[j] = v ? e : 0;
+  }
+  // this group's first block of h first (an unrouted slot's h is never written: such a
+  // group loads the buffer's first block instead and skips the quantization)
+  const int blk0 = min(gid, nblk - 1);
+  const bool q0 = gid < nblk && ((vmask >> (blk0 / kb)) & 1);
+  float v[32];
+  load32(A.h + (int64_t)(q0 ? blk0 : 0) * 256 + cp * 32, v);
+  __builtin_amdgcn_sched_barrier(0);  // keep these loads ahead of the weights'
+  uint4 w[TOPK][RPW][NL];
+  float s[TOPK][RPW][NL];
+#pragma unroll
+  for (int j = 0; j < TOPK; ++j)
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) {
+      const int64_t row = min(row0 + r, H - 1);
+      load_row<NL>(A.codes[2] + ej[j] * A.stride_codes[2] + row * kb * 128, A.scales[2] + ej[j] * A.stride_scales[2] + row * kb,
+                   kb, g, cp, ((vmask >> j) & 1) && row0 + r < H, w[j][r], s[j][r]);
+    }
+  quantize_to_lds(v, blk0, cp, s_hq, s_hd, s_hb, q0);
+  for (int blk = gid + WAVES * 8; blk < nblk; blk += WAVES * 8) {
+    if (!((vmask >> (blk / kb)) & 1)) continue;
+    load32(A.h + (int64_t)blk * 256 + cp * 32, v);
+    quantize_to_lds(v, blk, cp, s_hq, s_hd, s_hb);
+  }
+  __syncthreads();
+  if (blockIdx.x == 0) {  // stage buffers, once per call
+    for (int i = threadIdx.x; i < TOPK * I / 4; i += WAVES * 64)
+      if ((vmask >> (4 * i / I)) & 1) reinterpret_cast<int*>(A.hq)[i] = reinterpret_cast<const int*>(s_hq)[i];
+    for (int i = threadIdx.x; i < nblk; i += WAVES * 64)
+      if ((vmask >> (i / kb)) & 1) {
+        A.hd[i] = s_hd[i];
+        A.hb[i] = s_hb[i];
+      }
+  }
+  if (row0 >= H) return;
+  float acc[RPW];
+#pragma unroll
+  for (int r = 0; r < RPW; ++r) acc[r] = 0.0f;
+#pragma unroll
+  for (int j = 0; j < TOPK; ++j) {
+    if (!((vmask >> j) & 1)) continue;
+    int qa[NL][8];
+    float dd[NL];
+    int bb[NL];
+    load_acts<NL>(s_hq + j * I, s_hd + j * kb, s_hb + j * kb, kb, g, cp, true, qa, dd, bb);
+    const float wj = A.topk_w[j];
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) {
+      const float y = row_dot<NL>(w[j][r], s[j][r], qa, dd, bb);
+      acc[r] = fmaf(wj, y, acc[r]);
+      if (lane == 0 && row0 + r < H) A.yd[(int64_t)j * H + row0 + r] = y;
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < RPW; ++r)
+    if (lane == 0 && row0 + r < H) out[row0 + r] = acc[r];
+}
+
+// ---------------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------------
 
@@ -451,6 +639,74 @@ static moe_fn pick_down(int nl, int nt) {
   }
 }
 
+constexpr int kT1RpwGU = 4;    // rows of gate and of up per wave, single-token path
+constexpr int kT1WavesGU = 4;  // waves per workgroup
+constexpr int kT1RpwDn = 2;    // rows of down per wave (for every slot), single-token path
+constexpr int kT1WavesDn = 8;
+
+using t1gu_fn = void (*)(const float*, MoeArgs);
+using t1dn_fn = void (*)(MoeArgs, float*);
+
+static t1gu_fn pick_t1_gateup(int nl) {
+  switch (nl) {
+    case 1: return k_t1_gateup<1, kT1RpwGU, kT1WavesGU>;
+    case 2: return k_t1_gateup<2, kT1RpwGU, kT1WavesGU>;
+    case 3: return k_t1_gateup<3, kT1RpwGU / 2, kT1WavesGU>;
+    case 4: return k_t1_gateup<4, kT1RpwGU / 2, kT1WavesGU>;
+    case 5: return k_t1_gateup<5, 1, kT1WavesGU>;
+    case 6: return k_t1_gateup<6, 1, kT1WavesGU>;
+    case 7: return k_t1_gateup<7, 1, kT1WavesGU>;
+    default: return k_t1_gateup<8, 1, kT1WavesGU>;
+  }
+}
+static int t1_rpw_gu(int nl) { return nl <= 2 ? kT1RpwGU : (nl <= 4 ? kT1RpwGU / 2 : 1); }
+
+template <int NL>
+static t1dn_fn pick_t1_down_k(int topk) {
+  switch (topk) {
+    case 1: return k_t1_down<NL, kT1RpwDn, 1, kT1WavesDn>;
+    case 2: return k_t1_down<NL, kT1RpwDn, 2, kT1WavesDn>;
+    case 3: return k_t1_down<NL, kT1RpwDn, 3, kT1WavesDn>;
+    case 4: return k_t1_down<NL, kT1RpwDn, 4, kT1WavesDn>;
+    case 5: return k_t1_down<NL, kT1RpwDn, 5, kT1WavesDn>;
+    case 6: return k_t1_down<NL, kT1RpwDn, 6, kT1WavesDn>;
+    case 7: return k_t1_down<NL, kT1RpwDn, 7, kT1WavesDn>;
+    default: return k_t1_down<NL, kT1RpwDn, 8, kT1WavesDn>;
+  }
+}
+
+// topk * inter <= 16384 bytes of LDS bounds NL: inter <= 16384 / topk.
+static t1dn_fn pick_t1_down(int nl, int topk) {
+  switch (nl) {
+    case 1: return pick_t1_down_k<1>(topk);
+    case 2: return pick_t1_down_k<2>(topk);
+    case 3: case 4: return pick_t1_down_k<4>(topk);
+    default: return pick_t1_down_k<8>(topk);
+  }
+}
+
+// One stage's kernel; with timing events, launched with hipExtLaunchKernelGGL so the
+// start/stop events take the kernel's own dispatch timestamps.
+template <typename F, typename... Args>
+static tq_status launch_stage(void* const* events, int stage, F kernel, dim3 grid, int threads, hipStream_t st,
+                              const char* fn, Args... args) {
+  if (events)
+    hipExtLaunchKernelGGL(kernel, grid, dim3(threads), 0, st, (hipEvent_t)events[2 * stage],
+                          (hipEvent_t)events[2 * stage + 1], 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, dim3(threads), 0, st, args...);
+  return check_launch(fn);
+}
+
+// A stage with no kernel of its own on this path: its event pair is recorded back to back.
+static tq_status empty_stage(void* const* events, int stage, hipStream_t st, const char* fn) {
+  if (!events) return TQ_OK;
+  if (hipEventRecord((hipEvent_t)events[2 * stage], st) != hipSuccess ||
+      hipEventRecord((hipEvent_t)events[2 * stage + 1], st) != hipSuccess)
+    return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
+  return TQ_OK;
+}
+
 static tq_status validate_experts(const tq_experts* ex, const char* fn) {
   if (!ex) return fail(TQ_ERR_INVALID, "%s: null experts descriptor", fn);
   if (ex->n_experts < 1 || ex->n_experts > kMaxExperts)
@@ -485,11 +741,8 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
     return fail(TQ_ERR_INVALID, "%s: bad flags 0x%x", fn, flags);
   if (flags & TQ_MOE_FORCE_MFMA) return fail(TQ_ERR_INVALID, "%s: the MFMA expert path is not available", fn);
   if (t == 0) {
-    if (events) {
-      for (int i = 0; i <= kNumStages; ++i)
-        if (hipEventRecord((hipEvent_t)events[i], (hipStream_t)stream) != hipSuccess)
-          return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
-    }
+    for (int i = 0; i < kNumStages; ++i)
+      if ((st = empty_stage(events, i, (hipStream_t)stream, fn)) != TQ_OK) return st;
     return TQ_OK;
   }
   if (!x || !topk_idx || !topk_w || !out || !ws) return fail(TQ_ERR_INVALID, "%s: null pointer", fn);
@@ -545,24 +798,31 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   hipStream_t stm = (hipStream_t)stream;
 
   (void)hipGetLastError();
-  auto rec = [&](int i) -> bool { return !events || hipEventRecord((hipEvent_t)events[i], stm) == hipSuccess; };
-  if (!rec(0)) return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
-  hipLaunchKernelGGL(k_moe_prologue, dim3(nq + 1), dim3(256), 0, stm, x, A, nq);
-  if ((st = check_launch(fn)) != TQ_OK) return st;
-  if (!rec(1)) return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
-  hipLaunchKernelGGL(pick_gateup(nl_gu, nt), dim3(g_gu), dim3(256), 0, stm, A);
-  if ((st = check_launch(fn)) != TQ_OK) return st;
-  if (!rec(2)) return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
-  hipLaunchKernelGGL(k_moe_requant, dim3((unsigned)((hblocks + 31) / 32)), dim3(256), 0, stm, A, hblocks);
-  if ((st = check_launch(fn)) != TQ_OK) return st;
-  if (!rec(3)) return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
-  hipLaunchKernelGGL(pick_down(nl_dn, nt), dim3(g_dn), dim3(256), 0, stm, A);
-  if ((st = check_launch(fn)) != TQ_OK) return st;
-  if (!rec(4)) return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
+  if (t == 1 && topk <= kT1MaxTopk && (int64_t)topk * ex->inter <= kT1MaxHq && !(flags & TQ_MOE_FORCE_MFMA)) {
+    // single token: gate_up, then down with the requant and the combine fused; the
+    // prologue, requant and combine stages are empty on this path
+    const int rgu = t1_rpw_gu(nl_gu);
+    A.tiles_gu = (ex->inter + kT1WavesGU * rgu - 1) / (kT1WavesGU * rgu);
+    const unsigned tiles_dn = (unsigned)((ex->hidden + kT1WavesDn * kT1RpwDn - 1) / (kT1WavesDn * kT1RpwDn));
+    if ((st = empty_stage(events, 0, stm, fn)) != TQ_OK) return st;
+    if ((st = launch_stage(events, 1, pick_t1_gateup(nl_gu), dim3((unsigned)(topk * A.tiles_gu)), kT1WavesGU * 64, stm,
+                           fn, x, A)) != TQ_OK)
+      return st;
+    if ((st = empty_stage(events, 2, stm, fn)) != TQ_OK) return st;
+    if ((st = launch_stage(events, 3, pick_t1_down(nl_dn, topk), dim3(tiles_dn), kT1WavesDn * 64, stm, fn, A, out)) !=
+        TQ_OK)
+      return st;
+    return empty_stage(events, 4, stm, fn);
+  }
+  if ((st = launch_stage(events, 0, k_moe_prologue, dim3(nq + 1), 256, stm, fn, x, A, nq)) != TQ_OK) return st;
+  if ((st = launch_stage(events, 1, pick_gateup(nl_gu, nt), dim3(g_gu), 256, stm, fn, A)) != TQ_OK) return st;
+  if ((st = launch_stage(events, 2, k_moe_requant, dim3((unsigned)((hblocks + 31) / 32)), 256, stm, fn, A, hblocks)) !=
+      TQ_OK)
+    return st;
+  if ((st = launch_stage(events, 3, pick_down(nl_dn, nt), dim3(g_dn), 256, stm, fn, A)) != TQ_OK) return st;
   const int64_t nout = t * (ex->hidden / 4);
-  hipLaunchKernelGGL(k_moe_combine, dim3((unsigned)((nout + 255) / 256)), dim3(256), 0, stm, A, out);
-  if ((st = check_launch(fn)) != TQ_OK) return st;
-  if (!rec(5)) return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
+  if ((st = launch_stage(events, 4, k_moe_combine, dim3((unsigned)((nout + 255) / 256)), 256, stm, fn, A, out)) != TQ_OK)
+    return st;
   return TQ_OK;
 }
 
@@ -609,7 +869,7 @@ extern "C" tq_status tq_moe_grouped_timed(const tq_experts* ex, const float* x, 
                                           const float* topk_w, int32_t topk, float* out, void* ws, size_t ws_bytes,
                                           int32_t flags, void* stream, void* const* events) {
   if (!events) return tq::fail(TQ_ERR_INVALID, "tq_moe_grouped_timed: events may not be NULL");
-  for (int i = 0; i <= tq::kNumStages; ++i)
+  for (int i = 0; i < 2 * tq::kNumStages; ++i)
     if (!events[i]) return tq::fail(TQ_ERR_INVALID, "tq_moe_grouped_timed: null event %d", i);
   return tq::moe_run(ex, x, t, topk_idx, topk_w, topk, out, ws, ws_bytes, flags, stream, events,
                      "tq_moe_grouped_timed");

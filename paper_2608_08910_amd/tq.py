@@ -257,8 +257,9 @@ def tq_moe_stage_name(i: int) -> str:
 
 
 def tq_moe_grouped_timed(ex: TqExperts, x, topk_idx, topk_w, out, ws, events, flags: int = 0, stream=None):
-    """events: tq_moe_stage_count() + 1 torch.cuda.Event(enable_timing=True) objects."""
-    n = tq_moe_stage_count() + 1
+    """events: 2 * tq_moe_stage_count() torch.cuda.Event(enable_timing=True) objects;
+    events[2i], events[2i+1] bracket stage i."""
+    n = 2 * tq_moe_stage_count()
     if len(events) != n:
         raise ValueError(f"need {n} events")
     for ev in events:  # torch creates the HIP event on its first record
