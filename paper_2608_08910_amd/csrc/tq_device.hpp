@@ -80,11 +80,17 @@ __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<
 
 // Block quantizer on a group: each of the 8 lanes holds 32 consecutive values of one
 // 256-block (lane (l & 7) holds columns 32*(l&7) ..). Produces the lane's 32 int8 codes
-// packed into 8 dwords, and the block's fp32 scale d and code sum (group-uniform).
+// packed into 8 dwords, the sum of those 32 codes (qs), and the block's fp32 scale d
+// and code sum bsum (group-uniform).
 // Rule: amax = max|x| (exact), d = amax/127 and inv = 127/amax (IEEE division, correctly
 // rounded: this library is built without fast-math), q = rne(x * inv) with the multiply
 // rounded on its own; amax < 2^-100 (all-zero blocks included) gives d = 0, q = 0.
-__device__ __forceinline__ void quantize_group32(const float (&x)[32], int (&qw)[8], float& d, int& bsum) {
+// rne(y) for |y| <= 127.0001 (true here: |x| <= amax) is taken by adding 1.5 * 2^23: the
+// sum lies in [2^23, 2^24), where the fp32 spacing is 1, so the add rounds y to the
+// nearest integer with ties to even, and the low byte of the sum's bit pattern is that
+// integer in two's complement. |y| <= 127.0001 also makes a clamp to +-127 unnecessary.
+__device__ __forceinline__ void quantize_group32(const float (&x)[32], int (&qw)[8], int& qs, float& d, int& bsum) {
+#pragma clang fp contract(off)  // x * inv and + 1.5 * 2^23 must round separately
   float a = 0.0f;
 #pragma unroll
   for (int i = 0; i < 32; ++i) a = fmaxf(a, fabsf(x[i]));
@@ -92,27 +98,64 @@ __device__ __forceinline__ void quantize_group32(const float (&x)[32], int (&qw)
   if (amax < 0x1p-100f) {
 #pragma unroll
     for (int m = 0; m < 8; ++m) qw[m] = 0;
+    qs = 0;
     d = 0.0f;
     bsum = 0;
     return;
   }
   const float inv = 127.0f / amax;
   d = amax / 127.0f;
+  constexpr float kMagic = 12582912.0f;  // 1.5 * 2^23
   int s = 0;
 #pragma unroll
   for (int m = 0; m < 8; ++m) {
-    uint32_t packed = 0;
+    uint32_t b[4];
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      float r = rintf(__fmul_rn(x[4 * m + b], inv));
-      r = fminf(fmaxf(r, -127.0f), 127.0f);
-      const int qi = (int)r;
-      s += qi;
-      packed |= (uint32_t(qi) & 0xFFu) << (8 * b);
+    for (int k = 0; k < 4; ++k) {
+      const float y = x[4 * m + k] * inv;
+      b[k] = __float_as_uint(y + kMagic);
     }
-    qw[m] = int(packed);
+    // low bytes of the four sums -> one dword of int8 codes
+    const uint32_t lo01 = __builtin_amdgcn_perm(b[1], b[0], 0x0c0c0400u);
+    const uint32_t lo23 = __builtin_amdgcn_perm(b[3], b[2], 0x04000c0cu);
+    qw[m] = int(lo01 | lo23);
+    s = __builtin_amdgcn_sdot4(qw[m], 0x01010101, s, false);
   }
+  qs = s;
   bsum = group_sum_i32(s);
 }
+
+// ---------------------------------------------------------------------------------
+// Cross-lane reductions of many values at once (a butterfly: each exchange step halves
+// the number of values a lane carries and pairs lanes whose index differs in one bit).
+// ---------------------------------------------------------------------------------
+
+template <int M>
+__device__ __forceinline__ float lane_xor(float v) {
+  const int iv = __float_as_int(v);
+  if constexpr (M == 1) return __int_as_float(__builtin_amdgcn_update_dpp(0, iv, kDppXor1, 0xf, 0xf, false));
+  else if constexpr (M == 2) return __int_as_float(__builtin_amdgcn_update_dpp(0, iv, kDppXor2, 0xf, 0xf, false));
+  else if constexpr (M == 4) return __int_as_float(__builtin_amdgcn_ds_swizzle(iv, 0x101f));
+  else if constexpr (M == 8) return __int_as_float(__builtin_amdgcn_update_dpp(0, iv, kDppRowRor8, 0xf, 0xf, false));
+  else if constexpr (M == 16) return __int_as_float(__builtin_amdgcn_ds_swizzle(iv, kSwizzleXor16));
+  else return __int_as_float(__builtin_amdgcn_ds_bpermute((int)((__lane_id() ^ 32) << 2), iv));
+}
+
+// v[0 .. N2) -> v[0 .. N2/2): a lane whose index has bit M set keeps the upper half of
+// the values, the others the lower half, each adding its partner's (lane ^ M) copy.
+template <int N2, int M, int SZ>
+__device__ __forceinline__ void bfly_step(float (&v)[SZ]) {
+  static_assert(N2 <= SZ && N2 % 2 == 0, "bad butterfly step");
+  const bool up = (__lane_id() & M) != 0;
+#pragma unroll
+  for (int k = 0; k < N2 / 2; ++k) {
+    const float keep = up ? v[k + N2 / 2] : v[k];
+    const float send = up ? v[k] : v[k + N2 / 2];
+    v[k] = keep + lane_xor<M>(send);
+  }
+}
+
+template <int M>
+__device__ __forceinline__ float xor_sum(float v) { return v + lane_xor<M>(v); }
 
 }  // namespace tq

@@ -88,10 +88,9 @@ __device__ __forceinline__ void quantize_wave_blocks(const float* __restrict__ x
     v[4 * m + 2] = f.z;
     v[4 * m + 3] = f.w;
   }
-  int qw[8];
+  int qw[8], qs, bs;
   float dd;
-  int bs;
-  quantize_group32(v, qw, dd, bs);
+  quantize_group32(v, qw, qs, dd, bs);
   int4* qp = reinterpret_cast<int4*>(q + blk * 256 + cp * 32);
   qp[0] = make_int4(qw[0], qw[1], qw[2], qw[3]);
   qp[1] = make_int4(qw[4], qw[5], qw[6], qw[7]);
@@ -421,20 +420,20 @@ __global__ __launch_bounds__(256) void k_moe_combine(MoeArgs A, float* __restric
 constexpr int kT1MaxTopk = 8;
 constexpr int kT1MaxHq = 16384;  // topk * inter bytes of requantized hidden held in LDS
 
-// Quantize 256-block `blk` of src into LDS (one block per 8-lane group). The caller has
-// already loaded the lane's 32 values (v), ahead of its weight loads.
-// `store` is group-uniform; the quantization itself runs regardless, so that the loads
-// of v are not sunk into a branch behind the weight loads.
+// Quantize 256-block `blk` of src into LDS (one block per 8-lane group): codes, the
+// block scale and code sum, and each 32-column chunk's code sum (for the lanes that later
+// read the chunk). `store` is group-uniform; the quantization itself runs regardless, so
+// that the loads of v are not sunk into a branch behind the weight loads.
 __device__ __forceinline__ void quantize_to_lds(const float (&v)[32], int blk, int cp, int8_t* s_q, float* s_d,
-                                                int* s_b, bool store = true) {
-  int qw[8];
+                                                int* s_b, int* s_qs, bool store) {
+  int qw[8], qs, bs;
   float dd;
-  int bs;
-  quantize_group32(v, qw, dd, bs);
+  quantize_group32(v, qw, qs, dd, bs);
   if (!store) return;
   int4* qp = reinterpret_cast<int4*>(s_q + blk * 256 + cp * 32);
   qp[0] = make_int4(qw[0], qw[1], qw[2], qw[3]);
   qp[1] = make_int4(qw[4], qw[5], qw[6], qw[7]);
+  s_qs[blk * 8 + cp] = qs;
   if (cp == 0) {
     s_d[blk] = dd;
     s_b[blk] = bs;
@@ -453,13 +452,78 @@ __device__ __forceinline__ void load32(const float* p, float (&v)[32]) {
   }
 }
 
-// WAVES waves per workgroup; each wave owns RPW rows of gate and of up of one slot.
-template <int NL, int RPW, int WAVES>
+// A lane's slice of one token's quantized activations, from LDS: for load i, block
+// b = 8i + g, chunk cp: 32 codes, the chunk's code sum and the block scale. Blocks past
+// the end of the row (ragged k) read as zero.
+template <int NL>
+struct LaneActs {
+  int q[NL][8];
+  int qs[NL];
+  float d[NL];
+};
+
+template <int NL, bool RAGGED>
+__device__ __forceinline__ void lds_acts(const int8_t* s_q, const float* s_d, const int* s_qs, int kb, int g, int cp,
+                                         LaneActs<NL>& a) {
+#pragma unroll
+  for (int i = 0; i < NL; ++i) {
+    const int b = 8 * i + g;
+    const bool v = !RAGGED || b < kb;
+    const int bc = v ? b : kb - 1;
+    const int4* p = reinterpret_cast<const int4*>(s_q + bc * 256 + cp * 32);
+    const int4 lo = p[0], hi = p[1];
+    a.q[i][0] = v ? lo.x : 0; a.q[i][1] = v ? lo.y : 0; a.q[i][2] = v ? lo.z : 0; a.q[i][3] = v ? lo.w : 0;
+    a.q[i][4] = v ? hi.x : 0; a.q[i][5] = v ? hi.y : 0; a.q[i][6] = v ? hi.z : 0; a.q[i][7] = v ? hi.w : 0;
+    a.qs[i] = v ? s_qs[bc * 8 + cp] : 0;
+    a.d[i] = v ? s_d[bc] : 0.0f;
+  }
+}
+
+// One row's lane slice in registers: NL 16-byte code chunks and their f16 scales.
+template <int NL>
+struct LaneRow {
+  uint4 w[NL];
+  uint16_t s[NL];
+};
+
+// base: the row's codes (uniform); offsets are 32-bit from a uniform base, so the loads
+// take the scalar-base + vector-offset form. Chunks past the row end reload the last
+// block (their activations are zero).
+template <int NL>
+__device__ __forceinline__ void load_lane_row(const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
+                                              int kb, int g, int cp, LaneRow<NL>& r) {
+#pragma unroll
+  for (int i = 0; i < NL; ++i) {
+    const unsigned bc = (unsigned)min(8 * i + g, kb - 1);
+    r.w[i] = ldg16(codes + (bc * 128u + (unsigned)cp * 16u));
+    r.s[i] = scales[bc];
+  }
+}
+
+// The lane's contribution to one row against one token: per load, the exact integer dot
+// of its 32 codes (sum u*q - 4*qs = sum c*q, |.| <= 16256) times f32(s) * d.
+template <int NL>
+__device__ __forceinline__ float lane_row_dot(const LaneRow<NL>& r, const LaneActs<NL>& a) {
+  float acc = 0.0f;
+#pragma unroll
+  for (int i = 0; i < NL; ++i) {
+    const int p = dot_chunk_u(r.w[i], a.q[i]) - 4 * a.qs[i];
+    acc = fmaf(f16_bits_to_f32(r.s[i]) * a.d[i], (float)p, acc);
+  }
+  return acc;
+}
+
+// WAVES waves per workgroup; each wave owns RPW rows (a power of two) of gate and of up
+// of one slot. After the lane partials, one butterfly leaves row r's (g, u) in the lanes
+// whose low bits, reversed, spell r.
+template <int NL, int RPW, int WAVES, bool RAGGED>
 __global__ __launch_bounds__(WAVES * 64) void k_t1_gateup(const float* __restrict__ x, MoeArgs A) {
+  static_assert(RPW == 1 || RPW == 2 || RPW == 4 || RPW == 8, "RPW must be a power of two <= 8");
   __shared__ __attribute__((aligned(16))) int8_t s_q[kMaxK];
   __shared__ float s_d[kMaxK / 256];
   __shared__ int s_b[kMaxK / 256];
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  __shared__ int s_qs[kMaxK / 32];
+  const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 3, cp = lane & 7, gid = wv * 8 + g;
   const int kb = A.hidden / 256, I = A.inter;
   const int j = blockIdx.x / A.tiles_gu, tile = blockIdx.x - j * A.tiles_gu;
@@ -471,25 +535,20 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_gateup(const float* __restric
   // x first (its wait must not queue behind the weights), then every weight load
   float v[32];
   load32(x + min(gid, kb - 1) * 256 + cp * 32, v);
-  __builtin_amdgcn_sched_barrier(0);  // keep these loads ahead of the weights'
-  uint4 wg[RPW][NL], wu[RPW][NL];
-  float sg[RPW][NL], su[RPW][NL];
-  {
-    const uint8_t* gc = A.codes[0] + ec * A.stride_codes[0];
-    const uint8_t* uc = A.codes[1] + ec * A.stride_codes[1];
-    const uint16_t* gs = A.scales[0] + ec * A.stride_scales[0];
-    const uint16_t* us = A.scales[1] + ec * A.stride_scales[1];
+  __builtin_amdgcn_sched_barrier(0);
+  LaneRow<NL> wr[2 * RPW];  // [2r] gate row r, [2r + 1] up row r
 #pragma unroll
-    for (int r = 0; r < RPW; ++r) {
-      const int64_t row = min(row0 + r, I - 1);
-      load_row<NL>(gc + row * kb * 128, gs + row * kb, kb, g, cp, row0 + r < I, wg[r], sg[r]);
-      load_row<NL>(uc + row * kb * 128, us + row * kb, kb, g, cp, row0 + r < I, wu[r], su[r]);
-    }
+  for (int r = 0; r < RPW; ++r) {
+    const int64_t row = min(row0 + r, I - 1);
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+      load_lane_row<NL>(A.codes[m] + ec * A.stride_codes[m] + row * kb * 128,
+                        A.scales[m] + ec * A.stride_scales[m] + row * kb, kb, g, cp, wr[2 * r + m]);
   }
-  quantize_to_lds(v, min(gid, kb - 1), cp, s_q, s_d, s_b, gid < kb);
+  quantize_to_lds(v, min(gid, kb - 1), cp, s_q, s_d, s_b, s_qs, gid < kb);
   for (int blk = gid + WAVES * 8; blk < kb; blk += WAVES * 8) {
     load32(x + blk * 256 + cp * 32, v);
-    quantize_to_lds(v, blk, cp, s_q, s_d, s_b);
+    quantize_to_lds(v, blk, cp, s_q, s_d, s_b, s_qs, true);
   }
   __syncthreads();
   if (blockIdx.x == 0) {  // stage buffers and the status word, once per call
@@ -506,25 +565,44 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_gateup(const float* __restric
     }
   }
   if (!valid || row0 >= I) return;
-  int qa[NL][8];
-  float dd[NL];
-  int bb[NL];
-  load_acts<NL>(s_q, s_d, s_b, kb, g, cp, true, qa, dd, bb);
+  LaneActs<NL> act;
+  lds_acts<NL, RAGGED>(s_q, s_d, s_qs, kb, g, cp, act);
+  float val[2 * RPW];
 #pragma unroll
-  for (int r = 0; r < RPW; ++r) {
-    const float gv = row_dot<NL>(wg[r], sg[r], qa, dd, bb);
-    const float uv = row_dot<NL>(wu[r], su[r], qa, dd, bb);
-    if (lane == 0 && row0 + r < I) A.h[(int64_t)j * I + row0 + r] = silu_f32(gv) * uv;
+  for (int m = 0; m < 2 * RPW; ++m) val[m] = lane_row_dot<NL>(wr[m], act);
+  // butterfly over the row index, then plain sums over the remaining lane bits
+  if constexpr (RPW >= 2) bfly_step<2 * RPW, 1>(val);
+  if constexpr (RPW >= 4) bfly_step<RPW, 2>(val);
+  if constexpr (RPW >= 8) bfly_step<RPW / 2, 4>(val);
+#pragma unroll
+  for (int m = 0; m < 2; ++m) {
+    float t = val[m];
+    if constexpr (RPW < 2) t = xor_sum<1>(t);
+    if constexpr (RPW < 4) t = xor_sum<2>(t);
+    if constexpr (RPW < 8) t = xor_sum<4>(t);
+    t = xor_sum<32>(xor_sum<16>(xor_sum<8>(t)));
+    val[m] = t;
   }
+  // lane bits (0, 1, 2) reversed give the row this lane holds
+  const int rb = RPW == 1 ? 0 : (RPW == 2 ? (lane & 1) : (RPW == 4 ? ((lane & 1) << 1) | ((lane >> 1) & 1)
+                                                                    : ((lane & 1) << 2) | (lane & 2) | ((lane >> 2) & 1)));
+  if (lane < RPW && row0 + rb < I) A.h[(int64_t)j * I + row0 + rb] = silu_f32(val[0]) * val[1];
 }
 
-// WAVES waves per workgroup; each wave owns RPW rows of down for every slot.
-template <int NL, int RPW, int TOPK, int WAVES>
+// WAVES waves per workgroup; each wave owns RPW rows of down for every slot. Values
+// m = slot * RPW + row (padded to V, a power of two) go through one butterfly; lane
+// bits reversed give m. The per-slot results meet in LDS, where the row's lane forms
+// out = sum_j w_j * y_j in ascending j.
+template <int NL, int RPW, int TOPK, int WAVES, bool RAGGED>
 __global__ __launch_bounds__(WAVES * 64) void k_t1_down(MoeArgs A, float* __restrict__ out) {
+  constexpr int V = TOPK * RPW <= 2 ? 2 : (TOPK * RPW <= 4 ? 4 : (TOPK * RPW <= 8 ? 8 : (TOPK * RPW <= 16 ? 16 : 32)));
+  static_assert(TOPK * RPW <= 32 && (RPW & (RPW - 1)) == 0, "down tile too large");
   __shared__ __attribute__((aligned(16))) int8_t s_hq[kT1MaxHq];
   __shared__ float s_hd[kT1MaxHq / 256];
   __shared__ int s_hb[kT1MaxHq / 256];
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  __shared__ int s_qs[kT1MaxHq / 32];
+  __shared__ float s_y[WAVES][32];
+  const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 3, cp = lane & 7, gid = wv * 8 + g;
   const int kb = A.inter / 256, H = A.hidden, I = A.inter;
   const int nblk = TOPK * kb;
@@ -544,22 +622,21 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_down(MoeArgs A, float* __rest
   const bool q0 = gid < nblk && ((vmask >> (blk0 / kb)) & 1);
   float v[32];
   load32(A.h + (int64_t)(q0 ? blk0 : 0) * 256 + cp * 32, v);
-  __builtin_amdgcn_sched_barrier(0);  // keep these loads ahead of the weights'
-  uint4 w[TOPK][RPW][NL];
-  float s[TOPK][RPW][NL];
+  __builtin_amdgcn_sched_barrier(0);
+  LaneRow<NL> wr[TOPK][RPW];
 #pragma unroll
   for (int j = 0; j < TOPK; ++j)
 #pragma unroll
     for (int r = 0; r < RPW; ++r) {
       const int64_t row = min(row0 + r, H - 1);
-      load_row<NL>(A.codes[2] + ej[j] * A.stride_codes[2] + row * kb * 128, A.scales[2] + ej[j] * A.stride_scales[2] + row * kb,
-                   kb, g, cp, ((vmask >> j) & 1) && row0 + r < H, w[j][r], s[j][r]);
+      load_lane_row<NL>(A.codes[2] + ej[j] * A.stride_codes[2] + row * kb * 128,
+                        A.scales[2] + ej[j] * A.stride_scales[2] + row * kb, kb, g, cp, wr[j][r]);
     }
-  quantize_to_lds(v, blk0, cp, s_hq, s_hd, s_hb, q0);
+  quantize_to_lds(v, blk0, cp, s_hq, s_hd, s_hb, s_qs, q0);
   for (int blk = gid + WAVES * 8; blk < nblk; blk += WAVES * 8) {
     if (!((vmask >> (blk / kb)) & 1)) continue;
     load32(A.h + (int64_t)blk * 256 + cp * 32, v);
-    quantize_to_lds(v, blk, cp, s_hq, s_hd, s_hb);
+    quantize_to_lds(v, blk, cp, s_hq, s_hd, s_hb, s_qs, true);
   }
   __syncthreads();
   if (blockIdx.x == 0) {  // stage buffers, once per call
@@ -572,27 +649,45 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_down(MoeArgs A, float* __rest
       }
   }
   if (row0 >= H) return;
-  float acc[RPW];
+  float val[V];
 #pragma unroll
-  for (int r = 0; r < RPW; ++r) acc[r] = 0.0f;
+  for (int m = 0; m < V; ++m) val[m] = 0.0f;
 #pragma unroll
   for (int j = 0; j < TOPK; ++j) {
-    if (!((vmask >> j) & 1)) continue;
-    int qa[NL][8];
-    float dd[NL];
-    int bb[NL];
-    load_acts<NL>(s_hq + j * I, s_hd + j * kb, s_hb + j * kb, kb, g, cp, true, qa, dd, bb);
-    const float wj = A.topk_w[j];
+    LaneActs<NL> act;
+    lds_acts<NL, RAGGED>(s_hq + j * I, s_hd + j * kb, s_qs + j * kb * 8, kb, g, cp, act);
 #pragma unroll
-    for (int r = 0; r < RPW; ++r) {
-      const float y = row_dot<NL>(w[j][r], s[j][r], qa, dd, bb);
-      acc[r] = fmaf(wj, y, acc[r]);
-      if (lane == 0 && row0 + r < H) A.yd[(int64_t)j * H + row0 + r] = y;
-    }
+    for (int r = 0; r < RPW; ++r) val[j * RPW + r] = lane_row_dot<NL>(wr[j][r], act);
   }
+  bfly_step<V, 1>(val);
+  if constexpr (V >= 4) bfly_step<V / 2, 2>(val);
+  if constexpr (V >= 8) bfly_step<V / 4, 4>(val);
+  if constexpr (V >= 16) bfly_step<V / 8, 8>(val);
+  if constexpr (V >= 32) bfly_step<V / 16, 16>(val);
+  float t = val[0];
+  if constexpr (V < 4) t = xor_sum<2>(t);
+  if constexpr (V < 8) t = xor_sum<4>(t);
+  if constexpr (V < 16) t = xor_sum<8>(t);
+  if constexpr (V < 32) t = xor_sum<16>(t);
+  t = xor_sum<32>(t);
+  // lane l holds value m = bit-reverse of its low log2(V) bits
+  constexpr int LB = V == 2 ? 1 : (V == 4 ? 2 : (V == 8 ? 3 : (V == 16 ? 4 : 5)));
+  const int m = (int)(__builtin_bitreverse32((unsigned)lane) >> (32 - LB));
+  if (lane < V) s_y[wv][m] = t;
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  if (lane < RPW && row0 + lane < H) {
+    float acc = 0.0f;
 #pragma unroll
-  for (int r = 0; r < RPW; ++r)
-    if (lane == 0 && row0 + r < H) out[row0 + r] = acc[r];
+    for (int j = 0; j < TOPK; ++j) {
+      if (!((vmask >> j) & 1)) continue;
+      const float y = s_y[wv][j * RPW + lane];
+      acc = fmaf(A.topk_w[j], y, acc);
+      A.yd[(int64_t)j * H + row0 + lane] = y;
+    }
+    out[row0 + lane] = acc;
+  }
 }
 
 // ---------------------------------------------------------------------------------
@@ -639,50 +734,77 @@ static moe_fn pick_down(int nl, int nt) {
   }
 }
 
-constexpr int kT1RpwGU = 4;    // rows of gate and of up per wave, single-token path
-constexpr int kT1WavesGU = 4;  // waves per workgroup
-constexpr int kT1RpwDn = 2;    // rows of down per wave (for every slot), single-token path
-constexpr int kT1WavesDn = 8;
+// Tile shapes of the single-token path (measured on MI355X; overridable at build time).
+#ifndef TQ_T1_RPW_GU
+#define TQ_T1_RPW_GU 4  // rows of gate and of up per wave
+#endif
+#ifndef TQ_T1_WAVES_GU
+#define TQ_T1_WAVES_GU 4  // waves per gate/up workgroup
+#endif
+#ifndef TQ_T1_RPW_DN
+#define TQ_T1_RPW_DN 2  // rows of down per wave, for every slot
+#endif
+#ifndef TQ_T1_WAVES_DN
+#define TQ_T1_WAVES_DN 8  // waves per down workgroup
+#endif
+constexpr int kT1RpwGU = TQ_T1_RPW_GU;
+constexpr int kT1WavesGU = TQ_T1_WAVES_GU;
+constexpr int kT1RpwDn = TQ_T1_RPW_DN;
+constexpr int kT1WavesDn = TQ_T1_WAVES_DN;
 
 using t1gu_fn = void (*)(const float*, MoeArgs);
 using t1dn_fn = void (*)(MoeArgs, float*);
 
-static t1gu_fn pick_t1_gateup(int nl) {
+template <bool R>
+static t1gu_fn pick_t1_gateup_r(int nl) {
   switch (nl) {
-    case 1: return k_t1_gateup<1, kT1RpwGU, kT1WavesGU>;
-    case 2: return k_t1_gateup<2, kT1RpwGU, kT1WavesGU>;
-    case 3: return k_t1_gateup<3, kT1RpwGU / 2, kT1WavesGU>;
-    case 4: return k_t1_gateup<4, kT1RpwGU / 2, kT1WavesGU>;
-    case 5: return k_t1_gateup<5, 1, kT1WavesGU>;
-    case 6: return k_t1_gateup<6, 1, kT1WavesGU>;
-    case 7: return k_t1_gateup<7, 1, kT1WavesGU>;
-    default: return k_t1_gateup<8, 1, kT1WavesGU>;
+    case 1: return k_t1_gateup<1, kT1RpwGU, kT1WavesGU, R>;
+    case 2: return k_t1_gateup<2, kT1RpwGU, kT1WavesGU, R>;
+    case 3: return k_t1_gateup<3, (kT1RpwGU + 1) / 2, kT1WavesGU, R>;
+    case 4: return k_t1_gateup<4, (kT1RpwGU + 1) / 2, kT1WavesGU, R>;
+    case 5: return k_t1_gateup<5, 1, kT1WavesGU, R>;
+    case 6: return k_t1_gateup<6, 1, kT1WavesGU, R>;
+    case 7: return k_t1_gateup<7, 1, kT1WavesGU, R>;
+    default: return k_t1_gateup<8, 1, kT1WavesGU, R>;
   }
 }
-static int t1_rpw_gu(int nl) { return nl <= 2 ? kT1RpwGU : (nl <= 4 ? kT1RpwGU / 2 : 1); }
+// ragged: kb (blocks per row) not a multiple of 8, so the last 16-byte load of a row is
+// partly past its end
+static t1gu_fn pick_t1_gateup(int kb) {
+  const int nl = (kb + 7) / 8;
+  return kb % 8 ? pick_t1_gateup_r<true>(nl) : pick_t1_gateup_r<false>(nl);
+}
+static int t1_rpw_gu(int nl) { return nl <= 2 ? kT1RpwGU : (nl <= 4 ? (kT1RpwGU + 1) / 2 : 1); }
 
-template <int NL>
+template <int NL, bool R>
 static t1dn_fn pick_t1_down_k(int topk) {
   switch (topk) {
-    case 1: return k_t1_down<NL, kT1RpwDn, 1, kT1WavesDn>;
-    case 2: return k_t1_down<NL, kT1RpwDn, 2, kT1WavesDn>;
-    case 3: return k_t1_down<NL, kT1RpwDn, 3, kT1WavesDn>;
-    case 4: return k_t1_down<NL, kT1RpwDn, 4, kT1WavesDn>;
-    case 5: return k_t1_down<NL, kT1RpwDn, 5, kT1WavesDn>;
-    case 6: return k_t1_down<NL, kT1RpwDn, 6, kT1WavesDn>;
-    case 7: return k_t1_down<NL, kT1RpwDn, 7, kT1WavesDn>;
-    default: return k_t1_down<NL, kT1RpwDn, 8, kT1WavesDn>;
+    case 1: return k_t1_down<NL, kT1RpwDn, 1, kT1WavesDn, R>;
+    case 2: return k_t1_down<NL, kT1RpwDn, 2, kT1WavesDn, R>;
+    case 3: return k_t1_down<NL, kT1RpwDn, 3, kT1WavesDn, R>;
+    case 4: return k_t1_down<NL, kT1RpwDn, 4, kT1WavesDn, R>;
+    case 5: return k_t1_down<NL, kT1RpwDn, 5, kT1WavesDn, R>;
+    case 6: return k_t1_down<NL, kT1RpwDn, 6, kT1WavesDn, R>;
+    case 7: return k_t1_down<NL, kT1RpwDn, 7, kT1WavesDn, R>;
+    default: return k_t1_down<NL, kT1RpwDn, 8, kT1WavesDn, R>;
   }
 }
 
 // topk * inter <= 16384 bytes of LDS bounds NL: inter <= 16384 / topk.
-static t1dn_fn pick_t1_down(int nl, int topk) {
+template <bool R>
+static t1dn_fn pick_t1_down_r(int nl, int topk) {
   switch (nl) {
-    case 1: return pick_t1_down_k<1>(topk);
-    case 2: return pick_t1_down_k<2>(topk);
-    case 3: case 4: return pick_t1_down_k<4>(topk);
-    default: return pick_t1_down_k<8>(topk);
+    case 1: return pick_t1_down_k<1, R>(topk);
+    case 2: return pick_t1_down_k<2, R>(topk);
+    case 3: case 4: return pick_t1_down_k<4, R>(topk);
+    default: return pick_t1_down_k<8, R>(topk);
   }
+}
+static t1dn_fn pick_t1_down(int kb, int topk) {
+  const int nl = (kb + 7) / 8;
+  // NL is rounded up to 4 or 8 for nl > 2: those loads may run past the row end too
+  const bool ragged = kb % 8 != 0 || (nl > 2 && nl != 4 && nl != 8);
+  return ragged ? pick_t1_down_r<true>(nl, topk) : pick_t1_down_r<false>(nl, topk);
 }
 
 // One stage's kernel; with timing events, launched with hipExtLaunchKernelGGL so the
@@ -805,11 +927,11 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
     A.tiles_gu = (ex->inter + kT1WavesGU * rgu - 1) / (kT1WavesGU * rgu);
     const unsigned tiles_dn = (unsigned)((ex->hidden + kT1WavesDn * kT1RpwDn - 1) / (kT1WavesDn * kT1RpwDn));
     if ((st = empty_stage(events, 0, stm, fn)) != TQ_OK) return st;
-    if ((st = launch_stage(events, 1, pick_t1_gateup(nl_gu), dim3((unsigned)(topk * A.tiles_gu)), kT1WavesGU * 64, stm,
+    if ((st = launch_stage(events, 1, pick_t1_gateup(ex->hidden / 256), dim3((unsigned)(topk * A.tiles_gu)), kT1WavesGU * 64, stm,
                            fn, x, A)) != TQ_OK)
       return st;
     if ((st = empty_stage(events, 2, stm, fn)) != TQ_OK) return st;
-    if ((st = launch_stage(events, 3, pick_t1_down(nl_dn, topk), dim3(tiles_dn), kT1WavesDn * 64, stm, fn, A, out)) !=
+    if ((st = launch_stage(events, 3, pick_t1_down(ex->inter / 256, topk), dim3(tiles_dn), kT1WavesDn * 64, stm, fn, A, out)) !=
         TQ_OK)
       return st;
     return empty_stage(events, 4, stm, fn);

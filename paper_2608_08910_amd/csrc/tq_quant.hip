@@ -24,10 +24,9 @@ __global__ __launch_bounds__(256) void k_quantize(const float* __restrict__ x, i
     v[4 * m + 2] = f.z;
     v[4 * m + 3] = f.w;
   }
-  int qw[8];
+  int qw[8], qs, bs;
   float dd;
-  int bs;
-  quantize_group32(v, qw, dd, bs);
+  quantize_group32(v, qw, qs, dd, bs);
   int4* qp = reinterpret_cast<int4*>(q + blk * 256 + cp * 32);
   qp[0] = make_int4(qw[0], qw[1], qw[2], qw[3]);
   qp[1] = make_int4(qw[4], qw[5], qw[6], qw[7]);

@@ -16,7 +16,9 @@ import numpy as np
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libtq.so")
+# TQ_LIBRARY names an alternate build of the same library (e.g. one built with other tile
+# shapes); by default the in-tree build is loaded.
+LIB_PATH = os.environ.get("TQ_LIBRARY") or os.path.join(_HERE, "libtq.so")
 
 TQ_OK = 0
 TQ_ERR_INVALID = -1
