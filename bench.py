@@ -38,6 +38,27 @@ METRIC = "achieved HBM GB/s (% of peak) for tq expert GEMV; MoE-layer tokens/sec
 HBM_PEAK_GBS = 8000.0
 
 
+def recorded_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter summary, or
+    None if no record exists or the kernel's sources changed since it was taken."""
+    import glob
+    import hashlib
+    for path in glob.glob(os.path.join(ROOT, "profiles", "*traffic*.md")):
+        for line in open(path):
+            line = line.strip()
+            if not line.startswith('{"kernel"'):
+                continue
+            rec = json.loads(line)
+            if rec["kernel"] != kernel:
+                continue
+            h = hashlib.sha256()
+            for f in rec["sources"]:
+                h.update(open(os.path.join(ROOT, f), "rb").read())
+            if h.hexdigest() == rec["sources_sha256"]:
+                return rec["traffic_bytes_per_launch"]
+    return None
+
+
 def matrix_bytes(n: int, k: int) -> int:
     return n * k // 2 + n * (k // 256) * 2
 
@@ -94,7 +115,13 @@ def main():
         for _ in range(3):
             dst.copy_(src)
         torch.cuda.synchronize()
-        print(json.dumps({"calibrate_copy_bytes": src.numel() * 4, "copies": 3}))
+        t0 = time.perf_counter()
+        for _ in range(10):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        print(json.dumps({"calibrate_copy_bytes": src.numel() * 4, "copies": 13,
+                          "copy_GBps_read_plus_write": round(10 * 2 * src.numel() * 4 / el / 1e9, 1)}))
         return
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (--gpus {args.gpus} requested); "
@@ -178,6 +205,9 @@ def main():
     gu_bytes = float(np.mean([len(np.unique(sched[W + (j % K)][0])) for j in range(P)])) * 2 * matrix_bytes(I, H) \
         + T * H * 4 + T * topk * I * 4
     achieved = gu_bytes / (gu_ms * 1e-3) / 1e9
+    # the single-token step's gate/up kernel (hidden 4096: two 16-byte loads per row and lane)
+    gu_kernel = "k_t1_gateup<2, 4, 4, false>"
+    traffic = recorded_traffic(gu_kernel)
 
     res = {
         "metric": METRIC,
@@ -199,8 +229,9 @@ def main():
         "tokens_per_s": round(K * T / elapsed, 1),
         "stage_ms": {k: round(v, 5) for k, v in stage_ms.items()},
         "roofline": {"kernel": "gate_up", "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                     "bytes_per_launch": round(gu_bytes), "mean_ms": round(gu_ms, 5)},
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "bytes_per_launch": round(gu_bytes), "mean_ms": round(gu_ms, 5),
+                     "kernel_symbol": gu_kernel},
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(seed, H, I, topk)

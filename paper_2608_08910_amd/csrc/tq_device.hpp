@@ -78,6 +78,26 @@ __device__ __forceinline__ uint4 ldg16(const void* p) {
 
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 
+// Buffer resources: a wave-uniform base (SGPRs) plus a 32-bit per-lane offset and a
+// wave-uniform offset, so no per-lane 64-bit address arithmetic; reads past num_records
+// bytes return zero. Word 3 is the raw-buffer configuration of the gfx9 family.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// Cache-policy bits of buffer loads: nt (streamed once).
+constexpr int kBufNT = 2;
+
+__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, int aux = kBufNT) {
+  const u32x4 v = aux == kBufNT ? __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kBufNT)
+                                : __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ uint16_t buf_load_u16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
+}
+
 // Block quantizer on a group: each of the 8 lanes holds 32 consecutive values of one
 // 256-block (lane (l & 7) holds columns 32*(l&7) ..). Produces the lane's 32 int8 codes
 // packed into 8 dwords, the sum of those 32 codes (qs), and the block's fp32 scale d

@@ -486,17 +486,38 @@ struct LaneRow {
   uint16_t s[NL];
 };
 
-// base: the row's codes (uniform); offsets are 32-bit from a uniform base, so the loads
-// take the scalar-base + vector-offset form. Chunks past the row end reload the last
-// block (their activations are zero).
+// One matrix of one expert as buffer resources (codes and scales).
+struct MatRsrc {
+  __amdgpu_buffer_rsrc_t codes, scales;
+};
+
+__device__ __forceinline__ MatRsrc mat_rsrc(const uint8_t* codes, const uint16_t* scales, int n, int kb) {
+  return {make_rsrc(codes, (uint32_t)n * (uint32_t)kb * 128u), make_rsrc(scales, (uint32_t)n * (uint32_t)kb * 2u)};
+}
+
+// Row `row` (wave-uniform) of a matrix: the lane's NL chunks and their scales. Chunks past
+// the row end reload the row's last block (their activations are zero).
 template <int NL>
-__device__ __forceinline__ void load_lane_row(const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
-                                              int kb, int g, int cp, LaneRow<NL>& r) {
+__device__ __forceinline__ void load_lane_row(const MatRsrc& m, int row, int kb, int g, int cp, LaneRow<NL>& r) {
+  const uint32_t srow = (uint32_t)row * (uint32_t)kb;
 #pragma unroll
   for (int i = 0; i < NL; ++i) {
-    const unsigned bc = (unsigned)min(8 * i + g, kb - 1);
-    r.w[i] = ldg16(codes + (bc * 128u + (unsigned)cp * 16u));
-    r.s[i] = scales[bc];
+    const uint32_t bc = (uint32_t)min(8 * i + g, kb - 1);
+    r.w[i] = buf_load16(m.codes, bc * 128u + (uint32_t)cp * 16u, srow * 128u);
+    r.s[i] = buf_load_u16(m.scales, bc * 2u, srow * 2u);
+  }
+}
+
+// The lane's 32 fp32 values of 256-block `blk` of a row-major fp32 buffer.
+__device__ __forceinline__ void buf_load32f(__amdgpu_buffer_rsrc_t r, uint32_t blk, int cp, float (&v)[32]) {
+  const uint32_t o = (blk * 256u + (uint32_t)cp * 32u) * 4u;
+#pragma unroll
+  for (int m = 0; m < 8; ++m) {
+    const uint4 u = buf_load16(r, o + 16u * m, 0, 0);
+    v[4 * m + 0] = __uint_as_float(u.x);
+    v[4 * m + 1] = __uint_as_float(u.y);
+    v[4 * m + 2] = __uint_as_float(u.z);
+    v[4 * m + 3] = __uint_as_float(u.w);
   }
 }
 
@@ -533,21 +554,22 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_gateup(const float* __restric
   const int row0 = (tile * WAVES + wv) * RPW;
 
   // x first (its wait must not queue behind the weights), then every weight load
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, (uint32_t)A.hidden * 4u);
   float v[32];
-  load32(x + min(gid, kb - 1) * 256 + cp * 32, v);
+  buf_load32f(xr, (uint32_t)min(gid, kb - 1), cp, v);
   __builtin_amdgcn_sched_barrier(0);
+  const MatRsrc mr[2] = {mat_rsrc(A.codes[0] + ec * A.stride_codes[0], A.scales[0] + ec * A.stride_scales[0], I, kb),
+                         mat_rsrc(A.codes[1] + ec * A.stride_codes[1], A.scales[1] + ec * A.stride_scales[1], I, kb)};
   LaneRow<NL> wr[2 * RPW];  // [2r] gate row r, [2r + 1] up row r
 #pragma unroll
   for (int r = 0; r < RPW; ++r) {
-    const int64_t row = min(row0 + r, I - 1);
+    const int row = min(row0 + r, I - 1);
 #pragma unroll
-    for (int m = 0; m < 2; ++m)
-      load_lane_row<NL>(A.codes[m] + ec * A.stride_codes[m] + row * kb * 128,
-                        A.scales[m] + ec * A.stride_scales[m] + row * kb, kb, g, cp, wr[2 * r + m]);
+    for (int m = 0; m < 2; ++m) load_lane_row<NL>(mr[m], row, kb, g, cp, wr[2 * r + m]);
   }
   quantize_to_lds(v, min(gid, kb - 1), cp, s_q, s_d, s_b, s_qs, gid < kb);
   for (int blk = gid + WAVES * 8; blk < kb; blk += WAVES * 8) {
-    load32(x + blk * 256 + cp * 32, v);
+    buf_load32f(xr, (uint32_t)blk, cp, v);
     quantize_to_lds(v, blk, cp, s_q, s_d, s_b, s_qs, true);
   }
   __syncthreads();
@@ -620,22 +642,21 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_down(MoeArgs A, float* __rest
   // group loads the buffer's first block instead and skips the quantization)
   const int blk0 = min(gid, nblk - 1);
   const bool q0 = gid < nblk && ((vmask >> (blk0 / kb)) & 1);
+  const __amdgpu_buffer_rsrc_t hr = make_rsrc(A.h, (uint32_t)(TOPK * I) * 4u);
   float v[32];
-  load32(A.h + (int64_t)(q0 ? blk0 : 0) * 256 + cp * 32, v);
+  buf_load32f(hr, (uint32_t)(q0 ? blk0 : 0), cp, v);
   __builtin_amdgcn_sched_barrier(0);
   LaneRow<NL> wr[TOPK][RPW];
 #pragma unroll
-  for (int j = 0; j < TOPK; ++j)
+  for (int j = 0; j < TOPK; ++j) {
+    const MatRsrc mr = mat_rsrc(A.codes[2] + ej[j] * A.stride_codes[2], A.scales[2] + ej[j] * A.stride_scales[2], H, kb);
 #pragma unroll
-    for (int r = 0; r < RPW; ++r) {
-      const int64_t row = min(row0 + r, H - 1);
-      load_lane_row<NL>(A.codes[2] + ej[j] * A.stride_codes[2] + row * kb * 128,
-                        A.scales[2] + ej[j] * A.stride_scales[2] + row * kb, kb, g, cp, wr[j][r]);
-    }
+    for (int r = 0; r < RPW; ++r) load_lane_row<NL>(mr, min(row0 + r, H - 1), kb, g, cp, wr[j][r]);
+  }
   quantize_to_lds(v, blk0, cp, s_hq, s_hd, s_hb, s_qs, q0);
   for (int blk = gid + WAVES * 8; blk < nblk; blk += WAVES * 8) {
     if (!((vmask >> (blk / kb)) & 1)) continue;
-    load32(A.h + (int64_t)blk * 256 + cp * 32, v);
+    buf_load32f(hr, (uint32_t)blk, cp, v);
     quantize_to_lds(v, blk, cp, s_hq, s_hd, s_hb, s_qs, true);
   }
   __syncthreads();
