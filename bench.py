@@ -98,13 +98,25 @@ def cpu_baseline(seed: int, hidden: int, inter: int, topk: int, target_s: float 
     }
 
 
+# Benchmarkable workloads: the default is the layer the metric is quoted on (one MoE
+# layer at decode, batch 1); the others time the batched-decode and prefill layers.
+WORKLOADS = {
+    "decode1": dict(cfg=1, steps=2000, warmup=200, profile=256),
+    "decode32": dict(cfg=2, steps=300, warmup=30, profile=64),
+    "prefill2048": dict(cfg=3, steps=10, warmup=2, profile=4),
+}
+MFMA_I8_PEAK_TOPS = 5000.0
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=2000)
-    ap.add_argument("--warmup", type=int, default=200)
+    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="decode1")
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--profile-steps", type=int, default=256, help="steps of the per-kernel event pass")
+    ap.add_argument("--profile-steps", type=int, default=None, help="steps of the per-kernel event pass")
+    ap.add_argument("--flags", type=int, default=0, help="tq_moe_grouped flags (1 force VALU, 2 force MFMA)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (to scale HBM byte counters)")
     args = ap.parse_args()
@@ -132,8 +144,12 @@ def main():
     from paper_2608_08910_amd import tq
     from synth import gen
 
-    cfg = gen.CONFIGS[1]
+    wl = WORKLOADS[args.workload]
+    cfg = gen.CONFIGS[wl["cfg"]]
     E, H, I, T, topk, seed = cfg["experts"], cfg["hidden"], cfg["inter"], cfg["tokens"], cfg["topk"], gen.SEED
+    K = args.steps if args.steps is not None else wl["steps"]
+    W = args.warmup if args.warmup is not None else wl["warmup"]
+    P = args.profile_steps if args.profile_steps is not None else wl["profile"]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
 
@@ -144,17 +160,25 @@ def main():
             tq.tq_synth_weights(gen.matrix_key(seed, 0, e, p), ex.matrix(e, p))
     torch.cuda.synchronize()
 
-    K, W, P = args.steps, args.warmup, args.profile_steps
     total = W + K
-    sched = gen.bench_routing_schedule(seed, total, T, E, topk, cfg["routing"])
+    if T == 1:
+        # every step avoids the experts of the previous 3 steps (last-level-cache reuse)
+        sched = gen.bench_routing_schedule(seed, total, T, E, topk, cfg["routing"])
+    else:
+        # many tokens per step: the step's expert union is 1.2-3.3 GB, far beyond the cache
+        sched = [gen.routing(seed, 1000 + i, T, E, topk, cfg["routing"]) for i in range(total)]
     idx_all = torch.from_numpy(np.stack([s[0] for s in sched])).to(dev)          # [steps][T][topk]
     w_all = torch.from_numpy(np.stack([s[1] for s in sched])).to(dev)
-    x_all = torch.from_numpy(gen.activations(seed, 1000, total * T, H).reshape(total, T, H)).to(dev)
+    xs = gen.activations(seed, 1000, total * T, H).reshape(total, T, H)
+    if cfg.get("token_factor"):
+        xs = xs * np.stack([gen.token_factors(seed + 1 + i, T) for i in range(total)])[:, :, None]
+    x_all = torch.from_numpy(np.ascontiguousarray(xs, dtype=np.float32)).to(dev)
+    del xs
     out = torch.empty((T, H), dtype=torch.float32, device=dev)
     ws = torch.empty(tq.tq_moe_workspace_bytes(ex, T, topk), dtype=torch.uint8, device=dev)
 
     def step(i):
-        tq.tq_moe_grouped(ex, x_all[i], idx_all[i], w_all[i], out, ws)
+        tq.tq_moe_grouped(ex, x_all[i], idx_all[i], w_all[i], out, ws, args.flags)
 
     # eager sanity pass (also loads the code objects)
     for i in range(min(W, 8)):
@@ -185,8 +209,8 @@ def main():
     alg_bytes = sum(d * bytes_expert for d in distinct) + K * (T * H * 4 * 2 + T * topk * 8)
     gbs = alg_bytes / elapsed / 1e9
 
-    # per-kernel pass: events around every stage, eager launches queued behind a spin
-    # kernel so the GPU runs the stages back to back
+    # per-kernel pass: every stage's kernel launched with its own start/stop events,
+    # eager launches queued behind a spin kernel so the GPU runs them back to back
     nst = tq.tq_moe_stage_count()
     names = [tq.tq_moe_stage_name(i) for i in range(nst)]
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * nst)] for _ in range(P)]
@@ -194,21 +218,39 @@ def main():
     torch.cuda._sleep(int(2.4e9 * 0.05))  # ~50 ms of queue head-room
     for j in range(P):
         i = W + (j % K)
-        tq.tq_moe_grouped_timed(ex, x_all[i], idx_all[i], w_all[i], out, ws, evs[j])
+        tq.tq_moe_grouped_timed(ex, x_all[i], idx_all[i], w_all[i], out, ws, evs[j], args.flags)
     torch.cuda.synchronize()
     stage_ms = {n: float(np.mean([evs[j][2 * si].elapsed_time(evs[j][2 * si + 1]) for j in range(P)]))
                 for si, n in enumerate(names)}
-    gu = names.index("gate_up")
     gu_ms = stage_ms["gate_up"]
-    # gate_up moves the routed experts' gate and up codes + scales, reads x (fp32) and
-    # writes h (fp32, one row per slot)
-    gu_bytes = float(np.mean([len(np.unique(sched[W + (j % K)][0])) for j in range(P)])) * 2 * matrix_bytes(I, H) \
-        + T * H * 4 + T * topk * I * 4
-    achieved = gu_bytes / (gu_ms * 1e-3) / 1e9
-    # the single-token step's gate/up kernel (hidden 4096: two 16-byte loads per row and lane)
-    gu_kernel = "k_t1_gateup<2, 4, 4, false>"
-    traffic = recorded_traffic(gu_kernel)
+    prof = [sched[W + (j % K)] for j in range(P)]
+    n_distinct = float(np.mean([len(np.unique(r[0])) for r in prof]))
+    mfma = bool(args.flags & 2) or (not (args.flags & 1) and T * topk >= 1024)
+    if T == 1:
+        # the single-token gate/up kernel moves the routed experts' gate and up codes +
+        # scales, reads x (fp32) and writes h (fp32, one row per slot)
+        gu_bytes = n_distinct * 2 * matrix_bytes(I, H) + T * H * 4 + T * topk * I * 4
+        gu_kernel = "k_t1_gateup<2, 4, 4, false>"
+    else:
+        # the grouped gate/up kernels read the routed experts' gate and up planes and the
+        # quantized tokens (int8 + scale + sum per block), and write h per slot
+        gu_bytes = n_distinct * 2 * matrix_bytes(I, H) + T * (H + (H // 256) * 8) + T * topk * I * 4
+        gu_kernel = "k_moe_mfma<2>" if mfma else f"k_moe_gateup<2, {1 if T == 1 else 4}, 4>"
+    if mfma:
+        gu_ops = 2.0 * T * topk * (2 * I * H)  # int8 multiply-adds of gate and up, 2 ops each
+        achieved = gu_ops / (gu_ms * 1e-3) / 1e12
+        roof = {"kernel": "gate_up", "bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_I8_PEAK_TOPS,
+                "unit": "TOP/s", "frac": round(achieved / MFMA_I8_PEAK_TOPS, 4), "traffic": recorded_traffic(gu_kernel),
+                "ops_per_launch": gu_ops, "bytes_per_launch": round(gu_bytes), "mean_ms": round(gu_ms, 5),
+                "hbm_GBps": round(gu_bytes / (gu_ms * 1e-3) / 1e9, 1), "kernel_symbol": gu_kernel}
+    else:
+        achieved = gu_bytes / (gu_ms * 1e-3) / 1e9
+        roof = {"kernel": "gate_up", "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": recorded_traffic(gu_kernel),
+                "bytes_per_launch": round(gu_bytes), "mean_ms": round(gu_ms, 5), "kernel_symbol": gu_kernel}
 
+    routing_desc = ("uniform top-8, no expert reused within 3 steps" if T == 1 else
+                    f"{cfg['routing']} top-{topk}, fresh draw per step")
     res = {
         "metric": METRIC,
         "value": round(gbs, 2),
@@ -223,17 +265,14 @@ def main():
         "dtype": "int8",
         "data": "synthetic",
         "config": {"workload": cfg["name"], "experts": E, "hidden": H, "inter": I, "tokens_per_step": T,
-                   "topk": topk, "routing": "uniform top-8, no expert reused within 3 steps",
-                   "bits_per_weight": 4.0625, "resident_expert_bytes": E * bytes_expert},
+                   "topk": topk, "routing": routing_desc, "bits_per_weight": 4.0625,
+                   "resident_expert_bytes": E * bytes_expert, "path": "mfma" if mfma else "valu"},
         "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
         "tokens_per_s": round(K * T / elapsed, 1),
         "stage_ms": {k: round(v, 5) for k, v in stage_ms.items()},
-        "roofline": {"kernel": "gate_up", "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "bytes_per_launch": round(gu_bytes), "mean_ms": round(gu_ms, 5),
-                     "kernel_symbol": gu_kernel},
+        "roofline": roof,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.workload == "decode1":
         res["cpu_baseline"] = cpu_baseline(seed, H, I, topk)
     print(json.dumps(res), flush=True)
 

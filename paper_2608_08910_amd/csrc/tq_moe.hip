@@ -33,10 +33,14 @@ constexpr int kNumStages = 5;
 static const char* const kStageNames[kNumStages] = {"prologue", "gate_up", "requant", "down", "combine"};
 
 // Control words at the start of the workspace.
-enum Ctrl { kFlags = 0, kNActive = 1, kTasksGU = 2, kTasksDn = 3, kNValid = 4, kCtrlWords = 64 };
+enum Ctrl { kFlags = 0, kNActive = 1, kTasksGU = 2, kTasksDn = 3, kNValid = 4, kTasksMGU = 5, kTasksMDn = 6, kCtrlWords = 64 };
+
+constexpr int kMT = 64;  // tokens per MFMA tile (four 16-row MFMA tiles)
+constexpr int kMN = 64;  // weight rows per MFMA workgroup (four waves x 16)
+constexpr int64_t kMfmaMinSlots = 1024;  // automatic path choice: MFMA from this many slots
 
 struct Layout {
-  size_t ctrl, active, act_off, slot_list, xq, xd, xb, h, hq, hd, hb, yd, total;
+  size_t ctrl, active, act_off, tt_off, slot_list, xq, xd, xb, h, hq, hd, hb, yd, total;
 };
 
 static size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -53,6 +57,7 @@ static Layout make_layout(int n_experts, int hidden, int inter, int64_t t, int t
   L.ctrl = take(kCtrlWords * 4);
   L.active = take((size_t)n_experts * 4);
   L.act_off = take(((size_t)n_experts + 1) * 4);
+  L.tt_off = take(((size_t)n_experts + 1) * 4);
   L.slot_list = take(S * 4);
   L.xq = take((size_t)t * hidden);
   L.xd = take((size_t)t * (hidden / 256) * 4);
@@ -155,6 +160,15 @@ __device__ __forceinline__ float row_dot(const uint4 (&w)[NL], const float (&s)[
   return wave_sum_groups_f32(acc);
 }
 
+// One matrix of one expert as buffer resources (codes and scales).
+struct MatRsrc {
+  __amdgpu_buffer_rsrc_t codes, scales;
+};
+
+__device__ __forceinline__ MatRsrc mat_rsrc(const uint8_t* codes, const uint16_t* scales, int n, int kb) {
+  return {make_rsrc(codes, (uint32_t)n * (uint32_t)kb * 128u), make_rsrc(scales, (uint32_t)n * (uint32_t)kb * 2u)};
+}
+
 __device__ __forceinline__ float silu_f32(float z) { return z / (1.0f + expf(-z)); }
 
 struct MoeArgs {
@@ -168,6 +182,7 @@ struct MoeArgs {
   int32_t* ctrl;
   int32_t* active;
   int32_t* act_off;
+  int32_t* tt_off;  // per active expert: first token tile (kMT tokens) of the MFMA path
   int32_t* slot_list;
   int8_t* xq;
   float* xd;
@@ -177,7 +192,8 @@ struct MoeArgs {
   float* hd;
   int32_t* hb;
   float* yd;
-  int tiles_gu, tiles_dn;
+  int tiles_gu, tiles_dn;    // row tiles of the VALU kernels
+  int tiles_mgu, tiles_mdn;  // row tiles of the MFMA kernels
 };
 
 // ---------------------------------------------------------------------------------
@@ -193,7 +209,7 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
   __shared__ int s_cnt[kMaxExperts];   // slots per expert
   __shared__ int s_base[kMaxExperts];  // rank of an active expert, then its slot cursor
   __shared__ int s_ebr[kMaxExperts];   // expert of each rank
-  __shared__ int s_scan[256];
+  __shared__ int s_scan[256], s_scan2[256];
   __shared__ int s_nact, s_bad;
   const int tid = threadIdx.x, E = A.n_experts;
   const int64_t S = A.t * A.topk;
@@ -236,31 +252,43 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
   // exclusive scan of the slot counts in rank order, contiguous ranks per thread
   const int per = (n_active + 255) / 256;
   const int r0 = min(n_active, tid * per), r1 = min(n_active, r0 + per);
-  int ns = 0;
-  for (int r = r0; r < r1; ++r) ns += s_cnt[s_ebr[r]];
+  // (and of the kMT-token tiles of the MFMA path)
+  int ns = 0, nt = 0;
+  for (int r = r0; r < r1; ++r) {
+    ns += s_cnt[s_ebr[r]];
+    nt += (s_cnt[s_ebr[r]] + kMT - 1) / kMT;
+  }
   s_scan[tid] = ns;
+  s_scan2[tid] = nt;
   __syncthreads();
   for (int off = 1; off < 256; off <<= 1) {
     const int v = tid >= off ? s_scan[tid - off] : 0;
+    const int v2 = tid >= off ? s_scan2[tid - off] : 0;
     __syncthreads();
     s_scan[tid] += v;
+    s_scan2[tid] += v2;
     __syncthreads();
   }
-  int pos = s_scan[tid] - ns;
+  int pos = s_scan[tid] - ns, tpos = s_scan2[tid] - nt;
   for (int r = r0; r < r1; ++r) {
     const int e = s_ebr[r];
     A.active[r] = e;
     A.act_off[r] = pos;
+    A.tt_off[r] = tpos;
     s_base[e] = pos;  // rank no longer needed: becomes the expert's slot cursor
     pos += s_cnt[e];
+    tpos += (s_cnt[e] + kMT - 1) / kMT;
   }
   if (tid == 255) {
-    const int n_valid = s_scan[255];
+    const int n_valid = s_scan[255], n_tiles = s_scan2[255];
     A.act_off[n_active] = n_valid;
+    A.tt_off[n_active] = n_tiles;
     A.ctrl[kNActive] = n_active;
     A.ctrl[kNValid] = n_valid;
     A.ctrl[kTasksGU] = n_active * A.tiles_gu;
     A.ctrl[kTasksDn] = n_active * A.tiles_dn;
+    A.ctrl[kTasksMGU] = n_tiles * A.tiles_mgu;
+    A.ctrl[kTasksMDn] = n_tiles * A.tiles_mdn;
     A.ctrl[kFlags] = s_bad ? 1 : 0;
   }
   __syncthreads();
@@ -409,6 +437,187 @@ __global__ __launch_bounds__(256) void k_moe_combine(MoeArgs A, float* __restric
 }
 
 // ---------------------------------------------------------------------------------
+// Many tokens per expert (prefill-sized groups): the per-expert contraction is a dense
+// int8 GEMM, run on v_mfma_i32_16x16x64_i8. A workgroup owns one task: kMT tokens of one
+// active expert x kMN weight rows (x2 matrices for gate/up). Per 256-column block:
+//  - the token tile's codes are staged in LDS (double-buffered, rows padded to 272 bytes
+//    so the 16 lanes of an operand read hit distinct banks) with their d and bsum;
+//  - each wave unpacks its 16 weight rows' nibbles into B operands (lane: row l & 15,
+//    chunk 4t + (l >> 4), half h gives MFMA (t, h); the A operand takes the same 16
+//    columns of the token's codes, so every product pairs matching columns);
+//  - four MFMAs per 16x16 output tile accumulate sum u*q from -4*bsum (u = c + 4), i.e.
+//    the exact block sum isum, and one fp32 multiply-add per output applies f32(s) * d.
+// Tasks are ranked hottest expert first with token tiles innermost, so the workgroups
+// that read one weight tile run together and share it through L2.
+// ---------------------------------------------------------------------------------
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+constexpr int kAStride = 272;
+
+__device__ __forceinline__ v4i lds_v4i(const int8_t* p) {
+  const int4 v = *reinterpret_cast<const int4*>(p);
+  return v4i{v.x, v.y, v.z, v.w};
+}
+
+// One block's loads for the MFMA kernel: this thread's 64-byte quarter of a token row,
+// the token's block scale and code sum, and the lane's two 16-byte code chunks (and
+// scale) of each weight matrix.
+template <int NMAT>
+struct MfmaStage {
+  v4i a0, a1, a2, a3;
+  uint4 w[NMAT][2];
+  uint16_t s[NMAT];
+  float d;
+  int bs;
+};
+
+template <int NMAT>
+__device__ __forceinline__ void mfma_fetch(MfmaStage<NMAT>& st, const v4i* qrow, const float* dsrc, const int32_t* bsrc,
+                                           int64_t arow, const MatRsrc (&mr)[NMAT], int wrow, int kb, int g, int b) {
+  st.a0 = qrow[b * 16 + 0];
+  st.a1 = qrow[b * 16 + 1];
+  st.a2 = qrow[b * 16 + 2];
+  st.a3 = qrow[b * 16 + 3];
+  st.d = dsrc[arow * kb + b];
+  st.bs = bsrc[arow * kb + b];
+#pragma unroll
+  for (int m = 0; m < NMAT; ++m) {
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+      st.w[m][c] = buf_load16(mr[m].codes, (uint32_t)((wrow * kb + b) * 128 + (4 * c + g) * 16), 0);
+    st.s[m] = buf_load_u16(mr[m].scales, (uint32_t)((wrow * kb + b) * 2), 0);
+  }
+}
+
+template <int NMAT>  // 2: gate and up, h = SiLU(g) * u; 1: down, y per slot
+__global__ __launch_bounds__(256) void k_moe_mfma(MoeArgs A) {
+  __shared__ __attribute__((aligned(16))) int8_t s_a[2][kMT * kAStride];
+  __shared__ __attribute__((aligned(16))) float s_d[2][kMT];
+  __shared__ __attribute__((aligned(16))) int s_b[2][kMT];
+  __shared__ int s_slot[kMT];
+  const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int li = lane & 15, g = lane >> 4;
+  const int K = NMAT == 2 ? A.hidden : A.inter;
+  const int N = NMAT == 2 ? A.inter : A.hidden;
+  const int kb = K / 256;
+  const int RT = NMAT == 2 ? A.tiles_mgu : A.tiles_mdn;
+  const int n_active = A.ctrl[kNActive];
+  const int n_tasks = A.ctrl[NMAT == 2 ? kTasksMGU : kTasksMDn];
+  const int8_t* qsrc = NMAT == 2 ? A.xq : A.hq;
+  const float* dsrc = NMAT == 2 ? A.xd : A.hd;
+  const int32_t* bsrc = NMAT == 2 ? A.xb : A.hb;
+  const int tt = threadIdx.x >> 2, part = threadIdx.x & 3;  // staging: token row, 64-byte quarter
+  for (int task = blockIdx.x; task < n_tasks; task += gridDim.x) {
+    // active expert a with tt_off[a] * RT <= task < tt_off[a + 1] * RT
+    int lo = 0, hi = n_active - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (A.tt_off[mid] * RT <= task) lo = mid;
+      else hi = mid - 1;
+    }
+    const int a = lo;
+    const int ntt = A.tt_off[a + 1] - A.tt_off[a];
+    const int local = task - A.tt_off[a] * RT;
+    const int rtile = local / ntt, ttile = local - rtile * ntt;
+    const int64_t e = A.active[a];
+    const int off = A.act_off[a], cnt = A.act_off[a + 1] - off;
+    const int m0 = ttile * kMT, nvalid = min(kMT, cnt - m0);
+    __syncthreads();  // the previous task's readers of s_slot and s_a are done
+    if (threadIdx.x < kMT) s_slot[threadIdx.x] = A.slot_list[off + m0 + min((int)threadIdx.x, nvalid - 1)];
+    __syncthreads();
+    const int64_t arow = NMAT == 2 ? (int64_t)(s_slot[tt] / A.topk) : (int64_t)s_slot[tt];
+    const v4i* qrow = reinterpret_cast<const v4i*>(qsrc + arow * K + part * 64);  // per-lane row: plain loads
+    const int wrow = min(rtile * kMN + wv * 16 + li, N - 1);
+    MatRsrc mr[NMAT];
+#pragma unroll
+    for (int m = 0; m < NMAT; ++m) {
+      const int p = NMAT == 2 ? m : 2;
+      mr[m] = mat_rsrc(A.codes[p] + e * A.stride_codes[p], A.scales[p] + e * A.stride_scales[p], N, kb);
+    }
+    float acc[4][NMAT][4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc[mt][m][v] = 0.0f;
+
+    MfmaStage<NMAT> st;
+    mfma_fetch<NMAT>(st, qrow, dsrc, bsrc, arow, mr, wrow, kb, g, 0);
+    for (int b = 0; b < kb; ++b) {
+      const int buf = b & 1;
+      v4i* dst = reinterpret_cast<v4i*>(s_a[buf] + tt * kAStride + part * 64);
+      dst[0] = st.a0;
+      dst[1] = st.a1;
+      dst[2] = st.a2;
+      dst[3] = st.a3;
+      if (part == 0) {
+        s_d[buf][tt] = st.d;
+        s_b[buf][tt] = st.bs;
+      }
+      uint4 wc[NMAT][2];
+      float sf[NMAT];
+#pragma unroll
+      for (int m = 0; m < NMAT; ++m) {
+        wc[m][0] = st.w[m][0];
+        wc[m][1] = st.w[m][1];
+        sf[m] = f16_bits_to_f32(st.s[m]);
+      }
+      if (b + 1 < kb) mfma_fetch<NMAT>(st, qrow, dsrc, bsrc, arow, mr, wrow, kb, g, b + 1);
+      __syncthreads();
+      v4i bop[NMAT][2][2];
+#pragma unroll
+      for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const uint4 w = wc[m][c];
+          bop[m][c][0] = v4i{int(w.x & kLowNibbles), int(w.y & kLowNibbles), int(w.z & kLowNibbles), int(w.w & kLowNibbles)};
+          bop[m][c][1] = v4i{int((w.x >> 4) & kLowNibbles), int((w.y >> 4) & kLowNibbles), int((w.z >> 4) & kLowNibbles),
+                             int((w.w >> 4) & kLowNibbles)};
+        }
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        const int8_t* arow_lds = s_a[buf] + (mt * 16 + li) * kAStride;
+        v4i aop[2][2];
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) aop[c][h] = lds_v4i(arow_lds + 32 * (4 * c + g) + 16 * h);
+        const int4 bs4 = *reinterpret_cast<const int4*>(&s_b[buf][mt * 16 + 4 * g]);
+        const float4 d4 = *reinterpret_cast<const float4*>(&s_d[buf][mt * 16 + 4 * g]);
+#pragma unroll
+        for (int m = 0; m < NMAT; ++m) {
+          v4i C = v4i{-4 * bs4.x, -4 * bs4.y, -4 * bs4.z, -4 * bs4.w};
+          C = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[0][0], bop[m][0][0], C, 0, 0, 0);
+          C = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[0][1], bop[m][0][1], C, 0, 0, 0);
+          C = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[1][0], bop[m][1][0], C, 0, 0, 0);
+          C = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[1][1], bop[m][1][1], C, 0, 0, 0);
+          acc[mt][m][0] = fmaf(sf[m] * d4.x, (float)C[0], acc[mt][m][0]);
+          acc[mt][m][1] = fmaf(sf[m] * d4.y, (float)C[1], acc[mt][m][1]);
+          acc[mt][m][2] = fmaf(sf[m] * d4.z, (float)C[2], acc[mt][m][2]);
+          acc[mt][m][3] = fmaf(sf[m] * d4.w, (float)C[3], acc[mt][m][3]);
+        }
+      }
+    }
+    // output: token tile row mt*16 + 4g + v, weight row orow
+    const int orow = rtile * kMN + wv * 16 + li;
+    if (orow < N) {
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int t = mt * 16 + 4 * g + v;
+          if (t < nvalid) {
+            const int64_t slot = s_slot[t];
+            if constexpr (NMAT == 2) A.h[slot * A.inter + orow] = silu_f32(acc[mt][0][v]) * acc[mt][1][v];
+            else A.yd[slot * A.hidden + orow] = acc[mt][0][v];
+          }
+        }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------
 // Single-token step (t == 1, topk <= 8): two kernels and no dispatch pass. Each slot
 // is its own task (a duplicated expert is simply computed twice), so the expert comes
 // straight from topk_idx; x is quantized once per workgroup into LDS while the weight
@@ -485,15 +694,6 @@ struct LaneRow {
   uint4 w[NL];
   uint16_t s[NL];
 };
-
-// One matrix of one expert as buffer resources (codes and scales).
-struct MatRsrc {
-  __amdgpu_buffer_rsrc_t codes, scales;
-};
-
-__device__ __forceinline__ MatRsrc mat_rsrc(const uint8_t* codes, const uint16_t* scales, int n, int kb) {
-  return {make_rsrc(codes, (uint32_t)n * (uint32_t)kb * 128u), make_rsrc(scales, (uint32_t)n * (uint32_t)kb * 2u)};
-}
 
 // Row `row` (wave-uniform) of a matrix: the lane's NL chunks and their scales. Chunks past
 // the row end reload the row's last block (their activations are zero).
@@ -882,7 +1082,6 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
     return fail(TQ_ERR_INVALID, "%s: topk = %d outside [1, min(%d, n_experts)]", fn, topk, kMaxTopk);
   if (flags & ~(TQ_MOE_FORCE_VALU | TQ_MOE_FORCE_MFMA) || flags == (TQ_MOE_FORCE_VALU | TQ_MOE_FORCE_MFMA))
     return fail(TQ_ERR_INVALID, "%s: bad flags 0x%x", fn, flags);
-  if (flags & TQ_MOE_FORCE_MFMA) return fail(TQ_ERR_INVALID, "%s: the MFMA expert path is not available", fn);
   if (t == 0) {
     for (int i = 0; i < kNumStages; ++i)
       if ((st = empty_stage(events, i, (hipStream_t)stream, fn)) != TQ_OK) return st;
@@ -917,6 +1116,7 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   A.ctrl = reinterpret_cast<int32_t*>(base + L.ctrl);
   A.active = reinterpret_cast<int32_t*>(base + L.active);
   A.act_off = reinterpret_cast<int32_t*>(base + L.act_off);
+  A.tt_off = reinterpret_cast<int32_t*>(base + L.tt_off);
   A.slot_list = reinterpret_cast<int32_t*>(base + L.slot_list);
   A.xq = reinterpret_cast<int8_t*>(base + L.xq);
   A.xd = reinterpret_cast<float*>(base + L.xd);
@@ -957,12 +1157,24 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
       return st;
     return empty_stage(events, 4, stm, fn);
   }
+  // per-expert contraction on MFMA for prefill-sized groups (or when forced), VALU dot4
+  // otherwise
+  const bool mfma = (flags & TQ_MOE_FORCE_MFMA) || (!(flags & TQ_MOE_FORCE_VALU) && S >= kMfmaMinSlots);
+  A.tiles_mgu = (ex->inter + kMN - 1) / kMN;
+  A.tiles_mdn = (ex->hidden + kMN - 1) / kMN;
+  const int64_t max_tiles = S / kMT + max_active;
+  const unsigned g_mgu = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mgu, cap);
+  const unsigned g_mdn = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mdn, cap);
   if ((st = launch_stage(events, 0, k_moe_prologue, dim3(nq + 1), 256, stm, fn, x, A, nq)) != TQ_OK) return st;
-  if ((st = launch_stage(events, 1, pick_gateup(nl_gu, nt), dim3(g_gu), 256, stm, fn, A)) != TQ_OK) return st;
+  if (mfma) st = launch_stage(events, 1, k_moe_mfma<2>, dim3(g_mgu), 256, stm, fn, A);
+  else st = launch_stage(events, 1, pick_gateup(nl_gu, nt), dim3(g_gu), 256, stm, fn, A);
+  if (st != TQ_OK) return st;
   if ((st = launch_stage(events, 2, k_moe_requant, dim3((unsigned)((hblocks + 31) / 32)), 256, stm, fn, A, hblocks)) !=
       TQ_OK)
     return st;
-  if ((st = launch_stage(events, 3, pick_down(nl_dn, nt), dim3(g_dn), 256, stm, fn, A)) != TQ_OK) return st;
+  if (mfma) st = launch_stage(events, 3, k_moe_mfma<1>, dim3(g_mdn), 256, stm, fn, A);
+  else st = launch_stage(events, 3, pick_down(nl_dn, nt), dim3(g_dn), 256, stm, fn, A);
+  if (st != TQ_OK) return st;
   const int64_t nout = t * (ex->hidden / 4);
   if ((st = launch_stage(events, 4, k_moe_combine, dim3((unsigned)((nout + 255) / 256)), 256, stm, fn, A, out)) != TQ_OK)
     return st;

@@ -188,3 +188,30 @@ def test_moe_prefill_2048_sampled(tq, oracle, experts_h4096):
     tokens = sorted(set([int(np.where((idx == 0).any(1))[0][0]), int(np.where((idx == cold).any(1))[0][0]), 0, 777, 2047]))
     get = oracle_pkg.expert_getter(gen.SEED, 0, c["hidden"], c["inter"], oracle)
     check_moe(tq, oracle, experts_h4096, get, x, idx, w, out, ws, tokens)
+
+
+@pytest.mark.parametrize("E,H,I,T,topk", [(5, 512, 768, 150, 3), (4, 1280, 256, 70, 2)])
+def test_moe_mfma_forced_small(tq, oracle, E, H, I, T, topk):
+    """The int8 MFMA expert path on host-packed experts: one expert spans several
+    64-token tiles, hidden/inter give ragged row tiles and odd block counts."""
+    ex, logical = host_experts(tq, oracle, E, H, I, seed=21)
+    rng = np.random.default_rng(22)
+    x = (rng.standard_normal((T, H)) * np.exp(rng.uniform(-2, 2, (T, 1)))).astype(np.float32)
+    idx = np.stack([np.concatenate([[0], rng.choice(np.arange(1, E), topk - 1, replace=False)]) for _ in range(T)]).astype(np.int32)
+    w = rng.uniform(0.1, 1.0, (T, topk)).astype(np.float32)
+    announce(f"moe mfma E={E} H={H} I={I} T={T}")
+    out, ws = run_moe(tq, ex, x, idx, w, flags=tq.TQ_MOE_FORCE_MFMA)
+    check_moe(tq, oracle, ex, lambda e: logical[e], x, idx, w, out, ws, [0, 1, 63, 64, 65, T - 1])
+    out2, _ = run_moe(tq, ex, x, idx, w, flags=tq.TQ_MOE_FORCE_MFMA)
+    assert torch.equal(out, out2)
+
+
+def test_moe_mfma_forced_batch32(tq, oracle, experts_h4096):
+    """The batched-decode workload forced onto the MFMA path (all tokens checked)."""
+    c = gen.CONFIGS[2]
+    x = gen.activations(gen.SEED, 0, c["tokens"], c["hidden"])
+    idx, w = gen.routing(gen.SEED, 0, c["tokens"], c["experts"], c["topk"], c["routing"])
+    announce("moe mfma forced t=32")
+    out, ws = run_moe(tq, experts_h4096, x, idx, w, flags=tq.TQ_MOE_FORCE_MFMA)
+    get = oracle_pkg.expert_getter(gen.SEED, 0, c["hidden"], c["inter"], oracle)
+    check_moe(tq, oracle, experts_h4096, get, x, idx, w, out, ws, list(range(c["tokens"])))
