@@ -14,11 +14,14 @@
  * Persistent layout of one matrix with n output channels (rows) and k inputs
  * (k % 256 == 0, kb = k/256 blocks per row):
  *   codes  [n][kb][128] bytes, 128-byte aligned. Block (r, b) holds the 256 codes of
- *          row r, columns 256b .. 256b+255, as unsigned nibbles u = c + 4 (0..8; the
- *          values 9..15 never occur). Byte 16j + i (j = 0..7, i = 0..15) holds column
- *          256b + 32j + i in its low nibble and column 256b + 32j + 16 + i in its high
- *          nibble, so that the 16 bytes of chunk j unpack to 32 int8 codes whose
- *          activations are 32 contiguous bytes.
+ *          row r, columns 256b .. 256b+255, as 4-bit two's-complement nibbles c & 15
+ *          (c = 0..4 -> 0..4, c = -4..-1 -> 12..15; 5..11 never occur). Byte 16j + i
+ *          (j = 0..7, i = 0..15) holds column 256b + 32j + i in its low nibble and column
+ *          256b + 32j + 16 + i in its high nibble, so that the 16 bytes of chunk j unpack
+ *          to 32 int8 codes whose activations are 32 contiguous bytes. The sign sits in
+ *          each nibble's top bit: masking a byte's high nibble in place (b & 0xF0), or
+ *          shifting its low nibble up ((b << 4) & 0xF0), gives 16*c as a signed byte, so
+ *          the codes decode by two bitwise operations with no offset to correct.
  *   scales [n][kb] IEEE binary16 bit patterns (s of row r, block b).
  *   Bytes: 128 + 2 per 256 weights = 4.0625 bits/weight, the paper's figure.
  * Quantized activations of t tokens over k inputs:
@@ -30,7 +33,7 @@
  *   d = 0 and q = 0.
  * Block integer sum and combine (Sec. 2.2):
  *   isum[t][r][b] = sum_i c[r][256b+i] * q[t][256b+i] (exact int32; computed as
- *   sum u*q - 4*bsum), y[t][r] = sum_b f32(s[r][b]) * d[t][b] * isum[t][r][b] in fp32
+ *   (sum (16c)*q) >> 4), y[t][r] = sum_b f32(s[r][b]) * d[t][b] * isum[t][r][b] in fp32
  *   (block order unspecified).
  *
  * Conventions for every entry point:
@@ -44,7 +47,7 @@
  *    message is thread-local and valid until the calling thread's next call).
  *  - TQ_ERR_DEVICE reports a launch failure (the HIP error string is in tq_last_error).
  *  - Preconditions not checked (documented): activations are finite; codes hold only
- *    nibbles 0..8; buffers are at least as large as their stated shapes.
+ *    the nibbles of -4..4; buffers are at least as large as their stated shapes.
  *  - Thread-safe: no state besides the thread-local error message.
  */
 #ifndef TQ_H_
@@ -102,13 +105,13 @@ size_t tq_scales_bytes(int32_t n, int32_t k);
 
 /* Fold and pack on the host (Sec. 2.1 fold, Sec. 2.2 persistent format).
  * t1, t2: host [n][k] trits in {-1,0,1}; codes_out: host, tq_codes_bytes(n, k) bytes.
- * Writes c = 3*t1 + t2 as u = c + 4 nibbles in the layout above. TQ_ERR_INVALID if a
+ * Writes c = 3*t1 + t2 as nibbles c & 15 in the layout above. TQ_ERR_INVALID if a
  * trit is out of range (codes_out is then unspecified). */
 tq_status tq_fold_pack_host(const int8_t* t1, const int8_t* t2, int32_t n, int32_t k,
                             uint8_t* codes_out);
 
 /* Inverse of the packing on the host: codes (host, layout above) -> c_out (host [n][k]
- * int8 in -4..4). TQ_ERR_INVALID if a nibble exceeds 8. */
+ * int8 in -4..4). TQ_ERR_INVALID if a nibble is not that of -4..4 (5..11). */
 tq_status tq_unpack_host(const uint8_t* codes, int32_t n, int32_t k, int8_t* c_out);
 
 /* Synthetic matrix generated on the device, folded and packed in place: trits and
@@ -129,8 +132,9 @@ tq_status tq_quantize_act(const float* x, int64_t t, int32_t k, int8_t* q, float
                           int32_t* bsum, void* stream);
 
 /* The serving dot pass for one matrix and t tokens (Sec. 2.2): y[t][n] fp32 =
- * sum_b f32(s[r][b]) * d[t][b] * isum[t][r][b]. q, d, bsum as from tq_quantize_act
- * (q 16-byte aligned). isum_dbg: NULL, or a [t][n][kb] int32 buffer that receives the
+ * sum_b f32(s[r][b]) * d[t][b] * isum[t][r][b]. q, d as from tq_quantize_act (q 16-byte
+ * aligned); bsum is accepted so callers can pass the quantizer's whole output, but the
+ * signed nibbles need no offset correction and the kernel does not read it (may be NULL). isum_dbg: NULL, or a [t][n][kb] int32 buffer that receives the
  * exact block sums (debug and parity; same kernel, one extra store per block).
  * t >= 0 (t = 0 is a no-op). */
 tq_status tq_gemv(const tq_mat* w, const int8_t* q, const float* d, const int32_t* bsum,

@@ -22,8 +22,6 @@ constexpr int kDppRowRor8 = 0x128;    // lane i <- lane (i+8) mod 16 within each
 // ds_swizzle bit-mode offset: lane ^ 16 within each 32-lane half (and 0x1f, xor 0x10).
 constexpr int kSwizzleXor16 = 0x401f;
 
-constexpr uint32_t kLowNibbles = 0x0F0F0F0Fu;
-
 // Sum over the 8 lanes of a group; every lane of the group receives the sum.
 __device__ __forceinline__ int group_sum_i32(int v) {
   v += __builtin_amdgcn_update_dpp(0, v, kDppXor1, 0xf, 0xf, false);
@@ -39,33 +37,24 @@ __device__ __forceinline__ float group_max_f32(float v) {
   return v;
 }
 
-// Sum of one representative per group (lanes l, l^8, ..., l^56) over the whole wave;
-// the result is wave-uniform. Fixed order, so deterministic.
-__device__ __forceinline__ float wave_sum_groups_f32(float v) {
-  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), kDppRowRor8, 0xf, 0xf, false));
-  v += __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), kSwizzleXor16));
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)) +
-         __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
-}
-
 __device__ __forceinline__ float f16_bits_to_f32(uint16_t h) {
   return __half2float(__ushort_as_half(h));
 }
 
-// Integer dot of one 16-byte code chunk (32 unsigned nibbles u = c + 4) with the
-// chunk's 32 int8 activations a[0..7] (dwords: a[m] = columns 4m..4m+3 of the low
-// half, a[4+m] = columns 16+4m..16+4m+3).
-__device__ __forceinline__ int dot_chunk_u(const uint4 w, const int (&a)[8]) {
-  int acc = 0;
-  acc = __builtin_amdgcn_sdot4(int(w.x & kLowNibbles), a[0], acc, false);
-  acc = __builtin_amdgcn_sdot4(int((w.x >> 4) & kLowNibbles), a[4], acc, false);
-  acc = __builtin_amdgcn_sdot4(int(w.y & kLowNibbles), a[1], acc, false);
-  acc = __builtin_amdgcn_sdot4(int((w.y >> 4) & kLowNibbles), a[5], acc, false);
-  acc = __builtin_amdgcn_sdot4(int(w.z & kLowNibbles), a[2], acc, false);
-  acc = __builtin_amdgcn_sdot4(int((w.z >> 4) & kLowNibbles), a[6], acc, false);
-  acc = __builtin_amdgcn_sdot4(int(w.w & kLowNibbles), a[3], acc, false);
-  acc = __builtin_amdgcn_sdot4(int((w.w >> 4) & kLowNibbles), a[7], acc, false);
-  return acc;
+// Codes are 4-bit two's-complement nibbles (c & 15). Keeping a byte's high nibble in
+// place, or moving its low nibble up, leaves 16*c as a signed byte: the codes of a
+// 16-byte chunk become 32 int8 values 16c in two bitwise operations per half, ready for
+// the signed 4-way byte dot, and the dot's sum is exactly 16 times the code dot.
+constexpr uint32_t kHiNibbles = 0xF0F0F0F0u;
+
+__device__ __forceinline__ int lo16c(uint32_t w) { return int((w << 4) & kHiNibbles); }
+__device__ __forceinline__ int hi16c(uint32_t w) { return int(w & kHiNibbles); }
+
+// The 32 codes of one chunk as 16c bytes, in the order of the activation dwords:
+// c[m] = columns 4m..4m+3 (low nibbles of bytes 4m..4m+3), c[4+m] = columns 16+4m..
+__device__ __forceinline__ void unpack16c(const uint4 w, int (&c)[8]) {
+  c[0] = lo16c(w.x); c[1] = lo16c(w.y); c[2] = lo16c(w.z); c[3] = lo16c(w.w);
+  c[4] = hi16c(w.x); c[5] = hi16c(w.y); c[6] = hi16c(w.z); c[7] = hi16c(w.w);
 }
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -150,32 +139,117 @@ __device__ __forceinline__ void quantize_group32(const float (&x)[32], int (&qw)
 // the number of values a lane carries and pairs lanes whose index differs in one bit).
 // ---------------------------------------------------------------------------------
 
-template <int M>
-__device__ __forceinline__ float lane_xor(float v) {
-  const int iv = __float_as_int(v);
-  if constexpr (M == 1) return __int_as_float(__builtin_amdgcn_update_dpp(0, iv, kDppXor1, 0xf, 0xf, false));
-  else if constexpr (M == 2) return __int_as_float(__builtin_amdgcn_update_dpp(0, iv, kDppXor2, 0xf, 0xf, false));
-  else if constexpr (M == 4) return __int_as_float(__builtin_amdgcn_ds_swizzle(iv, 0x101f));
-  else if constexpr (M == 8) return __int_as_float(__builtin_amdgcn_update_dpp(0, iv, kDppRowRor8, 0xf, 0xf, false));
-  else if constexpr (M == 16) return __int_as_float(__builtin_amdgcn_ds_swizzle(iv, kSwizzleXor16));
-  else return __int_as_float(__builtin_amdgcn_ds_bpermute((int)((__lane_id() ^ 32) << 2), iv));
+constexpr int clog2(int n) { return n <= 1 ? 0 : 1 + clog2(n >> 1); }
+
+// The low L bits of x in reverse order (L <= 5).
+template <int L>
+__device__ __forceinline__ int rev_bits(int x) {
+  if constexpr (L == 0) return 0;
+  else return (int)(__builtin_bitreverse32((unsigned)x) >> (32 - L));
 }
+
+// The value of lane (lane ^ M).
+template <int M>
+__device__ __forceinline__ int lane_xor_i(int v) {
+  if constexpr (M == 1) return __builtin_amdgcn_update_dpp(0, v, kDppXor1, 0xf, 0xf, false);
+  else if constexpr (M == 2) return __builtin_amdgcn_update_dpp(0, v, kDppXor2, 0xf, 0xf, false);
+  else if constexpr (M == 4) return __builtin_amdgcn_ds_swizzle(v, 0x101f);  // bit mode, xor 4
+  else if constexpr (M == 8) return __builtin_amdgcn_update_dpp(0, v, kDppRowRor8, 0xf, 0xf, false);
+  else if constexpr (M == 16) return __builtin_amdgcn_ds_swizzle(v, kSwizzleXor16);
+  else return __builtin_amdgcn_ds_bpermute((int)((__lane_id() ^ 32) << 2), v);
+}
+
+template <int M>
+__device__ __forceinline__ float lane_xor(float v) { return __int_as_float(lane_xor_i<M>(__float_as_int(v))); }
+
+template <int M>
+__device__ __forceinline__ int lane_xchg(int v) { return lane_xor_i<M>(v); }
+template <int M>
+__device__ __forceinline__ float lane_xchg(float v) { return lane_xor<M>(v); }
 
 // v[0 .. N2) -> v[0 .. N2/2): a lane whose index has bit M set keeps the upper half of
 // the values, the others the lower half, each adding its partner's (lane ^ M) copy.
-template <int N2, int M, int SZ>
-__device__ __forceinline__ void bfly_step(float (&v)[SZ]) {
+template <int N2, int M, typename T, int SZ>
+__device__ __forceinline__ void bfly_step(T (&v)[SZ]) {
   static_assert(N2 <= SZ && N2 % 2 == 0, "bad butterfly step");
   const bool up = (__lane_id() & M) != 0;
 #pragma unroll
   for (int k = 0; k < N2 / 2; ++k) {
-    const float keep = up ? v[k + N2 / 2] : v[k];
-    const float send = up ? v[k] : v[k + N2 / 2];
-    v[k] = keep + lane_xor<M>(send);
+    const T keep = up ? v[k + N2 / 2] : v[k];
+    const T send = up ? v[k] : v[k + N2 / 2];
+    v[k] = keep + lane_xchg<M>(send);
   }
 }
 
 template <int M>
 __device__ __forceinline__ float xor_sum(float v) { return v + lane_xor<M>(v); }
+
+// Row totals of a wave's dot products in the order of operations of the serving pass:
+// exact integer block sums, one fp32 multiply-add per block, then the sum over blocks.
+//
+// A wave computes NI items (row x token pairs, a power of two), each for NM matrices
+// that share the item (gate and up). For load i a lane holds the integer partials
+// p[item * NM + m] of its 32 codes of block 8i + (lane >> 3); the 8 lanes of that block
+// differ in lane bits 0..2.
+//  block_sums (exact, once per load): a butterfly over lane bits 0..2 (LI halving
+//    steps, then plain sums over the bits left) leaves each lane KI = NI >> LI items,
+//    item = k + KI * rev(lane bits 0..LI-1), as whole-block sums.
+//  The caller then scales each kept block sum: acc[k * NM + m] += f32(s) * d * isum.
+//  block_totals (fp32, once per row): a butterfly over lane bits 3..5 (the 8 blocks of
+//    a load; LF halving steps, then plain sums) leaves one item per lane:
+//    item() = rev(lane bits 3..3+LF-1) + KI * rev(lane bits 0..LI-1).
+// Every lane of a wave ends up with a total; writer() picks one lane per item.
+template <int NI, int NM>
+struct RowReduce {
+  static_assert(NI >= 1 && NI <= 64 && (NI & (NI - 1)) == 0, "items: a power of two <= 64");
+  static constexpr int LI = clog2(NI) < 3 ? clog2(NI) : 3;
+  static constexpr int KI = NI >> LI;
+  static constexpr int LF = clog2(KI);
+  static constexpr int NV = NI * NM;
+
+  // kept item k after block_sums
+  __device__ static __forceinline__ int kept(int k, int lane) { return k + KI * rev_bits<LI>(lane & ((1 << LI) - 1)); }
+  // the item a lane holds after block_totals
+  __device__ static __forceinline__ int item(int lane) {
+    return rev_bits<LF>((lane >> 3) & ((1 << LF) - 1)) + KI * rev_bits<LI>(lane & ((1 << LI) - 1));
+  }
+  __device__ static __forceinline__ bool writer(int lane) { return ((lane & 7) >> LI) == 0 && ((lane >> 3) >> LF) == 0; }
+  // a lane that holds kept items (one lane per group of identical copies)
+  __device__ static __forceinline__ bool block_writer(int lane) { return ((lane & 7) >> LI) == 0; }
+
+  __device__ static __forceinline__ void block_sums(int (&v)[NV]) {
+    if constexpr (LI >= 1) bfly_step<NV, 1>(v);
+    if constexpr (LI >= 2) bfly_step<NV / 2, 2>(v);
+    if constexpr (LI >= 3) bfly_step<NV / 4, 4>(v);
+#pragma unroll
+    for (int k = 0; k < KI * NM; ++k) {
+      if constexpr (LI < 1) v[k] += lane_xor_i<1>(v[k]);
+      if constexpr (LI < 2) v[k] += lane_xor_i<2>(v[k]);
+      if constexpr (LI < 3) v[k] += lane_xor_i<4>(v[k]);
+    }
+  }
+
+  __device__ static __forceinline__ void block_totals(float (&a)[KI * NM]) {
+    if constexpr (LF >= 1) bfly_step<KI * NM, 8>(a);
+    if constexpr (LF >= 2) bfly_step<KI * NM / 2, 16>(a);
+    if constexpr (LF >= 3) bfly_step<KI * NM / 4, 32>(a);
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+      if constexpr (LF < 1) a[m] = xor_sum<8>(a[m]);
+      if constexpr (LF < 2) a[m] = xor_sum<16>(a[m]);
+      if constexpr (LF < 3) a[m] = xor_sum<32>(a[m]);
+    }
+  }
+};
+
+// Integer partials of one 16-byte chunk (32 codes, unpacked as 16c bytes) against 32
+// int8 activations: sum (16c) * q, an exact multiple of 16 (|.| <= 32 * 64 * 127; a whole
+// block's sum stays below 2^21, and >> 4 of it is the exact block sum of c * q).
+__device__ __forceinline__ int dot32x16(const int (&c)[8], const int (&a)[8]) {
+  int acc = 0;
+#pragma unroll
+  for (int m = 0; m < 8; ++m) acc = __builtin_amdgcn_sdot4(c[m], a[m], acc, false);
+  return acc;
+}
 
 }  // namespace tq

@@ -5,12 +5,14 @@
 // Decode is HBM-bound (0.5 byte of codes per weight, a few integer ops per weight per
 // token), so the kernel is shaped for the memory system: each wave owns RPW whole
 // rows, issues all of their 16-byte code loads up front (a wave load = 8 consecutive
-// blocks = 1 KB, fully coalesced), and keeps them in registers while it walks the
-// tokens NT at a time. A lane always covers the same columns of every row it owns
+// blocks = 1 KB, fully coalesced), and keeps them in registers, unpacked, while it walks
+// the tokens NT at a time. A lane always covers the same columns of every row it owns
 // (block 8i + l/8, chunk l & 7 for load i), so its activations sit in registers too,
-// loaded once per token chunk. The 8 lanes of a block reduce their partial dots with 3
-// DPP adds (exact int32), subtract 4*bsum (codes are stored as u = c + 4), multiply by
-// f32(s)*d, and the row total is one DPP/swizzle/readlane reduction.
+// loaded once per token chunk. Per load, the lanes' exact 32-code partials of all
+// RPW x NT (row, token) items meet in one integer butterfly over the 8 lanes of each
+// block (exact block sums, which the debug output stores), each kept block sum gets one
+// fp32 multiply-add by f32(s) * d, and one fp32 butterfly over the blocks gives the row
+// totals.
 #include "tq_device.hpp"
 #include "tq_internal.hpp"
 
@@ -19,81 +21,88 @@ namespace tq {
 template <int NL, int NT, int RPW>
 __global__ __launch_bounds__(256) void k_gemv(const uint8_t* __restrict__ codes,
                                               const uint16_t* __restrict__ scales, int n, int kb,
-                                              const int8_t* __restrict__ q, const float* __restrict__ d,
-                                              const int32_t* __restrict__ bsum, int t,
+                                              const int8_t* __restrict__ q, const float* __restrict__ d, int t,
                                               float* __restrict__ y, int32_t* __restrict__ isum_dbg) {
+  static_assert(RPW <= 8 && (RPW & (RPW - 1)) == 0, "RPW: a power of two <= 8");
+  using RR = RowReduce<RPW * NT, 1>;
+  constexpr int KI = RR::KI;
   const int lane = threadIdx.x & 63;
   const int g = lane >> 3, cp = lane & 7;
   const int row0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * RPW;
   if (row0 >= n) return;
   const int64_t k = (int64_t)kb * 256;
 
-  // Loads are unconditional from clamped addresses; invalid lanes are zeroed by a select
-  // (a predicated load becomes a branch that serializes the loads).
-  uint4 w[RPW][NL];
-  float s[RPW][NL];
+  // Loads are unconditional from clamped addresses (a predicated load becomes a branch
+  // that serializes the loads): rows past n are computed and not stored, blocks past kb
+  // get d = 0 and add exactly nothing.
+  int c[RPW][NL][8];
 #pragma unroll
   for (int r = 0; r < RPW; ++r) {
     const int64_t rc = min(row0 + r, n - 1);
-    const uint8_t* rowcodes = codes + rc * kb * 128;
-    const uint16_t* rowscales = scales + rc * kb;
 #pragma unroll
-    for (int i = 0; i < NL; ++i) {
-      const int b = 8 * i + g;
-      const bool ok = b < kb && row0 + r < n;
-      const int bc = b < kb ? b : kb - 1;
-      const uint4 raw = ldg16(rowcodes + bc * 128 + cp * 16);
-      const float sv = f16_bits_to_f32(rowscales[bc]);
-      w[r][i] = ok ? raw : make_uint4(0, 0, 0, 0);
-      s[r][i] = ok ? sv : 0.0f;
-    }
+    for (int i = 0; i < NL; ++i) unpack16c(ldg16(codes + (rc * kb + min(8 * i + g, kb - 1)) * 128 + cp * 16), c[r][i]);
   }
+  // after the block butterfly a lane keeps items of one row (RPW <= 8): its scales
+  const int lrow = min(row0 + rev_bits<clog2(RPW)>(lane & (RPW - 1)), n - 1);
+  float s[NL];
+#pragma unroll
+  for (int i = 0; i < NL; ++i) s[i] = f16_bits_to_f32(scales[(int64_t)lrow * kb + min(8 * i + g, kb - 1)]);
 
   for (int t0 = 0; t0 < t; t0 += NT) {
     int qa[NT][NL][8];
-    float dd[NT][NL];
-    int bb[NT][NL];
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
       for (int i = 0; i < NL; ++i) {
-        const int tok = t0 + tt, b = 8 * i + g;
-        const bool ok = tok < t && b < kb;
-        const int64_t tc = min(tok, t - 1);
-        const int bc = b < kb ? b : kb - 1;
-        const int4* p = reinterpret_cast<const int4*>(q + tc * k + bc * 256 + cp * 32);
+        const int64_t tc = min(t0 + tt, t - 1);
+        const int4* p = reinterpret_cast<const int4*>(q + tc * k + min(8 * i + g, kb - 1) * 256 + cp * 32);
         const int4 lo = p[0], hi = p[1];
-        const float dv = d[tc * kb + bc];
-        const int bv = bsum[tc * kb + bc];
-        qa[tt][i][0] = ok ? lo.x : 0; qa[tt][i][1] = ok ? lo.y : 0; qa[tt][i][2] = ok ? lo.z : 0;
-        qa[tt][i][3] = ok ? lo.w : 0; qa[tt][i][4] = ok ? hi.x : 0; qa[tt][i][5] = ok ? hi.y : 0;
-        qa[tt][i][6] = ok ? hi.z : 0; qa[tt][i][7] = ok ? hi.w : 0;
-        dd[tt][i] = ok ? dv : 0.0f;
-        bb[tt][i] = ok ? bv : 0;
+        qa[tt][i][0] = lo.x; qa[tt][i][1] = lo.y; qa[tt][i][2] = lo.z; qa[tt][i][3] = lo.w;
+        qa[tt][i][4] = hi.x; qa[tt][i][5] = hi.y; qa[tt][i][6] = hi.z; qa[tt][i][7] = hi.w;
       }
+    // the lane's kept items: their tokens' block scales (zero past t or past kb)
+    float dk[KI][NL];
 #pragma unroll
-    for (int r = 0; r < RPW; ++r) {
-      const int row = row0 + r;
+    for (int kk = 0; kk < KI; ++kk) {
+      const int tok = t0 + RR::kept(kk, lane) % NT;
 #pragma unroll
-      for (int tt = 0; tt < NT; ++tt) {
-        const int tok = t0 + tt;
-        float acc = 0.0f;
+      for (int i = 0; i < NL; ++i) {
+        const int b = 8 * i + g;
+        const float dv = d[(int64_t)min(tok, t - 1) * kb + min(b, kb - 1)];
+        dk[kk][i] = (tok < t && b < kb) ? dv : 0.0f;
+      }
+    }
+    float acc[KI];
 #pragma unroll
-        for (int i = 0; i < NL; ++i) {
-          const int is = group_sum_i32(dot_chunk_u(w[r][i], qa[tt][i])) - 4 * bb[tt][i];
-          if (isum_dbg != nullptr && cp == 0 && tok < t && row < n && 8 * i + g < kb)
-            isum_dbg[((int64_t)tok * n + row) * kb + 8 * i + g] = is;
-          acc = fmaf(s[r][i] * dd[tt][i], (float)is, acc);
+    for (int kk = 0; kk < KI; ++kk) acc[kk] = 0.0f;
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      int p[RPW * NT];
+#pragma unroll
+      for (int r = 0; r < RPW; ++r)
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt) p[r * NT + tt] = dot32x16(c[r][i], qa[tt][i]);
+      RR::block_sums(p);
+#pragma unroll
+      for (int kk = 0; kk < KI; ++kk) {
+        const int is = p[kk] >> 4;  // exact block sum of c * q
+        acc[kk] = fmaf(s[i] * dk[kk][i], (float)is, acc[kk]);
+        if (isum_dbg != nullptr && RR::block_writer(lane)) {
+          const int it = RR::kept(kk, lane), tok = t0 + it % NT, row = row0 + it / NT, b = 8 * i + g;
+          if (tok < t && row < n && b < kb) isum_dbg[((int64_t)tok * n + row) * kb + b] = is;
         }
-        const float tot = wave_sum_groups_f32(acc);
-        if (lane == 0 && tok < t && row < n) y[(int64_t)tok * n + row] = tot;
       }
+    }
+    RR::block_totals(acc);
+    if (RR::writer(lane)) {
+      const int it = RR::item(lane), tok = t0 + it % NT, row = row0 + it / NT;
+      if (tok < t && row < n) y[(int64_t)tok * n + row] = acc[0];
     }
   }
 }
 
-using gemv_fn = void (*)(const uint8_t*, const uint16_t*, int, int, const int8_t*, const float*,
-                         const int32_t*, int, float*, int32_t*);
+using gemv_fn = void (*)(const uint8_t*, const uint16_t*, int, int, const int8_t*, const float*, int, float*,
+                         int32_t*);
 
 template <int NL>
 static gemv_fn pick_gemv_nl(int nt, int rpw) {
@@ -127,9 +136,10 @@ extern "C" tq_status tq_gemv(const tq_mat* w, const int8_t* q, const float* d, c
     return fail(TQ_ERR_INVALID, "tq_gemv: k = %d must be a positive multiple of 256 <= %d", k, kMaxK);
   if (t < 0 || t > INT32_MAX) return fail(TQ_ERR_INVALID, "tq_gemv: t = %lld out of range", (long long)t);
   if (t == 0) return TQ_OK;
-  if (!w->codes || !w->scales || !q || !d || !bsum || !y) return fail(TQ_ERR_INVALID, "tq_gemv: null pointer");
+  if (!w->codes || !w->scales || !q || !d || !y) return fail(TQ_ERR_INVALID, "tq_gemv: null pointer");
   if (!aligned(w->codes, 128)) return fail(TQ_ERR_ALIGN, "tq_gemv: codes must be 128-byte aligned");
-  if (!aligned(q, 16) || !aligned(w->scales, 2) || !aligned(d, 4) || !aligned(bsum, 4) || !aligned(y, 4) ||
+  (void)bsum;  // signed codes: no offset correction
+  if (!aligned(q, 16) || !aligned(w->scales, 2) || !aligned(d, 4) || !aligned(y, 4) ||
       (isum_dbg && !aligned(isum_dbg, 4)))
     return fail(TQ_ERR_ALIGN, "tq_gemv: q must be 16-byte aligned, other buffers naturally aligned");
   if ((int64_t)t * n * (k / 256) > ((int64_t)1 << 40)) return fail(TQ_ERR_INVALID, "tq_gemv: problem too large");
@@ -141,6 +151,6 @@ extern "C" tq_status tq_gemv(const tq_mat* w, const int8_t* q, const float* d, c
   const unsigned wgs = (unsigned)((waves + 3) / 4);
   (void)hipGetLastError();
   hipLaunchKernelGGL(pick_gemv(nl, nt, rpw), dim3(wgs), dim3(256), 0, (hipStream_t)stream, w->codes, w->scales, n,
-                     kb, q, d, bsum, (int)t, y, isum_dbg);
+                     kb, q, d, (int)t, y, isum_dbg);
   return check_launch("tq_gemv");
 }

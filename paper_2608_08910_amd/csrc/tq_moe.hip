@@ -105,61 +105,6 @@ __device__ __forceinline__ void quantize_wave_blocks(const float* __restrict__ x
   }
 }
 
-// Loads are issued unconditionally from clamped (always valid) addresses and invalid
-// lanes are zeroed with a select afterwards: a predicated load becomes a branch, and the
-// compiler then waits for each load before issuing the next.
-
-// The lane's activation slice of one token: for load i, block 8i + g, chunk cp. The row
-// pointers are those of a valid token; `ok` zeroes the slice.
-template <int NL>
-__device__ __forceinline__ void load_acts(const int8_t* __restrict__ qrow, const float* __restrict__ drow,
-                                          const int32_t* __restrict__ brow, int kb, int g, int cp, bool ok,
-                                          int (&qa)[NL][8], float (&dd)[NL], int (&bb)[NL]) {
-#pragma unroll
-  for (int i = 0; i < NL; ++i) {
-    const int b = 8 * i + g;
-    const bool v = ok && b < kb;
-    const int bc = b < kb ? b : kb - 1;
-    const int4* p = reinterpret_cast<const int4*>(qrow + bc * 256 + cp * 32);
-    const int4 lo = p[0], hi = p[1];
-    const float dv = drow[bc];
-    const int bv = brow[bc];
-    qa[i][0] = v ? lo.x : 0; qa[i][1] = v ? lo.y : 0; qa[i][2] = v ? lo.z : 0; qa[i][3] = v ? lo.w : 0;
-    qa[i][4] = v ? hi.x : 0; qa[i][5] = v ? hi.y : 0; qa[i][6] = v ? hi.z : 0; qa[i][7] = v ? hi.w : 0;
-    dd[i] = v ? dv : 0.0f;
-    bb[i] = v ? bv : 0;
-  }
-}
-
-// One row's lane slice of codes and scales; rowcodes/rowscales point at a valid row.
-template <int NL>
-__device__ __forceinline__ void load_row(const uint8_t* __restrict__ rowcodes, const uint16_t* __restrict__ rowscales,
-                                         int kb, int g, int cp, bool ok, uint4 (&w)[NL], float (&s)[NL]) {
-#pragma unroll
-  for (int i = 0; i < NL; ++i) {
-    const int b = 8 * i + g;
-    const bool v = ok && b < kb;
-    const int bc = b < kb ? b : kb - 1;
-    const uint4 raw = ldg16(rowcodes + bc * 128 + cp * 16);
-    const float sv = f16_bits_to_f32(rowscales[bc]);
-    w[i] = v ? raw : make_uint4(0, 0, 0, 0);
-    s[i] = v ? sv : 0.0f;
-  }
-}
-
-// One row against one token: exact block sums, one multiply-add per block, wave total.
-template <int NL>
-__device__ __forceinline__ float row_dot(const uint4 (&w)[NL], const float (&s)[NL], const int (&qa)[NL][8],
-                                         const float (&dd)[NL], const int (&bb)[NL]) {
-  float acc = 0.0f;
-#pragma unroll
-  for (int i = 0; i < NL; ++i) {
-    const int is = group_sum_i32(dot_chunk_u(w[i], qa[i])) - 4 * bb[i];
-    acc = fmaf(s[i] * dd[i], (float)is, acc);
-  }
-  return wave_sum_groups_f32(acc);
-}
-
 // One matrix of one expert as buffer resources (codes and scales).
 struct MatRsrc {
   __amdgpu_buffer_rsrc_t codes, scales;
@@ -307,104 +252,148 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------------
-// gate_up: h[slot][row] = SiLU(Wg[e] xq) * (Wu[e] xq)
+// Grouped decode on the VALU (a few tokens per expert): task = (active expert, row
+// tile), tasks in rank order strided over the grid. Each wave owns RPW rows of every
+// matrix of the projection (gate and up, or down), reads them once and keeps them in
+// registers already unpacked to 16c bytes, then walks the expert's tokens NT at a time
+// (the last ones singly). Loads are issued unconditionally from clamped addresses
+// (a predicated load becomes a branch that waits for it), and a block that does not
+// exist (ragged k) or a token past the list gets d = 0, which adds exactly nothing.
 // ---------------------------------------------------------------------------------
 
-template <int NL, int NT, int RPW>
-__global__ __launch_bounds__(256) void k_moe_gateup(MoeArgs A) {
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int g = lane >> 3, cp = lane & 7;
-  const int kb = A.hidden / 256, I = A.inter;
-  const int n_tasks = A.ctrl[kTasksGU];
-  for (int task = blockIdx.x; task < n_tasks; task += gridDim.x) {
-    const int a = task / A.tiles_gu, tile = task - a * A.tiles_gu;
-    const int64_t e = A.active[a];
-    const int off = A.act_off[a], cnt = A.act_off[a + 1] - off;
-    const int row0 = (tile * 4 + wv) * RPW;
-    if (row0 >= I) continue;
-    const uint8_t* gc = A.codes[0] + e * A.stride_codes[0];
-    const uint8_t* uc = A.codes[1] + e * A.stride_codes[1];
-    const uint16_t* gs = A.scales[0] + e * A.stride_scales[0];
-    const uint16_t* us = A.scales[1] + e * A.stride_scales[1];
-    uint4 wg[RPW][NL], wu[RPW][NL];
-    float sg[RPW][NL], su[RPW][NL];
+// NT tokens (list positions c0 ..) against the wave's NMAT x RPW rows, whose codes the
+// lane holds unpacked (wc[m * RPW + r][i]) with the scales of its own row (sl[m][i]:
+// after the block butterfly a lane keeps items of one row, rev(lane bits) for RPW <= 8).
+// Items are (row r, token tt) = r * NT + tt, each for the NMAT matrices.
+template <int NMAT, int NL, int RPW, int NT, bool RAGGED>
+__device__ __forceinline__ void tb_tokens(const MoeArgs& A, const int (&wc)[NMAT * RPW][NL][8],
+                                          const float (&sl)[NMAT][NL], __amdgpu_buffer_rsrc_t qr,
+                                          __amdgpu_buffer_rsrc_t dr, int K, int kb, int N, int off, int cnt, int c0,
+                                          int row0, int lane, int g, int cp) {
+  using RR = RowReduce<RPW * NT, NMAT>;
+  constexpr int KI = RR::KI;
+  int slot[NT], arow[NT];
+  int qa[NT][NL][8];
 #pragma unroll
-    for (int r = 0; r < RPW; ++r) {
-      const int64_t row = min(row0 + r, I - 1);
-      load_row<NL>(gc + row * kb * 128, gs + row * kb, kb, g, cp, row0 + r < I, wg[r], sg[r]);
-      load_row<NL>(uc + row * kb * 128, us + row * kb, kb, g, cp, row0 + r < I, wu[r], su[r]);
+  for (int tt = 0; tt < NT; ++tt) {
+    slot[tt] = A.slot_list[off + min(c0 + tt, cnt - 1)];
+    arow[tt] = NMAT == 2 ? slot[tt] / A.topk : slot[tt];
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      const uint32_t bc = (uint32_t)min(8 * i + g, kb - 1);
+      const uint4 lo = buf_load16(qr, bc * 256u + (uint32_t)cp * 32u, (uint32_t)arow[tt] * (uint32_t)K, 0);
+      const uint4 hi = buf_load16(qr, bc * 256u + (uint32_t)cp * 32u + 16u, (uint32_t)arow[tt] * (uint32_t)K, 0);
+      qa[tt][i][0] = (int)lo.x; qa[tt][i][1] = (int)lo.y; qa[tt][i][2] = (int)lo.z; qa[tt][i][3] = (int)lo.w;
+      qa[tt][i][4] = (int)hi.x; qa[tt][i][5] = (int)hi.y; qa[tt][i][6] = (int)hi.z; qa[tt][i][7] = (int)hi.w;
     }
-    for (int c0 = 0; c0 < cnt; c0 += NT) {
-      int qa[NT][NL][8];
-      float dd[NT][NL];
-      int bb[NT][NL];
-      int slot[NT];
+  }
+  // block scales of the lane's kept items' tokens (zero past the list or past kb)
+  float dk[KI][NL];
 #pragma unroll
-      for (int tt = 0; tt < NT; ++tt) {
-        const bool ok = c0 + tt < cnt;
-        slot[tt] = A.slot_list[off + min(c0 + tt, cnt - 1)];
-        const int64_t tok = slot[tt] / A.topk;
-        load_acts<NL>(A.xq + tok * A.hidden, A.xd + tok * kb, A.xb + tok * kb, kb, g, cp, ok, qa[tt], dd[tt], bb[tt]);
-      }
+  for (int k = 0; k < KI; ++k) {
+    const int tt = RR::kept(k, lane) % NT;
+    int ar = arow[0];
 #pragma unroll
-      for (int r = 0; r < RPW; ++r) {
+    for (int u = 1; u < NT; ++u) ar = tt == u ? arow[u] : ar;
+    const bool tv = c0 + tt < cnt;
 #pragma unroll
-        for (int tt = 0; tt < NT; ++tt) {
-          const float gv = row_dot<NL>(wg[r], sg[r], qa[tt], dd[tt], bb[tt]);
-          const float uv = row_dot<NL>(wu[r], su[r], qa[tt], dd[tt], bb[tt]);
-          if (lane == 0 && c0 + tt < cnt && row0 + r < I) A.h[(int64_t)slot[tt] * I + row0 + r] = silu_f32(gv) * uv;
-        }
-      }
+    for (int i = 0; i < NL; ++i) {
+      const int b = 8 * i + g;
+      const uint32_t bc = (uint32_t)min(b, kb - 1);
+      const float dv = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(dr, bc * 4u, (uint32_t)ar * (uint32_t)kb * 4u, 0));
+      dk[k][i] = (tv && (!RAGGED || b < kb)) ? dv : 0.0f;
+    }
+  }
+  float acc[KI * NMAT];
+#pragma unroll
+  for (int v = 0; v < KI * NMAT; ++v) acc[v] = 0.0f;
+#pragma unroll
+  for (int i = 0; i < NL; ++i) {
+    int p[RPW * NT * NMAT];
+#pragma unroll
+    for (int r = 0; r < RPW; ++r)
+#pragma unroll
+      for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+        for (int m = 0; m < NMAT; ++m) p[(r * NT + tt) * NMAT + m] = dot32x16(wc[m * RPW + r][i], qa[tt][i]);
+    RR::block_sums(p);
+#pragma unroll
+    for (int k = 0; k < KI; ++k)
+#pragma unroll
+      for (int m = 0; m < NMAT; ++m)
+        acc[k * NMAT + m] = fmaf(sl[m][i] * dk[k][i], (float)(p[k * NMAT + m] >> 4), acc[k * NMAT + m]);
+  }
+  RR::block_totals(acc);
+  if (RR::writer(lane)) {
+    const int it = RR::item(lane), r = it / NT, tt = it % NT;
+    int sv = slot[0];
+#pragma unroll
+    for (int u = 1; u < NT; ++u) sv = tt == u ? slot[u] : sv;
+    if (row0 + r < N && c0 + tt < cnt) {
+      if constexpr (NMAT == 2) A.h[(int64_t)sv * A.inter + row0 + r] = silu_f32(acc[0]) * acc[1];
+      else A.yd[(int64_t)sv * A.hidden + row0 + r] = acc[0];
     }
   }
 }
 
-// ---------------------------------------------------------------------------------
-// down: yd[slot][row] = Wd[e] hq[slot]
-// ---------------------------------------------------------------------------------
-
-template <int NL, int NT, int RPW>
-__global__ __launch_bounds__(256) void k_moe_down(MoeArgs A) {
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+// NMAT == 2: h[slot][row] = SiLU(Wg[e] xq[token]) * (Wu[e] xq[token]);
+// NMAT == 1: yd[slot][row] = Wd[e] hq[slot].
+template <int NMAT, int NL, int RPW, int NT, int WAVES, bool RAGGED>
+__global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
+  static_assert(RPW <= 8 && (RPW & (RPW - 1)) == 0, "RPW: a power of two <= 8");
+  const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 3, cp = lane & 7;
-  const int kb = A.inter / 256, H = A.hidden;
-  const int n_tasks = A.ctrl[kTasksDn];
+  const int K = NMAT == 2 ? A.hidden : A.inter;
+  const int N = NMAT == 2 ? A.inter : A.hidden;
+  const int kb = K / 256;
+  const int tiles = NMAT == 2 ? A.tiles_gu : A.tiles_dn;
+  const int n_tasks = A.ctrl[NMAT == 2 ? kTasksGU : kTasksDn];
+  const uint32_t arows = (uint32_t)(NMAT == 2 ? A.t : A.t * A.topk);
+  const __amdgpu_buffer_rsrc_t qr = make_rsrc(NMAT == 2 ? A.xq : A.hq, arows * (uint32_t)K);
+  const __amdgpu_buffer_rsrc_t dr = make_rsrc(NMAT == 2 ? A.xd : A.hd, arows * (uint32_t)kb * 4u);
+  const int lr = rev_bits<clog2(RPW)>(lane & (RPW - 1));  // the lane's row after the block butterfly
   for (int task = blockIdx.x; task < n_tasks; task += gridDim.x) {
-    const int a = task / A.tiles_dn, tile = task - a * A.tiles_dn;
+    const int a = task / tiles, tile = task - a * tiles;
     const int64_t e = A.active[a];
     const int off = A.act_off[a], cnt = A.act_off[a + 1] - off;
-    const int row0 = (tile * 4 + wv) * RPW;
-    if (row0 >= H) continue;
-    const uint8_t* dc = A.codes[2] + e * A.stride_codes[2];
-    const uint16_t* ds = A.scales[2] + e * A.stride_scales[2];
-    uint4 w[RPW][NL];
-    float s[RPW][NL];
+    const int row0 = (tile * WAVES + wv) * RPW;
+    if (row0 >= N) continue;
+    int wc[NMAT * RPW][NL][8];
+    float sl[NMAT][NL];
+    {
+      uint4 raw[NMAT * RPW][NL];
+      uint16_t sr[NMAT][NL];
 #pragma unroll
-    for (int r = 0; r < RPW; ++r) {
-      const int64_t row = min(row0 + r, H - 1);
-      load_row<NL>(dc + row * kb * 128, ds + row * kb, kb, g, cp, row0 + r < H, w[r], s[r]);
-    }
-    for (int c0 = 0; c0 < cnt; c0 += NT) {
-      int qa[NT][NL][8];
-      float dd[NT][NL];
-      int bb[NT][NL];
-      int slot[NT];
+      for (int m = 0; m < NMAT; ++m) {
+        const int p = NMAT == 2 ? m : 2;
+        const MatRsrc mr = mat_rsrc(A.codes[p] + e * A.stride_codes[p], A.scales[p] + e * A.stride_scales[p], N, kb);
 #pragma unroll
-      for (int tt = 0; tt < NT; ++tt) {
-        const bool ok = c0 + tt < cnt;
-        slot[tt] = A.slot_list[off + min(c0 + tt, cnt - 1)];
-        const int64_t sl = slot[tt];
-        load_acts<NL>(A.hq + sl * A.inter, A.hd + sl * kb, A.hb + sl * kb, kb, g, cp, ok, qa[tt], dd[tt], bb[tt]);
-      }
+        for (int r = 0; r < RPW; ++r) {
+          const uint32_t srow = (uint32_t)min(row0 + r, N - 1) * (uint32_t)kb;
 #pragma unroll
-      for (int r = 0; r < RPW; ++r) {
-#pragma unroll
-        for (int tt = 0; tt < NT; ++tt) {
-          const float v = row_dot<NL>(w[r], s[r], qa[tt], dd[tt], bb[tt]);
-          if (lane == 0 && c0 + tt < cnt && row0 + r < H) A.yd[(int64_t)slot[tt] * H + row0 + r] = v;
+          for (int i = 0; i < NL; ++i) {
+            const uint32_t bc = (uint32_t)min(8 * i + g, kb - 1);
+            raw[m * RPW + r][i] = buf_load16(mr.codes, bc * 128u + (uint32_t)cp * 16u, srow * 128u);
+          }
         }
+        const uint32_t lrow = (uint32_t)min(row0 + lr, N - 1) * (uint32_t)kb;
+#pragma unroll
+        for (int i = 0; i < NL; ++i) sr[m][i] = buf_load_u16(mr.scales, (uint32_t)min(8 * i + g, kb - 1) * 2u, lrow * 2u);
       }
+#pragma unroll
+      for (int v = 0; v < NMAT * RPW; ++v)
+#pragma unroll
+        for (int i = 0; i < NL; ++i) unpack16c(raw[v][i], wc[v][i]);
+#pragma unroll
+      for (int m = 0; m < NMAT; ++m)
+#pragma unroll
+        for (int i = 0; i < NL; ++i) sl[m][i] = f16_bits_to_f32(sr[m][i]);
     }
+    int c0 = 0;
+    if constexpr (NT > 1)
+      for (; c0 + NT <= cnt; c0 += NT)
+        tb_tokens<NMAT, NL, RPW, NT, RAGGED>(A, wc, sl, qr, dr, K, kb, N, off, cnt, c0, row0, lane, g, cp);
+    for (; c0 < cnt; ++c0) tb_tokens<NMAT, NL, RPW, 1, RAGGED>(A, wc, sl, qr, dr, K, kb, N, off, cnt, c0, row0, lane, g, cp);
   }
 }
 
@@ -441,12 +430,12 @@ __global__ __launch_bounds__(256) void k_moe_combine(MoeArgs A, float* __restric
 // int8 GEMM, run on v_mfma_i32_16x16x64_i8. A workgroup owns one task: kMT tokens of one
 // active expert x kMN weight rows (x2 matrices for gate/up). Per 256-column block:
 //  - the token tile's codes are staged in LDS (double-buffered, rows padded to 272 bytes
-//    so the 16 lanes of an operand read hit distinct banks) with their d and bsum;
-//  - each wave unpacks its 16 weight rows' nibbles into B operands (lane: row l & 15,
+//    so the 16 lanes of an operand read hit distinct banks) with their d;
+//  - each wave unpacks its 16 weight rows' nibbles to 16c bytes as B operands (lane: row l & 15,
 //    chunk 4t + (l >> 4), half h gives MFMA (t, h); the A operand takes the same 16
 //    columns of the token's codes, so every product pairs matching columns);
-//  - four MFMAs per 16x16 output tile accumulate sum u*q from -4*bsum (u = c + 4), i.e.
-//    the exact block sum isum, and one fp32 multiply-add per output applies f32(s) * d.
+//  - four MFMAs per 16x16 output tile accumulate sum (16c)*q = 16 * isum exactly, and one
+//    fp32 multiply-add per output applies f32(s) * d to isum.
 // Tasks are ranked hottest expert first with token tiles innermost, so the workgroups
 // that read one weight tile run together and share it through L2.
 // ---------------------------------------------------------------------------------
@@ -460,26 +449,24 @@ __device__ __forceinline__ v4i lds_v4i(const int8_t* p) {
 }
 
 // One block's loads for the MFMA kernel: this thread's 64-byte quarter of a token row,
-// the token's block scale and code sum, and the lane's two 16-byte code chunks (and
-// scale) of each weight matrix.
+// the token's block scale, and the lane's two 16-byte code chunks (and scale) of each
+// weight matrix.
 template <int NMAT>
 struct MfmaStage {
   v4i a0, a1, a2, a3;
   uint4 w[NMAT][2];
   uint16_t s[NMAT];
   float d;
-  int bs;
 };
 
 template <int NMAT>
-__device__ __forceinline__ void mfma_fetch(MfmaStage<NMAT>& st, const v4i* qrow, const float* dsrc, const int32_t* bsrc,
-                                           int64_t arow, const MatRsrc (&mr)[NMAT], int wrow, int kb, int g, int b) {
+__device__ __forceinline__ void mfma_fetch(MfmaStage<NMAT>& st, const v4i* qrow, const float* dsrc, int64_t arow,
+                                           const MatRsrc (&mr)[NMAT], int wrow, int kb, int g, int b) {
   st.a0 = qrow[b * 16 + 0];
   st.a1 = qrow[b * 16 + 1];
   st.a2 = qrow[b * 16 + 2];
   st.a3 = qrow[b * 16 + 3];
   st.d = dsrc[arow * kb + b];
-  st.bs = bsrc[arow * kb + b];
 #pragma unroll
   for (int m = 0; m < NMAT; ++m) {
 #pragma unroll
@@ -493,7 +480,6 @@ template <int NMAT>  // 2: gate and up, h = SiLU(g) * u; 1: down, y per slot
 __global__ __launch_bounds__(256) void k_moe_mfma(MoeArgs A) {
   __shared__ __attribute__((aligned(16))) int8_t s_a[2][kMT * kAStride];
   __shared__ __attribute__((aligned(16))) float s_d[2][kMT];
-  __shared__ __attribute__((aligned(16))) int s_b[2][kMT];
   __shared__ int s_slot[kMT];
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int li = lane & 15, g = lane >> 4;
@@ -505,7 +491,6 @@ __global__ __launch_bounds__(256) void k_moe_mfma(MoeArgs A) {
   const int n_tasks = A.ctrl[NMAT == 2 ? kTasksMGU : kTasksMDn];
   const int8_t* qsrc = NMAT == 2 ? A.xq : A.hq;
   const float* dsrc = NMAT == 2 ? A.xd : A.hd;
-  const int32_t* bsrc = NMAT == 2 ? A.xb : A.hb;
   const int tt = threadIdx.x >> 2, part = threadIdx.x & 3;  // staging: token row, 64-byte quarter
   for (int task = blockIdx.x; task < n_tasks; task += gridDim.x) {
     // active expert a with tt_off[a] * RT <= task < tt_off[a + 1] * RT
@@ -543,7 +528,7 @@ __global__ __launch_bounds__(256) void k_moe_mfma(MoeArgs A) {
         for (int v = 0; v < 4; ++v) acc[mt][m][v] = 0.0f;
 
     MfmaStage<NMAT> st;
-    mfma_fetch<NMAT>(st, qrow, dsrc, bsrc, arow, mr, wrow, kb, g, 0);
+    mfma_fetch<NMAT>(st, qrow, dsrc, arow, mr, wrow, kb, g, 0);
     for (int b = 0; b < kb; ++b) {
       const int buf = b & 1;
       v4i* dst = reinterpret_cast<v4i*>(s_a[buf] + tt * kAStride + part * 64);
@@ -551,10 +536,7 @@ __global__ __launch_bounds__(256) void k_moe_mfma(MoeArgs A) {
       dst[1] = st.a1;
       dst[2] = st.a2;
       dst[3] = st.a3;
-      if (part == 0) {
-        s_d[buf][tt] = st.d;
-        s_b[buf][tt] = st.bs;
-      }
+      if (part == 0) s_d[buf][tt] = st.d;
       uint4 wc[NMAT][2];
       float sf[NMAT];
 #pragma unroll
@@ -563,7 +545,7 @@ __global__ __launch_bounds__(256) void k_moe_mfma(MoeArgs A) {
         wc[m][1] = st.w[m][1];
         sf[m] = f16_bits_to_f32(st.s[m]);
       }
-      if (b + 1 < kb) mfma_fetch<NMAT>(st, qrow, dsrc, bsrc, arow, mr, wrow, kb, g, b + 1);
+      if (b + 1 < kb) mfma_fetch<NMAT>(st, qrow, dsrc, arow, mr, wrow, kb, g, b + 1);
       __syncthreads();
       v4i bop[NMAT][2][2];
 #pragma unroll
@@ -571,9 +553,8 @@ __global__ __launch_bounds__(256) void k_moe_mfma(MoeArgs A) {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
           const uint4 w = wc[m][c];
-          bop[m][c][0] = v4i{int(w.x & kLowNibbles), int(w.y & kLowNibbles), int(w.z & kLowNibbles), int(w.w & kLowNibbles)};
-          bop[m][c][1] = v4i{int((w.x >> 4) & kLowNibbles), int((w.y >> 4) & kLowNibbles), int((w.z >> 4) & kLowNibbles),
-                             int((w.w >> 4) & kLowNibbles)};
+          bop[m][c][0] = v4i{lo16c(w.x), lo16c(w.y), lo16c(w.z), lo16c(w.w)};
+          bop[m][c][1] = v4i{hi16c(w.x), hi16c(w.y), hi16c(w.z), hi16c(w.w)};
         }
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt) {
@@ -583,19 +564,19 @@ __global__ __launch_bounds__(256) void k_moe_mfma(MoeArgs A) {
         for (int c = 0; c < 2; ++c)
 #pragma unroll
           for (int h = 0; h < 2; ++h) aop[c][h] = lds_v4i(arow_lds + 32 * (4 * c + g) + 16 * h);
-        const int4 bs4 = *reinterpret_cast<const int4*>(&s_b[buf][mt * 16 + 4 * g]);
         const float4 d4 = *reinterpret_cast<const float4*>(&s_d[buf][mt * 16 + 4 * g]);
 #pragma unroll
         for (int m = 0; m < NMAT; ++m) {
-          v4i C = v4i{-4 * bs4.x, -4 * bs4.y, -4 * bs4.z, -4 * bs4.w};
+          v4i C = v4i{0, 0, 0, 0};
           C = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[0][0], bop[m][0][0], C, 0, 0, 0);
           C = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[0][1], bop[m][0][1], C, 0, 0, 0);
           C = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[1][0], bop[m][1][0], C, 0, 0, 0);
           C = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[1][1], bop[m][1][1], C, 0, 0, 0);
-          acc[mt][m][0] = fmaf(sf[m] * d4.x, (float)C[0], acc[mt][m][0]);
-          acc[mt][m][1] = fmaf(sf[m] * d4.y, (float)C[1], acc[mt][m][1]);
-          acc[mt][m][2] = fmaf(sf[m] * d4.z, (float)C[2], acc[mt][m][2]);
-          acc[mt][m][3] = fmaf(sf[m] * d4.w, (float)C[3], acc[mt][m][3]);
+          // C = 16 * isum exactly (|C| < 2^21)
+          acc[mt][m][0] = fmaf(sf[m] * d4.x, (float)(C[0] >> 4), acc[mt][m][0]);
+          acc[mt][m][1] = fmaf(sf[m] * d4.y, (float)(C[1] >> 4), acc[mt][m][1]);
+          acc[mt][m][2] = fmaf(sf[m] * d4.z, (float)(C[2] >> 4), acc[mt][m][2]);
+          acc[mt][m][3] = fmaf(sf[m] * d4.w, (float)(C[3] >> 4), acc[mt][m][3]);
         }
       }
     }
@@ -630,11 +611,10 @@ constexpr int kT1MaxTopk = 8;
 constexpr int kT1MaxHq = 16384;  // topk * inter bytes of requantized hidden held in LDS
 
 // Quantize 256-block `blk` of src into LDS (one block per 8-lane group): codes, the
-// block scale and code sum, and each 32-column chunk's code sum (for the lanes that later
-// read the chunk). `store` is group-uniform; the quantization itself runs regardless, so
-// that the loads of v are not sunk into a branch behind the weight loads.
+// block scale and code sum. `store` is group-uniform; the quantization itself runs
+// regardless, so that the loads of v are not sunk into a branch behind the weight loads.
 __device__ __forceinline__ void quantize_to_lds(const float (&v)[32], int blk, int cp, int8_t* s_q, float* s_d,
-                                                int* s_b, int* s_qs, bool store) {
+                                                int* s_b, bool store) {
   int qw[8], qs, bs;
   float dd;
   quantize_group32(v, qw, qs, dd, bs);
@@ -642,7 +622,6 @@ __device__ __forceinline__ void quantize_to_lds(const float (&v)[32], int blk, i
   int4* qp = reinterpret_cast<int4*>(s_q + blk * 256 + cp * 32);
   qp[0] = make_int4(qw[0], qw[1], qw[2], qw[3]);
   qp[1] = make_int4(qw[4], qw[5], qw[6], qw[7]);
-  s_qs[blk * 8 + cp] = qs;
   if (cp == 0) {
     s_d[blk] = dd;
     s_b[blk] = bs;
@@ -662,50 +641,41 @@ __device__ __forceinline__ void load32(const float* p, float (&v)[32]) {
 }
 
 // A lane's slice of one token's quantized activations, from LDS: for load i, block
-// b = 8i + g, chunk cp: 32 codes, the chunk's code sum and the block scale. Blocks past
-// the end of the row (ragged k) read as zero.
+// b = 8i + g, chunk cp: 32 codes (blocks past the end of a row reread the last block;
+// their scale d is taken as zero).
 template <int NL>
-struct LaneActs {
-  int q[NL][8];
-  int qs[NL];
-  float d[NL];
-};
-
-template <int NL, bool RAGGED>
-__device__ __forceinline__ void lds_acts(const int8_t* s_q, const float* s_d, const int* s_qs, int kb, int g, int cp,
-                                         LaneActs<NL>& a) {
+__device__ __forceinline__ void lds_acts(const int8_t* s_q, int kb, int g, int cp, int (&q)[NL][8]) {
 #pragma unroll
   for (int i = 0; i < NL; ++i) {
-    const int b = 8 * i + g;
-    const bool v = !RAGGED || b < kb;
-    const int bc = v ? b : kb - 1;
-    const int4* p = reinterpret_cast<const int4*>(s_q + bc * 256 + cp * 32);
+    const int4* p = reinterpret_cast<const int4*>(s_q + min(8 * i + g, kb - 1) * 256 + cp * 32);
     const int4 lo = p[0], hi = p[1];
-    a.q[i][0] = v ? lo.x : 0; a.q[i][1] = v ? lo.y : 0; a.q[i][2] = v ? lo.z : 0; a.q[i][3] = v ? lo.w : 0;
-    a.q[i][4] = v ? hi.x : 0; a.q[i][5] = v ? hi.y : 0; a.q[i][6] = v ? hi.z : 0; a.q[i][7] = v ? hi.w : 0;
-    a.qs[i] = v ? s_qs[bc * 8 + cp] : 0;
-    a.d[i] = v ? s_d[bc] : 0.0f;
+    q[i][0] = lo.x; q[i][1] = lo.y; q[i][2] = lo.z; q[i][3] = lo.w;
+    q[i][4] = hi.x; q[i][5] = hi.y; q[i][6] = hi.z; q[i][7] = hi.w;
   }
 }
 
-// One row's lane slice in registers: NL 16-byte code chunks and their f16 scales.
+// Row `row` (wave-uniform) of a matrix: the lane's NL 16-byte code chunks. Chunks past
+// the row end reload the row's last block (their activations' scale is zero).
 template <int NL>
-struct LaneRow {
-  uint4 w[NL];
-  uint16_t s[NL];
-};
-
-// Row `row` (wave-uniform) of a matrix: the lane's NL chunks and their scales. Chunks past
-// the row end reload the row's last block (their activations are zero).
-template <int NL>
-__device__ __forceinline__ void load_lane_row(const MatRsrc& m, int row, int kb, int g, int cp, LaneRow<NL>& r) {
+__device__ __forceinline__ void load_lane_codes(const MatRsrc& m, int row, int kb, int g, int cp, uint4 (&w)[NL]) {
   const uint32_t srow = (uint32_t)row * (uint32_t)kb;
 #pragma unroll
-  for (int i = 0; i < NL; ++i) {
-    const uint32_t bc = (uint32_t)min(8 * i + g, kb - 1);
-    r.w[i] = buf_load16(m.codes, bc * 128u + (uint32_t)cp * 16u, srow * 128u);
-    r.s[i] = buf_load_u16(m.scales, bc * 2u, srow * 2u);
-  }
+  for (int i = 0; i < NL; ++i)
+    w[i] = buf_load16(m.codes, (uint32_t)min(8 * i + g, kb - 1) * 128u + (uint32_t)cp * 16u, srow * 128u);
+}
+
+// The lane's NL block scales of row `row` (per lane).
+template <int NL>
+__device__ __forceinline__ void load_lane_scales(const MatRsrc& m, int row, int kb, int g, uint16_t (&s)[NL]) {
+  const uint32_t srow = (uint32_t)row * (uint32_t)kb;
+#pragma unroll
+  for (int i = 0; i < NL; ++i) s[i] = buf_load_u16(m.scales, (uint32_t)min(8 * i + g, kb - 1) * 2u, srow * 2u);
+}
+
+__device__ __forceinline__ int dot_chunk16(const uint4 w, const int (&a)[8]) {
+  int c[8];
+  unpack16c(w, c);
+  return dot32x16(c, a);
 }
 
 // The lane's 32 fp32 values of 256-block `blk` of a row-major fp32 buffer.
@@ -721,19 +691,6 @@ __device__ __forceinline__ void buf_load32f(__amdgpu_buffer_rsrc_t r, uint32_t b
   }
 }
 
-// The lane's contribution to one row against one token: per load, the exact integer dot
-// of its 32 codes (sum u*q - 4*qs = sum c*q, |.| <= 16256) times f32(s) * d.
-template <int NL>
-__device__ __forceinline__ float lane_row_dot(const LaneRow<NL>& r, const LaneActs<NL>& a) {
-  float acc = 0.0f;
-#pragma unroll
-  for (int i = 0; i < NL; ++i) {
-    const int p = dot_chunk_u(r.w[i], a.q[i]) - 4 * a.qs[i];
-    acc = fmaf(f16_bits_to_f32(r.s[i]) * a.d[i], (float)p, acc);
-  }
-  return acc;
-}
-
 // WAVES waves per workgroup; each wave owns RPW rows (a power of two) of gate and of up
 // of one slot. After the lane partials, one butterfly leaves row r's (g, u) in the lanes
 // whose low bits, reversed, spell r.
@@ -743,7 +700,6 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_gateup(const float* __restric
   __shared__ __attribute__((aligned(16))) int8_t s_q[kMaxK];
   __shared__ float s_d[kMaxK / 256];
   __shared__ int s_b[kMaxK / 256];
-  __shared__ int s_qs[kMaxK / 32];
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 3, cp = lane & 7, gid = wv * 8 + g;
   const int kb = A.hidden / 256, I = A.inter;
@@ -760,17 +716,22 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_gateup(const float* __restric
   __builtin_amdgcn_sched_barrier(0);
   const MatRsrc mr[2] = {mat_rsrc(A.codes[0] + ec * A.stride_codes[0], A.scales[0] + ec * A.stride_scales[0], I, kb),
                          mat_rsrc(A.codes[1] + ec * A.stride_codes[1], A.scales[1] + ec * A.stride_scales[1], I, kb)};
-  LaneRow<NL> wr[2 * RPW];  // [2r] gate row r, [2r + 1] up row r
+  uint4 wr[2 * RPW][NL];  // [2r] gate row r, [2r + 1] up row r
 #pragma unroll
   for (int r = 0; r < RPW; ++r) {
     const int row = min(row0 + r, I - 1);
 #pragma unroll
-    for (int m = 0; m < 2; ++m) load_lane_row<NL>(mr[m], row, kb, g, cp, wr[2 * r + m]);
+    for (int m = 0; m < 2; ++m) load_lane_codes<NL>(mr[m], row, kb, g, cp, wr[2 * r + m]);
   }
-  quantize_to_lds(v, min(gid, kb - 1), cp, s_q, s_d, s_b, s_qs, gid < kb);
+  // after the block butterfly a lane keeps the row rev(lane bits): its scales
+  uint16_t sr[2][NL];
+  const int lrow = min(row0 + rev_bits<clog2(RPW)>(lane & (RPW - 1)), I - 1);
+#pragma unroll
+  for (int m = 0; m < 2; ++m) load_lane_scales<NL>(mr[m], lrow, kb, g, sr[m]);
+  quantize_to_lds(v, min(gid, kb - 1), cp, s_q, s_d, s_b, gid < kb);
   for (int blk = gid + WAVES * 8; blk < kb; blk += WAVES * 8) {
     buf_load32f(xr, (uint32_t)blk, cp, v);
-    quantize_to_lds(v, blk, cp, s_q, s_d, s_b, s_qs, true);
+    quantize_to_lds(v, blk, cp, s_q, s_d, s_b, true);
   }
   __syncthreads();
   if (blockIdx.x == 0) {  // stage buffers and the status word, once per call
@@ -787,28 +748,24 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_gateup(const float* __restric
     }
   }
   if (!valid || row0 >= I) return;
-  LaneActs<NL> act;
-  lds_acts<NL, RAGGED>(s_q, s_d, s_qs, kb, g, cp, act);
-  float val[2 * RPW];
+  int qa[NL][8];
+  lds_acts<NL>(s_q, kb, g, cp, qa);
+  using RR = RowReduce<RPW, 2>;
+  float acc[2] = {0.0f, 0.0f};
 #pragma unroll
-  for (int m = 0; m < 2 * RPW; ++m) val[m] = lane_row_dot<NL>(wr[m], act);
-  // butterfly over the row index, then plain sums over the remaining lane bits
-  if constexpr (RPW >= 2) bfly_step<2 * RPW, 1>(val);
-  if constexpr (RPW >= 4) bfly_step<RPW, 2>(val);
-  if constexpr (RPW >= 8) bfly_step<RPW / 2, 4>(val);
+  for (int i = 0; i < NL; ++i) {
+    const int b = 8 * i + g;
+    const float dv = (!RAGGED || b < kb) ? s_d[min(b, kb - 1)] : 0.0f;
+    int p[2 * RPW];
 #pragma unroll
-  for (int m = 0; m < 2; ++m) {
-    float t = val[m];
-    if constexpr (RPW < 2) t = xor_sum<1>(t);
-    if constexpr (RPW < 4) t = xor_sum<2>(t);
-    if constexpr (RPW < 8) t = xor_sum<4>(t);
-    t = xor_sum<32>(xor_sum<16>(xor_sum<8>(t)));
-    val[m] = t;
+    for (int v = 0; v < 2 * RPW; ++v) p[v] = dot_chunk16(wr[v][i], qa[i]);
+    RR::block_sums(p);
+#pragma unroll
+    for (int m = 0; m < 2; ++m) acc[m] = fmaf(f16_bits_to_f32(sr[m][i]) * dv, (float)(p[m] >> 4), acc[m]);
   }
-  // lane bits (0, 1, 2) reversed give the row this lane holds
-  const int rb = RPW == 1 ? 0 : (RPW == 2 ? (lane & 1) : (RPW == 4 ? ((lane & 1) << 1) | ((lane >> 1) & 1)
-                                                                    : ((lane & 1) << 2) | (lane & 2) | ((lane >> 2) & 1)));
-  if (lane < RPW && row0 + rb < I) A.h[(int64_t)j * I + row0 + rb] = silu_f32(val[0]) * val[1];
+  RR::block_totals(acc);
+  const int r = RR::item(lane);
+  if (RR::writer(lane) && row0 + r < I) A.h[(int64_t)j * I + row0 + r] = silu_f32(acc[0]) * acc[1];
 }
 
 // WAVES waves per workgroup; each wave owns RPW rows of down for every slot. Values
@@ -817,12 +774,11 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_gateup(const float* __restric
 // out = sum_j w_j * y_j in ascending j.
 template <int NL, int RPW, int TOPK, int WAVES, bool RAGGED>
 __global__ __launch_bounds__(WAVES * 64) void k_t1_down(MoeArgs A, float* __restrict__ out) {
-  constexpr int V = TOPK * RPW <= 2 ? 2 : (TOPK * RPW <= 4 ? 4 : (TOPK * RPW <= 8 ? 8 : (TOPK * RPW <= 16 ? 16 : 32)));
-  static_assert(TOPK * RPW <= 32 && (RPW & (RPW - 1)) == 0, "down tile too large");
+  constexpr int V = 1 << clog2(2 * TOPK * RPW - 1);  // items slot * RPW + row, padded to a power of two
+  static_assert(V <= 32 && (RPW & (RPW - 1)) == 0, "down tile too large");
   __shared__ __attribute__((aligned(16))) int8_t s_hq[kT1MaxHq];
   __shared__ float s_hd[kT1MaxHq / 256];
   __shared__ int s_hb[kT1MaxHq / 256];
-  __shared__ int s_qs[kT1MaxHq / 32];
   __shared__ float s_y[WAVES][32];
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 3, cp = lane & 7, gid = wv * 8 + g;
@@ -846,18 +802,35 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_down(MoeArgs A, float* __rest
   float v[32];
   buf_load32f(hr, (uint32_t)(q0 ? blk0 : 0), cp, v);
   __builtin_amdgcn_sched_barrier(0);
-  LaneRow<NL> wr[TOPK][RPW];
+  uint4 wr[TOPK][RPW][NL];
 #pragma unroll
   for (int j = 0; j < TOPK; ++j) {
     const MatRsrc mr = mat_rsrc(A.codes[2] + ej[j] * A.stride_codes[2], A.scales[2] + ej[j] * A.stride_scales[2], H, kb);
 #pragma unroll
-    for (int r = 0; r < RPW; ++r) load_lane_row<NL>(mr, min(row0 + r, H - 1), kb, g, cp, wr[j][r]);
+    for (int r = 0; r < RPW; ++r) load_lane_codes<NL>(mr, min(row0 + r, H - 1), kb, g, cp, wr[j][r]);
   }
-  quantize_to_lds(v, blk0, cp, s_hq, s_hd, s_hb, s_qs, q0);
+  // after the block butterfly a lane keeps KI items (slot jk, row rk): their scales
+  using RR = RowReduce<V, 1>;
+  constexpr int KI = RR::KI;
+  int jk[KI];
+  uint16_t sr[KI][NL];
+#pragma unroll
+  for (int k = 0; k < KI; ++k) {
+    const int it = RR::kept(k, lane);
+    jk[k] = it / RPW;
+    int64_t e = ej[0];
+#pragma unroll
+    for (int jj = 1; jj < TOPK; ++jj) e = jk[k] == jj ? ej[jj] : e;
+    const int row = min(row0 + it % RPW, H - 1);
+    const uint16_t* sp = A.scales[2] + e * A.stride_scales[2] + (int64_t)row * kb;
+#pragma unroll
+    for (int i = 0; i < NL; ++i) sr[k][i] = sp[min(8 * i + g, kb - 1)];
+  }
+  quantize_to_lds(v, blk0, cp, s_hq, s_hd, s_hb, q0);
   for (int blk = gid + WAVES * 8; blk < nblk; blk += WAVES * 8) {
     if (!((vmask >> (blk / kb)) & 1)) continue;
     buf_load32f(hr, (uint32_t)blk, cp, v);
-    quantize_to_lds(v, blk, cp, s_hq, s_hd, s_hb, s_qs, true);
+    quantize_to_lds(v, blk, cp, s_hq, s_hd, s_hb, true);
   }
   __syncthreads();
   if (blockIdx.x == 0) {  // stage buffers, once per call
@@ -870,31 +843,34 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_down(MoeArgs A, float* __rest
       }
   }
   if (row0 >= H) return;
-  float val[V];
+  float acc[KI];
 #pragma unroll
-  for (int m = 0; m < V; ++m) val[m] = 0.0f;
+  for (int k = 0; k < KI; ++k) acc[k] = 0.0f;
 #pragma unroll
-  for (int j = 0; j < TOPK; ++j) {
-    LaneActs<NL> act;
-    lds_acts<NL, RAGGED>(s_hq + j * I, s_hd + j * kb, s_qs + j * kb * 8, kb, g, cp, act);
+  for (int i = 0; i < NL; ++i) {
+    const int b = 8 * i + g;
+    int p[V];
 #pragma unroll
-    for (int r = 0; r < RPW; ++r) val[j * RPW + r] = lane_row_dot<NL>(wr[j][r], act);
+    for (int v = TOPK * RPW; v < V; ++v) p[v] = 0;
+#pragma unroll
+    for (int j = 0; j < TOPK; ++j) {
+      const int4* qp = reinterpret_cast<const int4*>(s_hq + j * I + min(b, kb - 1) * 256 + cp * 32);
+      const int4 lo = qp[0], hi = qp[1];
+      const int qa[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+#pragma unroll
+      for (int r = 0; r < RPW; ++r) p[j * RPW + r] = dot_chunk16(wr[j][r][i], qa);
+    }
+    RR::block_sums(p);
+#pragma unroll
+    for (int k = 0; k < KI; ++k) {
+      // padded items and unrouted slots: d = 0 (their LDS codes are never written)
+      const bool ok = jk[k] < TOPK && ((vmask >> jk[k]) & 1) && (!RAGGED || b < kb);
+      const float dv = ok ? s_hd[min(jk[k], TOPK - 1) * kb + min(b, kb - 1)] : 0.0f;
+      acc[k] = fmaf(f16_bits_to_f32(sr[k][i]) * dv, (float)(p[k] >> 4), acc[k]);
+    }
   }
-  bfly_step<V, 1>(val);
-  if constexpr (V >= 4) bfly_step<V / 2, 2>(val);
-  if constexpr (V >= 8) bfly_step<V / 4, 4>(val);
-  if constexpr (V >= 16) bfly_step<V / 8, 8>(val);
-  if constexpr (V >= 32) bfly_step<V / 16, 16>(val);
-  float t = val[0];
-  if constexpr (V < 4) t = xor_sum<2>(t);
-  if constexpr (V < 8) t = xor_sum<4>(t);
-  if constexpr (V < 16) t = xor_sum<8>(t);
-  if constexpr (V < 32) t = xor_sum<16>(t);
-  t = xor_sum<32>(t);
-  // lane l holds value m = bit-reverse of its low log2(V) bits
-  constexpr int LB = V == 2 ? 1 : (V == 4 ? 2 : (V == 8 ? 3 : (V == 16 ? 4 : 5)));
-  const int m = (int)(__builtin_bitreverse32((unsigned)lane) >> (32 - LB));
-  if (lane < V) s_y[wv][m] = t;
+  RR::block_totals(acc);
+  if (RR::writer(lane)) s_y[wv][RR::item(lane)] = acc[0];
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -917,42 +893,39 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_down(MoeArgs A, float* __rest
 
 using moe_fn = void (*)(MoeArgs);
 
-template <int NL, int RPW>
-static moe_fn pick_gu_nt(int nt) {
-  return nt == 1 ? k_moe_gateup<NL, 1, RPW> : k_moe_gateup<NL, 4, RPW>;
-}
-template <int NL, int RPW>
-static moe_fn pick_dn_nt(int nt) {
-  return nt == 1 ? k_moe_down<NL, 1, RPW> : k_moe_down<NL, 4, RPW>;
+// Grouped-decode tiles: each wave holds about 16 unpacked chunks per lane
+// (NMAT * RPW * NL), tokens in pairs (gate/up) or fours (down).
+constexpr int kTbWaves = 4;
+static int tb_rpw(int nmat, int nl) {
+  if (nmat == 2) return nl == 1 ? 8 : (nl == 2 ? 4 : (nl <= 4 ? 2 : 1));
+  return nl <= 2 ? 8 : (nl <= 4 ? 4 : 2);
 }
 
-// gate/up: RPW = 4 (NL <= 2), 2 (NL <= 4), 1 otherwise; down: twice that (one matrix).
-static int rpw_gu(int nl) { return nl <= 2 ? 4 : (nl <= 4 ? 2 : 1); }
-static int rpw_dn(int nl) { return nl == 1 ? 8 : (nl <= 2 ? 4 : (nl <= 4 ? 2 : 1)); }
+template <int NMAT, int NL, bool R>
+static moe_fn pick_tb_nl() {
+  constexpr int RPW = NMAT == 2 ? (NL == 1 ? 8 : (NL == 2 ? 4 : (NL <= 4 ? 2 : 1))) : (NL <= 2 ? 8 : (NL <= 4 ? 4 : 2));
+  constexpr int NT = NMAT == 2 ? 2 : 4;
+  return k_tb<NMAT, NL, RPW, NT, kTbWaves, R>;
+}
 
-static moe_fn pick_gateup(int nl, int nt) {
+template <int NMAT, bool R>
+static moe_fn pick_tb_r(int nl) {
   switch (nl) {
-    case 1: return pick_gu_nt<1, 4>(nt);
-    case 2: return pick_gu_nt<2, 4>(nt);
-    case 3: return pick_gu_nt<3, 2>(nt);
-    case 4: return pick_gu_nt<4, 2>(nt);
-    case 5: return pick_gu_nt<5, 1>(nt);
-    case 6: return pick_gu_nt<6, 1>(nt);
-    case 7: return pick_gu_nt<7, 1>(nt);
-    default: return pick_gu_nt<8, 1>(nt);
+    case 1: return pick_tb_nl<NMAT, 1, R>();
+    case 2: return pick_tb_nl<NMAT, 2, R>();
+    case 3: return pick_tb_nl<NMAT, 3, R>();
+    case 4: return pick_tb_nl<NMAT, 4, R>();
+    case 5: return pick_tb_nl<NMAT, 5, R>();
+    case 6: return pick_tb_nl<NMAT, 6, R>();
+    case 7: return pick_tb_nl<NMAT, 7, R>();
+    default: return pick_tb_nl<NMAT, 8, R>();
   }
 }
-static moe_fn pick_down(int nl, int nt) {
-  switch (nl) {
-    case 1: return pick_dn_nt<1, 8>(nt);
-    case 2: return pick_dn_nt<2, 4>(nt);
-    case 3: return pick_dn_nt<3, 2>(nt);
-    case 4: return pick_dn_nt<4, 2>(nt);
-    case 5: return pick_dn_nt<5, 1>(nt);
-    case 6: return pick_dn_nt<6, 1>(nt);
-    case 7: return pick_dn_nt<7, 1>(nt);
-    default: return pick_dn_nt<8, 1>(nt);
-  }
+
+template <int NMAT>
+static moe_fn pick_tb(int kb) {
+  const int nl = (kb + 7) / 8;
+  return kb % 8 == 0 ? pick_tb_r<NMAT, false>(nl) : pick_tb_r<NMAT, true>(nl);
 }
 
 // Tile shapes of the single-token path (measured on MI355X; overridable at build time).
@@ -1128,9 +1101,9 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   A.yd = reinterpret_cast<float*>(base + L.yd);
 
   const int nl_gu = (ex->hidden / 256 + 7) / 8, nl_dn = (ex->inter / 256 + 7) / 8;
-  const int nt = t == 1 ? 1 : 4;
-  A.tiles_gu = (ex->inter + 4 * rpw_gu(nl_gu) - 1) / (4 * rpw_gu(nl_gu));
-  A.tiles_dn = (ex->hidden + 4 * rpw_dn(nl_dn) - 1) / (4 * rpw_dn(nl_dn));
+  const int tr_gu = kTbWaves * tb_rpw(2, nl_gu), tr_dn = kTbWaves * tb_rpw(1, nl_dn);
+  A.tiles_gu = (ex->inter + tr_gu - 1) / tr_gu;
+  A.tiles_dn = (ex->hidden + tr_dn - 1) / tr_dn;
   const int64_t S = t * topk;
   const int64_t max_active = std::min<int64_t>(S, ex->n_experts);
   const int64_t cap = 256 * 16;  // workgroups per launch; the rest are strided over them
@@ -1159,7 +1132,10 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   }
   // per-expert contraction on MFMA for prefill-sized groups (or when forced), VALU dot4
   // otherwise
-  const bool mfma = (flags & TQ_MOE_FORCE_MFMA) || (!(flags & TQ_MOE_FORCE_VALU) && S >= kMfmaMinSlots);
+  // (the VALU kernels address activations with 32-bit buffer offsets)
+  const bool valu_fits = S * std::max(ex->hidden, ex->inter) < ((int64_t)1 << 31);
+  const bool mfma = (flags & TQ_MOE_FORCE_MFMA) || (!(flags & TQ_MOE_FORCE_VALU) && (S >= kMfmaMinSlots || !valu_fits));
+  if (!mfma && !valu_fits) return fail(TQ_ERR_INVALID, "%s: t * topk = %lld slots too many for the VALU path", fn, (long long)S);
   A.tiles_mgu = (ex->inter + kMN - 1) / kMN;
   A.tiles_mdn = (ex->hidden + kMN - 1) / kMN;
   const int64_t max_tiles = S / kMT + max_active;
@@ -1167,13 +1143,13 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   const unsigned g_mdn = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mdn, cap);
   if ((st = launch_stage(events, 0, k_moe_prologue, dim3(nq + 1), 256, stm, fn, x, A, nq)) != TQ_OK) return st;
   if (mfma) st = launch_stage(events, 1, k_moe_mfma<2>, dim3(g_mgu), 256, stm, fn, A);
-  else st = launch_stage(events, 1, pick_gateup(nl_gu, nt), dim3(g_gu), 256, stm, fn, A);
+  else st = launch_stage(events, 1, pick_tb<2>(ex->hidden / 256), dim3(g_gu), kTbWaves * 64, stm, fn, A);
   if (st != TQ_OK) return st;
   if ((st = launch_stage(events, 2, k_moe_requant, dim3((unsigned)((hblocks + 31) / 32)), 256, stm, fn, A, hblocks)) !=
       TQ_OK)
     return st;
   if (mfma) st = launch_stage(events, 3, k_moe_mfma<1>, dim3(g_mdn), 256, stm, fn, A);
-  else st = launch_stage(events, 3, pick_down(nl_dn, nt), dim3(g_dn), 256, stm, fn, A);
+  else st = launch_stage(events, 3, pick_tb<1>(ex->inter / 256), dim3(g_dn), kTbWaves * 64, stm, fn, A);
   if (st != TQ_OK) return st;
   const int64_t nout = t * (ex->hidden / 4);
   if ((st = launch_stage(events, 4, k_moe_combine, dim3((unsigned)((nout + 255) / 256)), 256, stm, fn, A, out)) != TQ_OK)

@@ -33,8 +33,8 @@ extern "C" tq_status tq_fold_pack_host(const int8_t* t1, const int8_t* t2, int32
           const int a1 = t1[lo], a2 = t2[lo], b1 = t1[hi], b2 = t2[hi];
           if (a1 < -1 || a1 > 1 || a2 < -1 || a2 > 1 || b1 < -1 || b1 > 1 || b2 < -1 || b2 > 1)
             return fail(TQ_ERR_INVALID, "tq_fold_pack_host: trit out of range near element %lld", (long long)lo);
-          const int ulo = 3 * a1 + a2 + 4, uhi = 3 * b1 + b2 + 4;
-          blk[16 * j + i] = (uint8_t)(ulo | (uhi << 4));
+          const int clo = 3 * a1 + a2, chi = 3 * b1 + b2;  // 4-bit two's complement nibbles
+          blk[16 * j + i] = (uint8_t)((clo & 0xF) | ((chi & 0xF) << 4));
         }
     }
   return TQ_OK;
@@ -54,11 +54,13 @@ extern "C" tq_status tq_unpack_host(const uint8_t* codes, int32_t n, int32_t k, 
       const uint8_t* blk = codes + (r * kb + b) * 128;
       for (int j = 0; j < 8; ++j)
         for (int i = 0; i < 16; ++i) {
-          const int ulo = blk[16 * j + i] & 0xF, uhi = blk[16 * j + i] >> 4;
-          if (ulo > 8 || uhi > 8)
-            return fail(TQ_ERR_INVALID, "tq_unpack_host: nibble > 8 in block (%lld, %lld)", (long long)r, (long long)b);
-          c_out[col0 + 32 * j + i] = (int8_t)(ulo - 4);
-          c_out[col0 + 32 * j + 16 + i] = (int8_t)(uhi - 4);
+          const int nlo = blk[16 * j + i] & 0xF, nhi = blk[16 * j + i] >> 4;
+          const int clo = nlo >= 8 ? nlo - 16 : nlo, chi = nhi >= 8 ? nhi - 16 : nhi;
+          if (clo < -4 || clo > 4 || chi < -4 || chi > 4)
+            return fail(TQ_ERR_INVALID, "tq_unpack_host: nibble outside -4..4 in block (%lld, %lld)", (long long)r,
+                        (long long)b);
+          c_out[col0 + 32 * j + i] = (int8_t)clo;
+          c_out[col0 + 32 * j + 16 + i] = (int8_t)chi;
         }
     }
   return TQ_OK;

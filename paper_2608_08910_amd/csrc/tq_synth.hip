@@ -15,13 +15,13 @@ __device__ __forceinline__ uint64_t splitmix64(uint64_t key, uint64_t i) {
   return z ^ (z >> 31);
 }
 
-// Unsigned nibble u = c + 4 of one element from its word: t1 from field (0 or 2), t2
-// from the next field; a 16-bit field f maps to the trit ((f * 3) >> 16) - 1.
+// Nibble c & 15 of one element from its word: t1 from field (0 or 2), t2 from the next
+// field; a 16-bit field f maps to the trit ((f * 3) >> 16) - 1.
 __device__ __forceinline__ uint32_t nibble_of(uint64_t word, int odd) {
   const uint32_t half = (uint32_t)(word >> (odd ? 32 : 0));
   const int a = (int)(((half & 0xFFFFu) * 3u) >> 16) - 1;
   const int b = (int)(((half >> 16) * 3u) >> 16) - 1;
-  return (uint32_t)(3 * a + b + 4);
+  return (uint32_t)(3 * a + b) & 0xFu;
 }
 
 // One thread per 16-byte chunk (32 weights), grid-stride over all chunks.

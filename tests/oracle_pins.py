@@ -254,7 +254,7 @@ def block_sums_equal_trit_plane_identity(o):
         sl = slice(b * 256, (b + 1) * 256)
         ref = 3 * (q[:, sl].astype(np.int64) @ t1[:, sl].T.astype(np.int64)) + q[:, sl].astype(np.int64) @ t2[:, sl].T.astype(np.int64)
         assert np.array_equal(isum[:, :, b], ref)
-    # offset form used by unsigned nibble codes u = c + 4: sum u*q - 4*sum q
+    # offset form of the same sum: with u = c + 4, sum u*q - 4*sum q
     u = c.astype(np.int64) + 4
     for b in range(k // 256):
         sl = slice(b * 256, (b + 1) * 256)

@@ -43,7 +43,7 @@ def test_format_size_is_paper_bits_per_weight():
 
 def test_pack_layout_bytes_hand_built():
     # one row, one block: column i holds code c_i; byte 16j+i must be
-    # (c[32j+i]+4) | (c[32j+16+i]+4) << 4
+    # (c[32j+i] & 15) | (c[32j+16+i] & 15) << 4 (4-bit two's complement nibbles)
     cols = np.arange(256)
     c = ((cols * 7) % 9 - 4).astype(np.int8)
     t1 = np.floor_divide(c.astype(int) + 4, 3) - 1
@@ -51,8 +51,15 @@ def test_pack_layout_bytes_hand_built():
     codes = tq.tq_fold_pack_host(t1.astype(np.int8)[None], t2.astype(np.int8)[None])
     for j in range(8):
         for i in range(16):
-            want = (int(c[32 * j + i]) + 4) | ((int(c[32 * j + 16 + i]) + 4) << 4)
+            want = (int(c[32 * j + i]) & 15) | ((int(c[32 * j + 16 + i]) & 15) << 4)
             assert codes[0, 0, 16 * j + i] == want
+    # masking a byte's high nibble, or moving its low nibble up, gives 16c as int8
+    b = codes[0, 0].astype(np.uint8)
+    for j in range(8):
+        hi16 = (b[16 * j:16 * j + 16] & 0xF0).view(np.int8).astype(int)
+        lo16 = ((b[16 * j:16 * j + 16] << 4) & 0xF0).astype(np.uint8).view(np.int8).astype(int)
+        assert np.array_equal(lo16, 16 * c[32 * j:32 * j + 16].astype(int))
+        assert np.array_equal(hi16, 16 * c[32 * j + 16:32 * j + 32].astype(int))
 
 
 def test_fold_pack_unpack_matches_oracle_fold(oracle):
@@ -63,7 +70,8 @@ def test_fold_pack_unpack_matches_oracle_fold(oracle):
         codes = tq.tq_fold_pack_host(t1, t2)
         assert codes.shape == (n, k // 256, 128)
         assert np.array_equal(tq.tq_unpack_host(codes, n, k), oracle.fold(t1, t2))
-        assert ((codes & 0xF) <= 8).all() and ((codes >> 4) <= 8).all()
+        for nib in (codes & 0xF, codes >> 4):  # nibbles of -4..4 only: 0..4, 12..15
+            assert ((nib <= 4) | (nib >= 12)).all()
 
 
 def test_fold_pack_rejects_bad_trits_and_unpack_bad_nibbles():
@@ -73,9 +81,14 @@ def test_fold_pack_rejects_bad_trits_and_unpack_bad_nibbles():
         tq.tq_fold_pack_host(bad, t)
     assert e.value.status == tq.TQ_ERR_INVALID and "trit" in str(e.value)
     codes = tq.tq_fold_pack_host(t, t)
-    codes[0, 0, 5] = 0x94  # high nibble 9
-    with pytest.raises(tq.TqError):
-        tq.tq_unpack_host(codes, 1, 256)
+    for bad_byte in (0x54, 0x0B, 0x84, 0x07):  # a nibble of 5, 11, 8 or 7: no code
+        c2 = codes.copy()
+        c2[0, 0, 5] = bad_byte
+        with pytest.raises(tq.TqError):
+            tq.tq_unpack_host(c2, 1, 256)
+    c2 = codes.copy()
+    c2[0, 0, 5] = 0xC4  # -4 and 4: valid
+    assert tq.tq_unpack_host(c2, 1, 256)[0, 5] == 4 and tq.tq_unpack_host(c2, 1, 256)[0, 21] == -4
 
 
 FAKE = 0x7F0000000000  # 256-byte aligned, never dereferenced: every call below is invalid

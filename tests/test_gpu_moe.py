@@ -215,3 +215,36 @@ def test_moe_mfma_forced_batch32(tq, oracle, experts_h4096):
     out, ws = run_moe(tq, experts_h4096, x, idx, w, flags=tq.TQ_MOE_FORCE_MFMA)
     get = oracle_pkg.expert_getter(gen.SEED, 0, c["hidden"], c["inter"], oracle)
     check_moe(tq, oracle, experts_h4096, get, x, idx, w, out, ws, list(range(c["tokens"])))
+
+
+@pytest.mark.parametrize("E,H,I,topk", [(4, 512, 768, 3), (3, 7168, 2048, 2), (9, 2304, 1280, 8), (2, 256, 256, 1),
+                                        (5, 4096, 4096, 4)])
+def test_moe_single_token_shapes(tq, oracle, E, H, I, topk):
+    """The single-token path (gate/up, then down with the requant and combine fused) at
+    block counts of 1 to 28 per row: ragged last loads, every slot count up to 8, a
+    duplicated expert."""
+    ex, logical = host_experts(tq, oracle, E, H, I, seed=31 + topk)
+    rng = np.random.default_rng(32 + topk)
+    x = (rng.standard_normal((1, H)) * 3).astype(np.float32)
+    idx = rng.choice(E, topk, replace=False).astype(np.int32)[None, :]
+    if topk >= 3:
+        idx[0, 2] = idx[0, 0]
+    w = rng.uniform(0.1, 1.0, (1, topk)).astype(np.float32)
+    announce(f"moe t=1 E={E} H={H} I={I} topk={topk}")
+    out, ws = run_moe(tq, ex, x, idx, w)
+    check_moe(tq, oracle, ex, lambda e: logical[e], x, idx, w, out, ws, [0])
+    assert tq.tq_moe_status(ws, ex, 1, topk) == 0
+
+
+@pytest.mark.parametrize("E,H,I,T,topk", [(3, 1024, 512, 40, 2), (4, 7168, 512, 9, 3)])
+def test_moe_grouped_valu_long_lists(tq, oracle, E, H, I, T, topk):
+    """The grouped VALU path with many tokens per expert (several token chunks plus a
+    remainder) and a ragged 28-block hidden size."""
+    ex, logical = host_experts(tq, oracle, E, H, I, seed=41)
+    rng = np.random.default_rng(42)
+    x = rng.standard_normal((T, H)).astype(np.float32)
+    idx = np.stack([rng.choice(E, topk, replace=False) for _ in range(T)]).astype(np.int32)
+    w = rng.uniform(0.1, 1.0, (T, topk)).astype(np.float32)
+    announce(f"moe valu E={E} H={H} I={I} T={T}")
+    out, ws = run_moe(tq, ex, x, idx, w, flags=tq.TQ_MOE_FORCE_VALU)
+    check_moe(tq, oracle, ex, lambda e: logical[e], x, idx, w, out, ws, list(range(T)))
