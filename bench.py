@@ -1,25 +1,34 @@
 """Benchmark of the tied-trit-plane expert dot pass on one MI355X.
 
-Workload (one step = one pass of the whole hot path): one routed-expert MoE layer at
-decode, batch 1 -- 256 experts resident in HBM (hidden 4096, expert intermediate 2048,
-gate/up/down in the folded 4.0625 bit/weight format, 3.27 GB), one token, top-8 experts
-uniform without replacement with softmax weights: quantize x, dispatch, gate/up dot pass
-with SiLU(gate)*up, requantize, down dot pass, weighted combine.
+Default workload (one step = one pass of the whole hot path): one routed-expert MoE
+layer at decode, batch 1 -- 256 experts resident in HBM (hidden 4096, expert
+intermediate 2048, gate/up/down in the folded 4.0625 bit/weight format, 3.27 GB), one
+token, top-8 experts uniform without replacement with softmax weights: quantize x,
+dispatch, gate/up dot pass with SiLU(gate)*up, requantize, down dot pass, weighted
+combine.
 
-Every step routes to experts not used in the previous 3 steps (a reuse distance above
-the 256 MB last-level cache), each with its own token; all inputs are resident in HBM
-before timing. Steps are captured in HIP graphs (W warmup steps, then exactly K timed
-steps) and timed by wall clock between device synchronizations.
+Other workloads (--workload): `decode32` (32 tokens, Zipf top-8), `prefill2048` (2048
+tokens, Zipf top-8, per-token log-uniform factors; the expert contraction runs on int8
+MFMA), `stack43` (a decode step through 43 such layers at hidden 7168, 8 tokens,
+Zipf top-8: 246 GB of experts resident), `gemv` (the single 2048 x 4096 matrix, one
+token: quantize + dot pass).
 
-`value` = algorithmic bytes moved per step (the routed experts' codes and scales, x in,
-out) x K / time, in GB/s; `tokens_per_s` = tokens x K / time.
+Cache hygiene: every step touches bytes that cannot still sit in the 256 MB last-level
+cache. Batch-1 steps route to experts not used in the previous 3 steps (reuse distance
+above the cache); the larger steps move 1-37 GB each; the GEMV rotates over 128
+distinct copies of its matrix (545 MB). All inputs are resident in HBM before timing.
+Steps are captured in HIP graphs (W warmup steps, then exactly K timed steps) and
+timed by wall clock between device synchronizations.
 
-The roofline object covers the dominant kernel (gate_up): its algorithmic bytes per
-launch divided by its mean duration, measured here with HIP events recorded on the
-launch stream around that kernel over a second run of the same steps.
+`value` = algorithmic bytes moved per step (the routed experts' codes and scales, or
+the matrix; activations in, outputs out) x K / time, in GB/s.
 
-The CPU baseline times the oracle (single-threaded C) on a bounded sample of the same
-layer on this host.
+The roofline object covers the dominant kernel: its algorithmic bytes (or int8 ops, on
+the MFMA path) per launch divided by its mean duration, measured here with HIP events
+recorded on the launch stream around that kernel over a second run of the same steps.
+
+The CPU baseline (default workload only) times the oracle (single-threaded C) on a
+bounded sample of the same layer on this host.
 """
 from __future__ import annotations
 
@@ -36,6 +45,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "achieved HBM GB/s (% of peak) for tq expert GEMV; MoE-layer tokens/sec"
 HBM_PEAK_GBS = 8000.0
+MFMA_I8_PEAK_TOPS = 5000.0
 
 
 def recorded_traffic(kernel: str):
@@ -98,14 +108,191 @@ def cpu_baseline(seed: int, hidden: int, inter: int, topk: int, target_s: float 
     }
 
 
-# Benchmarkable workloads: the default is the layer the metric is quoted on (one MoE
-# layer at decode, batch 1); the others time the batched-decode and prefill layers.
 WORKLOADS = {
     "decode1": dict(cfg=1, steps=2000, warmup=200, profile=256),
     "decode32": dict(cfg=2, steps=300, warmup=30, profile=64),
     "prefill2048": dict(cfg=3, steps=10, warmup=2, profile=4),
+    "stack43": dict(cfg=4, steps=20, warmup=3, profile=2),
+    "gemv": dict(cfg=0, steps=4000, warmup=400, profile=512),
 }
-MFMA_I8_PEAK_TOPS = 5000.0
+
+
+def time_graph(step, W: int, K: int) -> float:
+    """Capture W warmup and K timed steps in two HIP graphs; replay the warmup graph,
+    then time the K-step graph between device synchronizations (seconds)."""
+    import torch
+    for i in range(min(W, 4)):  # eager sanity pass (also loads the code objects)
+        step(i)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g_warm, g_time = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g_warm, stream=s):
+            for i in range(W):
+                step(i)
+        with torch.cuda.graph(g_time, stream=s):
+            for i in range(W, W + K):
+                step(i)
+    torch.cuda.synchronize()
+    g_warm.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    g_time.replay()
+    torch.cuda.synchronize()
+    return time.perf_counter() - t0
+
+
+def hbm_roof(kernel, nbytes, ms, symbol):
+    achieved = nbytes / (ms * 1e-3) / 1e9
+    return {"kernel": kernel, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": recorded_traffic(symbol),
+            "bytes_per_launch": round(nbytes), "mean_ms": round(ms, 5), "kernel_symbol": symbol}
+
+
+def run_gemv(args, wl, cfg):
+    import torch
+    from paper_2608_08910_amd import tq
+    from synth import gen
+
+    n, k, seed = cfg["n"], cfg["k"], gen.SEED
+    K = args.steps if args.steps is not None else wl["steps"]
+    W = args.warmup if args.warmup is not None else wl["warmup"]
+    P = args.profile_steps if args.profile_steps is not None else wl["profile"]
+    copies = 128  # 128 x 4.26 MB = 545 MB > the 256 MB last-level cache
+    mats = [tq.TqMatrix.empty(n, k) for _ in range(copies)]
+    for i, m in enumerate(mats):
+        tq.tq_synth_weights(gen.matrix_key(seed, 0xFFFF, i, 0), m)  # copy 0 is the workload's matrix
+    total = W + K
+    x_all = torch.from_numpy(gen.activations(seed, 1000, total, k)).cuda()
+    q = torch.empty((1, k), dtype=torch.int8, device="cuda")
+    d = torch.empty((1, k // 256), dtype=torch.float32, device="cuda")
+    b = torch.empty((1, k // 256), dtype=torch.int32, device="cuda")
+    y = torch.empty((1, n), dtype=torch.float32, device="cuda")
+
+    def step(i):
+        tq.tq_quantize_act(x_all[i:i + 1], q, d, b)
+        tq.tq_gemv(mats[i % copies], q, d, b, y)
+
+    elapsed = time_graph(step, W, K)
+    per_step = matrix_bytes(n, k) + k * 4 + n * 4
+    gbs = per_step * K / elapsed / 1e9
+    # per-kernel pass: events around each gemv launch, queued behind a spin kernel
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(P)]
+    torch.cuda.synchronize()
+    torch.cuda._sleep(int(2.4e9 * 0.02))
+    for j in range(P):
+        tq.tq_quantize_act(x_all[j:j + 1], q, d, b)
+        ev[j][0].record()
+        tq.tq_gemv(mats[j % copies], q, d, b, y)
+        ev[j][1].record()
+    torch.cuda.synchronize()
+    ms = float(np.mean([a.elapsed_time(c) for a, c in ev]))
+    roof = hbm_roof("gemv", matrix_bytes(n, k) + k + (k // 256) * 4 + n * 4, ms, "k_gemv<2, 1, 1>")
+    return dict(value=gbs, K=K, W=W, elapsed=elapsed, tokens=K, roof=roof,
+                config={"workload": cfg["name"], "n": n, "k": k, "tokens_per_step": 1, "bits_per_weight": 4.0625,
+                        "rotating_copies": copies, "path": "valu"},
+                extra={})
+
+
+def run_moe(args, wl, cfg):
+    import torch
+    from paper_2608_08910_amd import tq
+    from synth import gen
+
+    E, H, I, T, topk, seed = cfg["experts"], cfg["hidden"], cfg["inter"], cfg["tokens"], cfg["topk"], gen.SEED
+    L = cfg.get("layers", 1)
+    K = args.steps if args.steps is not None else wl["steps"]
+    W = args.warmup if args.warmup is not None else wl["warmup"]
+    P = args.profile_steps if args.profile_steps is not None else wl["profile"]
+    total = W + K
+
+    # resident experts, generated on the device (one set per layer)
+    layers = []
+    for l in range(L):
+        ex = tq.TqExperts.empty(E, H, I)
+        for e in range(E):
+            for p in range(3):
+                tq.tq_synth_weights(gen.matrix_key(seed, l, e, p), ex.matrix(e, p))
+        layers.append(ex)
+    torch.cuda.synchronize()
+
+    if T == 1:
+        # every step avoids the experts of the previous 3 steps (last-level-cache reuse)
+        sched = [gen.bench_routing_schedule(seed, total, T, E, topk, cfg["routing"])]
+    else:
+        # many tokens per step: a step's expert union is 0.9-3.3 GB per layer, far beyond the cache
+        sched = [[gen.routing(seed, 1000 + 97 * l + i, T, E, topk, cfg["routing"]) for i in range(total)]
+                 for l in range(L)]
+    idx_all = [torch.from_numpy(np.stack([s[0] for s in sl])).cuda() for sl in sched]  # [layer][step][T][topk]
+    w_all = [torch.from_numpy(np.stack([s[1] for s in sl])).cuda() for sl in sched]
+    x_all = []
+    for l in range(L):
+        xs = gen.activations(seed, 1000 + l, total * T, H).reshape(total, T, H)
+        if cfg.get("token_factor"):
+            xs = xs * np.stack([gen.token_factors(seed + 1 + i, T) for i in range(total)])[:, :, None]
+        x_all.append(torch.from_numpy(np.ascontiguousarray(xs, dtype=np.float32)).cuda())
+    out = torch.empty((T, H), dtype=torch.float32, device="cuda")
+    ws = torch.empty(tq.tq_moe_workspace_bytes(layers[0], T, topk), dtype=torch.uint8, device="cuda")
+
+    def step(i):
+        for l in range(L):
+            tq.tq_moe_grouped(layers[l], x_all[l][i], idx_all[l][i], w_all[l][i], out, ws, args.flags)
+
+    elapsed = time_graph(step, W, K)
+    bytes_expert = 2 * matrix_bytes(I, H) + matrix_bytes(H, I)
+    distinct = [len(np.unique(sched[l][i][0])) for l in range(L) for i in range(W, W + K)]
+    alg_bytes = sum(d * bytes_expert for d in distinct) + K * L * (T * H * 4 * 2 + T * topk * 8)
+    gbs = alg_bytes / elapsed / 1e9
+
+    # per-kernel pass: every stage's kernel launched with its own start/stop events,
+    # eager launches queued behind a spin kernel so the GPU runs them back to back
+    nst = tq.tq_moe_stage_count()
+    names = [tq.tq_moe_stage_name(i) for i in range(nst)]
+    runs = [(W + (j % K), l) for j in range(P) for l in range(L)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * nst)] for _ in runs]
+    torch.cuda.synchronize()
+    torch.cuda._sleep(int(2.4e9 * 0.05))  # ~50 ms of queue head-room
+    for (i, l), ev in zip(runs, evs):
+        tq.tq_moe_grouped_timed(layers[l], x_all[l][i], idx_all[l][i], w_all[l][i], out, ws, ev, args.flags)
+    torch.cuda.synchronize()
+    stage_ms = {n: float(np.mean([ev[2 * si].elapsed_time(ev[2 * si + 1]) for ev in evs]))
+                for si, n in enumerate(names)}
+    gu_ms = stage_ms["gate_up"]
+    n_distinct = float(np.mean([len(np.unique(sched[l][i][0])) for i, l in runs]))
+    mfma = bool(args.flags & 2) or (not (args.flags & 1) and T * topk >= 1024)
+    nl_gu = (H // 256 + 7) // 8
+    if T == 1:
+        # the single-token gate/up kernel moves the routed experts' gate and up codes +
+        # scales, reads x (fp32) and writes h (fp32, one row per slot)
+        gu_bytes = n_distinct * 2 * matrix_bytes(I, H) + T * H * 4 + T * topk * I * 4
+        rpw = 4 if nl_gu <= 2 else (2 if nl_gu <= 4 else 1)
+        gu_kernel = f"k_t1_gateup<{nl_gu}, {rpw}, 4, {'true' if (H // 256) % 8 else 'false'}>"
+    else:
+        # the grouped gate/up kernels read the routed experts' gate and up planes and the
+        # quantized tokens (int8 + scale per block), and write h per slot
+        gu_bytes = n_distinct * 2 * matrix_bytes(I, H) + T * (H + (H // 256) * 4) + T * topk * I * 4
+        rpw = 8 if nl_gu == 1 else (4 if nl_gu == 2 else (2 if nl_gu <= 4 else 1))
+        gu_kernel = "k_moe_mfma<2>" if mfma else \
+            f"k_tb<2, {nl_gu}, {rpw}, 2, 4, {'true' if (H // 256) % 8 else 'false'}>"
+    if mfma:
+        gu_ops = 2.0 * T * topk * (2 * I * H)  # int8 multiply-adds of gate and up, 2 ops each
+        achieved = gu_ops / (gu_ms * 1e-3) / 1e12
+        roof = {"kernel": "gate_up", "bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_I8_PEAK_TOPS,
+                "unit": "TOP/s", "frac": round(achieved / MFMA_I8_PEAK_TOPS, 4), "traffic": recorded_traffic(gu_kernel),
+                "ops_per_launch": gu_ops, "bytes_per_launch": round(gu_bytes), "mean_ms": round(gu_ms, 5),
+                "hbm_GBps": round(gu_bytes / (gu_ms * 1e-3) / 1e9, 1), "kernel_symbol": gu_kernel}
+    else:
+        roof = hbm_roof("gate_up", gu_bytes, gu_ms, gu_kernel)
+    routing_desc = ("uniform top-8, no expert reused within 3 steps" if T == 1 else
+                    f"{cfg['routing']} top-{topk}, fresh draw per step")
+    config = {"workload": cfg["name"], "layers": L, "experts": E, "hidden": H, "inter": I, "tokens_per_step": T,
+              "topk": topk, "routing": routing_desc, "bits_per_weight": 4.0625,
+              "resident_expert_bytes": L * E * bytes_expert, "path": "mfma" if mfma else "valu"}
+    extra = {"stage_ms": {k: round(v, 5) for k, v in stage_ms.items()},
+             "bytes_per_token": round(alg_bytes / (K * T)),
+             "mean_distinct_experts_per_layer": round(float(np.mean(distinct)), 2)}
+    return dict(value=gbs, K=K, W=W, elapsed=elapsed, tokens=K * T, roof=roof, config=config, extra=extra)
 
 
 def main():
@@ -141,119 +328,16 @@ def main():
         sys.exit(2)
 
     import torch
-    from paper_2608_08910_amd import tq
     from synth import gen
 
+    torch.cuda.set_device(0)
     wl = WORKLOADS[args.workload]
     cfg = gen.CONFIGS[wl["cfg"]]
-    E, H, I, T, topk, seed = cfg["experts"], cfg["hidden"], cfg["inter"], cfg["tokens"], cfg["topk"], gen.SEED
-    K = args.steps if args.steps is not None else wl["steps"]
-    W = args.warmup if args.warmup is not None else wl["warmup"]
-    P = args.profile_steps if args.profile_steps is not None else wl["profile"]
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-
-    # resident experts, generated on the device
-    ex = tq.TqExperts.empty(E, H, I, device=dev)
-    for e in range(E):
-        for p in range(3):
-            tq.tq_synth_weights(gen.matrix_key(seed, 0, e, p), ex.matrix(e, p))
-    torch.cuda.synchronize()
-
-    total = W + K
-    if T == 1:
-        # every step avoids the experts of the previous 3 steps (last-level-cache reuse)
-        sched = gen.bench_routing_schedule(seed, total, T, E, topk, cfg["routing"])
-    else:
-        # many tokens per step: the step's expert union is 1.2-3.3 GB, far beyond the cache
-        sched = [gen.routing(seed, 1000 + i, T, E, topk, cfg["routing"]) for i in range(total)]
-    idx_all = torch.from_numpy(np.stack([s[0] for s in sched])).to(dev)          # [steps][T][topk]
-    w_all = torch.from_numpy(np.stack([s[1] for s in sched])).to(dev)
-    xs = gen.activations(seed, 1000, total * T, H).reshape(total, T, H)
-    if cfg.get("token_factor"):
-        xs = xs * np.stack([gen.token_factors(seed + 1 + i, T) for i in range(total)])[:, :, None]
-    x_all = torch.from_numpy(np.ascontiguousarray(xs, dtype=np.float32)).to(dev)
-    del xs
-    out = torch.empty((T, H), dtype=torch.float32, device=dev)
-    ws = torch.empty(tq.tq_moe_workspace_bytes(ex, T, topk), dtype=torch.uint8, device=dev)
-
-    def step(i):
-        tq.tq_moe_grouped(ex, x_all[i], idx_all[i], w_all[i], out, ws, args.flags)
-
-    # eager sanity pass (also loads the code objects)
-    for i in range(min(W, 8)):
-        step(i)
-    torch.cuda.synchronize()
-
-    s = torch.cuda.Stream()
-    s.wait_stream(torch.cuda.current_stream())
-    g_warm, g_time = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
-    with torch.cuda.stream(s):
-        with torch.cuda.graph(g_warm, stream=s):
-            for i in range(W):
-                step(i)
-        with torch.cuda.graph(g_time, stream=s):
-            for i in range(W, W + K):
-                step(i)
-    torch.cuda.synchronize()
-
-    g_warm.replay()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    g_time.replay()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-
-    bytes_expert = 2 * matrix_bytes(I, H) + matrix_bytes(H, I)
-    distinct = [len(np.unique(sched[i][0])) for i in range(W, W + K)]
-    alg_bytes = sum(d * bytes_expert for d in distinct) + K * (T * H * 4 * 2 + T * topk * 8)
-    gbs = alg_bytes / elapsed / 1e9
-
-    # per-kernel pass: every stage's kernel launched with its own start/stop events,
-    # eager launches queued behind a spin kernel so the GPU runs them back to back
-    nst = tq.tq_moe_stage_count()
-    names = [tq.tq_moe_stage_name(i) for i in range(nst)]
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * nst)] for _ in range(P)]
-    torch.cuda.synchronize()
-    torch.cuda._sleep(int(2.4e9 * 0.05))  # ~50 ms of queue head-room
-    for j in range(P):
-        i = W + (j % K)
-        tq.tq_moe_grouped_timed(ex, x_all[i], idx_all[i], w_all[i], out, ws, evs[j], args.flags)
-    torch.cuda.synchronize()
-    stage_ms = {n: float(np.mean([evs[j][2 * si].elapsed_time(evs[j][2 * si + 1]) for j in range(P)]))
-                for si, n in enumerate(names)}
-    gu_ms = stage_ms["gate_up"]
-    prof = [sched[W + (j % K)] for j in range(P)]
-    n_distinct = float(np.mean([len(np.unique(r[0])) for r in prof]))
-    mfma = bool(args.flags & 2) or (not (args.flags & 1) and T * topk >= 1024)
-    if T == 1:
-        # the single-token gate/up kernel moves the routed experts' gate and up codes +
-        # scales, reads x (fp32) and writes h (fp32, one row per slot)
-        gu_bytes = n_distinct * 2 * matrix_bytes(I, H) + T * H * 4 + T * topk * I * 4
-        gu_kernel = "k_t1_gateup<2, 4, 4, false>"
-    else:
-        # the grouped gate/up kernels read the routed experts' gate and up planes and the
-        # quantized tokens (int8 + scale + sum per block), and write h per slot
-        gu_bytes = n_distinct * 2 * matrix_bytes(I, H) + T * (H + (H // 256) * 8) + T * topk * I * 4
-        gu_kernel = "k_moe_mfma<2>" if mfma else f"k_moe_gateup<2, {1 if T == 1 else 4}, 4>"
-    if mfma:
-        gu_ops = 2.0 * T * topk * (2 * I * H)  # int8 multiply-adds of gate and up, 2 ops each
-        achieved = gu_ops / (gu_ms * 1e-3) / 1e12
-        roof = {"kernel": "gate_up", "bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_I8_PEAK_TOPS,
-                "unit": "TOP/s", "frac": round(achieved / MFMA_I8_PEAK_TOPS, 4), "traffic": recorded_traffic(gu_kernel),
-                "ops_per_launch": gu_ops, "bytes_per_launch": round(gu_bytes), "mean_ms": round(gu_ms, 5),
-                "hbm_GBps": round(gu_bytes / (gu_ms * 1e-3) / 1e9, 1), "kernel_symbol": gu_kernel}
-    else:
-        achieved = gu_bytes / (gu_ms * 1e-3) / 1e9
-        roof = {"kernel": "gate_up", "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": recorded_traffic(gu_kernel),
-                "bytes_per_launch": round(gu_bytes), "mean_ms": round(gu_ms, 5), "kernel_symbol": gu_kernel}
-
-    routing_desc = ("uniform top-8, no expert reused within 3 steps" if T == 1 else
-                    f"{cfg['routing']} top-{topk}, fresh draw per step")
+    r = run_gemv(args, wl, cfg) if cfg["kind"] == "gemv" else run_moe(args, wl, cfg)
+    K, W, elapsed = r["K"], r["W"], r["elapsed"]
     res = {
         "metric": METRIC,
-        "value": round(gbs, 2),
+        "value": round(r["value"], 2),
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": K,
@@ -264,16 +348,14 @@ def main():
         "vs_baseline": None,
         "dtype": "int8",
         "data": "synthetic",
-        "config": {"workload": cfg["name"], "experts": E, "hidden": H, "inter": I, "tokens_per_step": T,
-                   "topk": topk, "routing": routing_desc, "bits_per_weight": 4.0625,
-                   "resident_expert_bytes": E * bytes_expert, "path": "mfma" if mfma else "valu"},
-        "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
-        "tokens_per_s": round(K * T / elapsed, 1),
-        "stage_ms": {k: round(v, 5) for k, v in stage_ms.items()},
-        "roofline": roof,
+        "config": r["config"],
+        "pct_of_hbm_peak": round(100 * r["value"] / HBM_PEAK_GBS, 2),
+        "tokens_per_s": round(r["tokens"] / elapsed, 1),
+        **r["extra"],
+        "roofline": r["roof"],
     }
     if not args.no_cpu_baseline and args.workload == "decode1":
-        res["cpu_baseline"] = cpu_baseline(seed, H, I, topk)
+        res["cpu_baseline"] = cpu_baseline(gen.SEED, cfg["hidden"], cfg["inter"], cfg["topk"])
     print(json.dumps(res), flush=True)
 
 
