@@ -233,7 +233,7 @@ def run_moe(args, wl, cfg):
             xs = xs * np.stack([gen.token_factors(seed + 1 + i, T) for i in range(total)])[:, :, None]
         x_all.append(torch.from_numpy(np.ascontiguousarray(xs, dtype=np.float32)).cuda())
     out = torch.empty((T, H), dtype=torch.float32, device="cuda")
-    ws = torch.empty(tq.tq_moe_workspace_bytes(layers[0], T, topk), dtype=torch.uint8, device="cuda")
+    ws = tq.moe_workspace(layers[0], T, topk)
 
     def step(i):
         for l in range(L):
@@ -260,35 +260,38 @@ def run_moe(args, wl, cfg):
                 for si, n in enumerate(names)}
     gu_ms = stage_ms["gate_up"]
     n_distinct = float(np.mean([len(np.unique(sched[l][i][0])) for i, l in runs]))
-    mfma = bool(args.flags & 2) or (not (args.flags & 1) and T * topk >= 1024)
-    nl_gu = (H // 256 + 7) // 8
-    if T == 1:
+    path = tq.tq_moe_path(layers[0], T, topk, args.flags)
+    mfma = path == tq.TQ_MOE_PATH_MFMA
+    nl_gu, nl_dn = (H // 256 + 7) // 8, (I // 256 + 7) // 8
+    ragged = "true" if (H // 256) % 8 else "false"
+    if path == tq.TQ_MOE_PATH_T1:
         # the single-token gate/up kernel moves the routed experts' gate and up codes +
         # scales, reads x (fp32) and writes h (fp32, one row per slot)
         gu_bytes = n_distinct * 2 * matrix_bytes(I, H) + T * H * 4 + T * topk * I * 4
-        rpw = 4 if nl_gu <= 2 else (2 if nl_gu <= 4 else 1)
-        gu_kernel = f"k_t1_gateup<{nl_gu}, {rpw}, 4, {'true' if (H // 256) % 8 else 'false'}>"
+        gu_kernel = f"k_t1_gateup<{nl_gu}, {4 if nl_gu <= 2 else (2 if nl_gu <= 4 else 1)}, 4, {ragged}>"
+        kname = "gate_up"
     else:
         # the grouped gate/up kernels read the routed experts' gate and up planes and the
         # quantized tokens (int8 + scale per block), and write h per slot
         gu_bytes = n_distinct * 2 * matrix_bytes(I, H) + T * (H + (H // 256) * 4) + T * topk * I * 4
         rpw = 8 if nl_gu == 1 else (4 if nl_gu == 2 else (2 if nl_gu <= 4 else 1))
-        gu_kernel = "k_moe_mfma<2>" if mfma else \
-            f"k_tb<2, {nl_gu}, {rpw}, 2, 4, {'true' if (H // 256) % 8 else 'false'}>"
+        gu_kernel = "k_moe_mfma<2>" if mfma else f"k_tb<2, {nl_gu}, {rpw}, 2, 4, {ragged}>"
+        kname = "gate_up"
     if mfma:
         gu_ops = 2.0 * T * topk * (2 * I * H)  # int8 multiply-adds of gate and up, 2 ops each
         achieved = gu_ops / (gu_ms * 1e-3) / 1e12
-        roof = {"kernel": "gate_up", "bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_I8_PEAK_TOPS,
+        roof = {"kernel": kname, "bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_I8_PEAK_TOPS,
                 "unit": "TOP/s", "frac": round(achieved / MFMA_I8_PEAK_TOPS, 4), "traffic": recorded_traffic(gu_kernel),
                 "ops_per_launch": gu_ops, "bytes_per_launch": round(gu_bytes), "mean_ms": round(gu_ms, 5),
                 "hbm_GBps": round(gu_bytes / (gu_ms * 1e-3) / 1e9, 1), "kernel_symbol": gu_kernel}
     else:
-        roof = hbm_roof("gate_up", gu_bytes, gu_ms, gu_kernel)
+        roof = hbm_roof(kname, gu_bytes, gu_ms, gu_kernel)
     routing_desc = ("uniform top-8, no expert reused within 3 steps" if T == 1 else
                     f"{cfg['routing']} top-{topk}, fresh draw per step")
     config = {"workload": cfg["name"], "layers": L, "experts": E, "hidden": H, "inter": I, "tokens_per_step": T,
               "topk": topk, "routing": routing_desc, "bits_per_weight": 4.0625,
-              "resident_expert_bytes": L * E * bytes_expert, "path": "mfma" if mfma else "valu"}
+              "resident_expert_bytes": L * E * bytes_expert,
+              "path": {0: "single_token", 1: "valu", 2: "mfma"}[path]}
     extra = {"stage_ms": {k: round(v, 5) for k, v in stage_ms.items()},
              "bytes_per_token": round(alg_bytes / (K * T)),
              "mean_distinct_experts_per_layer": round(float(np.mean(distinct)), 2)}

@@ -152,15 +152,25 @@ tq_status tq_gemv(const tq_mat* w, const int8_t* q, const float* d, const int32_
  * out: [t][hidden] fp32, overwritten. 1 <= topk <= 64, topk <= n_experts.
  * ws: device workspace of at least tq_moe_workspace_bytes(ex, t, topk) bytes, 256-byte
  * aligned; its contents on entry are ignored, and on return it holds the stage buffers
- * described by tq_moe_workspace_layout (for staged parity checks).
+ * described by tq_moe_workspace_layout (for staged parity checks). Calls that share a
+ * workspace must be ordered on one stream.
  * flags: 0 (automatic path choice), or TQ_MOE_FORCE_VALU / TQ_MOE_FORCE_MFMA to pin
- * the per-expert path (VALU dot4 for few tokens per expert, int8 MFMA for many). */
+ * the per-expert path (VALU dot4 for few tokens per expert, int8 MFMA for many).
+ * Single-token steps (t == 1, topk <= 8, topk * inter <= 16384) take a path of their
+ * own unless TQ_MOE_FORCE_MFMA is given (tq_moe_path). */
 #define TQ_MOE_FORCE_VALU 1
 #define TQ_MOE_FORCE_MFMA 2
 size_t tq_moe_workspace_bytes(const tq_experts* ex, int64_t t, int32_t topk);
-tq_status tq_moe_grouped(const tq_experts* ex, const float* x, int64_t t,
-                         const int32_t* topk_idx, const float* topk_w, int32_t topk,
-                         float* out, void* ws, size_t ws_bytes, int32_t flags, void* stream);
+
+/* The path tq_moe_grouped takes for these arguments: TQ_MOE_PATH_T1 (single token: a
+ * gate/up kernel, then a down kernel with the requantization and the weighted combine
+ * fused), TQ_MOE_PATH_VALU (dispatch + grouped VALU dot4 kernels), TQ_MOE_PATH_MFMA
+ * (dispatch + grouped int8 MFMA kernels); -1 if the arguments are invalid. Host only, no
+ * device work. */
+#define TQ_MOE_PATH_T1 0
+#define TQ_MOE_PATH_VALU 1
+#define TQ_MOE_PATH_MFMA 2
+int32_t tq_moe_path(const tq_experts* ex, int64_t t, int32_t topk, int32_t flags);
 
 /* Byte offsets, inside the workspace, of the stage buffers tq_moe_grouped leaves behind
  * (S = t * topk slots, slot s = t * topk + j):
@@ -190,7 +200,8 @@ tq_status tq_moe_grouped_timed(const tq_experts* ex, const float* x, int64_t t,
                                void* stream, void* const* events);
 
 /* Synchronizes `stream`, then copies the workspace's device flags word to *flags_out
- * (host). Returns TQ_OK, or TQ_ERR_DEVICE if the stream reports an error. */
+ * (host): bit 0 set if an expert id was out of range in the last call. Returns TQ_OK, or
+ * TQ_ERR_DEVICE if the stream reports an error. */
 tq_status tq_moe_status(const void* ws, const tq_experts* ex, int64_t t, int32_t topk,
                         int32_t* flags_out, void* stream);
 

@@ -33,7 +33,10 @@ constexpr int kNumStages = 5;
 static const char* const kStageNames[kNumStages] = {"prologue", "gate_up", "requant", "down", "combine"};
 
 // Control words at the start of the workspace.
-enum Ctrl { kFlags = 0, kNActive = 1, kTasksGU = 2, kTasksDn = 3, kNValid = 4, kTasksMGU = 5, kTasksMDn = 6, kCtrlWords = 64 };
+enum Ctrl {
+  kFlags = 0, kNActive = 1, kTasksGU = 2, kTasksDn = 3, kNValid = 4, kTasksMGU = 5, kTasksMDn = 6,
+  kCtrlWords = 64
+};
 
 constexpr int kMT = 64;  // tokens per MFMA tile (four 16-row MFMA tiles)
 constexpr int kMN = 64;  // weight rows per MFMA workgroup (four waves x 16)
@@ -678,12 +681,15 @@ __device__ __forceinline__ int dot_chunk16(const uint4 w, const int (&a)[8]) {
   return dot32x16(c, a);
 }
 
-// The lane's 32 fp32 values of 256-block `blk` of a row-major fp32 buffer.
+// The lane's 32 fp32 values of 256-block `blk` of a row-major fp32 buffer (AUX: cache
+// policy of the loads).
+template <int AUX = 0>
 __device__ __forceinline__ void buf_load32f(__amdgpu_buffer_rsrc_t r, uint32_t blk, int cp, float (&v)[32]) {
   const uint32_t o = (blk * 256u + (uint32_t)cp * 32u) * 4u;
 #pragma unroll
   for (int m = 0; m < 8; ++m) {
-    const uint4 u = buf_load16(r, o + 16u * m, 0, 0);
+    const u32x4 w = __builtin_amdgcn_raw_buffer_load_b128(r, o + 16u * m, 0, AUX);
+    const uint4 u = make_uint4(w.x, w.y, w.z, w.w);
     v[4 * m + 0] = __uint_as_float(u.x);
     v[4 * m + 1] = __uint_as_float(u.y);
     v[4 * m + 2] = __uint_as_float(u.z);
@@ -691,19 +697,37 @@ __device__ __forceinline__ void buf_load32f(__amdgpu_buffer_rsrc_t r, uint32_t b
   }
 }
 
-// WAVES waves per workgroup; each wave owns RPW rows (a power of two) of gate and of up
-// of one slot. After the lane partials, one butterfly leaves row r's (g, u) in the lanes
-// whose low bits, reversed, spell r.
+// Layout of the single-token kernels' LDS: the quantized activations of one token (x, or
+// the topk slots' h), their block scales and code sums, and per-wave row results.
+constexpr int kT1LdsQ = kMaxK > kT1MaxHq ? kMaxK : kT1MaxHq;
+constexpr int kT1LdsBytes = kT1LdsQ + 2 * (kT1LdsQ / 256) * 4 + 8 * 32 * 4;
+
+struct T1Lds {
+  int8_t* q;
+  float* d;
+  int* b;
+  float* y;  // [waves][32]
+  __device__ explicit T1Lds(uint8_t* raw)
+      : q(reinterpret_cast<int8_t*>(raw)),
+        d(reinterpret_cast<float*>(raw + kT1LdsQ)),
+        b(reinterpret_cast<int*>(raw + kT1LdsQ + (kT1LdsQ / 256) * 4)),
+        y(reinterpret_cast<float*>(raw + kT1LdsQ + 2 * (kT1LdsQ / 256) * 4)) {}
+};
+
+// Gate/up of one single-token workgroup `wg`: WAVES waves, each owning RPW rows (a power
+// of two) of gate and of up of one slot. x is quantized into LDS while the weight loads
+// are in flight; per load, one integer butterfly forms the exact block sums, and the
+// lanes that keep row rev(lane bits) apply the block scales; an fp32 butterfly over the
+// blocks leaves each row's (g, u) in one lane, which writes h = SiLU(g) * u.
+// `stage`: this workgroup also stores the quantized x and the status word.
 template <int NL, int RPW, int WAVES, bool RAGGED>
-__global__ __launch_bounds__(WAVES * 64) void k_t1_gateup(const float* __restrict__ x, MoeArgs A) {
+__device__ __forceinline__ void t1_gateup_wg(const float* __restrict__ x, const MoeArgs& A, int wg, bool stage,
+                                             T1Lds s) {
   static_assert(RPW == 1 || RPW == 2 || RPW == 4 || RPW == 8, "RPW must be a power of two <= 8");
-  __shared__ __attribute__((aligned(16))) int8_t s_q[kMaxK];
-  __shared__ float s_d[kMaxK / 256];
-  __shared__ int s_b[kMaxK / 256];
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 3, cp = lane & 7, gid = wv * 8 + g;
   const int kb = A.hidden / 256, I = A.inter;
-  const int j = blockIdx.x / A.tiles_gu, tile = blockIdx.x - j * A.tiles_gu;
+  const int j = wg / A.tiles_gu, tile = wg - j * A.tiles_gu;
   const int e = A.topk_idx[j];
   const bool valid = e >= 0 && e < A.n_experts;
   const int64_t ec = valid ? e : 0;
@@ -728,18 +752,18 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_gateup(const float* __restric
   const int lrow = min(row0 + rev_bits<clog2(RPW)>(lane & (RPW - 1)), I - 1);
 #pragma unroll
   for (int m = 0; m < 2; ++m) load_lane_scales<NL>(mr[m], lrow, kb, g, sr[m]);
-  quantize_to_lds(v, min(gid, kb - 1), cp, s_q, s_d, s_b, gid < kb);
+  quantize_to_lds(v, min(gid, kb - 1), cp, s.q, s.d, s.b, gid < kb);
   for (int blk = gid + WAVES * 8; blk < kb; blk += WAVES * 8) {
     buf_load32f(xr, (uint32_t)blk, cp, v);
-    quantize_to_lds(v, blk, cp, s_q, s_d, s_b, true);
+    quantize_to_lds(v, blk, cp, s.q, s.d, s.b, true);
   }
   __syncthreads();
-  if (blockIdx.x == 0) {  // stage buffers and the status word, once per call
+  if (stage) {  // stage buffers and the status word, once per call
     for (int i = threadIdx.x; i < kb * 64; i += WAVES * 64)
-      reinterpret_cast<int*>(A.xq)[i] = reinterpret_cast<const int*>(s_q)[i];
+      reinterpret_cast<int*>(A.xq)[i] = reinterpret_cast<const int*>(s.q)[i];
     for (int i = threadIdx.x; i < kb; i += WAVES * 64) {
-      A.xd[i] = s_d[i];
-      A.xb[i] = s_b[i];
+      A.xd[i] = s.d[i];
+      A.xb[i] = s.b[i];
     }
     if (threadIdx.x == 0) {
       int bad = 0;
@@ -749,13 +773,13 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_gateup(const float* __restric
   }
   if (!valid || row0 >= I) return;
   int qa[NL][8];
-  lds_acts<NL>(s_q, kb, g, cp, qa);
+  lds_acts<NL>(s.q, kb, g, cp, qa);
   using RR = RowReduce<RPW, 2>;
   float acc[2] = {0.0f, 0.0f};
 #pragma unroll
   for (int i = 0; i < NL; ++i) {
     const int b = 8 * i + g;
-    const float dv = (!RAGGED || b < kb) ? s_d[min(b, kb - 1)] : 0.0f;
+    const float dv = (!RAGGED || b < kb) ? s.d[min(b, kb - 1)] : 0.0f;
     int p[2 * RPW];
 #pragma unroll
     for (int v = 0; v < 2 * RPW; ++v) p[v] = dot_chunk16(wr[v][i], qa[i]);
@@ -768,23 +792,21 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_gateup(const float* __restric
   if (RR::writer(lane) && row0 + r < I) A.h[(int64_t)j * I + row0 + r] = silu_f32(acc[0]) * acc[1];
 }
 
-// WAVES waves per workgroup; each wave owns RPW rows of down for every slot. Values
-// m = slot * RPW + row (padded to V, a power of two) go through one butterfly; lane
-// bits reversed give m. The per-slot results meet in LDS, where the row's lane forms
-// out = sum_j w_j * y_j in ascending j.
+// Down of one single-token workgroup `wg`: WAVES waves, each owning RPW rows of down for
+// every slot. Items slot * RPW + row (padded to V, a power of two) meet in the integer
+// block butterfly; the lane that keeps an item applies its slot's block scale; the
+// fp32 butterfly over blocks leaves one item per lane; the per-slot results meet in
+// LDS, where the row's lane forms out = sum_j w_j * y_j in ascending j.
+// `stage`: this workgroup also stores the quantized h.
 template <int NL, int RPW, int TOPK, int WAVES, bool RAGGED>
-__global__ __launch_bounds__(WAVES * 64) void k_t1_down(MoeArgs A, float* __restrict__ out) {
+__device__ __forceinline__ void t1_down_wg(const MoeArgs& A, float* __restrict__ out, int wg, bool stage, T1Lds s) {
   constexpr int V = 1 << clog2(2 * TOPK * RPW - 1);  // items slot * RPW + row, padded to a power of two
   static_assert(V <= 32 && (RPW & (RPW - 1)) == 0, "down tile too large");
-  __shared__ __attribute__((aligned(16))) int8_t s_hq[kT1MaxHq];
-  __shared__ float s_hd[kT1MaxHq / 256];
-  __shared__ int s_hb[kT1MaxHq / 256];
-  __shared__ float s_y[WAVES][32];
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 3, cp = lane & 7, gid = wv * 8 + g;
   const int kb = A.inter / 256, H = A.hidden, I = A.inter;
   const int nblk = TOPK * kb;
-  const int row0 = (blockIdx.x * WAVES + wv) * RPW;
+  const int row0 = (wg * WAVES + wv) * RPW;
   int64_t ej[TOPK];
   unsigned vmask = 0;
 #pragma unroll
@@ -794,8 +816,9 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_down(MoeArgs A, float* __rest
     vmask |= (unsigned)v << j;
     ej[j] = v ? e : 0;
   }
-  // this group's first block of h first (an unrouted slot's h is never written: such a
-  // group loads the buffer's first block instead and skips the quantization)
+  // this group's first block of h first, so that its wait does not queue behind the
+  // weights (an unrouted slot's h is never written: such a group loads the buffer's
+  // first block instead and skips the quantization)
   const int blk0 = min(gid, nblk - 1);
   const bool q0 = gid < nblk && ((vmask >> (blk0 / kb)) & 1);
   const __amdgpu_buffer_rsrc_t hr = make_rsrc(A.h, (uint32_t)(TOPK * I) * 4u);
@@ -826,20 +849,20 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_down(MoeArgs A, float* __rest
 #pragma unroll
     for (int i = 0; i < NL; ++i) sr[k][i] = sp[min(8 * i + g, kb - 1)];
   }
-  quantize_to_lds(v, blk0, cp, s_hq, s_hd, s_hb, q0);
+  quantize_to_lds(v, blk0, cp, s.q, s.d, s.b, q0);
   for (int blk = gid + WAVES * 8; blk < nblk; blk += WAVES * 8) {
     if (!((vmask >> (blk / kb)) & 1)) continue;
     buf_load32f(hr, (uint32_t)blk, cp, v);
-    quantize_to_lds(v, blk, cp, s_hq, s_hd, s_hb, true);
+    quantize_to_lds(v, blk, cp, s.q, s.d, s.b, true);
   }
   __syncthreads();
-  if (blockIdx.x == 0) {  // stage buffers, once per call
+  if (stage) {  // stage buffers, once per call
     for (int i = threadIdx.x; i < TOPK * I / 4; i += WAVES * 64)
-      if ((vmask >> (4 * i / I)) & 1) reinterpret_cast<int*>(A.hq)[i] = reinterpret_cast<const int*>(s_hq)[i];
+      if ((vmask >> (4 * i / I)) & 1) reinterpret_cast<int*>(A.hq)[i] = reinterpret_cast<const int*>(s.q)[i];
     for (int i = threadIdx.x; i < nblk; i += WAVES * 64)
       if ((vmask >> (i / kb)) & 1) {
-        A.hd[i] = s_hd[i];
-        A.hb[i] = s_hb[i];
+        A.hd[i] = s.d[i];
+        A.hb[i] = s.b[i];
       }
   }
   if (row0 >= H) return;
@@ -854,7 +877,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_down(MoeArgs A, float* __rest
     for (int v = TOPK * RPW; v < V; ++v) p[v] = 0;
 #pragma unroll
     for (int j = 0; j < TOPK; ++j) {
-      const int4* qp = reinterpret_cast<const int4*>(s_hq + j * I + min(b, kb - 1) * 256 + cp * 32);
+      const int4* qp = reinterpret_cast<const int4*>(s.q + j * I + min(b, kb - 1) * 256 + cp * 32);
       const int4 lo = qp[0], hi = qp[1];
       const int qa[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
 #pragma unroll
@@ -865,12 +888,13 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_down(MoeArgs A, float* __rest
     for (int k = 0; k < KI; ++k) {
       // padded items and unrouted slots: d = 0 (their LDS codes are never written)
       const bool ok = jk[k] < TOPK && ((vmask >> jk[k]) & 1) && (!RAGGED || b < kb);
-      const float dv = ok ? s_hd[min(jk[k], TOPK - 1) * kb + min(b, kb - 1)] : 0.0f;
+      const float dv = ok ? s.d[min(jk[k], TOPK - 1) * kb + min(b, kb - 1)] : 0.0f;
       acc[k] = fmaf(f16_bits_to_f32(sr[k][i]) * dv, (float)(p[k] >> 4), acc[k]);
     }
   }
   RR::block_totals(acc);
-  if (RR::writer(lane)) s_y[wv][RR::item(lane)] = acc[0];
+  float* sy = s.y + wv * 32;
+  if (RR::writer(lane)) sy[RR::item(lane)] = acc[0];
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -879,12 +903,24 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_down(MoeArgs A, float* __rest
 #pragma unroll
     for (int j = 0; j < TOPK; ++j) {
       if (!((vmask >> j) & 1)) continue;
-      const float y = s_y[wv][j * RPW + lane];
+      const float y = sy[j * RPW + lane];
       acc = fmaf(A.topk_w[j], y, acc);
       A.yd[(int64_t)j * H + row0 + lane] = y;
     }
     out[row0 + lane] = acc;
   }
+}
+
+template <int NL, int RPW, int WAVES, bool RAGGED>
+__global__ __launch_bounds__(WAVES * 64) void k_t1_gateup(const float* __restrict__ x, MoeArgs A) {
+  __shared__ __attribute__((aligned(16))) uint8_t s_raw[kT1LdsBytes];
+  t1_gateup_wg<NL, RPW, WAVES, RAGGED>(x, A, blockIdx.x, blockIdx.x == 0, T1Lds(s_raw));
+}
+
+template <int NL, int RPW, int TOPK, int WAVES, bool RAGGED>
+__global__ __launch_bounds__(WAVES * 64) void k_t1_down(MoeArgs A, float* __restrict__ out) {
+  __shared__ __attribute__((aligned(16))) uint8_t s_raw[kT1LdsBytes];
+  t1_down_wg<NL, RPW, TOPK, WAVES, RAGGED>(A, out, blockIdx.x, blockIdx.x == 0, T1Lds(s_raw));
 }
 
 // ---------------------------------------------------------------------------------
@@ -1044,6 +1080,17 @@ static tq_status validate_experts(const tq_experts* ex, const char* fn) {
   return TQ_OK;
 }
 
+// The path a call takes (see tq_moe_path in tq.h).
+static int choose_path(const tq_experts* ex, int64_t t, int32_t topk, int32_t flags) {
+  if (t == 1 && topk <= kT1MaxTopk && (int64_t)topk * ex->inter <= kT1MaxHq && !(flags & TQ_MOE_FORCE_MFMA))
+    return TQ_MOE_PATH_T1;
+  // (the VALU kernels address activations with 32-bit buffer offsets)
+  const int64_t S = t * topk;
+  const bool valu_fits = S * std::max(ex->hidden, ex->inter) < ((int64_t)1 << 31);
+  const bool mfma = (flags & TQ_MOE_FORCE_MFMA) || (!(flags & TQ_MOE_FORCE_VALU) && (S >= kMfmaMinSlots || !valu_fits));
+  return mfma ? TQ_MOE_PATH_MFMA : (valu_fits ? TQ_MOE_PATH_VALU : -1);
+}
+
 static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const int32_t* topk_idx,
                          const float* topk_w, int32_t topk, float* out, void* ws, size_t ws_bytes, int32_t flags,
                          void* stream, void* const* events, const char* fn) {
@@ -1114,10 +1161,12 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   hipStream_t stm = (hipStream_t)stream;
 
   (void)hipGetLastError();
-  if (t == 1 && topk <= kT1MaxTopk && (int64_t)topk * ex->inter <= kT1MaxHq && !(flags & TQ_MOE_FORCE_MFMA)) {
+  const int path = choose_path(ex, t, topk, flags);
+  if (path < 0) return fail(TQ_ERR_INVALID, "%s: t * topk = %lld slots too many for the VALU path", fn, (long long)S);
+  if (path == TQ_MOE_PATH_T1) {
+    const int rgu = t1_rpw_gu(nl_gu);
     // single token: gate_up, then down with the requant and the combine fused; the
     // prologue, requant and combine stages are empty on this path
-    const int rgu = t1_rpw_gu(nl_gu);
     A.tiles_gu = (ex->inter + kT1WavesGU * rgu - 1) / (kT1WavesGU * rgu);
     const unsigned tiles_dn = (unsigned)((ex->hidden + kT1WavesDn * kT1RpwDn - 1) / (kT1WavesDn * kT1RpwDn));
     if ((st = empty_stage(events, 0, stm, fn)) != TQ_OK) return st;
@@ -1132,10 +1181,7 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   }
   // per-expert contraction on MFMA for prefill-sized groups (or when forced), VALU dot4
   // otherwise
-  // (the VALU kernels address activations with 32-bit buffer offsets)
-  const bool valu_fits = S * std::max(ex->hidden, ex->inter) < ((int64_t)1 << 31);
-  const bool mfma = (flags & TQ_MOE_FORCE_MFMA) || (!(flags & TQ_MOE_FORCE_VALU) && (S >= kMfmaMinSlots || !valu_fits));
-  if (!mfma && !valu_fits) return fail(TQ_ERR_INVALID, "%s: t * topk = %lld slots too many for the VALU path", fn, (long long)S);
+  const bool mfma = path == TQ_MOE_PATH_MFMA;
   A.tiles_mgu = (ex->inter + kMN - 1) / kMN;
   A.tiles_mdn = (ex->hidden + kMN - 1) / kMN;
   const int64_t max_tiles = S / kMT + max_active;
@@ -1190,6 +1236,17 @@ extern "C" tq_status tq_moe_grouped(const tq_experts* ex, const float* x, int64_
   return tq::moe_run(ex, x, t, topk_idx, topk_w, topk, out, ws, ws_bytes, flags, stream, nullptr, "tq_moe_grouped");
 }
 
+extern "C" int32_t tq_moe_path(const tq_experts* ex, int64_t t, int32_t topk, int32_t flags) {
+  using namespace tq;
+  clear_error();
+  if (validate_experts(ex, "tq_moe_path") != TQ_OK) return -1;
+  if (t < 1 || topk < 1 || topk > kMaxTopk || topk > ex->n_experts) {
+    fail(TQ_ERR_INVALID, "tq_moe_path: bad t or topk");
+    return -1;
+  }
+  return choose_path(ex, t, topk, flags);
+}
+
 extern "C" int32_t tq_moe_stage_count(void) { return tq::kNumStages; }
 
 extern "C" const char* tq_moe_stage_name(int32_t i) {
@@ -1216,7 +1273,9 @@ extern "C" tq_status tq_moe_status(const void* ws, const tq_experts* ex, int64_t
   const Layout L = make_layout(ex->n_experts, ex->hidden, ex->inter, t, topk);
   hipError_t e = hipStreamSynchronize((hipStream_t)stream);
   if (e != hipSuccess) return fail(TQ_ERR_DEVICE, "tq_moe_status: stream error: %s", hipGetErrorString(e));
-  e = hipMemcpy(flags_out, static_cast<const uint8_t*>(ws) + L.ctrl + 4 * kFlags, 4, hipMemcpyDeviceToHost);
+  int32_t ctrl[kCtrlWords];
+  e = hipMemcpy(ctrl, static_cast<const uint8_t*>(ws) + L.ctrl, sizeof(ctrl), hipMemcpyDeviceToHost);
   if (e != hipSuccess) return fail(TQ_ERR_DEVICE, "tq_moe_status: copy failed: %s", hipGetErrorString(e));
+  *flags_out = ctrl[kFlags];
   return TQ_OK;
 }

@@ -27,6 +27,7 @@ TQ_ERR_WORKSPACE = -3
 TQ_ERR_DEVICE = -4
 TQ_MOE_FORCE_VALU = 1
 TQ_MOE_FORCE_MFMA = 2
+TQ_MOE_PATH_T1, TQ_MOE_PATH_VALU, TQ_MOE_PATH_MFMA = 0, 1, 2
 
 
 class TqError(RuntimeError):
@@ -68,6 +69,7 @@ for _name, _args, _res in [
     ("tq_quantize_act", [_vp, _i64, _i32, _vp, _vp, _vp, _vp], _i32),
     ("tq_gemv", [_P(tq_mat), _vp, _vp, _vp, _i64, _vp, _vp, _vp], _i32),
     ("tq_moe_workspace_bytes", [_P(tq_experts), _i64, _i32], _sz),
+    ("tq_moe_path", [_P(tq_experts), _i64, _i32, _i32], _i32),
     ("tq_moe_workspace_layout", [_P(tq_experts), _i64, _i32, _P(tq_moe_layout)], _i32),
     ("tq_moe_grouped", [_P(tq_experts), _vp, _i64, _vp, _vp, _i32, _vp, _vp, _sz, _i32, _vp], _i32),
     ("tq_moe_grouped_timed", [_P(tq_experts), _vp, _i64, _vp, _vp, _i32, _vp, _vp, _sz, _i32, _vp, _P(_vp)], _i32),
@@ -228,6 +230,18 @@ class TqExperts:
 
 def tq_moe_workspace_bytes(ex: TqExperts, t: int, topk: int) -> int:
     return int(_L.tq_moe_workspace_bytes(ctypes.byref(ex.desc()), t, topk))
+
+
+def tq_moe_path(ex: TqExperts, t: int, topk: int, flags: int = 0) -> int:
+    p = int(_L.tq_moe_path(ctypes.byref(ex.desc()), t, topk, flags))
+    if p < 0:
+        raise TqError(TQ_ERR_INVALID, tq_last_error())
+    return p
+
+
+def moe_workspace(ex: TqExperts, t: int, topk: int, device="cuda") -> torch.Tensor:
+    """A device workspace of tq_moe_workspace_bytes(ex, t, topk) bytes for tq_moe_grouped."""
+    return torch.empty(tq_moe_workspace_bytes(ex, t, topk), dtype=torch.uint8, device=device)
 
 
 def tq_moe_workspace_layout(ex: TqExperts, t: int, topk: int) -> dict:

@@ -181,3 +181,26 @@ def test_moe_workspace_layout_is_consistent():
     assert offs[-1][0] + sizes[offs[-1][1]] <= lay.total
     assert lay.total == tq._L.tq_moe_workspace_bytes(ctypes.byref(d), 32, 8)
     assert lay.flags < offs[0][0]
+
+
+def test_moe_path_choice():
+    L = tq._L
+
+    def path(d, t, topk, flags=0):
+        return L.tq_moe_path(ctypes.byref(d), t, topk, flags)
+
+    d = _experts_desc(E=256, H=4096, I=2048)
+    assert path(d, 1, 8) == tq.TQ_MOE_PATH_T1
+    assert path(d, 1, 8, tq.TQ_MOE_FORCE_MFMA) == tq.TQ_MOE_PATH_MFMA
+    assert path(d, 1, 8, tq.TQ_MOE_FORCE_VALU) == tq.TQ_MOE_PATH_T1
+    assert path(d, 32, 8) == tq.TQ_MOE_PATH_VALU
+    assert path(d, 32, 8, tq.TQ_MOE_FORCE_MFMA) == tq.TQ_MOE_PATH_MFMA
+    assert path(d, 2048, 8) == tq.TQ_MOE_PATH_MFMA
+    assert path(d, 2048, 8, tq.TQ_MOE_FORCE_VALU) == tq.TQ_MOE_PATH_VALU
+    deep = _experts_desc(E=256, H=7168, I=2048)
+    assert path(deep, 8, 8) == tq.TQ_MOE_PATH_VALU
+    assert path(deep, 1, 8) == tq.TQ_MOE_PATH_T1
+    wide = _experts_desc(E=8, H=4096, I=4096)
+    assert path(wide, 1, 4) == tq.TQ_MOE_PATH_T1
+    assert path(wide, 1, 5) == tq.TQ_MOE_PATH_VALU  # 5 x 4096 requantized bytes exceed the LDS budget
+    assert path(d, 0, 8) == -1 and path(d, 1, 0) == -1

@@ -44,7 +44,7 @@ def run_moe(tq, ex, x, idx, w, flags=0):
     idd = torch.from_numpy(np.ascontiguousarray(idx)).cuda()
     wd = torch.from_numpy(np.ascontiguousarray(w)).cuda()
     out = torch.empty((t, ex.hidden), dtype=torch.float32, device="cuda")
-    ws = torch.empty(tq.tq_moe_workspace_bytes(ex, t, topk), dtype=torch.uint8, device="cuda")
+    ws = tq.moe_workspace(ex, t, topk)
     tq.tq_moe_grouped(ex, xd, idd, wd, out, ws, flags)
     torch.cuda.synchronize()
     return out, ws
@@ -248,3 +248,20 @@ def test_moe_grouped_valu_long_lists(tq, oracle, E, H, I, T, topk):
     announce(f"moe valu E={E} H={H} I={I} T={T}")
     out, ws = run_moe(tq, ex, x, idx, w, flags=tq.TQ_MOE_FORCE_VALU)
     check_moe(tq, oracle, ex, lambda e: logical[e], x, idx, w, out, ws, list(range(T)))
+
+
+def test_moe_workspace_shared_across_paths(tq, experts_h4096):
+    """One prepared workspace serves single-token and grouped calls in any order."""
+    c = gen.CONFIGS[2]
+    ws = tq.moe_workspace(experts_h4096, c["tokens"], c["topk"])
+    x = gen.activations(gen.SEED, 60, c["tokens"], c["hidden"])
+    idx, w = gen.routing(gen.SEED, 60, c["tokens"], c["experts"], c["topk"], c["routing"])
+    xd, idd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(idx).cuda(), torch.from_numpy(w).cuda()
+    outs = []
+    announce("moe workspace shared: t=1, t=32, t=1")
+    for t in (1, c["tokens"], 1):
+        out = torch.empty((t, c["hidden"]), dtype=torch.float32, device="cuda")
+        tq.tq_moe_grouped(experts_h4096, xd[:t], idd[:t], wd[:t], out, ws)
+        outs.append(out)
+        assert tq.tq_moe_status(ws, experts_h4096, t, c["topk"]) == 0
+    assert torch.equal(outs[0], outs[2]) and torch.equal(outs[0], outs[1][:1])

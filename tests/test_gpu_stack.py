@@ -43,7 +43,7 @@ def test_stack_43_layers_h7168_full_size(tq, oracle):
         x = gen.activations(gen.SEED, l, T, H)
         idx, w = gen.routing(gen.SEED, l, T, E, topk, c["routing"])
         xs.append(x); idxs.append(idx); wts.append(w)
-        ws_.append(torch.empty(tq.tq_moe_workspace_bytes(layers[l], T, topk), dtype=torch.uint8, device="cuda"))
+        ws_.append(tq.moe_workspace(layers[l], T, topk))
         outs.append(torch.empty((T, H), dtype=torch.float32, device="cuda"))
     xd = [torch.from_numpy(x).cuda() for x in xs]
     idd = [torch.from_numpy(i).cuda() for i in idxs]
