@@ -77,12 +77,14 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
 // Cache-policy bits of buffer loads: nt (streamed once).
 constexpr int kBufNT = 2;
 
+// soff must be wave-uniform (an SGPR operand); per-lane offsets go in voff.
 __device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, int aux = kBufNT) {
   const u32x4 v = aux == kBufNT ? __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kBufNT)
                                 : __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// soff must be wave-uniform (an SGPR operand); per-lane offsets go in voff.
 __device__ __forceinline__ uint16_t buf_load_u16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
   return __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
 }

@@ -379,9 +379,10 @@ __global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
             raw[m * RPW + r][i] = buf_load16(mr.codes, bc * 128u + (uint32_t)cp * 16u, srow * 128u);
           }
         }
+        // the lane's row (lane-varying, so in the vector offset)
         const uint32_t lrow = (uint32_t)min(row0 + lr, N - 1) * (uint32_t)kb;
 #pragma unroll
-        for (int i = 0; i < NL; ++i) sr[m][i] = buf_load_u16(mr.scales, (uint32_t)min(8 * i + g, kb - 1) * 2u, lrow * 2u);
+        for (int i = 0; i < NL; ++i) sr[m][i] = buf_load_u16(mr.scales, (lrow + (uint32_t)min(8 * i + g, kb - 1)) * 2u, 0);
       }
 #pragma unroll
       for (int v = 0; v < NMAT * RPW; ++v)
@@ -667,12 +668,13 @@ __device__ __forceinline__ void load_lane_codes(const MatRsrc& m, int row, int k
     w[i] = buf_load16(m.codes, (uint32_t)min(8 * i + g, kb - 1) * 128u + (uint32_t)cp * 16u, srow * 128u);
 }
 
-// The lane's NL block scales of row `row` (per lane).
+// The lane's NL block scales of row `row` (per lane, so it goes in the vector offset: a
+// lane-varying scalar offset would make the compiler loop over its distinct values).
 template <int NL>
 __device__ __forceinline__ void load_lane_scales(const MatRsrc& m, int row, int kb, int g, uint16_t (&s)[NL]) {
   const uint32_t srow = (uint32_t)row * (uint32_t)kb;
 #pragma unroll
-  for (int i = 0; i < NL; ++i) s[i] = buf_load_u16(m.scales, (uint32_t)min(8 * i + g, kb - 1) * 2u, srow * 2u);
+  for (int i = 0; i < NL; ++i) s[i] = buf_load_u16(m.scales, (srow + (uint32_t)min(8 * i + g, kb - 1)) * 2u, 0);
 }
 
 __device__ __forceinline__ int dot_chunk16(const uint4 w, const int (&a)[8]) {

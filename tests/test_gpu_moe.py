@@ -265,3 +265,87 @@ def test_moe_workspace_shared_across_paths(tq, experts_h4096):
         outs.append(out)
         assert tq.tq_moe_status(ws, experts_h4096, t, c["topk"]) == 0
     assert torch.equal(outs[0], outs[2]) and torch.equal(outs[0], outs[1][:1])
+
+
+def test_t1_repeated_calls_share_one_workspace(tq, oracle):
+    """Forty single-token calls in a row on one workspace, routing and x changing every
+    call: each output is bitwise the output of the same call on a fresh workspace, and
+    the last call's stages match the oracle."""
+    E, H, I, topk = 16, 1024, 512, 8
+    ex, logical = host_experts(tq, oracle, E, H, I, seed=71)
+    rng = np.random.default_rng(72)
+    n = 40
+    xs = rng.standard_normal((n, 1, H)).astype(np.float32)
+    idx = np.stack([rng.choice(E, topk, replace=False)[None, :] for _ in range(n)]).astype(np.int32)
+    w = rng.uniform(0.1, 1.0, (n, 1, topk)).astype(np.float32)
+    announce(f"moe t=1 repeated x{n} E={E} H={H} I={I}")
+    ws = tq.moe_workspace(ex, 1, topk)
+    outs = []
+    for i in range(n):
+        out = torch.empty((1, H), dtype=torch.float32, device="cuda")
+        tq.tq_moe_grouped(ex, torch.from_numpy(xs[i]).cuda(), torch.from_numpy(idx[i]).cuda(),
+                          torch.from_numpy(w[i]).cuda(), out, ws)
+        outs.append(out)
+    torch.cuda.synchronize()
+    assert tq.tq_moe_status(ws, ex, 1, topk) == 0
+    for i in (0, 17, n - 1):
+        fresh, _ = run_moe(tq, ex, xs[i], idx[i], w[i])
+        assert torch.equal(fresh, outs[i]), f"call {i}"
+    # the last call's stages against the oracle
+    check_moe(tq, oracle, ex, lambda e: logical[e], xs[-1], idx[-1], w[-1], outs[-1], ws, [0])
+
+
+def test_t1_unrouted_slots(tq, oracle):
+    """Out-of-range expert ids on the single-token path: flagged, and they contribute
+    nothing."""
+    E, H, I, topk = 5, 768, 512, 4
+    ex, logical = host_experts(tq, oracle, E, H, I, seed=81)
+    rng = np.random.default_rng(82)
+    x = rng.standard_normal((1, H)).astype(np.float32)
+    idx = np.array([[3, -2, 0, E]], np.int32)
+    w = np.array([[0.4, 0.3, 0.2, 0.1]], np.float32)
+    announce("moe t=1 unrouted slots")
+    out, ws = run_moe(tq, ex, x, idx, w)
+    assert tq.tq_moe_status(ws, ex, 1, topk) & 1
+    ref, ref_abs, _ = oracle.moe(x, np.array([[3, 0]], np.int32), np.array([[0.4, 0.2]], np.float32),
+                                 lambda e: logical[e])
+    assert_close(out.cpu().numpy()[0], ref[0], ref_abs[0] + 1e-30, rtol=1e-3, what="out with unrouted slots")
+
+
+def test_t1_graph_replays_match_eager(tq, oracle):
+    """Single-token calls captured in a HIP graph: every replay (with eager calls on the
+    same workspace between replays) gives bitwise the eager outputs."""
+    E, H, I, topk = 12, 4096, 2048, 8
+    ex, _ = host_experts(tq, oracle, E, H, I, seed=91)
+    rng = np.random.default_rng(92)
+    n = 4
+    xs = torch.from_numpy(rng.standard_normal((n, 1, H)).astype(np.float32)).cuda()
+    idx = torch.from_numpy(np.stack([rng.choice(E, topk, replace=False)[None, :] for _ in range(n)]).astype(np.int32)).cuda()
+    w = torch.from_numpy(rng.uniform(0.1, 1.0, (n, 1, topk)).astype(np.float32)).cuda()
+    ws = tq.moe_workspace(ex, 1, topk)
+    announce("moe t=1 graph capture")
+    eager = [torch.empty((1, H), dtype=torch.float32, device="cuda") for _ in range(n)]
+    for i in range(n):
+        tq.tq_moe_grouped(ex, xs[i], idx[i], w[i], eager[i], ws)
+    torch.cuda.synchronize()
+    outs = [torch.empty((1, H), dtype=torch.float32, device="cuda") for _ in range(n)]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            for i in range(n):
+                tq.tq_moe_grouped(ex, xs[i], idx[i], w[i], outs[i], ws, stream=s)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for o in outs:
+            o.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        for i in range(n):
+            assert torch.equal(outs[i], eager[i]), f"replay {rep} call {i}"
+        tmp = torch.empty((1, H), dtype=torch.float32, device="cuda")
+        tq.tq_moe_grouped(ex, xs[rep], idx[rep], w[rep], tmp, ws)  # eager work between replays
+        torch.cuda.synchronize()
+        assert torch.equal(tmp, eager[rep])
+    assert tq.tq_moe_status(ws, ex, 1, topk) == 0
