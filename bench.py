@@ -177,15 +177,14 @@ def run_gemv(args, wl, cfg):
     elapsed = time_graph(step, W, K)
     per_step = matrix_bytes(n, k) + k * 4 + n * 4
     gbs = per_step * K / elapsed / 1e9
-    # per-kernel pass: events around each gemv launch, queued behind a spin kernel
+    # per-kernel pass: each gemv launched with its own start/stop events (the kernel's
+    # timestamps), eager launches queued behind a spin kernel
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(P)]
     torch.cuda.synchronize()
     torch.cuda._sleep(int(2.4e9 * 0.02))
     for j in range(P):
         tq.tq_quantize_act(x_all[j:j + 1], q, d, b)
-        ev[j][0].record()
-        tq.tq_gemv(mats[j % copies], q, d, b, y)
-        ev[j][1].record()
+        tq.tq_gemv_timed(mats[j % copies], q, d, b, y, ev[j])
     torch.cuda.synchronize()
     ms = float(np.mean([a.elapsed_time(c) for a, c in ev]))
     roof = hbm_roof("gemv", matrix_bytes(n, k) + k + (k // 256) * 4 + n * 4, ms, "k_gemv<2, 1, 1>")

@@ -140,6 +140,13 @@ tq_status tq_quantize_act(const float* x, int64_t t, int32_t k, int8_t* q, float
 tq_status tq_gemv(const tq_mat* w, const int8_t* q, const float* d, const int32_t* bsum,
                   int64_t t, float* y, int32_t* isum_dbg, void* stream);
 
+/* As tq_gemv, and also times the kernel with two host-created HIP events (hipEvent_t,
+ * passed as void*): the kernel is launched with hipExtLaunchKernelGGL, so events[0] and
+ * events[1] carry its own start and stop timestamps. For benchmarks; neither event may
+ * be NULL. */
+tq_status tq_gemv_timed(const tq_mat* w, const int8_t* q, const float* d, const int32_t* bsum,
+                        int64_t t, float* y, int32_t* isum_dbg, void* stream, void* const* events);
+
 /* Routed-expert MoE layer over the folded experts (Sec. 2.2 dot pass applied to every
  * routed gate/up/down projection; the paper's layers are 43 x 3 projections x 256
  * experts, Sec. 2.1). For every token t and slot j < topk with e = topk_idx[t][j]:

@@ -13,6 +13,8 @@
 // block (exact block sums, which the debug output stores), each kept block sum gets one
 // fp32 multiply-add by f32(s) * d, and one fp32 butterfly over the blocks gives the row
 // totals.
+#include <hip/hip_ext.h>
+
 #include "tq_device.hpp"
 #include "tq_internal.hpp"
 
@@ -125,10 +127,9 @@ static gemv_fn pick_gemv(int nl, int nt, int rpw) {
 
 }  // namespace tq
 
-extern "C" tq_status tq_gemv(const tq_mat* w, const int8_t* q, const float* d, const int32_t* bsum,
-                             int64_t t, float* y, int32_t* isum_dbg, void* stream) {
-  using namespace tq;
-  clear_error();
+namespace tq {
+static tq_status gemv_run(const tq_mat* w, const int8_t* q, const float* d, const int32_t* bsum, int64_t t, float* y,
+                          int32_t* isum_dbg, void* stream, void* const* events) {
   if (!w) return fail(TQ_ERR_INVALID, "tq_gemv: null matrix descriptor");
   const int n = w->n, k = w->k;
   if (n < 1) return fail(TQ_ERR_INVALID, "tq_gemv: n = %d < 1", n);
@@ -150,7 +151,25 @@ extern "C" tq_status tq_gemv(const tq_mat* w, const int8_t* q, const float* d, c
   const int64_t waves = (n + rpw - 1) / rpw;
   const unsigned wgs = (unsigned)((waves + 3) / 4);
   (void)hipGetLastError();
-  hipLaunchKernelGGL(pick_gemv(nl, nt, rpw), dim3(wgs), dim3(256), 0, (hipStream_t)stream, w->codes, w->scales, n,
-                     kb, q, d, (int)t, y, isum_dbg);
+  if (events)
+    hipExtLaunchKernelGGL(pick_gemv(nl, nt, rpw), dim3(wgs), dim3(256), 0, (hipStream_t)stream, (hipEvent_t)events[0],
+                          (hipEvent_t)events[1], 0, w->codes, w->scales, n, kb, q, d, (int)t, y, isum_dbg);
+  else
+    hipLaunchKernelGGL(pick_gemv(nl, nt, rpw), dim3(wgs), dim3(256), 0, (hipStream_t)stream, w->codes, w->scales, n,
+                       kb, q, d, (int)t, y, isum_dbg);
   return check_launch("tq_gemv");
+}
+}  // namespace tq
+
+extern "C" tq_status tq_gemv(const tq_mat* w, const int8_t* q, const float* d, const int32_t* bsum,
+                             int64_t t, float* y, int32_t* isum_dbg, void* stream) {
+  tq::clear_error();
+  return tq::gemv_run(w, q, d, bsum, t, y, isum_dbg, stream, nullptr);
+}
+
+extern "C" tq_status tq_gemv_timed(const tq_mat* w, const int8_t* q, const float* d, const int32_t* bsum,
+                                   int64_t t, float* y, int32_t* isum_dbg, void* stream, void* const* events) {
+  tq::clear_error();
+  if (!events || !events[0] || !events[1]) return tq::fail(TQ_ERR_INVALID, "tq_gemv_timed: null event");
+  return tq::gemv_run(w, q, d, bsum, t, y, isum_dbg, stream, events);
 }

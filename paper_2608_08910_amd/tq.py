@@ -68,6 +68,7 @@ for _name, _args, _res in [
     ("tq_synth_weights", [ctypes.c_uint64, _i32, _i32, _vp, _vp, _vp], _i32),
     ("tq_quantize_act", [_vp, _i64, _i32, _vp, _vp, _vp, _vp], _i32),
     ("tq_gemv", [_P(tq_mat), _vp, _vp, _vp, _i64, _vp, _vp, _vp], _i32),
+    ("tq_gemv_timed", [_P(tq_mat), _vp, _vp, _vp, _i64, _vp, _vp, _vp, _P(_vp)], _i32),
     ("tq_moe_workspace_bytes", [_P(tq_experts), _i64, _i32], _sz),
     ("tq_moe_path", [_P(tq_experts), _i64, _i32, _i32], _i32),
     ("tq_moe_workspace_layout", [_P(tq_experts), _i64, _i32, _P(tq_moe_layout)], _i32),
@@ -186,6 +187,24 @@ def tq_gemv(m: TqMatrix, q: torch.Tensor, d: torch.Tensor, bsum: torch.Tensor, y
     _ok(_L.tq_gemv(ctypes.byref(desc), _dev(q, torch.int8, "q", (t, m.k)), _dev(d, torch.float32, "d", (t, m.k // 256)),
                    _dev(bsum, torch.int32, "bsum", (t, m.k // 256)), t, _dev(y, torch.float32, "y", (t, m.n)), dbg,
                    _stream(stream)))
+
+
+def tq_gemv_timed(m: TqMatrix, q: torch.Tensor, d: torch.Tensor, bsum: torch.Tensor, y: torch.Tensor, events,
+                  isum_dbg: torch.Tensor | None = None, stream=None):
+    """events: two torch.cuda.Event(enable_timing=True) that receive the kernel's own start
+    and stop timestamps."""
+    if len(events) != 2:
+        raise ValueError("need 2 events")
+    for ev in events:  # torch creates the HIP event on its first record
+        if ev.cuda_event == 0:
+            ev.record()
+    arr = (_vp * 2)(*[ev.cuda_event for ev in events])
+    t = q.shape[0]
+    desc = m.desc()
+    dbg = None if isum_dbg is None else _dev(isum_dbg, torch.int32, "isum_dbg", (t, m.n, m.k // 256))
+    _ok(_L.tq_gemv_timed(ctypes.byref(desc), _dev(q, torch.int8, "q", (t, m.k)), _dev(d, torch.float32, "d", (t, m.k // 256)),
+                         _dev(bsum, torch.int32, "bsum", (t, m.k // 256)), t, _dev(y, torch.float32, "y", (t, m.n)), dbg,
+                         _stream(stream), arr))
 
 
 # -- routed-expert MoE layer ----------------------------------------------------------------
