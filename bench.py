@@ -274,7 +274,8 @@ def run_moe(args, wl, cfg):
         # quantized tokens (int8 + scale per block), and write h per slot
         gu_bytes = n_distinct * 2 * matrix_bytes(I, H) + T * (H + (H // 256) * 4) + T * topk * I * 4
         rpw = 8 if nl_gu == 1 else (4 if nl_gu == 2 else (2 if nl_gu <= 4 else 1))
-        gu_kernel = "k_moe_mfma<2>" if mfma else f"k_tb<2, {nl_gu}, {rpw}, 2, 4, {ragged}>"
+        nt = 2 if nl_gu <= 2 else 1  # tokens per group of the grouped VALU kernel
+        gu_kernel = "k_moe_mfma<2>" if mfma else f"k_tb<2, {nl_gu}, {rpw}, {nt}, 4, {ragged}>"
         kname = "gate_up"
     if mfma:
         gu_ops = 2.0 * T * topk * (2 * I * H)  # int8 multiply-adds of gate and up, 2 ops each

@@ -264,36 +264,40 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
 // exist (ragged k) or a token past the list gets d = 0, which adds exactly nothing.
 // ---------------------------------------------------------------------------------
 
-// NT tokens (list positions c0 ..) against the wave's NMAT x RPW rows, whose codes the
-// lane holds unpacked (wc[m * RPW + r][i]) with the scales of its own row (sl[m][i]:
-// after the block butterfly a lane keeps items of one row, rev(lane bits) for RPW <= 8).
-// Items are (row r, token tt) = r * NT + tt, each for the NMAT matrices.
+// One group of NT tokens (list positions c0 .. c0 + NT - 1) as the lane needs it: their
+// slots, their 32 activation codes per load, and the block scales of the lane's kept
+// items (zero past the list or past kb). Positions past the list repeat the last one.
+template <int NMAT, int NL, int RPW, int NT>
+struct TbActs {
+  static constexpr int KI = RowReduce<RPW * NT, NMAT>::KI;
+  int slot[NT];
+  int q[NT][NL][8];
+  float d[KI][NL];
+};
+
+// sv: lane p holds the slot of list position p (p < 64); later positions from the list.
 template <int NMAT, int NL, int RPW, int NT, bool RAGGED>
-__device__ __forceinline__ void tb_tokens(const MoeArgs& A, const int (&wc)[NMAT * RPW][NL][8],
-                                          const float (&sl)[NMAT][NL], __amdgpu_buffer_rsrc_t qr,
-                                          __amdgpu_buffer_rsrc_t dr, int K, int kb, int N, int off, int cnt, int c0,
-                                          int row0, int lane, int g, int cp) {
+__device__ __forceinline__ void tb_acts_load(const MoeArgs& A, __amdgpu_buffer_rsrc_t qr, __amdgpu_buffer_rsrc_t dr,
+                                             int K, int kb, int sv, int off, int cnt, int c0, int lane, int g, int cp,
+                                             TbActs<NMAT, NL, RPW, NT>& T) {
   using RR = RowReduce<RPW * NT, NMAT>;
-  constexpr int KI = RR::KI;
-  int slot[NT], arow[NT];
-  int qa[NT][NL][8];
+  int arow[NT];
 #pragma unroll
   for (int tt = 0; tt < NT; ++tt) {
-    slot[tt] = A.slot_list[off + min(c0 + tt, cnt - 1)];
-    arow[tt] = NMAT == 2 ? slot[tt] / A.topk : slot[tt];
+    const int p = min(c0 + tt, cnt - 1);
+    T.slot[tt] = p < 64 ? __builtin_amdgcn_readlane(sv, p) : A.slot_list[off + p];
+    arow[tt] = NMAT == 2 ? T.slot[tt] / A.topk : T.slot[tt];
 #pragma unroll
     for (int i = 0; i < NL; ++i) {
       const uint32_t bc = (uint32_t)min(8 * i + g, kb - 1);
       const uint4 lo = buf_load16(qr, bc * 256u + (uint32_t)cp * 32u, (uint32_t)arow[tt] * (uint32_t)K, 0);
       const uint4 hi = buf_load16(qr, bc * 256u + (uint32_t)cp * 32u + 16u, (uint32_t)arow[tt] * (uint32_t)K, 0);
-      qa[tt][i][0] = (int)lo.x; qa[tt][i][1] = (int)lo.y; qa[tt][i][2] = (int)lo.z; qa[tt][i][3] = (int)lo.w;
-      qa[tt][i][4] = (int)hi.x; qa[tt][i][5] = (int)hi.y; qa[tt][i][6] = (int)hi.z; qa[tt][i][7] = (int)hi.w;
+      T.q[tt][i][0] = (int)lo.x; T.q[tt][i][1] = (int)lo.y; T.q[tt][i][2] = (int)lo.z; T.q[tt][i][3] = (int)lo.w;
+      T.q[tt][i][4] = (int)hi.x; T.q[tt][i][5] = (int)hi.y; T.q[tt][i][6] = (int)hi.z; T.q[tt][i][7] = (int)hi.w;
     }
   }
-  // block scales of the lane's kept items' tokens (zero past the list or past kb)
-  float dk[KI][NL];
 #pragma unroll
-  for (int k = 0; k < KI; ++k) {
+  for (int k = 0; k < RR::KI; ++k) {
     const int tt = RR::kept(k, lane) % NT;
     int ar = arow[0];
 #pragma unroll
@@ -303,10 +307,22 @@ __device__ __forceinline__ void tb_tokens(const MoeArgs& A, const int (&wc)[NMAT
     for (int i = 0; i < NL; ++i) {
       const int b = 8 * i + g;
       const uint32_t bc = (uint32_t)min(b, kb - 1);
-      const float dv = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(dr, bc * 4u, (uint32_t)ar * (uint32_t)kb * 4u, 0));
-      dk[k][i] = (tv && (!RAGGED || b < kb)) ? dv : 0.0f;
+      const float dv = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(dr, ((uint32_t)ar * (uint32_t)kb + bc) * 4u, 0, 0));
+      T.d[k][i] = (tv && (!RAGGED || b < kb)) ? dv : 0.0f;
     }
   }
+}
+
+// The token group against the wave's NMAT x RPW rows, whose codes the lane holds
+// unpacked (wc[m * RPW + r][i]) with the scales of its own row (sl[m][i]: after the
+// block butterfly a lane keeps items of one row, rev(lane bits) for RPW <= 8). Items are
+// (row r, token tt) = r * NT + tt, each for the NMAT matrices.
+template <int NMAT, int NL, int RPW, int NT>
+__device__ __forceinline__ void tb_acts_compute(const MoeArgs& A, const int (&wc)[NMAT * RPW][NL][8],
+                                                const float (&sl)[NMAT][NL], const TbActs<NMAT, NL, RPW, NT>& T, int N,
+                                                int cnt, int c0, int row0, int lane) {
+  using RR = RowReduce<RPW * NT, NMAT>;
+  constexpr int KI = RR::KI;
   float acc[KI * NMAT];
 #pragma unroll
   for (int v = 0; v < KI * NMAT; ++v) acc[v] = 0.0f;
@@ -318,20 +334,20 @@ __device__ __forceinline__ void tb_tokens(const MoeArgs& A, const int (&wc)[NMAT
 #pragma unroll
       for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
-        for (int m = 0; m < NMAT; ++m) p[(r * NT + tt) * NMAT + m] = dot32x16(wc[m * RPW + r][i], qa[tt][i]);
+        for (int m = 0; m < NMAT; ++m) p[(r * NT + tt) * NMAT + m] = dot32x16(wc[m * RPW + r][i], T.q[tt][i]);
     RR::block_sums(p);
 #pragma unroll
     for (int k = 0; k < KI; ++k)
 #pragma unroll
       for (int m = 0; m < NMAT; ++m)
-        acc[k * NMAT + m] = fmaf(sl[m][i] * dk[k][i], (float)(p[k * NMAT + m] >> 4), acc[k * NMAT + m]);
+        acc[k * NMAT + m] = fmaf(sl[m][i] * T.d[k][i], (float)(p[k * NMAT + m] >> 4), acc[k * NMAT + m]);
   }
   RR::block_totals(acc);
   if (RR::writer(lane)) {
     const int it = RR::item(lane), r = it / NT, tt = it % NT;
-    int sv = slot[0];
+    int sv = T.slot[0];
 #pragma unroll
-    for (int u = 1; u < NT; ++u) sv = tt == u ? slot[u] : sv;
+    for (int u = 1; u < NT; ++u) sv = tt == u ? T.slot[u] : sv;
     if (row0 + r < N && c0 + tt < cnt) {
       if constexpr (NMAT == 2) A.h[(int64_t)sv * A.inter + row0 + r] = silu_f32(acc[0]) * acc[1];
       else A.yd[(int64_t)sv * A.hidden + row0 + r] = acc[0];
@@ -341,6 +357,10 @@ __device__ __forceinline__ void tb_tokens(const MoeArgs& A, const int (&wc)[NMAT
 
 // NMAT == 2: h[slot][row] = SiLU(Wg[e] xq[token]) * (Wu[e] xq[token]);
 // NMAT == 1: yd[slot][row] = Wd[e] hq[slot].
+// Per task, in issue order: the expert's first 64 slots (one per lane), the wave's weight
+// rows, then the first token group's activations, which depend only on the slots, so
+// that their round trip overlaps the weights' (most tasks have a single group); further
+// groups load and compute in turn (the last one possibly part-empty).
 template <int NMAT, int NL, int RPW, int NT, int WAVES, bool RAGGED>
 __global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
   static_assert(RPW <= 8 && (RPW & (RPW - 1)) == 0, "RPW: a power of two <= 8");
@@ -361,6 +381,9 @@ __global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
     const int off = A.act_off[a], cnt = A.act_off[a + 1] - off;
     const int row0 = (tile * WAVES + wv) * RPW;
     if (row0 >= N) continue;
+    const int sv = A.slot_list[off + min(lane, cnt - 1)];
+    constexpr int NF = NT > 1 ? NT : 1;  // the first group's width
+    TbActs<NMAT, NL, RPW, NF> first;
     int wc[NMAT * RPW][NL][8];
     float sl[NMAT][NL];
     {
@@ -384,6 +407,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
 #pragma unroll
         for (int i = 0; i < NL; ++i) sr[m][i] = buf_load_u16(mr.scales, (lrow + (uint32_t)min(8 * i + g, kb - 1)) * 2u, 0);
       }
+      tb_acts_load<NMAT, NL, RPW, NF, RAGGED>(A, qr, dr, K, kb, sv, off, cnt, 0, lane, g, cp, first);
 #pragma unroll
       for (int v = 0; v < NMAT * RPW; ++v)
 #pragma unroll
@@ -393,11 +417,12 @@ __global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
 #pragma unroll
         for (int i = 0; i < NL; ++i) sl[m][i] = f16_bits_to_f32(sr[m][i]);
     }
-    int c0 = 0;
-    if constexpr (NT > 1)
-      for (; c0 + NT <= cnt; c0 += NT)
-        tb_tokens<NMAT, NL, RPW, NT, RAGGED>(A, wc, sl, qr, dr, K, kb, N, off, cnt, c0, row0, lane, g, cp);
-    for (; c0 < cnt; ++c0) tb_tokens<NMAT, NL, RPW, 1, RAGGED>(A, wc, sl, qr, dr, K, kb, N, off, cnt, c0, row0, lane, g, cp);
+    tb_acts_compute<NMAT, NL, RPW, NF>(A, wc, sl, first, N, cnt, 0, row0, lane);
+    for (int c0 = NF; c0 < cnt; c0 += NF) {
+      TbActs<NMAT, NL, RPW, NF> grp;
+      tb_acts_load<NMAT, NL, RPW, NF, RAGGED>(A, qr, dr, K, kb, sv, off, cnt, c0, lane, g, cp, grp);
+      tb_acts_compute<NMAT, NL, RPW, NF>(A, wc, sl, grp, N, cnt, c0, row0, lane);
+    }
   }
 }
 
@@ -932,7 +957,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_down(MoeArgs A, float* __rest
 using moe_fn = void (*)(MoeArgs);
 
 // Grouped-decode tiles: each wave holds about 16 unpacked chunks per lane
-// (NMAT * RPW * NL), tokens in pairs (gate/up) or fours (down).
+// (NMAT * RPW * NL).
 constexpr int kTbWaves = 4;
 static int tb_rpw(int nmat, int nl) {
   if (nmat == 2) return nl == 1 ? 8 : (nl == 2 ? 4 : (nl <= 4 ? 2 : 1));
@@ -942,7 +967,9 @@ static int tb_rpw(int nmat, int nl) {
 template <int NMAT, int NL, bool R>
 static moe_fn pick_tb_nl() {
   constexpr int RPW = NMAT == 2 ? (NL == 1 ? 8 : (NL == 2 ? 4 : (NL <= 4 ? 2 : 1))) : (NL <= 2 ? 8 : (NL <= 4 ? 4 : 2));
-  constexpr int NT = NMAT == 2 ? 2 : 4;
+  // tokens per group: pairs, single tokens where a pair's activations would crowd the
+  // registers that hold the weights
+  constexpr int NT = NL <= 2 ? 2 : 1;
   return k_tb<NMAT, NL, RPW, NT, kTbWaves, R>;
 }
 
