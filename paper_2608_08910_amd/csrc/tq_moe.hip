@@ -355,12 +355,30 @@ __device__ __forceinline__ void tb_acts_compute(const MoeArgs& A, const int (&wc
   }
 }
 
+// A task's scalars (its active expert's slot-list range and id) in one vector load:
+// lane 0 gets the range's start, lane 1 its end, lane 2 the expert id. Kept in a vector
+// register and read out lane by lane only where used, so that a fetch issued one task
+// ahead is not waited for at once.
+__device__ __forceinline__ int tb_task_fetch(const MoeArgs& A, int task, int tiles, int lane) {
+  const int a = task / tiles;
+  return *(lane == 2 ? A.active + a : A.act_off + a + (lane & 1));
+}
+struct TbTask {
+  int64_t e;
+  int off, cnt, tile;
+};
+__device__ __forceinline__ TbTask tb_task(int v, int task, int tiles) {
+  const int off = __builtin_amdgcn_readlane(v, 0);
+  return {(int64_t)__builtin_amdgcn_readlane(v, 2), off, __builtin_amdgcn_readlane(v, 1) - off, task % tiles};
+}
+
 // NMAT == 2: h[slot][row] = SiLU(Wg[e] xq[token]) * (Wu[e] xq[token]);
 // NMAT == 1: yd[slot][row] = Wd[e] hq[slot].
-// Per task, in issue order: the expert's first 64 slots (one per lane), the wave's weight
-// rows, then the first token group's activations, which depend only on the slots, so
-// that their round trip overlaps the weights' (most tasks have a single group); further
-// groups load and compute in turn (the last one possibly part-empty).
+// Per task, in issue order: the wave's weight rows, then the first token group's
+// activations (their slots, the expert's first 64, one per lane, came in during the task
+// before), so that their round trip overlaps the weights' (most tasks have a single
+// group); then the next task's slots; further groups load and compute in turn (the last
+// one possibly part-empty).
 template <int NMAT, int NL, int RPW, int NT, int WAVES, bool RAGGED>
 __global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
   static_assert(RPW <= 8 && (RPW & (RPW - 1)) == 0, "RPW: a power of two <= 8");
@@ -375,17 +393,29 @@ __global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
   const __amdgpu_buffer_rsrc_t qr = make_rsrc(NMAT == 2 ? A.xq : A.hq, arows * (uint32_t)K);
   const __amdgpu_buffer_rsrc_t dr = make_rsrc(NMAT == 2 ? A.xd : A.hd, arows * (uint32_t)kb * 4u);
   const int lr = rev_bits<clog2(RPW)>(lane & (RPW - 1));  // the lane's row after the block butterfly
-  for (int task = blockIdx.x; task < n_tasks; task += gridDim.x) {
-    const int a = task / tiles, tile = task - a * tiles;
-    const int64_t e = A.active[a];
-    const int off = A.act_off[a], cnt = A.act_off[a + 1] - off;
-    const int row0 = (tile * WAVES + wv) * RPW;
-    if (row0 >= N) continue;
-    const int sv = A.slot_list[off + min(lane, cnt - 1)];
+  int task = blockIdx.x;
+  if (task >= n_tasks) return;
+  // A task's scalars and slot list are fetched while the task before it runs (at its own
+  // start each would be another round trip ahead of the weight loads).
+  int tv = tb_task_fetch(A, task, tiles, lane);
+  int sv;
+  {
+    const TbTask t0 = tb_task(tv, task, tiles);
+    sv = A.slot_list[t0.off + min(lane, t0.cnt - 1)];
+  }
+  for (; task < n_tasks; task += gridDim.x) {
+    const TbTask cur = tb_task(tv, task, tiles);
+    const int task_next = min(task + (int)gridDim.x, n_tasks - 1);
+    const int tv_next = tb_task_fetch(A, task_next, tiles, lane);
+    const int64_t e = cur.e;
+    const int off = cur.off, cnt = cur.cnt;
+    // rows past N (a ragged last tile) load the last row and write nothing
+    const int row0 = (cur.tile * WAVES + wv) * RPW;
     constexpr int NF = NT > 1 ? NT : 1;  // the first group's width
     TbActs<NMAT, NL, RPW, NF> first;
     int wc[NMAT * RPW][NL][8];
     float sl[NMAT][NL];
+    int sv_next;
     {
       uint4 raw[NMAT * RPW][NL];
       uint16_t sr[NMAT][NL];
@@ -408,6 +438,13 @@ __global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
         for (int i = 0; i < NL; ++i) sr[m][i] = buf_load_u16(mr.scales, (lrow + (uint32_t)min(8 * i + g, kb - 1)) * 2u, 0);
       }
       tb_acts_load<NMAT, NL, RPW, NF, RAGGED>(A, qr, dr, K, kb, sv, off, cnt, 0, lane, g, cp, first);
+      // the next task's slots, after this task's loads and ahead of the wait for them
+      __builtin_amdgcn_sched_barrier(0);
+      {
+        const TbTask nxt = tb_task(tv_next, task_next, tiles);
+        sv_next = A.slot_list[nxt.off + min(lane, nxt.cnt - 1)];
+      }
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int v = 0; v < NMAT * RPW; ++v)
 #pragma unroll
@@ -423,6 +460,8 @@ __global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
       tb_acts_load<NMAT, NL, RPW, NF, RAGGED>(A, qr, dr, K, kb, sv, off, cnt, c0, lane, g, cp, grp);
       tb_acts_compute<NMAT, NL, RPW, NF>(A, wc, sl, grp, N, cnt, c0, row0, lane);
     }
+    tv = tv_next;
+    sv = sv_next;
   }
 }
 
@@ -440,16 +479,29 @@ __global__ __launch_bounds__(256) void k_moe_combine(MoeArgs A, float* __restric
   if (i >= A.t * H4) return;
   const int64_t tok = i / H4, c4 = i - tok * H4;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int j = 0; j < A.topk; ++j) {
-    const int64_t s = tok * A.topk + j;
-    const int e = A.topk_idx[s];
-    if (e < 0 || e >= A.n_experts) continue;
-    const float wj = A.topk_w[s];
-    const float4 v = reinterpret_cast<const float4*>(A.yd + s * A.hidden)[c4];
-    acc.x = fmaf(wj, v.x, acc.x);
-    acc.y = fmaf(wj, v.y, acc.y);
-    acc.z = fmaf(wj, v.z, acc.z);
-    acc.w = fmaf(wj, v.w, acc.w);
+  // eight slots at a time: their ids, weights and rows load together (one round trip,
+  // not one per slot; positions past topk reload the last slot and are skipped), then
+  // the sum goes on in ascending j, skipping unrouted slots (their rows are never written)
+  constexpr int kJ = 8;
+  for (int j0 = 0; j0 < A.topk; j0 += kJ) {
+    int e[kJ];
+    float w[kJ];
+    float4 v[kJ];
+#pragma unroll
+    for (int u = 0; u < kJ; ++u) {
+      const int64_t s = tok * A.topk + min(j0 + u, A.topk - 1);
+      e[u] = A.topk_idx[s];
+      w[u] = A.topk_w[s];
+      v[u] = reinterpret_cast<const float4*>(A.yd + s * A.hidden)[c4];
+    }
+#pragma unroll
+    for (int u = 0; u < kJ; ++u) {
+      if (j0 + u >= A.topk || e[u] < 0 || e[u] >= A.n_experts) continue;
+      acc.x = fmaf(w[u], v[u].x, acc.x);
+      acc.y = fmaf(w[u], v[u].y, acc.y);
+      acc.z = fmaf(w[u], v[u].z, acc.z);
+      acc.w = fmaf(w[u], v[u].w, acc.w);
+    }
   }
   reinterpret_cast<float4*>(out)[i] = acc;
 }
@@ -566,25 +618,23 @@ __global__ __launch_bounds__(256) void k_moe_mfma(MoeArgs A) {
       dst[2] = st.a2;
       dst[3] = st.a3;
       if (part == 0) s_d[buf][tt] = st.d;
-      uint4 wc[NMAT][2];
+      // this block's weights unpacked to 16c bytes (the B operands) and its scales / 16
+      // (the MFMA sums 16c * q = 16 isum; dividing the f16 scale by 16 is exact), before
+      // the stage registers take the next block's loads
       float sf[NMAT];
-#pragma unroll
-      for (int m = 0; m < NMAT; ++m) {
-        wc[m][0] = st.w[m][0];
-        wc[m][1] = st.w[m][1];
-        sf[m] = f16_bits_to_f32(st.s[m]);
-      }
-      if (b + 1 < kb) mfma_fetch<NMAT>(st, qrow, dsrc, arow, mr, wrow, kb, g, b + 1);
-      __syncthreads();
       v4i bop[NMAT][2][2];
 #pragma unroll
-      for (int m = 0; m < NMAT; ++m)
+      for (int m = 0; m < NMAT; ++m) {
+        sf[m] = f16_bits_to_f32(st.s[m]) * 0.0625f;
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
-          const uint4 w = wc[m][c];
+          const uint4 w = st.w[m][c];
           bop[m][c][0] = v4i{lo16c(w.x), lo16c(w.y), lo16c(w.z), lo16c(w.w)};
           bop[m][c][1] = v4i{hi16c(w.x), hi16c(w.y), hi16c(w.z), hi16c(w.w)};
         }
+      }
+      if (b + 1 < kb) mfma_fetch<NMAT>(st, qrow, dsrc, arow, mr, wrow, kb, g, b + 1);
+      __syncthreads();
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt) {
         const int8_t* arow_lds = s_a[buf] + (mt * 16 + li) * kAStride;
@@ -601,12 +651,15 @@ __global__ __launch_bounds__(256) void k_moe_mfma(MoeArgs A) {
           C = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[0][1], bop[m][0][1], C, 0, 0, 0);
           C = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[1][0], bop[m][1][0], C, 0, 0, 0);
           C = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[1][1], bop[m][1][1], C, 0, 0, 0);
-          // C = 16 * isum exactly (|C| < 2^21)
-          acc[mt][m][0] = fmaf(sf[m] * d4.x, (float)(C[0] >> 4), acc[mt][m][0]);
-          acc[mt][m][1] = fmaf(sf[m] * d4.y, (float)(C[1] >> 4), acc[mt][m][1]);
-          acc[mt][m][2] = fmaf(sf[m] * d4.z, (float)(C[2] >> 4), acc[mt][m][2]);
-          acc[mt][m][3] = fmaf(sf[m] * d4.w, (float)(C[3] >> 4), acc[mt][m][3]);
+          // C = 16 * isum exactly (|C| < 2^21, so (float)C is exact too)
+          acc[mt][m][0] = fmaf(sf[m] * d4.x, (float)C[0], acc[mt][m][0]);
+          acc[mt][m][1] = fmaf(sf[m] * d4.y, (float)C[1], acc[mt][m][1]);
+          acc[mt][m][2] = fmaf(sf[m] * d4.z, (float)C[2], acc[mt][m][2]);
+          acc[mt][m][3] = fmaf(sf[m] * d4.w, (float)C[3], acc[mt][m][3]);
         }
+        // one token sub-tile's operands live at a time: 153 instead of 172 registers,
+        // three workgroups per CU instead of two
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
     // output: token tile row mt*16 + 4g + v, weight row orow
@@ -835,10 +888,12 @@ __device__ __forceinline__ void t1_down_wg(const MoeArgs& A, float* __restrict__
   const int nblk = TOPK * kb;
   const int row0 = (wg * WAVES + wv) * RPW;
   int64_t ej[TOPK];
+  float wj[TOPK];  // routing weights, loaded now: in the combine each would be a round trip
   unsigned vmask = 0;
 #pragma unroll
   for (int j = 0; j < TOPK; ++j) {
     const int e = A.topk_idx[j];
+    wj[j] = A.topk_w[j];
     const bool v = e >= 0 && e < A.n_experts;
     vmask |= (unsigned)v << j;
     ej[j] = v ? e : 0;
@@ -931,7 +986,7 @@ __device__ __forceinline__ void t1_down_wg(const MoeArgs& A, float* __restrict__
     for (int j = 0; j < TOPK; ++j) {
       if (!((vmask >> j) & 1)) continue;
       const float y = sy[j * RPW + lane];
-      acc = fmaf(A.topk_w[j], y, acc);
+      acc = fmaf(wj[j], y, acc);
       A.yd[(int64_t)j * H + row0 + lane] = y;
     }
     out[row0 + lane] = acc;
