@@ -266,7 +266,8 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
 
 // One group of NT tokens (list positions c0 .. c0 + NT - 1) as the lane needs it: their
 // slots, their 32 activation codes per load, and the block scales of the lane's kept
-// items (zero past the list or past kb). Positions past the list repeat the last one.
+// items (as loaded: the compute zeroes those past the list or past kb, so that no use of
+// a loaded value sits among the loads). Positions past the list repeat the last one.
 template <int NMAT, int NL, int RPW, int NT>
 struct TbActs {
   static constexpr int KI = RowReduce<RPW * NT, NMAT>::KI;
@@ -302,13 +303,10 @@ __device__ __forceinline__ void tb_acts_load(const MoeArgs& A, __amdgpu_buffer_r
     int ar = arow[0];
 #pragma unroll
     for (int u = 1; u < NT; ++u) ar = tt == u ? arow[u] : ar;
-    const bool tv = c0 + tt < cnt;
 #pragma unroll
     for (int i = 0; i < NL; ++i) {
-      const int b = 8 * i + g;
-      const uint32_t bc = (uint32_t)min(b, kb - 1);
-      const float dv = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(dr, ((uint32_t)ar * (uint32_t)kb + bc) * 4u, 0, 0));
-      T.d[k][i] = (tv && (!RAGGED || b < kb)) ? dv : 0.0f;
+      const uint32_t bc = (uint32_t)min(8 * i + g, kb - 1);
+      T.d[k][i] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(dr, ((uint32_t)ar * (uint32_t)kb + bc) * 4u, 0, 0));
     }
   }
 }
@@ -317,15 +315,24 @@ __device__ __forceinline__ void tb_acts_load(const MoeArgs& A, __amdgpu_buffer_r
 // unpacked (wc[m * RPW + r][i]) with the scales of its own row (sl[m][i]: after the
 // block butterfly a lane keeps items of one row, rev(lane bits) for RPW <= 8). Items are
 // (row r, token tt) = r * NT + tt, each for the NMAT matrices.
-template <int NMAT, int NL, int RPW, int NT>
+template <int NMAT, int NL, int RPW, int NT, bool RAGGED>
 __device__ __forceinline__ void tb_acts_compute(const MoeArgs& A, const int (&wc)[NMAT * RPW][NL][8],
                                                 const float (&sl)[NMAT][NL], const TbActs<NMAT, NL, RPW, NT>& T, int N,
-                                                int cnt, int c0, int row0, int lane) {
+                                                int kb, int cnt, int c0, int row0, int lane) {
   using RR = RowReduce<RPW * NT, NMAT>;
   constexpr int KI = RR::KI;
+  const int g = lane >> 3;
   float acc[KI * NMAT];
 #pragma unroll
   for (int v = 0; v < KI * NMAT; ++v) acc[v] = 0.0f;
+  // a kept item's block scale, zero for a token past the list or a block past kb
+  float dk[KI][NL];
+#pragma unroll
+  for (int k = 0; k < KI; ++k) {
+    const bool tv = c0 + RR::kept(k, lane) % NT < cnt;
+#pragma unroll
+    for (int i = 0; i < NL; ++i) dk[k][i] = (tv && (!RAGGED || 8 * i + g < kb)) ? T.d[k][i] : 0.0f;
+  }
 #pragma unroll
   for (int i = 0; i < NL; ++i) {
     int p[RPW * NT * NMAT];
@@ -340,7 +347,7 @@ __device__ __forceinline__ void tb_acts_compute(const MoeArgs& A, const int (&wc
     for (int k = 0; k < KI; ++k)
 #pragma unroll
       for (int m = 0; m < NMAT; ++m)
-        acc[k * NMAT + m] = fmaf(sl[m][i] * T.d[k][i], (float)(p[k * NMAT + m] >> 4), acc[k * NMAT + m]);
+        acc[k * NMAT + m] = fmaf(sl[m][i] * dk[k][i], (float)(p[k * NMAT + m] >> 4), acc[k * NMAT + m]);
   }
   RR::block_totals(acc);
   if (RR::writer(lane)) {
@@ -379,7 +386,7 @@ __device__ __forceinline__ TbTask tb_task(int v, int task, int tiles) {
 // before), so that their round trip overlaps the weights' (most tasks have a single
 // group); then the next task's slots; further groups load and compute in turn (the last
 // one possibly part-empty).
-template <int NMAT, int NL, int RPW, int NT, int WAVES, bool RAGGED>
+template <int NMAT, int NL, int RPW, int NT, int NTL, int WAVES, bool RAGGED>
 __global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
   static_assert(RPW <= 8 && (RPW & (RPW - 1)) == 0, "RPW: a power of two <= 8");
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -454,11 +461,11 @@ __global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
 #pragma unroll
         for (int i = 0; i < NL; ++i) sl[m][i] = f16_bits_to_f32(sr[m][i]);
     }
-    tb_acts_compute<NMAT, NL, RPW, NF>(A, wc, sl, first, N, cnt, 0, row0, lane);
-    for (int c0 = NF; c0 < cnt; c0 += NF) {
-      TbActs<NMAT, NL, RPW, NF> grp;
-      tb_acts_load<NMAT, NL, RPW, NF, RAGGED>(A, qr, dr, K, kb, sv, off, cnt, c0, lane, g, cp, grp);
-      tb_acts_compute<NMAT, NL, RPW, NF>(A, wc, sl, grp, N, cnt, c0, row0, lane);
+    tb_acts_compute<NMAT, NL, RPW, NF, RAGGED>(A, wc, sl, first, N, kb, cnt, 0, row0, lane);
+    for (int c0 = NF; c0 < cnt; c0 += NTL) {
+      TbActs<NMAT, NL, RPW, NTL> grp;
+      tb_acts_load<NMAT, NL, RPW, NTL, RAGGED>(A, qr, dr, K, kb, sv, off, cnt, c0, lane, g, cp, grp);
+      tb_acts_compute<NMAT, NL, RPW, NTL, RAGGED>(A, wc, sl, grp, N, kb, cnt, c0, row0, lane);
     }
     tv = tv_next;
     sv = sv_next;
@@ -1025,7 +1032,14 @@ static moe_fn pick_tb_nl() {
   // tokens per group: pairs, single tokens where a pair's activations would crowd the
   // registers that hold the weights
   constexpr int NT = NL <= 2 ? 2 : 1;
-  return k_tb<NMAT, NL, RPW, NT, kTbWaves, R>;
+#ifndef TQ_TB_NTL2
+#define TQ_TB_NTL2 2
+#endif
+#ifndef TQ_TB_NTL4
+#define TQ_TB_NTL4 1
+#endif
+  constexpr int NTL = NL <= 2 ? TQ_TB_NTL2 : (NL <= 4 ? TQ_TB_NTL4 : 1);
+  return k_tb<NMAT, NL, RPW, NT, NTL, kTbWaves, R>;
 }
 
 template <int NMAT, bool R>
