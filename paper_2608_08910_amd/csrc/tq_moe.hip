@@ -22,6 +22,8 @@
 
 #include <algorithm>
 
+#include <type_traits>
+
 #include "tq_device.hpp"
 #include "tq_internal.hpp"
 
@@ -38,12 +40,14 @@ enum Ctrl {
   kCtrlWords = 64
 };
 
-constexpr int kMT = 64;  // tokens per MFMA tile (four 16-row MFMA tiles)
-constexpr int kMN = 64;  // weight rows per MFMA workgroup (four waves x 16)
+constexpr int kMT = 128;     // tokens per MFMA task tile (eight 16-row MFMA tiles)
+constexpr int kMWaves = 8;   // waves per MFMA workgroup, 16 weight rows each
+constexpr int kMN = 16 * kMWaves;  // weight rows per MFMA task tile
+constexpr int kMStages = 3;  // token-tile blocks in flight in LDS per MFMA workgroup
 constexpr int64_t kMfmaMinSlots = 1024;  // automatic path choice: MFMA from this many slots
 
 struct Layout {
-  size_t ctrl, active, act_off, tt_off, slot_list, xq, xd, xb, h, hq, hd, hb, yd, total;
+  size_t ctrl, active, act_off, tt_off, tile_exp, slot_list, xq, xd, xb, h, hq, hd, hb, yd, total;
 };
 
 static size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -61,6 +65,7 @@ static Layout make_layout(int n_experts, int hidden, int inter, int64_t t, int t
   L.active = take((size_t)n_experts * 4);
   L.act_off = take(((size_t)n_experts + 1) * 4);
   L.tt_off = take(((size_t)n_experts + 1) * 4);
+  L.tile_exp = take((S / kMT + (size_t)n_experts + 1) * 4);
   L.slot_list = take(S * 4);
   L.xq = take((size_t)t * hidden);
   L.xd = take((size_t)t * (hidden / 256) * 4);
@@ -131,6 +136,7 @@ struct MoeArgs {
   int32_t* active;
   int32_t* act_off;
   int32_t* tt_off;  // per active expert: first token tile (kMT tokens) of the MFMA path
+  int32_t* tile_exp;  // per token tile of the MFMA path: its active expert's rank
   int32_t* slot_list;
   int8_t* xq;
   float* xd;
@@ -225,7 +231,7 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
     A.tt_off[r] = tpos;
     s_base[e] = pos;  // rank no longer needed: becomes the expert's slot cursor
     pos += s_cnt[e];
-    tpos += (s_cnt[e] + kMT - 1) / kMT;
+    for (const int t1 = tpos + (s_cnt[e] + kMT - 1) / kMT; tpos < t1; ++tpos) A.tile_exp[tpos] = r;
   }
   if (tid == 255) {
     const int n_valid = s_scan[255], n_tiles = s_scan2[255];
@@ -515,91 +521,124 @@ __global__ __launch_bounds__(256) void k_moe_combine(MoeArgs A, float* __restric
 
 // ---------------------------------------------------------------------------------
 // Many tokens per expert (prefill-sized groups): the per-expert contraction is a dense
-// int8 GEMM, run on v_mfma_i32_16x16x64_i8. A workgroup owns one task: kMT tokens of one
-// active expert x kMN weight rows (x2 matrices for gate/up). Per 256-column block:
-//  - the token tile's codes are staged in LDS (double-buffered, rows padded to 272 bytes
-//    so the 16 lanes of an operand read hit distinct banks) with their d;
-//  - each wave unpacks its 16 weight rows' nibbles to 16c bytes as B operands (lane: row l & 15,
-//    chunk 4t + (l >> 4), half h gives MFMA (t, h); the A operand takes the same 16
-//    columns of the token's codes, so every product pairs matching columns);
+// int8 GEMM, run on v_mfma_i32_16x16x64_i8. A workgroup of kMWaves waves owns one task:
+// kMT tokens of one active expert x kMN weight rows (x2 matrices for gate/up); wave w
+// owns rows 16w .. 16w + 15 of the tile for all kMT tokens. The block scales of the
+// tile's tokens go to LDS once per task. Per 256-column block:
+//  - the token tile's codes (kMT x 256 bytes) travel by direct-to-LDS loads into a ring
+//    of kMStages stages, kMStages - 1 blocks ahead of the compute; 16-byte column c of
+//    row r sits at column c ^ (r & 15), so the 16 lanes that read one operand column of
+//    16 rows hit distinct banks;
+//  - each wave loads its 16 rows' nibbles kMStages - 1 blocks ahead into registers and
+//    unpacks them to 16c bytes as the B operands (lane: row l & 15, chunk 4t + (l >> 4),
+//    half h gives MFMA (t, h); the A operand takes the same 16 columns of the token's
+//    codes, so every product pairs matching columns);
 //  - four MFMAs per 16x16 output tile accumulate sum (16c)*q = 16 * isum exactly, and one
-//    fp32 multiply-add per output applies f32(s) * d to isum.
-// Tasks are ranked hottest expert first with token tiles innermost, so the workgroups
-// that read one weight tile run together and share it through L2.
+//    fp32 multiply-add per output applies (f32(s) / 16) * d to it; 16-token sub-tiles
+//    past the expert's last token are skipped.
+// Tasks run hottest expert first, row tiles innermost: the workgroups running together
+// share a token tile through L2, and the tasks of one weight tile run RT tasks apart.
 // ---------------------------------------------------------------------------------
 
 typedef int v4i __attribute__((ext_vector_type(4)));
-constexpr int kAStride = 272;
+typedef __attribute__((address_space(3))) void* lds_ptr;
+
+// A wave-uniform read of data that no kernel still running writes (here: the prologue's
+// control data), through the constant address space, so that it is a scalar load.
+template <typename T>
+__device__ __forceinline__ T ld_uniform(const T* p) {
+  return *reinterpret_cast<const __attribute__((address_space(4))) T*>(reinterpret_cast<uintptr_t>(p));
+}
 
 __device__ __forceinline__ v4i lds_v4i(const int8_t* p) {
   const int4 v = *reinterpret_cast<const int4*>(p);
   return v4i{v.x, v.y, v.z, v.w};
 }
 
-// One block's loads for the MFMA kernel: this thread's 64-byte quarter of a token row,
-// the token's block scale, and the lane's two 16-byte code chunks (and scale) of each
-// weight matrix.
+// s_waitcnt with only the vector-memory count constrained (gfx9 encoding: vmcnt in bits
+// 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt out of range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// One block's weights for one wave: the lane's two 16-byte code chunks and its row's
+// scale, per matrix.
 template <int NMAT>
-struct MfmaStage {
-  v4i a0, a1, a2, a3;
+struct MfmaB {
   uint4 w[NMAT][2];
   uint16_t s[NMAT];
-  float d;
 };
 
 template <int NMAT>
-__device__ __forceinline__ void mfma_fetch(MfmaStage<NMAT>& st, const v4i* qrow, const float* dsrc, int64_t arow,
-                                           const MatRsrc (&mr)[NMAT], int wrow, int kb, int g, int b) {
-  st.a0 = qrow[b * 16 + 0];
-  st.a1 = qrow[b * 16 + 1];
-  st.a2 = qrow[b * 16 + 2];
-  st.a3 = qrow[b * 16 + 3];
-  st.d = dsrc[arow * kb + b];
+__device__ __forceinline__ void mfma_b_fetch(MfmaB<NMAT>& B, const MatRsrc (&mr)[NMAT], int wrow, int kb, int g, int b) {
 #pragma unroll
   for (int m = 0; m < NMAT; ++m) {
 #pragma unroll
     for (int c = 0; c < 2; ++c)
-      st.w[m][c] = buf_load16(mr[m].codes, (uint32_t)((wrow * kb + b) * 128 + (4 * c + g) * 16), 0);
-    st.s[m] = buf_load_u16(mr[m].scales, (uint32_t)((wrow * kb + b) * 2), 0);
+      B.w[m][c] = buf_load16(mr[m].codes, (uint32_t)((wrow * kb + b) * 128 + (4 * c + g) * 16), 0);
+    B.s[m] = buf_load_u16(mr[m].scales, (uint32_t)((wrow * kb + b) * 2), 0);
   }
 }
 
+// Piece j of block b of the token tile into one ring stage: 1 KB of codes, rows
+// 4 (4w + j) .. + 3 (ap: the lane's source for this piece at block 0).
+__device__ __forceinline__ void mfma_a_dma(int8_t* sa, const int8_t* ap, int b, int wv, int j) {
+  __builtin_amdgcn_global_load_lds((const void*)(ap + b * 256), (lds_ptr)(sa + (wv * 4 + j) * 1024), 16, 0, 0);
+}
+
+// Per block and wave: four code pieces and three loads per matrix.
+template <int NMAT>
+constexpr int kMfmaLoadsPerBlock = 4 + 3 * NMAT;
+
 template <int NMAT>  // 2: gate and up, h = SiLU(g) * u; 1: down, y per slot
-__global__ __launch_bounds__(256) void k_moe_mfma(MoeArgs A) {
-  __shared__ __attribute__((aligned(16))) int8_t s_a[2][kMT * kAStride];
-  __shared__ __attribute__((aligned(16))) float s_d[2][kMT];
+__global__ __launch_bounds__(kMWaves * 64) void k_moe_mfma(MoeArgs A) {
+  // one variable per ring stage, and stages chosen at compile time, so that the compiler
+  // can tell a stage being filled from the one being read and does not wait for the fill
+  __shared__ __attribute__((aligned(16))) int8_t s_a0[kMT * 256], s_a1[kMT * 256], s_a2[kMT * 256];
+  __shared__ __attribute__((aligned(16))) float s_dall[(kMaxK / 256) * kMT];  // [block][token]
   __shared__ int s_slot[kMT];
+  static_assert(kMT == 128 && kMN == 16 * kMWaves && kMWaves == 8 && kMStages == 3, "tile geometry");
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int li = lane & 15, g = lane >> 4;
   const int K = NMAT == 2 ? A.hidden : A.inter;
   const int N = NMAT == 2 ? A.inter : A.hidden;
   const int kb = K / 256;
   const int RT = NMAT == 2 ? A.tiles_mgu : A.tiles_mdn;
-  const int n_active = A.ctrl[kNActive];
-  const int n_tasks = A.ctrl[NMAT == 2 ? kTasksMGU : kTasksMDn];
+  const int n_tasks = ld_uniform(A.ctrl + (NMAT == 2 ? kTasksMGU : kTasksMDn));
   const int8_t* qsrc = NMAT == 2 ? A.xq : A.hq;
   const float* dsrc = NMAT == 2 ? A.xd : A.hd;
-  const int tt = threadIdx.x >> 2, part = threadIdx.x & 3;  // staging: token row, 64-byte quarter
   for (int task = blockIdx.x; task < n_tasks; task += gridDim.x) {
-    // active expert a with tt_off[a] * RT <= task < tt_off[a + 1] * RT
-    int lo = 0, hi = n_active - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (A.tt_off[mid] * RT <= task) lo = mid;
-      else hi = mid - 1;
-    }
-    const int a = lo;
-    const int ntt = A.tt_off[a + 1] - A.tt_off[a];
-    const int local = task - A.tt_off[a] * RT;
-    const int rtile = local / ntt, ttile = local - rtile * ntt;
-    const int64_t e = A.active[a];
-    const int off = A.act_off[a], cnt = A.act_off[a + 1] - off;
+    // task = tile * RT + rtile: token tile `tile` (of active expert a) x row tile; the
+    // control data was written by the prologue kernel, so it is read through the scalar
+    // cache (not queued behind this compute unit's vector loads)
+    const int tile = task / RT, rtile = task - tile * RT;
+    const int a = ld_uniform(A.tile_exp + tile);
+    const int ttile = tile - ld_uniform(A.tt_off + a);
+    const int64_t e = ld_uniform(A.active + a);
+    const int off = ld_uniform(A.act_off + a), cnt = ld_uniform(A.act_off + a + 1) - off;
     const int m0 = ttile * kMT, nvalid = min(kMT, cnt - m0);
-    __syncthreads();  // the previous task's readers of s_slot and s_a are done
+    __syncthreads();  // the previous task is done with the ring and s_slot
     if (threadIdx.x < kMT) s_slot[threadIdx.x] = A.slot_list[off + m0 + min((int)threadIdx.x, nvalid - 1)];
     __syncthreads();
-    const int64_t arow = NMAT == 2 ? (int64_t)(s_slot[tt] / A.topk) : (int64_t)s_slot[tt];
-    const v4i* qrow = reinterpret_cast<const v4i*>(qsrc + arow * K + part * 64);  // per-lane row: plain loads
+    // the lane's direct-to-LDS sources: piece j covers rows 4 (4w + j) .. + 3, the lane
+    // row 4 (4w + j) + (l >> 4) at stored column l & 15, i.e. source column (l & 15) ^ (r & 15)
+    const int8_t* ap[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = (wv * 4 + j) * 4 + (lane >> 4);
+      const int sl = s_slot[r];
+      const int64_t arow = NMAT == 2 ? (int64_t)(sl / A.topk) : (int64_t)sl;
+      ap[j] = qsrc + arow * K + (((lane & 15) ^ (r & 15)) * 16);
+    }
+    // every block scale of the tile's tokens, once per task
+    for (int i = threadIdx.x; i < kMT * kb; i += kMWaves * 64) {
+      const int t = i / kb, b = i - t * kb, sl = s_slot[t];
+      s_dall[b * kMT + t] = dsrc[(NMAT == 2 ? (int64_t)(sl / A.topk) : (int64_t)sl) * kb + b];
+    }
+    __syncthreads();
+    const int nsub = (nvalid + 15) / 16;  // 16-token sub-tiles holding valid tokens
     const int wrow = min(rtile * kMN + wv * 16 + li, N - 1);
     MatRsrc mr[NMAT];
 #pragma unroll
@@ -607,50 +646,69 @@ __global__ __launch_bounds__(256) void k_moe_mfma(MoeArgs A) {
       const int p = NMAT == 2 ? m : 2;
       mr[m] = mat_rsrc(A.codes[p] + e * A.stride_codes[p], A.scales[p] + e * A.stride_scales[p], N, kb);
     }
-    float acc[4][NMAT][4];
+    float acc[kMT / 16][NMAT][4];
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
+    for (int mt = 0; mt < kMT / 16; ++mt)
 #pragma unroll
       for (int m = 0; m < NMAT; ++m)
 #pragma unroll
         for (int v = 0; v < 4; ++v) acc[mt][m][v] = 0.0f;
 
-    MfmaStage<NMAT> st;
-    mfma_fetch<NMAT>(st, qrow, dsrc, arow, mr, wrow, kb, g, 0);
-    for (int b = 0; b < kb; ++b) {
-      const int buf = b & 1;
-      v4i* dst = reinterpret_cast<v4i*>(s_a[buf] + tt * kAStride + part * 64);
-      dst[0] = st.a0;
-      dst[1] = st.a1;
-      dst[2] = st.a2;
-      dst[3] = st.a3;
-      if (part == 0) s_d[buf][tt] = st.d;
-      // this block's weights unpacked to 16c bytes (the B operands) and its scales / 16
-      // (the MFMA sums 16c * q = 16 isum; dividing the f16 scale by 16 is exact), before
-      // the stage registers take the next block's loads
+    // blocks 0 and 1 in flight; then per block b: wait until only block b + 1's loads may
+    // be outstanding (loads complete in issue order), unpack block b's weights, barrier
+    // (every wave's piece of block b is in LDS, and stage (b + 2) % 3 is no longer read),
+    // issue block b + 2, compute block b.
+    // Block b uses stage b % 3 and weight registers b % 2: the loop runs six blocks a turn.
+    MfmaB<NMAT> B0, B1;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) mfma_a_dma(s_a0, ap[j], 0, wv, j);
+    mfma_b_fetch<NMAT>(B0, mr, wrow, kb, g, 0);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) mfma_a_dma(s_a1, ap[j], min(1, kb - 1), wv, j);
+    mfma_b_fetch<NMAT>(B1, mr, wrow, kb, g, min(1, kb - 1));
+    const auto step = [&](int b, auto stage_c, MfmaB<NMAT>& Bs) {
+      constexpr int ST = decltype(stage_c)::value, NS = (ST + 2) % 3;
+      const int8_t* const sa = ST == 0 ? s_a0 : (ST == 1 ? s_a1 : s_a2);
+      int8_t* const na = NS == 0 ? s_a0 : (NS == 1 ? s_a1 : s_a2);
+      const float* const sd = s_dall + b * kMT;
+      wait_vmcnt<kMfmaLoadsPerBlock<NMAT>>();  // this wave's pieces of block b are in LDS
       float sf[NMAT];
       v4i bop[NMAT][2][2];
 #pragma unroll
       for (int m = 0; m < NMAT; ++m) {
-        sf[m] = f16_bits_to_f32(st.s[m]) * 0.0625f;
+        // the MFMA sums 16c * q = 16 isum; dividing the f16 scale by 16 is exact
+        sf[m] = f16_bits_to_f32(Bs.s[m]) * 0.0625f;
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
-          const uint4 w = st.w[m][c];
+          const uint4 w = Bs.w[m][c];
           bop[m][c][0] = v4i{lo16c(w.x), lo16c(w.y), lo16c(w.z), lo16c(w.w)};
           bop[m][c][1] = v4i{hi16c(w.x), hi16c(w.y), hi16c(w.z), hi16c(w.w)};
         }
       }
-      if (b + 1 < kb) mfma_fetch<NMAT>(st, qrow, dsrc, arow, mr, wrow, kb, g, b + 1);
-      __syncthreads();
+      // A bare barrier: __syncthreads' release fence would also wait for the loads in
+      // flight for the blocks ahead. The wait above covers this wave's part of block b;
+      // its LDS reads of the previous block were consumed (waited for) by its MFMAs; the
+      // signal fences keep the compiler from moving memory accesses across the barrier.
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      __builtin_amdgcn_s_barrier();
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      // block b + 2 is issued among the sub-tiles' MFMAs, so that the eight waves' loads
+      // do not queue up at once; unconditional, so that every path has the same loads in
+      // flight (past the last block: block kb - 1 again, into a stage and registers no
+      // longer read)
+      const int nb = min(b + 2, kb - 1);
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) {
-        const int8_t* arow_lds = s_a[buf] + (mt * 16 + li) * kAStride;
+      for (int mt = 0; mt < kMT / 16; ++mt) {
+        if (mt < 4) mfma_a_dma(na, ap[mt], nb, wv, mt);
+        if (mt == 4) mfma_b_fetch<NMAT>(Bs, mr, wrow, kb, g, nb);
+        if (mt >= nsub) continue;  // no valid token in this sub-tile
+        const int8_t* arow_lds = sa + (mt * 16 + li) * 256;
         v4i aop[2][2];
 #pragma unroll
         for (int c = 0; c < 2; ++c)
 #pragma unroll
-          for (int h = 0; h < 2; ++h) aop[c][h] = lds_v4i(arow_lds + 32 * (4 * c + g) + 16 * h);
-        const float4 d4 = *reinterpret_cast<const float4*>(&s_d[buf][mt * 16 + 4 * g]);
+          for (int h = 0; h < 2; ++h) aop[c][h] = lds_v4i(arow_lds + (((2 * (4 * c + g) + h) ^ li) * 16));
+        const float4 d4 = *reinterpret_cast<const float4*>(&sd[mt * 16 + 4 * g]);
 #pragma unroll
         for (int m = 0; m < NMAT; ++m) {
           v4i C = v4i{0, 0, 0, 0};
@@ -664,16 +722,32 @@ __global__ __launch_bounds__(256) void k_moe_mfma(MoeArgs A) {
           acc[mt][m][2] = fmaf(sf[m] * d4.z, (float)C[2], acc[mt][m][2]);
           acc[mt][m][3] = fmaf(sf[m] * d4.w, (float)C[3], acc[mt][m][3]);
         }
-        // one token sub-tile's operands live at a time: 153 instead of 172 registers,
-        // three workgroups per CU instead of two
-        __builtin_amdgcn_sched_barrier(0);
       }
+    };
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    // (a step is reached only through the one before it, and the loop repeats only
+    // after its sixth, so that the compiler sees the same loads in flight on every path)
+    for (int b = 0;; b += 6) {
+      step(b, I0{}, B0);
+      if (b + 1 >= kb) break;
+      step(b + 1, I1{}, B1);
+      if (b + 2 >= kb) break;
+      step(b + 2, I2{}, B0);
+      if (b + 3 >= kb) break;
+      step(b + 3, I0{}, B1);
+      if (b + 4 >= kb) break;
+      step(b + 4, I1{}, B0);
+      if (b + 5 >= kb) break;
+      step(b + 5, I2{}, B1);
+      if (b + 6 >= kb) break;
     }
     // output: token tile row mt*16 + 4g + v, weight row orow
     const int orow = rtile * kMN + wv * 16 + li;
     if (orow < N) {
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
+      for (int mt = 0; mt < kMT / 16; ++mt)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const int t = mt * 16 + 4 * g + v;
@@ -1235,6 +1309,7 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   A.active = reinterpret_cast<int32_t*>(base + L.active);
   A.act_off = reinterpret_cast<int32_t*>(base + L.act_off);
   A.tt_off = reinterpret_cast<int32_t*>(base + L.tt_off);
+  A.tile_exp = reinterpret_cast<int32_t*>(base + L.tile_exp);
   A.slot_list = reinterpret_cast<int32_t*>(base + L.slot_list);
   A.xq = reinterpret_cast<int8_t*>(base + L.xq);
   A.xd = reinterpret_cast<float*>(base + L.xd);
@@ -1283,16 +1358,19 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   A.tiles_mgu = (ex->inter + kMN - 1) / kMN;
   A.tiles_mdn = (ex->hidden + kMN - 1) / kMN;
   const int64_t max_tiles = S / kMT + max_active;
-  const unsigned g_mgu = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mgu, cap);
-  const unsigned g_mdn = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mdn, cap);
+#ifndef TQ_MFMA_GRID
+#define TQ_MFMA_GRID (256 * 16)
+#endif
+  const unsigned g_mgu = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mgu, TQ_MFMA_GRID);
+  const unsigned g_mdn = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mdn, TQ_MFMA_GRID);
   if ((st = launch_stage(events, 0, k_moe_prologue, dim3(nq + 1), 256, stm, fn, x, A, nq)) != TQ_OK) return st;
-  if (mfma) st = launch_stage(events, 1, k_moe_mfma<2>, dim3(g_mgu), 256, stm, fn, A);
+  if (mfma) st = launch_stage(events, 1, k_moe_mfma<2>, dim3(g_mgu), kMWaves * 64, stm, fn, A);
   else st = launch_stage(events, 1, pick_tb<2>(ex->hidden / 256), dim3(g_gu), kTbWaves * 64, stm, fn, A);
   if (st != TQ_OK) return st;
   if ((st = launch_stage(events, 2, k_moe_requant, dim3((unsigned)((hblocks + 31) / 32)), 256, stm, fn, A, hblocks)) !=
       TQ_OK)
     return st;
-  if (mfma) st = launch_stage(events, 3, k_moe_mfma<1>, dim3(g_mdn), 256, stm, fn, A);
+  if (mfma) st = launch_stage(events, 3, k_moe_mfma<1>, dim3(g_mdn), kMWaves * 64, stm, fn, A);
   else st = launch_stage(events, 3, pick_tb<1>(ex->inter / 256), dim3(g_dn), kTbWaves * 64, stm, fn, A);
   if (st != TQ_OK) return st;
   const int64_t nout = t * (ex->hidden / 4);

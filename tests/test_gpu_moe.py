@@ -193,7 +193,7 @@ def test_moe_prefill_2048_sampled(tq, oracle, experts_h4096):
 @pytest.mark.parametrize("E,H,I,T,topk", [(5, 512, 768, 150, 3), (4, 1280, 256, 70, 2)])
 def test_moe_mfma_forced_small(tq, oracle, E, H, I, T, topk):
     """The int8 MFMA expert path on host-packed experts: one expert spans several
-    64-token tiles, hidden/inter give ragged row tiles and odd block counts."""
+    128-token tiles, hidden/inter give ragged row tiles and odd block counts (1 to 5)."""
     ex, logical = host_experts(tq, oracle, E, H, I, seed=21)
     rng = np.random.default_rng(22)
     x = (rng.standard_normal((T, H)) * np.exp(rng.uniform(-2, 2, (T, 1)))).astype(np.float32)
