@@ -12,6 +12,9 @@ Definitions followed (paper sections):
                              rounding rule are this oracle's stated reading)
   integer dot + combine .... Sec. 2.2 (one integer dot pass, one float multiply-add
                              per block), evaluated exactly / in fp64
+  tied solver .............. Sec. 2.1 (alternating code and scale updates against one
+                             scale per group; start, stop rule and precision are this
+                             oracle's stated reading)
   routed-expert layer ...... gate/up/down projections of the routed experts (Sec. 1,
                              Sec. 2.1: 43 layers x 3 projections x 256 experts); the
                              layer's glue (SiLU(gate)*up, requantized hidden, softmax-
@@ -60,6 +63,8 @@ class Oracle:
             ("orc_gemv", [_vp, _vp, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _vp], ctypes.c_int),
             ("orc_splitmix64_word", [ctypes.c_uint64, ctypes.c_uint64], ctypes.c_uint64),
             ("orc_synth_matrix", [ctypes.c_uint64, _i64, _i64, _i64, _i64, _vp, _vp, _vp], ctypes.c_int),
+            ("orc_f32_to_f16", [ctypes.c_float], ctypes.c_uint16),
+            ("orc_tied_quantize", [_vp, _i64, _i64, ctypes.c_int, _vp, _vp, _vp], ctypes.c_int),
         ]:
             f = getattr(L, name)
             f.argtypes = args
@@ -146,6 +151,21 @@ class Oracle:
         return (y, a, isum) if want_isum else (y, a)
 
     # -- synthetic weights (input generation; SplitMix64 counter stream) -------------
+    # -- tied solver (Sec. 2.1) ---------------------------------------------------------
+    def f32_to_f16(self, x: float) -> int:
+        return int(self._L.orc_f32_to_f16(ctypes.c_float(x)))
+
+    def tied_quantize(self, w, max_iter: int = 16):
+        """W [n][k] fp32 -> (codes int8 [n][k] in -4..4, f16 scale bits [n][k/256],
+        code steps taken per block)."""
+        w = np.ascontiguousarray(w, dtype=np.float32)
+        n, k = w.shape
+        c = np.empty((n, k), dtype=np.int8)
+        s = np.empty((n, k // 256), dtype=np.uint16)
+        it = np.empty((n, k // 256), dtype=np.uint8)
+        self._check(self._L.orc_tied_quantize(_p(w), n, k, max_iter, _p(c), _p(s), _p(it)), "tied_quantize")
+        return c, s, it
+
     def splitmix64_word(self, key: int, i: int) -> int:
         return int(self._L.orc_splitmix64_word(key & (2**64 - 1), i))
 

@@ -243,3 +243,117 @@ int orc_synth_matrix(uint64_t key, int64_t n, int64_t k, int64_t row0, int64_t r
   }
   return ORC_OK;
 }
+
+/* ------------------------------------------------------------------------------ */
+/* Tied solver (Sec. 2.1, first paragraph): with the plane scales tied at           */
+/* alpha = (3s, s), fitting W ~ alpha1*T1 + alpha2*T2 by alternating plane and scale */
+/* updates is fitting the uniform nine-level quantizer W_hat = s*c, c in -4..4, per  */
+/* group of weights. Groups here are the format's 256-weight blocks (one scale per   */
+/* row and 256 columns, Sec. 2.2). The paper gives neither the start, the stopping   */
+/* rule nor the precision; the reading implemented (each half-step is the exact      */
+/* minimizer of the squared error given the other half):                           */
+/*  - amax = max |w|; a block with amax < 2^-100 (all-zero included) gets s = 0, c = 0;*/
+/*  - start s = amax / 4 (the largest weight on the outermost level);               */
+/*  - code step:  c_i = clamp(rne(fl32(w_i / s)), -4, 4), IEEE fp32 division;        */
+/*  - scale step: s = fl32(<w, c> / <c, c>), <c, c> an exact integer, <w, c> summed   */
+/*    in fp64 (the products are exact) by pairwise halving: v[i] += v[i + h] for      */
+/*    h = 128, 64, ..., 1, so that any implementation following the same order makes  */
+/*    the same decisions;                                                            */
+/*  - stop when a code step reproduces the previous codes (then the scale step would  */
+/*    reproduce s), or after max_iter code steps;                                    */
+/*  - the scale is stored as f16 (round to nearest even, saturating at 65504), and   */
+/*    the codes are the code step at the stored scale (all zero if it is 0).         */
+/* iters[block] = the number of code steps taken (0 for a zero block).                */
+/* ------------------------------------------------------------------------------ */
+
+/* fp32 -> binary16, round to nearest even, saturating to the largest finite value,
+ * from the format's definition (sign, 5-bit exponent with bias 15, 10-bit fraction;
+ * subnormals below 2^-14 in steps of 2^-24). Input finite. */
+uint16_t orc_f32_to_f16(float x) {
+  uint16_t sign = signbit(x) ? 0x8000 : 0;
+  double a = fabs((double)x);
+  if (a == 0.0) return sign;
+  int e;
+  frexp(a, &e); /* a = m * 2^e, 0.5 <= m < 1, so the leading bit has weight 2^(e-1) */
+  int ue = e - 1;
+  if (ue < -14) ue = -14; /* subnormal range: fixed step 2^-24 */
+  double step = ldexp(1.0, ue - 10);
+  double q = a / step;           /* exact: a power-of-two division */
+  double r = nearbyint(q);       /* round half to even (default rounding mode) */
+  double v = r * step;
+  if (v > 65504.0) v = 65504.0;  /* saturate (covers rounding up past the top binade) */
+  /* encode v (a representable value) */
+  if (v < ldexp(1.0, -14)) return (uint16_t)(sign | (uint16_t)(v / ldexp(1.0, -24)));
+  frexp(v, &e);
+  int be = e - 1 + 15;
+  uint16_t frac = (uint16_t)((v / ldexp(1.0, e - 1) - 1.0) * 1024.0);
+  return (uint16_t)(sign | (uint16_t)(be << 10) | frac);
+}
+
+static double pairwise_sum256(double* v) {
+  for (int h = 128; h >= 1; h /= 2)
+    for (int i = 0; i < h; ++i) v[i] = v[i] + v[i + h];
+  return v[0];
+}
+
+static void code_step(const float* w, float s, int8_t* c) {
+  for (int i = 0; i < 256; ++i) {
+    float t = w[i] / s;
+    float r = nearbyintf(t);
+    if (r > 4.0f) r = 4.0f;
+    if (r < -4.0f) r = -4.0f;
+    c[i] = (int8_t)r;
+  }
+}
+
+int orc_tied_quantize(const float* w, int64_t n, int64_t k, int max_iter, int8_t* c, uint16_t* s16,
+                      uint8_t* iters) {
+  if (k % 256 != 0 || max_iter < 1 || max_iter > 255) return ORC_BAD_INPUT;
+  const int64_t kb = k / 256;
+  for (int64_t r = 0; r < n; ++r) {
+    for (int64_t b = 0; b < kb; ++b) {
+      const float* wb = w + r * k + b * 256;
+      int8_t* cb = c + r * k + b * 256;
+      float amax = 0.0f;
+      for (int i = 0; i < 256; ++i) {
+        if (!isfinite(wb[i])) return ORC_BAD_INPUT;
+        if (fabsf(wb[i]) > amax) amax = fabsf(wb[i]);
+      }
+      if (!(amax >= 0x1p-100f)) {
+        for (int i = 0; i < 256; ++i) cb[i] = 0;
+        s16[r * kb + b] = 0;
+        if (iters) iters[r * kb + b] = 0;
+        continue;
+      }
+      float s = amax / 4.0f;
+      int8_t prev[256];
+      int it = 0;
+      for (;;) {
+        code_step(wb, s, cb);
+        ++it;
+        int same = it > 1;
+        for (int i = 0; i < 256 && same; ++i) same = cb[i] == prev[i];
+        if (same || it == max_iter) break;
+        double v[256];
+        int64_t cc = 0;
+        for (int i = 0; i < 256; ++i) {
+          v[i] = (double)wb[i] * (double)cb[i];
+          cc += (int64_t)cb[i] * cb[i];
+          prev[i] = cb[i];
+        }
+        if (cc == 0) break; /* not reached from the start above; kept as a guard */
+        s = (float)(pairwise_sum256(v) / (double)cc);
+      }
+      uint16_t h = orc_f32_to_f16(s);
+      s16[r * kb + b] = h;
+      if (iters) iters[r * kb + b] = (uint8_t)it;
+      float sd = (float)orc_f16_to_f64(h);
+      if (sd == 0.0f) {
+        for (int i = 0; i < 256; ++i) cb[i] = 0;
+      } else {
+        code_step(wb, sd, cb);
+      }
+    }
+  }
+  return ORC_OK;
+}

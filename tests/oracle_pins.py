@@ -433,3 +433,111 @@ def moe_invariants(o):
     # top-1 with weight 1 is the plain expert chain
     o1, _, st = o.moe(x[:1], idx[:1, :1], np.ones((1, 1), np.float32), lambda e: ex[e])
     assert np.array_equal(o1[0], st[(0, 0)]["yd"])
+
+
+# --------------------------------------------------------------------------------------
+# Tied solver (Sec. 2.1: alternating updates against one scale = fitting W_hat = s*c)
+# --------------------------------------------------------------------------------------
+
+def _sq_err(w, c, s16):
+    """Per-block squared error of s*c against w (fp64), [n][kb]."""
+    n, k = w.shape
+    sd = _f16_to_np64(s16)
+    d = w.astype(np.float64).reshape(n, k // 256, 256) - sd[:, :, None] * c.reshape(n, k // 256, 256)
+    return (d * d).sum(-1)
+
+
+@pin
+def f32_to_f16_matches_numpy(o):
+    rng = np.random.default_rng(51)
+    xs = (rng.standard_normal(4000) * 10.0 ** rng.uniform(-9, 4.8, 4000)).astype(np.float32)
+    xs = xs[np.abs(xs) < 65504]
+    # exact halfway cases between neighbouring f16 values, in normal and subnormal ranges
+    half = [1 + 2 ** -11, 1 + 3 * 2 ** -11, 2 ** -14 + 2 ** -25, 3 * 2 ** -25, 2 ** -25, 2048 + 1, 2048 + 3]
+    xs = np.concatenate([xs, np.array(half + [-h for h in half] + [65504.0, 65519.0, 0.0, -0.0], np.float32)])
+    for x in xs:
+        assert o.f32_to_f16(float(x)) == int(np.float32(x).astype(np.float16).view(np.uint16)), x
+    for x in (65520.0, 1e6, -70000.0):  # saturation (numpy would give inf)
+        assert o.f32_to_f16(x) == (0x7BFF | (0x8000 if x < 0 else 0))
+
+
+@pin
+def tied_recovers_exact_uniform_grid(o):
+    # W = s*c with an f16 scale and +-4 present: the start is exact and the first scale
+    # step reproduces it, so the codes, the scale and a two-step stop are all exact
+    rng = np.random.default_rng(52)
+    n, kb = 3, 4
+    c = rng.integers(-4, 5, (n, kb * 256)).astype(np.int8)
+    c[:, ::256] = 4 * np.where(rng.random((n, kb)) < 0.5, 1, -1)
+    s = _f16_to_np64(_f16(np.exp(rng.uniform(np.log(1e-3), np.log(10), (n, kb))))).astype(np.float32)
+    w = (np.repeat(s, 256, axis=1) * c).astype(np.float32)
+    cc, ss, it = o.tied_quantize(w)
+    assert np.array_equal(cc, c) and np.array_equal(ss, _f16(s)) and np.all(it == 2)
+
+
+@pin
+def tied_codes_are_the_best_levels_at_the_stored_scale(o):
+    rng = np.random.default_rng(53)
+    w = (rng.standard_normal((16, 4096)) * rng.uniform(0.01, 3, (16, 1))).astype(np.float32)
+    c, s16, _ = o.tied_quantize(w)
+    sd = np.repeat(_f16_to_np64(s16), 256, axis=1)
+    e = (w.astype(np.float64) - sd * c) ** 2
+    for v in range(-4, 5):  # exhaustive over the nine levels, element by element
+        assert np.all(e <= (w.astype(np.float64) - sd * v) ** 2 * (1 + 1e-12) + 1e-300)
+
+
+@pin
+def tied_single_step_is_round_half_even_at_the_start_scale(o):
+    # max_iter = 1: the scale stays amax/4 (f16-exact here) and the codes are the plain
+    # rounding of w/s, halves to even
+    s = 0.125
+    w = np.array([4, -4, 0.5, 1.5, 2.5, -2.5, -3.5, 0.49, 3.7, -0.5] * 25 + [0.0] * 6, np.float32) * s
+    w = np.tile(w, (2, 1))
+    c, s16, it = o.tied_quantize(w, max_iter=1)
+    assert np.all(it == 1) and np.all(_f16_to_np64(s16) == s)
+    assert np.array_equal(c, np.clip(np.rint(w / np.float32(s)), -4, 4).astype(np.int8))
+
+
+@pin
+def tied_improves_on_the_start_and_nears_the_best_scale(o):
+    rng = np.random.default_rng(54)
+    w = rng.standard_normal((6, 256)).astype(np.float32)
+    c, s16, _ = o.tied_quantize(w)
+    err = _sq_err(w, c, s16)[:, 0]
+    # the start: s = amax/4 (as f16), codes by rounding
+    s0 = _f16(np.abs(w).max(1) / 4.0)
+    c0 = np.clip(np.rint(w / _f16_to_np64(s0)[:, None]), -4, 4)
+    err0 = _sq_err(w, c0, s0[:, None])[:, 0]
+    assert np.all(err <= err0 * (1 + 1e-6))
+    # brute force over every f16 scale in a wide range, codes chosen per element
+    best = np.full(6, np.inf)
+    for sb in range(0x1000, 0x4400):  # 2^-12 .. 4
+        sd = float(np.uint16(sb).view(np.float16))
+        cb = np.clip(np.rint(w / sd), -4, 4)
+        best = np.minimum(best, ((w - sd * cb) ** 2).sum(1))
+    # (alternating minimization stops at a local optimum: within 8% here, where the
+    # start alone is 50-90% worse)
+    assert np.all(err >= best * (1 - 1e-9)) and np.all(err <= best * 1.2)
+
+
+@pin
+def tied_invariants(o):
+    rng = np.random.default_rng(55)
+    w = (rng.standard_normal((3, 768)) * 0.05).astype(np.float32)
+    w[1, 256:512] = 0.0                 # an all-zero block
+    w[2, :256] = np.float32(2.0 ** -110)  # a block below the 2^-100 floor
+    c, s16, it = o.tied_quantize(w)
+    for r, b in ((1, 1), (2, 0)):
+        assert s16[r, b] == 0 and it[r, b] == 0 and not c[r, 256 * b:256 * b + 256].any()
+    cn, sn, _ = o.tied_quantize(-w)  # odd symmetry
+    assert np.array_equal(cn, -c) and np.array_equal(sn, s16)
+    c4, s4, _ = o.tied_quantize(w * np.float32(4))  # power-of-two equivariance
+    keep = (s16 != 0) & (s16 < 0x7000)
+    assert np.array_equal(c4, c)
+    assert np.array_equal(_f16_to_np64(s4)[keep], 4 * _f16_to_np64(s16)[keep])
+    perm = [2, 0, 1]  # blocks are independent of one another
+    wp = w.reshape(3, 3, 256)[:, perm].reshape(3, 768)
+    cp, sp, _ = o.tied_quantize(wp)
+    assert np.array_equal(cp.reshape(3, 3, 256), c.reshape(3, 3, 256)[:, perm]) and np.array_equal(sp, s16[:, perm])
+    c2, s2, it2 = o.tied_quantize(w)  # deterministic
+    assert np.array_equal(c2, c) and np.array_equal(s2, s16) and np.array_equal(it2, it)

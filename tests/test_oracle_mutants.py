@@ -42,6 +42,15 @@ C_MUTANTS = {
     "synth_trit_shift": ("((f * 3u) >> 16) - 1", "((f * 3u) >> 15) - 1"),
     "synth_scale_counter": ("sm64_word(key, (uint64_t)(n * k / 2) + j)", "sm64_word(key, j)"),
     "synth_gamma": ("z = key + (i + 1) * 0x9E3779B97F4A7C15ull;", "z = key + i * 0x9E3779B97F4A7C15ull;"),
+    "f16_encode_truncates": ("double r = nearbyint(q);", "double r = trunc(q);"),
+    "f16_no_saturation": ("if (v > 65504.0) v = 65504.0;", "if (v > 65536.0) v = 65536.0;"),
+    "tied_start_amax_over_3": ("float s = amax / 4.0f;", "float s = amax / 3.0f;"),
+    "tied_clamp_3": ("if (r > 4.0f) r = 4.0f;", "if (r > 3.0f) r = 3.0f;"),
+    "tied_round_half_away": ("float r = nearbyintf(t);", "float r = roundf(t);"),
+    "tied_no_scale_step": ("s = (float)(pairwise_sum256(v) / (double)cc);", "(void)pairwise_sum256(v);"),
+    "tied_scale_over_count": ("s = (float)(pairwise_sum256(v) / (double)cc);", "s = (float)(pairwise_sum256(v) / 256.0);"),
+    "tied_final_codes_fp32_scale": ("code_step(wb, sd, cb);", "code_step(wb, s, cb);"),
+    "tied_no_zero_floor": ("if (!(amax >= 0x1p-100f)) {", "if (amax == 0.0f) {"),
 }
 
 
