@@ -11,7 +11,8 @@ Other workloads (--workload): `decode32` (32 tokens, Zipf top-8), `prefill2048` 
 tokens, Zipf top-8, per-token log-uniform factors; the expert contraction runs on int8
 MFMA), `stack43` (a decode step through 43 such layers at hidden 7168, 8 tokens,
 Zipf top-8: 246 GB of experts resident), `gemv` (the single 2048 x 4096 matrix, one
-token: quantize + dot pass).
+token: quantize + dot pass), `tiedquant` (the tied quantizer that produces the code
+plane: one 2048 x 4096 fp32 matrix per step, rotating over 32).
 
 Cache hygiene: every step touches bytes that cannot still sit in the 256 MB last-level
 cache. Batch-1 steps route to experts not used in the previous 3 steps (reuse distance
@@ -114,6 +115,7 @@ WORKLOADS = {
     "prefill2048": dict(cfg=3, steps=10, warmup=2, profile=4),
     "stack43": dict(cfg=4, steps=20, warmup=3, profile=2),
     "gemv": dict(cfg=0, steps=4000, warmup=400, profile=512),
+    "tiedquant": dict(cfg="quant", steps=64, warmup=8, profile=32),
 }
 
 
@@ -192,6 +194,70 @@ def run_gemv(args, wl, cfg):
                 config={"workload": cfg["name"], "n": n, "k": k, "tokens_per_step": 1, "bits_per_weight": 4.0625,
                         "rotating_copies": copies, "path": "valu"},
                 extra={})
+
+
+def cpu_baseline_quant(cfg, target_s: float = 10.0) -> dict:
+    """The oracle's tied solver (plain single-threaded C) on the workload's first matrix,
+    repeated to about target_s seconds."""
+    import oracle as oracle_pkg
+    from synth import gen
+
+    o = oracle_pkg.get()
+    w = gen.float_weights(gen.SEED, 0, cfg["n"], cfg["k"])
+    t0 = time.perf_counter()
+    o.tied_quantize(w[:64])
+    per_row = (time.perf_counter() - t0) / 64
+    reps = int(max(1, min(64, round(target_s / max(per_row * cfg["n"], 1e-6)))))
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        o.tied_quantize(w)
+    el = time.perf_counter() - t0
+    nbytes = reps * (cfg["n"] * cfg["k"] * 4 + matrix_bytes(cfg["n"], cfg["k"]))
+    return {"value": round(nbytes / el / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "weights_per_s": round(reps * cfg["n"] * cfg["k"] / el, 1),
+            "sample": f"the workload's first {cfg['n']} x {cfg['k']} matrix, {reps} times; {el:.1f} s on 1 host thread"}
+
+
+def run_quant(args, wl, cfg):
+    import torch
+    from paper_2608_08910_amd import tq
+    from synth import gen
+
+    M, n, k = cfg["matrices"], cfg["n"], cfg["k"]
+    K = args.steps if args.steps is not None else wl["steps"]
+    W = args.warmup if args.warmup is not None else wl["warmup"]
+    P = args.profile_steps if args.profile_steps is not None else wl["profile"]
+    # 32 x 33.5 MB of fp32 weights (1.07 GB, beyond the 256 MB last-level cache), one
+    # matrix per step in rotation
+    ws = [torch.from_numpy(gen.float_weights(gen.SEED, i, n, k)).cuda() for i in range(M)]
+    outs = [tq.TqMatrix.empty(n, k) for _ in range(M)]
+    iters = torch.empty((n, k // 256), dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+
+    def step(i):
+        tq.tq_tied_quantize(ws[i % M], outs[i % M])
+
+    elapsed = time_graph(step, W, K)
+    per_step = n * k * 4 + matrix_bytes(n, k)
+    gbs = per_step * K / elapsed / 1e9
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(P)]
+    torch.cuda.synchronize()
+    for j in range(P):
+        ev[j][0].record()
+        tq.tq_tied_quantize(ws[j % M], outs[j % M])
+        ev[j][1].record()
+    torch.cuda.synchronize()
+    ms = float(np.mean([a.elapsed_time(c) for a, c in ev]))
+    tq.tq_tied_quantize(ws[0], outs[0], iters)
+    torch.cuda.synchronize()
+    steps = iters.to(torch.float32)
+    roof = hbm_roof("tied_quantize", per_step, ms, "k_tied_quantize")
+    return dict(value=gbs, K=K, W=W, elapsed=elapsed, tokens=K, roof=roof,
+                config={"workload": cfg["name"], "matrices": M, "n": n, "k": k, "max_iter": 16,
+                        "weights": "N(0,1) x per-row spread log-uniform [0.005, 0.05], fp32"},
+                extra={"weights_per_s": round(n * k * K / elapsed, 1),
+                       "mean_code_steps_per_block": round(float(steps.mean()), 3),
+                       "max_code_steps_per_block": int(steps.max())})
 
 
 def run_moe(args, wl, cfg):
@@ -335,8 +401,9 @@ def main():
 
     torch.cuda.set_device(0)
     wl = WORKLOADS[args.workload]
-    cfg = gen.CONFIGS[wl["cfg"]]
-    r = run_gemv(args, wl, cfg) if cfg["kind"] == "gemv" else run_moe(args, wl, cfg)
+    cfg = gen.QUANT_CONFIG if wl["cfg"] == "quant" else gen.CONFIGS[wl["cfg"]]
+    run = {"gemv": run_gemv, "moe": run_moe, "quant": run_quant}[cfg["kind"]]
+    r = run(args, wl, cfg)
     K, W, elapsed = r["K"], r["W"], r["elapsed"]
     res = {
         "metric": METRIC,
@@ -359,6 +426,8 @@ def main():
     }
     if not args.no_cpu_baseline and args.workload == "decode1":
         res["cpu_baseline"] = cpu_baseline(gen.SEED, cfg["hidden"], cfg["inter"], cfg["topk"])
+    if not args.no_cpu_baseline and args.workload == "tiedquant":
+        res["cpu_baseline"] = cpu_baseline_quant(cfg)
     print(json.dumps(res), flush=True)
 
 

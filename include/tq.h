@@ -131,6 +131,22 @@ tq_status tq_synth_weights(uint64_t key, int32_t n, int32_t k, uint8_t* codes,
 tq_status tq_quantize_act(const float* x, int64_t t, int32_t k, int8_t* q, float* d,
                           int32_t* bsum, void* stream);
 
+/* Tied quantizer (Sec. 2.1: with the plane scales tied at alpha = (3s, s), the solver's
+ * alternating plane and scale updates fit the uniform quantizer W_hat = s*c, c in -4..4):
+ * w [n][k] fp32 (finite; 4-byte aligned) -> codes and scales in the persistent layout
+ * above (codes 128-byte aligned, tq_codes_bytes(n, k); scales [n][kb]). Per 256-weight
+ * block, the reading taken (the paper gives no start, stopping rule or precision):
+ *   amax = max|w|; amax < 2^-100 -> s = 0, c = 0. Otherwise start at s = amax/4, then
+ *   code step c = clamp(rne(fl32(w / s)), -4, 4) (IEEE fp32 division) and scale step
+ *   s = fl32(<w,c> / <c,c>), with <w,c> summed in fp64 by pairwise halving
+ *   (v[i] += v[i+h] for h = 128, 64, ..., 1) and <c,c> exact, until a code step repeats
+ *   the previous codes or max_iter code steps were taken (1..255). The stored scale is
+ *   f16(s) (nearest even, saturating at 65504) and the stored codes are the code step at
+ *   that scale (zero if it is 0). iters: NULL or [n][kb] bytes, the code steps taken per
+ *   block (0 for a zero block). Deterministic; n >= 0 (0 is a no-op). */
+tq_status tq_tied_quantize(const float* w, int32_t n, int32_t k, int32_t max_iter, uint8_t* codes,
+                           uint16_t* scales, uint8_t* iters, void* stream);
+
 /* The serving dot pass for one matrix and t tokens (Sec. 2.2): y[t][n] fp32 =
  * sum_b f32(s[r][b]) * d[t][b] * isum[t][r][b]. q, d as from tq_quantize_act (q 16-byte
  * aligned); bsum is accepted so callers can pass the quantizer's whole output, but the

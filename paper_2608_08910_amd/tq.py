@@ -67,6 +67,7 @@ for _name, _args, _res in [
     ("tq_unpack_host", [_vp, _i32, _i32, _vp], _i32),
     ("tq_synth_weights", [ctypes.c_uint64, _i32, _i32, _vp, _vp, _vp], _i32),
     ("tq_quantize_act", [_vp, _i64, _i32, _vp, _vp, _vp, _vp], _i32),
+    ("tq_tied_quantize", [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp], _i32),
     ("tq_gemv", [_P(tq_mat), _vp, _vp, _vp, _i64, _vp, _vp, _vp], _i32),
     ("tq_gemv_timed", [_P(tq_mat), _vp, _vp, _vp, _i64, _vp, _vp, _vp, _P(_vp)], _i32),
     ("tq_moe_workspace_bytes", [_P(tq_experts), _i64, _i32], _sz),
@@ -168,6 +169,19 @@ class TqMatrix:
 def tq_synth_weights(key: int, m: TqMatrix, stream=None):
     _ok(_L.tq_synth_weights(key & (2**64 - 1), m.n, m.k, _dev(m.codes, torch.uint8, "codes", (m.n, m.k // 256, 128)),
                             _dev(m.scales, torch.int16, "scales", (m.n, m.k // 256)), _stream(stream)))
+
+
+def tq_tied_quantize(w: torch.Tensor, m: TqMatrix, iters: torch.Tensor | None = None, max_iter: int = 16,
+                     stream=None):
+    """Tied quantizer: w [n][k] fp32 -> m's codes and f16 scales; iters: None or a
+    [n][k/256] uint8 tensor that receives the code steps taken per block."""
+    n, k = w.shape
+    if (m.n, m.k) != (n, k):
+        raise ValueError(f"tq_tied_quantize: matrix is {m.n}x{m.k}, weights {n}x{k}")
+    it = 0 if iters is None else _dev(iters, torch.uint8, "iters", (n, k // 256))
+    _ok(_L.tq_tied_quantize(_dev(w, torch.float32, "w"), n, k, max_iter,
+                            _dev(m.codes, torch.uint8, "codes", (n, k // 256, 128)),
+                            _dev(m.scales, torch.int16, "scales", (n, k // 256)), it or None, _stream(stream)))
 
 
 # -- dot pass -----------------------------------------------------------------------------

@@ -1,8 +1,8 @@
 """Seeded synthetic inputs for the tied-trit-plane expert dot pass.
 
 This module holds random draws only: activations, per-token scale factors, routing
-indices and routing weights, and the 64-bit keys that name each weight matrix's
-counter-based stream. None of the method's arithmetic (fold, pack, quantize, integer
+indices and routing weights, fp32 weights for the tied quantizer, and the 64-bit keys
+that name each weight matrix's counter-based stream. None of the method's arithmetic (fold, pack, quantize, integer
 dot, scale combine, SiLU, weighted combine) lives here; both the CPU oracle and the
 HIP path consume these draws, and each implements the method on its own.
 
@@ -53,6 +53,7 @@ _TAG_LOGIT = 3
 _TAG_FACTOR = 4
 _TAG_KEY = 5
 _TAG_BENCH = 6
+_TAG_FWEIGHT = 7
 
 PROJ_GATE, PROJ_UP, PROJ_DOWN = 0, 1, 2
 
@@ -76,6 +77,11 @@ CONFIGS = {
 }
 
 
+# The tied quantizer's workload (the producer of the persistent bytes): fp32 weights of
+# 32 expert projections at the paper model's 2048 x 4096 expert shape.
+QUANT_CONFIG = dict(name="tied_quantize_m32_2048x4096", kind="quant", matrices=32, n=2048, k=4096)
+
+
 def _rng(*key: int) -> np.random.Generator:
     return np.random.default_rng(np.random.SeedSequence(entropy=int(key[0]), spawn_key=tuple(int(v) for v in key[1:])))
 
@@ -94,6 +100,14 @@ def single_matrix_key(seed: int = SEED) -> int:
 def activations(seed: int, layer: int, tokens: int, width: int) -> np.ndarray:
     """N(0,1) fp32 activations [tokens][width]."""
     return _rng(seed, _TAG_ACT, layer).standard_normal((tokens, width), dtype=np.float32)
+
+
+def float_weights(seed: int, index: int, n: int, k: int) -> np.ndarray:
+    """fp32 weights [n][k] for the tied quantizer: N(0,1) times a per-row spread drawn
+    log-uniform on [0.005, 0.05] (the magnitude range of transformer projection weights)."""
+    r = _rng(seed, _TAG_FWEIGHT, index)
+    sigma = np.exp(np.log(0.005) + r.random((n, 1)) * (np.log(0.05) - np.log(0.005)))
+    return (r.standard_normal((n, k), dtype=np.float32) * sigma.astype(np.float32)).astype(np.float32)
 
 
 def token_factors(seed: int, tokens: int) -> np.ndarray:

@@ -116,6 +116,19 @@ def test_gemv_validation_errors_before_launch():
 
 
 @no_gpu_only
+def test_tied_quantize_validation_errors_before_launch():
+    L = tq._L
+    assert L.tq_tied_quantize(FAKE, 4, 300, 16, FAKE, FAKE, None, None) == tq.TQ_ERR_INVALID  # k % 256
+    assert L.tq_tied_quantize(FAKE, -1, 256, 16, FAKE, FAKE, None, None) == tq.TQ_ERR_INVALID  # n < 0
+    assert L.tq_tied_quantize(FAKE, 4, 256, 0, FAKE, FAKE, None, None) == tq.TQ_ERR_INVALID  # max_iter
+    assert L.tq_tied_quantize(FAKE, 4, 256, 256, FAKE, FAKE, None, None) == tq.TQ_ERR_INVALID
+    assert L.tq_tied_quantize(None, 4, 256, 16, FAKE, FAKE, None, None) == tq.TQ_ERR_INVALID
+    assert L.tq_tied_quantize(FAKE, 4, 256, 16, FAKE + 64, FAKE, None, None) == tq.TQ_ERR_ALIGN  # codes
+    assert L.tq_tied_quantize(FAKE + 2, 4, 256, 16, FAKE, FAKE, None, None) == tq.TQ_ERR_ALIGN  # w
+    assert L.tq_tied_quantize(FAKE, 0, 256, 16, FAKE, FAKE, None, None) == tq.TQ_OK  # nothing to do
+    assert "max_iter" in (L.tq_tied_quantize(FAKE, 4, 256, 0, FAKE, FAKE, None, None) and tq.tq_last_error())
+
+
 def test_quantize_validation_errors_before_launch():
     L = tq._L
     assert L.tq_quantize_act(FAKE, 1, 300, FAKE, FAKE, FAKE, None) == tq.TQ_ERR_INVALID
