@@ -12,12 +12,45 @@ namespace tq {
 // A wave owns one block; lane l holds weights l, l + 64, l + 128, l + 192 of it, so the
 // pairwise-halving sum adds within the lane for the first two levels (h = 128, 64) and
 // across lanes (xor 32 .. 1) for the rest.
+
+// The code step: c = clamp(rne(fl32(w / s)), -4, 4). The quotient is formed as
+// w * fl32(1 / s), which lies within |q| * 2^-22 of both w / s and fl32(w / s); rne only
+// changes value at half-integers, so unless one lies that close the product rounds like
+// the correctly rounded quotient. The few elements that near a half-integer (exact ties
+// among them) take the division.
 __device__ __forceinline__ void tied_code_step(const float (&w)[4], float s, int (&c)[4]) {
+  const float rs = 1.0f / s;
+  float r[4];
+  bool near = false;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const float r = rintf(w[j] / s);  // correctly rounded division, half to even
-    c[j] = (int)fminf(fmaxf(r, -4.0f), 4.0f);
+    const float q = w[j] * rs;
+    const float f = q - floorf(q);  // exact: the distance above the integer below
+    near |= fabsf(f - 0.5f) <= fabsf(q) * 0x1p-21f;
+    r[j] = rintf(q);
   }
+  if (__any(near)) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float q = w[j] * rs;
+      const float f = q - floorf(q);
+      if (fabsf(f - 0.5f) <= fabsf(q) * 0x1p-21f) r[j] = rintf(w[j] / s);  // correctly rounded division
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) c[j] = (int)fminf(fmaxf(r[j], -4.0f), 4.0f);
+}
+
+// a + (the same lane-pair partner's a), for a butterfly over lane bit M (both lanes of a
+// pair add the same two values, so they hold the same sum)
+template <int M>
+__device__ __forceinline__ double xor_add(double a) {
+  const int lo = __double2loint(a), hi = __double2hiint(a);
+  return a + __hiloint2double(lane_xor_i<M>(hi), lane_xor_i<M>(lo));
+}
+template <int M>
+__device__ __forceinline__ int xor_add(int a) {
+  return a + lane_xor_i<M>(a);
 }
 
 __global__ __launch_bounds__(256) void k_tied_quantize(const float* __restrict__ w, int64_t nblocks, int max_iter,
@@ -51,11 +84,19 @@ __global__ __launch_bounds__(256) void k_tied_quantize(const float* __restrict__
       p0 = p0 + p2;  // h = 128
       p1 = p1 + p3;
       p0 = p0 + p1;  // h = 64
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) p0 = p0 + __shfl_xor(p0, m);  // h = 32 .. 1 (a + b = b + a)
+      p0 = xor_add<32>(p0);  // h = 32 .. 1
+      p0 = xor_add<16>(p0);
+      p0 = xor_add<8>(p0);
+      p0 = xor_add<4>(p0);
+      p0 = xor_add<2>(p0);
+      p0 = xor_add<1>(p0);
       int cc = c[0] * c[0] + c[1] * c[1] + c[2] * c[2] + c[3] * c[3];
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) cc += __shfl_xor(cc, m);
+      cc = xor_add<32>(cc);
+      cc = xor_add<16>(cc);
+      cc = xor_add<8>(cc);
+      cc = xor_add<4>(cc);
+      cc = xor_add<2>(cc);
+      cc = xor_add<1>(cc);
 #pragma unroll
       for (int j = 0; j < 4; ++j) prev[j] = c[j];
       if (cc == 0) break;

@@ -43,16 +43,18 @@ def check(tq, oracle, w, max_iter=16):
 
 def edge_rows(k: int) -> np.ndarray:
     """Hand-built blocks, tiled to width k: zero, below the 2^-100 floor, an exact f16
-    grid, a scale in the f16 subnormal range, one past the f16 range (saturates), and a
-    block whose start scale lands codes on exact halves."""
+    grid, a scale in the f16 subnormal range, one past the f16 range (saturates), and
+    blocks whose start scale lands codes on exact halves (w / s = k + 0.5 exactly)."""
     rng = np.random.default_rng(7)
     rows = [np.zeros(256, np.float32), np.full(256, 2.0 ** -110, np.float32)]
     c = rng.integers(-4, 5, 256); c[3] = -4
     rows.append((np.float32(np.float16(0.0123)) * c).astype(np.float32))
     rows.append((rng.standard_normal(256) * 3e-7).astype(np.float32))
     rows.append((rng.standard_normal(256) * 1e5).astype(np.float32))
-    h = np.array([4, 0.5, 1.5, 2.5, -2.5, -3.5, -0.5, 3.5] * 32, np.float32) * np.float32(0.25)
-    rows.append(h)
+    h = np.array([4, 0.5, 1.5, 2.5, -2.5, -3.5, -0.5, 3.5] * 32, np.float32)
+    rows.append(h * np.float32(0.25))
+    rows.append(h * np.float32(0.1875))  # ties again at a start scale that is no power of two
+    rows.append(h * np.float32(np.float16(0.0123)))
     out = np.stack(rows)
     return np.tile(out, (1, k // 256))
 
