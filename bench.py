@@ -47,27 +47,35 @@ sys.path.insert(0, ROOT)
 METRIC = "achieved HBM GB/s (% of peak) for tq expert GEMV; MoE-layer tokens/sec"
 HBM_PEAK_GBS = 8000.0
 MFMA_I8_PEAK_TOPS = 5000.0
+# VALU issue: each of a CU's 4 SIMDs starts one wave64 VALU instruction every 4 cycles
+# (16 lanes a cycle); 256 CUs at 2.4 GHz
+VALU_PEAK_GINST = 256 * 4 * 2.4 / 4
 
 
-def recorded_traffic(kernel: str):
-    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter summary, or
-    None if no record exists or the kernel's sources changed since it was taken."""
+def _recorded(kernel: str, field: str, kind: str = "traffic"):
+    """`field` of the committed rocprofv3 counter record of `kernel` (profiles/*<kind>*.md),
+    or None if no record exists or the kernel's sources changed since it was taken."""
     import glob
     import hashlib
-    for path in glob.glob(os.path.join(ROOT, "profiles", "*traffic*.md")):
+    for path in glob.glob(os.path.join(ROOT, "profiles", f"*{kind}*.md")):
         for line in open(path):
             line = line.strip()
             if not line.startswith('{"kernel"'):
                 continue
             rec = json.loads(line)
-            if rec["kernel"] != kernel:
+            if rec["kernel"] != kernel or field not in rec:
                 continue
             h = hashlib.sha256()
             for f in rec["sources"]:
                 h.update(open(os.path.join(ROOT, f), "rb").read())
             if h.hexdigest() == rec["sources_sha256"]:
-                return rec["traffic_bytes_per_launch"]
+                return rec[field]
     return None
+
+
+def recorded_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` (FETCH_SIZE + WRITE_SIZE, calibrated)."""
+    return _recorded(kernel, "traffic_bytes_per_launch")
 
 
 def matrix_bytes(n: int, k: int) -> int:
@@ -251,7 +259,18 @@ def run_quant(args, wl, cfg):
     tq.tq_tied_quantize(ws[0], outs[0], iters)
     torch.cuda.synchronize()
     steps = iters.to(torch.float32)
-    roof = hbm_roof("tied_quantize", per_step, ms, "k_tied_quantize")
+    sym = "k_tied_quantize"
+    valu = _recorded(sym, "valu_insts_per_launch", "valu")
+    if valu is None:  # no current instruction count: fall back to the bytes
+        roof = hbm_roof("tied_quantize", per_step, ms, sym)
+    else:
+        # the kernel is bound by VALU issue: its wave64 VALU instructions per launch
+        # (SQ_INSTS_VALU, rocprofv3, committed record) over its mean duration
+        achieved = valu / (ms * 1e-3) / 1e9
+        roof = {"kernel": "tied_quantize", "bound": "alu", "achieved": round(achieved, 1), "peak": VALU_PEAK_GINST,
+                "unit": "G VALU wave64 instructions/s", "frac": round(achieved / VALU_PEAK_GINST, 4),
+                "traffic": recorded_traffic(sym), "valu_insts_per_launch": valu, "bytes_per_launch": per_step,
+                "hbm_GBps": round(per_step / (ms * 1e-3) / 1e9, 1), "mean_ms": round(ms, 5), "kernel_symbol": sym}
     return dict(value=gbs, K=K, W=W, elapsed=elapsed, tokens=K, roof=roof,
                 config={"workload": cfg["name"], "matrices": M, "n": n, "k": k, "max_iter": 16,
                         "weights": "N(0,1) x per-row spread log-uniform [0.005, 0.05], fp32"},
@@ -340,8 +359,8 @@ def run_moe(args, wl, cfg):
         # quantized tokens (int8 + scale per block), and write h per slot
         gu_bytes = n_distinct * 2 * matrix_bytes(I, H) + T * (H + (H // 256) * 4) + T * topk * I * 4
         rpw = 8 if nl_gu == 1 else (4 if nl_gu == 2 else (2 if nl_gu <= 4 else 1))
-        nt = 2 if nl_gu <= 2 else 1  # tokens per group of the grouped VALU kernel
-        gu_kernel = "k_moe_mfma<2>" if mfma else f"k_tb<2, {nl_gu}, {rpw}, {nt}, 4, {ragged}>"
+        nt = 2 if nl_gu <= 2 else 1  # tokens per group of the grouped VALU kernel (first, later)
+        gu_kernel = "k_moe_mfma<2>" if mfma else f"k_tb<2, {nl_gu}, {rpw}, {nt}, {nt}, 4, {ragged}>"
         kname = "gate_up"
     if mfma:
         gu_ops = 2.0 * T * topk * (2 * I * H)  # int8 multiply-adds of gate and up, 2 ops each
