@@ -12,6 +12,9 @@ Definitions followed (paper sections):
                              rounding rule are this oracle's stated reading)
   integer dot + combine .... Sec. 2.2 (one integer dot pass, one float multiply-add
                              per block), evaluated exactly / in fp64
+  free-scale two planes .... Sec. 2.1 (alpha1*T1 + alpha2*T2, free scales) and Sec. 4.1
+                             (the unfolded pair is served as two trit planes at 4.125
+                             bits per weight, one integer pass per plane)
   tied solver .............. Sec. 2.1 (alternating code and scale updates against one
                              scale per group; start, stop rule and precision are this
                              oracle's stated reading)
@@ -61,6 +64,7 @@ class Oracle:
             ("orc_quantize", [_vp, _i64, _i64, _i64, _vp, _vp, _vp], ctypes.c_int),
             ("orc_dot_i8", [_vp, _vp, _i64], ctypes.c_int64),
             ("orc_gemv", [_vp, _vp, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _vp], ctypes.c_int),
+            ("orc_gemv2", [_vp, _vp, _vp, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _vp], ctypes.c_int),
             ("orc_splitmix64_word", [ctypes.c_uint64, ctypes.c_uint64], ctypes.c_uint64),
             ("orc_synth_matrix", [ctypes.c_uint64, _i64, _i64, _i64, _i64, _vp, _vp, _vp], ctypes.c_int),
             ("orc_f32_to_f16", [ctypes.c_float], ctypes.c_uint16),
@@ -149,6 +153,29 @@ class Oracle:
         self._check(self._L.orc_gemv(_p(c), _p(s), n, k, _p(q), _p(d), t, _p(y), _p(a),
                                      _p(isum) if want_isum else None), "gemv")
         return (y, a, isum) if want_isum else (y, a)
+
+    def gemv2(self, t1, t2, a, q, d, want_isum: bool = False):
+        """Free-scale two-plane pass: t1, t2 trit planes [n][k] in -1..1, a f16 bits
+        [n][k/256][2] (alpha1, alpha2). y[t][r], absref[t][r] in fp64 (and isum
+        [t][r][b][2] int32, plane 1 then plane 2, if asked)."""
+        t1 = np.ascontiguousarray(t1, dtype=np.int8)
+        t2 = np.ascontiguousarray(t2, dtype=np.int8)
+        a = np.ascontiguousarray(a, dtype=np.uint16)
+        q = np.ascontiguousarray(q, dtype=np.int8)
+        d = np.ascontiguousarray(d, dtype=np.float32)
+        if q.ndim == 1:
+            q = q[None, :]
+            d = d.reshape(1, -1)
+        n, k = t1.shape
+        t = q.shape[0]
+        assert t2.shape == (n, k) and a.shape == (n, k // 256, 2)
+        assert q.shape == (t, k) and d.shape == (t, k // 256)
+        y = np.empty((t, n), dtype=np.float64)
+        ab = np.empty((t, n), dtype=np.float64)
+        isum = np.empty((t, n, k // 256, 2), dtype=np.int32) if want_isum else None
+        self._check(self._L.orc_gemv2(_p(t1), _p(t2), _p(a), n, k, _p(q), _p(d), t, _p(y), _p(ab),
+                                      _p(isum) if want_isum else None), "gemv2")
+        return (y, ab, isum) if want_isum else (y, ab)
 
     # -- synthetic weights (input generation; SplitMix64 counter stream) -------------
     # -- tied solver (Sec. 2.1) ---------------------------------------------------------

@@ -27,6 +27,10 @@
  *   orc_gemv ................ trit-plane identity 3(T1.q)+(T2.q), offset form, exact
  *                             integer products at unit scales, power-of-two scaling,
  *                             dequantized-matmul error bound, exact rational brute force
+ *   orc_gemv2 ............... tied scales (3s, s) reproduce the folded pass (integer
+ *                             identity 3(T1.q)+(T2.q)), one empty plane reduces to a
+ *                             single ternary plane, plane exchange, sign symmetry,
+ *                             dequantized-matmul error bound, exact rational brute force
  *   orc_splitmix64_word ..... SplitMix64's published seed-0 outputs
  *   orc_synth_matrix ........ the written recipe (pure-Python), trit/code/scale
  *                             distributions
@@ -196,6 +200,49 @@ int orc_gemv(const int8_t* c, const uint16_t* s, int64_t n, int64_t k, const int
         double term = orc_f16_to_f64(s[r * kb + b]) * (double)d[tt * kb + b] * (double)v;
         acc += term;
         aacc += fabs(term);
+      }
+      y[tt * n + r] = acc;
+      if (absref) absref[tt * n + r] = aacc;
+    }
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------------ */
+/* Free-scale two-plane serving pass (Sec. 2.1, first paragraph: W ~ alpha1*T1 +     */
+/* alpha2*T2 with two free scales per group; Sec. 4.1, the quality table's note: the  */
+/* free pair does not fold, so its serving format keeps the two trit planes apart,    */
+/* at 4.125 bits per weight, and the dot takes one integer pass per plane). Groups    */
+/* are 256-weight blocks with two f16 scales each (a[r][b][0] = alpha1,               */
+/* a[r][b][1] = alpha2: 2 x 16 bits per 256 weights, the 0.125 of 4.125):            */
+/*   isum_p[t][r][b] = sum_i Tp[r][256b+i] * q[t][256b+i]   (exact, p = 1, 2),        */
+/*   y[t][r] = sum_b d[t][b] * (alpha1[r][b] * isum_1 + alpha2[r][b] * isum_2),       */
+/* evaluated in fp64 in ascending b, plane 1's term before plane 2's; absref[t][r] is  */
+/* the sum of the terms' magnitudes. isum (nullable): [t][n][k/256][2].               */
+/* ------------------------------------------------------------------------------ */
+
+int orc_gemv2(const int8_t* t1, const int8_t* t2, const uint16_t* a, int64_t n, int64_t k,
+              const int8_t* q, const float* d, int64_t t, double* y, double* absref, int32_t* isum) {
+  if (k % 256 != 0) return ORC_BAD_INPUT;
+  int64_t kb = k / 256;
+  for (int64_t i = 0; i < n * k; ++i)
+    if (t1[i] < -1 || t1[i] > 1 || t2[i] < -1 || t2[i] > 1) return ORC_BAD_INPUT;
+  for (int64_t tt = 0; tt < t; ++tt)
+    for (int64_t r = 0; r < n; ++r) {
+      double acc = 0.0, aacc = 0.0;
+      for (int64_t b = 0; b < kb; ++b) {
+        const int8_t* qb = q + tt * k + b * 256;
+        int64_t v1 = orc_dot_i8(t1 + r * k + b * 256, qb, 256);
+        int64_t v2 = orc_dot_i8(t2 + r * k + b * 256, qb, 256);
+        if (isum) {
+          isum[((tt * n + r) * kb + b) * 2 + 0] = (int32_t)v1;
+          isum[((tt * n + r) * kb + b) * 2 + 1] = (int32_t)v2;
+        }
+        double db = (double)d[tt * kb + b];
+        double term1 = orc_f16_to_f64(a[(r * kb + b) * 2 + 0]) * db * (double)v1;
+        double term2 = orc_f16_to_f64(a[(r * kb + b) * 2 + 1]) * db * (double)v2;
+        acc += term1;
+        acc += term2;
+        aacc += fabs(term1) + fabs(term2);
       }
       y[tt * n + r] = acc;
       if (absref) absref[tt * n + r] = aacc;

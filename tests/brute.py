@@ -59,6 +59,24 @@ def gemv_exact(c, s, q, d):
     return out
 
 
+def gemv2_exact(t1, t2, a, q, d):
+    """Free-scale two-plane pass. t1, t2: rows of trits, a: rows of [alpha1, alpha2]
+    f16 bit pairs per block, q: list of ints, d: list of fp32. Exact rational y per row:
+    sum over blocks of d * (alpha1 * (T1 . q) + alpha2 * (T2 . q))."""
+    k = len(q)
+    out = []
+    for r in range(len(t1)):
+        acc = Fraction(0)
+        for b in range(k // 256):
+            cols = range(b * 256, (b + 1) * 256)
+            s1 = sum(int(t1[r][i]) * int(q[i]) for i in cols)
+            s2 = sum(int(t2[r][i]) * int(q[i]) for i in cols)
+            db = Fraction(float(d[b]))
+            acc += db * (f16_exact(int(a[r][b][0])) * s1 + f16_exact(int(a[r][b][1])) * s2)
+        out.append(acc)
+    return out
+
+
 def silu(z: float) -> float:
     return z / (1.0 + math.exp(-z))
 

@@ -332,6 +332,128 @@ def gemv_matches_exact_rational_brute_force(o):
 
 
 # --------------------------------------------------------------------------------------
+# Free-scale two-plane pass (Sec. 2.1 alpha1*T1 + alpha2*T2; Sec. 4.1: two trit planes at
+# 4.125 bits per weight, one integer pass per plane)
+# --------------------------------------------------------------------------------------
+
+def _planes(rng, n, k):
+    return (rng.integers(-1, 2, (n, k)).astype(np.int8), rng.integers(-1, 2, (n, k)).astype(np.int8))
+
+
+@pin
+def gemv2_plane_sums_scales_and_quantization_bound(o):
+    # isum per plane against numpy int64 matmuls; absref against the terms rebuilt from
+    # numpy's f16 decode; y against the dequantized two-plane matmul within the
+    # activation quantizer's error bound (|x - d q| <= d (0.5 + 2^-14) per element).
+    rng = np.random.default_rng(61)
+    n, k, t = 6, 1024, 3
+    t1, t2 = _planes(rng, n, k)
+    a = _f16(np.exp(rng.uniform(np.log(1e-3), np.log(1e-1), (n, k // 256, 2))))
+    x = rng.standard_normal((t, k)).astype(np.float32)
+    q, d, _ = o.quantize(x)
+    y, ab, isum = o.gemv2(t1, t2, a, q, d, want_isum=True)
+    af = _f16_to_np64(a)
+    terms = np.zeros((t, n))
+    for b in range(k // 256):
+        sl = slice(b * 256, (b + 1) * 256)
+        for p_, tp in enumerate((t1, t2)):
+            ref = q[:, sl].astype(np.int64) @ tp[:, sl].T.astype(np.int64)
+            assert np.array_equal(isum[:, :, b, p_], ref)
+            terms += np.abs(af[None, :, b, p_] * d[:, b, None].astype(np.float64) * ref)
+    assert np.allclose(ab, terms, rtol=1e-12, atol=0)
+    W = np.repeat(af[:, :, 0], 256, axis=1) * t1 + np.repeat(af[:, :, 1], 256, axis=1) * t2
+    ref = x.astype(np.float64) @ W.T
+    absw = np.abs(W).reshape(n, k // 256, 256).sum(2)
+    bound = (d.astype(np.float64)[:, None, :] * absw[None]).sum(2) * (0.5 + 2 ** -14)
+    assert np.all(np.abs(y - ref) <= bound * (1 + 1e-9) + 1e-12)
+    bad = t1.copy(); bad[2, 5] = 2
+    try:
+        o.gemv2(bad, t2, a, q, d)
+    except Exception:  # noqa: BLE001 - the oracle must refuse a value outside -1..1
+        pass
+    else:
+        raise AssertionError("gemv2 accepted a trit outside -1..1")
+
+
+@pin
+def gemv2_tied_scales_reproduce_the_folded_pass(o):
+    # alpha = (3s, s) with 3s exact in f16 (fraction bits a multiple of 4): the block sums
+    # meet the fold identity 3(T1.q) + (T2.q) = c.q exactly, checked with numpy on the
+    # folded codes, and y equals the folded pass up to fp64 rounding.
+    rng = np.random.default_rng(67)
+    n, k, t = 5, 768, 2
+    t1, t2 = _planes(rng, n, k)
+    c = (3 * t1.astype(np.int16) + t2).astype(np.int8)
+    s = (rng.integers(0x1419, 0x2E66, (n, k // 256)) & ~3).astype(np.uint16)
+    s3 = _f16(3 * _f16_to_np64(s))
+    assert np.array_equal(_f16_to_np64(s3), 3 * _f16_to_np64(s))
+    a = np.stack([s3, s], axis=2)
+    x = rng.standard_normal((t, k)).astype(np.float32)
+    q, d, _ = o.quantize(x)
+    y2, ab2, isum = o.gemv2(t1, t2, a, q, d, want_isum=True)
+    for b in range(k // 256):
+        sl = slice(b * 256, (b + 1) * 256)
+        folded = q[:, sl].astype(np.int64) @ c[:, sl].T.astype(np.int64)
+        assert np.array_equal(3 * isum[:, :, b, 0].astype(np.int64) + isum[:, :, b, 1], folded)
+    sf = _f16_to_np64(s)
+    yf = np.zeros((t, n))
+    for b in range(k // 256):
+        sl = slice(b * 256, (b + 1) * 256)
+        yf += sf[None, :, b] * d[:, b, None].astype(np.float64) * (q[:, sl].astype(np.int64) @ c[:, sl].T.astype(np.int64))
+    assert np.all(np.abs(y2 - yf) <= ab2 * 2.0 ** -45)
+
+
+@pin
+def gemv2_one_empty_plane_is_one_ternary_pass(o):
+    # With T2 = 0 the pass is the single-plane pass over T1 at scale alpha1 (codes in
+    # -1..1 are valid nine-level codes), term for term; likewise T1 = 0 with alpha2.
+    rng = np.random.default_rng(71)
+    n, k, t = 4, 512, 2
+    t1, t2 = _planes(rng, n, k)
+    z = np.zeros_like(t1)
+    a = _f16(rng.uniform(1e-3, 1e-1, (n, k // 256, 2)))
+    x = rng.standard_normal((t, k)).astype(np.float32)
+    q, d, _ = o.quantize(x)
+    for keep, p_ in ((t1, 0), (t2, 1)):
+        planes = (keep, z) if p_ == 0 else (z, keep)
+        y2, ab2 = o.gemv2(*planes, a, q, d)
+        y1, ab1 = o.gemv(keep, np.ascontiguousarray(a[:, :, p_]), q, d)
+        assert np.array_equal(y2, y1) and np.array_equal(ab2, ab1)
+
+
+@pin
+def gemv2_plane_exchange_and_sign_symmetry(o):
+    rng = np.random.default_rng(73)
+    n, k, t = 4, 512, 2
+    t1, t2 = _planes(rng, n, k)
+    a = _f16(rng.uniform(1e-3, 1e-1, (n, k // 256, 2)))
+    x = rng.standard_normal((t, k)).astype(np.float32)
+    q, d, _ = o.quantize(x)
+    y, ab, isum = o.gemv2(t1, t2, a, q, d, want_isum=True)
+    ys, abs_, isums = o.gemv2(t2, t1, np.ascontiguousarray(a[:, :, ::-1]), q, d, want_isum=True)
+    assert np.array_equal(isums, isum[..., ::-1])
+    assert np.all(np.abs(ys - y) <= ab * 2.0 ** -50) and np.allclose(abs_, ab, rtol=1e-14)
+    neg = a.copy(); neg[:, :, 1] ^= 0x8000  # -alpha2 with -T2: every term unchanged
+    yn, abn, isn = o.gemv2(t1, (-t2).astype(np.int8), neg, q, d, want_isum=True)
+    assert np.array_equal(yn, y) and np.array_equal(abn, ab)
+    assert np.array_equal(isn[..., 1], -isum[..., 1]) and np.array_equal(isn[..., 0], isum[..., 0])
+
+
+@pin
+def gemv2_matches_exact_rational_brute_force(o):
+    rng = np.random.default_rng(79)
+    n, k = 3, 512
+    t1, t2 = _planes(rng, n, k)
+    a = _f16(rng.uniform(1e-3, 1e-1, (n, k // 256, 2)))
+    x = rng.standard_normal((1, k)).astype(np.float32)
+    q, d, _ = o.quantize(x)
+    y, ab = o.gemv2(t1, t2, a, q, d)
+    ex = brute.gemv2_exact(t1.tolist(), t2.tolist(), a.tolist(), q[0].tolist(), d[0].tolist())
+    for r in range(n):
+        assert abs(Fraction(float(y[0, r])) - ex[r]) <= Fraction(float(ab[0, r])) * Fraction(1, 2 ** 50)
+
+
+# --------------------------------------------------------------------------------------
 # Synthetic weight stream (input generation): SplitMix64 published outputs + recipe
 # --------------------------------------------------------------------------------------
 

@@ -51,6 +51,15 @@ C_MUTANTS = {
     "tied_scale_over_count": ("s = (float)(pairwise_sum256(v) / (double)cc);", "s = (float)(pairwise_sum256(v) / 256.0);"),
     "tied_final_codes_fp32_scale": ("code_step(wb, sd, cb);", "code_step(wb, s, cb);"),
     "tied_no_zero_floor": ("if (!(amax >= 0x1p-100f)) {", "if (amax == 0.0f) {"),
+    "gemv2_alpha2_from_alpha1": ("orc_f16_to_f64(a[(r * kb + b) * 2 + 1])", "orc_f16_to_f64(a[(r * kb + b) * 2 + 0])"),
+    "gemv2_scale_stride": ("orc_f16_to_f64(a[(r * kb + b) * 2 + 0])", "orc_f16_to_f64(a[(r * kb + b) + 0])"),
+    "gemv2_plane2_dropped": ("        acc += term2;\n", ""),
+    "gemv2_plane2_reads_plane1": ("orc_dot_i8(t2 + r * k + b * 256, qb, 256)", "orc_dot_i8(t1 + r * k + b * 256, qb, 256)"),
+    "gemv2_isum_planes_swapped": ("isum[((tt * n + r) * kb + b) * 2 + 0] = (int32_t)v1;", "isum[((tt * n + r) * kb + b) * 2 + 0] = (int32_t)v2;"),
+    "gemv2_absref_plane1_only": ("aacc += fabs(term1) + fabs(term2);", "aacc += fabs(term1);"),
+    "gemv2_token_index_dropped": ("const int8_t* qb = q + tt * k + b * 256;", "const int8_t* qb = q + b * 256;"),
+    "gemv2_act_scale_dropped": ("double db = (double)d[tt * kb + b];", "double db = 1.0;"),
+    "gemv2_trit_range_unchecked": ("if (t1[i] < -1 || t1[i] > 1 || t2[i] < -1 || t2[i] > 1) return ORC_BAD_INPUT;\n  for (int64_t tt", "(void)0;\n  for (int64_t tt"),
 }
 
 
