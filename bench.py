@@ -12,7 +12,10 @@ tokens, Zipf top-8, per-token log-uniform factors; the expert contraction runs o
 MFMA), `stack43` (a decode step through 43 such layers at hidden 7168, 8 tokens,
 Zipf top-8: 246 GB of experts resident), `gemv` (the single 2048 x 4096 matrix, one
 token: quantize + dot pass), `tiedquant` (the tied quantizer that produces the code
-plane: one 2048 x 4096 fp32 matrix per step, rotating over 32).
+plane: one 2048 x 4096 fp32 matrix per step, rotating over 32), `twoplane` (the
+free-scale two-plane variant, 4.125 bits/weight: one decode step's routed gate and up
+rows as one 32768 x 4096 matrix, one token, rotating over 8 copies; the folded pass over
+the same trit planes is timed beside it, and both kernels at 1, 4 and 16 tokens).
 
 Cache hygiene: every step touches bytes that cannot still sit in the 256 MB last-level
 cache. Batch-1 steps route to experts not used in the previous 3 steps (reuse distance
@@ -124,6 +127,7 @@ WORKLOADS = {
     "stack43": dict(cfg=4, steps=20, warmup=3, profile=2),
     "gemv": dict(cfg=0, steps=4000, warmup=400, profile=512),
     "tiedquant": dict(cfg="quant", steps=64, warmup=8, profile=32),
+    "twoplane": dict(cfg="twoplane", steps=2000, warmup=200, profile=256),
 }
 
 
@@ -197,7 +201,7 @@ def run_gemv(args, wl, cfg):
         tq.tq_gemv_timed(mats[j % copies], q, d, b, y, ev[j])
     torch.cuda.synchronize()
     ms = float(np.mean([a.elapsed_time(c) for a, c in ev]))
-    roof = hbm_roof("gemv", matrix_bytes(n, k) + k + (k // 256) * 4 + n * 4, ms, "k_gemv<2, 1, 1>")
+    roof = hbm_roof("gemv", matrix_bytes(n, k) + k + (k // 256) * 4 + n * 4, ms, "k_gemv<2, 1, 1, false>")
     return dict(value=gbs, K=K, W=W, elapsed=elapsed, tokens=K, roof=roof,
                 config={"workload": cfg["name"], "n": n, "k": k, "tokens_per_step": 1, "bits_per_weight": 4.0625,
                         "rotating_copies": copies, "path": "valu"},
@@ -277,6 +281,112 @@ def run_quant(args, wl, cfg):
                 extra={"weights_per_s": round(n * k * K / elapsed, 1),
                        "mean_code_steps_per_block": round(float(steps.mean()), 3),
                        "max_code_steps_per_block": int(steps.max())})
+
+
+def cpu_baseline_twoplane(cfg, target_s: float = 10.0) -> dict:
+    """The oracle's two-plane pass (plain single-threaded C) over the workload's matrix,
+    one token per call, repeated to about target_s seconds."""
+    import oracle as oracle_pkg
+    from synth import gen
+
+    o = oracle_pkg.get()
+    n, k = cfg["n"], cfg["k"]
+    t1, t2, a = gen.two_plane_weights(gen.SEED, 0, n, k)
+    xs = gen.activations(gen.SEED, 1000, 64, k)
+    q, d, _ = o.quantize(xs)
+    t0 = time.perf_counter()
+    o.gemv2(t1, t2, a, q[:1], d[:1])
+    one = time.perf_counter() - t0
+    reps = int(max(1, min(64, round(target_s / max(one, 1e-6)))))
+    t0 = time.perf_counter()
+    for i in range(reps):
+        o.gemv2(t1, t2, a, q[i:i + 1], d[i:i + 1])
+    el = time.perf_counter() - t0
+    nbytes = reps * (two_plane_bytes(n, k) + k * 4 + n * 4)
+    return {"value": round(nbytes / el / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"the workload's {n} x {k} two-plane matrix, {reps} single-token passes (quantized "
+                      f"activations precomputed); {el:.1f} s on 1 host thread"}
+
+
+def two_plane_bytes(n: int, k: int) -> int:
+    return n * k // 2 + n * (k // 256) * 4
+
+
+def run_twoplane(args, wl, cfg):
+    """The free-scale two-plane pass on one decode step's routed gate and up rows, with
+    the folded pass over the same trit planes timed beside it."""
+    import torch
+    from paper_2608_08910_amd import tq
+    from synth import gen
+
+    n, k, seed = cfg["n"], cfg["k"], gen.SEED
+    kb = k // 256
+    K = args.steps if args.steps is not None else wl["steps"]
+    W = args.warmup if args.warmup is not None else wl["warmup"]
+    P = args.profile_steps if args.profile_steps is not None else wl["profile"]
+    copies = 8  # 8 x 69 MB per format > the 256 MB last-level cache
+    t1, t2, a = gen.two_plane_weights(seed, 0, n, k)
+    c2 = torch.from_numpy(tq.tq_pack2_host(t1, t2)).cuda()
+    s2 = torch.from_numpy(a.view(np.int16)).cuda()
+    cf = torch.from_numpy(tq.tq_fold_pack_host(t1, t2)).cuda()
+    sf = s2[:, :, 1].contiguous()
+    del t1, t2
+    mats2 = [tq.TqMatrix2(n, k, c2.clone(), s2.clone()) for _ in range(copies)]
+    matsf = [tq.TqMatrix(n, k, cf.clone(), sf.clone()) for _ in range(copies)]
+    total = W + K
+    x_all = torch.from_numpy(gen.activations(seed, 1000, total + 16, k)).cuda()
+    T_MAX = 16
+    q = torch.empty((T_MAX, k), dtype=torch.int8, device="cuda")
+    d = torch.empty((T_MAX, kb), dtype=torch.float32, device="cuda")
+    b = torch.empty((T_MAX, kb), dtype=torch.int32, device="cuda")
+    y = torch.empty((T_MAX, n), dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+
+    def step2(i):
+        tq.tq_quantize_act(x_all[i:i + 1], q[:1], d[:1], b[:1])
+        tq.tq_gemv2(mats2[i % copies], q[:1], d[:1], y[:1])
+
+    def stepf(i):
+        tq.tq_quantize_act(x_all[i:i + 1], q[:1], d[:1], b[:1])
+        tq.tq_gemv(matsf[i % copies], q[:1], d[:1], b[:1], y[:1])
+
+    elapsed = time_graph(step2, W, K)
+    elapsed_f = time_graph(stepf, W, K)
+    io = k * 4 + n * 4
+    gbs = (two_plane_bytes(n, k) + io) * K / elapsed / 1e9
+    gbs_f = (matrix_bytes(n, k) + io) * K / elapsed_f / 1e9
+
+    def kernel_ms(fn, t):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(P)]
+        torch.cuda.synchronize()
+        torch.cuda._sleep(int(2.4e9 * 0.02))
+        for j in range(P):
+            tq.tq_quantize_act(x_all[j:j + t], q[:t], d[:t], b[:t])
+            fn(j, t, ev[j])
+        torch.cuda.synchronize()
+        return float(np.mean([s.elapsed_time(e) for s, e in ev]))
+
+    def k2(j, t, ev):
+        tq.tq_gemv2_timed(mats2[j % copies], q[:t], d[:t], y[:t], ev)
+
+    def kf(j, t, ev):
+        tq.tq_gemv_timed(matsf[j % copies], q[:t], d[:t], b[:t], y[:t], ev)
+
+    by_tokens = {}
+    for t in (1, 4, 16):
+        m2, mf = kernel_ms(k2, t), kernel_ms(kf, t)
+        by_tokens[str(t)] = {"two_plane_ms": round(m2, 5), "folded_ms": round(mf, 5),
+                             "two_plane_GBps": round((two_plane_bytes(n, k) + t * (k + kb * 4 + n * 4)) / (m2 * 1e-3) / 1e9, 1),
+                             "folded_GBps": round((matrix_bytes(n, k) + t * (k + kb * 4 + n * 4)) / (mf * 1e-3) / 1e9, 1)}
+    ms = by_tokens["1"]["two_plane_ms"]
+    roof = hbm_roof("gemv2", two_plane_bytes(n, k) + k + kb * 4 + n * 4, ms, "k_gemv2<2, 1, 4, false>")
+    return dict(value=gbs, K=K, W=W, elapsed=elapsed, tokens=K, roof=roof,
+                config={"workload": cfg["name"], "n": n, "k": k, "tokens_per_step": 1, "bits_per_weight": 4.125,
+                        "rotating_copies": copies, "format": "free-scale two-plane (2 x 2-bit trit planes, 2 f16 scales "
+                                                             "per 256 weights)"},
+                extra={"folded_same_planes": {"value": round(gbs_f, 2), "ms_per_step": round(elapsed_f * 1e3 / K, 5),
+                                              "bits_per_weight": 4.0625},
+                       "kernel_ms_by_tokens": by_tokens})
 
 
 def run_moe(args, wl, cfg):
@@ -420,8 +530,8 @@ def main():
 
     torch.cuda.set_device(0)
     wl = WORKLOADS[args.workload]
-    cfg = gen.QUANT_CONFIG if wl["cfg"] == "quant" else gen.CONFIGS[wl["cfg"]]
-    run = {"gemv": run_gemv, "moe": run_moe, "quant": run_quant}[cfg["kind"]]
+    cfg = {"quant": gen.QUANT_CONFIG, "twoplane": gen.TWO_PLANE_CONFIG}.get(wl["cfg"]) or gen.CONFIGS[wl["cfg"]]
+    run = {"gemv": run_gemv, "moe": run_moe, "quant": run_quant, "twoplane": run_twoplane}[cfg["kind"]]
     r = run(args, wl, cfg)
     K, W, elapsed = r["K"], r["W"], r["elapsed"]
     res = {
@@ -447,6 +557,8 @@ def main():
         res["cpu_baseline"] = cpu_baseline(gen.SEED, cfg["hidden"], cfg["inter"], cfg["topk"])
     if not args.no_cpu_baseline and args.workload == "tiedquant":
         res["cpu_baseline"] = cpu_baseline_quant(cfg)
+    if not args.no_cpu_baseline and args.workload == "twoplane":
+        res["cpu_baseline"] = cpu_baseline_twoplane(cfg)
     print(json.dumps(res), flush=True)
 
 

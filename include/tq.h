@@ -163,6 +163,51 @@ tq_status tq_gemv(const tq_mat* w, const int8_t* q, const float* d, const int32_
 tq_status tq_gemv_timed(const tq_mat* w, const int8_t* q, const float* d, const int32_t* bsum,
                         int64_t t, float* y, int32_t* isum_dbg, void* stream, void* const* events);
 
+/* ---------------------------------------------------------------------------------
+ * Free-scale two-plane variant (Sec. 2.1: PTQTP's W ~ alpha1*T1 + alpha2*T2 with two
+ * free scales per group, the family the tie constrains; Sec. 4.1, the quality table's
+ * note: the free pair does not fold, and its serving format keeps two separate trit
+ * planes at 4.125 bits/weight). The ablation of the fold: same blocks, same activations,
+ * one integer pass per plane.
+ *   codes  [n][kb][128] bytes, 128-byte aligned. Chunk j (bytes 16j .. 16j+15 of a
+ *          block) covers columns 32j .. 32j+31: bytes 16j .. 16j+7 are plane 1, bytes
+ *          16j+8 .. 16j+15 plane 2. Within a plane's 8 bytes, byte 4u + b (u = 0, 1;
+ *          b = 0..3), bits 2s .. 2s+1 (s = 0..3) hold the trit of column
+ *          32j + 16u + 4s + b as 2-bit two's complement (00 = 0, 01 = +1, 11 = -1; 10
+ *          never occurs): shifted to a byte's top two bits it reads as 64*t.
+ *   scales [n][kb][2] IEEE binary16 bit patterns (alpha1, alpha2 of row r, block b),
+ *          4-byte aligned. Bytes: 128 + 4 per 256 weights = 4.125 bits/weight.
+ * Pass: isum_p[t][r][b] = sum_i Tp[r][256b+i] * q[t][256b+i] (exact int32, p = 1, 2),
+ *   y[t][r] = sum_b d[t][b] * (f32(alpha1) * isum_1 + f32(alpha2) * isum_2) in fp32.
+ * --------------------------------------------------------------------------------- */
+typedef struct {
+  int32_t n;
+  int32_t k;
+  const uint8_t* codes;
+  const uint16_t* scales; /* [n][kb][2] */
+} tq_mat2;
+
+/* Pack two trit planes on the host into the two-plane layout above. t1, t2: host
+ * [n][k] in {-1,0,1}; codes_out: host, tq_codes_bytes(n, k) bytes (the same byte count
+ * as the folded plane). TQ_ERR_INVALID if a trit is out of range (codes_out is then
+ * unspecified). The scales need no packing: [n][kb][2] f16 is their layout. */
+tq_status tq_pack2_host(const int8_t* t1, const int8_t* t2, int32_t n, int32_t k, uint8_t* codes_out);
+
+/* Inverse of tq_pack2_host on the host. TQ_ERR_INVALID on the unused pattern 10. */
+tq_status tq_unpack2_host(const uint8_t* codes, int32_t n, int32_t k, int8_t* t1_out, int8_t* t2_out);
+
+/* The two-plane pass for one matrix and t tokens (formula above). q, d as from
+ * tq_quantize_act (q 16-byte aligned). isum_dbg: NULL, or a [t][n][kb][2] int32 buffer
+ * that receives the exact per-plane block sums (plane 1 first). n >= 1, 256 <= k <=
+ * 16384, t >= 0 (t = 0 is a no-op). */
+tq_status tq_gemv2(const tq_mat2* w, const int8_t* q, const float* d, int64_t t, float* y,
+                   int32_t* isum_dbg, void* stream);
+
+/* As tq_gemv2, with the kernel's own start/stop timestamps in two host-created HIP
+ * events (as tq_gemv_timed). */
+tq_status tq_gemv2_timed(const tq_mat2* w, const int8_t* q, const float* d, int64_t t, float* y,
+                         int32_t* isum_dbg, void* stream, void* const* events);
+
 /* Routed-expert MoE layer over the folded experts (Sec. 2.2 dot pass applied to every
  * routed gate/up/down projection; the paper's layers are 43 x 3 projections x 256
  * experts, Sec. 2.1). For every token t and slot j < topk with e = topk_idx[t][j]:

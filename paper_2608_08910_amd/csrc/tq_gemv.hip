@@ -20,7 +20,9 @@
 
 namespace tq {
 
-template <int NL, int NT, int RPW>
+// LOOP = false: one chunk of at most NT tokens (t <= NT), no token loop, so nothing
+// loop-invariant is hoisted and kept live across it.
+template <int NL, int NT, int RPW, bool LOOP>
 __global__ __launch_bounds__(256) void k_gemv(const uint8_t* __restrict__ codes,
                                               const uint16_t* __restrict__ scales, int n, int kb,
                                               const int8_t* __restrict__ q, const float* __restrict__ d, int t,
@@ -34,24 +36,12 @@ __global__ __launch_bounds__(256) void k_gemv(const uint8_t* __restrict__ codes,
   if (row0 >= n) return;
   const int64_t k = (int64_t)kb * 256;
 
-  // Loads are unconditional from clamped addresses (a predicated load becomes a branch
-  // that serializes the loads): rows past n are computed and not stored, blocks past kb
-  // get d = 0 and add exactly nothing.
-  int c[RPW][NL][8];
-#pragma unroll
-  for (int r = 0; r < RPW; ++r) {
-    const int64_t rc = min(row0 + r, n - 1);
-#pragma unroll
-    for (int i = 0; i < NL; ++i) unpack16c(ldg16(codes + (rc * kb + min(8 * i + g, kb - 1)) * 128 + cp * 16), c[r][i]);
-  }
-  // after the block butterfly a lane keeps items of one row (RPW <= 8): its scales
-  const int lrow = min(row0 + rev_bits<clog2(RPW)>(lane & (RPW - 1)), n - 1);
-  float s[NL];
-#pragma unroll
-  for (int i = 0; i < NL; ++i) s[i] = f16_bits_to_f32(scales[(int64_t)lrow * kb + min(8 * i + g, kb - 1)]);
-
-  for (int t0 = 0; t0 < t; t0 += NT) {
-    int qa[NT][NL][8];
+  // The activations and block scales of a chunk of NT tokens. The first chunk's are
+  // requested before the weights: a compute unit returns loads in issue order, so these
+  // small, cache-resident loads would otherwise wait behind every weight load in flight.
+  int qa[NT][NL][8];
+  float dk[KI][NL];
+  auto load_acts = [&](int t0) {
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
@@ -62,18 +52,47 @@ __global__ __launch_bounds__(256) void k_gemv(const uint8_t* __restrict__ codes,
         qa[tt][i][0] = lo.x; qa[tt][i][1] = lo.y; qa[tt][i][2] = lo.z; qa[tt][i][3] = lo.w;
         qa[tt][i][4] = hi.x; qa[tt][i][5] = hi.y; qa[tt][i][6] = hi.z; qa[tt][i][7] = hi.w;
       }
-    // the lane's kept items: their tokens' block scales (zero past t or past kb)
-    float dk[KI][NL];
+    // the lane's kept items: their tokens' block scales (masked at use: a select here
+    // would make the compiler wait for these loads before issuing the weights)
 #pragma unroll
     for (int kk = 0; kk < KI; ++kk) {
       const int tok = t0 + RR::kept(kk, lane) % NT;
 #pragma unroll
       for (int i = 0; i < NL; ++i) {
         const int b = 8 * i + g;
-        const float dv = d[(int64_t)min(tok, t - 1) * kb + min(b, kb - 1)];
-        dk[kk][i] = (tok < t && b < kb) ? dv : 0.0f;
+        dk[kk][i] = d[(int64_t)min(tok, t - 1) * kb + min(b, kb - 1)];
       }
     }
+  };
+  load_acts(0);
+
+  // Loads are unconditional from clamped addresses (a predicated load becomes a branch
+  // that serializes the loads): rows past n are computed and not stored, blocks past kb
+  // get d = 0 and add exactly nothing. Buffer loads relative to the wave's first row:
+  // one 32-bit offset per load, no 64-bit address arithmetic per lane.
+  const int wrow0 = __builtin_amdgcn_readfirstlane(row0);
+  const int nrows = min(RPW, n - wrow0);
+  const __amdgpu_buffer_rsrc_t cr = make_rsrc(codes + (int64_t)wrow0 * kb * 128, (uint32_t)(nrows * kb * 128));
+  uint4 w[RPW][NL];
+#pragma unroll
+  for (int r = 0; r < RPW; ++r) {
+    const int rr = min(r, nrows - 1);
+#pragma unroll
+    for (int i = 0; i < NL; ++i) w[r][i] = buf_load16(cr, (uint32_t)((rr * kb + min(8 * i + g, kb - 1)) * 128 + cp * 16), 0);
+  }
+  // after the block butterfly a lane keeps items of one row (RPW <= 8): its scales
+  const int lrow = min(row0 + rev_bits<clog2(RPW)>(lane & (RPW - 1)), n - 1);
+  float s[NL];
+#pragma unroll
+  for (int i = 0; i < NL; ++i) s[i] = f16_bits_to_f32(scales[(int64_t)lrow * kb + min(8 * i + g, kb - 1)]);
+
+  __builtin_amdgcn_sched_barrier(0);  // every load above is issued before any math
+
+  // t >= 1 (the launcher returns early for t == 0): a do-while keeps the loads above
+  // in the kernel's entry block instead of sinking them under a loop guard
+  int t0 = 0;
+  do {
+    if (t0 > 0) load_acts(t0);
     float acc[KI];
 #pragma unroll
     for (int kk = 0; kk < KI; ++kk) acc[kk] = 0.0f;
@@ -83,14 +102,20 @@ __global__ __launch_bounds__(256) void k_gemv(const uint8_t* __restrict__ codes,
 #pragma unroll
       for (int r = 0; r < RPW; ++r)
 #pragma unroll
-        for (int tt = 0; tt < NT; ++tt) p[r * NT + tt] = dot32x16(c[r][i], qa[tt][i]);
+        for (int tt = 0; tt < NT; ++tt) {
+          int c[8];
+          unpack16c(w[r][i], c);
+          p[r * NT + tt] = dot32x16(c, qa[tt][i]);
+        }
       RR::block_sums(p);
 #pragma unroll
       for (int kk = 0; kk < KI; ++kk) {
         const int is = p[kk] >> 4;  // exact block sum of c * q
-        acc[kk] = fmaf(s[i] * dk[kk][i], (float)is, acc[kk]);
+        const int tok = t0 + RR::kept(kk, lane) % NT, b = 8 * i + g;
+        const float dv = (tok < t && b < kb) ? dk[kk][i] : 0.0f;
+        acc[kk] = fmaf(s[i] * dv, (float)is, acc[kk]);
         if (isum_dbg != nullptr && RR::block_writer(lane)) {
-          const int it = RR::kept(kk, lane), tok = t0 + it % NT, row = row0 + it / NT, b = 8 * i + g;
+          const int row = row0 + RR::kept(kk, lane) / NT;
           if (tok < t && row < n && b < kb) isum_dbg[((int64_t)tok * n + row) * kb + b] = is;
         }
       }
@@ -100,16 +125,24 @@ __global__ __launch_bounds__(256) void k_gemv(const uint8_t* __restrict__ codes,
       const int it = RR::item(lane), tok = t0 + it % NT, row = row0 + it / NT;
       if (tok < t && row < n) y[(int64_t)tok * n + row] = acc[0];
     }
-  }
+    t0 += NT;
+  } while (LOOP && t0 < t);
 }
 
 using gemv_fn = void (*)(const uint8_t*, const uint16_t*, int, int, const int8_t*, const float*, int, float*,
                          int32_t*);
 
+// Four rows per wave only where a row is at most two loads (the launcher's rule).
 template <int NL>
 static gemv_fn pick_gemv_nl(int nt, int rpw) {
-  if (nt == 1) return rpw == 1 ? k_gemv<NL, 1, 1> : k_gemv<NL, 1, 4>;
-  return rpw == 1 ? k_gemv<NL, 4, 1> : k_gemv<NL, 4, 4>;
+  // one token: a single pass; several: chunks of four
+  if constexpr (NL <= 2) {
+    if (nt == 1) return rpw == 1 ? k_gemv<NL, 1, 1, false> : k_gemv<NL, 1, 4, false>;
+    return rpw == 1 ? k_gemv<NL, 4, 1, true> : k_gemv<NL, 4, 4, true>;
+  } else {
+    (void)rpw;
+    return nt == 1 ? k_gemv<NL, 1, 1, false> : k_gemv<NL, 4, 1, true>;
+  }
 }
 
 static gemv_fn pick_gemv(int nl, int nt, int rpw) {
@@ -128,6 +161,11 @@ static gemv_fn pick_gemv(int nl, int nt, int rpw) {
 }  // namespace tq
 
 namespace tq {
+// Rows per wave for large matrices when several tokens share a chunk (build-time knob).
+#ifndef TQ_GEMV_RPW_MULTI
+#define TQ_GEMV_RPW_MULTI 4
+#endif
+
 static tq_status gemv_run(const tq_mat* w, const int8_t* q, const float* d, const int32_t* bsum, int64_t t, float* y,
                           int32_t* isum_dbg, void* stream, void* const* events) {
   if (!w) return fail(TQ_ERR_INVALID, "tq_gemv: null matrix descriptor");
@@ -147,7 +185,7 @@ static tq_status gemv_run(const tq_mat* w, const int8_t* q, const float* d, cons
   const int kb = k / 256, nl = (kb + 7) / 8;
   const int nt = t == 1 ? 1 : 4;
   // Few rows: one row per wave, to spread a small matrix over all CUs.
-  const int rpw = (n >= 16384 && nl <= 2) ? 4 : 1;
+  const int rpw = (n >= 16384 && nl <= 2) ? (nt == 1 ? 4 : TQ_GEMV_RPW_MULTI) : 1;
   const int64_t waves = (n + rpw - 1) / rpw;
   const unsigned wgs = (unsigned)((waves + 3) / 4);
   (void)hipGetLastError();

@@ -65,3 +65,65 @@ extern "C" tq_status tq_unpack_host(const uint8_t* codes, int32_t n, int32_t k, 
     }
   return TQ_OK;
 }
+
+// Free-scale two-plane layout (Sec. 2.1 alpha1*T1 + alpha2*T2; Sec. 4.1 two separate trit
+// planes at 4.125 bits per weight): block byte 16j + 8p + 4u + b, bit pair 2s, holds
+// plane p+1's trit of column 32j + 16u + 4s + b as 2-bit two's complement.
+static inline int64_t plane_byte(int j, int p, int u, int b) { return 16 * j + 8 * p + 4 * u + b; }
+
+extern "C" tq_status tq_pack2_host(const int8_t* t1, const int8_t* t2, int32_t n, int32_t k, uint8_t* codes_out) {
+  using namespace tq;
+  clear_error();
+  if (n < 0 || k <= 0 || k % 256 != 0)
+    return fail(TQ_ERR_INVALID, "tq_pack2_host: bad shape n=%d k=%d (k must be a multiple of 256)", n, k);
+  if (n == 0) return TQ_OK;
+  if (!t1 || !t2 || !codes_out) return fail(TQ_ERR_INVALID, "tq_pack2_host: null pointer");
+  const int64_t kb = k / 256;
+  for (int64_t r = 0; r < n; ++r)
+    for (int64_t blk = 0; blk < kb; ++blk) {
+      const int64_t col0 = r * k + blk * 256;
+      uint8_t* out = codes_out + (r * kb + blk) * 128;
+      std::memset(out, 0, 128);
+      for (int j = 0; j < 8; ++j)
+        for (int u = 0; u < 2; ++u)
+          for (int sh = 0; sh < 4; ++sh)
+            for (int b = 0; b < 4; ++b) {
+              const int64_t col = col0 + 32 * j + 16 * u + 4 * sh + b;
+              const int v[2] = {t1[col], t2[col]};
+              for (int p = 0; p < 2; ++p) {
+                if (v[p] < -1 || v[p] > 1)
+                  return fail(TQ_ERR_INVALID, "tq_pack2_host: trit out of range at element %lld", (long long)col);
+                out[plane_byte(j, p, u, b)] |= (uint8_t)((v[p] & 3) << (2 * sh));
+              }
+            }
+    }
+  return TQ_OK;
+}
+
+extern "C" tq_status tq_unpack2_host(const uint8_t* codes, int32_t n, int32_t k, int8_t* t1_out, int8_t* t2_out) {
+  using namespace tq;
+  clear_error();
+  if (n < 0 || k <= 0 || k % 256 != 0)
+    return fail(TQ_ERR_INVALID, "tq_unpack2_host: bad shape n=%d k=%d (k must be a multiple of 256)", n, k);
+  if (n == 0) return TQ_OK;
+  if (!codes || !t1_out || !t2_out) return fail(TQ_ERR_INVALID, "tq_unpack2_host: null pointer");
+  const int64_t kb = k / 256;
+  int8_t* outs[2] = {t1_out, t2_out};
+  for (int64_t r = 0; r < n; ++r)
+    for (int64_t blk = 0; blk < kb; ++blk) {
+      const int64_t col0 = r * k + blk * 256;
+      const uint8_t* in = codes + (r * kb + blk) * 128;
+      for (int j = 0; j < 8; ++j)
+        for (int u = 0; u < 2; ++u)
+          for (int sh = 0; sh < 4; ++sh)
+            for (int b = 0; b < 4; ++b)
+              for (int p = 0; p < 2; ++p) {
+                const int f = (in[plane_byte(j, p, u, b)] >> (2 * sh)) & 3;
+                if (f == 2)
+                  return fail(TQ_ERR_INVALID, "tq_unpack2_host: invalid trit pattern in block (%lld, %lld)",
+                              (long long)r, (long long)blk);
+                outs[p][col0 + 32 * j + 16 * u + 4 * sh + b] = (int8_t)(f == 3 ? -1 : f);
+              }
+    }
+  return TQ_OK;
+}

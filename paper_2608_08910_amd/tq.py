@@ -40,6 +40,10 @@ class tq_mat(ctypes.Structure):
     _fields_ = [("n", ctypes.c_int32), ("k", ctypes.c_int32), ("codes", ctypes.c_void_p), ("scales", ctypes.c_void_p)]
 
 
+class tq_mat2(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("k", ctypes.c_int32), ("codes", ctypes.c_void_p), ("scales", ctypes.c_void_p)]
+
+
 class tq_experts(ctypes.Structure):
     _fields_ = [
         ("n_experts", ctypes.c_int32), ("hidden", ctypes.c_int32), ("inter", ctypes.c_int32),
@@ -70,6 +74,10 @@ for _name, _args, _res in [
     ("tq_tied_quantize", [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp], _i32),
     ("tq_gemv", [_P(tq_mat), _vp, _vp, _vp, _i64, _vp, _vp, _vp], _i32),
     ("tq_gemv_timed", [_P(tq_mat), _vp, _vp, _vp, _i64, _vp, _vp, _vp, _P(_vp)], _i32),
+    ("tq_pack2_host", [_vp, _vp, _i32, _i32, _vp], _i32),
+    ("tq_unpack2_host", [_vp, _i32, _i32, _vp, _vp], _i32),
+    ("tq_gemv2", [_P(tq_mat2), _vp, _vp, _i64, _vp, _vp, _vp], _i32),
+    ("tq_gemv2_timed", [_P(tq_mat2), _vp, _vp, _i64, _vp, _vp, _vp, _P(_vp)], _i32),
     ("tq_moe_workspace_bytes", [_P(tq_experts), _i64, _i32], _sz),
     ("tq_moe_path", [_P(tq_experts), _i64, _i32, _i32], _i32),
     ("tq_moe_workspace_layout", [_P(tq_experts), _i64, _i32, _P(tq_moe_layout)], _i32),
@@ -219,6 +227,67 @@ def tq_gemv_timed(m: TqMatrix, q: torch.Tensor, d: torch.Tensor, bsum: torch.Ten
     _ok(_L.tq_gemv_timed(ctypes.byref(desc), _dev(q, torch.int8, "q", (t, m.k)), _dev(d, torch.float32, "d", (t, m.k // 256)),
                          _dev(bsum, torch.int32, "bsum", (t, m.k // 256)), t, _dev(y, torch.float32, "y", (t, m.n)), dbg,
                          _stream(stream), arr))
+
+
+# -- free-scale two-plane variant -----------------------------------------------------------
+
+def tq_pack2_host(t1: np.ndarray, t2: np.ndarray) -> np.ndarray:
+    """Host pack of two trit planes [n][k] into two-plane codes [n][k/256][128] (uint8)."""
+    n, k = t1.shape
+    out = np.empty((n, k // 256, 128), dtype=np.uint8)
+    _ok(_L.tq_pack2_host(_host(t1, np.int8, "t1"), _host(t2, np.int8, "t2", (n, k)), n, k, _host(out, np.uint8, "codes")))
+    return out
+
+
+def tq_unpack2_host(codes: np.ndarray, n: int, k: int):
+    t1 = np.empty((n, k), dtype=np.int8)
+    t2 = np.empty((n, k), dtype=np.int8)
+    _ok(_L.tq_unpack2_host(_host(codes, np.uint8, "codes"), n, k, _host(t1, np.int8, "t1_out"), _host(t2, np.int8, "t2_out")))
+    return t1, t2
+
+
+@dataclass
+class TqMatrix2:
+    """One matrix in the two-plane layout: codes [n][kb][128] uint8, scales [n][kb][2]
+    int16 (alpha1, alpha2 as f16 bit patterns)."""
+    n: int
+    k: int
+    codes: torch.Tensor
+    scales: torch.Tensor
+
+    @staticmethod
+    def empty(n: int, k: int, device="cuda") -> "TqMatrix2":
+        return TqMatrix2(n, k, torch.empty((n, k // 256, 128), dtype=torch.uint8, device=device),
+                         torch.empty((n, k // 256, 2), dtype=torch.int16, device=device))
+
+    def desc(self) -> tq_mat2:
+        _dev(self.codes, torch.uint8, "codes", (self.n, self.k // 256, 128))
+        _dev(self.scales, torch.int16, "scales", (self.n, self.k // 256, 2))
+        return tq_mat2(self.n, self.k, self.codes.data_ptr(), self.scales.data_ptr())
+
+
+def _gemv2_args(m: TqMatrix2, q, d, y, isum_dbg):
+    t = q.shape[0]
+    desc = m.desc()
+    dbg = None if isum_dbg is None else _dev(isum_dbg, torch.int32, "isum_dbg", (t, m.n, m.k // 256, 2))
+    return (ctypes.byref(desc), _dev(q, torch.int8, "q", (t, m.k)), _dev(d, torch.float32, "d", (t, m.k // 256)), t,
+            _dev(y, torch.float32, "y", (t, m.n)), dbg)
+
+
+def tq_gemv2(m: TqMatrix2, q: torch.Tensor, d: torch.Tensor, y: torch.Tensor, isum_dbg: torch.Tensor | None = None,
+             stream=None):
+    _ok(_L.tq_gemv2(*_gemv2_args(m, q, d, y, isum_dbg), _stream(stream)))
+
+
+def tq_gemv2_timed(m: TqMatrix2, q: torch.Tensor, d: torch.Tensor, y: torch.Tensor, events,
+                   isum_dbg: torch.Tensor | None = None, stream=None):
+    if len(events) != 2:
+        raise ValueError("need 2 events")
+    for ev in events:  # torch creates the HIP event on its first record
+        if ev.cuda_event == 0:
+            ev.record()
+    arr = (_vp * 2)(*[ev.cuda_event for ev in events])
+    _ok(_L.tq_gemv2_timed(*_gemv2_args(m, q, d, y, isum_dbg), _stream(stream), arr))
 
 
 # -- routed-expert MoE layer ----------------------------------------------------------------

@@ -1,7 +1,8 @@
 """Seeded synthetic inputs for the tied-trit-plane expert dot pass.
 
 This module holds random draws only: activations, per-token scale factors, routing
-indices and routing weights, fp32 weights for the tied quantizer, and the 64-bit keys
+indices and routing weights, fp32 weights for the tied quantizer, trit planes and scale
+pairs for the free-scale two-plane variant, and the 64-bit keys
 that name each weight matrix's counter-based stream. None of the method's arithmetic (fold, pack, quantize, integer
 dot, scale combine, SiLU, weighted combine) lives here; both the CPU oracle and the
 HIP path consume these draws, and each implements the method on its own.
@@ -54,6 +55,7 @@ _TAG_FACTOR = 4
 _TAG_KEY = 5
 _TAG_BENCH = 6
 _TAG_FWEIGHT = 7
+_TAG_TWOPLANE = 8
 
 PROJ_GATE, PROJ_UP, PROJ_DOWN = 0, 1, 2
 
@@ -82,6 +84,12 @@ CONFIGS = {
 QUANT_CONFIG = dict(name="tied_quantize_m32_2048x4096", kind="quant", matrices=32, n=2048, k=4096)
 
 
+# The free-scale two-plane variant's workload: one decode step's routed gate and up rows
+# (8 experts x 2 x 2048 rows of 4096 inputs) as one stacked matrix, one token, served
+# from the two-plane layout; the folded layout of the same planes is timed beside it.
+TWO_PLANE_CONFIG = dict(name="twoplane_gemv_32768x4096_t1", kind="twoplane", n=32768, k=4096, tokens=1)
+
+
 def _rng(*key: int) -> np.random.Generator:
     return np.random.default_rng(np.random.SeedSequence(entropy=int(key[0]), spawn_key=tuple(int(v) for v in key[1:])))
 
@@ -108,6 +116,20 @@ def float_weights(seed: int, index: int, n: int, k: int) -> np.ndarray:
     r = _rng(seed, _TAG_FWEIGHT, index)
     sigma = np.exp(np.log(0.005) + r.random((n, 1)) * (np.log(0.05) - np.log(0.005)))
     return (r.standard_normal((n, k), dtype=np.float32) * sigma.astype(np.float32)).astype(np.float32)
+
+
+def two_plane_weights(seed: int, index: int, n: int, k: int):
+    """A free-scale two-plane matrix: trit planes t1, t2 [n][k] (int8, uniform on
+    {-1, 0, 1}) and scale pairs [n][k/256][2] as f16 bit patterns (uint16): alpha2
+    log-uniform on [1e-3, 1e-1], alpha1 = alpha2 times 3 * U(0.75, 1.25), i.e. near the
+    tied ratio with a +-25% spread."""
+    r = _rng(seed, _TAG_TWOPLANE, index)
+    t1 = r.integers(-1, 2, (n, k), dtype=np.int8)
+    t2 = r.integers(-1, 2, (n, k), dtype=np.int8)
+    a2 = np.exp(r.uniform(np.log(1e-3), np.log(1e-1), (n, k // 256)))
+    a1 = a2 * 3.0 * r.uniform(0.75, 1.25, (n, k // 256))
+    a = np.stack([a1, a2], axis=2).astype(np.float16).view(np.uint16)
+    return t1, t2, np.ascontiguousarray(a)
 
 
 def token_factors(seed: int, tokens: int) -> np.ndarray:

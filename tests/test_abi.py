@@ -91,6 +91,55 @@ def test_fold_pack_rejects_bad_trits_and_unpack_bad_nibbles():
     assert tq.tq_unpack_host(c2, 1, 256)[0, 5] == 4 and tq.tq_unpack_host(c2, 1, 256)[0, 21] == -4
 
 
+def test_two_plane_size_is_paper_bits_per_weight():
+    # two trit planes at 2 bits plus two f16 scales per 256 weights (Table 1: 4.125)
+    want = GOLDEN["bits_per_weight"]["free_scale_two_plane"]
+    for n, k in ((2048, 4096), (4096, 2048), (1, 256)):
+        total = tq.tq_codes_bytes(n, k) + 2 * tq.tq_scales_bytes(n, k)
+        assert total * 8 / (n * k) == want
+
+
+def test_pack2_layout_bytes_hand_built():
+    # byte 16j + 8p + 4u + b, bits 2s..2s+1 = plane p's trit of column 32j + 16u + 4s + b,
+    # 2-bit two's complement; shifted to the byte's top pair it reads as 64t
+    cols = np.arange(256)
+    t1 = ((cols * 5) % 3 - 1).astype(np.int8)
+    t2 = ((cols * 7 + 1) % 3 - 1).astype(np.int8)
+    codes = tq.tq_pack2_host(t1[None], t2[None])[0, 0]
+    for j in range(8):
+        for p, tp in enumerate((t1, t2)):
+            for u in range(2):
+                for b in range(4):
+                    byte = int(codes[16 * j + 8 * p + 4 * u + b])
+                    for sh in range(4):
+                        col = 32 * j + 16 * u + 4 * sh + b
+                        assert (byte >> (2 * sh)) & 3 == int(tp[col]) & 3
+                        top = np.array([(byte << (6 - 2 * sh)) & 0xC0], np.uint8).view(np.int8)[0]
+                        assert int(top) == 64 * int(tp[col])
+
+
+def test_pack2_round_trip_and_rejections():
+    rng = np.random.default_rng(5)
+    for n, k in ((3, 256), (4, 768), (2, 7168)):
+        t1 = rng.integers(-1, 2, (n, k)).astype(np.int8)
+        t2 = rng.integers(-1, 2, (n, k)).astype(np.int8)
+        codes = tq.tq_pack2_host(t1, t2)
+        assert codes.shape == (n, k // 256, 128)
+        u1, u2 = tq.tq_unpack2_host(codes, n, k)
+        assert np.array_equal(u1, t1) and np.array_equal(u2, t2)
+        pairs = np.stack([(codes >> (2 * s)) & 3 for s in range(4)])
+        assert not (pairs == 2).any()  # the unused pattern never occurs
+    z = np.zeros((1, 256), np.int8)
+    bad = z.copy(); bad[0, 9] = -2
+    with pytest.raises(tq.TqError) as e:
+        tq.tq_pack2_host(z, bad)
+    assert e.value.status == tq.TQ_ERR_INVALID and "trit" in str(e.value)
+    codes = tq.tq_pack2_host(z, z)
+    codes[0, 0, 3] = 0x08  # pattern 10 in bits 2..3
+    with pytest.raises(tq.TqError):
+        tq.tq_unpack2_host(codes, 1, 256)
+
+
 FAKE = 0x7F0000000000  # 256-byte aligned, never dereferenced: every call below is invalid
 
 
@@ -113,6 +162,26 @@ def test_gemv_validation_errors_before_launch():
     assert st == tq.TQ_ERR_ALIGN  # q must be 16-byte aligned
     # t == 0 is a no-op that touches nothing
     assert L.tq_gemv(ctypes.byref(tq.tq_mat(16, 4096, FAKE, FAKE)), FAKE, FAKE, FAKE, 0, FAKE, None, None) == tq.TQ_OK
+
+
+@no_gpu_only
+def test_gemv2_validation_errors_before_launch():
+    L = tq._L
+    cases = [
+        (tq.tq_mat2(0, 4096, FAKE, FAKE), 1, tq.TQ_ERR_INVALID),       # n < 1
+        (tq.tq_mat2(16, 300, FAKE, FAKE), 1, tq.TQ_ERR_INVALID),       # k % 256
+        (tq.tq_mat2(16, 32768, FAKE, FAKE), 1, tq.TQ_ERR_INVALID),     # k too large
+        (tq.tq_mat2(16, 4096, FAKE + 16, FAKE), 1, tq.TQ_ERR_ALIGN),   # codes alignment
+        (tq.tq_mat2(16, 4096, FAKE, FAKE + 2), 1, tq.TQ_ERR_ALIGN),    # scale pairs: 4 bytes
+        (tq.tq_mat2(16, 4096, None, FAKE), 1, tq.TQ_ERR_INVALID),      # null codes
+        (tq.tq_mat2(16, 4096, FAKE, FAKE), -1, tq.TQ_ERR_INVALID),     # t < 0
+    ]
+    for m, t, want in cases:
+        st = L.tq_gemv2(ctypes.byref(m), FAKE, FAKE, t, FAKE, None, None)
+        assert st == want, (m.n, m.k, t, st, tq.tq_last_error())
+        assert tq.tq_last_error()
+    assert L.tq_gemv2(ctypes.byref(tq.tq_mat2(16, 4096, FAKE, FAKE)), FAKE + 4, FAKE, 1, FAKE, None, None) == tq.TQ_ERR_ALIGN
+    assert L.tq_gemv2(ctypes.byref(tq.tq_mat2(16, 4096, FAKE, FAKE)), FAKE, FAKE, 0, FAKE, None, None) == tq.TQ_OK
 
 
 @no_gpu_only
