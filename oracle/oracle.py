@@ -12,6 +12,8 @@ Definitions followed (paper sections):
                              rounding rule are this oracle's stated reading)
   integer dot + combine .... Sec. 2.2 (one integer dot pass, one float multiply-add
                              per block), evaluated exactly / in fp64
+  MXFP4 arm ................ Sec. 2.3 (doubled-e2m1 integer dot, e8m0 scale per 32
+                             absorbing the /2) with Sec. 2.1's description of the format
   free-scale two planes .... Sec. 2.1 (alpha1*T1 + alpha2*T2, free scales) and Sec. 4.1
                              (the unfolded pair is served as two trit planes at 4.125
                              bits per weight, one integer pass per plane)
@@ -65,6 +67,10 @@ class Oracle:
             ("orc_dot_i8", [_vp, _vp, _i64], ctypes.c_int64),
             ("orc_gemv", [_vp, _vp, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _vp], ctypes.c_int),
             ("orc_gemv2", [_vp, _vp, _vp, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _vp], ctypes.c_int),
+            ("orc_e2m1_to_f64", [ctypes.c_uint8], ctypes.c_double),
+            ("orc_e2m1_doubled", [ctypes.c_uint8], ctypes.c_int),
+            ("orc_e8m0_to_f64", [ctypes.c_uint8], ctypes.c_double),
+            ("orc_gemv_mx", [_vp, _vp, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _vp], ctypes.c_int),
             ("orc_splitmix64_word", [ctypes.c_uint64, ctypes.c_uint64], ctypes.c_uint64),
             ("orc_synth_matrix", [ctypes.c_uint64, _i64, _i64, _i64, _i64, _vp, _vp, _vp], ctypes.c_int),
             ("orc_f32_to_f16", [ctypes.c_float], ctypes.c_uint16),
@@ -175,6 +181,36 @@ class Oracle:
         isum = np.empty((t, n, k // 256, 2), dtype=np.int32) if want_isum else None
         self._check(self._L.orc_gemv2(_p(t1), _p(t2), _p(a), n, k, _p(q), _p(d), t, _p(y), _p(ab),
                                       _p(isum) if want_isum else None), "gemv2")
+        return (y, ab, isum) if want_isum else (y, ab)
+
+    # -- MXFP4 reference arm (Sec. 2.3) ---------------------------------------------
+    def e2m1_to_f64(self, code: int) -> float:
+        return float(self._L.orc_e2m1_to_f64(code))
+
+    def e2m1_doubled(self, code: int) -> int:
+        return int(self._L.orc_e2m1_doubled(code))
+
+    def e8m0_to_f64(self, e: int) -> float:
+        return float(self._L.orc_e8m0_to_f64(e))
+
+    def gemv_mx(self, c4, e8, q, d, want_isum: bool = False):
+        """MXFP4 integer arm: c4 [n][k] e2m1 codes (0..15), e8 [n][k/32] e8m0 scales.
+        y[t][r], absref[t][r] in fp64 (and isum [t][r][k/32] int32 if asked)."""
+        c4 = np.ascontiguousarray(c4, dtype=np.uint8)
+        e8 = np.ascontiguousarray(e8, dtype=np.uint8)
+        q = np.ascontiguousarray(q, dtype=np.int8)
+        d = np.ascontiguousarray(d, dtype=np.float32)
+        if q.ndim == 1:
+            q = q[None, :]
+            d = d.reshape(1, -1)
+        n, k = c4.shape
+        t = q.shape[0]
+        assert e8.shape == (n, k // 32) and q.shape == (t, k) and d.shape == (t, k // 256)
+        y = np.empty((t, n), dtype=np.float64)
+        ab = np.empty((t, n), dtype=np.float64)
+        isum = np.empty((t, n, k // 32), dtype=np.int32) if want_isum else None
+        self._check(self._L.orc_gemv_mx(_p(c4), _p(e8), n, k, _p(q), _p(d), t, _p(y), _p(ab),
+                                        _p(isum) if want_isum else None), "gemv_mx")
         return (y, ab, isum) if want_isum else (y, ab)
 
     # -- synthetic weights (input generation; SplitMix64 counter stream) -------------

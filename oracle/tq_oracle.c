@@ -27,6 +27,14 @@
  *   orc_gemv ................ trit-plane identity 3(T1.q)+(T2.q), offset form, exact
  *                             integer products at unit scales, power-of-two scaling,
  *                             dequantized-matmul error bound, exact rational brute force
+ *   orc_e2m1_to_f64 ......... the OCP table of e2m1 magnitudes (the paper's doubled set
+ *                             halved), sign symmetry, monotone magnitudes
+ *   orc_e2m1_doubled ........ the paper's doubled set; 2x the float decode, all codes
+ *   orc_e8m0_to_f64 ......... numpy's ldexp for every E, NaN at 255
+ *   orc_gemv_mx ............. the /2 absorbed exactly (equal to the float-dequantized
+ *                             dot in exact rational arithmetic), block-scale exponent
+ *                             steps double y exactly, per-32 isum against numpy,
+ *                             exact rational brute force
  *   orc_gemv2 ............... tied scales (3s, s) reproduce the folded pass (integer
  *                             identity 3(T1.q)+(T2.q)), one empty plane reduces to a
  *                             single ternary plane, plane exchange, sign symmetry,
@@ -243,6 +251,63 @@ int orc_gemv2(const int8_t* t1, const int8_t* t2, const uint16_t* a, int64_t n, 
         acc += term1;
         acc += term2;
         aacc += fabs(term1) + fabs(term2);
+      }
+      y[tt * n + r] = acc;
+      if (absref) absref[tt * n + r] = aacc;
+    }
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------------ */
+/* MXFP4 reference arm (Sec. 2.3; Sec. 2.1 for the format: fp4-e2m1 codes with one    */
+/* e8m0 scale per 32 elements). e2m1 is 1 sign bit, 2 exponent bits (bias 1) and 1    */
+/* mantissa bit; exponent 0 is subnormal. e8m0 is a biased power of two, 2^(E - 127), */
+/* with E = 255 reserved for NaN. The integer arm dots the doubled magnitudes (the     */
+/* e2m1 values times 2 are integers) against the int8 activations per 32-element      */
+/* block and folds the /2 into the power-of-two scale: 2^(E - 127) / 2 = 2^(E - 128).  */
+/* ------------------------------------------------------------------------------ */
+
+/* Value of an e2m1 code (low 4 bits of `code`) from the format definition. */
+double orc_e2m1_to_f64(uint8_t code) {
+  int sign = (code >> 3) & 1, e = (code >> 1) & 3, m = code & 1;
+  double v = (e == 0) ? 0.5 * m : ldexp(1.0 + 0.5 * m, e - 1);
+  return sign ? -v : v;
+}
+
+/* 2 * value of an e2m1 code, an integer in {0, +-1, +-2, +-3, +-4, +-6, +-8, +-12}. */
+int orc_e2m1_doubled(uint8_t code) {
+  int sign = (code >> 3) & 1, e = (code >> 1) & 3, m = code & 1;
+  int v = (e == 0) ? m : (2 + m) << (e - 1);
+  return sign ? -v : v;
+}
+
+/* Value of an e8m0 scale: 2^(E - 127); NaN for E = 255. */
+double orc_e8m0_to_f64(uint8_t e) { return e == 255 ? NAN : ldexp(1.0, (int)e - 127); }
+
+/* The integer arm's pass: c4 [n][k] e2m1 codes (0..15), e8 [n][k/32] e8m0 scales,
+ * q [t][k], d [t][k/256]. For every 32-element block j (within 256-block b = j / 8):
+ *   isum[t][r][j] = sum_i doubled(c4[r][32j+i]) * q[t][32j+i]   (exact),
+ *   y[t][r] = sum_j 2^(E[r][j] - 128) * d[t][b] * isum[t][r][j]  (fp64, ascending j);
+ * absref[t][r] = sum of the terms' magnitudes. isum (nullable): [t][n][k/32]. */
+int orc_gemv_mx(const uint8_t* c4, const uint8_t* e8, int64_t n, int64_t k, const int8_t* q,
+                const float* d, int64_t t, double* y, double* absref, int32_t* isum) {
+  if (k % 256 != 0) return ORC_BAD_INPUT;
+  int64_t kb = k / 256, k32 = k / 32;
+  for (int64_t i = 0; i < n * k; ++i)
+    if (c4[i] > 15) return ORC_BAD_INPUT;
+  for (int64_t i = 0; i < n * k32; ++i)
+    if (e8[i] == 255) return ORC_BAD_INPUT;
+  for (int64_t tt = 0; tt < t; ++tt)
+    for (int64_t r = 0; r < n; ++r) {
+      double acc = 0.0, aacc = 0.0;
+      for (int64_t j = 0; j < k32; ++j) {
+        int64_t v = 0;
+        for (int i = 0; i < 32; ++i)
+          v += (int64_t)orc_e2m1_doubled(c4[r * k + 32 * j + i]) * (int64_t)q[tt * k + 32 * j + i];
+        if (isum) isum[(tt * n + r) * k32 + j] = (int32_t)v;
+        double term = ldexp(1.0, (int)e8[r * k32 + j] - 128) * (double)d[tt * kb + j / 8] * (double)v;
+        acc += term;
+        aacc += fabs(term);
       }
       y[tt * n + r] = acc;
       if (absref) absref[tt * n + r] = aacc;

@@ -77,6 +77,22 @@ def gemv2_exact(t1, t2, a, q, d):
     return out
 
 
+def gemv_mx_exact(e2m1_values, c4, e8, q, d):
+    """MXFP4 pass in exact rationals from the float decode: weights = e2m1 value (from
+    the given 16-entry table) * 2^(E - 127), activations = d * q. c4: rows of codes, e8:
+    rows of exponents per 32, q: list of ints, d: list of fp32 per 256."""
+    k = len(q)
+    out = []
+    for r in range(len(c4)):
+        acc = Fraction(0)
+        for i in range(k):
+            e = int(e8[r][i // 32]) - 127
+            scale = Fraction(2) ** e
+            acc += Fraction(e2m1_values[int(c4[r][i])]) * scale * Fraction(float(d[i // 256])) * int(q[i])
+        out.append(acc)
+    return out
+
+
 def silu(z: float) -> float:
     return z / (1.0 + math.exp(-z))
 

@@ -454,6 +454,84 @@ def gemv2_matches_exact_rational_brute_force(o):
 
 
 # --------------------------------------------------------------------------------------
+# MXFP4 reference arm (Sec. 2.3: doubled-e2m1 integers, e8m0 scale per 32 absorbing /2)
+# --------------------------------------------------------------------------------------
+
+def _paper_e2m1_values():
+    """e2m1 values of codes 0..15 from the paper's doubled set (Sec. 2.3) halved; codes
+    8..15 are the negatives (the format's top bit is the sign)."""
+    mags = [Fraction(v, 2) for v in GOLDEN["doubled_e2m1_magnitudes"]["values"]]
+    return mags + [-m for m in mags]
+
+
+@pin
+def e2m1_decodes_match_the_paper_set(o):
+    doubled = GOLDEN["doubled_e2m1_magnitudes"]["values"]
+    assert [o.e2m1_doubled(c) for c in range(8)] == doubled
+    assert [o.e2m1_doubled(c | 8) for c in range(8)] == [-v for v in doubled]
+    vals = _paper_e2m1_values()
+    for c in range(16):
+        assert Fraction(o.e2m1_to_f64(c)) == vals[c]
+        assert 2 * Fraction(o.e2m1_to_f64(c)) == o.e2m1_doubled(c)
+    assert np.signbit(o.e2m1_to_f64(8))  # the sign bit of code 8 is a negative zero
+
+
+@pin
+def e8m0_matches_numpy_ldexp(o):
+    for e in range(255):
+        assert o.e8m0_to_f64(e) == float(np.ldexp(1.0, e - 127))
+    assert np.isnan(o.e8m0_to_f64(255))
+
+
+def _mx_case(rng, n, k, t):
+    c4 = rng.integers(0, 16, (n, k)).astype(np.uint8)
+    e8 = rng.integers(110, 135, (n, k // 32)).astype(np.uint8)
+    x = rng.standard_normal((t, k)).astype(np.float32)
+    return c4, e8, x
+
+
+@pin
+def gemv_mx_block_sums_and_exponent_steps(o):
+    rng = np.random.default_rng(83)
+    n, k, t = 5, 512, 3
+    c4, e8, x = _mx_case(rng, n, k, t)
+    q, d, _ = o.quantize(x)
+    y, ab, isum = o.gemv_mx(c4, e8, q, d, want_isum=True)
+    dbl = np.array([int(2 * v) for v in _paper_e2m1_values()], dtype=np.int64)[c4]
+    for j in range(k // 32):
+        sl = slice(32 * j, 32 * (j + 1))
+        assert np.array_equal(isum[:, :, j], q[:, sl].astype(np.int64) @ dbl[:, sl].T)
+    e2 = e8.copy(); e2[3] += 1  # every block scale of row 3 doubled: y doubles exactly
+    y2, ab2 = o.gemv_mx(c4, e2, q, d)
+    assert np.array_equal(y2[:, 3], 2 * y[:, 3]) and np.array_equal(np.delete(y2, 3, 1), np.delete(y, 3, 1))
+    e3 = e8.copy(); e3[1, 5] += 2  # one 32-block of row 1 times 4
+    y3, _ = o.gemv_mx(c4, e3, q, d)
+    term = np.ldexp(1.0, int(e8[1, 5]) - 128) * d[:, 0].astype(np.float64) * isum[:, 1, 5]
+    assert np.allclose(y3[:, 1] - y[:, 1], 3 * term, rtol=1e-12, atol=1e-300)
+    assert np.all(np.abs(y) <= ab * (1 + 1e-15))
+    for bad_c4, bad_e8 in ((np.where(c4 == 3, 16, c4).astype(np.uint8), e8), (c4, np.full_like(e8, 255))):
+        try:
+            o.gemv_mx(bad_c4, bad_e8, q, d)
+        except Exception:  # noqa: BLE001 - the oracle must refuse codes > 15 and NaN scales
+            continue
+        raise AssertionError("gemv_mx accepted an invalid code or a NaN scale")
+
+
+@pin
+def gemv_mx_absorbs_the_half_exactly(o):
+    # the integer arm (doubled codes, 2^(E - 128)) equals the float-dequantized dot
+    # (e2m1 values from the paper's set, 2^(E - 127)) in exact rational arithmetic
+    rng = np.random.default_rng(89)
+    n, k = 3, 512
+    c4, e8, x = _mx_case(rng, n, k, 1)
+    q, d, _ = o.quantize(x)
+    y, ab = o.gemv_mx(c4, e8, q, d)
+    ex = brute.gemv_mx_exact(_paper_e2m1_values(), c4.tolist(), e8.tolist(), q[0].tolist(), d[0].tolist())
+    for r in range(n):
+        assert abs(Fraction(float(y[0, r])) - ex[r]) <= Fraction(float(ab[0, r])) * Fraction(1, 2 ** 50)
+
+
+# --------------------------------------------------------------------------------------
 # Synthetic weight stream (input generation): SplitMix64 published outputs + recipe
 # --------------------------------------------------------------------------------------
 

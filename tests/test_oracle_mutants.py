@@ -51,6 +51,17 @@ C_MUTANTS = {
     "tied_scale_over_count": ("s = (float)(pairwise_sum256(v) / (double)cc);", "s = (float)(pairwise_sum256(v) / 256.0);"),
     "tied_final_codes_fp32_scale": ("code_step(wb, sd, cb);", "code_step(wb, s, cb);"),
     "tied_no_zero_floor": ("if (!(amax >= 0x1p-100f)) {", "if (amax == 0.0f) {"),
+    "e2m1_subnormal_step": ("double v = (e == 0) ? 0.5 * m : ldexp(1.0 + 0.5 * m, e - 1);", "double v = (e == 0) ? 1.0 * m : ldexp(1.0 + 0.5 * m, e - 1);"),
+    "e2m1_exponent_bias": ("double v = (e == 0) ? 0.5 * m : ldexp(1.0 + 0.5 * m, e - 1);", "double v = (e == 0) ? 0.5 * m : ldexp(1.0 + 0.5 * m, e);"),
+    "e2m1_doubled_shift": ("int v = (e == 0) ? m : (2 + m) << (e - 1);", "int v = (e == 0) ? m : (2 + m) << e;"),
+    "e2m1_doubled_mantissa": ("int v = (e == 0) ? m : (2 + m) << (e - 1);", "int v = (e == 0) ? m : (2 + 2 * m) << (e - 1);"),
+    "e2m1_doubled_unsigned": ("int v = (e == 0) ? m : (2 + m) << (e - 1);\n  return sign ? -v : v;", "int v = (e == 0) ? m : (2 + m) << (e - 1);\n  return sign ? v : v;"),
+    "e8m0_bias": ("return e == 255 ? NAN : ldexp(1.0, (int)e - 127);", "return e == 255 ? NAN : ldexp(1.0, (int)e - 128);"),
+    "mx_half_not_absorbed": ("ldexp(1.0, (int)e8[r * k32 + j] - 128)", "ldexp(1.0, (int)e8[r * k32 + j] - 127)"),
+    "mx_scale_index": ("ldexp(1.0, (int)e8[r * k32 + j] - 128)", "ldexp(1.0, (int)e8[j] - 128)"),
+    "mx_act_block_index": ("(double)d[tt * kb + j / 8]", "(double)d[tt * kb + j / 4]"),
+    "mx_nan_scale_accepted": ("    if (e8[i] == 255) return ORC_BAD_INPUT;\n", ""),
+    "mx_isum_token_dropped": ("(int64_t)q[tt * k + 32 * j + i];", "(int64_t)q[32 * j + i];"),
     "gemv2_alpha2_from_alpha1": ("orc_f16_to_f64(a[(r * kb + b) * 2 + 1])", "orc_f16_to_f64(a[(r * kb + b) * 2 + 0])"),
     "gemv2_scale_stride": ("orc_f16_to_f64(a[(r * kb + b) * 2 + 0])", "orc_f16_to_f64(a[(r * kb + b) + 0])"),
     "gemv2_plane2_dropped": ("        acc += term2;\n", ""),
