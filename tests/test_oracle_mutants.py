@@ -22,7 +22,8 @@ C_MUTANTS = {
     "two_plane_alpha_swapped": ("w[i] = alpha1 * (double)t1[i] + alpha2 * (double)t2[i];", "w[i] = alpha2 * (double)t1[i] + alpha1 * (double)t2[i];"),
     "f16_exponent_bias": ("ldexp((double)(1024 + f), e - 25)", "ldexp((double)(1024 + f), e - 24)"),
     "f16_subnormal_scale": ("v = ldexp((double)f, -24);", "v = ldexp((double)f, -25);"),
-    "f16_sign_dropped": ("return sign ? -v : v;", "return v;"),
+    "f16_sign_dropped": ("    v = ldexp((double)(1024 + f), e - 25); /* (1 + f/1024) * 2^(e-15) */\n  }\n  return sign ? -v : v;",
+                         "    v = ldexp((double)(1024 + f), e - 25); /* (1 + f/1024) * 2^(e-15) */\n  }\n  return v;"),
     "quant_round_half_away": ("float r = rintf(y);", "float r = roundf(y);"),
     "quant_scale_128": ("float inv = 127.0f / amax;", "float inv = 128.0f / amax;"),
     "quant_d_128": ("*d = amax / 127.0f;", "*d = amax / 128.0f;"),
@@ -37,7 +38,8 @@ C_MUTANTS = {
     "gemv_scale_transposed": ("orc_f16_to_f64(s[r * kb + b])", "orc_f16_to_f64(s[b * n + r])"),
     "gemv_act_scale_dropped": ("* (double)d[tt * kb + b] * (double)v;", "* (double)v;"),
     "gemv_block_offset": ("q + tt * k + b * 256, 256)", "q + tt * k + b * 255, 256)"),
-    "gemv_absref_signed": ("aacc += fabs(term);", "aacc += term;"),
+    "gemv_absref_signed": ("(double)d[tt * kb + b] * (double)v;\n        acc += term;\n        aacc += fabs(term);",
+                           "(double)d[tt * kb + b] * (double)v;\n        acc += term;\n        aacc += term;"),
     "synth_field_swap": ("int sh = (e & 1) ? 32 : 0;", "int sh = (e & 1) ? 0 : 32;"),
     "synth_trit_shift": ("((f * 3u) >> 16) - 1", "((f * 3u) >> 15) - 1"),
     "synth_scale_counter": ("sm64_word(key, (uint64_t)(n * k / 2) + j)", "sm64_word(key, j)"),
