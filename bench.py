@@ -15,7 +15,9 @@ token: quantize + dot pass), `tiedquant` (the tied quantizer that produces the c
 plane: one 2048 x 4096 fp32 matrix per step, rotating over 32), `twoplane` (the
 free-scale two-plane variant, 4.125 bits/weight: one decode step's routed gate and up
 rows as one 32768 x 4096 matrix, one token, rotating over 8 copies; the folded pass over
-the same trit planes is timed beside it, and both kernels at 1, 4 and 16 tokens).
+the same trit planes is timed beside it, and both kernels at 1, 4 and 16 tokens),
+`mxfp4` (the MXFP4 reference arm, 4.25 bits/weight, same shape and protocol, the folded
+pass over a folded matrix of that shape beside it).
 
 Cache hygiene: every step touches bytes that cannot still sit in the 256 MB last-level
 cache. Batch-1 steps route to experts not used in the previous 3 steps (reuse distance
@@ -128,6 +130,7 @@ WORKLOADS = {
     "gemv": dict(cfg=0, steps=4000, warmup=400, profile=512),
     "tiedquant": dict(cfg="quant", steps=64, warmup=8, profile=32),
     "twoplane": dict(cfg="twoplane", steps=2000, warmup=200, profile=256),
+    "mxfp4": dict(cfg="mxfp4", steps=2000, warmup=200, profile=256),
 }
 
 
@@ -389,6 +392,111 @@ def run_twoplane(args, wl, cfg):
                        "kernel_ms_by_tokens": by_tokens})
 
 
+def mx_bytes(n: int, k: int) -> int:
+    return n * k // 2 + n * (k // 32)
+
+
+def cpu_baseline_mx(cfg, target_s: float = 10.0) -> dict:
+    """The oracle's MXFP4 pass (plain single-threaded C) over the workload's matrix, one
+    token per call, repeated to about target_s seconds."""
+    import oracle as oracle_pkg
+    from synth import gen
+
+    o = oracle_pkg.get()
+    n, k = cfg["n"], cfg["k"]
+    c4, e8 = gen.mxfp4_weights(gen.SEED, 0, n, k)
+    q, d, _ = o.quantize(gen.activations(gen.SEED, 1000, 64, k))
+    t0 = time.perf_counter()
+    o.gemv_mx(c4, e8, q[:1], d[:1])
+    one = time.perf_counter() - t0
+    reps = int(max(1, min(64, round(target_s / max(one, 1e-6)))))
+    t0 = time.perf_counter()
+    for i in range(reps):
+        o.gemv_mx(c4, e8, q[i:i + 1], d[i:i + 1])
+    el = time.perf_counter() - t0
+    nbytes = reps * (mx_bytes(n, k) + k * 4 + n * 4)
+    return {"value": round(nbytes / el / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"the workload's {n} x {k} MXFP4 matrix, {reps} single-token passes (quantized activations "
+                      f"precomputed); {el:.1f} s on 1 host thread"}
+
+
+def run_mxfp4(args, wl, cfg):
+    """The MXFP4 reference arm's integer pass on one decode step's routed gate and up rows,
+    with the folded pass over a folded matrix of the same shape timed beside it."""
+    import torch
+    from paper_2608_08910_amd import tq
+    from synth import gen
+
+    n, k, seed = cfg["n"], cfg["k"], gen.SEED
+    kb = k // 256
+    K = args.steps if args.steps is not None else wl["steps"]
+    W = args.warmup if args.warmup is not None else wl["warmup"]
+    P = args.profile_steps if args.profile_steps is not None else wl["profile"]
+    copies = 8  # 8 x 71 MB per format > the 256 MB last-level cache
+    c4, e8 = gen.mxfp4_weights(seed, 0, n, k)
+    cm = torch.from_numpy(tq.tq_mx_pack_host(c4)).cuda()
+    sm = torch.from_numpy(e8).cuda()
+    del c4, e8
+    mats = [tq.TqMatrixMx(n, k, cm.clone(), sm.clone()) for _ in range(copies)]
+    matsf = [tq.TqMatrix.empty(n, k) for _ in range(copies)]
+    for i, m in enumerate(matsf):
+        tq.tq_synth_weights(gen.matrix_key(seed, 0xFFFE, i, 0), m)
+    total = W + K
+    x_all = torch.from_numpy(gen.activations(seed, 1000, total + 16, k)).cuda()
+    T_MAX = 16
+    q = torch.empty((T_MAX, k), dtype=torch.int8, device="cuda")
+    d = torch.empty((T_MAX, kb), dtype=torch.float32, device="cuda")
+    b = torch.empty((T_MAX, kb), dtype=torch.int32, device="cuda")
+    y = torch.empty((T_MAX, n), dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+
+    def step(i):
+        tq.tq_quantize_act(x_all[i:i + 1], q[:1], d[:1], b[:1])
+        tq.tq_gemv_mx(mats[i % copies], q[:1], d[:1], y[:1])
+
+    def stepf(i):
+        tq.tq_quantize_act(x_all[i:i + 1], q[:1], d[:1], b[:1])
+        tq.tq_gemv(matsf[i % copies], q[:1], d[:1], b[:1], y[:1])
+
+    elapsed = time_graph(step, W, K)
+    elapsed_f = time_graph(stepf, W, K)
+    io = k * 4 + n * 4
+    gbs = (mx_bytes(n, k) + io) * K / elapsed / 1e9
+    gbs_f = (matrix_bytes(n, k) + io) * K / elapsed_f / 1e9
+
+    def kernel_ms(fn, t):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(P)]
+        torch.cuda.synchronize()
+        torch.cuda._sleep(int(2.4e9 * 0.02))
+        for j in range(P):
+            tq.tq_quantize_act(x_all[j:j + t], q[:t], d[:t], b[:t])
+            fn(j, t, ev[j])
+        torch.cuda.synchronize()
+        return float(np.mean([s.elapsed_time(e) for s, e in ev]))
+
+    def km(j, t, ev):
+        tq.tq_gemv_mx_timed(mats[j % copies], q[:t], d[:t], y[:t], ev)
+
+    def kf(j, t, ev):
+        tq.tq_gemv_timed(matsf[j % copies], q[:t], d[:t], b[:t], y[:t], ev)
+
+    by_tokens = {}
+    for t in (1, 4, 16):
+        m1, mf = kernel_ms(km, t), kernel_ms(kf, t)
+        by_tokens[str(t)] = {"mxfp4_ms": round(m1, 5), "folded_ms": round(mf, 5),
+                             "mxfp4_GBps": round((mx_bytes(n, k) + t * (k + kb * 4 + n * 4)) / (m1 * 1e-3) / 1e9, 1),
+                             "folded_GBps": round((matrix_bytes(n, k) + t * (k + kb * 4 + n * 4)) / (mf * 1e-3) / 1e9, 1)}
+    ms = by_tokens["1"]["mxfp4_ms"]
+    roof = hbm_roof("gemv_mx", mx_bytes(n, k) + k + kb * 4 + n * 4, ms, "k_gemv_mx<2, 1, 2, false>")
+    return dict(value=gbs, K=K, W=W, elapsed=elapsed, tokens=K, roof=roof,
+                config={"workload": cfg["name"], "n": n, "k": k, "tokens_per_step": 1, "bits_per_weight": 4.25,
+                        "rotating_copies": copies, "format": "MXFP4 (e2m1 codes, e8m0 scale per 32), doubled-e2m1 "
+                                                             "integer dot"},
+                extra={"folded_same_shape": {"value": round(gbs_f, 2), "ms_per_step": round(elapsed_f * 1e3 / K, 5),
+                                             "bits_per_weight": 4.0625},
+                       "kernel_ms_by_tokens": by_tokens})
+
+
 def run_moe(args, wl, cfg):
     import torch
     from paper_2608_08910_amd import tq
@@ -530,8 +638,10 @@ def main():
 
     torch.cuda.set_device(0)
     wl = WORKLOADS[args.workload]
-    cfg = {"quant": gen.QUANT_CONFIG, "twoplane": gen.TWO_PLANE_CONFIG}.get(wl["cfg"]) or gen.CONFIGS[wl["cfg"]]
-    run = {"gemv": run_gemv, "moe": run_moe, "quant": run_quant, "twoplane": run_twoplane}[cfg["kind"]]
+    cfg = {"quant": gen.QUANT_CONFIG, "twoplane": gen.TWO_PLANE_CONFIG,
+           "mxfp4": gen.MXFP4_CONFIG}.get(wl["cfg"]) or gen.CONFIGS[wl["cfg"]]
+    run = {"gemv": run_gemv, "moe": run_moe, "quant": run_quant, "twoplane": run_twoplane,
+           "mxfp4": run_mxfp4}[cfg["kind"]]
     r = run(args, wl, cfg)
     K, W, elapsed = r["K"], r["W"], r["elapsed"]
     res = {
@@ -559,6 +669,8 @@ def main():
         res["cpu_baseline"] = cpu_baseline_quant(cfg)
     if not args.no_cpu_baseline and args.workload == "twoplane":
         res["cpu_baseline"] = cpu_baseline_twoplane(cfg)
+    if not args.no_cpu_baseline and args.workload == "mxfp4":
+        res["cpu_baseline"] = cpu_baseline_mx(cfg)
     print(json.dumps(res), flush=True)
 
 

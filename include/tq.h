@@ -208,6 +208,47 @@ tq_status tq_gemv2(const tq_mat2* w, const int8_t* q, const float* d, int64_t t,
 tq_status tq_gemv2_timed(const tq_mat2* w, const int8_t* q, const float* d, int64_t t, float* y,
                          int32_t* isum_dbg, void* stream, void* const* events);
 
+/* ---------------------------------------------------------------------------------
+ * MXFP4 reference arm (Sec. 2.3: the released expert bytes, fp4-e2m1 codes with one
+ * e8m0 scale per 32 elements, Sec. 2.1, served by an integer kernel through the doubled
+ * e2m1 values {0,1,2,3,4,6,8,12}, the e8m0 scale absorbing the /2).
+ *   codes  [n][kb][128] bytes, 128-byte aligned: 16-byte block j of a row covers
+ *          elements 32j .. 32j+31; its byte i holds element 32j+i in the low nibble and
+ *          32j+16+i in the high nibble, each an e2m1 code (bit 3 sign, bits 2..1 exponent
+ *          with bias 1, bit 0 mantissa; exponent 0 is subnormal).
+ *   scales [n][k/32] e8m0 bytes, 2^(E - 127) (E = 255, NaN, must not occur).
+ *   Bytes: 16 + 1 per 32 weights = 4.25 bits/weight, the paper's 17-byte blocks with
+ *   codes and scales in two planes.
+ * Pass: isum[t][r][j] = sum_i 2*e2m1(c[r][32j+i]) * q[t][32j+i] (exact int32),
+ *   y[t][r] = sum_j f32(2^(E[r][j] - 128) * d[t][j/8]) * isum[t][r][j] in fp32.
+ * Precondition (not checked): each 2^(E - 128) * d is a normal fp32 value and the sums
+ * stay within the fp32 range.
+ * --------------------------------------------------------------------------------- */
+typedef struct {
+  int32_t n;
+  int32_t k;
+  const uint8_t* codes;
+  const uint8_t* scales; /* [n][k/32] e8m0 */
+} tq_mat_mx;
+
+/* Pack e2m1 codes on the host into the layout above. c4: host [n][k] codes 0..15;
+ * codes_out: host, n * k / 2 bytes. TQ_ERR_INVALID if a code exceeds 15. */
+tq_status tq_mx_pack_host(const uint8_t* c4, int32_t n, int32_t k, uint8_t* codes_out);
+
+/* Inverse of tq_mx_pack_host on the host. */
+tq_status tq_mx_unpack_host(const uint8_t* codes, int32_t n, int32_t k, uint8_t* c4_out);
+
+/* The MXFP4 arm's pass for one matrix and t tokens (formula above). q, d as from
+ * tq_quantize_act (q 16-byte aligned). isum_dbg: NULL, or a [t][n][k/32] int32 buffer
+ * that receives the exact 32-element block sums. n >= 1, 256 <= k <= 16384, t >= 0. */
+tq_status tq_gemv_mx(const tq_mat_mx* w, const int8_t* q, const float* d, int64_t t, float* y,
+                     int32_t* isum_dbg, void* stream);
+
+/* As tq_gemv_mx, with the kernel's own start/stop timestamps in two host-created HIP
+ * events (as tq_gemv_timed). */
+tq_status tq_gemv_mx_timed(const tq_mat_mx* w, const int8_t* q, const float* d, int64_t t, float* y,
+                           int32_t* isum_dbg, void* stream, void* const* events);
+
 /* Routed-expert MoE layer over the folded experts (Sec. 2.2 dot pass applied to every
  * routed gate/up/down projection; the paper's layers are 43 x 3 projections x 256
  * experts, Sec. 2.1). For every token t and slot j < topk with e = topk_idx[t][j]:

@@ -127,3 +127,39 @@ extern "C" tq_status tq_unpack2_host(const uint8_t* codes, int32_t n, int32_t k,
     }
   return TQ_OK;
 }
+
+// MXFP4 arm (Sec. 2.3): e2m1 codes, two per byte in the order of a released 32-element
+// block (element i low nibble, element 16 + i high nibble of byte i).
+extern "C" tq_status tq_mx_pack_host(const uint8_t* c4, int32_t n, int32_t k, uint8_t* codes_out) {
+  using namespace tq;
+  clear_error();
+  if (n < 0 || k <= 0 || k % 256 != 0)
+    return fail(TQ_ERR_INVALID, "tq_mx_pack_host: bad shape n=%d k=%d (k must be a multiple of 256)", n, k);
+  if (n == 0) return TQ_OK;
+  if (!c4 || !codes_out) return fail(TQ_ERR_INVALID, "tq_mx_pack_host: null pointer");
+  const int64_t nblk = (int64_t)n * (k / 32);
+  for (int64_t j = 0; j < nblk; ++j)
+    for (int i = 0; i < 16; ++i) {
+      const uint8_t lo = c4[32 * j + i], hi = c4[32 * j + 16 + i];
+      if (lo > 15 || hi > 15)
+        return fail(TQ_ERR_INVALID, "tq_mx_pack_host: code above 15 in block %lld", (long long)j);
+      codes_out[16 * j + i] = (uint8_t)(lo | (hi << 4));
+    }
+  return TQ_OK;
+}
+
+extern "C" tq_status tq_mx_unpack_host(const uint8_t* codes, int32_t n, int32_t k, uint8_t* c4_out) {
+  using namespace tq;
+  clear_error();
+  if (n < 0 || k <= 0 || k % 256 != 0)
+    return fail(TQ_ERR_INVALID, "tq_mx_unpack_host: bad shape n=%d k=%d (k must be a multiple of 256)", n, k);
+  if (n == 0) return TQ_OK;
+  if (!codes || !c4_out) return fail(TQ_ERR_INVALID, "tq_mx_unpack_host: null pointer");
+  const int64_t nblk = (int64_t)n * (k / 32);
+  for (int64_t j = 0; j < nblk; ++j)
+    for (int i = 0; i < 16; ++i) {
+      c4_out[32 * j + i] = codes[16 * j + i] & 0xF;
+      c4_out[32 * j + 16 + i] = codes[16 * j + i] >> 4;
+    }
+  return TQ_OK;
+}

@@ -44,6 +44,10 @@ class tq_mat2(ctypes.Structure):
     _fields_ = [("n", ctypes.c_int32), ("k", ctypes.c_int32), ("codes", ctypes.c_void_p), ("scales", ctypes.c_void_p)]
 
 
+class tq_mat_mx(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("k", ctypes.c_int32), ("codes", ctypes.c_void_p), ("scales", ctypes.c_void_p)]
+
+
 class tq_experts(ctypes.Structure):
     _fields_ = [
         ("n_experts", ctypes.c_int32), ("hidden", ctypes.c_int32), ("inter", ctypes.c_int32),
@@ -78,6 +82,10 @@ for _name, _args, _res in [
     ("tq_unpack2_host", [_vp, _i32, _i32, _vp, _vp], _i32),
     ("tq_gemv2", [_P(tq_mat2), _vp, _vp, _i64, _vp, _vp, _vp], _i32),
     ("tq_gemv2_timed", [_P(tq_mat2), _vp, _vp, _i64, _vp, _vp, _vp, _P(_vp)], _i32),
+    ("tq_mx_pack_host", [_vp, _i32, _i32, _vp], _i32),
+    ("tq_mx_unpack_host", [_vp, _i32, _i32, _vp], _i32),
+    ("tq_gemv_mx", [_P(tq_mat_mx), _vp, _vp, _i64, _vp, _vp, _vp], _i32),
+    ("tq_gemv_mx_timed", [_P(tq_mat_mx), _vp, _vp, _i64, _vp, _vp, _vp, _P(_vp)], _i32),
     ("tq_moe_workspace_bytes", [_P(tq_experts), _i64, _i32], _sz),
     ("tq_moe_path", [_P(tq_experts), _i64, _i32, _i32], _i32),
     ("tq_moe_workspace_layout", [_P(tq_experts), _i64, _i32, _P(tq_moe_layout)], _i32),
@@ -288,6 +296,65 @@ def tq_gemv2_timed(m: TqMatrix2, q: torch.Tensor, d: torch.Tensor, y: torch.Tens
             ev.record()
     arr = (_vp * 2)(*[ev.cuda_event for ev in events])
     _ok(_L.tq_gemv2_timed(*_gemv2_args(m, q, d, y, isum_dbg), _stream(stream), arr))
+
+
+# -- MXFP4 reference arm ---------------------------------------------------------------------
+
+def tq_mx_pack_host(c4: np.ndarray) -> np.ndarray:
+    """Host pack of e2m1 codes [n][k] (0..15) into MXFP4 code bytes [n][k/256][128]."""
+    n, k = c4.shape
+    out = np.empty((n, k // 256, 128), dtype=np.uint8)
+    _ok(_L.tq_mx_pack_host(_host(c4, np.uint8, "c4"), n, k, _host(out, np.uint8, "codes")))
+    return out
+
+
+def tq_mx_unpack_host(codes: np.ndarray, n: int, k: int) -> np.ndarray:
+    out = np.empty((n, k), dtype=np.uint8)
+    _ok(_L.tq_mx_unpack_host(_host(codes, np.uint8, "codes"), n, k, _host(out, np.uint8, "c4_out")))
+    return out
+
+
+@dataclass
+class TqMatrixMx:
+    """One matrix of the MXFP4 arm: codes [n][kb][128] uint8, scales [n][k/32] uint8 (e8m0)."""
+    n: int
+    k: int
+    codes: torch.Tensor
+    scales: torch.Tensor
+
+    @staticmethod
+    def empty(n: int, k: int, device="cuda") -> "TqMatrixMx":
+        return TqMatrixMx(n, k, torch.empty((n, k // 256, 128), dtype=torch.uint8, device=device),
+                          torch.empty((n, k // 32), dtype=torch.uint8, device=device))
+
+    def desc(self) -> tq_mat_mx:
+        _dev(self.codes, torch.uint8, "codes", (self.n, self.k // 256, 128))
+        _dev(self.scales, torch.uint8, "scales", (self.n, self.k // 32))
+        return tq_mat_mx(self.n, self.k, self.codes.data_ptr(), self.scales.data_ptr())
+
+
+def _gemv_mx_args(m: TqMatrixMx, q, d, y, isum_dbg):
+    t = q.shape[0]
+    desc = m.desc()
+    dbg = None if isum_dbg is None else _dev(isum_dbg, torch.int32, "isum_dbg", (t, m.n, m.k // 32))
+    return (ctypes.byref(desc), _dev(q, torch.int8, "q", (t, m.k)), _dev(d, torch.float32, "d", (t, m.k // 256)), t,
+            _dev(y, torch.float32, "y", (t, m.n)), dbg)
+
+
+def tq_gemv_mx(m: TqMatrixMx, q: torch.Tensor, d: torch.Tensor, y: torch.Tensor, isum_dbg: torch.Tensor | None = None,
+               stream=None):
+    _ok(_L.tq_gemv_mx(*_gemv_mx_args(m, q, d, y, isum_dbg), _stream(stream)))
+
+
+def tq_gemv_mx_timed(m: TqMatrixMx, q: torch.Tensor, d: torch.Tensor, y: torch.Tensor, events,
+                     isum_dbg: torch.Tensor | None = None, stream=None):
+    if len(events) != 2:
+        raise ValueError("need 2 events")
+    for ev in events:  # torch creates the HIP event on its first record
+        if ev.cuda_event == 0:
+            ev.record()
+    arr = (_vp * 2)(*[ev.cuda_event for ev in events])
+    _ok(_L.tq_gemv_mx_timed(*_gemv_mx_args(m, q, d, y, isum_dbg), _stream(stream), arr))
 
 
 # -- routed-expert MoE layer ----------------------------------------------------------------

@@ -2,7 +2,8 @@
 
 This module holds random draws only: activations, per-token scale factors, routing
 indices and routing weights, fp32 weights for the tied quantizer, trit planes and scale
-pairs for the free-scale two-plane variant, and the 64-bit keys
+pairs for the free-scale two-plane variant, e2m1 codes and e8m0 exponents for the MXFP4
+arm, and the 64-bit keys
 that name each weight matrix's counter-based stream. None of the method's arithmetic (fold, pack, quantize, integer
 dot, scale combine, SiLU, weighted combine) lives here; both the CPU oracle and the
 HIP path consume these draws, and each implements the method on its own.
@@ -56,6 +57,7 @@ _TAG_KEY = 5
 _TAG_BENCH = 6
 _TAG_FWEIGHT = 7
 _TAG_TWOPLANE = 8
+_TAG_MXFP4 = 9
 
 PROJ_GATE, PROJ_UP, PROJ_DOWN = 0, 1, 2
 
@@ -88,6 +90,11 @@ QUANT_CONFIG = dict(name="tied_quantize_m32_2048x4096", kind="quant", matrices=3
 # (8 experts x 2 x 2048 rows of 4096 inputs) as one stacked matrix, one token, served
 # from the two-plane layout; the folded layout of the same planes is timed beside it.
 TWO_PLANE_CONFIG = dict(name="twoplane_gemv_32768x4096_t1", kind="twoplane", n=32768, k=4096, tokens=1)
+
+
+# The MXFP4 reference arm's workload: the same stacked decode rows in the released-bytes
+# format (e2m1 codes, one e8m0 scale per 32), one token.
+MXFP4_CONFIG = dict(name="mxfp4_gemv_32768x4096_t1", kind="mxfp4", n=32768, k=4096, tokens=1)
 
 
 def _rng(*key: int) -> np.random.Generator:
@@ -130,6 +137,15 @@ def two_plane_weights(seed: int, index: int, n: int, k: int):
     a1 = a2 * 3.0 * r.uniform(0.75, 1.25, (n, k // 256))
     a = np.stack([a1, a2], axis=2).astype(np.float16).view(np.uint16)
     return t1, t2, np.ascontiguousarray(a)
+
+
+def mxfp4_weights(seed: int, index: int, n: int, k: int):
+    """An MXFP4 matrix: e2m1 codes [n][k] (uint8, uniform on 0..15) and e8m0 exponents
+    [n][k/32] (uint8, uniform on 116..124, i.e. block scales 2^-11 .. 2^-3)."""
+    r = _rng(seed, _TAG_MXFP4, index)
+    c4 = r.integers(0, 16, (n, k), dtype=np.uint8)
+    e8 = r.integers(116, 125, (n, k // 32), dtype=np.uint8)
+    return c4, e8
 
 
 def token_factors(seed: int, tokens: int) -> np.ndarray:

@@ -140,6 +140,33 @@ def test_pack2_round_trip_and_rejections():
         tq.tq_unpack2_host(codes, 1, 256)
 
 
+def test_mx_size_is_paper_bits_per_weight():
+    # 16 code bytes + 1 e8m0 byte per 32 weights (Sec. 2.3: 17-byte / 32-element blocks)
+    bpw = GOLDEN["bits_per_weight"]
+    assert bpw["mxfp4_block_bytes"] * 8 / bpw["mxfp4_block_weights"] == bpw["mxfp4"]
+    for n, k in ((2048, 4096), (1, 256)):
+        total = tq.tq_codes_bytes(n, k) + n * (k // 32)
+        assert total * 8 / (n * k) == bpw["mxfp4"]
+
+
+def test_mx_pack_layout_round_trip_and_rejections():
+    # byte i of 16-byte block j: element 32j + i in the low nibble, 32j + 16 + i high
+    rng = np.random.default_rng(9)
+    c4 = rng.integers(0, 16, (3, 512)).astype(np.uint8)
+    codes = tq.tq_mx_pack_host(c4)
+    flat = codes.reshape(3, -1)
+    for r in range(3):
+        for j in range(512 // 32):
+            for i in range(16):
+                byte = int(flat[r, 16 * j + i])
+                assert byte & 15 == c4[r, 32 * j + i] and byte >> 4 == c4[r, 32 * j + 16 + i]
+    assert np.array_equal(tq.tq_mx_unpack_host(codes, 3, 512), c4)
+    bad = c4.copy(); bad[1, 7] = 16
+    with pytest.raises(tq.TqError) as e:
+        tq.tq_mx_pack_host(bad)
+    assert e.value.status == tq.TQ_ERR_INVALID
+
+
 FAKE = 0x7F0000000000  # 256-byte aligned, never dereferenced: every call below is invalid
 
 
@@ -182,6 +209,23 @@ def test_gemv2_validation_errors_before_launch():
         assert tq.tq_last_error()
     assert L.tq_gemv2(ctypes.byref(tq.tq_mat2(16, 4096, FAKE, FAKE)), FAKE + 4, FAKE, 1, FAKE, None, None) == tq.TQ_ERR_ALIGN
     assert L.tq_gemv2(ctypes.byref(tq.tq_mat2(16, 4096, FAKE, FAKE)), FAKE, FAKE, 0, FAKE, None, None) == tq.TQ_OK
+
+
+@no_gpu_only
+def test_gemv_mx_validation_errors_before_launch():
+    L = tq._L
+    for m, t, want in [
+        (tq.tq_mat_mx(0, 4096, FAKE, FAKE), 1, tq.TQ_ERR_INVALID),
+        (tq.tq_mat_mx(16, 300, FAKE, FAKE), 1, tq.TQ_ERR_INVALID),
+        (tq.tq_mat_mx(16, 32768, FAKE, FAKE), 1, tq.TQ_ERR_INVALID),
+        (tq.tq_mat_mx(16, 4096, FAKE + 16, FAKE), 1, tq.TQ_ERR_ALIGN),
+        (tq.tq_mat_mx(16, 4096, FAKE, None), 1, tq.TQ_ERR_INVALID),
+        (tq.tq_mat_mx(16, 4096, FAKE, FAKE), -1, tq.TQ_ERR_INVALID),
+    ]:
+        st = L.tq_gemv_mx(ctypes.byref(m), FAKE, FAKE, t, FAKE, None, None)
+        assert st == want, (m.n, m.k, t, st, tq.tq_last_error())
+    assert L.tq_gemv_mx(ctypes.byref(tq.tq_mat_mx(16, 4096, FAKE, FAKE + 1)), FAKE + 4, FAKE, 1, FAKE, None, None) == tq.TQ_ERR_ALIGN
+    assert L.tq_gemv_mx(ctypes.byref(tq.tq_mat_mx(16, 4096, FAKE, FAKE + 1)), FAKE, FAKE, 0, FAKE, None, None) == tq.TQ_OK
 
 
 @no_gpu_only
