@@ -17,7 +17,9 @@ free-scale two-plane variant, 4.125 bits/weight: one decode step's routed gate a
 rows as one 32768 x 4096 matrix, one token, rotating over 8 copies; the folded pass over
 the same trit planes is timed beside it, and both kernels at 1, 4 and 16 tokens),
 `mxfp4` (the MXFP4 reference arm, 4.25 bits/weight, same shape and protocol, the folded
-pass over a folded matrix of that shape beside it).
+pass over a folded matrix of that shape beside it), `stream` (the batch-1 decode layer
+with every expert in pinned host memory and an LRU pool of --slots expert slots in HBM:
+misses copied over the host link each step, eager steps).
 
 Cache hygiene: every step touches bytes that cannot still sit in the 256 MB last-level
 cache. Batch-1 steps route to experts not used in the previous 3 steps (reuse distance
@@ -131,6 +133,7 @@ WORKLOADS = {
     "tiedquant": dict(cfg="quant", steps=64, warmup=8, profile=32),
     "twoplane": dict(cfg="twoplane", steps=2000, warmup=200, profile=256),
     "mxfp4": dict(cfg="mxfp4", steps=2000, warmup=200, profile=256),
+    "stream": dict(cfg=1, steps=200, warmup=20, profile=0, stream=True),
 }
 
 
@@ -497,6 +500,84 @@ def run_mxfp4(args, wl, cfg):
                        "kernel_ms_by_tokens": by_tokens})
 
 
+PCIE5_X16_GBS = 63.0  # PCIe 5.0 x16, one direction: 32 GT/s x 16 lanes x 128/130
+
+
+def run_stream(args, wl, cfg):
+    """The batch-1 decode layer with its experts streamed: all 256 experts in pinned host
+    memory as contiguous records, an LRU pool of expert slots in HBM; per step the host
+    maps the routing to slots, the misses are copied host-to-device, and the same MoE
+    kernels run on the pool. Steps run eagerly (the host plans each step)."""
+    import torch
+    from paper_2608_08910_amd import tq
+    from synth import gen
+
+    E, H, I, T, topk, seed = cfg["experts"], cfg["hidden"], cfg["inter"], cfg["tokens"], cfg["topk"], gen.SEED
+    K = args.steps if args.steps is not None else wl["steps"]
+    W = args.warmup if args.warmup is not None else wl["warmup"]
+    S = args.slots
+    total = W + K
+    rb = tq.tq_expert_record_bytes(H, I)
+    store = tq.TqExpertRecords.empty(E, H, I, device="cpu", pin_memory=True)
+    # the host store: every expert generated on the device, rewritten as a record, copied out
+    tmp = tq.TqExperts.empty(1, H, I)
+    rec = tq.TqExpertRecords.empty(1, H, I)
+    d0 = tq.tq_experts_from_records(1 << 20, 1, H, I)
+    code_offs = [d0.gate_codes - (1 << 20), d0.up_codes - (1 << 20), d0.down_codes - (1 << 20)]
+    scale_offs = [d0.gate_scales - (1 << 20), d0.up_scales - (1 << 20), d0.down_scales - (1 << 20)]
+    for e in range(E):
+        for p in range(3):
+            tq.tq_synth_weights(gen.matrix_key(seed, 0, e, p), tmp.matrix(0, p))
+            c = tmp.codes[p].reshape(-1)
+            sc = tmp.scales[p].reshape(-1).view(torch.uint8)
+            rec.data[0, code_offs[p]:code_offs[p] + c.numel()] = c
+            rec.data[0, scale_offs[p]:scale_offs[p] + sc.numel()] = sc
+        store.data[e].copy_(rec.data[0])
+    torch.cuda.synchronize()
+    pool = tq.TqExpertRecords.empty(S, H, I)
+    cache = tq.TqCache(E, S)
+    sched = gen.bench_routing_schedule(seed, total, T, E, topk, cfg["routing"])
+    x_all = torch.from_numpy(gen.activations(seed, 1000, total * T, H).reshape(total, T, H)).cuda()
+    w_all = torch.from_numpy(np.stack([s_[1] for s_ in sched])).cuda()
+    slots_host = [torch.empty((T, topk), dtype=torch.int32, pin_memory=True) for _ in range(total)]
+    slots_dev = [torch.empty((T, topk), dtype=torch.int32, device="cuda") for _ in range(total)]
+    out = torch.empty((T, H), dtype=torch.float32, device="cuda")
+    ws = tq.moe_workspace(pool, T, topk)
+    misses_per_step = []
+
+    def step(i):
+        _, misses = cache.map(sched[i][0], slots_host[i].numpy())
+        misses_per_step.append(len(misses))
+        cache.fetch(store, pool, misses, slots_host[i], slots_dev[i])
+        tq.tq_moe_grouped(pool, x_all[i], slots_dev[i], w_all[i], out, ws)
+
+    for i in range(W):
+        step(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(W, W + K):
+        step(i)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    copied = sum(misses_per_step[W:]) * rb
+    bytes_expert = 2 * matrix_bytes(I, H) + matrix_bytes(H, I)
+    distinct = [len(np.unique(sched[i][0])) for i in range(W, W + K)]
+    alg_bytes = sum(d_ * bytes_expert for d_ in distinct) + K * (T * H * 4 * 2 + T * topk * 8)
+    link = copied / elapsed / 1e9
+    roof = {"kernel": "host_to_device_copies", "bound": "pcie", "achieved": round(link, 2), "peak": PCIE5_X16_GBS,
+            "unit": "GB/s", "frac": round(link / PCIE5_X16_GBS, 4), "traffic": None,
+            "bytes_per_step": round(copied / K), "note": "expert records copied per step over the host link "
+                                                        "(pinned host -> HBM); peak = PCIe 5.0 x16 one direction"}
+    return dict(value=alg_bytes / elapsed / 1e9, K=K, W=W, elapsed=elapsed, tokens=K * T, roof=roof,
+                config={"workload": cfg["name"] + f"_streamed_{S}slots", "experts": E, "hidden": H, "inter": I,
+                        "tokens_per_step": T, "topk": topk, "routing": "uniform top-8, no expert reused within 3 steps",
+                        "bits_per_weight": 4.0625, "host_store_bytes": E * rb, "hbm_slots": S,
+                        "hbm_pool_bytes": S * rb, "path": "single_token (eager steps)"},
+                extra={"misses_per_step": round(float(np.mean(misses_per_step[W:])), 3),
+                       "hit_rate": round(1.0 - sum(misses_per_step[W:]) / max(1, sum(distinct)), 4),
+                       "copied_GBps": round(link, 2)})
+
+
 def run_moe(args, wl, cfg):
     import torch
     from paper_2608_08910_amd import tq
@@ -610,6 +691,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=None, help="steps of the per-kernel event pass")
     ap.add_argument("--flags", type=int, default=0, help="tq_moe_grouped flags (1 force VALU, 2 force MFMA)")
+    ap.add_argument("--slots", type=int, default=64, help="HBM expert slots of the stream workload")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (to scale HBM byte counters)")
     args = ap.parse_args()
@@ -642,6 +724,8 @@ def main():
            "mxfp4": gen.MXFP4_CONFIG}.get(wl["cfg"]) or gen.CONFIGS[wl["cfg"]]
     run = {"gemv": run_gemv, "moe": run_moe, "quant": run_quant, "twoplane": run_twoplane,
            "mxfp4": run_mxfp4}[cfg["kind"]]
+    if wl.get("stream"):
+        run = run_stream
     r = run(args, wl, cfg)
     K, W, elapsed = r["K"], r["W"], r["elapsed"]
     res = {

@@ -314,6 +314,57 @@ tq_status tq_moe_grouped_timed(const tq_experts* ex, const float* x, int64_t t,
 tq_status tq_moe_status(const void* ws, const tq_experts* ex, int64_t t, int32_t topk,
                         int32_t* flags_out, void* stream);
 
+/* ---------------------------------------------------------------------------------
+ * Host-tier expert streaming (Sec. 2.2: "the fold is the file" -- an expert-projection
+ * miss is one contiguous read, and resident and streamed serving use the same bytes and
+ * kernels, so outputs are bitwise independent of where an expert was cached; the
+ * paper's store keeps pinned RAM and LRU slots in front of the file). Tiers here: every
+ * expert in pinned host memory, a pool of expert slots in HBM.
+ * An expert record is one contiguous range: gate, up, down codes, then gate, up, down
+ * scales, each piece 128-byte aligned, tq_expert_record_bytes(hidden, inter) bytes in
+ * all. The same record layout serves the host store ([n_experts] records) and the slot
+ * pool ([n_slots] records); tq_experts_from_records describes either to tq_moe_grouped.
+ * A streamed step: tq_cache_map (host: expert ids -> slots, LRU eviction), tq_cache_fetch
+ * (enqueue one host-to-device copy per miss and the slot ids), then tq_moe_grouped on
+ * the pool's descriptor with the slot ids as topk_idx, all on one stream.
+ * --------------------------------------------------------------------------------- */
+
+/* Bytes of one expert record (a multiple of 128); 0 for an invalid shape. */
+size_t tq_expert_record_bytes(int32_t hidden, int32_t inter);
+
+/* Fills *out (host) for n_records expert records at `base` (device or host address,
+ * 128-byte aligned): the projections' pointers inside record 0 and the record size as
+ * every stride. hidden, inter: multiples of 256 in [256, 16384]. */
+tq_status tq_experts_from_records(const void* base, int32_t n_records, int32_t hidden, int32_t inter,
+                                  tq_experts* out);
+
+/* Bytes of the LRU planner's state (host memory, owned by the caller, 8-byte aligned);
+ * 0 if n_experts or n_slots < 1. */
+size_t tq_cache_state_bytes(int32_t n_experts, int32_t n_slots);
+
+/* Empties the pool. */
+tq_status tq_cache_init(void* state, int32_t n_experts, int32_t n_slots);
+
+/* Host only. ids: host [n] expert ids of one step (duplicates allowed). Writes
+ * slots_out (host [n]): each id's slot. Experts not resident are placed in order of first
+ * appearance, each in an empty slot (lowest index) if any, else in the least recently
+ * used slot that this step does not use (lowest index on ties); misses_out (host, up to
+ * 2n int32) receives the (expert, slot) pairs to copy and *n_miss_out their count.
+ * TQ_ERR_INVALID, with the pool unchanged, if an id is outside [0, n_experts) or the
+ * step names more distinct experts than there are slots. Deterministic. */
+tq_status tq_cache_map(void* state, const int32_t* ids, int64_t n, int32_t* slots_out,
+                       int32_t* misses_out, int32_t* n_miss_out);
+
+/* Enqueues on `stream` one host-to-device copy of record_bytes per miss (host_store
+ * record `expert` -> dev_slots record `slot`), then the copy of the n slot ids
+ * slots_host -> slots_dev. host_store and slots_host should be pinned host memory (for
+ * asynchronous copies) and must stay unchanged until the copies have executed.
+ * Every miss and slot id is checked against the state's store and pool sizes before
+ * anything is enqueued. */
+tq_status tq_cache_fetch(const void* state, const void* host_store, void* dev_slots, size_t record_bytes,
+                         const int32_t* misses, int32_t n_miss, const int32_t* slots_host,
+                         int32_t* slots_dev, int64_t n, void* stream);
+
 /* Thread-local description of the last failed call on this thread ("" if none). */
 const char* tq_last_error(void);
 

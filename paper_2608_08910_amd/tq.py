@@ -86,6 +86,12 @@ for _name, _args, _res in [
     ("tq_mx_unpack_host", [_vp, _i32, _i32, _vp], _i32),
     ("tq_gemv_mx", [_P(tq_mat_mx), _vp, _vp, _i64, _vp, _vp, _vp], _i32),
     ("tq_gemv_mx_timed", [_P(tq_mat_mx), _vp, _vp, _i64, _vp, _vp, _vp, _P(_vp)], _i32),
+    ("tq_expert_record_bytes", [_i32, _i32], _sz),
+    ("tq_experts_from_records", [_vp, _i32, _i32, _i32, _P(tq_experts)], _i32),
+    ("tq_cache_state_bytes", [_i32, _i32], _sz),
+    ("tq_cache_init", [_vp, _i32, _i32], _i32),
+    ("tq_cache_map", [_vp, _vp, _i64, _vp, _vp, _P(_i32)], _i32),
+    ("tq_cache_fetch", [_vp, _vp, _vp, _sz, _vp, _i32, _vp, _vp, _i64, _vp], _i32),
     ("tq_moe_workspace_bytes", [_P(tq_experts), _i64, _i32], _sz),
     ("tq_moe_path", [_P(tq_experts), _i64, _i32, _i32], _i32),
     ("tq_moe_workspace_layout", [_P(tq_experts), _i64, _i32, _P(tq_moe_layout)], _i32),
@@ -395,6 +401,86 @@ class TqExperts:
             d.stride_codes[p] = n * (k // 256) * 128
             d.stride_scales[p] = n * (k // 256)
         return d
+
+
+# -- host-tier expert streaming --------------------------------------------------------------
+
+def tq_expert_record_bytes(hidden: int, inter: int) -> int:
+    return int(_L.tq_expert_record_bytes(hidden, inter))
+
+
+def tq_experts_from_records(base: int, n_records: int, hidden: int, inter: int) -> tq_experts:
+    d = tq_experts()
+    _ok(_L.tq_experts_from_records(base, n_records, hidden, inter, ctypes.byref(d)))
+    return d
+
+
+@dataclass
+class TqExpertRecords:
+    """Experts stored as contiguous records (one per expert, tq_expert_record_bytes each)
+    in one uint8 tensor [n_records][record_bytes] (device: resident experts or the slot
+    pool; pinned host: the host store). Usable wherever a TqExperts is."""
+    n_experts: int
+    hidden: int
+    inter: int
+    data: torch.Tensor
+
+    @staticmethod
+    def empty(n: int, hidden: int, inter: int, device="cuda", pin_memory: bool = False) -> "TqExpertRecords":
+        rb = tq_expert_record_bytes(hidden, inter)
+        if device == "cpu":
+            data = torch.empty((n, rb), dtype=torch.uint8, pin_memory=pin_memory)
+        else:
+            data = torch.empty((n, rb), dtype=torch.uint8, device=device)
+        return TqExpertRecords(n, hidden, inter, data)
+
+    @property
+    def record_bytes(self) -> int:
+        return tq_expert_record_bytes(self.hidden, self.inter)
+
+    def desc(self) -> tq_experts:
+        if tuple(self.data.shape) != (self.n_experts, self.record_bytes) or self.data.dtype != torch.uint8 \
+                or not self.data.is_contiguous():
+            raise ValueError("records: expected a contiguous uint8 tensor [n][record_bytes]")
+        return tq_experts_from_records(self.data.data_ptr(), self.n_experts, self.hidden, self.inter)
+
+
+class TqCache:
+    """The LRU slot planner's state (host memory) and its two calls."""
+
+    def __init__(self, n_experts: int, n_slots: int):
+        nb = int(_L.tq_cache_state_bytes(n_experts, n_slots))
+        if nb == 0:
+            raise TqError(TQ_ERR_INVALID, "tq_cache_state_bytes: invalid sizes")
+        self.state = np.zeros((nb + 7) // 8, dtype=np.int64)
+        self.n_experts, self.n_slots = n_experts, n_slots
+        _ok(_L.tq_cache_init(self.state.ctypes.data, n_experts, n_slots))
+
+    def map(self, ids: np.ndarray, slots_out: np.ndarray | None = None):
+        """ids: int32 expert ids (any shape). Returns (slots, misses [m][2] (expert, slot))."""
+        ids = np.ascontiguousarray(ids, dtype=np.int32)
+        slots = np.empty(ids.shape, dtype=np.int32) if slots_out is None else slots_out
+        if slots.shape != ids.shape or slots.dtype != np.int32 or not slots.flags["C_CONTIGUOUS"]:
+            raise ValueError("slots_out: int32, C-contiguous, same shape as ids")
+        misses = np.empty((max(ids.size, 1), 2), dtype=np.int32)
+        nm = ctypes.c_int32(0)
+        _ok(_L.tq_cache_map(self.state.ctypes.data, ids.ctypes.data, ids.size, slots.ctypes.data, misses.ctypes.data,
+                            ctypes.byref(nm)))
+        return slots, misses[:nm.value]
+
+    def fetch(self, store: TqExpertRecords, pool: TqExpertRecords, misses: np.ndarray, slots_host: torch.Tensor,
+              slots_dev: torch.Tensor, stream=None):
+        """Enqueue the misses' record copies (host store -> device pool) and the slot ids
+        (slots_host, a pinned int32 tensor -> slots_dev)."""
+        misses = np.ascontiguousarray(misses, dtype=np.int32)
+        if store.record_bytes != pool.record_bytes:
+            raise ValueError("store and pool records differ")
+        if slots_host.device.type != "cpu" or slots_host.dtype != torch.int32 or not slots_host.is_contiguous():
+            raise TypeError("slots_host: a contiguous int32 host tensor (pinned for an asynchronous copy)")
+        _dev(slots_dev, torch.int32, "slots_dev", tuple(slots_host.shape))
+        _ok(_L.tq_cache_fetch(self.state.ctypes.data, store.data.data_ptr(), pool.data.data_ptr(), pool.record_bytes,
+                              misses.ctypes.data if misses.size else None, misses.shape[0],
+                              slots_host.data_ptr(), slots_dev.data_ptr(), slots_host.numel(), _stream(stream)))
 
 
 def tq_moe_workspace_bytes(ex: TqExperts, t: int, topk: int) -> int:
