@@ -14,6 +14,9 @@ Definitions followed (paper sections):
                              per block), evaluated exactly / in fp64
   MXFP4 arm ................ Sec. 2.3 (doubled-e2m1 integer dot, e8m0 scale per 32
                              absorbing the /2) with Sec. 2.1's description of the format
+  free-scale solver ........ Sec. 2.1 (PTQTP's alternation with two free scales, started
+                             from the tied fit; start, stop rule and precision are this
+                             oracle's stated reading)
   free-scale two planes .... Sec. 2.1 (alpha1*T1 + alpha2*T2, free scales) and Sec. 4.1
                              (the unfolded pair is served as two trit planes at 4.125
                              bits per weight, one integer pass per plane)
@@ -67,6 +70,7 @@ class Oracle:
             ("orc_dot_i8", [_vp, _vp, _i64], ctypes.c_int64),
             ("orc_gemv", [_vp, _vp, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _vp], ctypes.c_int),
             ("orc_gemv2", [_vp, _vp, _vp, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _vp], ctypes.c_int),
+            ("orc_free_quantize", [_vp, _i64, _i64, ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
             ("orc_e2m1_to_f64", [ctypes.c_uint8], ctypes.c_double),
             ("orc_e2m1_doubled", [ctypes.c_uint8], ctypes.c_int),
             ("orc_e8m0_to_f64", [ctypes.c_uint8], ctypes.c_double),
@@ -228,6 +232,22 @@ class Oracle:
         it = np.empty((n, k // 256), dtype=np.uint8)
         self._check(self._L.orc_tied_quantize(_p(w), n, k, max_iter, _p(c), _p(s), _p(it)), "tied_quantize")
         return c, s, it
+
+    def free_quantize(self, w, c_tied, s_tied, max_iter: int = 16):
+        """Free-scale fit started from a tied fit: W [n][k] fp32, the tied codes and f16
+        scales -> (t1, t2 int8 [n][k], f16 scale pairs [n][k/256][2], plane steps per block)."""
+        w = np.ascontiguousarray(w, dtype=np.float32)
+        c_tied = np.ascontiguousarray(c_tied, dtype=np.int8)
+        s_tied = np.ascontiguousarray(s_tied, dtype=np.uint16)
+        n, k = w.shape
+        assert c_tied.shape == (n, k) and s_tied.shape == (n, k // 256)
+        t1 = np.empty((n, k), dtype=np.int8)
+        t2 = np.empty((n, k), dtype=np.int8)
+        a = np.empty((n, k // 256, 2), dtype=np.uint16)
+        it = np.empty((n, k // 256), dtype=np.uint8)
+        self._check(self._L.orc_free_quantize(_p(w), n, k, max_iter, _p(c_tied), _p(s_tied), _p(t1), _p(t2), _p(a),
+                                              _p(it)), "free_quantize")
+        return t1, t2, a, it
 
     def splitmix64_word(self, key: int, i: int) -> int:
         return int(self._L.orc_splitmix64_word(key & (2**64 - 1), i))

@@ -35,6 +35,10 @@
  *                             dot in exact rational arithmetic), block-scale exponent
  *                             steps double y exactly, per-32 isum against numpy,
  *                             exact rational brute force
+ *   orc_free_quantize ....... planes the best of the nine pairs at the stored scales
+ *                             (exhaustive per element), scales the f16 of numpy's least
+ *                             squares for the previous planes (one step), error below the
+ *                             tied fit's, exact recovery of a tied grid, invariants
  *   orc_gemv2 ............... tied scales (3s, s) reproduce the folded pass (integer
  *                             identity 3(T1.q)+(T2.q)), one empty plane reduces to a
  *                             single ternary plane, plane exchange, sign symmetry,
@@ -467,5 +471,106 @@ int orc_tied_quantize(const float* w, int64_t n, int64_t k, int max_iter, int8_t
       }
     }
   }
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------------ */
+/* Free-scale solver (Sec. 2.1, first paragraph: PTQTP fits W ~ alpha1*T1 + alpha2*T2 */
+/* per group by alternating plane and scale updates with two free scales; the tie     */
+/* alpha = (3s, s) is its constrained case, so the free fit is started from the tied  */
+/* fit and refines it). The paper gives neither start, stop rule nor precision; the   */
+/* reading implemented, per 256-weight block:                                         */
+/*  - start: planes = unfold(tied codes), alpha = (3 f(s), f(s)), f(s) the tied f16    */
+/*    scale; a zero tied scale gives a zero fit (alpha = 0, planes 0, 0 steps);         */
+/*  - scale step: least squares for the two scales given the planes. With            */
+/*    a = <T1,T1>, b = <T1,T2>, c = <T2,T2> (exact) and u = <w,T1>, v = <w,T2> (fp64,  */
+/*    pairwise halving as in the tied solver), det = a c - b^2; if det > 0,            */
+/*    alpha1 = fl32((c u - b v) / det) and alpha2 = fl32((a v - b u) / det), every fp64  */
+/*    operation rounded on its own; if det = 0 the scales stay;                        */
+/*  - plane step: each weight takes the first pair (t1, t2), in the order 0, -1, +1    */
+/*    for t1 and within it for t2, with the least |w - (alpha1 t1 + alpha2 t2)| in fp64;*/
+/*  - stop when a plane step reproduces the previous planes, or after max_iter steps;  */
+/*  - store alpha1, alpha2 as f16 (nearest even, saturating) and the planes of a plane */
+/*    step at the stored scales.                                                       */
+/* iters[block] = the plane steps taken before the final one (0 for a zero block).     */
+/* ------------------------------------------------------------------------------ */
+
+static const int kFreeOrder[3] = {0, -1, 1};
+
+static void free_plane_step(const float* w, float a1, float a2, int8_t* t1, int8_t* t2) {
+  for (int i = 0; i < 256; ++i) {
+    double best = INFINITY;
+    int b1 = 0, b2 = 0;
+    for (int x = 0; x < 3; ++x)
+      for (int y = 0; y < 3; ++y) {
+        int u1 = kFreeOrder[x], u2 = kFreeOrder[y];
+        double e = fabs((double)w[i] - ((double)a1 * u1 + (double)a2 * u2));
+        if (e < best) {
+          best = e;
+          b1 = u1;
+          b2 = u2;
+        }
+      }
+    t1[i] = (int8_t)b1;
+    t2[i] = (int8_t)b2;
+  }
+}
+
+int orc_free_quantize(const float* w, int64_t n, int64_t k, int max_iter, const int8_t* c_tied,
+                      const uint16_t* s_tied, int8_t* t1, int8_t* t2, uint16_t* a16, uint8_t* iters) {
+  if (k % 256 != 0 || max_iter < 1 || max_iter > 255) return ORC_BAD_INPUT;
+  const int64_t kb = k / 256;
+  for (int64_t r = 0; r < n; ++r)
+    for (int64_t b = 0; b < kb; ++b) {
+      const float* wb = w + r * k + b * 256;
+      int8_t* p1 = t1 + r * k + b * 256;
+      int8_t* p2 = t2 + r * k + b * 256;
+      uint16_t* ab = a16 + (r * kb + b) * 2;
+      for (int i = 0; i < 256; ++i)
+        if (!isfinite(wb[i])) return ORC_BAD_INPUT;
+      if (orc_unfold(c_tied + r * k + b * 256, 256, p1, p2) != ORC_OK) return ORC_BAD_INPUT;
+      const float s = (float)orc_f16_to_f64(s_tied[r * kb + b]);
+      if (s == 0.0f) {
+        for (int i = 0; i < 256; ++i) p1[i] = p2[i] = 0;
+        ab[0] = ab[1] = 0;
+        if (iters) iters[r * kb + b] = 0;
+        continue;
+      }
+      float a1 = 3.0f * s, a2 = s;
+      int it = 0;
+      for (;;) {
+        double vu[256], vv[256];
+        int64_t sa = 0, sb = 0, sc = 0;
+        for (int i = 0; i < 256; ++i) {
+          vu[i] = (double)wb[i] * (double)p1[i];
+          vv[i] = (double)wb[i] * (double)p2[i];
+          sa += p1[i] * p1[i];
+          sb += p1[i] * p2[i];
+          sc += p2[i] * p2[i];
+        }
+        const double u = pairwise_sum256(vu), v = pairwise_sum256(vv);
+        const int64_t det = sa * sc - sb * sb;
+        if (det > 0) {
+          const double num1 = (double)sc * u - (double)sb * v;
+          const double num2 = (double)sa * v - (double)sb * u;
+          a1 = (float)(num1 / (double)det);
+          a2 = (float)(num2 / (double)det);
+        }
+        int8_t q1[256], q2[256];
+        free_plane_step(wb, a1, a2, q1, q2);
+        ++it;
+        int same = 1;
+        for (int i = 0; i < 256; ++i) {
+          same &= q1[i] == p1[i] && q2[i] == p2[i];
+          p1[i] = q1[i];
+          p2[i] = q2[i];
+        }
+        if (same || it == max_iter) break;
+      }
+      ab[0] = orc_f32_to_f16(a1);
+      ab[1] = orc_f32_to_f16(a2);
+      if (iters) iters[r * kb + b] = (uint8_t)it;
+      free_plane_step(wb, (float)orc_f16_to_f64(ab[0]), (float)orc_f16_to_f64(ab[1]), p1, p2);
+    }
   return ORC_OK;
 }

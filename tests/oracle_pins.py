@@ -741,3 +741,107 @@ def tied_invariants(o):
     assert np.array_equal(cp.reshape(3, 3, 256), c.reshape(3, 3, 256)[:, perm]) and np.array_equal(sp, s16[:, perm])
     c2, s2, it2 = o.tied_quantize(w)  # deterministic
     assert np.array_equal(c2, c) and np.array_equal(s2, s16) and np.array_equal(it2, it)
+
+
+# --------------------------------------------------------------------------------------
+# Free-scale solver (Sec. 2.1: PTQTP's alternation with two free scales; started from the
+# tied fit, whose constrained family it contains)
+# --------------------------------------------------------------------------------------
+
+_FREE_ORDER = (0, -1, 1)
+
+
+def _free_fit(o, w, max_iter=16):
+    c, s, _ = o.tied_quantize(w)
+    t1, t2, a, it = o.free_quantize(w, c, s, max_iter)
+    return c, s, t1, t2, a, it
+
+
+def _block_sq_errs(w, t1, t2, a, c, s):
+    n, k = w.shape
+    kb = k // 256
+    W = w.astype(np.float64).reshape(n, kb, 256)
+    af = _f16_to_np64(a)
+    rf = t1.reshape(n, kb, 256) * af[:, :, 0, None] + t2.reshape(n, kb, 256) * af[:, :, 1, None]
+    rt = c.astype(np.float64).reshape(n, kb, 256) * _f16_to_np64(s)[:, :, None]
+    return ((W - rf) ** 2).sum(2), ((W - rt) ** 2).sum(2)
+
+
+@pin
+def free_planes_are_the_best_pairs_at_the_stored_scales(o):
+    # 131072 weights, also stopped early (max_iter 2), so that many elements sit near a
+    # decision boundary that moves when the scales are rounded to f16
+    w = np.random.default_rng(97).standard_normal((32, 4096)).astype(np.float32) * np.float32(0.02)
+    cands = [(x, y) for x in _FREE_ORDER for y in _FREE_ORDER]
+    for max_iter in (16, 2):
+        c, s, t1, t2, a, _ = _free_fit(o, w, max_iter)
+        af = _f16_to_np64(a).astype(np.float32).astype(np.float64)
+        a1 = np.repeat(af[:, :, 0], 256, axis=1)
+        a2 = np.repeat(af[:, :, 1], 256, axis=1)
+        errs = np.stack([np.abs(w.astype(np.float64) - (a1 * x + a2 * y)) for x, y in cands])  # [9][n][k]
+        best = np.argmin(errs, axis=0)  # first minimum in the documented order
+        assert np.array_equal(t1, np.array([c_[0] for c_ in cands])[best])
+        assert np.array_equal(t2, np.array([c_[1] for c_ in cands])[best])
+
+
+@pin
+def free_first_scale_step_is_least_squares_on_the_tied_planes(o):
+    rng = np.random.default_rng(101)
+    w = (rng.standard_normal((4, 512)) * 0.03).astype(np.float32)
+    c, s, _ = o.tied_quantize(w)
+    _, _, a, it = o.free_quantize(w, c, s, max_iter=1)
+    assert np.all(it == 1)
+    t1, t2 = o.unfold(c)
+    for r in range(4):
+        for b in range(2):
+            sl = slice(256 * b, 256 * (b + 1))
+            A = np.stack([t1[r, sl], t2[r, sl]], axis=1).astype(np.float64)
+            sol = np.linalg.lstsq(A, w[r, sl].astype(np.float64), rcond=None)[0]
+            got = _f16_to_np64(a[r, b])
+            assert np.all(np.abs(got - sol) <= np.abs(sol) * 2.0 ** -10), (r, b, got, sol)
+
+
+@pin
+def free_error_is_below_the_tied_fit(o):
+    # started from the tied fit, each half-step is a least-squares optimum given the
+    # other half: no block ends worse than the tied fit beyond the f16 rounding of its
+    # two scales, and the matrix's error is strictly lower (the paper's observation)
+    w = gen_float_weights(103, 32, 1024)
+    c, s, t1, t2, a, _ = _free_fit(o, w)
+    ef, et = _block_sq_errs(w, t1, t2, a, c, s)
+    assert np.all(ef <= et * (1 + 2.0 ** -10))
+    assert ef.sum() < et.sum() * (1 - 1e-4)
+
+
+@pin
+def free_recovers_a_tied_grid_exactly_and_invariants(o):
+    rng = np.random.default_rng(107)
+    n, k = 4, 768
+    cc = rng.integers(-4, 5, (n, k)).astype(np.int8)
+    cc[:, ::256] = 4  # every block reaches the outer level
+    sb = (rng.integers(0x1C00, 0x2800, (n, k // 256)) & ~3).astype(np.uint16)  # 3s exact in f16
+    w = (cc.astype(np.float64) * np.repeat(_f16_to_np64(sb), 256, axis=1)).astype(np.float32)
+    w[1, 256:512] = 0.0  # a zero block
+    c, s, t1, t2, a, it = _free_fit(o, w)
+    ef, _ = _block_sq_errs(w, t1, t2, a, c, s)
+    assert np.all(ef == 0.0)
+    assert np.all(a[1, 1] == 0) and it[1, 1] == 0 and not t1[1, 256:512].any() and not t2[1, 256:512].any()
+    live = np.ones((n, k // 256), bool); live[1, 1] = False
+    assert np.array_equal(_f16_to_np64(a[..., 0])[live], 3 * _f16_to_np64(sb)[live])
+    assert np.array_equal(a[..., 1][live], sb[live])
+    # a zero tied scale gives a zero fit whatever codes come with it
+    cz = c.copy(); cz[3, :256] = 3
+    sz = s.copy(); sz[3, 0] = 0
+    z = o.free_quantize(w, cz, sz)
+    assert not z[0][3, :256].any() and not z[1][3, :256].any() and not z[2][3, 0].any() and z[3][3, 0] == 0
+    # determinism and block independence: a row on its own gives the same fit
+    again = o.free_quantize(w, c, s)
+    assert all(np.array_equal(x, y) for x, y in zip(again, (t1, t2, a, it)))
+    one = o.free_quantize(w[2:3], c[2:3], s[2:3])
+    assert np.array_equal(one[0], t1[2:3]) and np.array_equal(one[2], a[2:3])
+
+
+def gen_float_weights(seed, n, k):
+    r = np.random.default_rng(seed)
+    sigma = np.exp(np.log(0.005) + r.random((n, 1)) * (np.log(0.05) - np.log(0.005)))
+    return (r.standard_normal((n, k)) * sigma).astype(np.float32)

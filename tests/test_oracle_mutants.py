@@ -64,6 +64,13 @@ C_MUTANTS = {
     "mx_act_block_index": ("(double)d[tt * kb + j / 8]", "(double)d[tt * kb + j / 4]"),
     "mx_nan_scale_accepted": ("    if (e8[i] == 255) return ORC_BAD_INPUT;\n", ""),
     "mx_isum_token_dropped": ("(int64_t)q[tt * k + 32 * j + i];", "(int64_t)q[32 * j + i];"),
+    "free_ls_sign": ("const double num1 = (double)sc * u - (double)sb * v;", "const double num1 = (double)sc * u + (double)sb * v;"),
+    "free_ls_cross_terms": ("const double num2 = (double)sa * v - (double)sb * u;", "const double num2 = (double)sa * v - (double)sb * v;"),
+    "free_no_scale_step": ("        if (det > 0) {\n          const double num1", "        if (det < 0) {\n          const double num1"),
+    "free_no_final_plane_step": ("      free_plane_step(wb, (float)orc_f16_to_f64(ab[0]), (float)orc_f16_to_f64(ab[1]), p1, p2);\n", ""),
+    "free_plane_error_signed": ("double e = fabs((double)w[i] - ((double)a1 * u1 + (double)a2 * u2));", "double e = (double)w[i] - ((double)a1 * u1 + (double)a2 * u2);"),
+    "free_planes_swapped_in_fit": ("vv[i] = (double)wb[i] * (double)p2[i];", "vv[i] = (double)wb[i] * (double)p1[i];"),
+    "free_zero_block_not_zero": ("        for (int i = 0; i < 256; ++i) p1[i] = p2[i] = 0;\n", ""),
     "gemv2_alpha2_from_alpha1": ("orc_f16_to_f64(a[(r * kb + b) * 2 + 1])", "orc_f16_to_f64(a[(r * kb + b) * 2 + 0])"),
     "gemv2_scale_stride": ("orc_f16_to_f64(a[(r * kb + b) * 2 + 0])", "orc_f16_to_f64(a[(r * kb + b) + 0])"),
     "gemv2_plane2_dropped": ("        acc += term2;\n", ""),
