@@ -19,7 +19,8 @@ the same trit planes is timed beside it, and both kernels at 1, 4 and 16 tokens)
 `mxfp4` (the MXFP4 reference arm, 4.25 bits/weight, same shape and protocol, the folded
 pass over a folded matrix of that shape beside it), `stream` (the batch-1 decode layer
 with every expert in pinned host memory and an LRU pool of --slots expert slots in HBM:
-misses copied over the host link each step, eager steps).
+misses copied over the host link each step, eager steps), `freequant` (the free-scale
+solver refining each matrix's tied fit, same matrices as `tiedquant`).
 
 Cache hygiene: every step touches bytes that cannot still sit in the 256 MB last-level
 cache. Batch-1 steps route to experts not used in the previous 3 steps (reuse distance
@@ -134,6 +135,7 @@ WORKLOADS = {
     "twoplane": dict(cfg="twoplane", steps=2000, warmup=200, profile=256),
     "mxfp4": dict(cfg="mxfp4", steps=2000, warmup=200, profile=256),
     "stream": dict(cfg=1, steps=200, warmup=20, profile=0, stream=True),
+    "freequant": dict(cfg="quant", steps=64, warmup=8, profile=32, free=True),
 }
 
 
@@ -247,46 +249,73 @@ def run_quant(args, wl, cfg):
     P = args.profile_steps if args.profile_steps is not None else wl["profile"]
     # 32 x 33.5 MB of fp32 weights (1.07 GB, beyond the 256 MB last-level cache), one
     # matrix per step in rotation
+    free = wl.get("free", False)
     ws = [torch.from_numpy(gen.float_weights(gen.SEED, i, n, k)).cuda() for i in range(M)]
     outs = [tq.TqMatrix.empty(n, k) for _ in range(M)]
     iters = torch.empty((n, k // 256), dtype=torch.uint8, device="cuda")
+    if free:
+        # the free-scale solver refines each matrix's tied fit (computed once, untimed)
+        for i in range(M):
+            tq.tq_tied_quantize(ws[i], outs[i])
+        outs2 = [tq.TqMatrix2.empty(n, k) for _ in range(M)]
     torch.cuda.synchronize()
 
+    def run(i, it=None):
+        if free:
+            tq.tq_free_quantize(ws[i % M], outs[i % M], outs2[i % M], it)
+        else:
+            tq.tq_tied_quantize(ws[i % M], outs[i % M], it)
+
     def step(i):
-        tq.tq_tied_quantize(ws[i % M], outs[i % M])
+        run(i)
 
     elapsed = time_graph(step, W, K)
-    per_step = n * k * 4 + matrix_bytes(n, k)
+    # bytes: fp32 weights in, the format out (and the tied fit in, for the free solver)
+    per_step = n * k * 4 + (matrix_bytes(n, k) + n * k // 2 + n * (k // 256) * 4 if free else matrix_bytes(n, k))
     gbs = per_step * K / elapsed / 1e9
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(P)]
     torch.cuda.synchronize()
     for j in range(P):
         ev[j][0].record()
-        tq.tq_tied_quantize(ws[j % M], outs[j % M])
+        run(j)
         ev[j][1].record()
     torch.cuda.synchronize()
     ms = float(np.mean([a.elapsed_time(c) for a, c in ev]))
-    tq.tq_tied_quantize(ws[0], outs[0], iters)
+    run(0, iters)
     torch.cuda.synchronize()
     steps = iters.to(torch.float32)
-    sym = "k_tied_quantize"
+    sym = "k_free_quantize" if free else "k_tied_quantize"
+    fit = {}
+    if free:
+        # relative Frobenius reconstruction error of both fits of matrix 0 (host, fp64)
+        w0 = ws[0].cpu().numpy().astype(np.float64).reshape(n, k // 256, 256)
+        tc = tq.tq_unpack_host(outs[0].codes.cpu().numpy(), n, k).astype(np.float64).reshape(n, k // 256, 256)
+        ts = outs[0].scales.cpu().numpy().view(np.float16).astype(np.float64)
+        p1, p2 = tq.tq_unpack2_host(outs2[0].codes.cpu().numpy(), n, k)
+        fa = outs2[0].scales.cpu().numpy().view(np.float16).astype(np.float64)
+        rt = tc * ts[:, :, None]
+        rf = p1.reshape(n, k // 256, 256) * fa[:, :, 0, None] + p2.reshape(n, k // 256, 256) * fa[:, :, 1, None]
+        nw = np.sqrt((w0 ** 2).sum())
+        fit = {"tied_rel_frobenius_error": round(float(np.sqrt(((w0 - rt) ** 2).sum()) / nw), 5),
+               "free_rel_frobenius_error": round(float(np.sqrt(((w0 - rf) ** 2).sum()) / nw), 5)}
     valu = _recorded(sym, "valu_insts_per_launch", "valu")
     if valu is None:  # no current instruction count: fall back to the bytes
-        roof = hbm_roof("tied_quantize", per_step, ms, sym)
+        roof = hbm_roof("free_quantize" if free else "tied_quantize", per_step, ms, sym)
     else:
         # the kernel is bound by VALU issue: its wave64 VALU instructions per launch
         # (SQ_INSTS_VALU, rocprofv3, committed record) over its mean duration
         achieved = valu / (ms * 1e-3) / 1e9
-        roof = {"kernel": "tied_quantize", "bound": "alu", "achieved": round(achieved, 1), "peak": VALU_PEAK_GINST,
+        roof = {"kernel": "free_quantize" if free else "tied_quantize", "bound": "alu", "achieved": round(achieved, 1), "peak": VALU_PEAK_GINST,
                 "unit": "G VALU wave64 instructions/s", "frac": round(achieved / VALU_PEAK_GINST, 4),
                 "traffic": recorded_traffic(sym), "valu_insts_per_launch": valu, "bytes_per_launch": per_step,
                 "hbm_GBps": round(per_step / (ms * 1e-3) / 1e9, 1), "mean_ms": round(ms, 5), "kernel_symbol": sym}
     return dict(value=gbs, K=K, W=W, elapsed=elapsed, tokens=K, roof=roof,
-                config={"workload": cfg["name"], "matrices": M, "n": n, "k": k, "max_iter": 16,
+                config={"workload": cfg["name"].replace("tied", "free") if free else cfg["name"], "matrices": M,
+                        "n": n, "k": k, "max_iter": 16,
                         "weights": "N(0,1) x per-row spread log-uniform [0.005, 0.05], fp32"},
                 extra={"weights_per_s": round(n * k * K / elapsed, 1),
-                       "mean_code_steps_per_block": round(float(steps.mean()), 3),
-                       "max_code_steps_per_block": int(steps.max())})
+                       ("mean_plane_steps_per_block" if free else "mean_code_steps_per_block"): round(float(steps.mean()), 3),
+                       ("max_plane_steps_per_block" if free else "max_code_steps_per_block"): int(steps.max()), **fit})
 
 
 def cpu_baseline_twoplane(cfg, target_s: float = 10.0) -> dict:

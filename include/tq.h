@@ -196,6 +196,29 @@ tq_status tq_pack2_host(const int8_t* t1, const int8_t* t2, int32_t n, int32_t k
 /* Inverse of tq_pack2_host on the host. TQ_ERR_INVALID on the unused pattern 10. */
 tq_status tq_unpack2_host(const uint8_t* codes, int32_t n, int32_t k, int8_t* t1_out, int8_t* t2_out);
 
+/* Free-scale solver (Sec. 2.1: PTQTP's alternation of plane and scale updates with two
+ * free scales per group), started from a tied fit of the same weights (tq_tied_quantize
+ * output: its codes and f16 scales) and written in the two-plane layout above. Per
+ * 256-weight block, the reading taken (the paper gives no start, stop rule or
+ * precision):
+ *   start: planes = the unfolded tied codes, (alpha1, alpha2) = (3 s, s) with s the tied
+ *   f16 scale; s = 0 gives a zero fit. Then, until a plane step repeats the previous
+ *   planes or max_iter plane steps were taken (1..255):
+ *   scale step: with a = <T1,T1>, b = <T1,T2>, c = <T2,T2> (exact), u = <w,T1> and
+ *   v = <w,T2> (fp64 products, pairwise-halving sums as in tq_tied_quantize), and
+ *   det = a c - b^2: if det > 0, alpha1 = fl32((c u - b v) / det), alpha2 =
+ *   fl32((a v - b u) / det), each fp64 operation rounded on its own (no fused
+ *   multiply-add); otherwise the scales stay;
+ *   plane step: each weight takes the first pair (t1, t2), t1 and then t2 in the order
+ *   0, -1, +1, with the least |w - (alpha1 t1 + alpha2 t2)| in fp64.
+ *   The stored scales are f16 (nearest even, saturating at +-65504) and the stored planes
+ *   a plane step at those scales. iters: NULL or [n][kb] bytes, the plane steps taken
+ *   per block (0 for a zero block). w finite, 4-byte aligned; tied codes 128-byte, tied
+ *   scales 2-byte, codes2 128-byte, scales2 ([n][kb][2]) 4-byte aligned. Deterministic. */
+tq_status tq_free_quantize(const float* w, int32_t n, int32_t k, int32_t max_iter, const uint8_t* tied_codes,
+                           const uint16_t* tied_scales, uint8_t* codes2, uint16_t* scales2, uint8_t* iters,
+                           void* stream);
+
 /* The two-plane pass for one matrix and t tokens (formula above). q, d as from
  * tq_quantize_act (q 16-byte aligned). isum_dbg: NULL, or a [t][n][kb][2] int32 buffer
  * that receives the exact per-plane block sums (plane 1 first). n >= 1, 256 <= k <=

@@ -80,6 +80,7 @@ for _name, _args, _res in [
     ("tq_gemv_timed", [_P(tq_mat), _vp, _vp, _vp, _i64, _vp, _vp, _vp, _P(_vp)], _i32),
     ("tq_pack2_host", [_vp, _vp, _i32, _i32, _vp], _i32),
     ("tq_unpack2_host", [_vp, _i32, _i32, _vp, _vp], _i32),
+    ("tq_free_quantize", [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
     ("tq_gemv2", [_P(tq_mat2), _vp, _vp, _i64, _vp, _vp, _vp], _i32),
     ("tq_gemv2_timed", [_P(tq_mat2), _vp, _vp, _i64, _vp, _vp, _vp, _P(_vp)], _i32),
     ("tq_mx_pack_host", [_vp, _i32, _i32, _vp], _i32),
@@ -278,6 +279,21 @@ class TqMatrix2:
         _dev(self.codes, torch.uint8, "codes", (self.n, self.k // 256, 128))
         _dev(self.scales, torch.int16, "scales", (self.n, self.k // 256, 2))
         return tq_mat2(self.n, self.k, self.codes.data_ptr(), self.scales.data_ptr())
+
+
+def tq_free_quantize(w: torch.Tensor, tied: TqMatrix, out: TqMatrix2, iters: torch.Tensor | None = None,
+                     max_iter: int = 16, stream=None):
+    """Free-scale solver: w [n][k] fp32 and its tied fit -> out's two planes and scale pairs;
+    iters: None or a [n][k/256] uint8 tensor that receives the plane steps per block."""
+    n, k = w.shape
+    if (tied.n, tied.k) != (n, k) or (out.n, out.k) != (n, k):
+        raise ValueError("tq_free_quantize: matrices must match the weights' shape")
+    it = 0 if iters is None else _dev(iters, torch.uint8, "iters", (n, k // 256))
+    _ok(_L.tq_free_quantize(_dev(w, torch.float32, "w"), n, k, max_iter,
+                            _dev(tied.codes, torch.uint8, "tied codes", (n, k // 256, 128)),
+                            _dev(tied.scales, torch.int16, "tied scales", (n, k // 256)),
+                            _dev(out.codes, torch.uint8, "codes2", (n, k // 256, 128)),
+                            _dev(out.scales, torch.int16, "scales2", (n, k // 256, 2)), it or None, _stream(stream)))
 
 
 def _gemv2_args(m: TqMatrix2, q, d, y, isum_dbg):

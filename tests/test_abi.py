@@ -229,6 +229,26 @@ def test_gemv_mx_validation_errors_before_launch():
 
 
 @no_gpu_only
+def test_free_quantize_validation_errors_before_launch():
+    L = tq._L
+    ok = (FAKE, 4, 256, 16, FAKE, FAKE, FAKE, FAKE, None, None)
+    def call(**kw):
+        args = list(ok)
+        for i, v in kw.items():
+            args[int(i[1:])] = v
+        return L.tq_free_quantize(*args)
+    assert call(a2=300) == tq.TQ_ERR_INVALID          # k % 256
+    assert call(a1=-1) == tq.TQ_ERR_INVALID           # n < 0
+    assert call(a3=0) == tq.TQ_ERR_INVALID            # max_iter
+    assert call(a3=256) == tq.TQ_ERR_INVALID
+    assert call(a4=None) == tq.TQ_ERR_INVALID         # tied codes
+    assert call(a6=FAKE + 64) == tq.TQ_ERR_ALIGN      # codes2
+    assert call(a7=FAKE + 2) == tq.TQ_ERR_ALIGN       # scale pairs
+    assert call(a5=FAKE + 1) == tq.TQ_ERR_ALIGN       # tied scales
+    assert call(a1=0) == tq.TQ_OK                     # nothing to do
+
+
+@no_gpu_only
 def test_tied_quantize_validation_errors_before_launch():
     L = tq._L
     assert L.tq_tied_quantize(FAKE, 4, 300, 16, FAKE, FAKE, None, None) == tq.TQ_ERR_INVALID  # k % 256
