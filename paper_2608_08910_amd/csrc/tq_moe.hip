@@ -533,9 +533,10 @@ __global__ __launch_bounds__(256) void k_moe_combine(MoeArgs A, float* __restric
 //    unpacks them to 16c bytes as the B operands (lane: row l & 15, chunk 4t + (l >> 4),
 //    half h gives MFMA (t, h); the A operand takes the same 16 columns of the token's
 //    codes, so every product pairs matching columns);
-//  - four MFMAs per 16x16 output tile accumulate sum (16c)*q = 16 * isum exactly, and one
-//    fp32 multiply-add per output applies (f32(s) / 16) * d to it; 16-token sub-tiles
-//    past the expert's last token are skipped.
+//  - four MFMAs per 16x16 output tile accumulate sum (16c)*q = 16 * isum exactly (two
+//    sub-tiles at a time, so that 2 * NMAT independent chains interleave), and one
+//    fp32 multiply-add per output applies (f32(s) / 16) * d to it; pairs of 16-token
+//    sub-tiles past the expert's last token are skipped.
 // Tasks run hottest expert first, row tiles innermost: the workgroups running together
 // share a token tile through L2, and the tasks of one weight tile run RT tasks apart.
 // ---------------------------------------------------------------------------------
@@ -697,31 +698,55 @@ __global__ __launch_bounds__(kMWaves * 64) void k_moe_mfma(MoeArgs A) {
       // flight (past the last block: block kb - 1 again, into a stage and registers no
       // longer read)
       const int nb = min(b + 2, kb - 1);
+      // sub-tiles in pairs: one straight-line stretch holds 2 * NMAT independent MFMA
+      // chains, so one chain's epilogue overlaps the others' MFMAs (a pair whose second
+      // sub-tile holds no valid token computes it anyway: its rows repeat the last valid
+      // token and are not stored)
 #pragma unroll
-      for (int mt = 0; mt < kMT / 16; ++mt) {
-        if (mt < 4) mfma_a_dma(na, ap[mt], nb, wv, mt);
-        if (mt == 4) mfma_b_fetch<NMAT>(Bs, mr, wrow, kb, g, nb);
-        if (mt >= nsub) continue;  // no valid token in this sub-tile
-        const int8_t* arow_lds = sa + (mt * 16 + li) * 256;
-        v4i aop[2][2];
+      for (int mp = 0; mp < kMT / 32; ++mp) {
+        if (mp < 2) {
+          mfma_a_dma(na, ap[2 * mp], nb, wv, 2 * mp);
+          mfma_a_dma(na, ap[2 * mp + 1], nb, wv, 2 * mp + 1);
+        }
+        if (mp == 2) mfma_b_fetch<NMAT>(Bs, mr, wrow, kb, g, nb);
+        if (2 * mp >= nsub) continue;  // no valid token in this pair
+        v4i aop[2][2][2];
+        float4 d4[2];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const int mt = 2 * mp + q;
+          const int8_t* arow_lds = sa + (mt * 16 + li) * 256;
+#pragma unroll
+          for (int c = 0; c < 2; ++c)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) aop[q][c][h] = lds_v4i(arow_lds + (((2 * (4 * c + g) + h) ^ li) * 16));
+          d4[q] = *reinterpret_cast<const float4*>(&sd[mt * 16 + 4 * g]);
+        }
+        v4i C[2][NMAT];
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+          for (int m = 0; m < NMAT; ++m) C[q][m] = v4i{0, 0, 0, 0};
 #pragma unroll
         for (int c = 0; c < 2; ++c)
 #pragma unroll
-          for (int h = 0; h < 2; ++h) aop[c][h] = lds_v4i(arow_lds + (((2 * (4 * c + g) + h) ^ li) * 16));
-        const float4 d4 = *reinterpret_cast<const float4*>(&sd[mt * 16 + 4 * g]);
+          for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int m = 0; m < NMAT; ++m) {
-          v4i C = v4i{0, 0, 0, 0};
-          C = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[0][0], bop[m][0][0], C, 0, 0, 0);
-          C = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[0][1], bop[m][0][1], C, 0, 0, 0);
-          C = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[1][0], bop[m][1][0], C, 0, 0, 0);
-          C = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[1][1], bop[m][1][1], C, 0, 0, 0);
-          // C = 16 * isum exactly (|C| < 2^21, so (float)C is exact too)
-          acc[mt][m][0] = fmaf(sf[m] * d4.x, (float)C[0], acc[mt][m][0]);
-          acc[mt][m][1] = fmaf(sf[m] * d4.y, (float)C[1], acc[mt][m][1]);
-          acc[mt][m][2] = fmaf(sf[m] * d4.z, (float)C[2], acc[mt][m][2]);
-          acc[mt][m][3] = fmaf(sf[m] * d4.w, (float)C[3], acc[mt][m][3]);
-        }
+            for (int q = 0; q < 2; ++q)
+#pragma unroll
+              for (int m = 0; m < NMAT; ++m)
+                C[q][m] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[q][c][h], bop[m][c][h], C[q][m], 0, 0, 0);
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+          for (int m = 0; m < NMAT; ++m) {
+            // C = 16 * isum exactly (|C| < 2^21, so (float)C is exact too)
+            const int mt = 2 * mp + q;
+            acc[mt][m][0] = fmaf(sf[m] * d4[q].x, (float)C[q][m][0], acc[mt][m][0]);
+            acc[mt][m][1] = fmaf(sf[m] * d4[q].y, (float)C[q][m][1], acc[mt][m][1]);
+            acc[mt][m][2] = fmaf(sf[m] * d4[q].z, (float)C[q][m][2], acc[mt][m][2]);
+            acc[mt][m][3] = fmaf(sf[m] * d4[q].w, (float)C[q][m][3], acc[mt][m][3]);
+          }
       }
     };
     using I0 = std::integral_constant<int, 0>;
