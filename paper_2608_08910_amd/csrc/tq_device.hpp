@@ -57,23 +57,6 @@ __device__ __forceinline__ void unpack16c(const uint4 w, int (&c)[8]) {
   c[4] = hi16c(w.x); c[5] = hi16c(w.y); c[6] = hi16c(w.z); c[7] = hi16c(w.w);
 }
 
-// Free-scale two-plane chunks: the 16 bytes of chunk j hold plane 1's 32 trits in bytes
-// 0..7 and plane 2's in bytes 8..15; within a plane's two dwords, dword u, byte b, bit
-// pair 2s..2s+1 is column 32j + 16u + 4s + b as a 2-bit two's-complement trit (00 = 0,
-// 01 = +1, 11 = -1). Shifting the pair to a byte's top bits and masking leaves 64*t as a
-// signed byte, so a plane decodes in one or two bitwise operations per activation dword
-// and the byte dot's sum is exactly 64 times the trit dot.
-constexpr uint32_t kTopPairs = 0xC0C0C0C0u;
-
-// One plane's 32 trits (dwords w0, w1) as 64t bytes in the order of the activation
-// dwords: t[4u + s] = columns 16u + 4s .. 16u + 4s + 3.
-__device__ __forceinline__ void unpack64t(uint32_t w0, uint32_t w1, int (&t)[8]) {
-  t[0] = int((w0 << 6) & kTopPairs); t[1] = int((w0 << 4) & kTopPairs);
-  t[2] = int((w0 << 2) & kTopPairs); t[3] = int(w0 & kTopPairs);
-  t[4] = int((w1 << 6) & kTopPairs); t[5] = int((w1 << 4) & kTopPairs);
-  t[6] = int((w1 << 2) & kTopPairs); t[7] = int(w1 & kTopPairs);
-}
-
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // 16-byte streaming load (nontemporal: expert weights are read once per step).
