@@ -151,17 +151,18 @@ struct MoeArgs {
 };
 
 // ---------------------------------------------------------------------------------
-// prologue: quantize x (workgroups 0 .. nq-1) + dispatch (last workgroup)
+// prologue: dispatch (workgroup 0, dispatched first so that it runs beside the
+// quantization rather than after it) + quantize x (workgroups 1 .. nq)
 // ---------------------------------------------------------------------------------
 
-__global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ x, MoeArgs A, int nq) {
-  if ((int)blockIdx.x < nq) {
+__global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ x, MoeArgs A) {
+  if (blockIdx.x > 0) {
     const int64_t nblocks = A.t * (A.hidden / 256);
-    quantize_wave_blocks(x, nblocks, (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6), A.xq, A.xd, A.xb);
+    quantize_wave_blocks(x, nblocks, (int64_t)(blockIdx.x - 1) * 4 + (threadIdx.x >> 6), A.xq, A.xd, A.xb);
     return;
   }
   __shared__ int s_cnt[kMaxExperts];   // slots per expert
-  __shared__ int s_base[kMaxExperts];  // rank of an active expert, then its slot cursor
+  __shared__ __attribute__((aligned(16))) int s_base[kMaxExperts];  // rank key, then the slot cursor
   __shared__ int s_ebr[kMaxExperts];   // expert of each rank
   __shared__ int s_scan[256], s_scan2[256];
   __shared__ int s_nact, s_bad;
@@ -173,33 +174,74 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
     s_nact = 0;
   }
   __syncthreads();
-  for (int64_t s = tid; s < S; s += 256) {
-    const int e = A.topk_idx[s];
-    if (e >= 0 && e < E) atomicAdd(&s_cnt[e], 1);
-    else s_bad = 1;
+  // The slots' expert ids, kSB per thread at a time, all requested before any is used
+  // (one round trip per batch rather than one per slot); a step of at most 256 * kSB
+  // slots keeps its one batch in registers for the placement pass at the end.
+  constexpr int kSB = 16;
+  int ev[kSB];
+  const auto load_ids = [&](int64_t s0) {
+#pragma unroll
+    for (int i = 0; i < kSB; ++i) ev[i] = A.topk_idx[min(s0 + tid + 256 * i, S - 1)];
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  for (int64_t s0 = 0; s0 < S; s0 += 256 * kSB) {
+    load_ids(s0);
+#pragma unroll
+    for (int i = 0; i < kSB; ++i) {
+      if (s0 + tid + 256 * i >= S) continue;
+      const int e = ev[i];
+      if (e >= 0 && e < E) atomicAdd(&s_cnt[e], 1);
+      else s_bad = 1;
+    }
   }
   __syncthreads();
   // Rank the active experts. With more than one token per step, hottest first (count
   // descending, id ascending): the work queues below hand out tasks in rank order, so
-  // the longest tasks start first, one per workgroup. One token: id order.
-  const bool by_count = A.t > 1 && E <= 1024;
-  for (int e = tid; e < E; e += 256) {
-    const int c = s_cnt[e];
-    int r = -1;
-    if (c > 0) {
-      r = 0;
-      if (by_count) {
-        for (int e2 = 0; e2 < E; ++e2) {
-          const int c2 = s_cnt[e2];
-          r += (c2 > c) | ((c2 == c) & (e2 < e));
-        }
-      } else {
-        for (int e2 = 0; e2 < e; ++e2) r += s_cnt[e2] > 0;
+  // the longest tasks start first, one per workgroup. One token (or more experts or
+  // slots than the key below holds): id order. The order only schedules work; no
+  // output depends on it.
+  const bool by_count = A.t > 1 && E <= 1024 && S < ((int64_t)1 << 19);
+  if (by_count) {
+    // key = count above (2047 - id): distinct, and larger exactly for an earlier rank;
+    // 0 for an inactive expert. A rank counts the larger keys, four per broadcast LDS
+    // read (a loop of dependent single reads costs an LDS round trip per expert).
+    const int E4 = (E + 3) & ~3;
+    for (int e = tid; e < E4; e += 256) {
+      const int c = e < E ? s_cnt[e] : 0;
+      s_base[e] = c > 0 ? (c << 11) | (2047 - e) : 0;
+      if (c > 0) atomicAdd(&s_nact, 1);
+    }
+    __syncthreads();
+    const int4* k4 = reinterpret_cast<const int4*>(s_base);
+    for (int e = tid; e < E; e += 256) {
+      const int k = s_base[e];
+      if (k == 0) continue;
+      int r = 0;
+#pragma unroll 8
+      for (int i = 0; i < E4 / 4; ++i) {
+        const int4 v = k4[i];
+        r += (v.x > k) + (v.y > k) + (v.z > k) + (v.w > k);
       }
       s_ebr[r] = e;
-      atomicAdd(&s_nact, 1);
     }
-    s_base[e] = r;
+  } else {
+    // an expert's rank is the number of active experts below it: a scan of the active
+    // flags over contiguous id ranges
+    const int per = (E + 255) / 256, e0 = min(E, tid * per), e1 = min(E, e0 + per);
+    int na = 0;
+    for (int e = e0; e < e1; ++e) na += s_cnt[e] > 0;
+    s_scan[tid] = na;
+    __syncthreads();
+    for (int off = 1; off < 256; off <<= 1) {
+      const int v = tid >= off ? s_scan[tid - off] : 0;
+      __syncthreads();
+      s_scan[tid] += v;
+      __syncthreads();
+    }
+    int r = s_scan[tid] - na;
+    for (int e = e0; e < e1; ++e)
+      if (s_cnt[e] > 0) s_ebr[r++] = e;
+    if (tid == 255) s_nact = s_scan[255];
   }
   __syncthreads();
   const int n_active = s_nact;
@@ -229,7 +271,7 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
     A.active[r] = e;
     A.act_off[r] = pos;
     A.tt_off[r] = tpos;
-    s_base[e] = pos;  // rank no longer needed: becomes the expert's slot cursor
+    s_base[e] = pos;  // key no longer needed: becomes the expert's slot cursor
     pos += s_cnt[e];
     for (const int t1 = tpos + (s_cnt[e] + kMT - 1) / kMT; tpos < t1; ++tpos) A.tile_exp[tpos] = r;
   }
@@ -246,16 +288,22 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
     A.ctrl[kFlags] = s_bad ? 1 : 0;
   }
   __syncthreads();
-  for (int64_t s = tid; s < S; s += 256) {
-    const int e = A.topk_idx[s];
-    if (e >= 0 && e < E) {
-      const int p = atomicAdd(&s_base[e], 1);
-      A.slot_list[p] = (int)s;
-    } else {
-      // an unrouted slot: its hidden row is defined (zero) so the requant stage reads
-      // finite values; the combine skips the slot.
-      float4* hp = reinterpret_cast<float4*>(A.h + s * A.inter);
-      for (int c = 0; c < A.inter / 4; ++c) hp[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int64_t s0 = 0; s0 < S; s0 += 256 * kSB) {
+    if (S > 256 * kSB) load_ids(s0);  // otherwise ev still holds the only batch
+#pragma unroll
+    for (int i = 0; i < kSB; ++i) {
+      const int64_t s = s0 + tid + 256 * i;
+      if (s >= S) continue;
+      const int e = ev[i];
+      if (e >= 0 && e < E) {
+        const int p = atomicAdd(&s_base[e], 1);
+        A.slot_list[p] = (int)s;
+      } else {
+        // an unrouted slot: its hidden row is defined (zero) so the requant stage reads
+        // finite values; the combine skips the slot.
+        float4* hp = reinterpret_cast<float4*>(A.h + s * A.inter);
+        for (int c = 0; c < A.inter / 4; ++c) hp[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
     }
   }
 }
@@ -1388,7 +1436,7 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
 #endif
   const unsigned g_mgu = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mgu, TQ_MFMA_GRID);
   const unsigned g_mdn = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mdn, TQ_MFMA_GRID);
-  if ((st = launch_stage(events, 0, k_moe_prologue, dim3(nq + 1), 256, stm, fn, x, A, nq)) != TQ_OK) return st;
+  if ((st = launch_stage(events, 0, k_moe_prologue, dim3(nq + 1), 256, stm, fn, x, A)) != TQ_OK) return st;
   if (mfma) st = launch_stage(events, 1, k_moe_mfma<2>, dim3(g_mgu), kMWaves * 64, stm, fn, A);
   else st = launch_stage(events, 1, pick_tb<2>(ex->hidden / 256), dim3(g_gu), kTbWaves * 64, stm, fn, A);
   if (st != TQ_OK) return st;
