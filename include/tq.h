@@ -292,6 +292,9 @@ tq_status tq_gemv_mx_timed(const tq_mat_mx* w, const int8_t* q, const float* d, 
  * own unless TQ_MOE_FORCE_MFMA is given (tq_moe_path). */
 #define TQ_MOE_FORCE_VALU 1
 #define TQ_MOE_FORCE_MFMA 2
+tq_status tq_moe_grouped(const tq_experts* ex, const float* x, int64_t t,
+                         const int32_t* topk_idx, const float* topk_w, int32_t topk,
+                         float* out, void* ws, size_t ws_bytes, int32_t flags, void* stream);
 size_t tq_moe_workspace_bytes(const tq_experts* ex, int64_t t, int32_t topk);
 
 /* The path tq_moe_grouped takes for these arguments: TQ_MOE_PATH_T1 (single token: a

@@ -32,6 +32,34 @@ def test_every_declared_symbol_is_exported():
     assert not missing, missing
 
 
+def test_every_defined_entry_point_is_declared():
+    # the reverse direction: an extern "C" definition in the sources without a declaration
+    # in the header would be an entry point no C caller can see
+    csrc = os.path.join(ROOT, "paper_2608_08910_amd", "csrc")
+    defined = set()
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".cpp")):
+            src = open(os.path.join(csrc, f)).read()
+            defined |= set(re.findall(r'extern "C"\s+[\w\s\*]*?\b(tq_[a-z0-9_]+)\s*\(', src))
+    assert {"tq_quantize_act", "tq_gemv", "tq_moe_grouped"} <= defined
+    missing = sorted(defined - set(declared_functions()))
+    assert not missing, missing
+
+
+@pytest.mark.parametrize("lang", ["c", "c++"])
+def test_header_compiles_standalone(lang, tmp_path):
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc" if lang == "c" else "g++")
+    if cc is None:
+        pytest.skip("no host compiler")
+    src = tmp_path / ("h.c" if lang == "c" else "h.cpp")
+    src.write_text('#include "tq.h"\nint main(void) { return (int)sizeof(tq_experts) > 0 ? 0 : 1; }\n')
+    r = subprocess.run([cc, "-fsyntax-only", "-Wall", "-Werror", "-I", os.path.join(ROOT, "include"), str(src)],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+
+
 def test_format_size_is_paper_bits_per_weight():
     bpw = GOLDEN["bits_per_weight"]
     assert bpw["tq2_0_fx4_block_bytes"] * 8 / bpw["tq2_0_fx4_block_weights"] == bpw["tq2_0_fx4"]
