@@ -349,3 +349,47 @@ def test_t1_graph_replays_match_eager(tq, oracle):
         torch.cuda.synchronize()
         assert torch.equal(tmp, eager[rep])
     assert tq.tq_moe_status(ws, ex, 1, topk) == 0
+
+
+@pytest.mark.parametrize("flags,T", [(1, 24), (2, 40)])
+def test_grouped_graph_replays_match_eager(tq, oracle, flags, T):
+    """Grouped calls (forced VALU, forced MFMA) captured in a HIP graph, each call with its
+    own routing: every replay (with eager calls on the same workspace between replays)
+    gives bitwise the eager outputs, so the dispatch's counters and lists are rebuilt on
+    every replay."""
+    E, H, I, topk = 16, 1024, 512, 4
+    ex, _ = host_experts(tq, oracle, E, H, I, seed=93 + flags)
+    rng = np.random.default_rng(94 + flags)
+    n = 3
+    xs = torch.from_numpy(rng.standard_normal((n, T, H)).astype(np.float32)).cuda()
+    idx = torch.from_numpy(np.stack([np.stack([rng.choice(E, topk, replace=False) for _ in range(T)])
+                                     for _ in range(n)]).astype(np.int32)).cuda()
+    w = torch.from_numpy(rng.uniform(0.1, 1.0, (n, T, topk)).astype(np.float32)).cuda()
+    ws = tq.moe_workspace(ex, T, topk)
+    announce(f"moe grouped graph capture flags={flags} T={T}")
+    eager = [torch.empty((T, H), dtype=torch.float32, device="cuda") for _ in range(n)]
+    for i in range(n):
+        tq.tq_moe_grouped(ex, xs[i], idx[i], w[i], eager[i], ws, flags=flags)
+    torch.cuda.synchronize()
+    outs = [torch.empty((T, H), dtype=torch.float32, device="cuda") for _ in range(n)]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            for i in range(n):
+                tq.tq_moe_grouped(ex, xs[i], idx[i], w[i], outs[i], ws, flags=flags, stream=s)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for o in outs:
+            o.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        for i in range(n):
+            assert torch.equal(outs[i], eager[i]), f"replay {rep} call {i}"
+        tmp = torch.empty((T, H), dtype=torch.float32, device="cuda")
+        tq.tq_moe_grouped(ex, xs[rep], idx[rep], w[rep], tmp, ws, flags=flags)  # eager work between replays
+        torch.cuda.synchronize()
+        assert torch.equal(tmp, eager[rep])
+    assert tq.tq_moe_status(ws, ex, T, topk) == 0
+    assert tq.tq_moe_path(ex, T, topk, flags) == flags
