@@ -970,7 +970,8 @@ __device__ __forceinline__ void t1_gateup_wg(const float* __restrict__ x, const 
   // x first (its wait must not queue behind the weights), then every weight load
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, (uint32_t)A.hidden * 4u);
   float v[32];
-  buf_load32f(xr, (uint32_t)min(gid, kb - 1), cp, v);
+  const bool xw = wv * 8 < kb;  // wave-uniform: the wave has blocks of x to quantize
+  if (xw) buf_load32f(xr, (uint32_t)min(gid, kb - 1), cp, v);
   __builtin_amdgcn_sched_barrier(0);
   const MatRsrc mr[2] = {mat_rsrc(A.codes[0] + ec * A.stride_codes[0], A.scales[0] + ec * A.stride_scales[0], I, kb),
                          mat_rsrc(A.codes[1] + ec * A.stride_codes[1], A.scales[1] + ec * A.stride_scales[1], I, kb)};
@@ -986,7 +987,7 @@ __device__ __forceinline__ void t1_gateup_wg(const float* __restrict__ x, const 
   const int lrow = min(row0 + rev_bits<clog2(RPW)>(lane & (RPW - 1)), I - 1);
 #pragma unroll
   for (int m = 0; m < 2; ++m) load_lane_scales<NL>(mr[m], lrow, kb, g, sr[m]);
-  quantize_to_lds(v, min(gid, kb - 1), cp, s.q, s.d, s.b, gid < kb);
+  if (xw) quantize_to_lds(v, min(gid, kb - 1), cp, s.q, s.d, s.b, gid < kb);
   for (int blk = gid + WAVES * 8; blk < kb; blk += WAVES * 8) {
     buf_load32f(xr, (uint32_t)blk, cp, v);
     quantize_to_lds(v, blk, cp, s.q, s.d, s.b, true);
