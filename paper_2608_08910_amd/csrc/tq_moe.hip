@@ -934,7 +934,7 @@ __device__ __forceinline__ void buf_load32f(__amdgpu_buffer_rsrc_t r, uint32_t b
 // Layout of the single-token kernels' LDS: the quantized activations of one token (x, or
 // the topk slots' h), their block scales and code sums, and per-wave row results.
 constexpr int kT1LdsQ = kMaxK > kT1MaxHq ? kMaxK : kT1MaxHq;
-constexpr int kT1MaxWaves = 16;  // waves of a single-token workgroup the row-result area holds
+constexpr int kT1MaxWaves = 8;  // waves of a single-token down workgroup the row-result area holds
 constexpr int kT1LdsBytes = kT1LdsQ + 2 * (kT1LdsQ / 256) * 4 + kT1MaxWaves * 32 * 4;
 
 struct T1Lds {
@@ -1060,10 +1060,9 @@ __device__ __forceinline__ void t1_down_wg(const MoeArgs& A, float* __restrict__
   // first block instead and skips the quantization)
   const int blk0 = min(gid, nblk - 1);
   const bool q0 = gid < nblk && ((vmask >> (blk0 / kb)) & 1);
-  const bool hw = wv * 8 < nblk;  // wave-uniform: the wave has blocks of h to quantize
   const __amdgpu_buffer_rsrc_t hr = make_rsrc(A.h, (uint32_t)(TOPK * I) * 4u);
   float v[32];
-  if (hw) buf_load32f(hr, (uint32_t)(q0 ? blk0 : 0), cp, v);
+  buf_load32f(hr, (uint32_t)(q0 ? blk0 : 0), cp, v);
   __builtin_amdgcn_sched_barrier(0);
   uint4 wr[TOPK][RPW][NL];
 #pragma unroll
@@ -1089,7 +1088,7 @@ __device__ __forceinline__ void t1_down_wg(const MoeArgs& A, float* __restrict__
 #pragma unroll
     for (int i = 0; i < NL; ++i) sr[k][i] = sp[min(8 * i + g, kb - 1)];
   }
-  if (hw) quantize_to_lds(v, blk0, cp, s.q, s.d, s.b, q0);
+  quantize_to_lds(v, blk0, cp, s.q, s.d, s.b, q0);
   for (int blk = gid + WAVES * 8; blk < nblk; blk += WAVES * 8) {
     if (!((vmask >> (blk / kb)) & 1)) continue;
     buf_load32f(hr, (uint32_t)blk, cp, v);
