@@ -341,9 +341,10 @@ tq_status tq_moe_status(const void* ws, const tq_experts* ex, int64_t t, int32_t
                         int32_t* flags_out, void* stream);
 
 /* ---------------------------------------------------------------------------------
- * Host-tier expert streaming (Sec. 2.2: "the fold is the file" -- an expert-projection
- * miss is one contiguous read, and resident and streamed serving use the same bytes and
- * kernels, so outputs are bitwise independent of where an expert was cached; the
+ * Host-tier expert streaming (Sec. 2.2: the folded planes are the stored file itself,
+ * so an expert-projection miss is one contiguous read, and resident and streamed
+ * serving use the same bytes and kernels, so outputs are bitwise independent of where
+ * an expert was cached; the
  * paper's store keeps pinned RAM and LRU slots in front of the file). Tiers here: every
  * expert in pinned host memory, a pool of expert slots in HBM.
  * An expert record is one contiguous range: gate, up, down codes, then gate, up, down

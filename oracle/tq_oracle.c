@@ -97,7 +97,7 @@ int orc_two_plane_dequant(const int8_t* t1, const int8_t* t2, int64_t n, double 
 
 /* ------------------------------------------------------------------------------ */
 /* IEEE 754 binary16 decode. The tied scale s is serialized as f16 (Sec. 2.1,     */
-/* "scales serialize to f16"; Sec. 2.2, four f16 column scales per block).          */
+/* the scales are stored as f16; Sec. 2.2, four f16 column scales per block).       */
 /* 1 sign bit, 5 exponent bits (bias 15), 10 fraction bits.                         */
 /* ------------------------------------------------------------------------------ */
 

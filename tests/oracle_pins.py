@@ -100,7 +100,7 @@ def level_sets_match_paper(o):
 
 
 # --------------------------------------------------------------------------------------
-# f16 scale decode (Sec. 2.1: scales serialize to f16)
+# f16 scale decode (Sec. 2.1: the scales are stored as f16)
 # --------------------------------------------------------------------------------------
 
 @pin
