@@ -166,8 +166,8 @@ tq_status tq_gemv_timed(const tq_mat* w, const int8_t* q, const float* d, const 
 /* ---------------------------------------------------------------------------------
  * Free-scale two-plane variant (Sec. 2.1: PTQTP's W ~ alpha1*T1 + alpha2*T2 with two
  * free scales per group, the family the tie constrains; Sec. 4.1, the quality table's
- * note: the free pair does not fold, and its serving format keeps two separate trit
- * planes at 4.125 bits/weight). The ablation of the fold: same blocks, same activations,
+ * note: the free pair does not fold, so it is served as its two trit planes, stored
+ * apart: 4.125 bits/weight). The ablation of the fold: same blocks, same activations,
  * one integer pass per plane.
  *   codes  [n][kb][128] bytes, 128-byte aligned. Chunk j (bytes 16j .. 16j+15 of a
  *          block) covers columns 32j .. 32j+31: bytes 16j .. 16j+7 are plane 1, bytes
@@ -232,8 +232,8 @@ tq_status tq_gemv2_timed(const tq_mat2* w, const int8_t* q, const float* d, int6
                          int32_t* isum_dbg, void* stream, void* const* events);
 
 /* ---------------------------------------------------------------------------------
- * MXFP4 reference arm (Sec. 2.3: the released expert bytes, fp4-e2m1 codes with one
- * e8m0 scale per 32 elements, Sec. 2.1, served by an integer kernel through the doubled
+ * MXFP4 reference arm (Sec. 2.3: the released expert bytes, e2m1 (fp4) codes whose
+ * groups of 32 share an e8m0 scale, Sec. 2.1, served by an integer kernel through the doubled
  * e2m1 values {0,1,2,3,4,6,8,12}, the e8m0 scale absorbing the /2).
  *   codes  [n][kb][128] bytes, 128-byte aligned: 16-byte block j of a row covers
  *          elements 32j .. 32j+31; its byte i holds element 32j+i in the low nibble and
@@ -342,9 +342,9 @@ tq_status tq_moe_status(const void* ws, const tq_experts* ex, int64_t t, int32_t
 
 /* ---------------------------------------------------------------------------------
  * Host-tier expert streaming (Sec. 2.2: the folded planes are the stored file itself,
- * so an expert-projection miss is one contiguous read, and resident and streamed
- * serving use the same bytes and kernels, so outputs are bitwise independent of where
- * an expert was cached; the
+ * so fetching a missing expert projection costs a single contiguous read, and serving
+ * from HBM or from the host tier runs the same kernels on the same bytes: an expert
+ * gives the same output bits wherever it was cached; the
  * paper's store keeps pinned RAM and LRU slots in front of the file). Tiers here: every
  * expert in pinned host memory, a pool of expert slots in HBM.
  * An expert record is one contiguous range: gate, up, down codes, then gate, up, down

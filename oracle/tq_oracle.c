@@ -263,8 +263,8 @@ int orc_gemv2(const int8_t* t1, const int8_t* t2, const uint16_t* a, int64_t n, 
 }
 
 /* ------------------------------------------------------------------------------ */
-/* MXFP4 reference arm (Sec. 2.3; Sec. 2.1 for the format: fp4-e2m1 codes with one    */
-/* e8m0 scale per 32 elements). e2m1 is 1 sign bit, 2 exponent bits (bias 1) and 1    */
+/* MXFP4 reference arm (Sec. 2.3; Sec. 2.1 for the format: e2m1 (fp4) codes, groups  */
+/* of 32 sharing an e8m0 scale). e2m1 is 1 sign bit, 2 exponent bits (bias 1) and 1    */
 /* mantissa bit; exponent 0 is subnormal. e8m0 is a biased power of two, 2^(E - 127), */
 /* with E = 255 reserved for NaN. The integer arm dots the doubled magnitudes (the     */
 /* e2m1 values times 2 are integers) against the int8 activations per 32-element      */

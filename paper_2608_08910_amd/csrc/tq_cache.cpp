@@ -1,7 +1,7 @@
 // Host-tier expert streaming (Sec. 2.2: the folded planes are the stored file itself, so
-// an expert-projection miss is one contiguous read, and resident and streamed serving
-// use the same bytes and kernels, so outputs do not depend on where an expert was
-// cached; the paper's serving stack keeps pinned RAM and LRU slots in front of the file).
+// fetching a missing expert projection costs a single contiguous read, and serving from
+// HBM or from the host tier runs the same kernels on the same bytes: outputs do not
+// depend on where an expert was cached; the paper's serving stack keeps pinned RAM and LRU slots in front of the file).
 //
 // On MI355X the tiers are pinned host memory (every expert) and a pool of expert slots
 // in HBM. Each expert is one contiguous record, so a miss is one host-to-device copy; a

@@ -1,6 +1,6 @@
 // The free-scale two-plane serving pass (Sec. 2.1: W ~ alpha1*T1 + alpha2*T2 with two
-// free scales per group; Sec. 4.1: the pair does not fold, so it is served as two
-// separate trit planes at 4.125 bits per weight, one integer pass per plane).
+// free scales per group; Sec. 4.1: the pair does not fold, so it is served as its two
+// trit planes stored apart (4.125 bits/weight), one integer pass per plane).
 //
 // Same memory plan as the folded pass: a 256-weight block is 128 bytes of trits (two
 // planes x 2 bits), 8 lanes per block, a wave's 16-byte load covers 8 consecutive blocks

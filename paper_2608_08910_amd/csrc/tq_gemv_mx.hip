@@ -1,5 +1,5 @@
-// The MXFP4 reference arm's integer pass (Sec. 2.3): fp4-e2m1 codes with one e8m0 scale
-// per 32 elements (the released expert bytes), dotted against the int8 block-quantized
+// The MXFP4 reference arm's integer pass (Sec. 2.3): e2m1 (fp4) codes whose groups of 32
+// share an e8m0 scale (the released expert bytes), dotted against the int8 block-quantized
 // activations through the doubled-e2m1 integers {0, 1, 2, 3, 4, 6, 8, 12} (signed), the
 // e8m0 scale absorbing the /2: weight = 2^(E - 128) * doubled(code).
 //

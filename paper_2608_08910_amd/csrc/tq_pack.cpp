@@ -66,8 +66,8 @@ extern "C" tq_status tq_unpack_host(const uint8_t* codes, int32_t n, int32_t k, 
   return TQ_OK;
 }
 
-// Free-scale two-plane layout (Sec. 2.1 alpha1*T1 + alpha2*T2; Sec. 4.1 two separate trit
-// planes at 4.125 bits per weight): block byte 16j + 8p + 4u + b, bit pair 2s, holds
+// Free-scale two-plane layout (Sec. 2.1 alpha1*T1 + alpha2*T2; Sec. 4.1: the two trit planes
+// stored apart, 4.125 bits/weight): block byte 16j + 8p + 4u + b, bit pair 2s, holds
 // plane p+1's trit of column 32j + 16u + 4s + b as 2-bit two's complement.
 static inline int64_t plane_byte(int j, int p, int u, int b) { return 16 * j + 8 * p + 4 * u + b; }
 
