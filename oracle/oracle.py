@@ -10,16 +10,16 @@ Definitions followed (paper sections):
   f16 scale, dequant ....... Sec. 2.1 (W_hat = s*c, scales serialized to f16)
   activation quantizer ..... Sec. 2.2 (block-quantized activations; block, scale and
                              rounding rule are this oracle's stated reading)
-  integer dot + combine .... Sec. 2.2 (one integer dot pass, one float multiply-add
-                             per block), evaluated exactly / in fp64
+  integer dot + combine .... Sec. 2.2 (one integer dot pass, a single fp32
+                             multiply-add for each block), evaluated exactly / in fp64
   MXFP4 arm ................ Sec. 2.3 (doubled-e2m1 integer dot, e8m0 scale per 32
                              absorbing the /2) with Sec. 2.1's description of the format
   free-scale solver ........ Sec. 2.1 (PTQTP's alternation with two free scales, started
                              from the tied fit; start, stop rule and precision are this
                              oracle's stated reading)
   free-scale two planes .... Sec. 2.1 (alpha1*T1 + alpha2*T2, free scales) and Sec. 4.1
-                             (the unfolded pair is served as two trit planes at 4.125
-                             bits per weight, one integer pass per plane)
+                             (the unfolded pair is served as its two planes, stored
+                             apart: 4.125 bits/weight, one integer pass per plane)
   tied solver .............. Sec. 2.1 (alternating code and scale updates against one
                              scale per group; start, stop rule and precision are this
                              oracle's stated reading)

@@ -332,8 +332,8 @@ def gemv_matches_exact_rational_brute_force(o):
 
 
 # --------------------------------------------------------------------------------------
-# Free-scale two-plane pass (Sec. 2.1 alpha1*T1 + alpha2*T2; Sec. 4.1: two trit planes at
-# 4.125 bits per weight, one integer pass per plane)
+# Free-scale two-plane pass (Sec. 2.1 alpha1*T1 + alpha2*T2; Sec. 4.1: the planes stored
+# apart, 4.125 bits/weight, one integer pass per plane)
 # --------------------------------------------------------------------------------------
 
 def _planes(rng, n, k):
