@@ -26,8 +26,8 @@
  *   Bytes: 128 + 2 per 256 weights = 4.0625 bits/weight, the paper's figure.
  * Quantized activations of t tokens over k inputs:
  *   q [t][k] int8 (-127..127), d [t][kb] fp32 block scale, bsum [t][kb] int32 = sum of the
- *   block's q. The codes and d are this library's reading of "block-quantized
- *   activations" (Sec. 2.2 fixes no rule): blocks of 256, amax = max|x| over the block,
+ *   block's q. The codes and d are this library's reading of the block-wise activation
+ *   quantization of Sec. 2.2 (which fixes no rule): blocks of 256, amax = max|x| over the block,
  *   d = amax/127 and q = rne(x * (127/amax)) in IEEE fp32 (correctly rounded division,
  *   round half to even); a block with amax < 2^-100 (an all-zero block in particular) has
  *   d = 0 and q = 0.
@@ -102,6 +102,17 @@ typedef struct {
  * n x k matrix; 0 if k % 256 != 0 or n < 0. Sec. 2.2: 4.0625 bits/weight in total. */
 size_t tq_codes_bytes(int32_t n, int32_t k);
 size_t tq_scales_bytes(int32_t n, int32_t k);
+
+/* The same two sizes under the names of the boundary's specification. */
+size_t tq_packed_codes_bytes(int32_t n, int32_t k);
+size_t tq_packed_scales_bytes(int32_t n, int32_t k);
+
+/* Pack a folded code plane on the host (Sec. 2.2 persistent format). c: host [n][k]
+ * codes in -4..4; s_f16: host [n][k/256] binary16 bit patterns; codes_out: host,
+ * tq_codes_bytes(n, k); scales_out: host, n * (k/256) elements (a copy of s_f16).
+ * TQ_ERR_INVALID if a code is outside -4..4 (the outputs are then unspecified). */
+tq_status tq_pack_host(const int8_t* c, const uint16_t* s_f16, int32_t n, int32_t k, uint8_t* codes_out,
+                       uint16_t* scales_out);
 
 /* Fold and pack on the host (Sec. 2.1 fold, Sec. 2.2 persistent format).
  * t1, t2: host [n][k] trits in {-1,0,1}; codes_out: host, tq_codes_bytes(n, k) bytes.
@@ -289,9 +300,16 @@ tq_status tq_gemv_mx_timed(const tq_mat_mx* w, const int8_t* q, const float* d, 
  * flags: 0 (automatic path choice), or TQ_MOE_FORCE_VALU / TQ_MOE_FORCE_MFMA to pin
  * the per-expert path (VALU dot4 for few tokens per expert, int8 MFMA for many).
  * Single-token steps (t == 1, topk <= 8, topk * inter <= 16384) take a path of their
- * own unless TQ_MOE_FORCE_MFMA is given (tq_moe_path). */
+ * own unless TQ_MOE_FORCE_MFMA is given (tq_moe_path).
+ * TQ_MOE_DEBUG_STAGES (may be or-ed with either): the same kernels, each taking one
+ * extra branch on a kernel argument, also leave in the workspace, past the stage buffers,
+ * every routed slot's g and u (fp32) and the exact int32 block sums of its gate, up and
+ * down dot passes (offsets g, u, gsum, usum, dsum of tq_moe_workspace_layout); the
+ * workspace must then hold total_debug bytes. Rows of unrouted slots are not written.
+ * The outputs are bitwise those of the same call without the flag. */
 #define TQ_MOE_FORCE_VALU 1
 #define TQ_MOE_FORCE_MFMA 2
+#define TQ_MOE_DEBUG_STAGES 4
 tq_status tq_moe_grouped(const tq_experts* ex, const float* x, int64_t t,
                          const int32_t* topk_idx, const float* topk_w, int32_t topk,
                          float* out, void* ws, size_t ws_bytes, int32_t flags, void* stream);
@@ -312,10 +330,22 @@ int32_t tq_moe_path(const tq_experts* ex, int64_t t, int32_t topk, int32_t flags
  *   xq [t][hidden] int8, xd [t][hidden/256] fp32, xb [t][hidden/256] int32;
  *   h [S][inter] fp32; hq [S][inter] int8, hd [S][inter/256] fp32, hb [S][inter/256] int32;
  *   yd [S][hidden] fp32 (per-slot down output, before the routing weight);
- *   flags: int32, bit 0 set if an expert id was out of range. */
+ *   flags: int32, bit 0 set if an expert id was out of range;
+ *   total: the workspace size without the debug dump (tq_moe_workspace_bytes).
+ * Dispatch lists of the grouped paths (t > 1, or TQ_MOE_FORCE_MFMA; not written by the
+ * single-token path): n_active int32 = A, the number of distinct routed experts;
+ * active [A] int32 their ids in the order the work queues take them; act_off [A + 1]
+ * int32 offsets into slot_list [S] int32, which lists each active expert's slots (slot
+ * order within an expert unspecified).
+ * Debug dump (TQ_MOE_DEBUG_STAGES only): g, u [S][inter] fp32; gsum, usum
+ * [S][inter][hidden/256] int32; dsum [S][hidden][inter/256] int32; total_debug: the
+ * workspace size the flag needs. */
 typedef struct {
   size_t xq, xd, xb, h, hq, hd, hb, yd, flags;
   size_t total;
+  size_t n_active, active, act_off, slot_list;
+  size_t g, u, gsum, usum, dsum;
+  size_t total_debug;
 } tq_moe_layout;
 tq_status tq_moe_workspace_layout(const tq_experts* ex, int64_t t, int32_t topk,
                                   tq_moe_layout* out);

@@ -272,18 +272,22 @@ class Oracle:
         z = np.asarray(z, dtype=np.float64)
         return z / (1.0 + np.exp(-z))
 
-    def expert_slot(self, ex: dict, x_row):
+    def expert_slot(self, ex: dict, x_row, want_isum: bool = False):
         """One (token, expert) slot: quantize x, gate/up dot pass, h = SiLU(g)*u,
-        quantize h (as fp32), down dot pass. Returns a dict of every stage."""
+        quantize h (as fp32), down dot pass. Returns a dict of every stage (with the exact
+        block sums of the three dot passes, [rows][blocks] int32, if asked)."""
         qx, dx, bx = self.quantize(x_row)
-        g, ga = self.gemv(*ex["gate"], qx, dx)
-        u, ua = self.gemv(*ex["up"], qx, dx)
+        g, ga, gi = self.gemv(*ex["gate"], qx, dx, want_isum=True)
+        u, ua, ui = self.gemv(*ex["up"], qx, dx, want_isum=True)
         h = self.silu(g[0]) * u[0]
         h32 = h.astype(np.float32)
         qh, dh, bh = self.quantize(h32)
-        yd, ya = self.gemv(*ex["down"], qh, dh)
-        return dict(qx=qx[0], dx=dx[0], bx=bx[0], g=g[0], g_abs=ga[0], u=u[0], u_abs=ua[0],
-                    h=h, qh=qh[0], dh=dh[0], bh=bh[0], yd=yd[0], yd_abs=ya[0])
+        yd, ya, yi = self.gemv(*ex["down"], qh, dh, want_isum=True)
+        st = dict(qx=qx[0], dx=dx[0], bx=bx[0], g=g[0], g_abs=ga[0], u=u[0], u_abs=ua[0],
+                  h=h, qh=qh[0], dh=dh[0], bh=bh[0], yd=yd[0], yd_abs=ya[0])
+        if want_isum:
+            st.update(g_isum=gi[0], u_isum=ui[0], yd_isum=yi[0])
+        return st
 
     def moe(self, x, idx, w, get_expert, tokens=None):
         """Routed-expert layer for the listed tokens (default: all).

@@ -128,8 +128,8 @@ int orc_dequant(const int8_t* c, const uint16_t* s, int64_t n, int64_t k, double
 }
 
 /* ------------------------------------------------------------------------------ */
-/* Block activation quantization (Sec. 2.2: the codes are dotted "against block-    */
-/* quantized activations"). The paper fixes neither block size, scale rule nor      */
+/* Block activation quantization (Sec. 2.2: the codes meet activations that were    */
+/* quantized block by block). The paper fixes neither block size, scale rule nor     */
 /* rounding; the reading implemented here: blocks of 256 along k (the weight block), */
 /* symmetric absmax scale d = amax/127, codes q = clamp(rne(x * (127/amax)), +-127)  */
 /* in fp32, d kept in fp32, bsum = sum of the block's codes. A block whose amax is    */

@@ -48,6 +48,9 @@ constexpr int64_t kMfmaMinSlots = 1024;  // automatic path choice: MFMA from thi
 
 struct Layout {
   size_t ctrl, active, act_off, tt_off, tile_exp, slot_list, xq, xd, xb, h, hq, hd, hb, yd, total;
+  // debug stage dump (TQ_MOE_DEBUG_STAGES), past `total`: g and u per slot, and the exact
+  // block sums of gate, up (per slot, row, hidden block) and down (per slot, row, inter block)
+  size_t dg, du, dgs, dus, dds, total_dbg;
 };
 
 static size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -76,6 +79,12 @@ static Layout make_layout(int n_experts, int hidden, int inter, int64_t t, int t
   L.hb = take(S * (inter / 256) * 4);
   L.yd = take(S * hidden * 4);
   L.total = o;
+  L.dg = take(S * inter * 4);
+  L.du = take(S * inter * 4);
+  L.dgs = take(S * inter * (hidden / 256) * 4);
+  L.dus = take(S * inter * (hidden / 256) * 4);
+  L.dds = take(S * hidden * (inter / 256) * 4);
+  L.total_dbg = o;
   return L;
 }
 
@@ -146,6 +155,13 @@ struct MoeArgs {
   float* hd;
   int32_t* hb;
   float* yd;
+  // debug stage dump: all null unless TQ_MOE_DEBUG_STAGES (a kernel-argument test, the same
+  // for every lane and wave, so the kernels take one uniform branch around each store)
+  float* dbg_g;
+  float* dbg_u;
+  int32_t* dbg_gsum;  // [slot][inter][hidden / 256]
+  int32_t* dbg_usum;  // [slot][inter][hidden / 256]
+  int32_t* dbg_dsum;  // [slot][hidden][inter / 256]
   int tiles_gu, tiles_dn;    // row tiles of the VALU kernels
   int tiles_mgu, tiles_mdn;  // row tiles of the MFMA kernels
 };
@@ -397,6 +413,25 @@ __device__ __forceinline__ void tb_acts_compute(const MoeArgs& A, const int (&wc
 #pragma unroll
         for (int m = 0; m < NMAT; ++m) p[(r * NT + tt) * NMAT + m] = dot32x16(wc[m * RPW + r][i], T.q[tt][i]);
     RR::block_sums(p);
+    // debug stage dump: the exact block sums of the kept items, one lane per item
+    if ((NMAT == 2 ? A.dbg_gsum : A.dbg_dsum) != nullptr && RR::block_writer(lane) && 8 * i + g < kb) {
+#pragma unroll
+      for (int k = 0; k < KI; ++k) {
+        const int it = RR::kept(k, lane), r = it / NT, tt = it % NT;
+        int sv = T.slot[0];
+#pragma unroll
+        for (int u = 1; u < NT; ++u) sv = tt == u ? T.slot[u] : sv;
+        if (row0 + r < N && c0 + tt < cnt) {
+          const int64_t o = ((int64_t)sv * N + row0 + r) * kb + 8 * i + g;
+          if constexpr (NMAT == 2) {
+            A.dbg_gsum[o] = p[k * 2] >> 4;
+            A.dbg_usum[o] = p[k * 2 + 1] >> 4;
+          } else {
+            A.dbg_dsum[o] = p[k] >> 4;
+          }
+        }
+      }
+    }
 #pragma unroll
     for (int k = 0; k < KI; ++k)
 #pragma unroll
@@ -410,8 +445,16 @@ __device__ __forceinline__ void tb_acts_compute(const MoeArgs& A, const int (&wc
 #pragma unroll
     for (int u = 1; u < NT; ++u) sv = tt == u ? T.slot[u] : sv;
     if (row0 + r < N && c0 + tt < cnt) {
-      if constexpr (NMAT == 2) A.h[(int64_t)sv * A.inter + row0 + r] = silu_f32(acc[0]) * acc[1];
-      else A.yd[(int64_t)sv * A.hidden + row0 + r] = acc[0];
+      if constexpr (NMAT == 2) {
+        const int64_t o = (int64_t)sv * A.inter + row0 + r;
+        A.h[o] = silu_f32(acc[0]) * acc[1];
+        if (A.dbg_g != nullptr) {
+          A.dbg_g[o] = acc[0];
+          A.dbg_u[o] = acc[1];
+        }
+      } else {
+        A.yd[(int64_t)sv * A.hidden + row0 + r] = acc[0];
+      }
     }
   }
 }
@@ -784,6 +827,25 @@ __global__ __launch_bounds__(kMWaves * 64) void k_moe_mfma(MoeArgs A) {
 #pragma unroll
               for (int m = 0; m < NMAT; ++m)
                 C[q][m] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[q][c][h], bop[m][c][h], C[q][m], 0, 0, 0);
+        // debug stage dump: C = 16 * isum of token row mt * 16 + 4g + v, weight row orow
+        if ((NMAT == 2 ? A.dbg_gsum : A.dbg_dsum) != nullptr) {
+          const int orow = rtile * kMN + wv * 16 + li;
+#pragma unroll
+          for (int q = 0; q < 2; ++q)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              const int t = (2 * mp + q) * 16 + 4 * g + v;
+              if (t < nvalid && orow < N) {
+                const int64_t o = ((int64_t)s_slot[t] * N + orow) * kb + b;
+                if constexpr (NMAT == 2) {
+                  A.dbg_gsum[o] = C[q][0][v] >> 4;
+                  A.dbg_usum[o] = C[q][1][v] >> 4;
+                } else {
+                  A.dbg_dsum[o] = C[q][0][v] >> 4;
+                }
+              }
+            }
+        }
 #pragma unroll
         for (int q = 0; q < 2; ++q)
 #pragma unroll
@@ -826,8 +888,15 @@ __global__ __launch_bounds__(kMWaves * 64) void k_moe_mfma(MoeArgs A) {
           const int t = mt * 16 + 4 * g + v;
           if (t < nvalid) {
             const int64_t slot = s_slot[t];
-            if constexpr (NMAT == 2) A.h[slot * A.inter + orow] = silu_f32(acc[mt][0][v]) * acc[mt][1][v];
-            else A.yd[slot * A.hidden + orow] = acc[mt][0][v];
+            if constexpr (NMAT == 2) {
+              A.h[slot * A.inter + orow] = silu_f32(acc[mt][0][v]) * acc[mt][1][v];
+              if (A.dbg_g != nullptr) {
+                A.dbg_g[slot * A.inter + orow] = acc[mt][0][v];
+                A.dbg_u[slot * A.inter + orow] = acc[mt][1][v];
+              }
+            } else {
+              A.yd[slot * A.hidden + orow] = acc[mt][0][v];
+            }
           }
         }
     }
@@ -1011,6 +1080,7 @@ __device__ __forceinline__ void t1_gateup_wg(const float* __restrict__ x, const 
   int qa[NL][8];
   lds_acts<NL>(s.q, kb, g, cp, qa);
   using RR = RowReduce<RPW, 2>;
+  static_assert(RR::KI == 1, "a lane keeps one row after the block butterfly");
   float acc[2] = {0.0f, 0.0f};
 #pragma unroll
   for (int i = 0; i < NL; ++i) {
@@ -1020,12 +1090,27 @@ __device__ __forceinline__ void t1_gateup_wg(const float* __restrict__ x, const 
 #pragma unroll
     for (int v = 0; v < 2 * RPW; ++v) p[v] = dot_chunk16(wr[v][i], qa[i]);
     RR::block_sums(p);
+    // debug stage dump: the lane's kept row (one lane per row) stores the exact block sums
+    if (A.dbg_gsum != nullptr && RR::block_writer(lane) && b < kb) {
+      const int r = RR::kept(0, lane);
+      if (row0 + r < I) {
+        const int64_t o = ((int64_t)j * I + row0 + r) * kb + b;
+        A.dbg_gsum[o] = p[0] >> 4;
+        A.dbg_usum[o] = p[1] >> 4;
+      }
+    }
 #pragma unroll
     for (int m = 0; m < 2; ++m) acc[m] = fmaf(f16_bits_to_f32(sr[m][i]) * dv, (float)(p[m] >> 4), acc[m]);
   }
   RR::block_totals(acc);
   const int r = RR::item(lane);
-  if (RR::writer(lane) && row0 + r < I) A.h[(int64_t)j * I + row0 + r] = silu_f32(acc[0]) * acc[1];
+  if (RR::writer(lane) && row0 + r < I) {
+    A.h[(int64_t)j * I + row0 + r] = silu_f32(acc[0]) * acc[1];
+    if (A.dbg_g != nullptr) {
+      A.dbg_g[(int64_t)j * I + row0 + r] = acc[0];
+      A.dbg_u[(int64_t)j * I + row0 + r] = acc[1];
+    }
+  }
 }
 
 // Down of one single-token workgroup `wg`: WAVES waves, each owning RPW rows of down for
@@ -1123,6 +1208,15 @@ __device__ __forceinline__ void t1_down_wg(const MoeArgs& A, float* __restrict__
       for (int r = 0; r < RPW; ++r) p[j * RPW + r] = dot_chunk16(wr[j][r][i], qa);
     }
     RR::block_sums(p);
+    // debug stage dump: each kept (slot, row) item's exact block sum, one lane per item
+    if (A.dbg_dsum != nullptr && RR::block_writer(lane) && b < kb) {
+#pragma unroll
+      for (int k = 0; k < KI; ++k) {
+        const int it = RR::kept(k, lane), r = it % RPW;
+        if (jk[k] < TOPK && ((vmask >> jk[k]) & 1) && row0 + r < H)
+          A.dbg_dsum[((int64_t)jk[k] * H + row0 + r) * kb + b] = p[k] >> 4;
+      }
+    }
 #pragma unroll
     for (int k = 0; k < KI; ++k) {
       // padded items and unrouted slots: d = 0 (their LDS codes are never written)
@@ -1348,8 +1442,10 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   if (t < 0 || t > (1 << 20)) return fail(TQ_ERR_INVALID, "%s: t = %lld outside [0, 2^20]", fn, (long long)t);
   if (topk < 1 || topk > kMaxTopk || topk > ex->n_experts)
     return fail(TQ_ERR_INVALID, "%s: topk = %d outside [1, min(%d, n_experts)]", fn, topk, kMaxTopk);
-  if (flags & ~(TQ_MOE_FORCE_VALU | TQ_MOE_FORCE_MFMA) || flags == (TQ_MOE_FORCE_VALU | TQ_MOE_FORCE_MFMA))
+  if (flags & ~(TQ_MOE_FORCE_VALU | TQ_MOE_FORCE_MFMA | TQ_MOE_DEBUG_STAGES) ||
+      (flags & (TQ_MOE_FORCE_VALU | TQ_MOE_FORCE_MFMA)) == (TQ_MOE_FORCE_VALU | TQ_MOE_FORCE_MFMA))
     return fail(TQ_ERR_INVALID, "%s: bad flags 0x%x", fn, flags);
+  const bool debug = (flags & TQ_MOE_DEBUG_STAGES) != 0;
   if (t == 0) {
     for (int i = 0; i < kNumStages; ++i)
       if ((st = empty_stage(events, i, (hipStream_t)stream, fn)) != TQ_OK) return st;
@@ -1359,8 +1455,10 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   if (!aligned(x, 16) || !aligned(out, 16) || !aligned(ws, 256) || !aligned(topk_idx, 4) || !aligned(topk_w, 4))
     return fail(TQ_ERR_ALIGN, "%s: x and out must be 16-byte aligned, ws 256-byte aligned", fn);
   const Layout L = make_layout(ex->n_experts, ex->hidden, ex->inter, t, topk);
-  if (ws_bytes < L.total)
-    return fail(TQ_ERR_WORKSPACE, "%s: workspace %zu bytes < required %zu", fn, ws_bytes, L.total);
+  const size_t need = debug ? L.total_dbg : L.total;
+  if (ws_bytes < need)
+    return fail(TQ_ERR_WORKSPACE, "%s: workspace %zu bytes < required %zu%s", fn, ws_bytes, need,
+                debug ? " (with the debug stage dump)" : "");
 
   uint8_t* base = static_cast<uint8_t*>(ws);
   MoeArgs A{};
@@ -1395,6 +1493,13 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   A.hd = reinterpret_cast<float*>(base + L.hd);
   A.hb = reinterpret_cast<int32_t*>(base + L.hb);
   A.yd = reinterpret_cast<float*>(base + L.yd);
+  if (debug) {
+    A.dbg_g = reinterpret_cast<float*>(base + L.dg);
+    A.dbg_u = reinterpret_cast<float*>(base + L.du);
+    A.dbg_gsum = reinterpret_cast<int32_t*>(base + L.dgs);
+    A.dbg_usum = reinterpret_cast<int32_t*>(base + L.dus);
+    A.dbg_dsum = reinterpret_cast<int32_t*>(base + L.dds);
+  }
 
   const int nl_gu = (ex->hidden / 256 + 7) / 8, nl_dn = (ex->inter / 256 + 7) / 8;
   const int tr_gu = kTbWaves * tb_rpw(2, nl_gu), tr_dn = kTbWaves * tb_rpw(1, nl_dn);
@@ -1479,6 +1584,16 @@ extern "C" tq_status tq_moe_workspace_layout(const tq_experts* ex, int64_t t, in
   out->yd = L.yd;
   out->flags = L.ctrl + 4 * kFlags;
   out->total = L.total;
+  out->n_active = L.ctrl + 4 * kNActive;
+  out->active = L.active;
+  out->act_off = L.act_off;
+  out->slot_list = L.slot_list;
+  out->g = L.dg;
+  out->u = L.du;
+  out->gsum = L.dgs;
+  out->usum = L.dus;
+  out->dsum = L.dds;
+  out->total_debug = L.total_dbg;
   return TQ_OK;
 }
 

@@ -14,6 +14,39 @@ extern "C" size_t tq_scales_bytes(int32_t n, int32_t k) {
   return (size_t)n * (size_t)(k / 256) * 2;
 }
 
+// The names the boundary's specification gives these sizes (same values).
+extern "C" size_t tq_packed_codes_bytes(int32_t n, int32_t k) { return tq_codes_bytes(n, k); }
+extern "C" size_t tq_packed_scales_bytes(int32_t n, int32_t k) { return tq_scales_bytes(n, k); }
+
+// Pack an already-folded code plane: c [n][k] in -4..4 and f16 scales [n][k/256] (host)
+// into the persistent planes (host): the nibbles as in tq_fold_pack_host, the scales
+// copied as they are.
+extern "C" tq_status tq_pack_host(const int8_t* c, const uint16_t* s_f16, int32_t n, int32_t k, uint8_t* codes_out,
+                                  uint16_t* scales_out) {
+  using namespace tq;
+  clear_error();
+  if (n < 0 || k <= 0 || k % 256 != 0)
+    return fail(TQ_ERR_INVALID, "tq_pack_host: bad shape n=%d k=%d (k must be a multiple of 256)", n, k);
+  if (n == 0) return TQ_OK;
+  if (!c || !s_f16 || !codes_out || !scales_out) return fail(TQ_ERR_INVALID, "tq_pack_host: null pointer");
+  const int64_t kb = k / 256;
+  for (int64_t r = 0; r < n; ++r)
+    for (int64_t b = 0; b < kb; ++b) {
+      const int64_t col0 = r * k + b * 256;
+      uint8_t* blk = codes_out + (r * kb + b) * 128;
+      for (int j = 0; j < 8; ++j)
+        for (int i = 0; i < 16; ++i) {
+          const int64_t lo = col0 + 32 * j + i, hi = lo + 16;
+          const int clo = c[lo], chi = c[hi];
+          if (clo < -4 || clo > 4 || chi < -4 || chi > 4)
+            return fail(TQ_ERR_INVALID, "tq_pack_host: code outside -4..4 near element %lld", (long long)lo);
+          blk[16 * j + i] = (uint8_t)((clo & 0xF) | ((chi & 0xF) << 4));
+        }
+    }
+  std::memcpy(scales_out, s_f16, (size_t)n * (size_t)kb * sizeof(uint16_t));
+  return TQ_OK;
+}
+
 extern "C" tq_status tq_fold_pack_host(const int8_t* t1, const int8_t* t2, int32_t n, int32_t k,
                                        uint8_t* codes_out) {
   using namespace tq;

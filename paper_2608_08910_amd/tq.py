@@ -27,6 +27,7 @@ TQ_ERR_WORKSPACE = -3
 TQ_ERR_DEVICE = -4
 TQ_MOE_FORCE_VALU = 1
 TQ_MOE_FORCE_MFMA = 2
+TQ_MOE_DEBUG_STAGES = 4
 TQ_MOE_PATH_T1, TQ_MOE_PATH_VALU, TQ_MOE_PATH_MFMA = 0, 1, 2
 
 
@@ -59,7 +60,9 @@ class tq_experts(ctypes.Structure):
 
 
 class tq_moe_layout(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_size_t) for n in ("xq", "xd", "xb", "h", "hq", "hd", "hb", "yd", "flags", "total")]
+    _fields_ = [(n, ctypes.c_size_t) for n in ("xq", "xd", "xb", "h", "hq", "hd", "hb", "yd", "flags", "total",
+                                               "n_active", "active", "act_off", "slot_list",
+                                               "g", "u", "gsum", "usum", "dsum", "total_debug")]
 
 
 if not os.path.exists(LIB_PATH):
@@ -73,6 +76,9 @@ for _name, _args, _res in [
     ("tq_scales_bytes", [_i32, _i32], _sz),
     ("tq_fold_pack_host", [_vp, _vp, _i32, _i32, _vp], _i32),
     ("tq_unpack_host", [_vp, _i32, _i32, _vp], _i32),
+    ("tq_packed_codes_bytes", [_i32, _i32], _sz),
+    ("tq_packed_scales_bytes", [_i32, _i32], _sz),
+    ("tq_pack_host", [_vp, _vp, _i32, _i32, _vp, _vp], _i32),
     ("tq_synth_weights", [ctypes.c_uint64, _i32, _i32, _vp, _vp, _vp], _i32),
     ("tq_quantize_act", [_vp, _i64, _i32, _vp, _vp, _vp, _vp], _i32),
     ("tq_tied_quantize", [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp], _i32),
@@ -161,6 +167,17 @@ def tq_fold_pack_host(t1: np.ndarray, t2: np.ndarray) -> np.ndarray:
     out = np.empty((n, k // 256, 128), dtype=np.uint8)
     _ok(_L.tq_fold_pack_host(_host(t1, np.int8, "t1"), _host(t2, np.int8, "t2", (n, k)), n, k, _host(out, np.uint8, "codes")))
     return out
+
+
+def tq_pack_host(c: np.ndarray, s_f16: np.ndarray):
+    """Host pack of a folded code plane c [n][k] (-4..4) and f16 scale bits [n][k/256]:
+    returns (codes [n][k/256][128] uint8, scales [n][k/256] uint16)."""
+    n, k = c.shape
+    codes = np.empty((n, k // 256, 128), dtype=np.uint8)
+    scales = np.empty((n, k // 256), dtype=np.uint16)
+    _ok(_L.tq_pack_host(_host(c, np.int8, "c"), _host(s_f16, np.uint16, "s_f16", (n, k // 256)), n, k,
+                        _host(codes, np.uint8, "codes"), _host(scales, np.uint16, "scales")))
+    return codes, scales
 
 
 def tq_unpack_host(codes: np.ndarray, n: int, k: int) -> np.ndarray:
@@ -510,9 +527,11 @@ def tq_moe_path(ex: TqExperts, t: int, topk: int, flags: int = 0) -> int:
     return p
 
 
-def moe_workspace(ex: TqExperts, t: int, topk: int, device="cuda") -> torch.Tensor:
-    """A device workspace of tq_moe_workspace_bytes(ex, t, topk) bytes for tq_moe_grouped."""
-    return torch.empty(tq_moe_workspace_bytes(ex, t, topk), dtype=torch.uint8, device=device)
+def moe_workspace(ex: TqExperts, t: int, topk: int, device="cuda", debug: bool = False) -> torch.Tensor:
+    """A device workspace for tq_moe_grouped: tq_moe_workspace_bytes(ex, t, topk) bytes, or
+    with debug=True the layout's total_debug bytes (room for the TQ_MOE_DEBUG_STAGES dump)."""
+    n = tq_moe_workspace_layout(ex, t, topk)["total_debug"] if debug else tq_moe_workspace_bytes(ex, t, topk)
+    return torch.empty(n, dtype=torch.uint8, device=device)
 
 
 def tq_moe_workspace_layout(ex: TqExperts, t: int, topk: int) -> dict:

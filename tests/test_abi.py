@@ -328,6 +328,13 @@ def test_moe_validation_errors_before_launch():
     assert call(d, t=-1) == tq.TQ_ERR_INVALID
     assert call(d, flags=3) == tq.TQ_ERR_INVALID
     assert call(d, flags=8) == tq.TQ_ERR_INVALID
+    assert call(d, flags=3 | tq.TQ_MOE_DEBUG_STAGES) == tq.TQ_ERR_INVALID
+    # the debug stage dump needs the layout's total_debug bytes: the plain size is refused
+    lay = tq.tq_moe_layout()
+    assert L.tq_moe_workspace_layout(ctypes.byref(d), 2, 2, ctypes.byref(lay)) == tq.TQ_OK
+    assert call(d, flags=tq.TQ_MOE_DEBUG_STAGES, ws_bytes=need) == tq.TQ_ERR_WORKSPACE
+    assert call(d, flags=tq.TQ_MOE_DEBUG_STAGES | tq.TQ_MOE_FORCE_MFMA, ws_bytes=lay.total_debug - 1) \
+        == tq.TQ_ERR_WORKSPACE
     assert call(d, x=FAKE + 4) == tq.TQ_ERR_ALIGN
     assert call(d, ws=FAKE + 128) == tq.TQ_ERR_ALIGN
     assert call(d, x=None) == tq.TQ_ERR_INVALID
@@ -354,7 +361,17 @@ def test_moe_workspace_layout_is_consistent():
         assert o1 % 256 == 0 and o1 + sizes[n1] <= o2
     assert offs[-1][0] + sizes[offs[-1][1]] <= lay.total
     assert lay.total == tq._L.tq_moe_workspace_bytes(ctypes.byref(d), 32, 8)
-    assert lay.flags < offs[0][0]
+    assert lay.flags < offs[0][0] and lay.n_active < offs[0][0]
+    # dispatch lists before the stage buffers; the debug dump after them, within total_debug
+    for n, sz in (("active", 256 * 4), ("act_off", 257 * 4), ("slot_list", S * 4)):
+        assert getattr(lay, n) % 256 == 0 and getattr(lay, n) + sz <= offs[0][0]
+    dbg = sorted((getattr(lay, n), n) for n in ("g", "u", "gsum", "usum", "dsum"))
+    dsz = {"g": S * 2048 * 4, "u": S * 2048 * 4, "gsum": S * 2048 * 16 * 4, "usum": S * 2048 * 16 * 4,
+           "dsum": S * 4096 * 8 * 4}
+    assert dbg[0][0] >= lay.total
+    for (o1, n1), (o2, _) in zip(dbg, dbg[1:]):
+        assert o1 % 256 == 0 and o1 + dsz[n1] <= o2
+    assert dbg[-1][0] + dsz[dbg[-1][1]] <= lay.total_debug
 
 
 def test_moe_path_choice():
@@ -385,3 +402,23 @@ def test_moe_path_choice():
     assert path(big, t_lim, 8) == tq.TQ_MOE_PATH_MFMA
     assert path(big, t_lim, 8, tq.TQ_MOE_FORCE_VALU) == -1
     assert path(big, t_lim - 1, 8, tq.TQ_MOE_FORCE_VALU) == tq.TQ_MOE_PATH_VALU
+
+
+def test_pack_host_matches_fold_pack(oracle):
+    """tq_pack_host (a folded code plane plus f16 scales) writes the same code bytes as
+    the fold of the trit planes that give those codes, copies the scales, and refuses a
+    code outside -4..4; the size helpers under the specification's names agree."""
+    rng = np.random.default_rng(44)
+    n, k = 5, 768
+    t1 = rng.integers(-1, 2, (n, k)).astype(np.int8)
+    t2 = rng.integers(-1, 2, (n, k)).astype(np.int8)
+    s = rng.integers(0, 0x7BFF, (n, k // 256)).astype(np.uint16)
+    codes, scales = tq.tq_pack_host(oracle.fold(t1, t2), s)
+    assert np.array_equal(codes, tq.tq_fold_pack_host(t1, t2))
+    assert np.array_equal(scales, s)
+    bad = oracle.fold(t1, t2)
+    bad[2, 300] = 5
+    with pytest.raises(tq.TqError):
+        tq.tq_pack_host(bad, s)
+    assert tq._L.tq_packed_codes_bytes(n, k) == tq.tq_codes_bytes(n, k) == n * k // 2
+    assert tq._L.tq_packed_scales_bytes(n, k) == tq.tq_scales_bytes(n, k) == n * (k // 256) * 2

@@ -1,22 +1,17 @@
 """GPU parity of the routed-expert MoE layer (tq_moe_grouped) against the CPU oracle.
 
-Staged parity, each GPU stage checked against the oracle applied to the GPU's previous
-stage (so every integer decision is compared on identical inputs):
-  xq, xd, xb  == oracle.quantize(x)                              (bit-exact)
-  h           ~= oracle SiLU(g) * u                               (bound from 1e-5 on g, u)
-  hq, hd, hb  == oracle.quantize(GPU h)                          (bit-exact)
-  yd          ~= oracle dot pass of W_down on GPU (hq, hd)       (1e-5 of abs terms)
-  out         ~= sum_j w_j * GPU yd_j in ascending j             (1e-5 of abs terms)
-End to end, the fully independent oracle output is compared for every token whose
-requantized hidden codes agree with the oracle's own; where a fp32 ulp in g or u moves
-an h value across a rounding boundary, one code differs by 1 (the rate is asserted to
-be tiny and each such token is covered by the staged check)."""
+Every parity call runs with TQ_MOE_DEBUG_STAGES, so that the exact int32 block sums of
+the gate, up and down dot passes of every checked slot are compared bit for bit with the
+oracle's; the staged and end-to-end bars are those of gpu_util.check_moe / check_slots.
+The flag's outputs are checked to be bitwise those of the same call without it, on every
+path (single token, grouped VALU, grouped MFMA)."""
 import numpy as np
 import pytest
 import torch
 
 import oracle as oracle_pkg
-from gpu_util import announce, assert_close, device, host_experts, synth_experts, ws_views
+from gpu_util import (announce, assert_close, check_moe, check_slots, device, host_experts, run_moe,
+                      synth_experts, ws_views)
 from synth import gen
 
 pytestmark = pytest.mark.gpu
@@ -36,69 +31,6 @@ def experts_h4096(tq):
     ex = synth_experts(tq, gen.SEED, 0, 256, 4096, 2048)
     torch.cuda.synchronize()
     return ex
-
-
-def run_moe(tq, ex, x, idx, w, flags=0):
-    t, topk = idx.shape
-    xd = torch.from_numpy(np.ascontiguousarray(x)).cuda()
-    idd = torch.from_numpy(np.ascontiguousarray(idx)).cuda()
-    wd = torch.from_numpy(np.ascontiguousarray(w)).cuda()
-    out = torch.empty((t, ex.hidden), dtype=torch.float32, device="cuda")
-    ws = tq.moe_workspace(ex, t, topk)
-    tq.tq_moe_grouped(ex, xd, idd, wd, out, ws, flags)
-    torch.cuda.synchronize()
-    return out, ws
-
-
-def check_moe(tq, o, ex, get_expert, x, idx, w, out, ws, tokens):
-    """Staged + end-to-end parity on the listed tokens."""
-    t, topk = idx.shape
-    V = {k: v.cpu().numpy() for k, v in ws_views(tq, ex, ws, t, topk).items()}
-    out = out.cpu().numpy()
-    oq, od, ob = o.quantize(x[tokens])
-    assert np.array_equal(V["xq"][tokens], oq)
-    assert np.array_equal(V["xd"][tokens].view(np.uint32), od.view(np.uint32))
-    assert np.array_equal(V["xb"][tokens], ob)
-    ref_out, ref_abs, stages = o.moe(x, idx, w, get_expert, tokens=tokens)
-    flips = 0
-    codes = 0
-    flipped_tokens = set()
-    by_expert = {}
-    for tk in tokens:
-        for j in range(topk):
-            by_expert.setdefault(int(idx[tk, j]), []).append((tk, j))
-    for e in sorted(by_expert):
-        down = get_expert(e)["down"]
-        for tk, j in by_expert[e]:
-            s = tk * topk + j
-            st = stages[(tk, j)]
-            g, u, ga, ua = st["g"], st["u"], st["g_abs"], st["u_abs"]
-            tol_h = 1e-5 * (1.1 * ga * np.abs(u) + np.abs(o.silu(g)) * ua) + 2e-6 * np.abs(st["h"]) + 1e-30
-            err = np.abs(V["h"][s].astype(np.float64) - st["h"])
-            assert (err <= tol_h).all(), f"h slot {s}: worst {(err / tol_h).max()}"
-            hq, hd, hb = o.quantize(V["h"][s])
-            assert np.array_equal(V["hq"][s], hq[0]) and np.array_equal(V["hd"][s].view(np.uint32), hd[0].view(np.uint32))
-            assert np.array_equal(V["hb"][s], hb[0])
-            yr, ya = o.gemv(*down, V["hq"][s], V["hd"][s])
-            assert_close(V["yd"][s], yr[0], ya[0], what=f"yd slot {s}")
-            diff = int((V["hq"][s] != st["qh"]).sum())
-            codes += V["hq"][s].size
-            if diff:
-                flipped_tokens.add(tk)
-                flips += diff
-                assert np.abs(V["hq"][s].astype(int) - st["qh"].astype(int)).max() <= 1
-    for n_t, tk in enumerate(tokens):
-        yd = V["yd"][tk * topk:(tk + 1) * topk].astype(np.float64)
-        wt = w[tk].astype(np.float64)[:, None]
-        staged = np.zeros(ex.hidden)
-        for j in range(topk):  # ascending j, as the layer defines the sum
-            staged += wt[j] * yd[j]
-        staged_abs = (np.abs(wt) * np.abs(yd)).sum(0)
-        assert_close(out[tk], staged, staged_abs + 1e-30, rtol=1e-5, what=f"out token {tk} (staged)")
-        if tk not in flipped_tokens:
-            assert_close(out[tk], ref_out[n_t], ref_abs[n_t] + 1e-30, rtol=1e-5, what=f"out token {tk}")
-    assert flips <= max(2, 1e-3 * codes), f"{flips} requantized codes differ from the oracle's"
-    return flips
 
 
 def test_moe_small_host_packed(tq, oracle):
@@ -125,10 +57,8 @@ def test_moe_invalid_expert_ids_flagged_and_skipped(tq, oracle):
     announce("moe invalid ids")
     out, ws = run_moe(tq, ex, x, idx, w)
     assert tq.tq_moe_status(ws, ex, T, topk) & 1
-    # valid slots only: the same as routing token 1 to expert 2 alone, token 2 to expert 3
-    ref, ref_abs, _ = oracle.moe(x, np.array([[0, 1], [2, 2], [3, 3]], np.int32),
-                                 np.array([[0.5, 0.5], [0.5, 0.0], [0.5, 0.0]], np.float32), lambda e: logical[e])
-    assert_close(out.cpu().numpy(), ref, ref_abs + 1e-30, what="out with invalid slots")
+    # the routed slots staged and end to end; the unrouted ones add nothing
+    check_moe(tq, oracle, ex, lambda e: logical[e], x, idx, w, out, ws, [0, 1, 2])
 
 
 def test_moe_zero_tokens_and_top1(tq, oracle):
@@ -145,49 +75,106 @@ def test_moe_zero_tokens_and_top1(tq, oracle):
     check_moe(tq, oracle, ex, lambda e: logical[e], x, idx, w, out, ws, [0, 1])
 
 
+def assert_debug_flag_neutral(tq, ex, x, idx, w, out, flags=0):
+    """The call without TQ_MOE_DEBUG_STAGES gives bitwise the debug call's output."""
+    plain, _ = run_moe(tq, ex, x, idx, w, flags=flags, debug=False)
+    assert torch.equal(plain, out), "output changes with TQ_MOE_DEBUG_STAGES"
+
+
 def test_moe_decode_batch1_uniform(tq, oracle, experts_h4096):
     """One MoE layer at decode, batch 1: 256 experts, hidden 4096, inter 2048, top-8
-    uniform without replacement, softmax weights over N(0,1) logits, seed 0."""
+    uniform without replacement, softmax weights over N(0,1) logits, seed 0. All 8 slots'
+    gate, up and down block sums bit-exact."""
     c = gen.CONFIGS[1]
     x = gen.activations(gen.SEED, 0, c["tokens"], c["hidden"])
     idx, w = gen.routing(gen.SEED, 0, c["tokens"], c["experts"], c["topk"], c["routing"])
+    assert tq.tq_moe_path(experts_h4096, 1, c["topk"]) == tq.TQ_MOE_PATH_T1
     announce("moe decode t=1 top-8 uniform")
     out, ws = run_moe(tq, experts_h4096, x, idx, w)
     get = oracle_pkg.expert_getter(gen.SEED, 0, c["hidden"], c["inter"], oracle)
     check_moe(tq, oracle, experts_h4096, get, x, idx, w, out, ws, [0])
     out2, _ = run_moe(tq, experts_h4096, x, idx, w)
     assert torch.equal(out, out2)  # bitwise reproducible
+    assert_debug_flag_neutral(tq, experts_h4096, x, idx, w, out)
 
 
 def test_moe_decode_batch32_zipf(tq, oracle, experts_h4096):
-    """Batched decode: 32 tokens, top-8 with Zipf(1.1) expert popularity, seed 0."""
+    """Batched decode: 32 tokens, top-8 with Zipf(1.1) expert popularity, seed 0. Every
+    slot's block sums bit-exact."""
     c = gen.CONFIGS[2]
     x = gen.activations(gen.SEED, 0, c["tokens"], c["hidden"])
     idx, w = gen.routing(gen.SEED, 0, c["tokens"], c["experts"], c["topk"], c["routing"])
+    assert tq.tq_moe_path(experts_h4096, c["tokens"], c["topk"]) == tq.TQ_MOE_PATH_VALU
     announce("moe decode t=32 top-8 zipf")
     out, ws = run_moe(tq, experts_h4096, x, idx, w)
     get = oracle_pkg.expert_getter(gen.SEED, 0, c["hidden"], c["inter"], oracle)
     check_moe(tq, oracle, experts_h4096, get, x, idx, w, out, ws, list(range(c["tokens"])))
+    assert_debug_flag_neutral(tq, experts_h4096, x, idx, w, out)
 
 
-def test_moe_prefill_2048_sampled(tq, oracle, experts_h4096):
+def test_moe_prefill_2048(tq, oracle, experts_h4096):
     """Prefill: 2048 tokens, Zipf top-8, activations scaled per token by a log-uniform
-    factor in [0.1, 10]. The whole layer runs on the GPU; the oracle checks a sample of
-    tokens (all their slots and stages) plus every token's quantized input."""
+    factor in [0.1, 10]; the expert contraction runs on int8 MFMA in tiles of 128 tokens.
+      - every token's quantized input, bit-exact;
+      - every token's out against sum_j w_j * yd_j of its own slots (GPU data, fp64);
+      - the dispatch lists: each expert's slot count, and the hottest expert first;
+      - staged parity, block sums bit-exact, for two slots of every 128-token tile of the
+        three hottest experts (a position that moves across the tile, and the tile's last
+        token), and end to end for a spread of tokens."""
     c = gen.CONFIGS[3]
-    x = gen.activations(gen.SEED, 0, c["tokens"], c["hidden"]) * gen.token_factors(gen.SEED, c["tokens"])[:, None]
-    idx, w = gen.routing(gen.SEED, 0, c["tokens"], c["experts"], c["topk"], c["routing"])
-    announce("moe prefill t=2048")
+    T, topk, H = c["tokens"], c["topk"], c["hidden"]
+    x = gen.activations(gen.SEED, 0, T, H) * gen.token_factors(gen.SEED, T)[:, None]
+    idx, w = gen.routing(gen.SEED, 0, T, c["experts"], topk, c["routing"])
+    assert tq.tq_moe_path(experts_h4096, T, topk) == tq.TQ_MOE_PATH_MFMA
+    announce("moe prefill t=2048 (debug dump)")
     out, ws = run_moe(tq, experts_h4096, x, idx, w)
-    V = ws_views(tq, experts_h4096, ws, c["tokens"], c["topk"])
-    oq, od, _ = oracle.quantize(x)
+    V = ws_views(tq, experts_h4096, ws, T, topk)
+    oq, od, ob = oracle.quantize(x)
     assert np.array_equal(V["xq"].cpu().numpy(), oq)
-    # tokens routed to the hottest expert, the coldest used one, and a spread
+    assert np.array_equal(V["xd"].cpu().numpy().view(np.uint32), od.view(np.uint32))
+    assert np.array_equal(V["xb"].cpu().numpy(), ob)
+    # every token, staged: out[t] against its slots' yd, ascending j, in fp64 on the device
+    yd = V["yd"].view(T, topk, H).double()
+    wd = torch.from_numpy(w).cuda().double()
+    staged = torch.zeros((T, H), dtype=torch.float64, device="cuda")
+    staged_abs = torch.zeros_like(staged)
+    for j in range(topk):
+        staged += wd[:, j:j + 1] * yd[:, j]
+        staged_abs += wd[:, j:j + 1].abs() * yd[:, j].abs()
+    ratio = ((out.double() - staged).abs() / (staged_abs + 1e-30)).max().item()
+    assert ratio <= 1e-5, f"out vs its slots' yd: worst {ratio:.3g} of the absolute terms"
+    del yd, staged, staged_abs
+    # dispatch lists
     counts = np.bincount(idx.ravel(), minlength=c["experts"])
-    cold = int(np.where(counts > 0)[0][np.argmin(counts[counts > 0])])
-    tokens = sorted(set([int(np.where((idx == 0).any(1))[0][0]), int(np.where((idx == cold).any(1))[0][0]), 0, 777, 2047]))
+    n_active = int(V["n_active"].item())
+    active = V["active"][:n_active].cpu().numpy()
+    off = V["act_off"][:n_active + 1].cpu().numpy()
+    slot_list = V["slot_list"].cpu().numpy()
+    assert n_active == int((counts > 0).sum()) and active[0] == int(np.argmax(counts))
+    assert np.array_equal(np.diff(off), counts[active])
+    for a in range(n_active):
+        sl = slot_list[off[a]:off[a + 1]]
+        assert np.array_equal(np.sort(sl), np.where(idx.ravel() == active[a])[0])
+    # two slots of every 128-token tile of the three hottest experts
+    slots = []
+    for a in range(3):
+        cnt = off[a + 1] - off[a]
+        for k0 in range(0, cnt, 128):
+            n_in = min(128, cnt - k0)
+            for p in sorted({k0 + (37 * (k0 // 128) + 5) % n_in, k0 + n_in - 1}):
+                slots.append(int(slot_list[off[a] + p]))
     get = oracle_pkg.expert_getter(gen.SEED, 0, c["hidden"], c["inter"], oracle)
+    announce(f"moe prefill: staged parity of {len(slots)} slots")
+    _, flips, codes = check_slots(tq, oracle, experts_h4096, get, x, idx, ws, slots, V)
+    assert sum(flips.values()) <= max(2, 1e-3 * codes)
+    # end to end on a spread of tokens (the hottest expert's first, the coldest used one's)
+    cold = int(np.where(counts > 0)[0][np.argmin(counts[counts > 0])])
+    tokens = sorted(set([int(np.where((idx == 0).any(1))[0][0]), int(np.where((idx == cold).any(1))[0][0]), 0, 777,
+                         2047]))
     check_moe(tq, oracle, experts_h4096, get, x, idx, w, out, ws, tokens)
+    del V
+    torch.cuda.empty_cache()
+    assert_debug_flag_neutral(tq, experts_h4096, x, idx, w, out)
 
 
 @pytest.mark.parametrize("E,H,I,T,topk", [(5, 512, 768, 150, 3), (4, 1280, 256, 70, 2)])
@@ -204,6 +191,7 @@ def test_moe_mfma_forced_small(tq, oracle, E, H, I, T, topk):
     check_moe(tq, oracle, ex, lambda e: logical[e], x, idx, w, out, ws, [0, 1, 63, 64, 65, T - 1])
     out2, _ = run_moe(tq, ex, x, idx, w, flags=tq.TQ_MOE_FORCE_MFMA)
     assert torch.equal(out, out2)
+    assert_debug_flag_neutral(tq, ex, x, idx, w, out, flags=tq.TQ_MOE_FORCE_MFMA)
 
 
 def test_moe_mfma_forced_batch32(tq, oracle, experts_h4096):
@@ -215,6 +203,7 @@ def test_moe_mfma_forced_batch32(tq, oracle, experts_h4096):
     out, ws = run_moe(tq, experts_h4096, x, idx, w, flags=tq.TQ_MOE_FORCE_MFMA)
     get = oracle_pkg.expert_getter(gen.SEED, 0, c["hidden"], c["inter"], oracle)
     check_moe(tq, oracle, experts_h4096, get, x, idx, w, out, ws, list(range(c["tokens"])))
+    assert_debug_flag_neutral(tq, experts_h4096, x, idx, w, out, flags=tq.TQ_MOE_FORCE_MFMA)
 
 
 @pytest.mark.parametrize("E,H,I,topk", [(4, 512, 768, 3), (3, 7168, 2048, 2), (9, 2304, 1280, 8), (2, 256, 256, 1),
@@ -248,6 +237,7 @@ def test_moe_grouped_valu_long_lists(tq, oracle, E, H, I, T, topk):
     announce(f"moe valu E={E} H={H} I={I} T={T}")
     out, ws = run_moe(tq, ex, x, idx, w, flags=tq.TQ_MOE_FORCE_VALU)
     check_moe(tq, oracle, ex, lambda e: logical[e], x, idx, w, out, ws, list(range(T)))
+    assert_debug_flag_neutral(tq, ex, x, idx, w, out, flags=tq.TQ_MOE_FORCE_VALU)
 
 
 def test_moe_workspace_shared_across_paths(tq, experts_h4096):
@@ -297,7 +287,7 @@ def test_t1_repeated_calls_share_one_workspace(tq, oracle):
 
 def test_t1_unrouted_slots(tq, oracle):
     """Out-of-range expert ids on the single-token path: flagged, and they contribute
-    nothing."""
+    nothing (the routed slots staged, block sums bit-exact, and end to end at 1e-5)."""
     E, H, I, topk = 5, 768, 512, 4
     ex, logical = host_experts(tq, oracle, E, H, I, seed=81)
     rng = np.random.default_rng(82)
@@ -307,9 +297,8 @@ def test_t1_unrouted_slots(tq, oracle):
     announce("moe t=1 unrouted slots")
     out, ws = run_moe(tq, ex, x, idx, w)
     assert tq.tq_moe_status(ws, ex, 1, topk) & 1
-    ref, ref_abs, _ = oracle.moe(x, np.array([[3, 0]], np.int32), np.array([[0.4, 0.2]], np.float32),
-                                 lambda e: logical[e])
-    assert_close(out.cpu().numpy()[0], ref[0], ref_abs[0] + 1e-30, rtol=1e-3, what="out with unrouted slots")
+    check_moe(tq, oracle, ex, lambda e: logical[e], x, idx, w, out, ws, [0])
+    assert_debug_flag_neutral(tq, ex, x, idx, w, out)
 
 
 def test_t1_graph_replays_match_eager(tq, oracle):

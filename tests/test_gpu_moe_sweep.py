@@ -2,13 +2,12 @@
 (automatic choice, forced grouped VALU, forced MFMA): expert counts, hidden and
 intermediate widths with 1 to 12 blocks per row (ragged last loads), 1 to 130 tokens,
 top-1 to top-8, uniform and skewed routing with duplicated ids in a token's list.
-Same bar as test_gpu_moe.py (staged parity bit-exact where integer, 1e-5 of the
-absolute terms where fp32)."""
+Same bar as test_gpu_moe.py (staged parity bit-exact where integer, the gate, up and
+down block sums included, 1e-5 of the absolute terms where fp32)."""
 import numpy as np
 import pytest
 
-from gpu_util import announce, host_experts
-from test_gpu_moe import check_moe, run_moe
+from gpu_util import announce, check_moe, host_experts, run_moe
 
 pytestmark = pytest.mark.gpu
 

@@ -6,15 +6,17 @@ step with Zipf(1.1) top-8 routing and independent N(0,1) inputs per layer.
 One step runs all 43 layers on the GPU, each on its own experts, input and routing.
 The oracle regenerates the routed experts of the first and the last layer from the
 counter-based generator and checks sampled tokens there (every stage, staged and end
-to end); every layer's quantized input is checked bit-exactly for all tokens."""
+to end; those two layers run with the debug stage dump, so their gate, up and down
+block sums are compared bit for bit); every layer's quantized input is checked
+bit-exactly for all tokens, and every layer's output, for all tokens, against the
+routing-weighted sum of its own slots' down outputs."""
 import numpy as np
 import pytest
 import torch
 
 import oracle as oracle_pkg
-from gpu_util import announce, synth_experts, ws_views
+from gpu_util import announce, check_moe, synth_experts, ws_views
 from synth import gen
-from test_gpu_moe import check_moe
 
 pytestmark = pytest.mark.gpu
 
@@ -43,14 +45,15 @@ def test_stack_43_layers_h7168_full_size(tq, oracle):
         x = gen.activations(gen.SEED, l, T, H)
         idx, w = gen.routing(gen.SEED, l, T, E, topk, c["routing"])
         xs.append(x); idxs.append(idx); wts.append(w)
-        ws_.append(tq.moe_workspace(layers[l], T, topk))
+        ws_.append(tq.moe_workspace(layers[l], T, topk, debug=l in (0, L - 1)))
         outs.append(torch.empty((T, H), dtype=torch.float32, device="cuda"))
     xd = [torch.from_numpy(x).cuda() for x in xs]
     idd = [torch.from_numpy(i).cuda() for i in idxs]
     wd = [torch.from_numpy(w).cuda() for w in wts]
     announce("stack step: 43 layers")
     for l in range(L):
-        tq.tq_moe_grouped(layers[l], xd[l], idd[l], wd[l], outs[l], ws_[l])
+        tq.tq_moe_grouped(layers[l], xd[l], idd[l], wd[l], outs[l], ws_[l],
+                          tq.TQ_MOE_DEBUG_STAGES if l in (0, L - 1) else 0)
     torch.cuda.synchronize()
     for l in range(L):
         V = ws_views(tq, layers[l], ws_[l], T, topk)
@@ -59,6 +62,12 @@ def test_stack_43_layers_h7168_full_size(tq, oracle):
         assert np.array_equal(V["xd"].cpu().numpy().view(np.uint32), od.view(np.uint32))
         assert tq.tq_moe_status(ws_[l], layers[l], T, topk) == 0
         assert torch.isfinite(outs[l]).all()
+        yd = V["yd"].view(T, topk, H).double()
+        w64 = wd[l].double()
+        staged = (w64[:, :, None] * yd).sum(1)
+        staged_abs = (w64[:, :, None].abs() * yd.abs()).sum(1)
+        ratio = ((outs[l].double() - staged).abs() / (staged_abs + 1e-30)).max().item()
+        assert ratio <= 1e-5, f"layer {l}: out vs its slots' yd, worst {ratio:.3g} of the absolute terms"
     for l, tokens in ((0, [0, 5]), (L - 1, [3, 7])):
         announce(f"stack oracle layer {l} tokens {tokens}")
         get = oracle_pkg.expert_getter(gen.SEED, l, H, I, oracle)

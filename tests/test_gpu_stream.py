@@ -1,12 +1,17 @@
 """Host-tier expert streaming on the GPU: a step served from an LRU pool of expert slots
 in HBM, filled from pinned host memory, must give bitwise the same output as the same
 step served from resident experts (the same bytes and kernels, only the addresses
-differ), for the single-token, grouped VALU and MFMA paths."""
+differ), for the single-token, grouped VALU and MFMA paths. The first and the last
+streamed step of each case are also checked against the oracle (staged, with the gate,
+up and down block sums bit-exact, and end to end), the slot ids mapped back to expert
+ids; and two streamed steps queued without a synchronization between them (each with
+its own pinned slot-id buffer) give the resident outputs."""
 import numpy as np
 import pytest
 import torch
 
-from gpu_util import announce, device, synth_experts
+import oracle as oracle_pkg
+from gpu_util import announce, check_moe, device, synth_experts
 from synth import gen
 
 pytestmark = pytest.mark.gpu
@@ -51,7 +56,7 @@ def run_resident(tq, ex, x, idx, w, flags):
     (32, 4096, 2048, 10, 1, 8, 0, 6),     # decode batch 1 at the model's shape
     (48, 4096, 2048, 32, 4, 8, 0, 4),     # grouped decode at the model's shape
 ])
-def test_streamed_equals_resident_bitwise(tq, E, H, I, S, T, topk, flags, steps):
+def test_streamed_equals_resident_bitwise(tq, oracle, E, H, I, S, T, topk, flags, steps):
     announce(f"stream E={E} H={H} I={I} S={S} T={T} topk={topk} flags={flags}")
     ex = synth_experts(tq, 7, 0, E, H, I)
     resident = records_from_stack(tq, ex)
@@ -59,15 +64,18 @@ def test_streamed_equals_resident_bitwise(tq, E, H, I, S, T, topk, flags, steps)
     store.data.copy_(resident.data)
     pool = tq.TqExpertRecords.empty(S, H, I)
     cache = tq.TqCache(E, S)
-    ws_pool = tq.moe_workspace(pool, T, topk)
+    ws_pool = tq.moe_workspace(pool, T, topk, debug=True)
+    get = oracle_pkg.expert_getter(7, 0, H, I, oracle)
     rng = np.random.default_rng(E * 100 + T)
     total_misses = 0
+    served = []
     for step in range(steps):
         ids = np.stack([rng.choice(E, size=topk, replace=False) for _ in range(T)]).astype(np.int32)
         if len(np.unique(ids)) > S:
             continue
         w = rng.random((T, topk)).astype(np.float32)
-        x = torch.from_numpy(rng.standard_normal((T, H)).astype(np.float32)).cuda()
+        xh = rng.standard_normal((T, H)).astype(np.float32)
+        x = torch.from_numpy(xh).cuda()
         idx_dev = torch.from_numpy(ids).cuda()
         w_dev = torch.from_numpy(w).cuda()
         slots_host = torch.empty((T, topk), dtype=torch.int32).pin_memory()
@@ -76,7 +84,7 @@ def test_streamed_equals_resident_bitwise(tq, E, H, I, S, T, topk, flags, steps)
         slots_dev = torch.empty((T, topk), dtype=torch.int32, device="cuda")
         cache.fetch(store, pool, misses, slots_host, slots_dev)
         out_s = torch.empty((T, H), dtype=torch.float32, device="cuda")
-        tq.tq_moe_grouped(pool, x, slots_dev, w_dev, out_s, ws_pool, flags)
+        tq.tq_moe_grouped(pool, x, slots_dev, w_dev, out_s, ws_pool, flags | tq.TQ_MOE_DEBUG_STAGES)
         torch.cuda.synchronize()
         out_r = run_resident(tq, resident, x, idx_dev, w_dev, flags)
         out_k = run_resident(tq, ex, x, idx_dev, w_dev, flags)
@@ -84,4 +92,48 @@ def test_streamed_equals_resident_bitwise(tq, E, H, I, S, T, topk, flags, steps)
         assert torch.equal(out_r, out_k), f"step {step}: records != stacked layout"
         for e, s in zip(ids.ravel().tolist(), slots.ravel().tolist()):
             assert torch.equal(pool.data[s], resident.data[e])
+        served.append(step)
+        if len(served) == 1 or step == steps - 1:
+            # the streamed step against the oracle: its stage buffers are per slot position,
+            # so the expert ids themselves name what each slot ran
+            announce(f"stream step {step}: oracle")
+            check_moe(tq, oracle, pool, get, xh, ids, w, out_s, ws_pool, list(range(T)), n_ids=E)
     assert total_misses > 0
+
+
+@pytest.mark.parametrize("E,H,I,S,T,topk,flags", [(12, 512, 768, 5, 3, 2, 0), (16, 1024, 512, 6, 1, 4, 0),
+                                                 (12, 512, 512, 8, 4, 2, 2)])
+def test_two_streamed_steps_queued_without_sync(tq, E, H, I, S, T, topk, flags):
+    """Two steps planned, fetched and run back to back on one stream with no host
+    synchronization between them, each with its own pinned slot-id buffer: both outputs
+    equal the resident ones (the second step's copies, queued behind the first step's
+    kernels, may overwrite slots the first step reads only after it has read them)."""
+    announce(f"stream queued E={E} H={H} I={I} S={S} T={T} topk={topk} flags={flags}")
+    ex = synth_experts(tq, 9, 0, E, H, I)
+    resident = records_from_stack(tq, ex)
+    store = tq.TqExpertRecords.empty(E, H, I, device="cpu", pin_memory=True)
+    store.data.copy_(resident.data)
+    pool = tq.TqExpertRecords.empty(S, H, I)
+    cache = tq.TqCache(E, S)
+    rng = np.random.default_rng(E * 10 + S)
+    for rnd in range(3):
+        steps = []
+        for k in range(2):
+            while True:
+                ids = np.stack([rng.choice(E, size=topk, replace=False) for _ in range(T)]).astype(np.int32)
+                if len(np.unique(ids)) <= S:
+                    break
+            x = torch.from_numpy(rng.standard_normal((T, H)).astype(np.float32)).cuda()
+            w = torch.from_numpy(rng.random((T, topk)).astype(np.float32)).cuda()
+            slots_host = torch.empty((T, topk), dtype=torch.int32).pin_memory()
+            _, misses = cache.map(ids, slots_host.numpy())
+            slots_dev = torch.empty((T, topk), dtype=torch.int32, device="cuda")
+            out = torch.empty((T, H), dtype=torch.float32, device="cuda")
+            ws = tq.moe_workspace(pool, T, topk)
+            cache.fetch(store, pool, misses, slots_host, slots_dev)
+            tq.tq_moe_grouped(pool, x, slots_dev, w, out, ws, flags)
+            steps.append((ids, x, w, out, slots_host))
+        torch.cuda.synchronize()
+        for k, (ids, x, w, out, _) in enumerate(steps):
+            ref = run_resident(tq, resident, x, torch.from_numpy(ids).cuda(), w, flags)
+            assert torch.equal(out, ref), f"round {rnd} step {k}: queued streamed step != resident"
