@@ -315,6 +315,23 @@ tq_status tq_moe_grouped(const tq_experts* ex, const float* x, int64_t t,
                          float* out, void* ws, size_t ws_bytes, int32_t flags, void* stream);
 size_t tq_moe_workspace_bytes(const tq_experts* ex, int64_t t, int32_t topk);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation): tq_moe_grouped with its workspace
+ * taken from a fixed device array of tq_moe_noalloc_max_bytes() bytes (16 MiB) that the
+ * library holds on every GPU it runs on until the process ends, one array per device,
+ * that of the calling thread's current device (the stream must belong to it). The call
+ * itself allocates and frees nothing. Arguments and results as tq_moe_grouped; the
+ * caller still owns x, topk_idx, topk_w and out. TQ_ERR_WORKSPACE, before any launch, if
+ * the call's workspace (tq_moe_workspace_bytes, or the layout's total_debug with
+ * TQ_MOE_DEBUG_STAGES) exceeds the array: about 600 slots (t * topk) at hidden 4096 and
+ * inter 2048. Every call on a GPU shares that GPU's array, and the array keeps the last
+ * call's stage buffers (readable at the offsets of tq_moe_workspace_layout only by the
+ * library): calls that may overlap on one GPU (other streams, other threads) race and
+ * must be ordered by the caller. No part of the array needs clearing between calls. */
+size_t tq_moe_noalloc_max_bytes(void);
+tq_status tq_moe_grouped_noalloc(const tq_experts* ex, const float* x, int64_t t, const int32_t* topk_idx,
+                                 const float* topk_w, int32_t topk, float* out, int32_t flags, void* stream);
+
 /* The path tq_moe_grouped takes for these arguments: TQ_MOE_PATH_T1 (single token: a
  * gate/up kernel, then a down kernel with the requantization and the weighted combine
  * fused), TQ_MOE_PATH_VALU (dispatch + grouped VALU dot4 kernels), TQ_MOE_PATH_MFMA

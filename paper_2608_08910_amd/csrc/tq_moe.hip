@@ -21,7 +21,7 @@
 #include <hip/hip_ext.h>
 
 #include <algorithm>
-
+#include <mutex>
 #include <type_traits>
 
 #include "tq_device.hpp"
@@ -1601,6 +1601,67 @@ extern "C" tq_status tq_moe_grouped(const tq_experts* ex, const float* x, int64_
                                     const float* topk_w, int32_t topk, float* out, void* ws, size_t ws_bytes,
                                     int32_t flags, void* stream) {
   return tq::moe_run(ex, x, t, topk_idx, topk_w, topk, out, ws, ws_bytes, flags, stream, nullptr, "tq_moe_grouped");
+}
+
+// ---------------------------------------------------------------------------------
+// A variant of tq_moe_grouped that allocates nothing: its workspace is a fixed device
+// array, one per GPU, that lives until the process ends. Host code never passes the
+// array's name to a kernel (on the host it only stands for the symbol): the device
+// address comes from hipGetSymbolAddress, once per device, with that device current.
+// ---------------------------------------------------------------------------------
+namespace tq {
+
+constexpr size_t kNoAllocScratchBytes = size_t(16) << 20;
+constexpr int kMaxDevices = 64;
+
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxDevices];
+
+// The calling thread's current device's copy of `scratch` (looked up on the first call on
+// that device).
+static tq_status scratch_ptr(void** out, const char* fn) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(TQ_ERR_DEVICE, "%s: hipGetDevice failed: %s", fn, hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(TQ_ERR_DEVICE, "%s: device %d beyond %d", fn, dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(TQ_ERR_DEVICE, "%s: hipGetSymbolAddress(scratch) failed on device %d: %s", fn, dev,
+                  hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return TQ_OK;
+}
+
+}  // namespace tq
+
+extern "C" size_t tq_moe_noalloc_max_bytes(void) { return tq::kNoAllocScratchBytes; }
+
+extern "C" tq_status tq_moe_grouped_noalloc(const tq_experts* ex, const float* x, int64_t t, const int32_t* topk_idx,
+                                            const float* topk_w, int32_t topk, float* out, int32_t flags,
+                                            void* stream) {
+  using namespace tq;
+  const char* fn = "tq_moe_grouped_noalloc";
+  clear_error();
+  tq_status st = validate_experts(ex, fn);
+  if (st != TQ_OK) return st;
+  if (t < 0 || topk < 1) return fail(TQ_ERR_INVALID, "%s: bad t = %lld or topk = %d", fn, (long long)t, topk);
+  const Layout L = make_layout(ex->n_experts, ex->hidden, ex->inter, t, topk);
+  const size_t need = (flags & TQ_MOE_DEBUG_STAGES) ? L.total_dbg : L.total;
+  if (need > kNoAllocScratchBytes)
+    return fail(TQ_ERR_WORKSPACE,
+                "%s: this call needs %zu bytes of scratch, more than the fixed %zu (fewer tokens per call, or "
+                "tq_moe_grouped with a caller workspace)",
+                fn, need, kNoAllocScratchBytes);
+  void* ws = nullptr;
+  if ((st = scratch_ptr(&ws, fn)) != TQ_OK) return st;
+  return moe_run(ex, x, t, topk_idx, topk_w, topk, out, ws, kNoAllocScratchBytes, flags, stream, nullptr, fn);
 }
 
 extern "C" int32_t tq_moe_path(const tq_experts* ex, int64_t t, int32_t topk, int32_t flags) {

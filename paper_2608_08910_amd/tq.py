@@ -104,6 +104,8 @@ for _name, _args, _res in [
     ("tq_moe_workspace_layout", [_P(tq_experts), _i64, _i32, _P(tq_moe_layout)], _i32),
     ("tq_moe_grouped", [_P(tq_experts), _vp, _i64, _vp, _vp, _i32, _vp, _vp, _sz, _i32, _vp], _i32),
     ("tq_moe_grouped_timed", [_P(tq_experts), _vp, _i64, _vp, _vp, _i32, _vp, _vp, _sz, _i32, _vp, _P(_vp)], _i32),
+    ("tq_moe_noalloc_max_bytes", [], _sz),
+    ("tq_moe_grouped_noalloc", [_P(tq_experts), _vp, _i64, _vp, _vp, _i32, _vp, _i32, _vp], _i32),
     ("tq_moe_stage_count", [], _i32),
     ("tq_moe_stage_name", [_i32], ctypes.c_char_p),
     ("tq_moe_status", [_vp, _P(tq_experts), _i64, _i32, _P(_i32), _vp], _i32),
@@ -552,6 +554,22 @@ def _moe_args(ex, x, topk_idx, topk_w, out, ws):
 
 def tq_moe_grouped(ex: TqExperts, x, topk_idx, topk_w, out, ws, flags: int = 0, stream=None):
     _ok(_L.tq_moe_grouped(*_moe_args(ex, x, topk_idx, topk_w, out, ws), flags, _stream(stream)))
+
+
+def tq_moe_noalloc_max_bytes() -> int:
+    return int(_L.tq_moe_noalloc_max_bytes())
+
+
+def tq_moe_grouped_noalloc(ex: TqExperts, x, topk_idx, topk_w, out, flags: int = 0, stream=None):
+    """tq_moe_grouped on the library's fixed per-device scratch array (no workspace)."""
+    t, h = x.shape
+    topk = topk_idx.shape[1]
+    if h != ex.hidden:
+        raise ValueError(f"x: hidden {h} != experts' hidden {ex.hidden}")
+    _ok(_L.tq_moe_grouped_noalloc(ctypes.byref(ex.desc()), _dev(x, torch.float32, "x"), t,
+                                  _dev(topk_idx, torch.int32, "topk_idx", (t, topk)),
+                                  _dev(topk_w, torch.float32, "topk_w", (t, topk)), topk,
+                                  _dev(out, torch.float32, "out", (t, h)), flags, _stream(stream)))
 
 
 def tq_moe_stage_count() -> int:
