@@ -90,8 +90,22 @@ def matrix_bytes(n: int, k: int) -> int:
     return n * k // 2 + n * (k // 256) * 2
 
 
-def cpu_baseline(seed: int, hidden: int, inter: int, topk: int, target_s: float = 12.0) -> dict:
-    """Oracle (plain single-threaded C + numpy glue) on a bounded sample of the same layer."""
+def host_info() -> dict:
+    """The host the CPU legs ran on: logical CPUs, the ones this process may use, the model."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "usable_cpus": len(os.sched_getaffinity(0)), "cpu_model": model}
+
+
+def cpu_baseline(seed: int, hidden: int, inter: int, topk: int, target_s: float = 8.0) -> dict:
+    """The oracle (plain C, its dot pass row-parallel under OpenMP, + numpy glue) on a
+    bounded sample of the same layer, on all usable host cores and on one."""
     import oracle as oracle_pkg
     from synth import gen
 
@@ -105,23 +119,35 @@ def cpu_baseline(seed: int, hidden: int, inter: int, topk: int, target_s: float 
         }
     idx = np.arange(topk, dtype=np.int32)[None, :]
     w = np.full((1, topk), 1.0 / topk, np.float32)
-    x0 = gen.activations(seed, 0, 1, hidden)
-    t0 = time.perf_counter()
-    o.moe(x0, idx, w, experts.__getitem__)
-    one = time.perf_counter() - t0
-    n_tok = int(max(1, min(200, target_s / max(one, 1e-3))))
-    xs = gen.activations(seed, 1, n_tok, hidden)
-    t0 = time.perf_counter()
-    for i in range(n_tok):
-        o.moe(xs[i:i + 1], idx, w, experts.__getitem__)
-    el = time.perf_counter() - t0
     per_tok = topk * (2 * matrix_bytes(inter, hidden) + matrix_bytes(hidden, inter)) + 2 * hidden * 4
+    info = host_info()
+
+    def leg(threads: int, salt: int):
+        used = o.set_threads(threads)
+        x0 = gen.activations(seed, salt, 1, hidden)
+        t0 = time.perf_counter()
+        o.moe(x0, idx, w, experts.__getitem__)
+        one = time.perf_counter() - t0
+        n_tok = int(max(1, min(400, target_s / max(one, 1e-3))))
+        xs = gen.activations(seed, salt + 1, n_tok, hidden)
+        t0 = time.perf_counter()
+        for i in range(n_tok):
+            o.moe(xs[i:i + 1], idx, w, experts.__getitem__)
+        el = time.perf_counter() - t0
+        return used, n_tok, el
+
+    used_all, n_all, el_all = leg(info["usable_cpus"], 1)
+    _, n_one, el_one = leg(1, 3)
+    o.set_threads(info["usable_cpus"])
     return {
-        "value": round(per_tok * n_tok / el / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-        "tokens_per_s": round(n_tok / el, 3),
-        "sample": f"{n_tok} tokens of the batch-1 decode layer, each routed to the same {topk} pre-generated "
-                  f"experts (hidden {hidden}, inter {inter}); oracle compute only, weight generation excluded; "
-                  f"{el:.1f} s on 1 host thread",
+        "value": round(per_tok * n_all / el_all / 1e9, 4), "unit": "GB/s", "cores": used_all, "kind": "oracle",
+        "tokens_per_s": round(n_all / el_all, 3),
+        "one_core": {"value": round(per_tok * n_one / el_one / 1e9, 4), "unit": "GB/s", "cores": 1,
+                     "tokens_per_s": round(n_one / el_one, 3)},
+        **info,
+        "sample": f"{n_all} tokens ({el_all:.1f} s on {used_all} OpenMP threads) and {n_one} tokens ({el_one:.1f} s "
+                  f"on 1 thread) of the batch-1 decode layer, each routed to the same {topk} pre-generated experts "
+                  f"(hidden {hidden}, inter {inter}); oracle compute only, weight generation excluded",
     }
 
 
@@ -139,9 +165,14 @@ WORKLOADS = {
 }
 
 
-def time_graph(step, W: int, K: int) -> float:
+REPLAYS = 20  # repeats of the timed graph for the median and min-max band
+
+
+def time_graph(step, W: int, K: int):
     """Capture W warmup and K timed steps in two HIP graphs; replay the warmup graph,
-    then time the K-step graph between device synchronizations (seconds)."""
+    then time the K-step graph between device synchronizations (seconds). Then replay
+    the K-step graph REPLAYS more times, each bracketed by HIP events on its stream, for
+    the band (seconds per replay)."""
     import torch
     for i in range(min(W, 4)):  # eager sanity pass (also loads the code objects)
         step(i)
@@ -162,14 +193,56 @@ def time_graph(step, W: int, K: int) -> float:
     t0 = time.perf_counter()
     g_time.replay()
     torch.cuda.synchronize()
-    return time.perf_counter() - t0
+    elapsed = time.perf_counter() - t0
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(REPLAYS)]
+    with torch.cuda.stream(s):
+        for a, b in evs:
+            a.record(s)
+            g_time.replay()
+            b.record(s)
+    torch.cuda.synchronize()
+    return elapsed, [a.elapsed_time(b) * 1e-3 for a, b in evs]
 
 
 def hbm_roof(kernel, nbytes, ms, symbol):
+    """The dominant kernel against the HBM roof. `frac` uses `mean_ms`: the mean of the
+    kernel's own start/stop timestamps (HIP events of hipExtLaunchKernelGGL) over the eager
+    launches of the per-kernel pass. Beside it, the committed rocprofv3 record of the same
+    kernel (its AverageNs), while the kernel's sources are unchanged since it was taken."""
     achieved = nbytes / (ms * 1e-3) / 1e9
-    return {"kernel": kernel, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": recorded_traffic(symbol),
-            "bytes_per_launch": round(nbytes), "mean_ms": round(ms, 5), "kernel_symbol": symbol}
+    r = {"kernel": kernel, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+         "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": recorded_traffic(symbol),
+         "bytes_per_launch": round(nbytes), "mean_ms": round(ms, 5), "kernel_symbol": symbol,
+         "frac_timing": "hip events: the kernel's own start/stop timestamps, mean over the per-kernel pass"}
+    avg_ns = _recorded(symbol, "average_ns", kind="kernel_stats")
+    if avg_ns is not None:
+        r["rocprof_mean_ms"] = round(avg_ns * 1e-6, 5)
+        r["frac_rocprof"] = round(nbytes / (avg_ns * 1e-9) / 1e9 / HBM_PEAK_GBS, 4)
+    return r
+
+
+def stream_ceiling(nbytes: float, launches: int) -> dict:
+    """A plain streaming read of nbytes in one launch (tq_stream_read_timed), from a
+    device buffer at rotating offsets (each read's bytes last touched at least 1 GiB of
+    reads earlier, beyond the 256 MB last-level cache); the launches queued back to back
+    behind a spin kernel, each timed by its own start/stop timestamps. Median over the
+    launches."""
+    import torch
+    from paper_2608_08910_amd import tq
+    nb = int(nbytes + 255) // 256 * 256
+    span = max(1 << 30, 3 * nb) // 256 * 256
+    buf = torch.empty(span + nb, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(launches)]
+    torch.cuda.synchronize()
+    torch.cuda._sleep(int(2.4e9 * 0.02))
+    for i in range(launches):
+        off = (i * nb) % span
+        tq.tq_stream_read_timed(buf[off:], nb, sink, ev[i])
+    torch.cuda.synchronize()
+    ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
+    del buf
+    return {"bytes": nb, "ms": round(ms, 5), "GBps": round(nb / (ms * 1e-3) / 1e9, 1)}
 
 
 def run_gemv(args, wl, cfg):
@@ -193,27 +266,31 @@ def run_gemv(args, wl, cfg):
     y = torch.empty((1, n), dtype=torch.float32, device="cuda")
 
     def step(i):
-        tq.tq_quantize_act(x_all[i:i + 1], q, d, b)
-        tq.tq_gemv(mats[i % copies], q, d, b, y)
+        # fp32 activations in, quantized inside the dot-pass launch
+        tq.tq_gemv_f32(mats[i % copies], x_all[i:i + 1], y, q, d, b)
 
-    elapsed = time_graph(step, W, K)
+    elapsed, reps = time_graph(step, W, K)
     per_step = matrix_bytes(n, k) + k * 4 + n * 4
     gbs = per_step * K / elapsed / 1e9
-    # per-kernel pass: each gemv launched with its own start/stop events (the kernel's
+    # per-kernel pass: each launch with its own start/stop events (the kernel's
     # timestamps), eager launches queued behind a spin kernel
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(P)]
     torch.cuda.synchronize()
     torch.cuda._sleep(int(2.4e9 * 0.02))
     for j in range(P):
-        tq.tq_quantize_act(x_all[j:j + 1], q, d, b)
-        tq.tq_gemv_timed(mats[j % copies], q, d, b, y, ev[j])
+        tq.tq_gemv_f32_timed(mats[j % copies], x_all[j:j + 1], y, q, d, b, ev[j])
     torch.cuda.synchronize()
     ms = float(np.mean([a.elapsed_time(c) for a, c in ev]))
-    roof = hbm_roof("gemv", matrix_bytes(n, k) + k + (k // 256) * 4 + n * 4, ms, "k_gemv<2, 1, 1, false>")
-    return dict(value=gbs, K=K, W=W, elapsed=elapsed, tokens=K, roof=roof,
+    # the kernel reads the codes, scales and x (fp32) and writes y (and q, d, bsum once)
+    roof = hbm_roof("gemv", per_step, ms, "k_gemv_x<2, 1, 4, false>")
+    ceil = stream_ceiling(per_step, 64)
+    step_ms = elapsed * 1e3 / K
+    return dict(value=gbs, K=K, W=W, elapsed=elapsed, reps=reps, tokens=K, roof=roof,
                 config={"workload": cfg["name"], "n": n, "k": k, "tokens_per_step": 1, "bits_per_weight": 4.0625,
-                        "rotating_copies": copies, "path": "valu"},
-                extra={})
+                        "rotating_copies": copies, "path": "valu, quantization fused (tq_gemv_f32)"},
+                extra={"stream_ceiling": {"step_bytes": ceil["bytes"], "stream_read_GBps": ceil["GBps"],
+                                          "stream_read_ms": ceil["ms"],
+                                          "step_frac_of_stream_read": round(ceil["ms"] / step_ms, 4)}})
 
 
 def cpu_baseline_quant(cfg, target_s: float = 10.0) -> dict:
@@ -269,7 +346,7 @@ def run_quant(args, wl, cfg):
     def step(i):
         run(i)
 
-    elapsed = time_graph(step, W, K)
+    elapsed, reps = time_graph(step, W, K)
     # bytes: fp32 weights in, the format out (and the tied fit in, for the free solver)
     per_step = n * k * 4 + (matrix_bytes(n, k) + n * k // 2 + n * (k // 256) * 4 if free else matrix_bytes(n, k))
     gbs = per_step * K / elapsed / 1e9
@@ -309,7 +386,7 @@ def run_quant(args, wl, cfg):
                 "unit": "G VALU wave64 instructions/s", "frac": round(achieved / VALU_PEAK_GINST, 4),
                 "traffic": recorded_traffic(sym), "valu_insts_per_launch": valu, "bytes_per_launch": per_step,
                 "hbm_GBps": round(per_step / (ms * 1e-3) / 1e9, 1), "mean_ms": round(ms, 5), "kernel_symbol": sym}
-    return dict(value=gbs, K=K, W=W, elapsed=elapsed, tokens=K, roof=roof,
+    return dict(value=gbs, K=K, W=W, elapsed=elapsed, reps=reps, tokens=K, roof=roof,
                 config={"workload": cfg["name"].replace("tied", "free") if free else cfg["name"], "matrices": M,
                         "n": n, "k": k, "max_iter": 16,
                         "weights": "N(0,1) x per-row spread log-uniform [0.005, 0.05], fp32"},
@@ -385,8 +462,8 @@ def run_twoplane(args, wl, cfg):
         tq.tq_quantize_act(x_all[i:i + 1], q[:1], d[:1], b[:1])
         tq.tq_gemv(matsf[i % copies], q[:1], d[:1], b[:1], y[:1])
 
-    elapsed = time_graph(step2, W, K)
-    elapsed_f = time_graph(stepf, W, K)
+    elapsed, reps = time_graph(step2, W, K)
+    elapsed_f, _ = time_graph(stepf, W, K)
     io = k * 4 + n * 4
     gbs = (two_plane_bytes(n, k) + io) * K / elapsed / 1e9
     gbs_f = (matrix_bytes(n, k) + io) * K / elapsed_f / 1e9
@@ -415,7 +492,7 @@ def run_twoplane(args, wl, cfg):
                              "folded_GBps": round((matrix_bytes(n, k) + t * (k + kb * 4 + n * 4)) / (mf * 1e-3) / 1e9, 1)}
     ms = by_tokens["1"]["two_plane_ms"]
     roof = hbm_roof("gemv2", two_plane_bytes(n, k) + k + kb * 4 + n * 4, ms, "k_gemv2<2, 1, 4, false>")
-    return dict(value=gbs, K=K, W=W, elapsed=elapsed, tokens=K, roof=roof,
+    return dict(value=gbs, K=K, W=W, elapsed=elapsed, reps=reps, tokens=K, roof=roof,
                 config={"workload": cfg["name"], "n": n, "k": k, "tokens_per_step": 1, "bits_per_weight": 4.125,
                         "rotating_copies": copies, "format": "free-scale two-plane (2 x 2-bit trit planes, 2 f16 scales "
                                                              "per 256 weights)"},
@@ -490,8 +567,8 @@ def run_mxfp4(args, wl, cfg):
         tq.tq_quantize_act(x_all[i:i + 1], q[:1], d[:1], b[:1])
         tq.tq_gemv(matsf[i % copies], q[:1], d[:1], b[:1], y[:1])
 
-    elapsed = time_graph(step, W, K)
-    elapsed_f = time_graph(stepf, W, K)
+    elapsed, reps = time_graph(step, W, K)
+    elapsed_f, _ = time_graph(stepf, W, K)
     io = k * 4 + n * 4
     gbs = (mx_bytes(n, k) + io) * K / elapsed / 1e9
     gbs_f = (matrix_bytes(n, k) + io) * K / elapsed_f / 1e9
@@ -520,7 +597,7 @@ def run_mxfp4(args, wl, cfg):
                              "folded_GBps": round((matrix_bytes(n, k) + t * (k + kb * 4 + n * 4)) / (mf * 1e-3) / 1e9, 1)}
     ms = by_tokens["1"]["mxfp4_ms"]
     roof = hbm_roof("gemv_mx", mx_bytes(n, k) + k + kb * 4 + n * 4, ms, "k_gemv_mx<2, 1, 2, false>")
-    return dict(value=gbs, K=K, W=W, elapsed=elapsed, tokens=K, roof=roof,
+    return dict(value=gbs, K=K, W=W, elapsed=elapsed, reps=reps, tokens=K, roof=roof,
                 config={"workload": cfg["name"], "n": n, "k": k, "tokens_per_step": 1, "bits_per_weight": 4.25,
                         "rotating_copies": copies, "format": "MXFP4 (e2m1 codes, e8m0 scale per 32), doubled-e2m1 "
                                                              "integer dot"},
@@ -597,7 +674,7 @@ def run_stream(args, wl, cfg):
             "unit": "GB/s", "frac": round(link / PCIE5_X16_GBS, 4), "traffic": None,
             "bytes_per_step": round(copied / K), "note": "expert records copied per step over the host link "
                                                         "(pinned host -> HBM); peak = PCIe 5.0 x16 one direction"}
-    return dict(value=alg_bytes / elapsed / 1e9, K=K, W=W, elapsed=elapsed, tokens=K * T, roof=roof,
+    return dict(value=alg_bytes / elapsed / 1e9, K=K, W=W, elapsed=elapsed, reps=None, tokens=K * T, roof=roof,
                 config={"workload": cfg["name"] + f"_streamed_{S}slots", "experts": E, "hidden": H, "inter": I,
                         "tokens_per_step": T, "topk": topk, "routing": "uniform top-8, no expert reused within 3 steps",
                         "bits_per_weight": 4.0625, "host_store_bytes": E * rb, "hbm_slots": S,
@@ -630,8 +707,9 @@ def run_moe(args, wl, cfg):
     torch.cuda.synchronize()
 
     if T == 1:
-        # every step avoids the experts of the previous 3 steps (last-level-cache reuse)
-        sched = [gen.bench_routing_schedule(seed, total, T, E, topk, cfg["routing"])]
+        # every step avoids the experts of the previous 3 steps (last-level-cache reuse),
+        # and the last timed steps those of the first ones (the timed graph is replayed)
+        sched = [gen.bench_routing_schedule(seed, total, T, E, topk, cfg["routing"], wrap_from=W)]
     else:
         # many tokens per step: a step's expert union is 0.9-3.3 GB per layer, far beyond the cache
         sched = [[gen.routing(seed, 1000 + 97 * l + i, T, E, topk, cfg["routing"]) for i in range(total)]
@@ -651,7 +729,7 @@ def run_moe(args, wl, cfg):
         for l in range(L):
             tq.tq_moe_grouped(layers[l], x_all[l][i], idx_all[l][i], w_all[l][i], out, ws, args.flags)
 
-    elapsed = time_graph(step, W, K)
+    elapsed, reps = time_graph(step, W, K)
     bytes_expert = 2 * matrix_bytes(I, H) + matrix_bytes(H, I)
     distinct = [len(np.unique(sched[l][i][0])) for l in range(L) for i in range(W, W + K)]
     alg_bytes = sum(d * bytes_expert for d in distinct) + K * L * (T * H * 4 * 2 + T * topk * 8)
@@ -668,11 +746,14 @@ def run_moe(args, wl, cfg):
     for (i, l), ev in zip(runs, evs):
         tq.tq_moe_grouped_timed(layers[l], x_all[l][i], idx_all[l][i], w_all[l][i], out, ws, ev, args.flags)
     torch.cuda.synchronize()
-    stage_ms = {n: float(np.mean([ev[2 * si].elapsed_time(ev[2 * si + 1]) for ev in evs]))
+    path = tq.tq_moe_path(layers[0], T, topk, args.flags)
+    # the single-token path launches no prologue, requant or combine kernel (their event
+    # pairs are recorded back to back): those stages are reported as null
+    empty = {"prologue", "requant", "combine"} if path == tq.TQ_MOE_PATH_T1 else set()
+    stage_ms = {n: (None if n in empty else float(np.mean([ev[2 * si].elapsed_time(ev[2 * si + 1]) for ev in evs])))
                 for si, n in enumerate(names)}
     gu_ms = stage_ms["gate_up"]
     n_distinct = float(np.mean([len(np.unique(sched[l][i][0])) for i, l in runs]))
-    path = tq.tq_moe_path(layers[0], T, topk, args.flags)
     mfma = path == tq.TQ_MOE_PATH_MFMA
     nl_gu, nl_dn = (H // 256 + 7) // 8, (I // 256 + 7) // 8
     ragged = "true" if (H // 256) % 8 else "false"
@@ -699,16 +780,52 @@ def run_moe(args, wl, cfg):
                 "hbm_GBps": round(gu_bytes / (gu_ms * 1e-3) / 1e9, 1), "kernel_symbol": gu_kernel}
     else:
         roof = hbm_roof(kname, gu_bytes, gu_ms, gu_kernel)
+    # the down kernel beside it: the routed experts' down planes, h in (fp32 per slot on the
+    # single-token path, which requantizes it itself; int8 + scale per block otherwise),
+    # the output (or the per-slot rows) out
+    if path == tq.TQ_MOE_PATH_T1:
+        dn_bytes = n_distinct * matrix_bytes(H, I) + T * topk * I * 4 + T * H * 4
+        dn_kernel = f"k_t1_down<{nl_dn}, 2, {topk}, 8, {'true' if (I // 256) % 8 else 'false'}>"
+    else:
+        dn_bytes = n_distinct * matrix_bytes(H, I) + T * topk * (I + (I // 256) * 4) + T * topk * H * 4
+        dn_kernel = "k_moe_mfma<1>" if mfma else "k_tb<1, ...>"
+    dn_ms = stage_ms["down"]
+    down = {"kernel_symbol": dn_kernel, "bytes_per_launch": round(dn_bytes), "mean_ms": round(dn_ms, 5),
+            "GBps": round(dn_bytes / (dn_ms * 1e-3) / 1e9, 1),
+            "frac_of_hbm_peak": round(dn_bytes / (dn_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    # second ceiling: a plain streaming read of the step's bytes (per layer) and of the
+    # dominant kernel's, measured here
+    step_bytes = alg_bytes / (K * L)
+    ceil_step = stream_ceiling(step_bytes, 32 if step_bytes < 4e8 else 6)
+    ceil_gu = stream_ceiling(gu_bytes, 32 if gu_bytes < 4e8 else 6)
+    layer_ms = elapsed * 1e3 / (K * L)
+    ceiling = {"step_bytes": ceil_step["bytes"], "stream_read_GBps": ceil_step["GBps"],
+               "stream_read_ms": ceil_step["ms"], "layer_GBps": round(step_bytes / (layer_ms * 1e-3) / 1e9, 1),
+               "layer_frac_of_stream_read": round(ceil_step["ms"] / layer_ms, 4),
+               "dominant_kernel_bytes": ceil_gu["bytes"], "dominant_stream_read_GBps": ceil_gu["GBps"],
+               "dominant_kernel_frac_of_stream_read": round(ceil_gu["ms"] / gu_ms, 4)}
     routing_desc = ("uniform top-8, no expert reused within 3 steps" if T == 1 else
                     f"{cfg['routing']} top-{topk}, fresh draw per step")
     config = {"workload": cfg["name"], "layers": L, "experts": E, "hidden": H, "inter": I, "tokens_per_step": T,
               "topk": topk, "routing": routing_desc, "bits_per_weight": 4.0625,
               "resident_expert_bytes": L * E * bytes_expert,
               "path": {0: "single_token", 1: "valu", 2: "mfma"}[path]}
-    extra = {"stage_ms": {k: round(v, 5) for k, v in stage_ms.items()},
+    extra = {"stage_ms": {k: (None if v is None else round(v, 5)) for k, v in stage_ms.items()},
+             "down_kernel": down, "stream_ceiling": ceiling,
              "bytes_per_token": round(alg_bytes / (K * T)),
              "mean_distinct_experts_per_layer": round(float(np.mean(distinct)), 2)}
-    return dict(value=gbs, K=K, W=W, elapsed=elapsed, tokens=K * T, roof=roof, config=config, extra=extra)
+    if T > 1:
+        # the routing actually timed: per-expert slot counts of each timed step and layer
+        counts = [np.bincount(sched[l][i][0].ravel(), minlength=E) for l in range(L) for i in range(W, W + K)]
+        first = np.sort(counts[0])[::-1]
+        vals, nexp = np.unique(counts[0][counts[0] > 0], return_counts=True)
+        extra["routing_histogram"] = {
+            "steps_x_layers": len(counts),
+            "active_experts_mean": round(float(np.mean([(c > 0).sum() for c in counts])), 2),
+            "max_slots_per_expert_mean": round(float(np.mean([c.max() for c in counts])), 2),
+            "first_timed_step_top16_counts": first[:16].tolist(),
+            "first_timed_step_experts_by_count": {int(v): int(n) for v, n in zip(vals, nexp)}}
+    return dict(value=gbs, K=K, W=W, elapsed=elapsed, reps=reps, tokens=K * T, roof=roof, config=config, extra=extra)
 
 
 def main():
@@ -776,6 +893,14 @@ def main():
         **r["extra"],
         "roofline": r["roof"],
     }
+    if r.get("reps"):
+        per_step = np.array(r["reps"]) * 1e3 / K
+        vals = r["value"] * (elapsed / np.array(r["reps"]))
+        res["band"] = {"replays": len(per_step), "of": f"the {K}-step timed graph, each replay bracketed by HIP events",
+                       "ms_per_step": {"median": round(float(np.median(per_step)), 5),
+                                       "min": round(float(per_step.min()), 5), "max": round(float(per_step.max()), 5)},
+                       "value": {"median": round(float(np.median(vals)), 2), "min": round(float(vals.min()), 2),
+                                 "max": round(float(vals.max()), 2)}}
     if not args.no_cpu_baseline and args.workload == "decode1":
         res["cpu_baseline"] = cpu_baseline(gen.SEED, cfg["hidden"], cfg["inter"], cfg["topk"])
     if not args.no_cpu_baseline and args.workload == "tiedquant":

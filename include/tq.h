@@ -174,6 +174,22 @@ tq_status tq_gemv(const tq_mat* w, const int8_t* q, const float* d, const int32_
 tq_status tq_gemv_timed(const tq_mat* w, const int8_t* q, const float* d, const int32_t* bsum,
                         int64_t t, float* y, int32_t* isum_dbg, void* stream, void* const* events);
 
+/* The dot pass for one matrix on fp32 activations (Sec. 2.2, quantization included):
+ * x [t][k] fp32 (16-byte aligned) is quantized per 256-block by the rule above into
+ * q [t][k] (16-byte aligned), d [t][kb], bsum [t][kb] (outputs, caller-owned), and
+ * y [t][n] = the tq_gemv pass on them. One token is one launch: every workgroup
+ * quantizes x into its LDS beside its weight loads (workgroup 0 also writes q, d,
+ * bsum), and y is bitwise what tq_quantize_act followed by tq_gemv gives. Several tokens
+ * (or n * k / 2 >= 2^32 code bytes): those two launches. isum_dbg as in tq_gemv. */
+tq_status tq_gemv_f32(const tq_mat* w, const float* x, int64_t t, float* y, int8_t* q, float* d, int32_t* bsum,
+                      int32_t* isum_dbg, void* stream);
+
+/* As tq_gemv_f32, timed with two host-created HIP events: at one token they carry the
+ * kernel's own start/stop timestamps; otherwise they are recorded on the stream before
+ * the quantizer and after the dot pass. */
+tq_status tq_gemv_f32_timed(const tq_mat* w, const float* x, int64_t t, float* y, int8_t* q, float* d,
+                            int32_t* bsum, int32_t* isum_dbg, void* stream, void* const* events);
+
 /* ---------------------------------------------------------------------------------
  * Free-scale two-plane variant (Sec. 2.1: PTQTP's W ~ alpha1*T1 + alpha2*T2 with two
  * free scales per group, the family the tie constrains; Sec. 4.1, the quality table's
@@ -438,6 +454,13 @@ tq_status tq_cache_map(void* state, const int32_t* ids, int64_t n, int32_t* slot
 tq_status tq_cache_fetch(const void* state, const void* host_store, void* dev_slots, size_t record_bytes,
                          const int32_t* misses, int32_t n_miss, const int32_t* slots_host,
                          int32_t* slots_dev, int64_t n, void* stream);
+
+/* Benchmark ceiling (not part of the method): one launch that reads `bytes` (a multiple
+ * of 16) from src with nontemporal 16-byte loads, each byte once, and keeps only an XOR of
+ * them (sink: one uint32 that is practically never written), timed like tq_gemv_timed
+ * (events[0], events[1]: the kernel's own start and stop timestamps). The dot pass's
+ * throughput is reported as a fraction of this rate on the same byte count. */
+tq_status tq_stream_read_timed(const void* src, size_t bytes, uint32_t* sink, void* stream, void* const* events);
 
 /* Thread-local description of the last failed call on this thread ("" if none). */
 const char* tq_last_error(void);

@@ -11,7 +11,9 @@ LIB = os.path.join(HERE, "liboracle.so")
 
 # -ffp-contract=off: the quantizer's multiply must round on its own (no fused
 # multiply-add); no -ffast-math anywhere.
-CFLAGS = ["-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math",
+# -fopenmp: orc_gemv's row loop may run on several threads (whole rows per thread, the
+# same arithmetic per row).
+CFLAGS = ["-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
           "-Wall", "-Wextra", "-Werror"]
 
 

@@ -79,10 +79,16 @@ class Oracle:
             ("orc_synth_matrix", [ctypes.c_uint64, _i64, _i64, _i64, _i64, _vp, _vp, _vp], ctypes.c_int),
             ("orc_f32_to_f16", [ctypes.c_float], ctypes.c_uint16),
             ("orc_tied_quantize", [_vp, _i64, _i64, ctypes.c_int, _vp, _vp, _vp], ctypes.c_int),
+            ("orc_set_threads", [ctypes.c_int], ctypes.c_int),
         ]:
             f = getattr(L, name)
             f.argtypes = args
             f.restype = res
+
+    def set_threads(self, n: int = 0) -> int:
+        """Threads of the row-parallel dot pass (n <= 0: leave as is); returns the count
+        in effect."""
+        return int(self._L.orc_set_threads(n))
 
     @staticmethod
     def _check(rc: int, what: str):

@@ -11,7 +11,10 @@
  *    kernels decide them in; the paper fixes none): correctly rounded division and
  *    multiplication, round-half-to-even, no fused multiply-add (build with
  *    -ffp-contract=off);
- *  - the scale combine is evaluated in fp64.
+ *  - the scale combine is evaluated in fp64;
+ *  - built with OpenMP, orc_gemv hands whole output rows to threads (nothing else is
+ *    parallel, and no row's arithmetic depends on the thread count): the benchmark
+ *    times the oracle on one core and on all of them.
  *
  * Pins (tests/oracle_pins.py; every function below has at least one, none re-derives
  * the function's own formula, and tests/test_oracle_mutants.py checks that planted
@@ -53,6 +56,9 @@
 #include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 #define ORC_OK 0
 #define ORC_BAD_INPUT (-1)
@@ -62,6 +68,18 @@
 /* With scales tied at alpha = (3s, s), the two trit planes combine into a single    */
 /* code c = 3*t1 + t2, which takes the nine values -4..4.                            */
 /* ------------------------------------------------------------------------------ */
+
+/* Threads for the row-parallel loops (the benchmark times the oracle on one core and on
+   all of them); returns the count now in effect (1 without OpenMP). */
+int orc_set_threads(int n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+  return omp_get_max_threads();
+#else
+  (void)n;
+  return 1;
+#endif
+}
 
 int orc_fold(const int8_t* t1, const int8_t* t2, int64_t n, int8_t* c) {
   for (int64_t i = 0; i < n; ++i) {
@@ -202,12 +220,16 @@ int orc_gemv(const int8_t* c, const uint16_t* s, int64_t n, int64_t k, const int
              const float* d, int64_t t, double* y, double* absref, int32_t* isum) {
   if (k % 256 != 0) return ORC_BAD_INPUT;
   int64_t kb = k / 256;
+  int bad = 0;
+  /* OpenMP (when built with it) only hands whole output rows to threads: each row's
+     integer sums and its fp64 combine run in the same order whatever the thread count. */
+#pragma omp parallel for collapse(2) schedule(static) reduction(| : bad)
   for (int64_t tt = 0; tt < t; ++tt)
     for (int64_t r = 0; r < n; ++r) {
       double acc = 0.0, aacc = 0.0;
       for (int64_t b = 0; b < kb; ++b) {
         int64_t v = orc_dot_i8(c + r * k + b * 256, q + tt * k + b * 256, 256);
-        if (v > INT32_MAX || v < INT32_MIN) return ORC_BAD_INPUT;
+        if (v > INT32_MAX || v < INT32_MIN) bad = 1;
         if (isum) isum[(tt * n + r) * kb + b] = (int32_t)v;
         double term = orc_f16_to_f64(s[r * kb + b]) * (double)d[tt * kb + b] * (double)v;
         acc += term;
@@ -216,7 +238,7 @@ int orc_gemv(const int8_t* c, const uint16_t* s, int64_t n, int64_t k, const int
       y[tt * n + r] = acc;
       if (absref) absref[tt * n + r] = aacc;
     }
-  return ORC_OK;
+  return bad ? ORC_BAD_INPUT : ORC_OK;
 }
 
 /* ------------------------------------------------------------------------------ */

@@ -129,6 +129,121 @@ __global__ __launch_bounds__(256) void k_gemv(const uint8_t* __restrict__ codes,
   } while (LOOP && t0 < t);
 }
 
+// One token with fp32 activations, quantization fused: each workgroup quantizes x into LDS
+// (8-lane group gid owns block gid, further blocks strided over the groups; waves with no
+// block skip the load), with its weight loads issued right behind the x loads so that
+// both are in flight together; after one barrier the pass runs as k_gemv's at one token
+// (same butterflies, same per-block fp32 multiply-add, so the same bits as quantizing
+// first and running k_gemv with the same rows per wave). Workgroup 0 also stores the
+// quantized activations for the caller. Rows past n load the last row and store nothing.
+template <int NL, int RPW, int WAVES, bool RAGGED>
+__global__ __launch_bounds__(WAVES * 64) void k_gemv_x(const uint8_t* __restrict__ codes,
+                                                       const uint16_t* __restrict__ scales, int n, int kb,
+                                                       const float* __restrict__ x, int8_t* __restrict__ q_out,
+                                                       float* __restrict__ d_out, int32_t* __restrict__ b_out,
+                                                       float* __restrict__ y, int32_t* __restrict__ isum_dbg) {
+  static_assert(RPW <= 8 && (RPW & (RPW - 1)) == 0, "RPW: a power of two <= 8");
+  __shared__ __attribute__((aligned(16))) int8_t s_q[kMaxK];
+  __shared__ float s_d[kMaxK / 256];
+  __shared__ int s_b[kMaxK / 256];
+  using RR = RowReduce<RPW, 1>;
+  static_assert(RR::KI == 1, "a lane keeps one row after the block butterfly");
+  const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane >> 3, cp = lane & 7, gid = wv * 8 + g;
+  const int row0 = (blockIdx.x * WAVES + wv) * RPW;
+
+  // x first (its wait must not queue behind the weights), then every weight load
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, (uint32_t)kb * 1024u);
+  float v[32];
+  const bool xw = wv * 8 < kb;  // wave-uniform: the wave has blocks of x to quantize
+  if (xw) buf_load32f(xr, (uint32_t)min(gid, kb - 1), cp, v);
+  __builtin_amdgcn_sched_barrier(0);
+  const __amdgpu_buffer_rsrc_t cr = make_rsrc(codes, (uint32_t)n * (uint32_t)kb * 128u);
+  const __amdgpu_buffer_rsrc_t sr = make_rsrc(scales, (uint32_t)n * (uint32_t)kb * 2u);
+  uint4 w[RPW][NL];
+#pragma unroll
+  for (int r = 0; r < RPW; ++r) {
+    const uint32_t srow = (uint32_t)min(row0 + r, n - 1) * (uint32_t)kb * 128u;
+#pragma unroll
+    for (int i = 0; i < NL; ++i)
+      w[r][i] = buf_load16(cr, (uint32_t)min(8 * i + g, kb - 1) * 128u + (uint32_t)cp * 16u, srow);
+  }
+  // after the block butterfly a lane keeps the row rev(lane bits): its scales
+  const uint32_t lrow = (uint32_t)min(row0 + rev_bits<clog2(RPW)>(lane & (RPW - 1)), n - 1) * (uint32_t)kb;
+  uint16_t sh[NL];
+#pragma unroll
+  for (int i = 0; i < NL; ++i) sh[i] = buf_load_u16(sr, (lrow + (uint32_t)min(8 * i + g, kb - 1)) * 2u, 0);
+  if (xw) quantize_to_lds(v, min(gid, kb - 1), cp, s_q, s_d, s_b, gid < kb);
+  for (int blk = gid + WAVES * 8; blk < kb; blk += WAVES * 8) {
+    buf_load32f(xr, (uint32_t)blk, cp, v);
+    quantize_to_lds(v, blk, cp, s_q, s_d, s_b, true);
+  }
+  __syncthreads();
+  if (blockIdx.x == 0) {  // the quantized activations, once per call
+    for (int i = threadIdx.x; i < kb * 64; i += WAVES * 64)
+      reinterpret_cast<int*>(q_out)[i] = reinterpret_cast<const int*>(s_q)[i];
+    for (int i = threadIdx.x; i < kb; i += WAVES * 64) {
+      d_out[i] = s_d[i];
+      b_out[i] = s_b[i];
+    }
+  }
+  if (row0 >= n) return;
+  float acc[1] = {0.0f};
+#pragma unroll
+  for (int i = 0; i < NL; ++i) {
+    const int b = 8 * i + g, bc = min(b, kb - 1);
+    const int4* qp = reinterpret_cast<const int4*>(s_q + bc * 256 + cp * 32);
+    const int4 lo = qp[0], hi = qp[1];
+    const int qa[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    int p[RPW];
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) {
+      int c[8];
+      unpack16c(w[r][i], c);
+      p[r] = dot32x16(c, qa);
+    }
+    RR::block_sums(p);
+    const int is = p[0] >> 4;  // exact block sum of c * q
+    const float dv = (!RAGGED || b < kb) ? s_d[bc] : 0.0f;
+    acc[0] = fmaf(f16_bits_to_f32(sh[i]) * dv, (float)is, acc[0]);
+    if (isum_dbg != nullptr && RR::block_writer(lane) && b < kb) {
+      const int row = row0 + RR::kept(0, lane);
+      if (row < n) isum_dbg[(int64_t)row * kb + b] = is;
+    }
+  }
+  RR::block_totals(acc);
+  if (RR::writer(lane)) {
+    const int row = row0 + RR::item(lane);
+    if (row < n) y[row] = acc[0];
+  }
+}
+
+using gemv_x_fn = void (*)(const uint8_t*, const uint16_t*, int, int, const float*, int8_t*, float*, int32_t*,
+                           float*, int32_t*);
+constexpr int kGemvXWaves = 4;
+
+template <int RPW, bool R>
+static gemv_x_fn pick_gemv_x_r(int nl) {
+  switch (nl) {
+    case 1: return k_gemv_x<1, RPW, kGemvXWaves, R>;
+    case 2: return k_gemv_x<2, RPW, kGemvXWaves, R>;
+    case 3: return k_gemv_x<3, RPW, kGemvXWaves, R>;
+    case 4: return k_gemv_x<4, RPW, kGemvXWaves, R>;
+    case 5: return k_gemv_x<5, RPW, kGemvXWaves, R>;
+    case 6: return k_gemv_x<6, RPW, kGemvXWaves, R>;
+    case 7: return k_gemv_x<7, RPW, kGemvXWaves, R>;
+    default: return k_gemv_x<8, RPW, kGemvXWaves, R>;
+  }
+}
+
+// The same rows per wave as k_gemv at one token (so both give the same bits).
+static gemv_x_fn pick_gemv_x(int kb, int rpw) {
+  const int nl = (kb + 7) / 8;
+  const bool r = kb % 8 != 0;
+  if (rpw == 4) return r ? pick_gemv_x_r<4, true>(nl) : pick_gemv_x_r<4, false>(nl);
+  return r ? pick_gemv_x_r<1, true>(nl) : pick_gemv_x_r<1, false>(nl);
+}
+
 using gemv_fn = void (*)(const uint8_t*, const uint16_t*, int, int, const int8_t*, const float*, int, float*,
                          int32_t*);
 
@@ -198,6 +313,62 @@ static tq_status gemv_run(const tq_mat* w, const int8_t* q, const float* d, cons
   return check_launch("tq_gemv");
 }
 }  // namespace tq
+
+namespace tq {
+static tq_status gemv_f32_run(const tq_mat* w, const float* x, int64_t t, float* y, int8_t* q, float* d, int32_t* bsum,
+                              int32_t* isum_dbg, void* stream, void* const* events) {
+  const char* fn = events ? "tq_gemv_f32_timed" : "tq_gemv_f32";
+  if (!w) return fail(TQ_ERR_INVALID, "%s: null matrix descriptor", fn);
+  const int n = w->n, k = w->k;
+  if (n < 1) return fail(TQ_ERR_INVALID, "%s: n = %d < 1", fn, n);
+  if (k <= 0 || k % 256 != 0 || k > kMaxK)
+    return fail(TQ_ERR_INVALID, "%s: k = %d must be a positive multiple of 256 <= %d", fn, k, kMaxK);
+  if (t < 0 || t > INT32_MAX) return fail(TQ_ERR_INVALID, "%s: t = %lld out of range", fn, (long long)t);
+  if (t == 0) return TQ_OK;
+  if (!w->codes || !w->scales || !x || !y || !q || !d || !bsum) return fail(TQ_ERR_INVALID, "%s: null pointer", fn);
+  if (!aligned(w->codes, 128)) return fail(TQ_ERR_ALIGN, "%s: codes must be 128-byte aligned", fn);
+  if (!aligned(x, 16) || !aligned(q, 16) || !aligned(w->scales, 2) || !aligned(d, 4) || !aligned(bsum, 4) ||
+      !aligned(y, 4) || (isum_dbg && !aligned(isum_dbg, 4)))
+    return fail(TQ_ERR_ALIGN, "%s: x and q must be 16-byte aligned, other buffers naturally aligned", fn);
+  const int kb = k / 256;
+  if (t > 1 || (int64_t)n * kb * 128 >= ((int64_t)1 << 32)) {
+    // several tokens (or a matrix beyond 32-bit offsets): quantize, then the dot pass
+    if (events && hipEventRecord((hipEvent_t)events[0], (hipStream_t)stream) != hipSuccess)
+      return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
+    tq_status st = tq_quantize_act(x, t, k, q, d, bsum, stream);
+    if (st != TQ_OK) return st;
+    if ((st = tq_gemv(w, q, d, bsum, t, y, isum_dbg, stream)) != TQ_OK) return st;
+    if (events && hipEventRecord((hipEvent_t)events[1], (hipStream_t)stream) != hipSuccess)
+      return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
+    return TQ_OK;
+  }
+  const int nl = (kb + 7) / 8;
+  const int rpw = (n >= 16384 && nl <= 2) ? 4 : 1;
+  const unsigned wgs = (unsigned)(((int64_t)n + kGemvXWaves * rpw - 1) / (kGemvXWaves * rpw));
+  (void)hipGetLastError();
+  if (events)
+    hipExtLaunchKernelGGL(pick_gemv_x(kb, rpw), dim3(wgs), dim3(kGemvXWaves * 64), 0, (hipStream_t)stream,
+                          (hipEvent_t)events[0], (hipEvent_t)events[1], 0, w->codes, w->scales, n, kb, x, q, d, bsum, y,
+                          isum_dbg);
+  else
+    hipLaunchKernelGGL(pick_gemv_x(kb, rpw), dim3(wgs), dim3(kGemvXWaves * 64), 0, (hipStream_t)stream, w->codes,
+                       w->scales, n, kb, x, q, d, bsum, y, isum_dbg);
+  return check_launch(fn);
+}
+}  // namespace tq
+
+extern "C" tq_status tq_gemv_f32(const tq_mat* w, const float* x, int64_t t, float* y, int8_t* q, float* d,
+                                 int32_t* bsum, int32_t* isum_dbg, void* stream) {
+  tq::clear_error();
+  return tq::gemv_f32_run(w, x, t, y, q, d, bsum, isum_dbg, stream, nullptr);
+}
+
+extern "C" tq_status tq_gemv_f32_timed(const tq_mat* w, const float* x, int64_t t, float* y, int8_t* q, float* d,
+                                       int32_t* bsum, int32_t* isum_dbg, void* stream, void* const* events) {
+  tq::clear_error();
+  if (!events || !events[0] || !events[1]) return tq::fail(TQ_ERR_INVALID, "tq_gemv_f32_timed: null event");
+  return tq::gemv_f32_run(w, x, t, y, q, d, bsum, isum_dbg, stream, events);
+}
 
 extern "C" tq_status tq_gemv(const tq_mat* w, const int8_t* q, const float* d, const int32_t* bsum,
                              int64_t t, float* y, int32_t* isum_dbg, void* stream) {

@@ -915,36 +915,6 @@ __global__ __launch_bounds__(kMWaves * 64) void k_moe_mfma(MoeArgs A) {
 constexpr int kT1MaxTopk = 8;
 constexpr int kT1MaxHq = 16384;  // topk * inter bytes of requantized hidden held in LDS
 
-// Quantize 256-block `blk` of src into LDS (one block per 8-lane group): codes, the
-// block scale and code sum. `store` is group-uniform; the quantization itself runs
-// regardless, so that the loads of v are not sunk into a branch behind the weight loads.
-__device__ __forceinline__ void quantize_to_lds(const float (&v)[32], int blk, int cp, int8_t* s_q, float* s_d,
-                                                int* s_b, bool store) {
-  int qw[8], qs, bs;
-  float dd;
-  quantize_group32(v, qw, qs, dd, bs);
-  if (!store) return;
-  int4* qp = reinterpret_cast<int4*>(s_q + blk * 256 + cp * 32);
-  qp[0] = make_int4(qw[0], qw[1], qw[2], qw[3]);
-  qp[1] = make_int4(qw[4], qw[5], qw[6], qw[7]);
-  if (cp == 0) {
-    s_d[blk] = dd;
-    s_b[blk] = bs;
-  }
-}
-
-__device__ __forceinline__ void load32(const float* p, float (&v)[32]) {
-  const float4* q = reinterpret_cast<const float4*>(p);
-#pragma unroll
-  for (int m = 0; m < 8; ++m) {
-    const float4 f = q[m];
-    v[4 * m + 0] = f.x;
-    v[4 * m + 1] = f.y;
-    v[4 * m + 2] = f.z;
-    v[4 * m + 3] = f.w;
-  }
-}
-
 // A lane's slice of one token's quantized activations, from LDS: for load i, block
 // b = 8i + g, chunk cp: 32 codes (blocks past the end of a row reread the last block;
 // their scale d is taken as zero).
@@ -982,22 +952,6 @@ __device__ __forceinline__ int dot_chunk16(const uint4 w, const int (&a)[8]) {
   int c[8];
   unpack16c(w, c);
   return dot32x16(c, a);
-}
-
-// The lane's 32 fp32 values of 256-block `blk` of a row-major fp32 buffer (AUX: cache
-// policy of the loads).
-template <int AUX = 0>
-__device__ __forceinline__ void buf_load32f(__amdgpu_buffer_rsrc_t r, uint32_t blk, int cp, float (&v)[32]) {
-  const uint32_t o = (blk * 256u + (uint32_t)cp * 32u) * 4u;
-#pragma unroll
-  for (int m = 0; m < 8; ++m) {
-    const u32x4 w = __builtin_amdgcn_raw_buffer_load_b128(r, o + 16u * m, 0, AUX);
-    const uint4 u = make_uint4(w.x, w.y, w.z, w.w);
-    v[4 * m + 0] = __uint_as_float(u.x);
-    v[4 * m + 1] = __uint_as_float(u.y);
-    v[4 * m + 2] = __uint_as_float(u.z);
-    v[4 * m + 3] = __uint_as_float(u.w);
-  }
 }
 
 // Layout of the single-token kernels' LDS: the quantized activations of one token (x, or

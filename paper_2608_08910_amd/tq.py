@@ -84,6 +84,8 @@ for _name, _args, _res in [
     ("tq_tied_quantize", [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp], _i32),
     ("tq_gemv", [_P(tq_mat), _vp, _vp, _vp, _i64, _vp, _vp, _vp], _i32),
     ("tq_gemv_timed", [_P(tq_mat), _vp, _vp, _vp, _i64, _vp, _vp, _vp, _P(_vp)], _i32),
+    ("tq_gemv_f32", [_P(tq_mat), _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
+    ("tq_gemv_f32_timed", [_P(tq_mat), _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _P(_vp)], _i32),
     ("tq_pack2_host", [_vp, _vp, _i32, _i32, _vp], _i32),
     ("tq_unpack2_host", [_vp, _i32, _i32, _vp, _vp], _i32),
     ("tq_free_quantize", [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp], _i32),
@@ -104,6 +106,7 @@ for _name, _args, _res in [
     ("tq_moe_workspace_layout", [_P(tq_experts), _i64, _i32, _P(tq_moe_layout)], _i32),
     ("tq_moe_grouped", [_P(tq_experts), _vp, _i64, _vp, _vp, _i32, _vp, _vp, _sz, _i32, _vp], _i32),
     ("tq_moe_grouped_timed", [_P(tq_experts), _vp, _i64, _vp, _vp, _i32, _vp, _vp, _sz, _i32, _vp, _P(_vp)], _i32),
+    ("tq_stream_read_timed", [_vp, _sz, _vp, _vp, _P(_vp)], _i32),
     ("tq_moe_noalloc_max_bytes", [], _sz),
     ("tq_moe_grouped_noalloc", [_P(tq_experts), _vp, _i64, _vp, _vp, _i32, _vp, _i32, _vp], _i32),
     ("tq_moe_stage_count", [], _i32),
@@ -261,6 +264,32 @@ def tq_gemv_timed(m: TqMatrix, q: torch.Tensor, d: torch.Tensor, bsum: torch.Ten
     _ok(_L.tq_gemv_timed(ctypes.byref(desc), _dev(q, torch.int8, "q", (t, m.k)), _dev(d, torch.float32, "d", (t, m.k // 256)),
                          _dev(bsum, torch.int32, "bsum", (t, m.k // 256)), t, _dev(y, torch.float32, "y", (t, m.n)), dbg,
                          _stream(stream), arr))
+
+
+def _gemv_f32_args(m: TqMatrix, x, y, q, d, bsum, isum_dbg):
+    t = x.shape[0]
+    dbg = None if isum_dbg is None else _dev(isum_dbg, torch.int32, "isum_dbg", (t, m.n, m.k // 256))
+    return (ctypes.byref(m.desc()), _dev(x, torch.float32, "x", (t, m.k)), t, _dev(y, torch.float32, "y", (t, m.n)),
+            _dev(q, torch.int8, "q", (t, m.k)), _dev(d, torch.float32, "d", (t, m.k // 256)),
+            _dev(bsum, torch.int32, "bsum", (t, m.k // 256)), dbg)
+
+
+def tq_gemv_f32(m: TqMatrix, x: torch.Tensor, y: torch.Tensor, q: torch.Tensor, d: torch.Tensor, bsum: torch.Tensor,
+                isum_dbg: torch.Tensor | None = None, stream=None):
+    """The dot pass on fp32 activations (quantized in the same launch at one token);
+    q, d, bsum receive the quantized activations."""
+    _ok(_L.tq_gemv_f32(*_gemv_f32_args(m, x, y, q, d, bsum, isum_dbg), _stream(stream)))
+
+
+def tq_gemv_f32_timed(m: TqMatrix, x: torch.Tensor, y: torch.Tensor, q: torch.Tensor, d: torch.Tensor,
+                      bsum: torch.Tensor, events, isum_dbg: torch.Tensor | None = None, stream=None):
+    if len(events) != 2:
+        raise ValueError("need 2 events")
+    for ev in events:
+        if ev.cuda_event == 0:
+            ev.record()
+    arr = (_vp * 2)(*[ev.cuda_event for ev in events])
+    _ok(_L.tq_gemv_f32_timed(*_gemv_f32_args(m, x, y, q, d, bsum, isum_dbg), _stream(stream), arr))
 
 
 # -- free-scale two-plane variant -----------------------------------------------------------
@@ -554,6 +583,19 @@ def _moe_args(ex, x, topk_idx, topk_w, out, ws):
 
 def tq_moe_grouped(ex: TqExperts, x, topk_idx, topk_w, out, ws, flags: int = 0, stream=None):
     _ok(_L.tq_moe_grouped(*_moe_args(ex, x, topk_idx, topk_w, out, ws), flags, _stream(stream)))
+
+
+def tq_stream_read_timed(src: torch.Tensor, nbytes: int, sink: torch.Tensor, events, stream=None):
+    """The benchmark's streaming-read ceiling: read nbytes from the start of src (a
+    contiguous device tensor) in one launch, timed by events (two torch.cuda.Event)."""
+    if not src.is_cuda or not src.is_contiguous() or src.numel() * src.element_size() < nbytes:
+        raise ValueError("src: a contiguous device tensor of at least nbytes")
+    _dev(sink, torch.int32, "sink")
+    for ev in events:
+        if ev.cuda_event == 0:
+            ev.record()
+    arr = (_vp * 2)(events[0].cuda_event, events[1].cuda_event)
+    _ok(_L.tq_stream_read_timed(src.data_ptr(), nbytes, sink.data_ptr(), _stream(stream), arr))
 
 
 def tq_moe_noalloc_max_bytes() -> int:

@@ -184,16 +184,23 @@ def routing(seed: int, layer: int, tokens: int, experts: int, topk: int, kind: s
 
 
 def bench_routing_schedule(seed: int, steps: int, tokens: int, experts: int, topk: int,
-                           kind: str, exclude_recent: int = 3):
+                           kind: str, exclude_recent: int = 3, wrap_from: int | None = None):
     """A sequence of per-step routings for timing. Each step's experts avoid those of
     the previous ``exclude_recent`` steps, so that an expert's bytes are never re-read
     while still resident in a 256 MB last-level cache (the reuse distance exceeds
-    ``exclude_recent`` steps of expert bytes). Returns lists of (idx, w)."""
+    ``exclude_recent`` steps of expert bytes). With ``wrap_from``, the last
+    ``exclude_recent`` steps also avoid the experts of steps ``wrap_from`` onwards (as
+    many), so that steps wrap_from .. steps-1 can be replayed in a loop. Returns lists of
+    (idx, w)."""
     rng = _rng(seed, _TAG_BENCH, steps)
     out = []
     recent: list[set[int]] = []
-    for _ in range(steps):
+    for i in range(steps):
         banned = set().union(*recent) if recent else set()
+        if wrap_from is not None and i >= steps - exclude_recent and i - wrap_from >= exclude_recent:
+            for k in range(wrap_from, min(wrap_from + exclude_recent, steps)):
+                if k < len(out):
+                    banned |= set(int(e) for e in out[k][0].ravel())
         allowed = np.array([e for e in range(experts) if e not in banned])
         if kind == "uniform":
             idx = np.stack([rng.choice(allowed, size=topk, replace=False) for _ in range(tokens)])

@@ -1,5 +1,6 @@
 """GPU parity of the activation quantizer, the synthetic-weight generator and the single-
-matrix dot pass (tq_quantize_act, tq_synth_weights, tq_gemv) against the CPU oracle.
+matrix dot pass (tq_quantize_act, tq_synth_weights, tq_gemv, and tq_gemv_f32 with the
+quantization fused into the pass) against the CPU oracle.
 
 Bar: quantized activations, block scales, block code sums, packed codes and the exact
 int32 block sums are bit-exact; fp32 outputs agree within 1e-5 of the sum of the
@@ -154,3 +155,64 @@ def test_gemv_without_debug_output_matches(tq):
     _, _, _, y1, _ = run_gemv(tq, m, x, want_isum=True)
     _, _, _, y2, _ = run_gemv(tq, m, x, want_isum=False)
     assert torch.equal(y1, y2)
+
+
+def run_gemv_f32(tq, m, x: np.ndarray, want_isum=True):
+    t, k = x.shape
+    xd = torch.from_numpy(np.ascontiguousarray(x)).cuda()
+    q = torch.full((t, k), 99, dtype=torch.int8, device="cuda")
+    d = torch.full((t, k // 256), float("nan"), dtype=torch.float32, device="cuda")
+    b = torch.full((t, k // 256), -7, dtype=torch.int32, device="cuda")
+    y = torch.full((t, m.n), float("nan"), dtype=torch.float32, device="cuda")
+    isum = torch.full((t, m.n, k // 256), -1, dtype=torch.int32, device="cuda") if want_isum else None
+    tq.tq_gemv_f32(m, xd, y, q, d, b, isum)
+    torch.cuda.synchronize()
+    return q, d, b, y, isum
+
+
+@pytest.mark.parametrize("n,k,t", [(1, 256, 1), (5, 768, 1), (67, 2048, 1), (2048, 4096, 1), (19, 7168, 1),
+                                   (8, 16384, 1), (300, 3840, 1), (16384, 4096, 1), (16387, 512, 1), (130, 1280, 6)])
+def test_gemv_f32_fused_quantization(tq, oracle, n, k, t):
+    """tq_gemv_f32 (quantization fused into the dot-pass launch at one token): q, d, bsum
+    and the block sums bit-exact against the oracle, y within 1e-5 of the absolute terms
+    and bitwise equal to tq_quantize_act + tq_gemv (same rows per wave, same order);
+    several tokens take the two-launch path with the same guarantees."""
+    rng = np.random.default_rng(n * 11 + k + t)
+    t1 = rng.integers(-1, 2, (n, k)).astype(np.int8)
+    t2 = rng.integers(-1, 2, (n, k)).astype(np.int8)
+    s = np.asarray(np.exp(rng.uniform(np.log(1e-3), np.log(1e-1), (n, k // 256))), np.float16).view(np.uint16)
+    m = tq.TqMatrix(n, k, torch.from_numpy(tq.tq_fold_pack_host(t1, t2)).cuda(), torch.from_numpy(s.view(np.int16)).cuda())
+    x = rng.standard_normal((t, k)).astype(np.float32) * np.float32(3.0)
+    if k >= 1024:
+        x[0, 256:512] = 0.0  # an all-zero block: d = 0, q = 0
+    announce(f"gemv_f32 n={n} k={k} t={t}")
+    q, d, b, y, isum = run_gemv_f32(tq, m, x)
+    oq, od, ob = oracle.quantize(x)
+    assert np.array_equal(q.cpu().numpy(), oq)
+    assert np.array_equal(d.cpu().numpy().view(np.uint32), od.view(np.uint32))
+    assert np.array_equal(b.cpu().numpy(), ob)
+    yr, ar, ir = oracle.gemv(oracle.fold(t1, t2), s, oq, od, want_isum=True)
+    assert np.array_equal(isum.cpu().numpy(), ir)
+    assert_close(y.cpu().numpy(), yr, ar + 1e-30, what="y")
+    _, _, _, y2, _ = run_gemv(tq, m, x, want_isum=False)
+    assert torch.equal(y, y2), "fused quantization changes y"
+    _, _, _, y3, _ = run_gemv_f32(tq, m, x, want_isum=False)
+    assert torch.equal(y, y3), "debug output changes y"
+
+
+def test_gemv_f32_single_matrix_2048x4096(tq, oracle):
+    """The single-GEMV workload through the fused entry point: 2048 x 4096, one token,
+    seed 0."""
+    n, k = gen.CONFIGS[0]["n"], gen.CONFIGS[0]["k"]
+    key = gen.single_matrix_key(gen.SEED)
+    m = tq.TqMatrix.empty(n, k)
+    announce("gemv_f32 2048x4096 seed 0")
+    tq.tq_synth_weights(key, m)
+    c_ref, s_ref = oracle.synth_codes(key, n, k)
+    x = gen.activations(gen.SEED, 0, 1, k)
+    q, d, b, y, isum = run_gemv_f32(tq, m, x)
+    oq, od, ob = oracle.quantize(x)
+    assert np.array_equal(q.cpu().numpy(), oq) and np.array_equal(b.cpu().numpy(), ob)
+    yr, ar, ir = oracle.gemv(c_ref, s_ref, oq, od, want_isum=True)
+    assert np.array_equal(isum.cpu().numpy(), ir)
+    assert_close(y.cpu().numpy(), yr, ar, what="y")
