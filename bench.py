@@ -747,11 +747,11 @@ def run_moe(args, wl, cfg):
         tq.tq_moe_grouped_timed(layers[l], x_all[l][i], idx_all[l][i], w_all[l][i], out, ws, ev, args.flags)
     torch.cuda.synchronize()
     path = tq.tq_moe_path(layers[0], T, topk, args.flags)
-    # the single-token path launches no prologue, requant or combine kernel (their event
-    # pairs are recorded back to back): those stages are reported as null
-    empty = {"prologue", "requant", "combine"} if path == tq.TQ_MOE_PATH_T1 else set()
-    stage_ms = {n: (None if n in empty else float(np.mean([ev[2 * si].elapsed_time(ev[2 * si + 1]) for ev in evs])))
-                for si, n in enumerate(names)}
+    # stages with no kernel on the path taken (their event pairs are recorded back to
+    # back) are reported as null: the single-token path runs gate_up and down only
+    kernel_stages = {"gate_up", "down"} if path == tq.TQ_MOE_PATH_T1 else set(names)
+    stage_ms = {n: (float(np.mean([ev[2 * si].elapsed_time(ev[2 * si + 1]) for ev in evs])) if n in kernel_stages
+                    else None) for si, n in enumerate(names)}
     gu_ms = stage_ms["gate_up"]
     n_distinct = float(np.mean([len(np.unique(sched[l][i][0])) for i, l in runs]))
     mfma = path == tq.TQ_MOE_PATH_MFMA
@@ -790,9 +790,10 @@ def run_moe(args, wl, cfg):
         dn_bytes = n_distinct * matrix_bytes(H, I) + T * topk * (I + (I // 256) * 4) + T * topk * H * 4
         dn_kernel = "k_moe_mfma<1>" if mfma else "k_tb<1, ...>"
     dn_ms = stage_ms["down"]
-    down = {"kernel_symbol": dn_kernel, "bytes_per_launch": round(dn_bytes), "mean_ms": round(dn_ms, 5),
-            "GBps": round(dn_bytes / (dn_ms * 1e-3) / 1e9, 1),
-            "frac_of_hbm_peak": round(dn_bytes / (dn_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    down = {
+        "kernel_symbol": dn_kernel, "bytes_per_launch": round(dn_bytes), "mean_ms": round(dn_ms, 5),
+        "GBps": round(dn_bytes / (dn_ms * 1e-3) / 1e9, 1),
+        "frac_of_hbm_peak": round(dn_bytes / (dn_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
     # second ceiling: a plain streaming read of the step's bytes (per layer) and of the
     # dominant kernel's, measured here
     step_bytes = alg_bytes / (K * L)

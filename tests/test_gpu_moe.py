@@ -93,6 +93,7 @@ def test_moe_decode_batch1_uniform(tq, oracle, experts_h4096):
     out, ws = run_moe(tq, experts_h4096, x, idx, w)
     get = oracle_pkg.expert_getter(gen.SEED, 0, c["hidden"], c["inter"], oracle)
     check_moe(tq, oracle, experts_h4096, get, x, idx, w, out, ws, [0])
+    assert tq.tq_moe_status(ws, experts_h4096, 1, c["topk"]) == 0
     out2, _ = run_moe(tq, experts_h4096, x, idx, w)
     assert torch.equal(out, out2)  # bitwise reproducible
     assert_debug_flag_neutral(tq, experts_h4096, x, idx, w, out)
@@ -207,7 +208,8 @@ def test_moe_mfma_forced_batch32(tq, oracle, experts_h4096):
 
 
 @pytest.mark.parametrize("E,H,I,topk", [(4, 512, 768, 3), (3, 7168, 2048, 2), (9, 2304, 1280, 8), (2, 256, 256, 1),
-                                        (5, 4096, 4096, 4)])
+                                        (5, 4096, 4096, 4), (10, 7168, 2048, 8), (12, 8192, 512, 8),
+                                        (8, 1024, 1792, 8), (9, 256, 2048, 8)])
 def test_moe_single_token_shapes(tq, oracle, E, H, I, topk):
     """The single-token path (gate/up, then down with the requant and combine fused) at
     block counts of 1 to 28 per row: ragged last loads, every slot count up to 8, a
