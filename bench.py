@@ -166,14 +166,25 @@ WORKLOADS = {
 
 
 REPLAYS = 20  # repeats of the timed graph for the median and min-max band
+USE_GRAPH = True  # --no-graph: eager launches (for profiler counter passes, which only need the dispatches)
 
 
 def time_graph(step, W: int, K: int):
     """Capture W warmup and K timed steps in two HIP graphs; replay the warmup graph,
     then time the K-step graph between device synchronizations (seconds). Then replay
     the K-step graph REPLAYS more times, each bracketed by HIP events on its stream, for
-    the band (seconds per replay)."""
+    the band (seconds per replay). Without graphs (USE_GRAPH false): the same steps
+    launched eagerly, timed by wall clock, no band."""
     import torch
+    if not USE_GRAPH:
+        for i in range(W):
+            step(i)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(W, W + K):
+            step(i)
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0, None
     for i in range(min(W, 4)):  # eager sanity pass (also loads the code objects)
         step(i)
     torch.cuda.synchronize()
@@ -839,9 +850,14 @@ def main():
     ap.add_argument("--profile-steps", type=int, default=None, help="steps of the per-kernel event pass")
     ap.add_argument("--flags", type=int, default=0, help="tq_moe_grouped flags (1 force VALU, 2 force MFMA)")
     ap.add_argument("--slots", type=int, default=64, help="HBM expert slots of the stream workload")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="launch the steps eagerly instead of in HIP graphs, and skip the replay band (for "
+                         "profiler counter passes, which only need the kernels' dispatches)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (to scale HBM byte counters)")
     args = ap.parse_args()
+    global USE_GRAPH
+    USE_GRAPH = not args.no_graph
     if args.calibrate_copy:
         import torch
         src = torch.ones(1 << 28, dtype=torch.float32, device="cuda:0")  # 1 GiB
@@ -894,6 +910,8 @@ def main():
         **r["extra"],
         "roofline": r["roof"],
     }
+    if not USE_GRAPH:
+        res["timing_note"] = "eager launches (--no-graph): not the graph-timed figure"
     if r.get("reps"):
         per_step = np.array(r["reps"]) * 1e3 / K
         vals = r["value"] * (elapsed / np.array(r["reps"]))
