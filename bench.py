@@ -788,7 +788,12 @@ def run_moe(args, wl, cfg):
         roof = {"kernel": kname, "bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_I8_PEAK_TOPS,
                 "unit": "TOP/s", "frac": round(achieved / MFMA_I8_PEAK_TOPS, 4), "traffic": recorded_traffic(gu_kernel),
                 "ops_per_launch": gu_ops, "bytes_per_launch": round(gu_bytes), "mean_ms": round(gu_ms, 5),
-                "hbm_GBps": round(gu_bytes / (gu_ms * 1e-3) / 1e9, 1), "kernel_symbol": gu_kernel}
+                "hbm_GBps": round(gu_bytes / (gu_ms * 1e-3) / 1e9, 1), "kernel_symbol": gu_kernel,
+                "frac_timing": "hip events: the kernel's own start/stop timestamps, mean over the per-kernel pass"}
+        avg_ns = _recorded(gu_kernel, "average_ns", kind="kernel_stats")
+        if avg_ns is not None:
+            roof["rocprof_mean_ms"] = round(avg_ns * 1e-6, 5)
+            roof["frac_rocprof"] = round(gu_ops / (avg_ns * 1e-9) / 1e12 / MFMA_I8_PEAK_TOPS, 4)
     else:
         roof = hbm_roof(kname, gu_bytes, gu_ms, gu_kernel)
     # the down kernel beside it: the routed experts' down planes, h in (fp32 per slot on the
