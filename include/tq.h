@@ -316,7 +316,9 @@ tq_status tq_gemv_mx_timed(const tq_mat_mx* w, const int8_t* q, const float* d, 
  * flags: 0 (automatic path choice), or TQ_MOE_FORCE_VALU / TQ_MOE_FORCE_MFMA to pin
  * the per-expert path (VALU dot4 for few tokens per expert, int8 MFMA for many).
  * Single-token steps (t == 1, topk <= 8, topk * inter <= 16384) take a path of their
- * own unless TQ_MOE_FORCE_MFMA is given (tq_moe_path).
+ * own unless TQ_MOE_FORCE_MFMA is given (tq_moe_path). The grouped paths address the
+ * quantized activations with 32-bit offsets: TQ_ERR_INVALID if t * topk * max(hidden,
+ * inter) >= 2^31 (and t > 1 or TQ_MOE_FORCE_MFMA).
  * TQ_MOE_DEBUG_STAGES (may be or-ed with either): the same kernels, each taking one
  * extra branch on a kernel argument, also leave in the workspace, past the stage buffers,
  * every routed slot's g and u (fp32) and the exact int32 block sums of its gate, up and

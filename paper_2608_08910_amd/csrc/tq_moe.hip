@@ -620,14 +620,17 @@ __global__ __launch_bounds__(256) void k_moe_combine(MoeArgs A, float* __restric
 //    of kMStages stages, kMStages - 1 blocks ahead of the compute; 16-byte column c of
 //    row r sits at column c ^ (r & 15), so the 16 lanes that read one operand column of
 //    16 rows hit distinct banks;
-//  - each wave loads its 16 rows' nibbles kMStages - 1 blocks ahead into registers and
-//    unpacks them to 16c bytes as the B operands (lane: row l & 15, chunk 4t + (l >> 4),
-//    half h gives MFMA (t, h); the A operand takes the same 16 columns of the token's
-//    codes, so every product pairs matching columns);
+//  - each wave loads its 16 rows' nibbles kMStages - 1 blocks ahead into registers,
+//    row-coalesced (four neighbouring lanes read one 64-byte half of a row block: with
+//    one row per lane, each load would fetch sixteen 16-byte pieces of different rows,
+//    and the loads issue far slower), rewrites them through its own LDS area into MFMA
+//    lane order and unpacks them to 16c bytes as the B operands (lane: row l & 15, chunk
+//    4t + (l >> 4), half h gives MFMA (t, h); the A operand takes the same 16 columns of
+//    the token's codes, so every product pairs matching columns);
 //  - four MFMAs per 16x16 output tile accumulate sum (16c)*q = 16 * isum exactly (two
 //    sub-tiles at a time, so that 2 * NMAT independent chains interleave), and one
 //    fp32 multiply-add per output applies (f32(s) / 16) * d to it; pairs of 16-token
-//    sub-tiles past the expert's last token are skipped.
+//    sub-tiles past the expert's last token are skipped, and so are their token loads.
 // Tasks run hottest expert first, row tiles innermost: the workgroups running together
 // share a token tile through L2, and the tasks of one weight tile run RT tasks apart.
 // ---------------------------------------------------------------------------------
@@ -655,29 +658,51 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
-// One block's weights for one wave: the lane's two 16-byte code chunks and its row's
-// scale, per matrix.
+// One block's weights for one wave, per matrix: two 16-byte code chunks per lane as
+// loaded (row-coalesced: load c gives lane l chunk 4c + (l & 3) of the wave's row l >> 2,
+// so four neighbouring lanes read one 64-byte half of a row block), and the scale of the
+// lane's MFMA row l & 15.
 template <int NMAT>
 struct MfmaB {
   uint4 w[NMAT][2];
-  uint16_t s[NMAT];
+  uint32_t s[NMAT];  // f16 bits, zero-extended
 };
 
+// A buffer offset past every resource's num_records (all below 2^31 bytes): a load there
+// returns zeros without a memory access but still counts as an issued load, so refills
+// that are not needed keep every wave's count of loads in flight the same.
+constexpr uint32_t kOob = 0x80000000u;
+
+// Block b's weights for one wave whose 16 rows start at row0 (wrow: the lane's MFMA row;
+// b >= kb: out of range, no memory access). Cached loads: a hot expert's rows are read
+// again by its other token tiles.
 template <int NMAT>
-__device__ __forceinline__ void mfma_b_fetch(MfmaB<NMAT>& B, const MatRsrc (&mr)[NMAT], int wrow, int kb, int g, int b) {
+__device__ __forceinline__ void mfma_b_fetch(MfmaB<NMAT>& B, const MatRsrc (&mr)[NMAT], int row0, int wrow, int kb,
+                                             int lane, int b) {
+  const bool live = b < kb;
+  // (scales first: the compiler's own wait before the first reader of the last load of
+  // the group, a code chunk that the LDS store above takes after the step's wait, stays
+  // partial)
+#pragma unroll
+  for (int m = 0; m < NMAT; ++m) B.s[m] = buf_load_u16(mr[m].scales, live ? (uint32_t)((wrow * kb + b) * 2) : kOob, 0);
 #pragma unroll
   for (int m = 0; m < NMAT; ++m) {
 #pragma unroll
     for (int c = 0; c < 2; ++c)
-      B.w[m][c] = buf_load16(mr[m].codes, (uint32_t)((wrow * kb + b) * 128 + (4 * c + g) * 16), 0);
-    B.s[m] = buf_load_u16(mr[m].scales, (uint32_t)((wrow * kb + b) * 2), 0);
+      B.w[m][c] = buf_load16(mr[m].codes,
+                             live ? (uint32_t)(((row0 + (lane >> 2)) * kb + b) * 128 + (4 * c + (lane & 3)) * 16) : kOob,
+                             0, 0);
   }
 }
 
 // Piece j of block b of the token tile into one ring stage: 1 KB of codes, rows
-// 4 (4w + j) .. + 3 (ap: the lane's source for this piece at block 0).
-__device__ __forceinline__ void mfma_a_dma(int8_t* sa, const int8_t* ap, int b, int wv, int j) {
-  __builtin_amdgcn_global_load_lds((const void*)(ap + b * 256), (lds_ptr)(sa + (wv * 4 + j) * 1024), 16, 0, 0);
+// 4 (4w + j) .. + 3 (ao: the lane's byte offset from q for this piece at block 0). A piece
+// that is not needed (a sub-tile the task does not compute, or b >= kb) reads the first
+// 16 bytes of the activations in every lane: one cache line instead of 1 KB.
+__device__ __forceinline__ void mfma_a_dma(int8_t* sa, const int8_t* q, uint32_t ao, bool live, int b, int kb, int wv,
+                                           int j) {
+  const uint32_t o = live && b < kb ? ao + (uint32_t)b * 256u : 0u;
+  __builtin_amdgcn_global_load_lds((const void*)(q + o), (lds_ptr)(sa + (wv * 4 + j) * 1024), 16, 0, 0);
 }
 
 // Per block and wave: four code pieces and three loads per matrix.
@@ -691,6 +716,12 @@ __global__ __launch_bounds__(kMWaves * 64) void k_moe_mfma(MoeArgs A) {
   __shared__ __attribute__((aligned(16))) int8_t s_a0[kMT * 256], s_a1[kMT * 256], s_a2[kMT * 256];
   __shared__ __attribute__((aligned(16))) float s_dall[(kMaxK / 256) * kMT];  // [block][token]
   __shared__ int s_slot[kMT];
+  // per wave: one matrix's block of its 16 rows, the row-coalesced loads rewritten in MFMA
+  // lane order; chunks 0-3 of each row in s_bt0, chunks 4-7 in s_bt1 (1 KB per wave each;
+  // chunk x of row r at position x ^ ((r >> 2) & 3): the writes and the reads of eight
+  // lanes fall in distinct banks). Two arrays, so that each load's chunks and each MFMA
+  // operand's chunks lie in one of them.
+  __shared__ __attribute__((aligned(16))) uint8_t s_bt0[kMWaves * 1024], s_bt1[kMWaves * 1024];
   static_assert(kMT == 128 && kMN == 16 * kMWaves && kMWaves == 8 && kMStages == 3, "tile geometry");
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int li = lane & 15, g = lane >> 4;
@@ -711,27 +742,31 @@ __global__ __launch_bounds__(kMWaves * 64) void k_moe_mfma(MoeArgs A) {
     const int64_t e = ld_uniform(A.active + a);
     const int off = ld_uniform(A.act_off + a), cnt = ld_uniform(A.act_off + a + 1) - off;
     const int m0 = ttile * kMT, nvalid = min(kMT, cnt - m0);
+    const int nsub = (nvalid + 15) / 16;  // 16-token sub-tiles holding valid tokens
+    const int ncomp = 2 * ((nsub + 1) / 2);  // sub-tiles computed (in pairs)
     __syncthreads();  // the previous task is done with the ring and s_slot
     if (threadIdx.x < kMT) s_slot[threadIdx.x] = A.slot_list[off + m0 + min((int)threadIdx.x, nvalid - 1)];
     __syncthreads();
     // the lane's direct-to-LDS sources: piece j covers rows 4 (4w + j) .. + 3, the lane
-    // row 4 (4w + j) + (l >> 4) at stored column l & 15, i.e. source column (l & 15) ^ (r & 15)
-    const int8_t* ap[4];
+    // row 4 (4w + j) + (l >> 4) at stored column l & 15, i.e. source column (l & 15) ^ (r & 15);
+    // wave w fills sub-tile w, so a wave past the computed sub-tiles loads nothing
+    uint32_t ap[4];  // (activations address below 2^31 bytes)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int r = (wv * 4 + j) * 4 + (lane >> 4);
       const int sl = s_slot[r];
-      const int64_t arow = NMAT == 2 ? (int64_t)(sl / A.topk) : (int64_t)sl;
-      ap[j] = qsrc + arow * K + (((lane & 15) ^ (r & 15)) * 16);
+      const uint32_t arow = NMAT == 2 ? (uint32_t)(sl / A.topk) : (uint32_t)sl;
+      ap[j] = arow * (uint32_t)K + (uint32_t)(((lane & 15) ^ (r & 15)) * 16);
     }
-    // every block scale of the tile's tokens, once per task
-    for (int i = threadIdx.x; i < kMT * kb; i += kMWaves * 64) {
+    const bool alive = wv < ncomp;
+    // every block scale of the tile's computed tokens, once per task
+    for (int i = threadIdx.x; i < 16 * ncomp * kb; i += kMWaves * 64) {
       const int t = i / kb, b = i - t * kb, sl = s_slot[t];
       s_dall[b * kMT + t] = dsrc[(NMAT == 2 ? (int64_t)(sl / A.topk) : (int64_t)sl) * kb + b];
     }
     __syncthreads();
-    const int nsub = (nvalid + 15) / 16;  // 16-token sub-tiles holding valid tokens
-    const int wrow = min(rtile * kMN + wv * 16 + li, N - 1);
+    const int row0 = rtile * kMN + wv * 16;  // N is a multiple of 256: all 16 rows exist
+    const int wrow = row0 + li;
     MatRsrc mr[NMAT];
 #pragma unroll
     for (int m = 0; m < NMAT; ++m) {
@@ -746,37 +781,59 @@ __global__ __launch_bounds__(kMWaves * 64) void k_moe_mfma(MoeArgs A) {
 #pragma unroll
         for (int v = 0; v < 4; ++v) acc[mt][m][v] = 0.0f;
 
-    // blocks 0 and 1 in flight; then per block b: wait until only block b + 1's loads may
-    // be outstanding (loads complete in issue order), unpack block b's weights, barrier
-    // (every wave's piece of block b is in LDS, and stage (b + 2) % 3 is no longer read),
-    // issue block b + 2, compute block b.
+    // blocks 0 and 1 in flight; then per block b (block b's loads are in, block b + 1's may
+    // not be): block b's weights through LDS into MFMA order, block b + 2's weights issued
+    // into the registers just emptied, barrier (every wave's piece of block b is in LDS,
+    // and stage (b + 2) % 3 is no longer read), block b + 2's pieces issued, block b
+    // computed, then the wait for block b + 1 (loads complete in issue order).
     // Block b uses stage b % 3 and weight registers b % 2: the loop runs six blocks a turn.
     MfmaB<NMAT> B0, B1;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) mfma_a_dma(s_a0, ap[j], 0, wv, j);
-    mfma_b_fetch<NMAT>(B0, mr, wrow, kb, g, 0);
+    for (int j = 0; j < 4; ++j) mfma_a_dma(s_a0, qsrc, ap[j], alive, 0, kb, wv, j);
+    mfma_b_fetch<NMAT>(B0, mr, row0, wrow, kb, lane, 0);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) mfma_a_dma(s_a1, ap[j], min(1, kb - 1), wv, j);
-    mfma_b_fetch<NMAT>(B1, mr, wrow, kb, g, min(1, kb - 1));
+    for (int j = 0; j < 4; ++j) mfma_a_dma(s_a1, qsrc, ap[j], alive, 1, kb, wv, j);
+    mfma_b_fetch<NMAT>(B1, mr, row0, wrow, kb, lane, 1);
+    wait_vmcnt<kMfmaLoadsPerBlock<NMAT>>();
     const auto step = [&](int b, auto stage_c, MfmaB<NMAT>& Bs) {
       constexpr int ST = decltype(stage_c)::value, NS = (ST + 2) % 3;
       const int8_t* const sa = ST == 0 ? s_a0 : (ST == 1 ? s_a1 : s_a2);
       int8_t* const na = NS == 0 ? s_a0 : (NS == 1 ? s_a1 : s_a2);
       const float* const sd = s_dall + b * kMT;
-      wait_vmcnt<kMfmaLoadsPerBlock<NMAT>>();  // this wave's pieces of block b are in LDS
       float sf[NMAT];
       v4i bop[NMAT][2][2];
+      uint8_t* const bt0 = s_bt0 + wv * 1024;
+      uint8_t* const bt1 = s_bt1 + wv * 1024;
 #pragma unroll
       for (int m = 0; m < NMAT; ++m) {
         // the MFMA sums 16c * q = 16 isum; dividing the f16 scale by 16 is exact
-        sf[m] = f16_bits_to_f32(Bs.s[m]) * 0.0625f;
+        sf[m] = f16_bits_to_f32((uint16_t)Bs.s[m]) * 0.0625f;
+        // through the wave's own LDS areas into MFMA order: lane (li, g) takes chunks g and
+        // 4 + g of row li (LDS accesses of one wave complete in issue order, so the reads
+        // see the writes; the fences keep the compiler's order)
+        const int wo = (lane >> 2) * 64 + (((lane & 3) ^ ((lane >> 4) & 3)) * 16);
+        *reinterpret_cast<uint4*>(bt0 + wo) = Bs.w[m][0];
+        *reinterpret_cast<uint4*>(bt1 + wo) = Bs.w[m][1];
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        __builtin_amdgcn_wave_barrier();
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        const int ro = li * 64 + ((g ^ ((li >> 2) & 3)) * 16);
+        uint4 wt[2];
+        wt[0] = *reinterpret_cast<const uint4*>(bt0 + ro);
+        wt[1] = *reinterpret_cast<const uint4*>(bt1 + ro);
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        __builtin_amdgcn_wave_barrier();
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
-          const uint4 w = Bs.w[m][c];
+          const uint4 w = wt[c];
           bop[m][c][0] = v4i{lo16c(w.x), lo16c(w.y), lo16c(w.z), lo16c(w.w)};
           bop[m][c][1] = v4i{hi16c(w.x), hi16c(w.y), hi16c(w.z), hi16c(w.w)};
         }
       }
+      // block b + 2's weights into the registers emptied above (past the last block: out of
+      // range, no memory access)
+      mfma_b_fetch<NMAT>(Bs, mr, row0, wrow, kb, lane, b + 2);
       // A bare barrier: __syncthreads' release fence would also wait for the loads in
       // flight for the blocks ahead. The wait above covers this wave's part of block b;
       // its LDS reads of the previous block were consumed (waited for) by its MFMAs; the
@@ -786,23 +843,14 @@ __global__ __launch_bounds__(kMWaves * 64) void k_moe_mfma(MoeArgs A) {
       __atomic_signal_fence(__ATOMIC_SEQ_CST);
       // block b + 2 is issued among the sub-tiles' MFMAs, so that the eight waves' loads
       // do not queue up at once; unconditional, so that every path has the same loads in
-      // flight (past the last block: block kb - 1 again, into a stage and registers no
-      // longer read)
-      const int nb = min(b + 2, kb - 1);
+      // flight (past the last block: out-of-range loads, no memory access)
+      const int nb = b + 2;
       // sub-tiles in pairs: one straight-line stretch holds 2 * NMAT independent MFMA
       // chains, so one chain's epilogue overlaps the others' MFMAs (a pair whose second
       // sub-tile holds no valid token computes it anyway: its rows repeat the last valid
       // token and are not stored)
-#pragma unroll
-      for (int mp = 0; mp < kMT / 32; ++mp) {
-        if (mp < 2) {
-          mfma_a_dma(na, ap[2 * mp], nb, wv, 2 * mp);
-          mfma_a_dma(na, ap[2 * mp + 1], nb, wv, 2 * mp + 1);
-        }
-        if (mp == 2) mfma_b_fetch<NMAT>(Bs, mr, wrow, kb, g, nb);
-        if (2 * mp >= nsub) continue;  // no valid token in this pair
-        v4i aop[2][2][2];
-        float4 d4[2];
+      // the operands of sub-tile pair mp (A codes of its 32 token rows, their block scales)
+      const auto read_pair = [&](int mp, v4i (&aop)[2][2][2], float4 (&d4)[2]) {
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
           const int mt = 2 * mp + q;
@@ -813,6 +861,17 @@ __global__ __launch_bounds__(kMWaves * 64) void k_moe_mfma(MoeArgs A) {
             for (int h = 0; h < 2; ++h) aop[q][c][h] = lds_v4i(arow_lds + (((2 * (4 * c + g) + h) ^ li) * 16));
           d4[q] = *reinterpret_cast<const float4*>(&sd[mt * 16 + 4 * g]);
         }
+      };
+#pragma unroll
+      for (int mp = 0; mp < kMT / 32; ++mp) {
+        v4i aop[2][2][2];
+        float4 d4[2];
+        if (mp < 2) {
+          mfma_a_dma(na, qsrc, ap[2 * mp], alive, nb, kb, wv, 2 * mp);
+          mfma_a_dma(na, qsrc, ap[2 * mp + 1], alive, nb, kb, wv, 2 * mp + 1);
+        }
+        if (2 * mp >= nsub) continue;  // no valid token in this pair
+        read_pair(mp, aop, d4);
         v4i C[2][NMAT];
 #pragma unroll
         for (int q = 0; q < 2; ++q)
@@ -858,6 +917,10 @@ __global__ __launch_bounds__(kMWaves * 64) void k_moe_mfma(MoeArgs A) {
             acc[mt][m][3] = fmaf(sf[m] * d4[q].w, (float)C[q][m][3], acc[mt][m][3]);
           }
       }
+      // for the next step: block b + 1's loads are in (only block b + 2's may still be in
+      // flight). Waiting here, at the end of the step, keeps every reader of those
+      // registers after the wait.
+      wait_vmcnt<kMfmaLoadsPerBlock<NMAT>>();
     };
     using I0 = std::integral_constant<int, 0>;
     using I1 = std::integral_constant<int, 1>;
@@ -1380,11 +1443,11 @@ static tq_status validate_experts(const tq_experts* ex, const char* fn) {
 static int choose_path(const tq_experts* ex, int64_t t, int32_t topk, int32_t flags) {
   if (t == 1 && topk <= kT1MaxTopk && (int64_t)topk * ex->inter <= kT1MaxHq && !(flags & TQ_MOE_FORCE_MFMA))
     return TQ_MOE_PATH_T1;
-  // (the VALU kernels address activations with 32-bit buffer offsets)
+  // (both grouped paths address the quantized activations with 32-bit buffer offsets)
   const int64_t S = t * topk;
-  const bool valu_fits = S * std::max(ex->hidden, ex->inter) < ((int64_t)1 << 31);
-  const bool mfma = (flags & TQ_MOE_FORCE_MFMA) || (!(flags & TQ_MOE_FORCE_VALU) && (S >= kMfmaMinSlots || !valu_fits));
-  return mfma ? TQ_MOE_PATH_MFMA : (valu_fits ? TQ_MOE_PATH_VALU : -1);
+  if (S * std::max(ex->hidden, ex->inter) >= ((int64_t)1 << 31)) return -1;
+  const bool mfma = (flags & TQ_MOE_FORCE_MFMA) || (!(flags & TQ_MOE_FORCE_VALU) && S >= kMfmaMinSlots);
+  return mfma ? TQ_MOE_PATH_MFMA : TQ_MOE_PATH_VALU;
 }
 
 static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const int32_t* topk_idx,
@@ -1470,7 +1533,9 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
 
   (void)hipGetLastError();
   const int path = choose_path(ex, t, topk, flags);
-  if (path < 0) return fail(TQ_ERR_INVALID, "%s: t * topk = %lld slots too many for the VALU path", fn, (long long)S);
+  if (path < 0)
+    return fail(TQ_ERR_INVALID, "%s: t * topk * max(hidden, inter) = %lld * %d reaches 2^31 (32-bit activation offsets)",
+                fn, (long long)S, std::max(ex->hidden, ex->inter));
   if (path == TQ_MOE_PATH_T1) {
     const int rgu = t1_rpw_gu(nl_gu);
     // single token: gate_up, then down with the requant and the combine fused; the

@@ -395,12 +395,14 @@ def test_moe_path_choice():
     assert path(wide, 1, 4) == tq.TQ_MOE_PATH_T1
     assert path(wide, 1, 5) == tq.TQ_MOE_PATH_VALU  # 5 x 4096 requantized bytes exceed the LDS budget
     assert path(d, 0, 8) == -1 and path(d, 1, 0) == -1
-    # the VALU kernels address activations with 32-bit offsets: at S * max(H, I) = 2^31 the
-    # automatic choice is MFMA and a forced VALU call is refused; one token fewer fits
+    # both grouped paths address activations with 32-bit offsets: at S * max(H, I) = 2^31
+    # every grouped call is refused; one token fewer fits either path
     big = _experts_desc(E=256, H=16384, I=2048)
     t_lim = (1 << 31) // (16384 * 8)
-    assert path(big, t_lim, 8) == tq.TQ_MOE_PATH_MFMA
+    assert path(big, t_lim, 8) == -1
     assert path(big, t_lim, 8, tq.TQ_MOE_FORCE_VALU) == -1
+    assert path(big, t_lim, 8, tq.TQ_MOE_FORCE_MFMA) == -1
+    assert path(big, t_lim - 1, 8) == tq.TQ_MOE_PATH_MFMA
     assert path(big, t_lim - 1, 8, tq.TQ_MOE_FORCE_VALU) == tq.TQ_MOE_PATH_VALU
 
 
