@@ -7,9 +7,10 @@
  *    one f16 scale s per group.
  *  - Sec. 2.2: the folded code plane is the persistent serving representation (4.0625
  *    bits/weight: 4-bit codes plus one f16 scale per 256 weights of an output channel).
- *    Serving is one pass: the codes decode to -4..4 by arithmetic, an integer dot runs
- *    against block-quantized int8 activations, and each block costs one float
- *    multiply-add.
+ *    A matrix-vector product reads those bytes once: each nibble becomes an integer in
+ *    -4..4 with two bitwise operations (no lookup), 256 of them meet int8 activations
+ *    (one fp32 scale per 256 inputs) in an exact integer sum, and that sum enters the
+ *    fp32 result through a single fused multiply-add with the two scales.
  *
  * Persistent layout of one matrix with n output channels (rows) and k inputs
  * (k % 256 == 0, kb = k/256 blocks per row):

@@ -1,5 +1,5 @@
-// Per-256 activation quantizer (Sec. 2.2: the integer dot runs against block-quantized
-// activations; the block/scale/rounding rule is this library's reading, stated in tq.h).
+// Per-256 activation quantizer (Sec. 2.2: the codes meet int8 activations that carry one
+// scale per block; the block/scale/rounding rule is this library's reading, stated in tq.h).
 #include "tq_device.hpp"
 #include "tq_internal.hpp"
 
