@@ -970,9 +970,9 @@ __global__ __launch_bounds__(kMWaves * 64) void k_moe_mfma(MoeArgs A) {
 // Single-token step (t == 1, topk <= 8): two kernels and no dispatch pass. Each slot
 // is its own task (a duplicated expert is simply computed twice), so the expert comes
 // straight from topk_idx; x is quantized once per workgroup into LDS while the weight
-// loads are in flight; the down kernel requantizes every slot's h into LDS once per
-// workgroup and folds the weighted combine into registers, in ascending slot order
-// (the same fmaf chain as k_moe_combine, so both paths give identical bits).
+// loads are in flight; in the down kernel each slot's wave requantizes that slot's h in
+// registers, and the workgroup folds the weighted combine in ascending slot order (the
+// same fmaf chain as k_moe_combine).
 // ---------------------------------------------------------------------------------
 
 constexpr int kT1MaxTopk = 8;
@@ -1017,22 +1017,19 @@ __device__ __forceinline__ int dot_chunk16(const uint4 w, const int (&a)[8]) {
   return dot32x16(c, a);
 }
 
-// Layout of the single-token kernels' LDS: the quantized activations of one token (x, or
-// the topk slots' h), their block scales and code sums, and per-wave row results.
-constexpr int kT1LdsQ = kMaxK > kT1MaxHq ? kMaxK : kT1MaxHq;
-constexpr int kT1MaxWaves = 8;  // waves of a single-token down workgroup the row-result area holds
-constexpr int kT1LdsBytes = kT1LdsQ + 2 * (kT1LdsQ / 256) * 4 + kT1MaxWaves * 32 * 4;
+// Layout of the single-token gate/up kernel's LDS: the quantized activations of the
+// token, their block scales and code sums.
+constexpr int kT1LdsQ = kMaxK;
+constexpr int kT1LdsBytes = kT1LdsQ + 2 * (kT1LdsQ / 256) * 4;
 
 struct T1Lds {
   int8_t* q;
   float* d;
   int* b;
-  float* y;  // [waves][32]
   __device__ explicit T1Lds(uint8_t* raw)
       : q(reinterpret_cast<int8_t*>(raw)),
         d(reinterpret_cast<float*>(raw + kT1LdsQ)),
-        b(reinterpret_cast<int*>(raw + kT1LdsQ + (kT1LdsQ / 256) * 4)),
-        y(reinterpret_cast<float*>(raw + kT1LdsQ + 2 * (kT1LdsQ / 256) * 4)) {}
+        b(reinterpret_cast<int*>(raw + kT1LdsQ + (kT1LdsQ / 256) * 4)) {}
 };
 
 // Gate/up of one single-token workgroup `wg`: WAVES waves, each owning RPW rows (a power
@@ -1062,13 +1059,18 @@ __device__ __forceinline__ void t1_gateup_wg(const float* __restrict__ x, const 
   __builtin_amdgcn_sched_barrier(0);
   const MatRsrc mr[2] = {mat_rsrc(A.codes[0] + ec * A.stride_codes[0], A.scales[0] + ec * A.stride_scales[0], I, kb),
                          mat_rsrc(A.codes[1] + ec * A.stride_codes[1], A.scales[1] + ec * A.stride_scales[1], I, kb)};
+  // loads in the order of use: every row's chunk of load 0, then of load 1, ...
   uint4 wr[2 * RPW][NL];  // [2r] gate row r, [2r + 1] up row r
 #pragma unroll
-  for (int r = 0; r < RPW; ++r) {
-    const int row = min(row0 + r, I - 1);
+  for (int i = 0; i < NL; ++i)
 #pragma unroll
-    for (int m = 0; m < 2; ++m) load_lane_codes<NL>(mr[m], row, kb, g, cp, wr[2 * r + m]);
-  }
+    for (int r = 0; r < RPW; ++r) {
+      const uint32_t srow = (uint32_t)min(row0 + r, I - 1) * (uint32_t)kb;
+#pragma unroll
+      for (int m = 0; m < 2; ++m)
+        wr[2 * r + m][i] =
+            buf_load16(mr[m].codes, (uint32_t)min(8 * i + g, kb - 1) * 128u + (uint32_t)cp * 16u, srow * 128u);
+    }
   // after the block butterfly a lane keeps the row rev(lane bits): its scales
   uint16_t sr[2][NL];
   const int lrow = min(row0 + rev_bits<clog2(RPW)>(lane & (RPW - 1)), I - 1);
@@ -1130,134 +1132,110 @@ __device__ __forceinline__ void t1_gateup_wg(const float* __restrict__ x, const 
   }
 }
 
-// Down of one single-token workgroup `wg`: WAVES waves, each owning RPW rows of down for
-// every slot. Items slot * RPW + row (padded to V, a power of two) meet in the integer
-// block butterfly; the lane that keeps an item applies its slot's block scale; the
-// fp32 butterfly over blocks leaves one item per lane; the per-slot results meet in
-// LDS, where the row's lane forms out = sum_j w_j * y_j in ascending j.
+// Down of one single-token workgroup `wg`: one wave per slot (TOPK waves), wave j owning
+// rows row0 .. row0 + ROWS - 1 of slot j's down matrix. A wave quantizes its own slot's h
+// in registers (each 8-lane group holds one 256-block of it: the block's absmax and code
+// sum come from group butterflies), so no wave waits for another before its dot products
+// and each wave's arithmetic follows its own weight loads. Per load, the ROWS rows meet
+// in the integer block butterfly; the lane that keeps a row applies the block's scales;
+// the fp32 butterfly over blocks leaves one row per lane; the slots' row results meet in
+// LDS, where ROWS lanes form out = sum_j w_j * y_j in ascending j.
 // `stage`: this workgroup also stores the quantized h.
-template <int NL, int RPW, int TOPK, int WAVES, bool RAGGED>
-__device__ __forceinline__ void t1_down_wg(const MoeArgs& A, float* __restrict__ out, int wg, bool stage, T1Lds s) {
-  constexpr int V = 1 << clog2(2 * TOPK * RPW - 1);  // items slot * RPW + row, padded to a power of two
-  static_assert(V <= 32 && (RPW & (RPW - 1)) == 0, "down tile too large");
-  static_assert(WAVES <= kT1MaxWaves, "the row-result area holds kT1MaxWaves waves");
-  const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int g = lane >> 3, cp = lane & 7, gid = wv * 8 + g;
+template <int NL, int ROWS, int TOPK, bool RAGGED>
+__device__ __forceinline__ void t1_down_wg(const MoeArgs& A, float* __restrict__ out, int wg, bool stage,
+                                           float* __restrict__ s_y) {
+  static_assert(ROWS >= 1 && ROWS <= 32 && (ROWS & (ROWS - 1)) == 0, "rows per wave: a power of two <= 32");
+  constexpr int NH = NL < 2 ? NL : 2;  // blocks of h loaded ahead of the weights
+  const int lane = threadIdx.x & 63, j = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane >> 3, cp = lane & 7;
   const int kb = A.inter / 256, H = A.hidden, I = A.inter;
-  const int nblk = TOPK * kb;
-  const int row0 = (wg * WAVES + wv) * RPW;
-  int64_t ej[TOPK];
-  float wj[TOPK];  // routing weights, loaded now: in the combine each would be a round trip
-  unsigned vmask = 0;
-#pragma unroll
-  for (int j = 0; j < TOPK; ++j) {
-    const int e = A.topk_idx[j];
-    wj[j] = A.topk_w[j];
-    const bool v = e >= 0 && e < A.n_experts;
-    vmask |= (unsigned)v << j;
-    ej[j] = v ? e : 0;
-  }
-  // this group's first block of h first, so that its wait does not queue behind the
-  // weights (an unrouted slot's h is never written: such a group loads the buffer's
-  // first block instead and skips the quantization)
-  const int blk0 = min(gid, nblk - 1);
-  const bool q0 = gid < nblk && ((vmask >> (blk0 / kb)) & 1);
-  const __amdgpu_buffer_rsrc_t hr = make_rsrc(A.h, (uint32_t)(TOPK * I) * 4u);
-  float v[32];
-  buf_load32f(hr, (uint32_t)(q0 ? blk0 : 0), cp, v);
-  __builtin_amdgcn_sched_barrier(0);
-  uint4 wr[TOPK][RPW][NL];
-#pragma unroll
-  for (int j = 0; j < TOPK; ++j) {
-    const MatRsrc mr = mat_rsrc(A.codes[2] + ej[j] * A.stride_codes[2], A.scales[2] + ej[j] * A.stride_scales[2], H, kb);
-#pragma unroll
-    for (int r = 0; r < RPW; ++r) load_lane_codes<NL>(mr, min(row0 + r, H - 1), kb, g, cp, wr[j][r]);
-  }
-  // after the block butterfly a lane keeps KI items (slot jk, row rk): their scales
-  using RR = RowReduce<V, 1>;
+  const int row0 = wg * ROWS;
+  const int e = A.topk_idx[j];
+  using RR = RowReduce<ROWS, 1>;
   constexpr int KI = RR::KI;
-  int jk[KI];
-  uint16_t sr[KI][NL];
+  if (e >= 0 && e < A.n_experts && row0 < H) {  // wave-uniform: an unrouted slot's h is never written
+    // the slot's h first (its waits must not queue behind the weights), then every weight load
+    const __amdgpu_buffer_rsrc_t hr = make_rsrc(A.h + (int64_t)j * I, (uint32_t)I * 4u);
+    float vh[NH][32];
 #pragma unroll
-  for (int k = 0; k < KI; ++k) {
-    const int it = RR::kept(k, lane);
-    jk[k] = it / RPW;
-    int64_t e = ej[0];
+    for (int i = 0; i < NH; ++i) buf_load32f(hr, (uint32_t)min(8 * i + g, kb - 1), cp, vh[i]);
+    __builtin_amdgcn_sched_barrier(0);
+    const MatRsrc mr = mat_rsrc(A.codes[2] + (int64_t)e * A.stride_codes[2], A.scales[2] + (int64_t)e * A.stride_scales[2],
+                                H, kb);
+    // loads in the order of use: every row's chunk of load 0, then of load 1, ...
+    uint4 wr[ROWS][NL];
 #pragma unroll
-    for (int jj = 1; jj < TOPK; ++jj) e = jk[k] == jj ? ej[jj] : e;
-    const int row = min(row0 + it % RPW, H - 1);
-    const uint16_t* sp = A.scales[2] + e * A.stride_scales[2] + (int64_t)row * kb;
+    for (int i = 0; i < NL; ++i)
 #pragma unroll
-    for (int i = 0; i < NL; ++i) sr[k][i] = sp[min(8 * i + g, kb - 1)];
-  }
-  quantize_to_lds(v, blk0, cp, s.q, s.d, s.b, q0);
-  for (int blk = gid + WAVES * 8; blk < nblk; blk += WAVES * 8) {
-    if (!((vmask >> (blk / kb)) & 1)) continue;
-    buf_load32f(hr, (uint32_t)blk, cp, v);
-    quantize_to_lds(v, blk, cp, s.q, s.d, s.b, true);
-  }
-  __syncthreads();
-  if (stage) {  // stage buffers, once per call
-    for (int i = threadIdx.x; i < TOPK * I / 4; i += WAVES * 64)
-      if ((vmask >> (4 * i / I)) & 1) reinterpret_cast<int*>(A.hq)[i] = reinterpret_cast<const int*>(s.q)[i];
-    for (int i = threadIdx.x; i < nblk; i += WAVES * 64)
-      if ((vmask >> (i / kb)) & 1) {
-        A.hd[i] = s.d[i];
-        A.hb[i] = s.b[i];
-      }
-  }
-  if (row0 >= H) return;
-  float acc[KI];
-#pragma unroll
-  for (int k = 0; k < KI; ++k) acc[k] = 0.0f;
-#pragma unroll
-  for (int i = 0; i < NL; ++i) {
-    const int b = 8 * i + g;
-    int p[V];
-#pragma unroll
-    for (int v = TOPK * RPW; v < V; ++v) p[v] = 0;
-#pragma unroll
-    for (int j = 0; j < TOPK; ++j) {
-      const int4* qp = reinterpret_cast<const int4*>(s.q + j * I + min(b, kb - 1) * 256 + cp * 32);
-      const int4 lo = qp[0], hi = qp[1];
-      const int qa[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-#pragma unroll
-      for (int r = 0; r < RPW; ++r) p[j * RPW + r] = dot_chunk16(wr[j][r][i], qa);
-    }
-    RR::block_sums(p);
-    // debug stage dump: each kept (slot, row) item's exact block sum, one lane per item
-    if (A.dbg_dsum != nullptr && RR::block_writer(lane) && b < kb) {
-#pragma unroll
-      for (int k = 0; k < KI; ++k) {
-        const int it = RR::kept(k, lane), r = it % RPW;
-        if (jk[k] < TOPK && ((vmask >> jk[k]) & 1) && row0 + r < H)
-          A.dbg_dsum[((int64_t)jk[k] * H + row0 + r) * kb + b] = p[k] >> 4;
-      }
-    }
+      for (int r = 0; r < ROWS; ++r)
+        wr[r][i] = buf_load16(mr.codes, (uint32_t)min(8 * i + g, kb - 1) * 128u + (uint32_t)cp * 16u,
+                              (uint32_t)min(row0 + r, H - 1) * (uint32_t)kb * 128u);
+    // after the block butterfly a lane keeps KI rows: their scales
+    uint16_t sr[KI][NL];
 #pragma unroll
     for (int k = 0; k < KI; ++k) {
-      // padded items and unrouted slots: d = 0 (their LDS codes are never written)
-      const bool ok = jk[k] < TOPK && ((vmask >> jk[k]) & 1) && (!RAGGED || b < kb);
-      const float dv = ok ? s.d[min(jk[k], TOPK - 1) * kb + min(b, kb - 1)] : 0.0f;
-      acc[k] = fmaf(f16_bits_to_f32(sr[k][i]) * dv, (float)(p[k] >> 4), acc[k]);
-    }
-  }
-  RR::block_totals(acc);
-  float* sy = s.y + wv * 32;
-  if (RR::writer(lane)) sy[RR::item(lane)] = acc[0];
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  if (lane < RPW && row0 + lane < H) {
-    float acc = 0.0f;
+      const uint32_t srow = (uint32_t)min(row0 + RR::kept(k, lane), H - 1) * (uint32_t)kb;
 #pragma unroll
-    for (int j = 0; j < TOPK; ++j) {
-      if (!((vmask >> j) & 1)) continue;
-      const float y = sy[j * RPW + lane];
-      acc = fmaf(wj[j], y, acc);
-      A.yd[(int64_t)j * H + row0 + lane] = y;
+      for (int i = 0; i < NL; ++i) sr[k][i] = buf_load_u16(mr.scales, (srow + (uint32_t)min(8 * i + g, kb - 1)) * 2u, 0);
     }
-    out[row0 + lane] = acc;
+    float acc[KI];
+#pragma unroll
+    for (int k = 0; k < KI; ++k) acc[k] = 0.0f;
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      const int b = 8 * i + g;
+      // block b of the slot's h: codes, scale and code sum (blocks past the row end repeat
+      // the last block; their scale is taken as zero below and they are not stored)
+      int qw[8], qs, bs;
+      float dq;
+      if (i < NH) {
+        quantize_group32(vh[i < NH ? i : 0], qw, qs, dq, bs);
+      } else {
+        float v[32];
+        buf_load32f(hr, (uint32_t)min(b, kb - 1), cp, v);
+        quantize_group32(v, qw, qs, dq, bs);
+      }
+      if (stage && b < kb) {
+        int4* qp = reinterpret_cast<int4*>(A.hq + (int64_t)j * I + b * 256 + cp * 32);
+        qp[0] = make_int4(qw[0], qw[1], qw[2], qw[3]);
+        qp[1] = make_int4(qw[4], qw[5], qw[6], qw[7]);
+        if (cp == 0) {
+          A.hd[j * kb + b] = dq;
+          A.hb[j * kb + b] = bs;
+        }
+      }
+      int p[ROWS];
+#pragma unroll
+      for (int r = 0; r < ROWS; ++r) p[r] = dot_chunk16(wr[r][i], qw);
+      RR::block_sums(p);
+      // debug stage dump: each kept row's exact block sum, one lane per (row, block)
+      if (A.dbg_dsum != nullptr && RR::block_writer(lane) && b < kb) {
+#pragma unroll
+        for (int k = 0; k < KI; ++k) {
+          const int r = RR::kept(k, lane);
+          if (row0 + r < H) A.dbg_dsum[((int64_t)j * H + row0 + r) * kb + b] = p[k] >> 4;
+        }
+      }
+      const float dv = (!RAGGED || b < kb) ? dq : 0.0f;
+#pragma unroll
+      for (int k = 0; k < KI; ++k) acc[k] = fmaf(f16_bits_to_f32(sr[k][i]) * dv, (float)(p[k] >> 4), acc[k]);
+    }
+    RR::block_totals(acc);
+    if (RR::writer(lane)) s_y[j * ROWS + RR::item(lane)] = acc[0];
+  }
+  __syncthreads();
+  const int t = threadIdx.x;
+  if (t < ROWS && row0 + t < H) {
+    float o = 0.0f;
+#pragma unroll
+    for (int jj = 0; jj < TOPK; ++jj) {
+      const int ej = A.topk_idx[jj];
+      if (ej < 0 || ej >= A.n_experts) continue;
+      const float y = s_y[jj * ROWS + t];
+      o = fmaf(A.topk_w[jj], y, o);
+      A.yd[(int64_t)jj * H + row0 + t] = y;
+    }
+    out[row0 + t] = o;
   }
 }
 
@@ -1267,10 +1245,10 @@ __global__ __launch_bounds__(WAVES * 64) void k_t1_gateup(const float* __restric
   t1_gateup_wg<NL, RPW, WAVES, RAGGED>(x, A, blockIdx.x, blockIdx.x == 0, T1Lds(s_raw));
 }
 
-template <int NL, int RPW, int TOPK, int WAVES, bool RAGGED>
-__global__ __launch_bounds__(WAVES * 64) void k_t1_down(MoeArgs A, float* __restrict__ out) {
-  __shared__ __attribute__((aligned(16))) uint8_t s_raw[kT1LdsBytes];
-  t1_down_wg<NL, RPW, TOPK, WAVES, RAGGED>(A, out, blockIdx.x, blockIdx.x == 0, T1Lds(s_raw));
+template <int NL, int ROWS, int TOPK, bool RAGGED>
+__global__ __launch_bounds__(TOPK * 64) void k_t1_down(MoeArgs A, float* __restrict__ out) {
+  __shared__ float s_y[TOPK * ROWS];
+  t1_down_wg<NL, ROWS, TOPK, RAGGED>(A, out, blockIdx.x, blockIdx.x == 0, s_y);
 }
 
 // ---------------------------------------------------------------------------------
@@ -1330,16 +1308,8 @@ static moe_fn pick_tb(int kb) {
 #ifndef TQ_T1_WAVES_GU
 #define TQ_T1_WAVES_GU 4  // waves per gate/up workgroup
 #endif
-#ifndef TQ_T1_RPW_DN
-#define TQ_T1_RPW_DN 2  // rows of down per wave, for every slot
-#endif
-#ifndef TQ_T1_WAVES_DN
-#define TQ_T1_WAVES_DN 8  // waves per down workgroup
-#endif
 constexpr int kT1RpwGU = TQ_T1_RPW_GU;
 constexpr int kT1WavesGU = TQ_T1_WAVES_GU;
-constexpr int kT1RpwDn = TQ_T1_RPW_DN;
-constexpr int kT1WavesDn = TQ_T1_WAVES_DN;
 
 using t1gu_fn = void (*)(const float*, MoeArgs);
 using t1dn_fn = void (*)(MoeArgs, float*);
@@ -1365,34 +1335,47 @@ static t1gu_fn pick_t1_gateup(int kb) {
 }
 static int t1_rpw_gu(int nl) { return nl <= 2 ? kT1RpwGU : (nl <= 4 ? (kT1RpwGU + 1) / 2 : 1); }
 
+// Rows of down per wave (one wave per slot): 16 loads of 1 KB per wave at NL = 1 and
+// eight or more slots, fewer rows with fewer slots (so that a step still has about 2048
+// waves) or longer rows (so that a wave's chunks stay within its registers).
+constexpr int t1_down_rows(int nl, int topk) {
+  const int r = (16 / nl) * (topk < 4 ? topk : 4) / 4;
+  return r < 1 ? 1 : 1 << clog2(r);  // rounded down to a power of two
+}
+
 template <int NL, bool R>
 static t1dn_fn pick_t1_down_k(int topk) {
   switch (topk) {
-    case 1: return k_t1_down<NL, kT1RpwDn, 1, kT1WavesDn, R>;
-    case 2: return k_t1_down<NL, kT1RpwDn, 2, kT1WavesDn, R>;
-    case 3: return k_t1_down<NL, kT1RpwDn, 3, kT1WavesDn, R>;
-    case 4: return k_t1_down<NL, kT1RpwDn, 4, kT1WavesDn, R>;
-    case 5: return k_t1_down<NL, kT1RpwDn, 5, kT1WavesDn, R>;
-    case 6: return k_t1_down<NL, kT1RpwDn, 6, kT1WavesDn, R>;
-    case 7: return k_t1_down<NL, kT1RpwDn, 7, kT1WavesDn, R>;
-    default: return k_t1_down<NL, kT1RpwDn, 8, kT1WavesDn, R>;
+    case 1: return k_t1_down<NL, t1_down_rows(NL, 1), 1, R>;
+    case 2: return k_t1_down<NL, t1_down_rows(NL, 2), 2, R>;
+    case 3: return k_t1_down<NL, t1_down_rows(NL, 3), 3, R>;
+    case 4: return k_t1_down<NL, t1_down_rows(NL, 4), 4, R>;
+    case 5: return k_t1_down<NL, t1_down_rows(NL, 5), 5, R>;
+    case 6: return k_t1_down<NL, t1_down_rows(NL, 6), 6, R>;
+    case 7: return k_t1_down<NL, t1_down_rows(NL, 7), 7, R>;
+    default: return k_t1_down<NL, t1_down_rows(NL, 8), 8, R>;
   }
 }
 
-// topk * inter <= 16384 bytes of LDS bounds NL: inter <= 16384 / topk.
+static int t1_down_nl(int kb) {
+  const int nl = (kb + 7) / 8;
+  return nl <= 2 ? nl : (nl <= 4 ? 4 : 8);
+}
+
+// topk * inter <= 16384 (the single-token path's bound) keeps NL <= 8.
 template <bool R>
 static t1dn_fn pick_t1_down_r(int nl, int topk) {
   switch (nl) {
     case 1: return pick_t1_down_k<1, R>(topk);
     case 2: return pick_t1_down_k<2, R>(topk);
-    case 3: case 4: return pick_t1_down_k<4, R>(topk);
+    case 4: return pick_t1_down_k<4, R>(topk);
     default: return pick_t1_down_k<8, R>(topk);
   }
 }
 static t1dn_fn pick_t1_down(int kb, int topk) {
-  const int nl = (kb + 7) / 8;
+  const int nl = t1_down_nl(kb);
   // NL is rounded up to 4 or 8 for nl > 2: those loads may run past the row end too
-  const bool ragged = kb % 8 != 0 || (nl > 2 && nl != 4 && nl != 8);
+  const bool ragged = kb % 8 != 0 || nl * 8 != kb;
   return ragged ? pick_t1_down_r<true>(nl, topk) : pick_t1_down_r<false>(nl, topk);
 }
 
@@ -1541,13 +1524,14 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
     // single token: gate_up, then down with the requant and the combine fused; the
     // prologue, requant and combine stages are empty on this path
     A.tiles_gu = (ex->inter + kT1WavesGU * rgu - 1) / (kT1WavesGU * rgu);
-    const unsigned tiles_dn = (unsigned)((ex->hidden + kT1WavesDn * kT1RpwDn - 1) / (kT1WavesDn * kT1RpwDn));
+    const int rows_dn = t1_down_rows(t1_down_nl(ex->inter / 256), topk);
+    const unsigned tiles_dn = (unsigned)((ex->hidden + rows_dn - 1) / rows_dn);
     if ((st = empty_stage(events, 0, stm, fn)) != TQ_OK) return st;
     if ((st = launch_stage(events, 1, pick_t1_gateup(ex->hidden / 256), dim3((unsigned)(topk * A.tiles_gu)), kT1WavesGU * 64, stm,
                            fn, x, A)) != TQ_OK)
       return st;
     if ((st = empty_stage(events, 2, stm, fn)) != TQ_OK) return st;
-    if ((st = launch_stage(events, 3, pick_t1_down(ex->inter / 256, topk), dim3(tiles_dn), kT1WavesDn * 64, stm, fn, A, out)) !=
+    if ((st = launch_stage(events, 3, pick_t1_down(ex->inter / 256, topk), dim3(tiles_dn), topk * 64, stm, fn, A, out)) !=
         TQ_OK)
       return st;
     return empty_stage(events, 4, stm, fn);
