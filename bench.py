@@ -780,7 +780,9 @@ def run_moe(args, wl, cfg):
         gu_bytes = n_distinct * 2 * matrix_bytes(I, H) + T * (H + (H // 256) * 4) + T * topk * I * 4
         rpw = 8 if nl_gu == 1 else (4 if nl_gu == 2 else (2 if nl_gu <= 4 else 1))
         nt = 2 if nl_gu <= 2 else 1  # tokens per group of the grouped VALU kernel (first, later)
-        gu_kernel = "k_moe_mfma<2>" if mfma else f"k_tb<2, {nl_gu}, {rpw}, {nt}, {nt}, 4, {ragged}>"
+        # the MFMA stage is two launches: 128-token tiles, then the experts of at most 32 slots
+        gu_kernel = ("k_moe_mfma<2, 128, 8, false> + k_moe_mfma<2, 32, 4, true>" if mfma
+                     else f"k_tb<2, {nl_gu}, {rpw}, {nt}, {nt}, 4, {ragged}>")
         kname = "gate_up"
     if mfma:
         gu_ops = 2.0 * T * topk * (2 * I * H)  # int8 multiply-adds of gate and up, 2 ops each
@@ -801,10 +803,13 @@ def run_moe(args, wl, cfg):
     # the output (or the per-slot rows) out
     if path == tq.TQ_MOE_PATH_T1:
         dn_bytes = n_distinct * matrix_bytes(H, I) + T * topk * I * 4 + T * H * 4
-        dn_kernel = f"k_t1_down<{nl_dn}, 2, {topk}, 8, {'true' if (I // 256) % 8 else 'false'}>"
+        nl4 = nl_dn if nl_dn <= 2 else (4 if nl_dn <= 4 else 8)
+        r = (16 // nl4) * min(topk, 4) // 4
+        rows = 1 if r < 1 else 1 << (r.bit_length() - 1)
+        dn_kernel = f"k_t1_down<{nl4}, {rows}, {topk}, {'true' if (I // 256) % 8 or nl4 * 8 != I // 256 else 'false'}>"
     else:
         dn_bytes = n_distinct * matrix_bytes(H, I) + T * topk * (I + (I // 256) * 4) + T * topk * H * 4
-        dn_kernel = "k_moe_mfma<1>" if mfma else "k_tb<1, ...>"
+        dn_kernel = "k_moe_mfma<1, 128, 8, false> + k_moe_mfma<1, 32, 4, true>" if mfma else "k_tb<1, ...>"
     dn_ms = stage_ms["down"]
     down = {
         "kernel_symbol": dn_kernel, "bytes_per_launch": round(dn_bytes), "mean_ms": round(dn_ms, 5),

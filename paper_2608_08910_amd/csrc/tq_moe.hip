@@ -37,13 +37,19 @@ static const char* const kStageNames[kNumStages] = {"prologue", "gate_up", "requ
 // Control words at the start of the workspace.
 enum Ctrl {
   kFlags = 0, kNActive = 1, kTasksGU = 2, kTasksDn = 3, kNValid = 4, kTasksMGU = 5, kTasksMDn = 6,
-  kCtrlWords = 64
+  kTSmall = 7, kTasksMGUs = 8, kTasksMDns = 9, kCtrlWords = 64
 };
 
 constexpr int kMT = 128;     // tokens per MFMA task tile (eight 16-row MFMA tiles)
 constexpr int kMWaves = 8;   // waves per MFMA workgroup, 16 weight rows each
 constexpr int kMN = 16 * kMWaves;  // weight rows per MFMA task tile
 constexpr int kMStages = 3;  // token-tile blocks in flight in LDS per MFMA workgroup
+// Experts with at most kMTs slots (most of them at prefill under Zipf routing) run as a
+// second MFMA launch with kMTs-token tiles and kMWavesS-wave workgroups: several such
+// workgroups share a compute unit, so one's loads, MFMAs and epilogue overlap another's.
+constexpr int kMTs = 32;
+constexpr int kMWavesS = 4;
+constexpr int kMNs = 16 * kMWavesS;
 constexpr int64_t kMfmaMinSlots = 1024;  // automatic path choice: MFMA from this many slots
 
 struct Layout {
@@ -164,6 +170,7 @@ struct MoeArgs {
   int32_t* dbg_dsum;  // [slot][hidden][inter / 256]
   int tiles_gu, tiles_dn;    // row tiles of the VALU kernels
   int tiles_mgu, tiles_mdn;  // row tiles of the MFMA kernels
+  int tiles_mgus, tiles_mdns;  // row tiles of the small-tile MFMA kernels
 };
 
 // ---------------------------------------------------------------------------------
@@ -181,13 +188,14 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
   __shared__ __attribute__((aligned(16))) int s_base[kMaxExperts];  // rank key, then the slot cursor
   __shared__ int s_ebr[kMaxExperts];   // expert of each rank
   __shared__ int s_scan[256], s_scan2[256];
-  __shared__ int s_nact, s_bad;
+  __shared__ int s_nact, s_bad, s_tsmall;
   const int tid = threadIdx.x, E = A.n_experts;
   const int64_t S = A.t * A.topk;
   for (int e = tid; e < E; e += 256) s_cnt[e] = 0;
   if (tid == 0) {
     s_bad = 0;
     s_nact = 0;
+    s_tsmall = 0x7fffffff;
   }
   __syncthreads();
   // The slots' expert ids, kSB per thread at a time, all requested before any is used
@@ -284,6 +292,8 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
   int pos = s_scan[tid] - ns, tpos = s_scan2[tid] - nt;
   for (int r = r0; r < r1; ++r) {
     const int e = s_ebr[r];
+    // in count order the experts of at most kMTs slots form the tail of the tile list
+    if (by_count && s_cnt[e] <= kMTs) atomicMin(&s_tsmall, tpos);
     A.active[r] = e;
     A.act_off[r] = pos;
     A.tt_off[r] = tpos;
@@ -291,16 +301,21 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
     pos += s_cnt[e];
     for (const int t1 = tpos + (s_cnt[e] + kMT - 1) / kMT; tpos < t1; ++tpos) A.tile_exp[tpos] = r;
   }
+  __syncthreads();
   if (tid == 255) {
     const int n_valid = s_scan[255], n_tiles = s_scan2[255];
+    const int t_small = min(s_tsmall, n_tiles);
     A.act_off[n_active] = n_valid;
     A.tt_off[n_active] = n_tiles;
     A.ctrl[kNActive] = n_active;
     A.ctrl[kNValid] = n_valid;
     A.ctrl[kTasksGU] = n_active * A.tiles_gu;
     A.ctrl[kTasksDn] = n_active * A.tiles_dn;
-    A.ctrl[kTasksMGU] = n_tiles * A.tiles_mgu;
-    A.ctrl[kTasksMDn] = n_tiles * A.tiles_mdn;
+    A.ctrl[kTasksMGU] = t_small * A.tiles_mgu;
+    A.ctrl[kTasksMDn] = t_small * A.tiles_mdn;
+    A.ctrl[kTSmall] = t_small;
+    A.ctrl[kTasksMGUs] = (n_tiles - t_small) * A.tiles_mgus;
+    A.ctrl[kTasksMDns] = (n_tiles - t_small) * A.tiles_mdns;
     A.ctrl[kFlags] = s_bad ? 1 : 0;
   }
   __syncthreads();
@@ -699,73 +714,79 @@ __device__ __forceinline__ void mfma_b_fetch(MfmaB<NMAT>& B, const MatRsrc (&mr)
 // 4 (4w + j) .. + 3 (ao: the lane's byte offset from q for this piece at block 0). A piece
 // that is not needed (a sub-tile the task does not compute, or b >= kb) reads the first
 // 16 bytes of the activations in every lane: one cache line instead of 1 KB.
+template <int PW>
 __device__ __forceinline__ void mfma_a_dma(int8_t* sa, const int8_t* q, uint32_t ao, bool live, int b, int kb, int wv,
                                            int j) {
   const uint32_t o = live && b < kb ? ao + (uint32_t)b * 256u : 0u;
-  __builtin_amdgcn_global_load_lds((const void*)(q + o), (lds_ptr)(sa + (wv * 4 + j) * 1024), 16, 0, 0);
+  __builtin_amdgcn_global_load_lds((const void*)(q + o), (lds_ptr)(sa + (wv * PW + j) * 1024), 16, 0, 0);
 }
 
-// Per block and wave: four code pieces and three loads per matrix.
-template <int NMAT>
-constexpr int kMfmaLoadsPerBlock = 4 + 3 * NMAT;
+// Per block and wave: PW code pieces and three loads per matrix.
+template <int NMAT, int PW>
+constexpr int kMfmaLoadsPerBlock = PW + 3 * NMAT;
 
-template <int NMAT>  // 2: gate and up, h = SiLU(g) * u; 1: down, y per slot
-__global__ __launch_bounds__(kMWaves * 64) void k_moe_mfma(MoeArgs A) {
+// NMAT 2: gate and up, h = SiLU(g) * u; 1: down, y per slot. MT tokens x 16 WAVES rows per
+// task; SMALL: the launch for the tail of the tile list (experts of at most kMTs slots).
+template <int NMAT, int MT, int WAVES, bool SMALL>
+__global__ __launch_bounds__(WAVES * 64) void k_moe_mfma(MoeArgs A) {
+  constexpr int MN = 16 * WAVES;        // weight rows per task
+  constexpr int PW = MT / (4 * WAVES);  // 1 KB token pieces (4 token rows) per wave and block
   // one variable per ring stage, and stages chosen at compile time, so that the compiler
   // can tell a stage being filled from the one being read and does not wait for the fill
-  __shared__ __attribute__((aligned(16))) int8_t s_a0[kMT * 256], s_a1[kMT * 256], s_a2[kMT * 256];
-  __shared__ __attribute__((aligned(16))) float s_dall[(kMaxK / 256) * kMT];  // [block][token]
-  __shared__ int s_slot[kMT];
+  __shared__ __attribute__((aligned(16))) int8_t s_a0[MT * 256], s_a1[MT * 256], s_a2[MT * 256];
+  __shared__ __attribute__((aligned(16))) float s_dall[(kMaxK / 256) * MT];  // [block][token]
+  __shared__ int s_slot[MT];
   // per wave: one matrix's block of its 16 rows, the row-coalesced loads rewritten in MFMA
   // lane order; chunks 0-3 of each row in s_bt0, chunks 4-7 in s_bt1 (1 KB per wave each;
   // chunk x of row r at position x ^ ((r >> 2) & 3): the writes and the reads of eight
   // lanes fall in distinct banks). Two arrays, so that each load's chunks and each MFMA
   // operand's chunks lie in one of them.
-  __shared__ __attribute__((aligned(16))) uint8_t s_bt0[kMWaves * 1024], s_bt1[kMWaves * 1024];
-  static_assert(kMT == 128 && kMN == 16 * kMWaves && kMWaves == 8 && kMStages == 3, "tile geometry");
+  __shared__ __attribute__((aligned(16))) uint8_t s_bt0[WAVES * 1024], s_bt1[WAVES * 1024];
+  static_assert(MT % 32 == 0 && PW >= 2 && PW % 2 == 0 && 4 * PW * WAVES == MT && kMStages == 3, "tile geometry");
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int li = lane & 15, g = lane >> 4;
   const int K = NMAT == 2 ? A.hidden : A.inter;
   const int N = NMAT == 2 ? A.inter : A.hidden;
   const int kb = K / 256;
-  const int RT = NMAT == 2 ? A.tiles_mgu : A.tiles_mdn;
-  const int n_tasks = ld_uniform(A.ctrl + (NMAT == 2 ? kTasksMGU : kTasksMDn));
+  const int RT = SMALL ? (NMAT == 2 ? A.tiles_mgus : A.tiles_mdns) : (NMAT == 2 ? A.tiles_mgu : A.tiles_mdn);
+  const int n_tasks = ld_uniform(A.ctrl + (SMALL ? (NMAT == 2 ? kTasksMGUs : kTasksMDns) : (NMAT == 2 ? kTasksMGU : kTasksMDn)));
+  const int tile0 = SMALL ? ld_uniform(A.ctrl + kTSmall) : 0;
   const int8_t* qsrc = NMAT == 2 ? A.xq : A.hq;
   const float* dsrc = NMAT == 2 ? A.xd : A.hd;
   for (int task = blockIdx.x; task < n_tasks; task += gridDim.x) {
     // task = tile * RT + rtile: token tile `tile` (of active expert a) x row tile; the
     // control data was written by the prologue kernel, so it is read through the scalar
     // cache (not queued behind this compute unit's vector loads)
-    const int tile = task / RT, rtile = task - tile * RT;
+    const int tile = tile0 + task / RT, rtile = task - (task / RT) * RT;
     const int a = ld_uniform(A.tile_exp + tile);
     const int ttile = tile - ld_uniform(A.tt_off + a);
     const int64_t e = ld_uniform(A.active + a);
     const int off = ld_uniform(A.act_off + a), cnt = ld_uniform(A.act_off + a + 1) - off;
-    const int m0 = ttile * kMT, nvalid = min(kMT, cnt - m0);
+    const int m0 = ttile * kMT, nvalid = min(MT, cnt - m0);  // (SMALL: one tile, ttile 0)
     const int nsub = (nvalid + 15) / 16;  // 16-token sub-tiles holding valid tokens
     const int ncomp = 2 * ((nsub + 1) / 2);  // sub-tiles computed (in pairs)
     __syncthreads();  // the previous task is done with the ring and s_slot
-    if (threadIdx.x < kMT) s_slot[threadIdx.x] = A.slot_list[off + m0 + min((int)threadIdx.x, nvalid - 1)];
+    if (threadIdx.x < MT) s_slot[threadIdx.x] = A.slot_list[off + m0 + min((int)threadIdx.x, nvalid - 1)];
     __syncthreads();
-    // the lane's direct-to-LDS sources: piece j covers rows 4 (4w + j) .. + 3, the lane
-    // row 4 (4w + j) + (l >> 4) at stored column l & 15, i.e. source column (l & 15) ^ (r & 15);
-    // wave w fills sub-tile w, so a wave past the computed sub-tiles loads nothing
-    uint32_t ap[4];  // (activations address below 2^31 bytes)
+    // the lane's direct-to-LDS sources: piece j covers rows 4 (PW w + j) .. + 3, the lane
+    // row 4 (PW w + j) + (l >> 4) at stored column l & 15, i.e. source column (l & 15) ^ (r & 15);
+    // wave w fills rows 4 PW w .. 4 PW (w + 1) - 1, so a wave past the computed sub-tiles loads nothing
+    uint32_t ap[PW];  // (activations address below 2^31 bytes)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = (wv * 4 + j) * 4 + (lane >> 4);
+    for (int j = 0; j < PW; ++j) {
+      const int r = (wv * PW + j) * 4 + (lane >> 4);
       const int sl = s_slot[r];
       const uint32_t arow = NMAT == 2 ? (uint32_t)(sl / A.topk) : (uint32_t)sl;
       ap[j] = arow * (uint32_t)K + (uint32_t)(((lane & 15) ^ (r & 15)) * 16);
     }
-    const bool alive = wv < ncomp;
+    const bool alive = 4 * PW * wv < 16 * ncomp;
     // every block scale of the tile's computed tokens, once per task
-    for (int i = threadIdx.x; i < 16 * ncomp * kb; i += kMWaves * 64) {
+    for (int i = threadIdx.x; i < 16 * ncomp * kb; i += WAVES * 64) {
       const int t = i / kb, b = i - t * kb, sl = s_slot[t];
-      s_dall[b * kMT + t] = dsrc[(NMAT == 2 ? (int64_t)(sl / A.topk) : (int64_t)sl) * kb + b];
+      s_dall[b * MT + t] = dsrc[(NMAT == 2 ? (int64_t)(sl / A.topk) : (int64_t)sl) * kb + b];
     }
     __syncthreads();
-    const int row0 = rtile * kMN + wv * 16;  // N is a multiple of 256: all 16 rows exist
+    const int row0 = rtile * MN + wv * 16;  // N is a multiple of 256: all 16 rows exist
     const int wrow = row0 + li;
     MatRsrc mr[NMAT];
 #pragma unroll
@@ -773,9 +794,9 @@ __global__ __launch_bounds__(kMWaves * 64) void k_moe_mfma(MoeArgs A) {
       const int p = NMAT == 2 ? m : 2;
       mr[m] = mat_rsrc(A.codes[p] + e * A.stride_codes[p], A.scales[p] + e * A.stride_scales[p], N, kb);
     }
-    float acc[kMT / 16][NMAT][4];
+    float acc[MT / 16][NMAT][4];
 #pragma unroll
-    for (int mt = 0; mt < kMT / 16; ++mt)
+    for (int mt = 0; mt < MT / 16; ++mt)
 #pragma unroll
       for (int m = 0; m < NMAT; ++m)
 #pragma unroll
@@ -789,17 +810,17 @@ __global__ __launch_bounds__(kMWaves * 64) void k_moe_mfma(MoeArgs A) {
     // Block b uses stage b % 3 and weight registers b % 2: the loop runs six blocks a turn.
     MfmaB<NMAT> B0, B1;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) mfma_a_dma(s_a0, qsrc, ap[j], alive, 0, kb, wv, j);
+    for (int j = 0; j < PW; ++j) mfma_a_dma<PW>(s_a0, qsrc, ap[j], alive, 0, kb, wv, j);
     mfma_b_fetch<NMAT>(B0, mr, row0, wrow, kb, lane, 0);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) mfma_a_dma(s_a1, qsrc, ap[j], alive, 1, kb, wv, j);
+    for (int j = 0; j < PW; ++j) mfma_a_dma<PW>(s_a1, qsrc, ap[j], alive, 1, kb, wv, j);
     mfma_b_fetch<NMAT>(B1, mr, row0, wrow, kb, lane, 1);
-    wait_vmcnt<kMfmaLoadsPerBlock<NMAT>>();
+    wait_vmcnt<kMfmaLoadsPerBlock<NMAT, PW>>();
     const auto step = [&](int b, auto stage_c, MfmaB<NMAT>& Bs) {
       constexpr int ST = decltype(stage_c)::value, NS = (ST + 2) % 3;
       const int8_t* const sa = ST == 0 ? s_a0 : (ST == 1 ? s_a1 : s_a2);
       int8_t* const na = NS == 0 ? s_a0 : (NS == 1 ? s_a1 : s_a2);
-      const float* const sd = s_dall + b * kMT;
+      const float* const sd = s_dall + b * MT;
       float sf[NMAT];
       v4i bop[NMAT][2][2];
       uint8_t* const bt0 = s_bt0 + wv * 1024;
@@ -863,12 +884,12 @@ __global__ __launch_bounds__(kMWaves * 64) void k_moe_mfma(MoeArgs A) {
         }
       };
 #pragma unroll
-      for (int mp = 0; mp < kMT / 32; ++mp) {
+      for (int mp = 0; mp < MT / 32; ++mp) {
         v4i aop[2][2][2];
         float4 d4[2];
-        if (mp < 2) {
-          mfma_a_dma(na, qsrc, ap[2 * mp], alive, nb, kb, wv, 2 * mp);
-          mfma_a_dma(na, qsrc, ap[2 * mp + 1], alive, nb, kb, wv, 2 * mp + 1);
+        if (mp < PW / 2) {
+          mfma_a_dma<PW>(na, qsrc, ap[2 * mp], alive, nb, kb, wv, 2 * mp);
+          mfma_a_dma<PW>(na, qsrc, ap[2 * mp + 1], alive, nb, kb, wv, 2 * mp + 1);
         }
         if (2 * mp >= nsub) continue;  // no valid token in this pair
         read_pair(mp, aop, d4);
@@ -888,7 +909,7 @@ __global__ __launch_bounds__(kMWaves * 64) void k_moe_mfma(MoeArgs A) {
                 C[q][m] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[q][c][h], bop[m][c][h], C[q][m], 0, 0, 0);
         // debug stage dump: C = 16 * isum of token row mt * 16 + 4g + v, weight row orow
         if ((NMAT == 2 ? A.dbg_gsum : A.dbg_dsum) != nullptr) {
-          const int orow = rtile * kMN + wv * 16 + li;
+          const int orow = rtile * MN + wv * 16 + li;
 #pragma unroll
           for (int q = 0; q < 2; ++q)
 #pragma unroll
@@ -920,7 +941,7 @@ __global__ __launch_bounds__(kMWaves * 64) void k_moe_mfma(MoeArgs A) {
       // for the next step: block b + 1's loads are in (only block b + 2's may still be in
       // flight). Waiting here, at the end of the step, keeps every reader of those
       // registers after the wait.
-      wait_vmcnt<kMfmaLoadsPerBlock<NMAT>>();
+      wait_vmcnt<kMfmaLoadsPerBlock<NMAT, PW>>();
     };
     using I0 = std::integral_constant<int, 0>;
     using I1 = std::integral_constant<int, 1>;
@@ -942,10 +963,10 @@ __global__ __launch_bounds__(kMWaves * 64) void k_moe_mfma(MoeArgs A) {
       if (b + 6 >= kb) break;
     }
     // output: token tile row mt*16 + 4g + v, weight row orow
-    const int orow = rtile * kMN + wv * 16 + li;
+    const int orow = rtile * MN + wv * 16 + li;
     if (orow < N) {
 #pragma unroll
-      for (int mt = 0; mt < kMT / 16; ++mt)
+      for (int mt = 0; mt < MT / 16; ++mt)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const int t = mt * 16 + 4 * g + v;
@@ -1392,6 +1413,21 @@ static tq_status launch_stage(void* const* events, int stage, F kernel, dim3 gri
   return check_launch(fn);
 }
 
+// A stage of two kernels on one stream (the start event before the first, the stop event
+// after the second).
+template <typename F1, typename F2, typename... Args>
+static tq_status launch_stage2(void* const* events, int stage, F1 k1, dim3 g1, int t1, F2 k2, dim3 g2, int t2,
+                               hipStream_t st, const char* fn, Args... args) {
+  if (events) {
+    hipExtLaunchKernelGGL(k1, g1, dim3(t1), 0, st, (hipEvent_t)events[2 * stage], nullptr, 0, args...);
+    hipExtLaunchKernelGGL(k2, g2, dim3(t2), 0, st, nullptr, (hipEvent_t)events[2 * stage + 1], 0, args...);
+  } else {
+    hipLaunchKernelGGL(k1, g1, dim3(t1), 0, st, args...);
+    hipLaunchKernelGGL(k2, g2, dim3(t2), 0, st, args...);
+  }
+  return check_launch(fn);
+}
+
 // A stage with no kernel of its own on this path: its event pair is recorded back to back.
 static tq_status empty_stage(void* const* events, int stage, hipStream_t st, const char* fn) {
   if (!events) return TQ_OK;
@@ -1541,20 +1577,29 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   const bool mfma = path == TQ_MOE_PATH_MFMA;
   A.tiles_mgu = (ex->inter + kMN - 1) / kMN;
   A.tiles_mdn = (ex->hidden + kMN - 1) / kMN;
+  A.tiles_mgus = (ex->inter + kMNs - 1) / kMNs;
+  A.tiles_mdns = (ex->hidden + kMNs - 1) / kMNs;
   const int64_t max_tiles = S / kMT + max_active;
 #ifndef TQ_MFMA_GRID
 #define TQ_MFMA_GRID (256 * 16)
 #endif
   const unsigned g_mgu = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mgu, TQ_MFMA_GRID);
   const unsigned g_mdn = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mdn, TQ_MFMA_GRID);
+  // (one tile per expert of at most kMTs slots)
+  const unsigned g_mgus = (unsigned)std::min<int64_t>(max_active * A.tiles_mgus, TQ_MFMA_GRID);
+  const unsigned g_mdns = (unsigned)std::min<int64_t>(max_active * A.tiles_mdns, TQ_MFMA_GRID);
   if ((st = launch_stage(events, 0, k_moe_prologue, dim3(nq + 1), 256, stm, fn, x, A)) != TQ_OK) return st;
-  if (mfma) st = launch_stage(events, 1, k_moe_mfma<2>, dim3(g_mgu), kMWaves * 64, stm, fn, A);
+  if (mfma)
+    st = launch_stage2(events, 1, k_moe_mfma<2, kMT, kMWaves, false>, dim3(g_mgu), kMWaves * 64,
+                       k_moe_mfma<2, kMTs, kMWavesS, true>, dim3(g_mgus), kMWavesS * 64, stm, fn, A);
   else st = launch_stage(events, 1, pick_tb<2>(ex->hidden / 256), dim3(g_gu), kTbWaves * 64, stm, fn, A);
   if (st != TQ_OK) return st;
   if ((st = launch_stage(events, 2, k_moe_requant, dim3((unsigned)((hblocks + 31) / 32)), 256, stm, fn, A, hblocks)) !=
       TQ_OK)
     return st;
-  if (mfma) st = launch_stage(events, 3, k_moe_mfma<1>, dim3(g_mdn), kMWaves * 64, stm, fn, A);
+  if (mfma)
+    st = launch_stage2(events, 3, k_moe_mfma<1, kMT, kMWaves, false>, dim3(g_mdn), kMWaves * 64,
+                       k_moe_mfma<1, kMTs, kMWavesS, true>, dim3(g_mdns), kMWavesS * 64, stm, fn, A);
   else st = launch_stage(events, 3, pick_tb<1>(ex->inter / 256), dim3(g_dn), kTbWaves * 64, stm, fn, A);
   if (st != TQ_OK) return st;
   const int64_t nout = t * (ex->hidden / 4);
