@@ -728,7 +728,9 @@ constexpr int kMfmaLoadsPerBlock = PW + 3 * NMAT;
 // NMAT 2: gate and up, h = SiLU(g) * u; 1: down, y per slot. MT tokens x 16 WAVES rows per
 // task; SMALL: the launch for the tail of the tile list (experts of at most kMTs slots).
 template <int NMAT, int MT, int WAVES, bool SMALL>
-__global__ __launch_bounds__(WAVES * 64) void k_moe_mfma(MoeArgs A) {
+// (the small-tile gate/up instance is held to the registers of three waves per SIMD)
+__global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMALL && NMAT == 2 ? 3 : 1))) void k_moe_mfma(
+    MoeArgs A) {
   constexpr int MN = 16 * WAVES;        // weight rows per task
   constexpr int PW = MT / (4 * WAVES);  // 1 KB token pieces (4 token rows) per wave and block
   // one variable per ring stage, and stages chosen at compile time, so that the compiler
@@ -883,16 +885,19 @@ __global__ __launch_bounds__(WAVES * 64) void k_moe_mfma(MoeArgs A) {
           d4[q] = *reinterpret_cast<const float4*>(&sd[mt * 16 + 4 * g]);
         }
       };
+      // the next pair's operands are read from LDS right after the current pair's MFMAs
+      // are issued (into the same registers), so their LDS latency overlaps the current
+      // pair's epilogue
+      v4i aop[2][2][2];
+      float4 d4[2], d4n[2];
+      read_pair(0, aop, d4);
 #pragma unroll
       for (int mp = 0; mp < MT / 32; ++mp) {
-        v4i aop[2][2][2];
-        float4 d4[2];
         if (mp < PW / 2) {
           mfma_a_dma<PW>(na, qsrc, ap[2 * mp], alive, nb, kb, wv, 2 * mp);
           mfma_a_dma<PW>(na, qsrc, ap[2 * mp + 1], alive, nb, kb, wv, 2 * mp + 1);
         }
         if (2 * mp >= nsub) continue;  // no valid token in this pair
-        read_pair(mp, aop, d4);
         v4i C[2][NMAT];
 #pragma unroll
         for (int q = 0; q < 2; ++q)
@@ -907,6 +912,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_moe_mfma(MoeArgs A) {
 #pragma unroll
               for (int m = 0; m < NMAT; ++m)
                 C[q][m] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[q][c][h], bop[m][c][h], C[q][m], 0, 0, 0);
+        if (mp + 1 < MT / 32 && 2 * (mp + 1) < nsub) read_pair(mp + 1, aop, d4n);
         // debug stage dump: C = 16 * isum of token row mt * 16 + 4g + v, weight row orow
         if ((NMAT == 2 ? A.dbg_gsum : A.dbg_dsum) != nullptr) {
           const int orow = rtile * MN + wv * 16 + li;
@@ -937,6 +943,8 @@ __global__ __launch_bounds__(WAVES * 64) void k_moe_mfma(MoeArgs A) {
             acc[mt][m][2] = fmaf(sf[m] * d4[q].z, (float)C[q][m][2], acc[mt][m][2]);
             acc[mt][m][3] = fmaf(sf[m] * d4[q].w, (float)C[q][m][3], acc[mt][m][3]);
           }
+        d4[0] = d4n[0];
+        d4[1] = d4n[1];
       }
       // for the next step: block b + 1's loads are in (only block b + 2's may still be in
       // flight). Waiting here, at the end of the step, keeps every reader of those
