@@ -209,11 +209,13 @@ def test_moe_mfma_forced_batch32(tq, oracle, experts_h4096):
 
 @pytest.mark.parametrize("E,H,I,topk", [(4, 512, 768, 3), (3, 7168, 2048, 2), (9, 2304, 1280, 8), (2, 256, 256, 1),
                                         (5, 4096, 4096, 4), (10, 7168, 2048, 8), (12, 8192, 512, 8),
-                                        (8, 1024, 1792, 8), (9, 256, 2048, 8)])
+                                        (8, 1024, 1792, 8), (9, 256, 2048, 8), (3, 512, 8192, 2),
+                                        (3, 256, 6400, 2), (2, 256, 16384, 1)])
 def test_moe_single_token_shapes(tq, oracle, E, H, I, topk):
     """The single-token path (gate/up, then down with the requant and combine fused) at
-    block counts of 1 to 28 per row: ragged last loads, every slot count up to 8, a
-    duplicated expert."""
+    block counts of 1 to 64 per row: ragged last loads, every slot count up to 8, a
+    duplicated expert, and down rows of 4 and 8 loads per lane (long intermediate rows at
+    one or two slots)."""
     ex, logical = host_experts(tq, oracle, E, H, I, seed=31 + topk)
     rng = np.random.default_rng(32 + topk)
     x = (rng.standard_normal((1, H)) * 3).astype(np.float32)
