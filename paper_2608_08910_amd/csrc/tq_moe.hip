@@ -1061,6 +1061,46 @@ struct T1Lds {
         b(reinterpret_cast<int*>(raw + kT1LdsQ + (kT1LdsQ / 256) * 4)) {}
 };
 
+// The activation quantizer on 16 lanes per 256-block (16 values a lane, lane (l & 15)
+// holding values 16 (l & 15) .. + 15): the same rule as quantize_group32 (absmax by a
+// butterfly over the 16 lanes, d = amax / 127 and inv = 127 / amax by IEEE division,
+// q = rne(x * inv) by the 1.5 * 2^23 add), written to LDS at block blk; the block's d and
+// code sum go to LDS from its first lane. Half the values a lane of the 8-lane form
+// handles, so the block is ready sooner.
+__device__ __forceinline__ void quantize16_to_lds(const float (&x)[16], int blk, int c16, int8_t* s_q, float* s_d,
+                                                  int* s_b, bool store) {
+#pragma clang fp contract(off)
+  float a = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) a = fmaxf(a, fabsf(x[i]));
+  a = group_max_f32(a);
+  a = fmaxf(a, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(a), kDppRowRor8, 0xf, 0xf, false)));
+  int qw[4] = {0, 0, 0, 0};
+  float d = 0.0f;
+  int s = 0;
+  if (a >= 0x1p-100f) {
+    const float inv = 127.0f / a;
+    d = a / 127.0f;
+    constexpr float kMagic = 12582912.0f;  // 1.5 * 2^23
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      uint32_t b[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) b[k] = __float_as_uint(x[4 * m + k] * inv + kMagic);
+      qw[m] = int(__builtin_amdgcn_perm(b[1], b[0], 0x0c0c0400u) | __builtin_amdgcn_perm(b[3], b[2], 0x04000c0cu));
+      s = __builtin_amdgcn_sdot4(qw[m], 0x01010101, s, false);
+    }
+  }
+  s = group_sum_i32(s);
+  s += __builtin_amdgcn_update_dpp(0, s, kDppRowRor8, 0xf, 0xf, false);
+  if (!store) return;
+  *reinterpret_cast<int4*>(s_q + blk * 256 + c16 * 16) = make_int4(qw[0], qw[1], qw[2], qw[3]);
+  if (c16 == 0) {
+    s_d[blk] = d;
+    s_b[blk] = s;
+  }
+}
+
 // Gate/up of one single-token workgroup `wg`: WAVES waves, each owning RPW rows (a power
 // of two) of gate and of up of one slot. x is quantized into LDS while the weight loads
 // are in flight; per load, one integer butterfly forms the exact block sums, and the
@@ -1072,7 +1112,7 @@ __device__ __forceinline__ void t1_gateup_wg(const float* __restrict__ x, const 
                                              T1Lds s) {
   static_assert(RPW == 1 || RPW == 2 || RPW == 4 || RPW == 8, "RPW must be a power of two <= 8");
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int g = lane >> 3, cp = lane & 7, gid = wv * 8 + g;
+  const int g = lane >> 3, cp = lane & 7;
   const int kb = A.hidden / 256, I = A.inter;
   const int j = wg / A.tiles_gu, tile = wg - j * A.tiles_gu;
   const int e = A.topk_idx[j];
@@ -1080,11 +1120,24 @@ __device__ __forceinline__ void t1_gateup_wg(const float* __restrict__ x, const 
   const int64_t ec = valid ? e : 0;
   const int row0 = (tile * WAVES + wv) * RPW;
 
-  // x first (its wait must not queue behind the weights), then every weight load
+  // x first (its wait must not queue behind the weights), then every weight load; a
+  // workgroup quantizes x with 16 lanes per block: block 4 w + (l >> 4) of wave w, values
+  // 16 (l & 15) .. + 15
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, (uint32_t)A.hidden * 4u);
-  float v[32];
-  const bool xw = wv * 8 < kb;  // wave-uniform: the wave has blocks of x to quantize
-  if (xw) buf_load32f(xr, (uint32_t)min(gid, kb - 1), cp, v);
+  const int xb = wv * 4 + (lane >> 4), c16 = lane & 15;
+  float v[16];
+  const bool xw = wv * 4 < kb;  // wave-uniform: the wave has blocks of x to quantize
+  if (xw) {
+    const uint32_t o = ((uint32_t)min(xb, kb - 1) * 256u + (uint32_t)c16 * 16u) * 4u;
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      const u32x4 w4 = __builtin_amdgcn_raw_buffer_load_b128(xr, o + 16u * m, 0, 0);
+      v[4 * m + 0] = __uint_as_float(w4.x);
+      v[4 * m + 1] = __uint_as_float(w4.y);
+      v[4 * m + 2] = __uint_as_float(w4.z);
+      v[4 * m + 3] = __uint_as_float(w4.w);
+    }
+  }
   __builtin_amdgcn_sched_barrier(0);
   const MatRsrc mr[2] = {mat_rsrc(A.codes[0] + ec * A.stride_codes[0], A.scales[0] + ec * A.stride_scales[0], I, kb),
                          mat_rsrc(A.codes[1] + ec * A.stride_codes[1], A.scales[1] + ec * A.stride_scales[1], I, kb)};
@@ -1105,10 +1158,18 @@ __device__ __forceinline__ void t1_gateup_wg(const float* __restrict__ x, const 
   const int lrow = min(row0 + rev_bits<clog2(RPW)>(lane & (RPW - 1)), I - 1);
 #pragma unroll
   for (int m = 0; m < 2; ++m) load_lane_scales<NL>(mr[m], lrow, kb, g, sr[m]);
-  if (xw) quantize_to_lds(v, min(gid, kb - 1), cp, s.q, s.d, s.b, gid < kb);
-  for (int blk = gid + WAVES * 8; blk < kb; blk += WAVES * 8) {
-    buf_load32f(xr, (uint32_t)blk, cp, v);
-    quantize_to_lds(v, blk, cp, s.q, s.d, s.b, true);
+  if (xw) quantize16_to_lds(v, min(xb, kb - 1), c16, s.q, s.d, s.b, xb < kb);
+  for (int blk = xb + WAVES * 4; blk < kb; blk += WAVES * 4) {
+    const uint32_t o = ((uint32_t)blk * 256u + (uint32_t)c16 * 16u) * 4u;
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      const u32x4 w4 = __builtin_amdgcn_raw_buffer_load_b128(xr, o + 16u * m, 0, 0);
+      v[4 * m + 0] = __uint_as_float(w4.x);
+      v[4 * m + 1] = __uint_as_float(w4.y);
+      v[4 * m + 2] = __uint_as_float(w4.z);
+      v[4 * m + 3] = __uint_as_float(w4.w);
+    }
+    quantize16_to_lds(v, blk, c16, s.q, s.d, s.b, true);
   }
   __syncthreads();
   if (stage) {  // stage buffers and the status word, once per call
