@@ -37,7 +37,7 @@ static const char* const kStageNames[kNumStages] = {"prologue", "gate_up", "requ
 // Control words at the start of the workspace.
 enum Ctrl {
   kFlags = 0, kNActive = 1, kTasksGU = 2, kTasksDn = 3, kNValid = 4, kTasksMGU = 5, kTasksMDn = 6,
-  kTSmall = 7, kTasksMGUs = 8, kTasksMDns = 9, kCtrlWords = 64
+  kTSmall = 7, kTasksMGUs = 8, kTasksMDns = 9, kTSingle = 10, kCtrlWords = 64
 };
 
 constexpr int kMT = 128;     // tokens per MFMA task tile (eight 16-row MFMA tiles)
@@ -188,7 +188,7 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
   __shared__ __attribute__((aligned(16))) int s_base[kMaxExperts];  // rank key, then the slot cursor
   __shared__ int s_ebr[kMaxExperts];   // expert of each rank
   __shared__ int s_scan[256], s_scan2[256];
-  __shared__ int s_nact, s_bad, s_tsmall;
+  __shared__ int s_nact, s_bad, s_tsmall, s_tsingle;
   const int tid = threadIdx.x, E = A.n_experts;
   const int64_t S = A.t * A.topk;
   for (int e = tid; e < E; e += 256) s_cnt[e] = 0;
@@ -196,6 +196,7 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
     s_bad = 0;
     s_nact = 0;
     s_tsmall = 0x7fffffff;
+    s_tsingle = 0x7fffffff;
   }
   __syncthreads();
   // The slots' expert ids, kSB per thread at a time, all requested before any is used
@@ -293,7 +294,9 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
   for (int r = r0; r < r1; ++r) {
     const int e = s_ebr[r];
     // in count order the experts of at most kMTs slots form the tail of the tile list
+    // (and the experts of one kMT-token tile the tail of the first launch's tiles)
     if (by_count && s_cnt[e] <= kMTs) atomicMin(&s_tsmall, tpos);
+    if (by_count && s_cnt[e] <= kMT) atomicMin(&s_tsingle, tpos);
     A.active[r] = e;
     A.act_off[r] = pos;
     A.tt_off[r] = tpos;
@@ -314,6 +317,7 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
     A.ctrl[kTasksMGU] = t_small * A.tiles_mgu;
     A.ctrl[kTasksMDn] = t_small * A.tiles_mdn;
     A.ctrl[kTSmall] = t_small;
+    A.ctrl[kTSingle] = min(s_tsingle, t_small);
     A.ctrl[kTasksMGUs] = (n_tiles - t_small) * A.tiles_mgus;
     A.ctrl[kTasksMDns] = (n_tiles - t_small) * A.tiles_mdns;
     A.ctrl[kFlags] = s_bad ? 1 : 0;
@@ -727,7 +731,9 @@ constexpr int kMfmaLoadsPerBlock = PW + 3 * NMAT;
 
 // NMAT 2: gate and up, h = SiLU(g) * u; 1: down, y per slot. MT tokens x 16 WAVES rows per
 // task; SMALL: the launch for the tail of the tile list (experts of at most kMTs slots).
-template <int NMAT, int MT, int WAVES, bool SMALL>
+// DBG: the instance that also writes the debug stage dumps (launched only when they are
+// requested, so that the production instances carry no dump code or its registers).
+template <int NMAT, int MT, int WAVES, bool SMALL, bool DBG>
 // (the small-tile gate/up instance is held to the registers of three waves per SIMD)
 __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMALL && NMAT == 2 ? 3 : 1))) void k_moe_mfma(
     MoeArgs A) {
@@ -736,7 +742,10 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
   // one variable per ring stage, and stages chosen at compile time, so that the compiler
   // can tell a stage being filled from the one being read and does not wait for the fill
   __shared__ __attribute__((aligned(16))) int8_t s_a0[MT * 256], s_a1[MT * 256], s_a2[MT * 256];
-  __shared__ __attribute__((aligned(16))) float s_dall[(kMaxK / 256) * MT];  // [block][token]
+  // [block][token], rows padded by 4 floats: the fill below (consecutive lanes take
+  // consecutive blocks of one token) then writes distinct banks at 16 blocks
+  constexpr int DS = MT + 4;
+  __shared__ __attribute__((aligned(16))) float s_dall[(kMaxK / 256) * DS];
   __shared__ int s_slot[MT];
   // per wave: one matrix's block of its 16 rows, the row-coalesced loads rewritten in MFMA
   // lane order; chunks 0-3 of each row in s_bt0, chunks 4-7 in s_bt1 (1 KB per wave each;
@@ -755,11 +764,27 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
   const int tile0 = SMALL ? ld_uniform(A.ctrl + kTSmall) : 0;
   const int8_t* qsrc = NMAT == 2 ? A.xq : A.hq;
   const float* dsrc = NMAT == 2 ? A.xd : A.hd;
+  // Tiles before t1 (experts of several tiles): task = tile * RT + rtile, so one row tile
+  // of all of an expert's token tiles runs on one XCD (the grid and RT are multiples of
+  // 8, and workgroups go to the XCDs in turn) and its weights are fetched once. From t1
+  // on every expert has one tile; in whole rounds of 8 such tiles, all row tiles of a
+  // token tile run on one XCD, so that its token rows are fetched into one L2 only.
+  const int t1 = SMALL ? tile0 : ld_uniform(A.ctrl + kTSingle);
+  const int n_single = (SMALL ? n_tasks / RT : ld_uniform(A.ctrl + kTSmall) - t1);
+  const int base1 = (t1 - tile0) * RT, full1 = (n_single / 8) * 8 * RT;
   for (int task = blockIdx.x; task < n_tasks; task += gridDim.x) {
-    // task = tile * RT + rtile: token tile `tile` (of active expert a) x row tile; the
-    // control data was written by the prologue kernel, so it is read through the scalar
-    // cache (not queued behind this compute unit's vector loads)
-    const int tile = tile0 + task / RT, rtile = task - (task / RT) * RT;
+    // the control data was written by the prologue kernel, so it is read through the
+    // scalar cache (not queued behind this compute unit's vector loads)
+    int tile, rtile;
+    const int k = task - base1;
+    if (k < 0 || k >= full1) {
+      tile = tile0 + task / RT;
+      rtile = task - (task / RT) * RT;
+    } else {
+      const int x = k & 7, i = k >> 3;  // XCD x's i-th task
+      tile = t1 + x + 8 * (i / RT);
+      rtile = i - (i / RT) * RT;
+    }
     const int a = ld_uniform(A.tile_exp + tile);
     const int ttile = tile - ld_uniform(A.tt_off + a);
     const int64_t e = ld_uniform(A.active + a);
@@ -785,7 +810,7 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
     // every block scale of the tile's computed tokens, once per task
     for (int i = threadIdx.x; i < 16 * ncomp * kb; i += WAVES * 64) {
       const int t = i / kb, b = i - t * kb, sl = s_slot[t];
-      s_dall[b * MT + t] = dsrc[(NMAT == 2 ? (int64_t)(sl / A.topk) : (int64_t)sl) * kb + b];
+      s_dall[b * DS + t] = dsrc[(NMAT == 2 ? (int64_t)(sl / A.topk) : (int64_t)sl) * kb + b];
     }
     __syncthreads();
     const int row0 = rtile * MN + wv * 16;  // N is a multiple of 256: all 16 rows exist
@@ -822,7 +847,7 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
       constexpr int ST = decltype(stage_c)::value, NS = (ST + 2) % 3;
       const int8_t* const sa = ST == 0 ? s_a0 : (ST == 1 ? s_a1 : s_a2);
       int8_t* const na = NS == 0 ? s_a0 : (NS == 1 ? s_a1 : s_a2);
-      const float* const sd = s_dall + b * MT;
+      const float* const sd = s_dall + b * DS;
       float sf[NMAT];
       v4i bop[NMAT][2][2];
       uint8_t* const bt0 = s_bt0 + wv * 1024;
@@ -914,7 +939,7 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
                 C[q][m] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[q][c][h], bop[m][c][h], C[q][m], 0, 0, 0);
         if (mp + 1 < MT / 32 && 2 * (mp + 1) < nsub) read_pair(mp + 1, aop, d4n);
         // debug stage dump: C = 16 * isum of token row mt * 16 + 4g + v, weight row orow
-        if ((NMAT == 2 ? A.dbg_gsum : A.dbg_dsum) != nullptr) {
+        if (DBG && (NMAT == 2 ? A.dbg_gsum : A.dbg_dsum) != nullptr) {
           const int orow = rtile * MN + wv * 16 + li;
 #pragma unroll
           for (int q = 0; q < 2; ++q)
@@ -982,7 +1007,7 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
             const int64_t slot = s_slot[t];
             if constexpr (NMAT == 2) {
               A.h[slot * A.inter + orow] = silu_f32(acc[mt][0][v]) * acc[mt][1][v];
-              if (A.dbg_g != nullptr) {
+              if (DBG && A.dbg_g != nullptr) {
                 A.dbg_g[slot * A.inter + orow] = acc[mt][0][v];
                 A.dbg_u[slot * A.inter + orow] = acc[mt][1][v];
               }
@@ -1658,17 +1683,23 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   const unsigned g_mgus = (unsigned)std::min<int64_t>(max_active * A.tiles_mgus, TQ_MFMA_GRID);
   const unsigned g_mdns = (unsigned)std::min<int64_t>(max_active * A.tiles_mdns, TQ_MFMA_GRID);
   if ((st = launch_stage(events, 0, k_moe_prologue, dim3(nq + 1), 256, stm, fn, x, A)) != TQ_OK) return st;
-  if (mfma)
-    st = launch_stage2(events, 1, k_moe_mfma<2, kMT, kMWaves, false>, dim3(g_mgu), kMWaves * 64,
-                       k_moe_mfma<2, kMTs, kMWavesS, true>, dim3(g_mgus), kMWavesS * 64, stm, fn, A);
+  if (mfma && debug)
+    st = launch_stage2(events, 1, k_moe_mfma<2, kMT, kMWaves, false, true>, dim3(g_mgu), kMWaves * 64,
+                       k_moe_mfma<2, kMTs, kMWavesS, true, true>, dim3(g_mgus), kMWavesS * 64, stm, fn, A);
+  else if (mfma)
+    st = launch_stage2(events, 1, k_moe_mfma<2, kMT, kMWaves, false, false>, dim3(g_mgu), kMWaves * 64,
+                       k_moe_mfma<2, kMTs, kMWavesS, true, false>, dim3(g_mgus), kMWavesS * 64, stm, fn, A);
   else st = launch_stage(events, 1, pick_tb<2>(ex->hidden / 256), dim3(g_gu), kTbWaves * 64, stm, fn, A);
   if (st != TQ_OK) return st;
   if ((st = launch_stage(events, 2, k_moe_requant, dim3((unsigned)((hblocks + 31) / 32)), 256, stm, fn, A, hblocks)) !=
       TQ_OK)
     return st;
-  if (mfma)
-    st = launch_stage2(events, 3, k_moe_mfma<1, kMT, kMWaves, false>, dim3(g_mdn), kMWaves * 64,
-                       k_moe_mfma<1, kMTs, kMWavesS, true>, dim3(g_mdns), kMWavesS * 64, stm, fn, A);
+  if (mfma && debug)
+    st = launch_stage2(events, 3, k_moe_mfma<1, kMT, kMWaves, false, true>, dim3(g_mdn), kMWaves * 64,
+                       k_moe_mfma<1, kMTs, kMWavesS, true, true>, dim3(g_mdns), kMWavesS * 64, stm, fn, A);
+  else if (mfma)
+    st = launch_stage2(events, 3, k_moe_mfma<1, kMT, kMWaves, false, false>, dim3(g_mdn), kMWaves * 64,
+                       k_moe_mfma<1, kMTs, kMWavesS, true, false>, dim3(g_mdns), kMWavesS * 64, stm, fn, A);
   else st = launch_stage(events, 3, pick_tb<1>(ex->inter / 256), dim3(g_dn), kTbWaves * 64, stm, fn, A);
   if (st != TQ_OK) return st;
   const int64_t nout = t * (ex->hidden / 4);
