@@ -836,12 +836,17 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
     // computed, then the wait for block b + 1 (loads complete in issue order).
     // Block b uses stage b % 3 and weight registers b % 2: the loop runs six blocks a turn.
     MfmaB<NMAT> B0, B1;
-#pragma unroll
-    for (int j = 0; j < PW; ++j) mfma_a_dma<PW>(s_a0, qsrc, ap[j], alive, 0, kb, wv, j);
+    // (per block, weights first, then the token pieces: the order the steps issue them in;
+    // the scheduling barriers keep block 0's loads ahead of block 1's, which the wait below
+    // counts on)
     mfma_b_fetch<NMAT>(B0, mr, row0, wrow, kb, lane, 0);
 #pragma unroll
-    for (int j = 0; j < PW; ++j) mfma_a_dma<PW>(s_a1, qsrc, ap[j], alive, 1, kb, wv, j);
+    for (int j = 0; j < PW; ++j) mfma_a_dma<PW>(s_a0, qsrc, ap[j], alive, 0, kb, wv, j);
+    __builtin_amdgcn_sched_barrier(0);
     mfma_b_fetch<NMAT>(B1, mr, row0, wrow, kb, lane, 1);
+#pragma unroll
+    for (int j = 0; j < PW; ++j) mfma_a_dma<PW>(s_a1, qsrc, ap[j], alive, 1, kb, wv, j);
+    __builtin_amdgcn_sched_barrier(0);
     wait_vmcnt<kMfmaLoadsPerBlock<NMAT, PW>>();
     const auto step = [&](int b, auto stage_c, MfmaB<NMAT>& Bs) {
       constexpr int ST = decltype(stage_c)::value, NS = (ST + 2) % 3;
