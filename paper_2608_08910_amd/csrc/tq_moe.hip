@@ -792,8 +792,35 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
     const int m0 = ttile * kMT, nvalid = min(MT, cnt - m0);  // (SMALL: one tile, ttile 0)
     const int nsub = (nvalid + 15) / 16;  // 16-token sub-tiles holding valid tokens
     const int ncomp = 2 * ((nsub + 1) / 2);  // sub-tiles computed (in pairs)
-    __syncthreads();  // the previous task is done with the ring and s_slot
-    if (threadIdx.x < MT) s_slot[threadIdx.x] = A.slot_list[off + m0 + min((int)threadIdx.x, nvalid - 1)];
+    const int row0 = rtile * MN + wv * 16;  // N is a multiple of 256: all 16 rows exist
+    const int wrow = row0 + li;
+    MatRsrc mr[NMAT];
+#pragma unroll
+    for (int m = 0; m < NMAT; ++m) {
+      const int p = NMAT == 2 ? m : 2;
+      mr[m] = mat_rsrc(A.codes[p] + e * A.stride_codes[p], A.scales[p] + e * A.stride_scales[p], N, kb);
+    }
+    __syncthreads();  // the previous task is done with the ring, s_slot and s_dall
+    // Set-up in the order that keeps its round trips short: the slot list first (the token
+    // side waits on it), then the weights of blocks 0 and 1, which need only the expert and
+    // the row tile and so travel while the token side is set up; then, from the slots, the
+    // token pieces of blocks 0 and 1 and the tile's block scales. Loads complete in issue
+    // order, so each wait below covers exactly what precedes it.
+    int my_slot = 0;
+    if (threadIdx.x < MT) my_slot = A.slot_list[off + m0 + min((int)threadIdx.x, nvalid - 1)];
+    __builtin_amdgcn_sched_barrier(0);
+    // blocks 0 and 1 in flight; then per block b (block b's loads are in, block b + 1's may
+    // not be): block b's weights through LDS into MFMA order, block b + 2's weights issued
+    // into the registers just emptied, barrier (every wave's piece of block b is in LDS,
+    // and stage (b + 2) % 3 is no longer read), block b + 2's pieces issued, block b
+    // computed, then the wait for block b + 1 (loads complete in issue order).
+    // Block b uses stage b % 3 and weight registers b % 2: the loop runs six blocks a turn.
+    MfmaB<NMAT> B0, B1;
+    mfma_b_fetch<NMAT>(B0, mr, row0, wrow, kb, lane, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_b_fetch<NMAT>(B1, mr, row0, wrow, kb, lane, 1);
+    __builtin_amdgcn_sched_barrier(0);
+    if (threadIdx.x < MT) s_slot[threadIdx.x] = my_slot;
     __syncthreads();
     // the lane's direct-to-LDS sources: piece j covers rows 4 (PW w + j) .. + 3, the lane
     // row 4 (PW w + j) + (l >> 4) at stored column l & 15, i.e. source column (l & 15) ^ (r & 15);
@@ -807,20 +834,18 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
       ap[j] = arow * (uint32_t)K + (uint32_t)(((lane & 15) ^ (r & 15)) * 16);
     }
     const bool alive = 4 * PW * wv < 16 * ncomp;
+#pragma unroll
+    for (int j = 0; j < PW; ++j) mfma_a_dma<PW>(s_a0, qsrc, ap[j], alive, 0, kb, wv, j);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < PW; ++j) mfma_a_dma<PW>(s_a1, qsrc, ap[j], alive, 1, kb, wv, j);
+    __builtin_amdgcn_sched_barrier(0);
     // every block scale of the tile's computed tokens, once per task
     for (int i = threadIdx.x; i < 16 * ncomp * kb; i += WAVES * 64) {
       const int t = i / kb, b = i - t * kb, sl = s_slot[t];
       s_dall[b * DS + t] = dsrc[(NMAT == 2 ? (int64_t)(sl / A.topk) : (int64_t)sl) * kb + b];
     }
     __syncthreads();
-    const int row0 = rtile * MN + wv * 16;  // N is a multiple of 256: all 16 rows exist
-    const int wrow = row0 + li;
-    MatRsrc mr[NMAT];
-#pragma unroll
-    for (int m = 0; m < NMAT; ++m) {
-      const int p = NMAT == 2 ? m : 2;
-      mr[m] = mat_rsrc(A.codes[p] + e * A.stride_codes[p], A.scales[p] + e * A.stride_scales[p], N, kb);
-    }
     float acc[MT / 16][NMAT][4];
 #pragma unroll
     for (int mt = 0; mt < MT / 16; ++mt)
@@ -828,26 +853,7 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
       for (int m = 0; m < NMAT; ++m)
 #pragma unroll
         for (int v = 0; v < 4; ++v) acc[mt][m][v] = 0.0f;
-
-    // blocks 0 and 1 in flight; then per block b (block b's loads are in, block b + 1's may
-    // not be): block b's weights through LDS into MFMA order, block b + 2's weights issued
-    // into the registers just emptied, barrier (every wave's piece of block b is in LDS,
-    // and stage (b + 2) % 3 is no longer read), block b + 2's pieces issued, block b
-    // computed, then the wait for block b + 1 (loads complete in issue order).
-    // Block b uses stage b % 3 and weight registers b % 2: the loop runs six blocks a turn.
-    MfmaB<NMAT> B0, B1;
-    // (per block, weights first, then the token pieces: the order the steps issue them in;
-    // the scheduling barriers keep block 0's loads ahead of block 1's, which the wait below
-    // counts on)
-    mfma_b_fetch<NMAT>(B0, mr, row0, wrow, kb, lane, 0);
-#pragma unroll
-    for (int j = 0; j < PW; ++j) mfma_a_dma<PW>(s_a0, qsrc, ap[j], alive, 0, kb, wv, j);
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_b_fetch<NMAT>(B1, mr, row0, wrow, kb, lane, 1);
-#pragma unroll
-    for (int j = 0; j < PW; ++j) mfma_a_dma<PW>(s_a1, qsrc, ap[j], alive, 1, kb, wv, j);
-    __builtin_amdgcn_sched_barrier(0);
-    wait_vmcnt<kMfmaLoadsPerBlock<NMAT, PW>>();
+    // (every load above has completed: the block scales were loaded last)
     const auto step = [&](int b, auto stage_c, MfmaB<NMAT>& Bs) {
       constexpr int ST = decltype(stage_c)::value, NS = (ST + 2) % 3;
       const int8_t* const sa = ST == 0 ? s_a0 : (ST == 1 ? s_a1 : s_a2);
