@@ -678,9 +678,9 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 // One block's weights for one wave, per matrix: two 16-byte code chunks per lane as
-// loaded (row-coalesced: load c gives lane l chunk 4c + (l & 3) of the wave's row l >> 2,
-// so four neighbouring lanes read one 64-byte half of a row block), and the scale of the
-// lane's MFMA row l & 15.
+// loaded (row-coalesced: load c gives lane l chunk l & 7 of the wave's row 8c + (l >> 3),
+// so eight neighbouring lanes read one row's whole 128-byte block, one cache line), and
+// the scale of the lane's MFMA row l & 15.
 template <int NMAT>
 struct MfmaB {
   uint4 w[NMAT][2];
@@ -709,7 +709,7 @@ __device__ __forceinline__ void mfma_b_fetch(MfmaB<NMAT>& B, const MatRsrc (&mr)
 #pragma unroll
     for (int c = 0; c < 2; ++c)
       B.w[m][c] = buf_load16(mr[m].codes,
-                             live ? (uint32_t)(((row0 + (lane >> 2)) * kb + b) * 128 + (4 * c + (lane & 3)) * 16) : kOob,
+                             live ? (uint32_t)(((row0 + 8 * c + (lane >> 3)) * kb + b) * 128 + (lane & 7) * 16) : kOob,
                              0, 0);
   }
 }
@@ -747,12 +747,11 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
   constexpr int DS = MT + 4;
   __shared__ __attribute__((aligned(16))) float s_dall[(kMaxK / 256) * DS];
   __shared__ int s_slot[MT];
-  // per wave: one matrix's block of its 16 rows, the row-coalesced loads rewritten in MFMA
-  // lane order; chunks 0-3 of each row in s_bt0, chunks 4-7 in s_bt1 (1 KB per wave each;
-  // chunk x of row r at position x ^ ((r >> 2) & 3): the writes and the reads of eight
-  // lanes fall in distinct banks). Two arrays, so that each load's chunks and each MFMA
-  // operand's chunks lie in one of them.
-  __shared__ __attribute__((aligned(16))) uint8_t s_bt0[WAVES * 1024], s_bt1[WAVES * 1024];
+  // per wave: one matrix's block of its 16 rows (2 KB), the row-coalesced loads rewritten
+  // in MFMA lane order; chunk x of row r at position x ^ ((r >> 1) & 7) of the row, so that
+  // eight lanes writing one row, and eight lanes reading one chunk of eight rows, fall in
+  // distinct banks
+  __shared__ __attribute__((aligned(16))) uint8_t s_bt[WAVES * 2048];
   static_assert(MT % 32 == 0 && PW >= 2 && PW % 2 == 0 && 4 * PW * WAVES == MT && kMStages == 3, "tile geometry");
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int li = lane & 15, g = lane >> 4;
@@ -861,8 +860,7 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
       const float* const sd = s_dall + b * DS;
       float sf[NMAT];
       v4i bop[NMAT][2][2];
-      uint8_t* const bt0 = s_bt0 + wv * 1024;
-      uint8_t* const bt1 = s_bt1 + wv * 1024;
+      uint8_t* const bt = s_bt + wv * 2048;
 #pragma unroll
       for (int m = 0; m < NMAT; ++m) {
         // the MFMA sums 16c * q = 16 isum; dividing the f16 scale by 16 is exact
@@ -870,16 +868,16 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
         // through the wave's own LDS areas into MFMA order: lane (li, g) takes chunks g and
         // 4 + g of row li (LDS accesses of one wave complete in issue order, so the reads
         // see the writes; the fences keep the compiler's order)
-        const int wo = (lane >> 2) * 64 + (((lane & 3) ^ ((lane >> 4) & 3)) * 16);
-        *reinterpret_cast<uint4*>(bt0 + wo) = Bs.w[m][0];
-        *reinterpret_cast<uint4*>(bt1 + wo) = Bs.w[m][1];
+        const int wr = lane >> 3;  // (row wr of the first load, 8 + wr of the second)
+        *reinterpret_cast<uint4*>(bt + wr * 128 + (((lane & 7) ^ ((wr >> 1) & 7)) * 16)) = Bs.w[m][0];
+        *reinterpret_cast<uint4*>(bt + (8 + wr) * 128 + (((lane & 7) ^ (((8 + wr) >> 1) & 7)) * 16)) = Bs.w[m][1];
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
         __builtin_amdgcn_wave_barrier();
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
-        const int ro = li * 64 + ((g ^ ((li >> 2) & 3)) * 16);
+        const int rs = (li >> 1) & 7;
         uint4 wt[2];
-        wt[0] = *reinterpret_cast<const uint4*>(bt0 + ro);
-        wt[1] = *reinterpret_cast<const uint4*>(bt1 + ro);
+        wt[0] = *reinterpret_cast<const uint4*>(bt + li * 128 + ((g ^ rs) * 16));
+        wt[1] = *reinterpret_cast<const uint4*>(bt + li * 128 + (((4 + g) ^ rs) * 16));
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
         __builtin_amdgcn_wave_barrier();
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
