@@ -733,11 +733,17 @@ constexpr int kMfmaLoadsPerBlock = PW + 3 * NMAT;
 // task; SMALL: the launch for the tail of the tile list (experts of at most kMTs slots).
 // DBG: the instance that also writes the debug stage dumps (launched only when they are
 // requested, so that the production instances carry no dump code or its registers).
-template <int NMAT, int MT, int WAVES, bool SMALL, bool DBG>
+// DN2: the down projection with two 16-row tiles of the matrix per wave, run as the two
+// "matrices" of the NMAT = 2 path (the second's resource starts 16 rows on), so that each
+// token operand read from LDS feeds two MFMAs, as in gate/up.
+template <int NMAT, int MT, int WAVES, bool SMALL, bool DBG, bool DN2 = false>
 // (the small-tile gate/up instance is held to the registers of three waves per SIMD)
-__global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMALL && NMAT == 2 ? 3 : 1))) void k_moe_mfma(
+__global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMALL && NMAT == 2 && !DN2 ? 3 : 1))) void k_moe_mfma(
     MoeArgs A) {
-  constexpr int MN = 16 * WAVES;        // weight rows per task
+  static_assert(!DN2 || NMAT == 2, "DN2 runs two row tiles as two matrices");
+  constexpr bool GU = NMAT == 2 && !DN2;  // the gate/up projection
+  constexpr int RW = DN2 ? 32 : 16;       // weight rows per wave
+  constexpr int MN = RW * WAVES;          // weight rows per task
   constexpr int PW = MT / (4 * WAVES);  // 1 KB token pieces (4 token rows) per wave and block
   // one variable per ring stage, and stages chosen at compile time, so that the compiler
   // can tell a stage being filled from the one being read and does not wait for the fill
@@ -755,14 +761,14 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
   static_assert(MT % 32 == 0 && PW >= 2 && PW % 2 == 0 && 4 * PW * WAVES == MT && kMStages == 3, "tile geometry");
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int li = lane & 15, g = lane >> 4;
-  const int K = NMAT == 2 ? A.hidden : A.inter;
-  const int N = NMAT == 2 ? A.inter : A.hidden;
+  const int K = GU ? A.hidden : A.inter;
+  const int N = GU ? A.inter : A.hidden;
   const int kb = K / 256;
-  const int RT = SMALL ? (NMAT == 2 ? A.tiles_mgus : A.tiles_mdns) : (NMAT == 2 ? A.tiles_mgu : A.tiles_mdn);
-  const int n_tasks = ld_uniform(A.ctrl + (SMALL ? (NMAT == 2 ? kTasksMGUs : kTasksMDns) : (NMAT == 2 ? kTasksMGU : kTasksMDn)));
+  const int RT = SMALL ? (GU ? A.tiles_mgus : A.tiles_mdns) : (GU ? A.tiles_mgu : A.tiles_mdn);
+  const int n_tasks = ld_uniform(A.ctrl + (SMALL ? (GU ? kTasksMGUs : kTasksMDns) : (GU ? kTasksMGU : kTasksMDn)));
   const int tile0 = SMALL ? ld_uniform(A.ctrl + kTSmall) : 0;
-  const int8_t* qsrc = NMAT == 2 ? A.xq : A.hq;
-  const float* dsrc = NMAT == 2 ? A.xd : A.hd;
+  const int8_t* qsrc = GU ? A.xq : A.hq;
+  const float* dsrc = GU ? A.xd : A.hd;
   // Tiles before t1 (experts of several tiles): task = tile * RT + rtile, so one row tile
   // of all of an expert's token tiles runs on one XCD (the grid and RT are multiples of
   // 8, and workgroups go to the XCDs in turn) and its weights are fetched once. From t1
@@ -791,13 +797,16 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
     const int m0 = ttile * kMT, nvalid = min(MT, cnt - m0);  // (SMALL: one tile, ttile 0)
     const int nsub = (nvalid + 15) / 16;  // 16-token sub-tiles holding valid tokens
     const int ncomp = 2 * ((nsub + 1) / 2);  // sub-tiles computed (in pairs)
-    const int row0 = rtile * MN + wv * 16;  // N is a multiple of 256: all 16 rows exist
+    const int row0 = rtile * MN + wv * RW;  // N is a multiple of 256: all the wave's rows exist
     const int wrow = row0 + li;
     MatRsrc mr[NMAT];
 #pragma unroll
     for (int m = 0; m < NMAT; ++m) {
-      const int p = NMAT == 2 ? m : 2;
-      mr[m] = mat_rsrc(A.codes[p] + e * A.stride_codes[p], A.scales[p] + e * A.stride_scales[p], N, kb);
+      const int p = GU ? m : 2;
+      // (DN2: the second tile's resource starts 16 rows on)
+      const int64_t r16 = DN2 ? 16 * m : 0;
+      mr[m] = mat_rsrc(A.codes[p] + e * A.stride_codes[p] + r16 * kb * 128, A.scales[p] + e * A.stride_scales[p] + r16 * kb,
+                       N - (int)r16, kb);
     }
     __syncthreads();  // the previous task is done with the ring, s_slot and s_dall
     // Set-up in the order that keeps its round trips short: the slot list first (the token
@@ -829,7 +838,7 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
     for (int j = 0; j < PW; ++j) {
       const int r = (wv * PW + j) * 4 + (lane >> 4);
       const int sl = s_slot[r];
-      const uint32_t arow = NMAT == 2 ? (uint32_t)(sl / A.topk) : (uint32_t)sl;
+      const uint32_t arow = GU ? (uint32_t)(sl / A.topk) : (uint32_t)sl;
       ap[j] = arow * (uint32_t)K + (uint32_t)(((lane & 15) ^ (r & 15)) * 16);
     }
     const bool alive = 4 * PW * wv < 16 * ncomp;
@@ -842,7 +851,7 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
     // every block scale of the tile's computed tokens, once per task
     for (int i = threadIdx.x; i < 16 * ncomp * kb; i += WAVES * 64) {
       const int t = i / kb, b = i - t * kb, sl = s_slot[t];
-      s_dall[b * DS + t] = dsrc[(NMAT == 2 ? (int64_t)(sl / A.topk) : (int64_t)sl) * kb + b];
+      s_dall[b * DS + t] = dsrc[(GU ? (int64_t)(sl / A.topk) : (int64_t)sl) * kb + b];
     }
     __syncthreads();
     float acc[MT / 16][NMAT][4];
@@ -948,8 +957,8 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
                 C[q][m] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop[q][c][h], bop[m][c][h], C[q][m], 0, 0, 0);
         if (mp + 1 < MT / 32 && 2 * (mp + 1) < nsub) read_pair(mp + 1, aop, d4n);
         // debug stage dump: C = 16 * isum of token row mt * 16 + 4g + v, weight row orow
-        if (DBG && (NMAT == 2 ? A.dbg_gsum : A.dbg_dsum) != nullptr) {
-          const int orow = rtile * MN + wv * 16 + li;
+        if (DBG && (GU ? A.dbg_gsum : A.dbg_dsum) != nullptr) {
+          const int orow = rtile * MN + wv * RW + li;
 #pragma unroll
           for (int q = 0; q < 2; ++q)
 #pragma unroll
@@ -957,11 +966,12 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
               const int t = (2 * mp + q) * 16 + 4 * g + v;
               if (t < nvalid && orow < N) {
                 const int64_t o = ((int64_t)s_slot[t] * N + orow) * kb + b;
-                if constexpr (NMAT == 2) {
+                if constexpr (GU) {
                   A.dbg_gsum[o] = C[q][0][v] >> 4;
                   A.dbg_usum[o] = C[q][1][v] >> 4;
                 } else {
-                  A.dbg_dsum[o] = C[q][0][v] >> 4;
+#pragma unroll
+                  for (int m = 0; m < NMAT; ++m) A.dbg_dsum[o + (int64_t)16 * m * kb] = C[q][m][v] >> 4;
                 }
               }
             }
@@ -1004,8 +1014,8 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
       step(b + 5, I2{}, B1);
       if (b + 6 >= kb) break;
     }
-    // output: token tile row mt*16 + 4g + v, weight row orow
-    const int orow = rtile * MN + wv * 16 + li;
+    // output: token tile row mt*16 + 4g + v, weight row orow (DN2: and orow + 16)
+    const int orow = rtile * MN + wv * RW + li;
     if (orow < N) {
 #pragma unroll
       for (int mt = 0; mt < MT / 16; ++mt)
@@ -1014,14 +1024,15 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
           const int t = mt * 16 + 4 * g + v;
           if (t < nvalid) {
             const int64_t slot = s_slot[t];
-            if constexpr (NMAT == 2) {
+            if constexpr (GU) {
               A.h[slot * A.inter + orow] = silu_f32(acc[mt][0][v]) * acc[mt][1][v];
               if (DBG && A.dbg_g != nullptr) {
                 A.dbg_g[slot * A.inter + orow] = acc[mt][0][v];
                 A.dbg_u[slot * A.inter + orow] = acc[mt][1][v];
               }
             } else {
-              A.yd[slot * A.hidden + orow] = acc[mt][0][v];
+#pragma unroll
+              for (int m = 0; m < NMAT; ++m) A.yd[slot * A.hidden + orow + 16 * m] = acc[mt][m][v];
             }
           }
         }
@@ -1679,7 +1690,7 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   // otherwise
   const bool mfma = path == TQ_MOE_PATH_MFMA;
   A.tiles_mgu = (ex->inter + kMN - 1) / kMN;
-  A.tiles_mdn = (ex->hidden + kMN - 1) / kMN;
+  A.tiles_mdn = (ex->hidden + 2 * kMN - 1) / (2 * kMN);  // (two 16-row tiles per wave)
   A.tiles_mgus = (ex->inter + kMNs - 1) / kMNs;
   A.tiles_mdns = (ex->hidden + kMNs - 1) / kMNs;
   const int64_t max_tiles = S / kMT + max_active;
@@ -1704,10 +1715,10 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
       TQ_OK)
     return st;
   if (mfma && debug)
-    st = launch_stage2(events, 3, k_moe_mfma<1, kMT, kMWaves, false, true>, dim3(g_mdn), kMWaves * 64,
+    st = launch_stage2(events, 3, k_moe_mfma<2, kMT, kMWaves, false, true, true>, dim3(g_mdn), kMWaves * 64,
                        k_moe_mfma<1, kMTs, kMWavesS, true, true>, dim3(g_mdns), kMWavesS * 64, stm, fn, A);
   else if (mfma)
-    st = launch_stage2(events, 3, k_moe_mfma<1, kMT, kMWaves, false, false>, dim3(g_mdn), kMWaves * 64,
+    st = launch_stage2(events, 3, k_moe_mfma<2, kMT, kMWaves, false, false, true>, dim3(g_mdn), kMWaves * 64,
                        k_moe_mfma<1, kMTs, kMWavesS, true, false>, dim3(g_mdns), kMWavesS * 64, stm, fn, A);
   else st = launch_stage(events, 3, pick_tb<1>(ex->inter / 256), dim3(g_dn), kTbWaves * 64, stm, fn, A);
   if (st != TQ_OK) return st;
