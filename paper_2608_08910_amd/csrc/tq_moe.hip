@@ -738,7 +738,7 @@ constexpr int kMfmaLoadsPerBlock = PW + 3 * NMAT;
 // token operand read from LDS feeds two MFMAs, as in gate/up.
 template <int NMAT, int MT, int WAVES, bool SMALL, bool DBG, bool DN2 = false>
 // (the small-tile gate/up instance is held to the registers of three waves per SIMD)
-__global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMALL && NMAT == 2 && !DN2 ? 3 : 1))) void k_moe_mfma(
+__global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMALL && NMAT == 2 ? 3 : 1))) void k_moe_mfma(
     MoeArgs A) {
   static_assert(!DN2 || NMAT == 2, "DN2 runs two row tiles as two matrices");
   constexpr bool GU = NMAT == 2 && !DN2;  // the gate/up projection
@@ -1692,7 +1692,7 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   A.tiles_mgu = (ex->inter + kMN - 1) / kMN;
   A.tiles_mdn = (ex->hidden + 2 * kMN - 1) / (2 * kMN);  // (two 16-row tiles per wave)
   A.tiles_mgus = (ex->inter + kMNs - 1) / kMNs;
-  A.tiles_mdns = (ex->hidden + kMNs - 1) / kMNs;
+  A.tiles_mdns = (ex->hidden + 2 * kMNs - 1) / (2 * kMNs);
   const int64_t max_tiles = S / kMT + max_active;
 #ifndef TQ_MFMA_GRID
 #define TQ_MFMA_GRID (256 * 16)
@@ -1716,10 +1716,10 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
     return st;
   if (mfma && debug)
     st = launch_stage2(events, 3, k_moe_mfma<2, kMT, kMWaves, false, true, true>, dim3(g_mdn), kMWaves * 64,
-                       k_moe_mfma<1, kMTs, kMWavesS, true, true>, dim3(g_mdns), kMWavesS * 64, stm, fn, A);
+                       k_moe_mfma<2, kMTs, kMWavesS, true, true, true>, dim3(g_mdns), kMWavesS * 64, stm, fn, A);
   else if (mfma)
     st = launch_stage2(events, 3, k_moe_mfma<2, kMT, kMWaves, false, false, true>, dim3(g_mdn), kMWaves * 64,
-                       k_moe_mfma<1, kMTs, kMWavesS, true, false>, dim3(g_mdns), kMWavesS * 64, stm, fn, A);
+                       k_moe_mfma<2, kMTs, kMWavesS, true, false, true>, dim3(g_mdns), kMWavesS * 64, stm, fn, A);
   else st = launch_stage(events, 3, pick_tb<1>(ex->inter / 256), dim3(g_dn), kTbWaves * 64, stm, fn, A);
   if (st != TQ_OK) return st;
   const int64_t nout = t * (ex->hidden / 4);
