@@ -781,7 +781,7 @@ def run_moe(args, wl, cfg):
         rpw = 8 if nl_gu == 1 else (4 if nl_gu == 2 else (2 if nl_gu <= 4 else 1))
         nt = 2 if nl_gu <= 2 else 1  # tokens per group of the grouped VALU kernel (first, later)
         # the MFMA stage is two launches: 128-token tiles, then the experts of at most 32 slots
-        gu_kernel = ("k_moe_mfma<2, 128, 8, false> + k_moe_mfma<2, 32, 4, true>" if mfma
+        gu_kernel = ("k_moe_mfma<2, 128, 8, false, false, false> + k_moe_mfma<2, 32, 4, true, false, false>" if mfma
                      else f"k_tb<2, {nl_gu}, {rpw}, {nt}, {nt}, 4, {ragged}>")
         kname = "gate_up"
     if mfma:
@@ -809,7 +809,9 @@ def run_moe(args, wl, cfg):
         dn_kernel = f"k_t1_down<{nl4}, {rows}, {topk}, {'true' if (I // 256) % 8 or nl4 * 8 != I // 256 else 'false'}>"
     else:
         dn_bytes = n_distinct * matrix_bytes(H, I) + T * topk * (I + (I // 256) * 4) + T * topk * H * 4
-        dn_kernel = "k_moe_mfma<1, 128, 8, false> + k_moe_mfma<1, 32, 4, true>" if mfma else "k_tb<1, ...>"
+        # (down: two 16-row tiles per wave, run as the kernel's two-matrix path)
+        dn_kernel = ("k_moe_mfma<2, 128, 8, false, false, true> + k_moe_mfma<2, 32, 4, true, false, true>" if mfma
+                     else "k_tb<1, ...>")
     dn_ms = stage_ms["down"]
     down = {
         "kernel_symbol": dn_kernel, "bytes_per_launch": round(dn_bytes), "mean_ms": round(dn_ms, 5),
