@@ -154,7 +154,9 @@ def cpu_baseline(seed: int, hidden: int, inter: int, topk: int, target_s: float 
 WORKLOADS = {
     "decode1": dict(cfg=1, steps=2000, warmup=200, profile=256),
     "decode32": dict(cfg=2, steps=300, warmup=30, profile=64),
-    "prefill2048": dict(cfg=3, steps=10, warmup=2, profile=4),
+    # (a graph's first replay carries about 1 ms of one-time launch cost: enough steps that
+    # it stays near 1% of the timed region)
+    "prefill2048": dict(cfg=3, steps=100, warmup=10, profile=4),
     "stack43": dict(cfg=4, steps=20, warmup=3, profile=2),
     "gemv": dict(cfg=0, steps=4000, warmup=400, profile=512),
     "tiedquant": dict(cfg="quant", steps=64, warmup=8, profile=32),
