@@ -178,6 +178,54 @@ def test_moe_prefill_2048(tq, oracle, experts_h4096):
     assert_debug_flag_neutral(tq, experts_h4096, x, idx, w, out)
 
 
+def test_moe_prefill_2048_paths_agree(tq, experts_h4096):
+    """Every slot and output of the 2048-token prefill layer, MFMA path (the production
+    instances, no debug dump) against the grouped VALU path, which the sampled oracle
+    checks cover on their own: a tile the MFMA task order leaves out, repeats or places on
+    the wrong rows shows up here whichever tokens it holds, as an error of the size of the
+    values themselves. The int32 block dots are exact on both paths, which differ only in
+    the fp32 order of the block-scaled sums:
+      - h of every slot within 1e-5 of the slot's largest |h| (gate/up tiles);
+      - the requantized codes of h equal but for rare one-step flips near a rounding
+        boundary (at most one code in 1e4), with block scales within 1e-6;
+      - yd of every slot whose codes of h came out identical within 1e-5 of the slot's
+        largest |yd| (down tiles); every slot's within 1e-2, since one flip moves a slot's
+        whole row by about a thousandth of its size;
+      - out of every token within 1e-2 of the token's largest output."""
+    c = gen.CONFIGS[3]
+    T, topk, H = c["tokens"], c["topk"], c["hidden"]
+    x = gen.activations(gen.SEED, 0, T, H) * gen.token_factors(gen.SEED, T)[:, None]
+    idx, w = gen.routing(gen.SEED, 0, T, c["experts"], topk, c["routing"])
+    announce("moe prefill t=2048: MFMA path against VALU path, every slot and output")
+
+    def rel(a, b, dim=1):
+        return ((a - b).abs() / b.abs().amax(dim=dim, keepdim=True).clamp_min(1e-30)).amax(dim=dim)
+
+    out_m, ws_m = run_moe(tq, experts_h4096, x, idx, w, debug=False)
+    out_v, ws_v = run_moe(tq, experts_h4096, x, idx, w, flags=tq.TQ_MOE_FORCE_VALU, debug=False)
+    Vm, Vv = ws_views(tq, experts_h4096, ws_m, T, topk), ws_views(tq, experts_h4096, ws_v, T, topk)
+    assert torch.isfinite(out_m).all() and torch.isfinite(Vm["h"]).all()
+    h_rel = rel(Vm["h"], Vv["h"]).max().item()
+    dq = Vm["hq"].int() - Vv["hq"].int()
+    n_flip = int((dq != 0).sum().item())
+    hd_rel = ((Vm["hd"] - Vv["hd"]).abs() / Vv["hd"].abs().clamp_min(1e-30)).max().item()
+    clean = (dq != 0).sum(dim=1).eq(0)
+    yd_rel = rel(Vm["yd"], Vv["yd"])
+    yd_clean, yd_all = yd_rel[clean].max().item(), yd_rel.max().item()
+    out_rel = rel(out_m, out_v).max().item()
+    msg = (f"MFMA vs VALU path: h {h_rel:.3g}; {n_flip} code flips (max step {dq.abs().max().item()}), "
+           f"hd {hd_rel:.3g}; yd {yd_clean:.3g} on {int(clean.sum())} clean slots of {clean.numel()}, "
+           f"{yd_all:.3g} on all; out {out_rel:.3g}")
+    print(msg)
+    assert h_rel <= 1e-5, msg
+    assert dq.abs().max().item() <= 1 and n_flip <= 1e-4 * dq.numel(), msg
+    assert hd_rel <= 1e-6, msg
+    assert yd_clean <= 1e-5 and yd_all <= 1e-2, msg
+    assert out_rel <= 1e-2, msg
+    del out_m, out_v, ws_m, ws_v, Vm, Vv, dq, yd_rel
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("E,H,I,T,topk", [(5, 512, 768, 150, 3), (4, 1280, 256, 70, 2)])
 def test_moe_mfma_forced_small(tq, oracle, E, H, I, T, topk):
     """The int8 MFMA expert path on host-packed experts: one expert spans several
