@@ -793,7 +793,9 @@ def run_moe(args, wl, cfg):
                 "unit": "TOP/s", "frac": round(achieved / MFMA_I8_PEAK_TOPS, 4), "traffic": recorded_traffic(gu_kernel),
                 "ops_per_launch": gu_ops, "bytes_per_launch": round(gu_bytes), "mean_ms": round(gu_ms, 5),
                 "hbm_GBps": round(gu_bytes / (gu_ms * 1e-3) / 1e9, 1), "kernel_symbol": gu_kernel,
-                "frac_timing": "hip events: the kernel's own start/stop timestamps, mean over the per-kernel pass"}
+                "frac_timing": "hip events recorded on the stream before the fork and after the join of the "
+                               "stage's two launches, which run side by side on two streams (the span of both, "
+                               "event commands included); mean over the per-kernel pass"}
         avg_ns = _recorded(gu_kernel, "average_ns", kind="kernel_stats")
         if avg_ns is not None:
             roof["rocprof_mean_ms"] = round(avg_ns * 1e-6, 5)

@@ -320,6 +320,13 @@ tq_status tq_gemv_mx_timed(const tq_mat_mx* w, const int8_t* q, const float* d, 
  * own unless TQ_MOE_FORCE_MFMA is given (tq_moe_path). The grouped paths address the
  * quantized activations with 32-bit offsets: TQ_ERR_INVALID if t * topk * max(hidden,
  * inter) >= 2^31 (and t > 1 or TQ_MOE_FORCE_MFMA).
+ * Streams: every launch follows the work queued on `stream`, and work queued on `stream`
+ * after the call follows every launch. The grouped MFMA path runs each projection as two
+ * launches that write disjoint outputs, the second on a stream the library owns (one per
+ * device, default priority, created by the first such call on the device that is not
+ * made under stream capture), forked from and joined back to `stream` by events; under
+ * capture the fork and join become graph edges. Until that stream exists, or if it
+ * could not be created, the two launches run in order on `stream`.
  * TQ_MOE_DEBUG_STAGES (may be or-ed with either): the same kernels, each taking one
  * extra branch on a kernel argument, also leave in the workspace, past the stage buffers,
  * every routed slot's g and u (fp32) and the exact int32 block sums of its gate, up and
@@ -389,10 +396,12 @@ tq_status tq_moe_workspace_layout(const tq_experts* ex, int64_t t, int32_t topk,
 /* As tq_moe_grouped, and also times each stage with host-created HIP events
  * (hipEvent_t, passed as void*): events[2*i] and events[2*i + 1] bracket stage i, for
  * i < tq_moe_stage_count(). A stage's kernel is launched with hipExtLaunchKernelGGL, so
- * its pair carries that kernel's own start and stop timestamps; a stage with no kernel
- * on the path taken (a single-token step fuses the prologue, requant and combine into
- * its two kernels) has its pair recorded back to back. For per-stage timing in
- * benchmarks; no event may be NULL. */
+ * its pair carries that kernel's own start and stop timestamps; a grouped MFMA stage run
+ * as two launches on two streams has its pair recorded on `stream` before the fork and
+ * after the join (it spans both launches, and the event commands' own cost); a stage
+ * with no kernel on the path taken (a single-token step fuses the prologue, requant and
+ * combine into its two kernels) has its pair recorded back to back. For per-stage timing
+ * in benchmarks; no event may be NULL. */
 int32_t tq_moe_stage_count(void);
 const char* tq_moe_stage_name(int32_t i);
 tq_status tq_moe_grouped_timed(const tq_experts* ex, const float* x, int64_t t,

@@ -1551,6 +1551,81 @@ static tq_status empty_stage(void* const* events, int stage, hipStream_t st, con
   return TQ_OK;
 }
 
+constexpr int kMaxDevices = 64;
+
+// The grouped MFMA path's second stream. Each projection runs as two launches that touch
+// disjoint outputs (the 128-token tiles of the experts of more than kMTs slots, and the
+// experts of at most kMTs slots): the first is bound by MFMA issue and LDS operand reads,
+// the second by its weight stream, so the second runs beside the first on a stream the
+// library owns (one per device, default priority), forked from the caller's stream and
+// joined back to it by events. It is created by the first grouped MFMA call on a device
+// that is not being captured; until then, or if creating it failed, both launches run in
+// order on the caller's stream. `mu` serializes the fork-launch-join sequences of
+// callers on different host threads, which share the two events.
+struct SideStream {
+  std::mutex mu;
+  bool tried = false;
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+  int cus = 0;  // compute units of the device
+};
+static SideStream g_side[kMaxDevices];
+
+static SideStream* side_stream(hipStream_t st) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  SideStream& ss = g_side[dev];
+  std::lock_guard<std::mutex> lock(ss.mu);
+  if (!ss.tried) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(st, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) {
+      (void)hipGetLastError();
+      return nullptr;  // (no stream or event is created inside a capture)
+    }
+    ss.tried = true;
+    const bool ok = hipDeviceGetAttribute(&ss.cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+                    ss.cus >= 8 && hipStreamCreateWithFlags(&ss.s, hipStreamNonBlocking) == hipSuccess &&
+                    hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming) == hipSuccess &&
+                    hipEventCreateWithFlags(&ss.join, hipEventDisableTiming) == hipSuccess;
+    if (!ok) {
+      if (ss.join) (void)hipEventDestroy(ss.join);
+      if (ss.fork) (void)hipEventDestroy(ss.fork);
+      if (ss.s) (void)hipStreamDestroy(ss.s);
+      ss.s = nullptr;
+      ss.fork = ss.join = nullptr;
+      (void)hipGetLastError();
+    }
+  }
+  return ss.s ? &ss : nullptr;
+}
+
+// A stage of two independent kernels: k1 on `st`, k2 on the side stream, both after the
+// work queued on `st` so far, with `st` waiting for both before anything queued after.
+// With timing events the stage's pair is recorded on `st` before the fork and after the
+// join (it spans both launches). Without a side stream: launch_stage2.
+template <typename F1, typename F2, typename... Args>
+static tq_status launch_pair(void* const* events, int stage, SideStream* ss, F1 k1, dim3 g1, int t1, F2 k2, dim3 g2,
+                             int t2, hipStream_t st, const char* fn, Args... args) {
+  if (!ss) return launch_stage2(events, stage, k1, g1, t1, k2, g2, t2, st, fn, args...);
+  std::lock_guard<std::mutex> lock(ss->mu);
+  if (events && hipEventRecord((hipEvent_t)events[2 * stage], st) != hipSuccess)
+    return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
+  if (hipEventRecord(ss->fork, st) != hipSuccess || hipStreamWaitEvent(ss->s, ss->fork, 0) != hipSuccess)
+    return fail(TQ_ERR_DEVICE, "%s: fork to the side stream failed", fn);
+  hipLaunchKernelGGL(k1, g1, dim3(t1), 0, st, args...);
+  hipLaunchKernelGGL(k2, g2, dim3(t2), 0, ss->s, args...);
+  tq_status r = check_launch(fn);
+  if (hipEventRecord(ss->join, ss->s) != hipSuccess || hipStreamWaitEvent(st, ss->join, 0) != hipSuccess)
+    return fail(TQ_ERR_DEVICE, "%s: join from the side stream failed", fn);
+  if (r != TQ_OK) return r;
+  if (events && hipEventRecord((hipEvent_t)events[2 * stage + 1], st) != hipSuccess)
+    return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
+  return TQ_OK;
+}
+
 static tq_status validate_experts(const tq_experts* ex, const char* fn) {
   if (!ex) return fail(TQ_ERR_INVALID, "%s: null experts descriptor", fn);
   if (ex->n_experts < 1 || ex->n_experts > kMaxExperts)
@@ -1697,17 +1772,22 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
 #ifndef TQ_MFMA_GRID
 #define TQ_MFMA_GRID (256 * 16)
 #endif
-  const unsigned g_mgu = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mgu, TQ_MFMA_GRID);
-  const unsigned g_mdn = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mdn, TQ_MFMA_GRID);
+  // Beside the small-tile launch, the 128-token launch keeps five eighths of the compute
+  // units (a multiple of 8 workgroups, one per unit, striding over the tasks); the other
+  // units run the small tiles, and so do the first ones as they free up.
+  SideStream* ss = mfma ? side_stream(stm) : nullptr;
+  const int64_t big_cap = ss ? std::max(8, ss->cus * 5 / 8 / 8 * 8) : TQ_MFMA_GRID;
+  const unsigned g_mgu = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mgu, big_cap);
+  const unsigned g_mdn = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mdn, big_cap);
   // (one tile per expert of at most kMTs slots)
   const unsigned g_mgus = (unsigned)std::min<int64_t>(max_active * A.tiles_mgus, TQ_MFMA_GRID);
   const unsigned g_mdns = (unsigned)std::min<int64_t>(max_active * A.tiles_mdns, TQ_MFMA_GRID);
   if ((st = launch_stage(events, 0, k_moe_prologue, dim3(nq + 1), 256, stm, fn, x, A)) != TQ_OK) return st;
   if (mfma && debug)
-    st = launch_stage2(events, 1, k_moe_mfma<2, kMT, kMWaves, false, true>, dim3(g_mgu), kMWaves * 64,
+    st = launch_pair(events, 1, ss, k_moe_mfma<2, kMT, kMWaves, false, true>, dim3(g_mgu), kMWaves * 64,
                        k_moe_mfma<2, kMTs, kMWavesS, true, true>, dim3(g_mgus), kMWavesS * 64, stm, fn, A);
   else if (mfma)
-    st = launch_stage2(events, 1, k_moe_mfma<2, kMT, kMWaves, false, false>, dim3(g_mgu), kMWaves * 64,
+    st = launch_pair(events, 1, ss, k_moe_mfma<2, kMT, kMWaves, false, false>, dim3(g_mgu), kMWaves * 64,
                        k_moe_mfma<2, kMTs, kMWavesS, true, false>, dim3(g_mgus), kMWavesS * 64, stm, fn, A);
   else st = launch_stage(events, 1, pick_tb<2>(ex->hidden / 256), dim3(g_gu), kTbWaves * 64, stm, fn, A);
   if (st != TQ_OK) return st;
@@ -1715,10 +1795,10 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
       TQ_OK)
     return st;
   if (mfma && debug)
-    st = launch_stage2(events, 3, k_moe_mfma<2, kMT, kMWaves, false, true, true>, dim3(g_mdn), kMWaves * 64,
+    st = launch_pair(events, 3, ss, k_moe_mfma<2, kMT, kMWaves, false, true, true>, dim3(g_mdn), kMWaves * 64,
                        k_moe_mfma<2, kMTs, kMWavesS, true, true, true>, dim3(g_mdns), kMWavesS * 64, stm, fn, A);
   else if (mfma)
-    st = launch_stage2(events, 3, k_moe_mfma<2, kMT, kMWaves, false, false, true>, dim3(g_mdn), kMWaves * 64,
+    st = launch_pair(events, 3, ss, k_moe_mfma<2, kMT, kMWaves, false, false, true>, dim3(g_mdn), kMWaves * 64,
                        k_moe_mfma<2, kMTs, kMWavesS, true, false, true>, dim3(g_mdns), kMWavesS * 64, stm, fn, A);
   else st = launch_stage(events, 3, pick_tb<1>(ex->inter / 256), dim3(g_dn), kTbWaves * 64, stm, fn, A);
   if (st != TQ_OK) return st;
@@ -1780,7 +1860,6 @@ extern "C" tq_status tq_moe_grouped(const tq_experts* ex, const float* x, int64_
 namespace tq {
 
 constexpr size_t kNoAllocScratchBytes = size_t(16) << 20;
-constexpr int kMaxDevices = 64;
 
 static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
 
