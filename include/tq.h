@@ -353,7 +353,10 @@ size_t tq_moe_workspace_bytes(const tq_experts* ex, int64_t t, int32_t topk);
  * inter 2048. Every call on a GPU shares that GPU's array, and the array keeps the last
  * call's stage buffers (readable at the offsets of tq_moe_workspace_layout only by the
  * library): calls that may overlap on one GPU (other streams, other threads) race and
- * must be ordered by the caller. No part of the array needs clearing between calls. */
+ * must be ordered by the caller. No part of the array needs clearing between calls. It
+ * creates no stream or event either: the grouped MFMA path's second stream (see
+ * tq_moe_grouped) serves it once an earlier tq_moe_grouped call on the device made one;
+ * until then its two launches per projection run in order on `stream`. */
 size_t tq_moe_noalloc_max_bytes(void);
 tq_status tq_moe_grouped_noalloc(const tq_experts* ex, const float* x, int64_t t, const int32_t* topk_idx,
                                  const float* topk_w, int32_t topk, float* out, int32_t flags, void* stream);

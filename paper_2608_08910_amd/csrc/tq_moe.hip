@@ -1559,8 +1559,9 @@ constexpr int kMaxDevices = 64;
 // the second by its weight stream, so the second runs beside the first on a stream the
 // library owns (one per device, default priority), forked from the caller's stream and
 // joined back to it by events. It is created by the first grouped MFMA call on a device
-// that is not being captured; until then, or if creating it failed, both launches run in
-// order on the caller's stream. `mu` serializes the fork-launch-join sequences of
+// that is not being captured and may allocate (tq_moe_grouped_noalloc uses it only once
+// it exists); until then, or if creating it failed, both launches run in order on the
+// caller's stream. `mu` serializes the fork-launch-join sequences of
 // callers on different host threads, which share the two events.
 struct SideStream {
   std::mutex mu;
@@ -1571,7 +1572,7 @@ struct SideStream {
 };
 static SideStream g_side[kMaxDevices];
 
-static SideStream* side_stream(hipStream_t st) {
+static SideStream* side_stream(hipStream_t st, bool may_create) {
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
     (void)hipGetLastError();
@@ -1580,6 +1581,7 @@ static SideStream* side_stream(hipStream_t st) {
   SideStream& ss = g_side[dev];
   std::lock_guard<std::mutex> lock(ss.mu);
   if (!ss.tried) {
+    if (!may_create) return nullptr;
     hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
     if (hipStreamIsCapturing(st, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) {
       (void)hipGetLastError();
@@ -1660,7 +1662,7 @@ static int choose_path(const tq_experts* ex, int64_t t, int32_t topk, int32_t fl
 
 static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const int32_t* topk_idx,
                          const float* topk_w, int32_t topk, float* out, void* ws, size_t ws_bytes, int32_t flags,
-                         void* stream, void* const* events, const char* fn) {
+                         void* stream, void* const* events, const char* fn, bool may_allocate = true) {
   clear_error();
   tq_status st = validate_experts(ex, fn);
   if (st != TQ_OK) return st;
@@ -1775,7 +1777,7 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   // Beside the small-tile launch, the 128-token launch keeps five eighths of the compute
   // units (a multiple of 8 workgroups, one per unit, striding over the tasks); the other
   // units run the small tiles, and so do the first ones as they free up.
-  SideStream* ss = mfma ? side_stream(stm) : nullptr;
+  SideStream* ss = mfma ? side_stream(stm, may_allocate) : nullptr;
   const int64_t big_cap = ss ? std::max(8, ss->cus * 5 / 8 / 8 * 8) : TQ_MFMA_GRID;
   const unsigned g_mgu = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mgu, big_cap);
   const unsigned g_mdn = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mdn, big_cap);
@@ -1908,7 +1910,8 @@ extern "C" tq_status tq_moe_grouped_noalloc(const tq_experts* ex, const float* x
                 fn, need, kNoAllocScratchBytes);
   void* ws = nullptr;
   if ((st = scratch_ptr(&ws, fn)) != TQ_OK) return st;
-  return moe_run(ex, x, t, topk_idx, topk_w, topk, out, ws, kNoAllocScratchBytes, flags, stream, nullptr, fn);
+  return moe_run(ex, x, t, topk_idx, topk_w, topk, out, ws, kNoAllocScratchBytes, flags, stream, nullptr, fn,
+                 /*may_allocate=*/false);
 }
 
 extern "C" int32_t tq_moe_path(const tq_experts* ex, int64_t t, int32_t topk, int32_t flags) {
