@@ -792,6 +792,8 @@ def run_moe(args, wl, cfg):
         # the MFMA stage is two launches: 128-token tiles, then the experts of at most 32 slots
         gu_kernel = ("k_moe_mfma<2, 128, 8, false, false, false> + k_moe_mfma<2, 32, 4, true, false, false>" if mfma
                      else f"k_tb<2, {nl_gu}, {rpw}, {nt}, {nt}, 4, {ragged}>")
+        if path == tq.TQ_MOE_PATH_MIXED:  # the hot experts' 32-token MFMA tiles beside it
+            gu_kernel += " + k_moe_mfma<2, 32, 4, true, false, false>"
         kname = "gate_up"
     if mfma:
         gu_ops = 2.0 * T * topk * (2 * I * H)  # int8 multiply-adds of gate and up, 2 ops each
@@ -809,6 +811,10 @@ def run_moe(args, wl, cfg):
             roof["frac_rocprof"] = round(gu_ops / (avg_ns * 1e-9) / 1e12 / MFMA_I8_PEAK_TOPS, 4)
     else:
         roof = hbm_roof(kname, gu_bytes, gu_ms, gu_kernel)
+        if path == tq.TQ_MOE_PATH_MIXED:
+            roof["frac_timing"] = ("hip events recorded on the stream before the fork and after the join of the "
+                                   "stage's two launches (the VALU kernel, and beside it on a second stream the "
+                                   "32-token MFMA tiles of the experts of 9 to 32 slots); mean over the per-kernel pass")
     # the down kernel beside it: the routed experts' down planes, h in (fp32 per slot on the
     # single-token path, which requantizes it itself; int8 + scale per block otherwise),
     # the output (or the per-slot rows) out
@@ -823,6 +829,8 @@ def run_moe(args, wl, cfg):
         # (down: two 16-row tiles per wave, run as the kernel's two-matrix path)
         dn_kernel = ("k_moe_mfma<2, 128, 8, false, false, true> + k_moe_mfma<2, 32, 4, true, false, true>" if mfma
                      else "k_tb<1, ...>")
+        if path == tq.TQ_MOE_PATH_MIXED:
+            dn_kernel += " + k_moe_mfma<2, 32, 4, true, false, true>"
     dn_ms = stage_ms["down"]
     down = {
         "kernel_symbol": dn_kernel, "bytes_per_launch": round(dn_bytes), "mean_ms": round(dn_ms, 5),
@@ -844,7 +852,7 @@ def run_moe(args, wl, cfg):
     config = {"workload": cfg["name"], "layers": L, "experts": E, "hidden": H, "inter": I, "tokens_per_step": T,
               "topk": topk, "routing": routing_desc, "bits_per_weight": 4.0625,
               "resident_expert_bytes": L * E * bytes_expert,
-              "path": {0: "single_token", 1: "valu", 2: "mfma"}[path]}
+              "path": {0: "single_token", 1: "valu", 2: "mfma", 3: "mixed_valu_mfma"}[path]}
     extra = {"stage_ms": {k: (None if v is None else round(v, 5)) for k, v in stage_ms.items()},
              "down_kernel": down, "stream_ceiling": ceiling,
              "bytes_per_token": round(alg_bytes / (K * T)),

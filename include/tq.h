@@ -315,16 +315,18 @@ tq_status tq_gemv_mx_timed(const tq_mat_mx* w, const int8_t* q, const float* d, 
  * described by tq_moe_workspace_layout (for staged parity checks). Calls that share a
  * workspace must be ordered on one stream.
  * flags: 0 (automatic path choice), or TQ_MOE_FORCE_VALU / TQ_MOE_FORCE_MFMA to pin
- * the per-expert path (VALU dot4 for few tokens per expert, int8 MFMA for many).
+ * the per-expert path (VALU dot4 for few tokens per expert, int8 MFMA for many; the
+ * automatic choice mixes the two below 1024 slots, see tq_moe_path).
  * Single-token steps (t == 1, topk <= 8, topk * inter <= 16384) take a path of their
  * own unless TQ_MOE_FORCE_MFMA is given (tq_moe_path). The grouped paths address the
  * quantized activations with 32-bit offsets: TQ_ERR_INVALID if t * topk * max(hidden,
  * inter) >= 2^31 (and t > 1 or TQ_MOE_FORCE_MFMA).
  * Streams: every launch follows the work queued on `stream`, and work queued on `stream`
- * after the call follows every launch. The grouped MFMA path runs each projection as two
- * launches that write disjoint outputs, the second on a stream the library owns (one per
- * device, default priority, created by the first such call on the device that is not
- * made under stream capture), forked from and joined back to `stream` by events; under
+ * after the call follows every launch. The grouped MFMA and mixed paths run each
+ * projection as two launches that write disjoint outputs, the second on a stream the
+ * library owns (one per device, default priority, created by the first such call on the
+ * device that is not made under stream capture), forked from and joined back to
+ * `stream` by events; under
  * capture the fork and join become graph edges. Until that stream exists, or if it
  * could not be created, the two launches run in order on `stream`.
  * TQ_MOE_DEBUG_STAGES (may be or-ed with either): the same kernels, each taking one
@@ -364,11 +366,15 @@ tq_status tq_moe_grouped_noalloc(const tq_experts* ex, const float* x, int64_t t
 /* The path tq_moe_grouped takes for these arguments: TQ_MOE_PATH_T1 (single token: a
  * gate/up kernel, then a down kernel with the requantization and the weighted combine
  * fused), TQ_MOE_PATH_VALU (dispatch + grouped VALU dot4 kernels), TQ_MOE_PATH_MFMA
- * (dispatch + grouped int8 MFMA kernels); -1 if the arguments are invalid. Host only, no
- * device work. */
+ * (dispatch + grouped int8 MFMA kernels), TQ_MOE_PATH_MIXED (the automatic choice for
+ * fewer than 1024 slots and more than 8 tokens: dispatch + the grouped VALU kernels for
+ * the experts of at most 8 or more than 32 slots, and beside them the 32-token MFMA
+ * kernels for the experts of 9 to 32 slots, on the second stream described at
+ * tq_moe_grouped); -1 if the arguments are invalid. Host only, no device work. */
 #define TQ_MOE_PATH_T1 0
 #define TQ_MOE_PATH_VALU 1
 #define TQ_MOE_PATH_MFMA 2
+#define TQ_MOE_PATH_MIXED 3
 int32_t tq_moe_path(const tq_experts* ex, int64_t t, int32_t topk, int32_t flags);
 
 /* Byte offsets, inside the workspace, of the stage buffers tq_moe_grouped leaves behind

@@ -37,7 +37,7 @@ static const char* const kStageNames[kNumStages] = {"prologue", "gate_up", "requ
 // Control words at the start of the workspace.
 enum Ctrl {
   kFlags = 0, kNActive = 1, kTasksGU = 2, kTasksDn = 3, kNValid = 4, kTasksMGU = 5, kTasksMDn = 6,
-  kTSmall = 7, kTasksMGUs = 8, kTasksMDns = 9, kTSingle = 10, kCtrlWords = 64
+  kTSmall = 7, kTasksMGUs = 8, kTasksMDns = 9, kTSingle = 10, kR32 = 11, kRSkip = 12, kCtrlWords = 64
 };
 
 constexpr int kMT = 128;     // tokens per MFMA task tile (eight 16-row MFMA tiles)
@@ -51,6 +51,13 @@ constexpr int kMTs = 32;
 constexpr int kMWavesS = 4;
 constexpr int kMNs = 16 * kMWavesS;
 constexpr int64_t kMfmaMinSlots = 1024;  // automatic path choice: MFMA from this many slots
+// Mixed path (automatic choice below kMfmaMinSlots slots, more than kHybMin tokens): the
+// experts of more than kHybMin and at most kMTs slots run on the kMTs-token MFMA kernel
+// beside the grouped VALU kernel, which takes the others. On the VALU kernel such an
+// expert's task walks its tokens two at a time, every group's activation loads queued
+// behind the compute unit's weight loads; on MFMA its tokens share one pass over the
+// weights.
+constexpr int kHybMin = 8;
 
 struct Layout {
   size_t ctrl, active, act_off, tt_off, tile_exp, slot_list, xq, xd, xb, h, hq, hd, hb, yd, total;
@@ -171,6 +178,7 @@ struct MoeArgs {
   int tiles_gu, tiles_dn;    // row tiles of the VALU kernels
   int tiles_mgu, tiles_mdn;  // row tiles of the MFMA kernels
   int tiles_mgus, tiles_mdns;  // row tiles of the small-tile MFMA kernels
+  int hyb;  // mixed path: experts of more than hyb and at most kMTs slots go to MFMA (0: off)
 };
 
 // ---------------------------------------------------------------------------------
@@ -188,7 +196,7 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
   __shared__ __attribute__((aligned(16))) int s_base[kMaxExperts];  // rank key, then the slot cursor
   __shared__ int s_ebr[kMaxExperts];   // expert of each rank
   __shared__ int s_scan[256], s_scan2[256];
-  __shared__ int s_nact, s_bad, s_tsmall, s_tsingle;
+  __shared__ int s_nact, s_bad, s_tsmall, s_tsingle, s_r32, s_rhot, s_thot;
   const int tid = threadIdx.x, E = A.n_experts;
   const int64_t S = A.t * A.topk;
   for (int e = tid; e < E; e += 256) s_cnt[e] = 0;
@@ -197,6 +205,9 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
     s_nact = 0;
     s_tsmall = 0x7fffffff;
     s_tsingle = 0x7fffffff;
+    s_r32 = 0x7fffffff;
+    s_rhot = 0x7fffffff;
+    s_thot = 0x7fffffff;
   }
   __syncthreads();
   // The slots' expert ids, kSB per thread at a time, all requested before any is used
@@ -293,10 +304,23 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
   int pos = s_scan[tid] - ns, tpos = s_scan2[tid] - nt;
   for (int r = r0; r < r1; ++r) {
     const int e = s_ebr[r];
-    // in count order the experts of at most kMTs slots form the tail of the tile list
-    // (and the experts of one kMT-token tile the tail of the first launch's tiles)
-    if (by_count && s_cnt[e] <= kMTs) atomicMin(&s_tsmall, tpos);
-    if (by_count && s_cnt[e] <= kMT) atomicMin(&s_tsingle, tpos);
+    // In count order the experts of at most kMTs slots form the tail of the tile list, the
+    // experts of one kMT-token tile the tail of the first launch's tiles and, on the mixed
+    // path, the experts of at most hyb slots the tail of the small-tile ones: the rank at
+    // which the count first falls to a bound records itself and its first tile (one plain
+    // store each, where an atomic minimum over the tail would queue on one LDS word).
+    if (by_count) {
+      const int c = s_cnt[e], cprev = r > 0 ? s_cnt[s_ebr[r - 1]] : 0x7fffffff;
+      if (c <= kMTs && cprev > kMTs) {
+        s_tsmall = tpos;
+        s_r32 = r;
+      }
+      if (c <= kMT && cprev > kMT) s_tsingle = tpos;
+      if (c <= A.hyb && cprev > A.hyb) {
+        s_rhot = r;
+        s_thot = tpos;
+      }
+    }
     A.active[r] = e;
     A.act_off[r] = pos;
     A.tt_off[r] = tpos;
@@ -320,6 +344,21 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
     A.ctrl[kTSingle] = min(s_tsingle, t_small);
     A.ctrl[kTasksMGUs] = (n_tiles - t_small) * A.tiles_mgus;
     A.ctrl[kTasksMDns] = (n_tiles - t_small) * A.tiles_mdns;
+    A.ctrl[kR32] = 0;
+    A.ctrl[kRSkip] = 0;
+    if (A.hyb > 0) {
+      // ranks r32 .. rhot - 1 (more than hyb, at most kMTs slots: one tile each, tiles
+      // t_small .. t_hot - 1) go to the small-tile MFMA launch; the VALU kernel takes
+      // ranks 0 .. r32 - 1 and rhot .. n_active - 1
+      const int r32 = min(s_r32, n_active), rhot = max(r32, min(s_rhot, n_active));
+      const int t_hot = max(t_small, min(s_thot, n_tiles));
+      A.ctrl[kR32] = r32;
+      A.ctrl[kRSkip] = rhot - r32;
+      A.ctrl[kTasksGU] = (n_active - (rhot - r32)) * A.tiles_gu;
+      A.ctrl[kTasksDn] = (n_active - (rhot - r32)) * A.tiles_dn;
+      A.ctrl[kTasksMGUs] = (t_hot - t_small) * A.tiles_mgus;
+      A.ctrl[kTasksMDns] = (t_hot - t_small) * A.tiles_mdns;
+    }
     A.ctrl[kFlags] = s_bad ? 1 : 0;
   }
   __syncthreads();
@@ -482,8 +521,10 @@ __device__ __forceinline__ void tb_acts_compute(const MoeArgs& A, const int (&wc
 // lane 0 gets the range's start, lane 1 its end, lane 2 the expert id. Kept in a vector
 // register and read out lane by lane only where used, so that a fetch issued one task
 // ahead is not waited for at once.
-__device__ __forceinline__ int tb_task_fetch(const MoeArgs& A, int task, int tiles, int lane) {
-  const int a = task / tiles;
+// (on the mixed path the VALU kernel's task ranks skip the rskip ranks from r32 on)
+__device__ __forceinline__ int tb_task_fetch(const MoeArgs& A, int task, int tiles, int lane, int r32, int rskip) {
+  int a = task / tiles;
+  a += a >= r32 ? rskip : 0;
   return *(lane == 2 ? A.active + a : A.act_off + a + (lane & 1));
 }
 struct TbTask {
@@ -512,6 +553,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
   const int kb = K / 256;
   const int tiles = NMAT == 2 ? A.tiles_gu : A.tiles_dn;
   const int n_tasks = A.ctrl[NMAT == 2 ? kTasksGU : kTasksDn];
+  const int r32 = A.ctrl[kR32], rskip = A.ctrl[kRSkip];
   const uint32_t arows = (uint32_t)(NMAT == 2 ? A.t : A.t * A.topk);
   const __amdgpu_buffer_rsrc_t qr = make_rsrc(NMAT == 2 ? A.xq : A.hq, arows * (uint32_t)K);
   const __amdgpu_buffer_rsrc_t dr = make_rsrc(NMAT == 2 ? A.xd : A.hd, arows * (uint32_t)kb * 4u);
@@ -520,7 +562,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
   if (task >= n_tasks) return;
   // A task's scalars and slot list are fetched while the task before it runs (at its own
   // start each would be another round trip ahead of the weight loads).
-  int tv = tb_task_fetch(A, task, tiles, lane);
+  int tv = tb_task_fetch(A, task, tiles, lane, r32, rskip);
   int sv;
   {
     const TbTask t0 = tb_task(tv, task, tiles);
@@ -529,7 +571,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
   for (; task < n_tasks; task += gridDim.x) {
     const TbTask cur = tb_task(tv, task, tiles);
     const int task_next = min(task + (int)gridDim.x, n_tasks - 1);
-    const int tv_next = tb_task_fetch(A, task_next, tiles, lane);
+    const int tv_next = tb_task_fetch(A, task_next, tiles, lane, r32, rskip);
     const int64_t e = cur.e;
     const int off = cur.off, cnt = cur.cnt;
     // rows past N (a ragged last tile) load the last row and write nothing
@@ -1656,8 +1698,9 @@ static int choose_path(const tq_experts* ex, int64_t t, int32_t topk, int32_t fl
   // (both grouped paths address the quantized activations with 32-bit buffer offsets)
   const int64_t S = t * topk;
   if (S * std::max(ex->hidden, ex->inter) >= ((int64_t)1 << 31)) return -1;
-  const bool mfma = (flags & TQ_MOE_FORCE_MFMA) || (!(flags & TQ_MOE_FORCE_VALU) && S >= kMfmaMinSlots);
-  return mfma ? TQ_MOE_PATH_MFMA : TQ_MOE_PATH_VALU;
+  if ((flags & TQ_MOE_FORCE_MFMA) || (!(flags & TQ_MOE_FORCE_VALU) && S >= kMfmaMinSlots)) return TQ_MOE_PATH_MFMA;
+  // (with at most kHybMin tokens no expert has more slots, duplicated ids aside)
+  return !(flags & TQ_MOE_FORCE_VALU) && t > kHybMin ? TQ_MOE_PATH_MIXED : TQ_MOE_PATH_VALU;
 }
 
 static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const int32_t* topk_idx,
@@ -1765,7 +1808,8 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   }
   // per-expert contraction on MFMA for prefill-sized groups (or when forced), VALU dot4
   // otherwise
-  const bool mfma = path == TQ_MOE_PATH_MFMA;
+  const bool mfma = path == TQ_MOE_PATH_MFMA, mixed = path == TQ_MOE_PATH_MIXED;
+  A.hyb = mixed ? kHybMin : 0;
   A.tiles_mgu = (ex->inter + kMN - 1) / kMN;
   A.tiles_mdn = (ex->hidden + 2 * kMN - 1) / (2 * kMN);  // (two 16-row tiles per wave)
   A.tiles_mgus = (ex->inter + kMNs - 1) / kMNs;
@@ -1777,7 +1821,7 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   // Beside the small-tile launch, the 128-token launch keeps five eighths of the compute
   // units (a multiple of 8 workgroups, one per unit, striding over the tasks); the other
   // units run the small tiles, and so do the first ones as they free up.
-  SideStream* ss = mfma ? side_stream(stm, may_allocate) : nullptr;
+  SideStream* ss = mfma || mixed ? side_stream(stm, may_allocate) : nullptr;
   const int64_t big_cap = ss ? std::max(8, ss->cus * 5 / 8 / 8 * 8) : TQ_MFMA_GRID;
   const unsigned g_mgu = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mgu, big_cap);
   const unsigned g_mdn = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mdn, big_cap);
@@ -1791,6 +1835,10 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   else if (mfma)
     st = launch_pair(events, 1, ss, k_moe_mfma<2, kMT, kMWaves, false, false>, dim3(g_mgu), kMWaves * 64,
                        k_moe_mfma<2, kMTs, kMWavesS, true, false>, dim3(g_mgus), kMWavesS * 64, stm, fn, A);
+  else if (mixed)  // (the VALU kernel on the caller's stream, the hot experts' MFMA tiles beside it)
+    st = launch_pair(events, 1, ss, pick_tb<2>(ex->hidden / 256), dim3(g_gu), kTbWaves * 64,
+                     debug ? k_moe_mfma<2, kMTs, kMWavesS, true, true> : k_moe_mfma<2, kMTs, kMWavesS, true, false>,
+                     dim3(g_mgus), kMWavesS * 64, stm, fn, A);
   else st = launch_stage(events, 1, pick_tb<2>(ex->hidden / 256), dim3(g_gu), kTbWaves * 64, stm, fn, A);
   if (st != TQ_OK) return st;
   if ((st = launch_stage(events, 2, k_moe_requant, dim3((unsigned)((hblocks + 31) / 32)), 256, stm, fn, A, hblocks)) !=
@@ -1802,6 +1850,11 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   else if (mfma)
     st = launch_pair(events, 3, ss, k_moe_mfma<2, kMT, kMWaves, false, false, true>, dim3(g_mdn), kMWaves * 64,
                        k_moe_mfma<2, kMTs, kMWavesS, true, false, true>, dim3(g_mdns), kMWavesS * 64, stm, fn, A);
+  else if (mixed)
+    st = launch_pair(events, 3, ss, pick_tb<1>(ex->inter / 256), dim3(g_dn), kTbWaves * 64,
+                     debug ? k_moe_mfma<2, kMTs, kMWavesS, true, true, true>
+                           : k_moe_mfma<2, kMTs, kMWavesS, true, false, true>,
+                     dim3(g_mdns), kMWavesS * 64, stm, fn, A);
   else st = launch_stage(events, 3, pick_tb<1>(ex->inter / 256), dim3(g_dn), kTbWaves * 64, stm, fn, A);
   if (st != TQ_OK) return st;
   const int64_t nout = t * (ex->hidden / 4);

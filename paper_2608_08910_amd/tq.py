@@ -28,7 +28,7 @@ TQ_ERR_DEVICE = -4
 TQ_MOE_FORCE_VALU = 1
 TQ_MOE_FORCE_MFMA = 2
 TQ_MOE_DEBUG_STAGES = 4
-TQ_MOE_PATH_T1, TQ_MOE_PATH_VALU, TQ_MOE_PATH_MFMA = 0, 1, 2
+TQ_MOE_PATH_T1, TQ_MOE_PATH_VALU, TQ_MOE_PATH_MFMA, TQ_MOE_PATH_MIXED = 0, 1, 2, 3
 
 
 class TqError(RuntimeError):

@@ -100,12 +100,15 @@ def test_moe_decode_batch1_uniform(tq, oracle, experts_h4096):
 
 
 def test_moe_decode_batch32_zipf(tq, oracle, experts_h4096):
-    """Batched decode: 32 tokens, top-8 with Zipf(1.1) expert popularity, seed 0. Every
-    slot's block sums bit-exact."""
+    """Batched decode: 32 tokens, top-8 with Zipf(1.1) expert popularity, seed 0, on the
+    mixed path (the experts of 9 to 32 slots on the 32-token MFMA kernel, the others on
+    the grouped VALU kernel). Every slot's block sums bit-exact."""
     c = gen.CONFIGS[2]
     x = gen.activations(gen.SEED, 0, c["tokens"], c["hidden"])
     idx, w = gen.routing(gen.SEED, 0, c["tokens"], c["experts"], c["topk"], c["routing"])
-    assert tq.tq_moe_path(experts_h4096, c["tokens"], c["topk"]) == tq.TQ_MOE_PATH_VALU
+    assert tq.tq_moe_path(experts_h4096, c["tokens"], c["topk"]) == tq.TQ_MOE_PATH_MIXED
+    counts = np.bincount(idx.ravel(), minlength=c["experts"])
+    assert (counts > 8).any() and ((counts > 0) & (counts <= 8)).any()  # both kernels have experts
     announce("moe decode t=32 top-8 zipf")
     out, ws = run_moe(tq, experts_h4096, x, idx, w)
     get = oracle_pkg.expert_getter(gen.SEED, 0, c["hidden"], c["inter"], oracle)
@@ -293,7 +296,11 @@ def test_moe_grouped_valu_long_lists(tq, oracle, E, H, I, T, topk):
 
 
 def test_moe_workspace_shared_across_paths(tq, experts_h4096):
-    """One prepared workspace serves single-token and grouped calls in any order."""
+    """One prepared workspace serves single-token and grouped calls in any order (the
+    grouped call pinned to the VALU kernels, whose per-row arithmetic is the single-token
+    kernels' own, so that token 0's output agrees bitwise; the mixed path's MFMA tiles
+    sum the block terms in another fp32 order and are checked against the oracle in the
+    32-token test)."""
     c = gen.CONFIGS[2]
     ws = tq.moe_workspace(experts_h4096, c["tokens"], c["topk"])
     x = gen.activations(gen.SEED, 60, c["tokens"], c["hidden"])
@@ -303,7 +310,7 @@ def test_moe_workspace_shared_across_paths(tq, experts_h4096):
     announce("moe workspace shared: t=1, t=32, t=1")
     for t in (1, c["tokens"], 1):
         out = torch.empty((t, c["hidden"]), dtype=torch.float32, device="cuda")
-        tq.tq_moe_grouped(experts_h4096, xd[:t], idd[:t], wd[:t], out, ws)
+        tq.tq_moe_grouped(experts_h4096, xd[:t], idd[:t], wd[:t], out, ws, tq.TQ_MOE_FORCE_VALU)
         outs.append(out)
         assert tq.tq_moe_status(ws, experts_h4096, t, c["topk"]) == 0
     assert torch.equal(outs[0], outs[2]) and torch.equal(outs[0], outs[1][:1])
@@ -392,12 +399,12 @@ def test_t1_graph_replays_match_eager(tq, oracle):
     assert tq.tq_moe_status(ws, ex, 1, topk) == 0
 
 
-@pytest.mark.parametrize("flags,T", [(1, 24), (2, 40)])
+@pytest.mark.parametrize("flags,T", [(1, 24), (2, 40), (0, 40)])
 def test_grouped_graph_replays_match_eager(tq, oracle, flags, T):
-    """Grouped calls (forced VALU, forced MFMA) captured in a HIP graph, each call with its
-    own routing: every replay (with eager calls on the same workspace between replays)
-    gives bitwise the eager outputs, so the dispatch's counters and lists are rebuilt on
-    every replay."""
+    """Grouped calls (forced VALU, forced MFMA, automatic: the mixed path) captured in a
+    HIP graph, each call with its own routing: every replay (with eager calls on the same
+    workspace between replays) gives bitwise the eager outputs, so the dispatch's counters
+    and lists are rebuilt on every replay."""
     E, H, I, topk = 16, 1024, 512, 4
     ex, _ = host_experts(tq, oracle, E, H, I, seed=93 + flags)
     rng = np.random.default_rng(94 + flags)
@@ -433,4 +440,5 @@ def test_grouped_graph_replays_match_eager(tq, oracle, flags, T):
         torch.cuda.synchronize()
         assert torch.equal(tmp, eager[rep])
     assert tq.tq_moe_status(ws, ex, T, topk) == 0
-    assert tq.tq_moe_path(ex, T, topk, flags) == flags
+    assert tq.tq_moe_path(ex, T, topk, flags) == {1: tq.TQ_MOE_PATH_VALU, 2: tq.TQ_MOE_PATH_MFMA,
+                                                   0: tq.TQ_MOE_PATH_MIXED}[flags]
