@@ -697,6 +697,19 @@ def run_stream(args, wl, cfg):
                        "copied_GBps": round(link, 2)})
 
 
+def mixed_kernel(nmat: int, kb: int) -> str:
+    """The mixed path's one-launch kernel for a projection of kb blocks per row (NL rounded
+    up to 1, 2, 4 or 8; the VALU role's tile as the grouped VALU kernel's)."""
+    nl = (kb + 7) // 8
+    nl4 = nl if nl <= 2 else (4 if nl <= 4 else 8)
+    if nmat == 2:
+        rpw = 8 if nl4 == 1 else (4 if nl4 == 2 else (2 if nl4 <= 4 else 1))
+    else:
+        rpw = 8 if nl4 <= 2 else (4 if nl4 <= 4 else 2)
+    nt = 2 if nl4 <= 2 else 1
+    return f"k_mixed<{nmat}, {nl4}, {rpw}, {nt}, {nt}, {'true' if kb != 8 * nl4 else 'false'}>"
+
+
 def run_moe(args, wl, cfg):
     import torch
     from paper_2608_08910_amd import tq
@@ -792,8 +805,8 @@ def run_moe(args, wl, cfg):
         # the MFMA stage is two launches: 128-token tiles, then the experts of at most 32 slots
         gu_kernel = ("k_moe_mfma<2, 128, 8, false, false, false> + k_moe_mfma<2, 32, 4, true, false, false>" if mfma
                      else f"k_tb<2, {nl_gu}, {rpw}, {nt}, {nt}, 4, {ragged}>")
-        if path == tq.TQ_MOE_PATH_MIXED:  # the hot experts' 32-token MFMA tiles beside it
-            gu_kernel += " + k_moe_mfma<2, 32, 4, true, false, false>"
+        if path == tq.TQ_MOE_PATH_MIXED:  # one launch: the VALU tasks and the 32-token MFMA tiles
+            gu_kernel = mixed_kernel(2, H // 256)
         kname = "gate_up"
     if mfma:
         gu_ops = 2.0 * T * topk * (2 * I * H)  # int8 multiply-adds of gate and up, 2 ops each
@@ -811,10 +824,6 @@ def run_moe(args, wl, cfg):
             roof["frac_rocprof"] = round(gu_ops / (avg_ns * 1e-9) / 1e12 / MFMA_I8_PEAK_TOPS, 4)
     else:
         roof = hbm_roof(kname, gu_bytes, gu_ms, gu_kernel)
-        if path == tq.TQ_MOE_PATH_MIXED:
-            roof["frac_timing"] = ("hip events recorded on the stream before the fork and after the join of the "
-                                   "stage's two launches (the VALU kernel, and beside it on a second stream the "
-                                   "32-token MFMA tiles of the experts of 9 to 32 slots); mean over the per-kernel pass")
     # the down kernel beside it: the routed experts' down planes, h in (fp32 per slot on the
     # single-token path, which requantizes it itself; int8 + scale per block otherwise),
     # the output (or the per-slot rows) out
@@ -830,7 +839,7 @@ def run_moe(args, wl, cfg):
         dn_kernel = ("k_moe_mfma<2, 128, 8, false, false, true> + k_moe_mfma<2, 32, 4, true, false, true>" if mfma
                      else "k_tb<1, ...>")
         if path == tq.TQ_MOE_PATH_MIXED:
-            dn_kernel += " + k_moe_mfma<2, 32, 4, true, false, true>"
+            dn_kernel = mixed_kernel(1, I // 256)
     dn_ms = stage_ms["down"]
     down = {
         "kernel_symbol": dn_kernel, "bytes_per_launch": round(dn_bytes), "mean_ms": round(dn_ms, 5),

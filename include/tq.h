@@ -322,13 +322,13 @@ tq_status tq_gemv_mx_timed(const tq_mat_mx* w, const int8_t* q, const float* d, 
  * quantized activations with 32-bit offsets: TQ_ERR_INVALID if t * topk * max(hidden,
  * inter) >= 2^31 (and t > 1 or TQ_MOE_FORCE_MFMA).
  * Streams: every launch follows the work queued on `stream`, and work queued on `stream`
- * after the call follows every launch. The grouped MFMA and mixed paths run each
- * projection as two launches that write disjoint outputs, the second on a stream the
- * library owns (one per device, default priority, created by the first such call on the
- * device that is not made under stream capture), forked from and joined back to
- * `stream` by events; under
- * capture the fork and join become graph edges. Until that stream exists, or if it
- * could not be created, the two launches run in order on `stream`.
+ * after the call follows every launch. The grouped MFMA path (and the mixed path with
+ * TQ_MOE_DEBUG_STAGES) runs each projection as two launches that write disjoint
+ * outputs, the second on a stream the library owns (one per device, default priority,
+ * created by the first such call on the device that is not made under stream capture),
+ * forked from and joined back to `stream` by events; under capture the fork and join
+ * become graph edges. Until that stream exists, or if it could not be created, the two
+ * launches run in order on `stream`.
  * TQ_MOE_DEBUG_STAGES (may be or-ed with either): the same kernels, each taking one
  * extra branch on a kernel argument, also leave in the workspace, past the stage buffers,
  * every routed slot's g and u (fp32) and the exact int32 block sums of its gate, up and
@@ -367,10 +367,10 @@ tq_status tq_moe_grouped_noalloc(const tq_experts* ex, const float* x, int64_t t
  * gate/up kernel, then a down kernel with the requantization and the weighted combine
  * fused), TQ_MOE_PATH_VALU (dispatch + grouped VALU dot4 kernels), TQ_MOE_PATH_MFMA
  * (dispatch + grouped int8 MFMA kernels), TQ_MOE_PATH_MIXED (the automatic choice for
- * fewer than 1024 slots and more than 8 tokens: dispatch + the grouped VALU kernels for
- * the experts of at most 8 or more than 32 slots, and beside them the 32-token MFMA
- * kernels for the experts of 9 to 32 slots, on the second stream described at
- * tq_moe_grouped); -1 if the arguments are invalid. Host only, no device work. */
+ * fewer than 1024 slots and more than 8 tokens: dispatch + one launch per projection
+ * whose first workgroups run the 32-token MFMA tiles of the experts of 9 to 32 slots and
+ * the others the grouped VALU tasks of the remaining experts); -1 if the arguments are
+ * invalid. Host only, no device work. */
 #define TQ_MOE_PATH_T1 0
 #define TQ_MOE_PATH_VALU 1
 #define TQ_MOE_PATH_MFMA 2

@@ -21,6 +21,7 @@
 #include <hip/hip_ext.h>
 
 #include <algorithm>
+#include <atomic>
 #include <mutex>
 #include <type_traits>
 
@@ -58,6 +59,7 @@ constexpr int64_t kMfmaMinSlots = 1024;  // automatic path choice: MFMA from thi
 // behind the compute unit's weight loads; on MFMA its tokens share one pass over the
 // weights.
 constexpr int kHybMin = 8;
+constexpr int kTbWaves = 4;  // waves per grouped VALU workgroup
 
 struct Layout {
   size_t ctrl, active, act_off, tt_off, tile_exp, slot_list, xq, xd, xb, h, hq, hd, hb, yd, total;
@@ -543,8 +545,10 @@ __device__ __forceinline__ TbTask tb_task(int v, int task, int tiles) {
 // before), so that their round trip overlaps the weights' (most tasks have a single
 // group); then the next task's slots; further groups load and compute in turn (the last
 // one possibly part-empty).
+// `bid` of `nblk`: the workgroup's index among those that run this role (the whole grid
+// for k_tb, the workgroups past the MFMA ones in k_mixed).
 template <int NMAT, int NL, int RPW, int NT, int NTL, int WAVES, bool RAGGED>
-__global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
+__device__ __forceinline__ void tb_run(const MoeArgs& A, int bid, int nblk) {
   static_assert(RPW <= 8 && (RPW & (RPW - 1)) == 0, "RPW: a power of two <= 8");
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 3, cp = lane & 7;
@@ -558,7 +562,7 @@ __global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
   const __amdgpu_buffer_rsrc_t qr = make_rsrc(NMAT == 2 ? A.xq : A.hq, arows * (uint32_t)K);
   const __amdgpu_buffer_rsrc_t dr = make_rsrc(NMAT == 2 ? A.xd : A.hd, arows * (uint32_t)kb * 4u);
   const int lr = rev_bits<clog2(RPW)>(lane & (RPW - 1));  // the lane's row after the block butterfly
-  int task = blockIdx.x;
+  int task = bid;
   if (task >= n_tasks) return;
   // A task's scalars and slot list are fetched while the task before it runs (at its own
   // start each would be another round trip ahead of the weight loads).
@@ -568,9 +572,9 @@ __global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
     const TbTask t0 = tb_task(tv, task, tiles);
     sv = A.slot_list[t0.off + min(lane, t0.cnt - 1)];
   }
-  for (; task < n_tasks; task += gridDim.x) {
+  for (; task < n_tasks; task += nblk) {
     const TbTask cur = tb_task(tv, task, tiles);
-    const int task_next = min(task + (int)gridDim.x, n_tasks - 1);
+    const int task_next = min(task + nblk, n_tasks - 1);
     const int tv_next = tb_task_fetch(A, task_next, tiles, lane, r32, rskip);
     const int64_t e = cur.e;
     const int off = cur.off, cnt = cur.cnt;
@@ -628,6 +632,11 @@ __global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
     tv = tv_next;
     sv = sv_next;
   }
+}
+
+template <int NMAT, int NL, int RPW, int NT, int NTL, int WAVES, bool RAGGED>
+__global__ __launch_bounds__(WAVES * 64) void k_tb(MoeArgs A) {
+  tb_run<NMAT, NL, RPW, NT, NTL, WAVES, RAGGED>(A, blockIdx.x, gridDim.x);
 }
 
 // ---------------------------------------------------------------------------------
@@ -778,10 +787,10 @@ constexpr int kMfmaLoadsPerBlock = PW + 3 * NMAT;
 // DN2: the down projection with two 16-row tiles of the matrix per wave, run as the two
 // "matrices" of the NMAT = 2 path (the second's resource starts 16 rows on), so that each
 // token operand read from LDS feeds two MFMAs, as in gate/up.
-template <int NMAT, int MT, int WAVES, bool SMALL, bool DBG, bool DN2 = false>
-// (the small-tile gate/up instance is held to the registers of three waves per SIMD)
-__global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMALL && NMAT == 2 ? 3 : 1))) void k_moe_mfma(
-    MoeArgs A) {
+// `bid` of `nblk` as in tb_run (the whole grid for k_moe_mfma, the first workgroups of
+// k_mixed).
+template <int NMAT, int MT, int WAVES, bool SMALL, bool DBG, bool DN2>
+__device__ __forceinline__ void mfma_run(const MoeArgs& A, int bid, int nblk) {
   static_assert(!DN2 || NMAT == 2, "DN2 runs two row tiles as two matrices");
   constexpr bool GU = NMAT == 2 && !DN2;  // the gate/up projection
   constexpr int RW = DN2 ? 32 : 16;       // weight rows per wave
@@ -819,7 +828,7 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
   const int t1 = SMALL ? tile0 : ld_uniform(A.ctrl + kTSingle);
   const int n_single = (SMALL ? n_tasks / RT : ld_uniform(A.ctrl + kTSmall) - t1);
   const int base1 = (t1 - tile0) * RT, full1 = (n_single / 8) * 8 * RT;
-  for (int task = blockIdx.x; task < n_tasks; task += gridDim.x) {
+  for (int task = bid; task < n_tasks; task += nblk) {
     // the control data was written by the prologue kernel, so it is read through the
     // scalar cache (not queued behind this compute unit's vector loads)
     int tile, rtile;
@@ -1080,6 +1089,31 @@ __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMAL
         }
     }
   }
+}
+
+template <int NMAT, int MT, int WAVES, bool SMALL, bool DBG, bool DN2 = false>
+// (the small-tile gate/up instance is held to the registers of three waves per SIMD)
+__global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMALL && NMAT == 2 ? 3 : 1))) void k_moe_mfma(
+    MoeArgs A) {
+  mfma_run<NMAT, MT, WAVES, SMALL, DBG, DN2>(A, blockIdx.x, gridDim.x);
+}
+
+// The mixed path's projection in one launch: workgroups 0 .. n_mfma - 1 run the kMTs-token
+// MFMA tasks of the experts of more than hyb and at most kMTs slots, the rest the grouped
+// VALU tasks of the other experts (a uniform branch per workgroup; both roles are four
+// waves). One launch instead of two streams joined by events: on this device each such
+// edge between queues costs several microseconds of idle time. NMAT: as in k_tb (1 =
+// down, whose MFMA role runs the two-tile DN2 form). The one-load down instance is held
+// to the registers of three waves per SIMD (its LDS allows three workgroups per compute
+// unit; without the bound the MFMA role's registers would leave it two).
+template <int NMAT, int NL, int RPW, int NT, int NTL, bool RAGGED>
+__global__ __launch_bounds__(kTbWaves * 64) __attribute__((amdgpu_waves_per_eu(NMAT == 1 && NL == 1 ? 3 : 1))) void
+k_mixed(MoeArgs A, int n_mfma) {
+  static_assert(kTbWaves == kMWavesS, "both roles run four-wave workgroups");
+  if ((int)blockIdx.x < n_mfma)
+    mfma_run<2, kMTs, kMWavesS, true, false, NMAT == 1>(A, blockIdx.x, n_mfma);
+  else
+    tb_run<NMAT, NL, RPW, NT, NTL, kTbWaves, RAGGED>(A, blockIdx.x - n_mfma, gridDim.x - n_mfma);
 }
 
 // ---------------------------------------------------------------------------------
@@ -1434,28 +1468,36 @@ __global__ __launch_bounds__(TOPK * 64) void k_t1_down(MoeArgs A, float* __restr
 
 using moe_fn = void (*)(MoeArgs);
 
+constexpr int kMaxDevices = 64;  // per-device host state (side stream, compute units, scratch)
+
 // Grouped-decode tiles: each wave holds about 16 unpacked chunks per lane
-// (NMAT * RPW * NL).
-constexpr int kTbWaves = 4;
+// (NMAT * RPW * NL), in kTbWaves-wave workgroups.
 static int tb_rpw(int nmat, int nl) {
   if (nmat == 2) return nl == 1 ? 8 : (nl == 2 ? 4 : (nl <= 4 ? 2 : 1));
   return nl <= 2 ? 8 : (nl <= 4 ? 4 : 2);
 }
 
-template <int NMAT, int NL, bool R>
-static moe_fn pick_tb_nl() {
-  constexpr int RPW = NMAT == 2 ? (NL == 1 ? 8 : (NL == 2 ? 4 : (NL <= 4 ? 2 : 1))) : (NL <= 2 ? 8 : (NL <= 4 ? 4 : 2));
-  // tokens per group: pairs, single tokens where a pair's activations would crowd the
-  // registers that hold the weights
-  constexpr int NT = NL <= 2 ? 2 : 1;
 #ifndef TQ_TB_NTL2
 #define TQ_TB_NTL2 2
 #endif
 #ifndef TQ_TB_NTL4
 #define TQ_TB_NTL4 1
 #endif
-  constexpr int NTL = NL <= 2 ? TQ_TB_NTL2 : (NL <= 4 ? TQ_TB_NTL4 : 1);
-  return k_tb<NMAT, NL, RPW, NT, NTL, kTbWaves, R>;
+// The grouped VALU kernel's tile for NL loads per lane: rows per wave (as tb_rpw), the
+// first token group's width (pairs, single tokens where a pair's activations would crowd
+// the registers that hold the weights) and the later groups' width.
+template <int NMAT, int NL>
+struct TbShape {
+  static constexpr int RPW =
+      NMAT == 2 ? (NL == 1 ? 8 : (NL == 2 ? 4 : (NL <= 4 ? 2 : 1))) : (NL <= 2 ? 8 : (NL <= 4 ? 4 : 2));
+  static constexpr int NT = NL <= 2 ? 2 : 1;
+  static constexpr int NTL = NL <= 2 ? TQ_TB_NTL2 : (NL <= 4 ? TQ_TB_NTL4 : 1);
+};
+
+template <int NMAT, int NL, bool R>
+static moe_fn pick_tb_nl() {
+  using S = TbShape<NMAT, NL>;
+  return k_tb<NMAT, NL, S::RPW, S::NT, S::NTL, kTbWaves, R>;
 }
 
 template <int NMAT, bool R>
@@ -1476,6 +1518,46 @@ template <int NMAT>
 static moe_fn pick_tb(int kb) {
   const int nl = (kb + 7) / 8;
   return kb % 8 == 0 ? pick_tb_r<NMAT, false>(nl) : pick_tb_r<NMAT, true>(nl);
+}
+
+// The mixed path's one-launch kernel: NL rounded up to 1, 2, 4 or 8 (the extra loads of
+// a row reread its last block, whose scale is then taken as zero; the tile shapes of a
+// rounded NL equal those of the exact one), which keeps the instances few.
+using mixed_fn = void (*)(MoeArgs, int);
+template <int NMAT, int NL>
+static mixed_fn pick_mixed_nl(bool ragged) {
+  using S = TbShape<NMAT, NL>;
+  return ragged ? k_mixed<NMAT, NL, S::RPW, S::NT, S::NTL, true> : k_mixed<NMAT, NL, S::RPW, S::NT, S::NTL, false>;
+}
+template <int NMAT>
+static mixed_fn pick_mixed(int kb) {
+  const int nl = (kb + 7) / 8, nl4 = nl <= 2 ? nl : (nl <= 4 ? 4 : 8);
+  const bool ragged = kb != 8 * nl4;
+  switch (nl4) {
+    case 1: return pick_mixed_nl<NMAT, 1>(ragged);
+    case 2: return pick_mixed_nl<NMAT, 2>(ragged);
+    case 4: return pick_mixed_nl<NMAT, 4>(ragged);
+    default: return pick_mixed_nl<NMAT, 8>(ragged);
+  }
+}
+
+// Compute units of the calling thread's current device (queried once per device).
+static int device_cus() {
+  static std::atomic<int> cache[kMaxDevices];
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  int v = cache[dev].load(std::memory_order_relaxed);
+  if (v == 0) {
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v < 8) {
+      (void)hipGetLastError();
+      v = 256;
+    }
+    cache[dev].store(v, std::memory_order_relaxed);
+  }
+  return v;
 }
 
 // Tile shapes of the single-token path (measured on MI355X; overridable at build time).
@@ -1592,8 +1674,6 @@ static tq_status empty_stage(void* const* events, int stage, hipStream_t st, con
     return fail(TQ_ERR_DEVICE, "%s: hipEventRecord failed", fn);
   return TQ_OK;
 }
-
-constexpr int kMaxDevices = 64;
 
 // The grouped MFMA path's second stream. Each projection runs as two launches that touch
 // disjoint outputs (the 128-token tiles of the experts of more than kMTs slots, and the
@@ -1821,13 +1901,20 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   // Beside the small-tile launch, the 128-token launch keeps five eighths of the compute
   // units (a multiple of 8 workgroups, one per unit, striding over the tasks); the other
   // units run the small tiles, and so do the first ones as they free up.
-  SideStream* ss = mfma || mixed ? side_stream(stm, may_allocate) : nullptr;
+  // (the mixed path runs one launch per projection; only its debug instances, kept out
+  // of that launch, take the side stream)
+  SideStream* ss = mfma || (mixed && debug) ? side_stream(stm, may_allocate) : nullptr;
   const int64_t big_cap = ss ? std::max(8, ss->cus * 5 / 8 / 8 * 8) : TQ_MFMA_GRID;
   const unsigned g_mgu = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mgu, big_cap);
   const unsigned g_mdn = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mdn, big_cap);
   // (one tile per expert of at most kMTs slots)
   const unsigned g_mgus = (unsigned)std::min<int64_t>(max_active * A.tiles_mgus, TQ_MFMA_GRID);
   const unsigned g_mdns = (unsigned)std::min<int64_t>(max_active * A.tiles_mdns, TQ_MFMA_GRID);
+  // mixed path, one launch: at most one MFMA-role workgroup per compute unit (a multiple
+  // of 8, striding over the tasks; they come first, so the longest tasks start first)
+  const int cus8 = std::max(8, device_cus() / 8 * 8);
+  const int n_mgus = (int)std::min<int64_t>((max_active * A.tiles_mgus + 7) / 8 * 8, cus8);
+  const int n_mdns = (int)std::min<int64_t>((max_active * A.tiles_mdns + 7) / 8 * 8, cus8);
   if ((st = launch_stage(events, 0, k_moe_prologue, dim3(nq + 1), 256, stm, fn, x, A)) != TQ_OK) return st;
   if (mfma && debug)
     st = launch_pair(events, 1, ss, k_moe_mfma<2, kMT, kMWaves, false, true>, dim3(g_mgu), kMWaves * 64,
@@ -1835,10 +1922,12 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   else if (mfma)
     st = launch_pair(events, 1, ss, k_moe_mfma<2, kMT, kMWaves, false, false>, dim3(g_mgu), kMWaves * 64,
                        k_moe_mfma<2, kMTs, kMWavesS, true, false>, dim3(g_mgus), kMWavesS * 64, stm, fn, A);
-  else if (mixed)  // (the VALU kernel on the caller's stream, the hot experts' MFMA tiles beside it)
+  else if (mixed && !debug)
+    st = launch_stage(events, 1, pick_mixed<2>(ex->hidden / 256), dim3((unsigned)n_mgus + g_gu), kTbWaves * 64, stm, fn,
+                      A, n_mgus);
+  else if (mixed)  // (debug: the VALU kernel on the caller's stream, the MFMA tiles beside it)
     st = launch_pair(events, 1, ss, pick_tb<2>(ex->hidden / 256), dim3(g_gu), kTbWaves * 64,
-                     debug ? k_moe_mfma<2, kMTs, kMWavesS, true, true> : k_moe_mfma<2, kMTs, kMWavesS, true, false>,
-                     dim3(g_mgus), kMWavesS * 64, stm, fn, A);
+                     k_moe_mfma<2, kMTs, kMWavesS, true, true>, dim3(g_mgus), kMWavesS * 64, stm, fn, A);
   else st = launch_stage(events, 1, pick_tb<2>(ex->hidden / 256), dim3(g_gu), kTbWaves * 64, stm, fn, A);
   if (st != TQ_OK) return st;
   if ((st = launch_stage(events, 2, k_moe_requant, dim3((unsigned)((hblocks + 31) / 32)), 256, stm, fn, A, hblocks)) !=
@@ -1850,11 +1939,12 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   else if (mfma)
     st = launch_pair(events, 3, ss, k_moe_mfma<2, kMT, kMWaves, false, false, true>, dim3(g_mdn), kMWaves * 64,
                        k_moe_mfma<2, kMTs, kMWavesS, true, false, true>, dim3(g_mdns), kMWavesS * 64, stm, fn, A);
+  else if (mixed && !debug)
+    st = launch_stage(events, 3, pick_mixed<1>(ex->inter / 256), dim3((unsigned)n_mdns + g_dn), kTbWaves * 64, stm, fn,
+                      A, n_mdns);
   else if (mixed)
     st = launch_pair(events, 3, ss, pick_tb<1>(ex->inter / 256), dim3(g_dn), kTbWaves * 64,
-                     debug ? k_moe_mfma<2, kMTs, kMWavesS, true, true, true>
-                           : k_moe_mfma<2, kMTs, kMWavesS, true, false, true>,
-                     dim3(g_mdns), kMWavesS * 64, stm, fn, A);
+                     k_moe_mfma<2, kMTs, kMWavesS, true, true, true>, dim3(g_mdns), kMWavesS * 64, stm, fn, A);
   else st = launch_stage(events, 3, pick_tb<1>(ex->inter / 256), dim3(g_dn), kTbWaves * 64, stm, fn, A);
   if (st != TQ_OK) return st;
   const int64_t nout = t * (ex->hidden / 4);
