@@ -367,8 +367,8 @@ tq_status tq_moe_grouped_noalloc(const tq_experts* ex, const float* x, int64_t t
  * gate/up kernel, then a down kernel with the requantization and the weighted combine
  * fused), TQ_MOE_PATH_VALU (dispatch + grouped VALU dot4 kernels), TQ_MOE_PATH_MFMA
  * (dispatch + grouped int8 MFMA kernels), TQ_MOE_PATH_MIXED (the automatic choice for
- * fewer than 1024 slots and more than 8 tokens: dispatch + one launch per projection
- * whose first workgroups run the 32-token MFMA tiles of the experts of 9 to 32 slots and
+ * fewer than 1024 slots and more than 2 tokens: dispatch + one launch per projection
+ * whose first workgroups run the 32-token MFMA tiles of the experts of 3 to 32 slots and
  * the others the grouped VALU tasks of the remaining experts); -1 if the arguments are
  * invalid. Host only, no device work. */
 #define TQ_MOE_PATH_T1 0

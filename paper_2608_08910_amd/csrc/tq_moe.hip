@@ -58,7 +58,7 @@ constexpr int64_t kMfmaMinSlots = 1024;  // automatic path choice: MFMA from thi
 // expert's task walks its tokens two at a time, every group's activation loads queued
 // behind the compute unit's weight loads; on MFMA its tokens share one pass over the
 // weights.
-constexpr int kHybMin = 8;
+constexpr int kHybMin = 2;  // (measured on MI355X: 2 and 3 best at 8 and 32 tokens per step)
 constexpr int kTbWaves = 4;  // waves per grouped VALU workgroup
 
 struct Layout {

@@ -101,14 +101,14 @@ def test_moe_decode_batch1_uniform(tq, oracle, experts_h4096):
 
 def test_moe_decode_batch32_zipf(tq, oracle, experts_h4096):
     """Batched decode: 32 tokens, top-8 with Zipf(1.1) expert popularity, seed 0, on the
-    mixed path (the experts of 9 to 32 slots on the 32-token MFMA kernel, the others on
+    mixed path (the experts of 3 to 32 slots on the 32-token MFMA kernel, the others on
     the grouped VALU kernel). Every slot's block sums bit-exact."""
     c = gen.CONFIGS[2]
     x = gen.activations(gen.SEED, 0, c["tokens"], c["hidden"])
     idx, w = gen.routing(gen.SEED, 0, c["tokens"], c["experts"], c["topk"], c["routing"])
     assert tq.tq_moe_path(experts_h4096, c["tokens"], c["topk"]) == tq.TQ_MOE_PATH_MIXED
     counts = np.bincount(idx.ravel(), minlength=c["experts"])
-    assert (counts > 8).any() and ((counts > 0) & (counts <= 8)).any()  # both kernels have experts
+    assert (counts > 2).any() and ((counts > 0) & (counts <= 2)).any()  # both kernels have experts
     announce("moe decode t=32 top-8 zipf")
     out, ws = run_moe(tq, experts_h4096, x, idx, w)
     get = oracle_pkg.expert_getter(gen.SEED, 0, c["hidden"], c["inter"], oracle)
