@@ -229,6 +229,27 @@ def test_moe_prefill_2048_paths_agree(tq, experts_h4096):
     torch.cuda.empty_cache()
 
 
+def test_moe_mixed_all_rank_ranges(tq, oracle):
+    """The mixed path with every rank range populated: expert 0 in all 40 tokens (more than
+    32 slots: VALU), experts 1-5 with 16 slots each (MFMA role), experts 6 and 7 with one
+    slot each (VALU, past the MFMA ranks); hidden 17 blocks (loads per lane rounded up from
+    3 to 4, ragged) and inter 9 blocks (ragged). Every token staged against the oracle
+    (debug run), and the one-launch production kernels bitwise equal to it."""
+    E, H, I, T, topk = 8, 256 * 17, 256 * 9, 40, 3
+    ex, logical = host_experts(tq, oracle, E, H, I, seed=71)
+    rng = np.random.default_rng(72)
+    x = rng.standard_normal((T, H)).astype(np.float32)
+    idx = np.array([[0, 1 + t % 5, 6 + t if t < 2 else 1 + (t + 2) % 5] for t in range(T)], np.int32)
+    counts = np.bincount(idx.ravel(), minlength=E)
+    assert counts[0] > 32 and (counts[1:6] > 2).all() and (counts[1:6] <= 32).all() and counts[6] == counts[7] == 1
+    w = rng.uniform(0.1, 1.0, (T, topk)).astype(np.float32)
+    assert tq.tq_moe_path(ex, T, topk) == tq.TQ_MOE_PATH_MIXED
+    announce("moe mixed path, all rank ranges")
+    out, ws = run_moe(tq, ex, x, idx, w)
+    check_moe(tq, oracle, ex, lambda e: logical[e], x, idx, w, out, ws, list(range(T)))
+    assert_debug_flag_neutral(tq, ex, x, idx, w, out)
+
+
 @pytest.mark.parametrize("E,H,I,T,topk", [(5, 512, 768, 150, 3), (4, 1280, 256, 70, 2)])
 def test_moe_mfma_forced_small(tq, oracle, E, H, I, T, topk):
     """The int8 MFMA expert path on host-packed experts: one expert spans several

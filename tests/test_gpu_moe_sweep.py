@@ -6,6 +6,7 @@ Same bar as test_gpu_moe.py (staged parity bit-exact where integer, the gate, up
 down block sums included, 1e-5 of the absolute terms where fp32)."""
 import numpy as np
 import pytest
+import torch
 
 from gpu_util import announce, check_moe, host_experts, run_moe
 
@@ -53,3 +54,7 @@ def test_moe_sweep(tq, oracle, i, E, H, I, T, topk, flags, skew):
     tokens = sorted(set([0, T // 2, T - 1]))
     check_moe(tq, oracle, ex, lambda e: logical[e], x, idx, w, out, ws, tokens)
     assert tq.tq_moe_status(ws, ex, T, topk) == 0
+    # the production kernels (no debug dump: on the mixed path one launch per projection)
+    # give bitwise the checked outputs
+    plain, _ = run_moe(tq, ex, x, idx, w, flags=flags, debug=False)
+    assert torch.equal(plain, out), "output changes with TQ_MOE_DEBUG_STAGES"

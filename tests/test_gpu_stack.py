@@ -68,6 +68,17 @@ def test_stack_43_layers_h7168_full_size(tq, oracle):
         staged_abs = (w64[:, :, None].abs() * yd.abs()).sum(1)
         ratio = ((outs[l].double() - staged).abs() / (staged_abs + 1e-30)).max().item()
         assert ratio <= 1e-5, f"layer {l}: out vs its slots' yd, worst {ratio:.3g} of the absolute terms"
+    # the first and last layers again without the debug dump: the one-launch mixed kernels
+    # (hidden 7168: 28 blocks a row, four loads per lane, the last partly past the row
+    # end) give bitwise the outputs of the debug run's separate VALU and MFMA kernels,
+    # which the oracle checks below
+    assert tq.tq_moe_path(layers[0], T, topk) == tq.TQ_MOE_PATH_MIXED
+    for l in (0, L - 1):
+        assert (np.bincount(idxs[l].ravel(), minlength=E) > 2).any()  # the MFMA role has experts
+        plain = torch.empty_like(outs[l])
+        tq.tq_moe_grouped(layers[l], xd[l], idd[l], wd[l], plain, tq.moe_workspace(layers[l], T, topk))
+        torch.cuda.synchronize()
+        assert torch.equal(plain, outs[l]), f"layer {l}: output changes with TQ_MOE_DEBUG_STAGES"
     for l, tokens in ((0, [0, 5]), (L - 1, [3, 7])):
         announce(f"stack oracle layer {l} tokens {tokens}")
         get = oracle_pkg.expert_getter(gen.SEED, l, H, I, oracle)
