@@ -1680,17 +1680,17 @@ static tq_status empty_stage(void* const* events, int stage, hipStream_t st, con
 // experts of at most kMTs slots): the first is bound by MFMA issue and LDS operand reads,
 // the second by its weight stream, so the second runs beside the first on a stream the
 // library owns (one per device, default priority), forked from the caller's stream and
-// joined back to it by events. It is created by the first grouped MFMA call on a device
-// that is not being captured and may allocate (tq_moe_grouped_noalloc uses it only once
-// it exists); until then, or if creating it failed, both launches run in order on the
-// caller's stream. `mu` serializes the fork-launch-join sequences of
-// callers on different host threads, which share the two events.
+// joined back to it by events (the mixed path's debug instances use it too; its
+// production kernels run as one launch). It is created by the first such call on a
+// device that is not being captured and may allocate (tq_moe_grouped_noalloc uses it
+// only once it exists); until then, or if creating it failed, both launches run in order
+// on the caller's stream. `mu` serializes the fork-launch-join sequences of callers on
+// different host threads, which share the two events.
 struct SideStream {
   std::mutex mu;
   bool tried = false;
   hipStream_t s = nullptr;
   hipEvent_t fork = nullptr, join = nullptr;
-  int cus = 0;  // compute units of the device
 };
 static SideStream g_side[kMaxDevices];
 
@@ -1710,8 +1710,7 @@ static SideStream* side_stream(hipStream_t st, bool may_create) {
       return nullptr;  // (no stream or event is created inside a capture)
     }
     ss.tried = true;
-    const bool ok = hipDeviceGetAttribute(&ss.cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-                    ss.cus >= 8 && hipStreamCreateWithFlags(&ss.s, hipStreamNonBlocking) == hipSuccess &&
+    const bool ok = hipStreamCreateWithFlags(&ss.s, hipStreamNonBlocking) == hipSuccess &&
                     hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming) == hipSuccess &&
                     hipEventCreateWithFlags(&ss.join, hipEventDisableTiming) == hipSuccess;
     if (!ok) {
@@ -1904,7 +1903,7 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   // (the mixed path runs one launch per projection; only its debug instances, kept out
   // of that launch, take the side stream)
   SideStream* ss = mfma || (mixed && debug) ? side_stream(stm, may_allocate) : nullptr;
-  const int64_t big_cap = ss ? std::max(8, ss->cus * 5 / 8 / 8 * 8) : TQ_MFMA_GRID;
+  const int64_t big_cap = ss ? std::max(8, device_cus() * 5 / 8 / 8 * 8) : TQ_MFMA_GRID;
   const unsigned g_mgu = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mgu, big_cap);
   const unsigned g_mdn = (unsigned)std::min<int64_t>(max_tiles * A.tiles_mdn, big_cap);
   // (one tile per expert of at most kMTs slots)
