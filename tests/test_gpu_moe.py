@@ -250,6 +250,27 @@ def test_moe_mixed_all_rank_ranges(tq, oracle):
     assert_debug_flag_neutral(tq, ex, x, idx, w, out)
 
 
+def test_moe_mixed_boundary_counts(tq, oracle):
+    """The mixed path's rank ranges at their bounds: experts of exactly 33 slots (VALU),
+    32, 28 and 3 (MFMA role), 2 and 1 (VALU); ragged rows (3 and 5 blocks). Every token
+    staged against the oracle, and the production kernels bitwise equal to the debug run."""
+    E, H, I, T, topk = 8, 256 * 3, 256 * 5, 33, 3
+    ex, logical = host_experts(tq, oracle, E, H, I, seed=81)
+    rng = np.random.default_rng(82)
+    x = rng.standard_normal((T, H)).astype(np.float32)
+    col1 = [1 if t < 32 else 2 for t in range(T)]
+    col2 = [2 if t < 2 else (3 if t < 4 else (4 if t == 4 else 5)) for t in range(T)]
+    idx = np.array([[0, col1[t], col2[t]] for t in range(T)], np.int32)
+    assert all(len(set(r)) == topk for r in idx.tolist())
+    assert np.bincount(idx.ravel(), minlength=E).tolist() == [33, 32, 3, 2, 1, 28, 0, 0]
+    w = rng.uniform(0.1, 1.0, (T, topk)).astype(np.float32)
+    assert tq.tq_moe_path(ex, T, topk) == tq.TQ_MOE_PATH_MIXED
+    announce("moe mixed path, boundary counts")
+    out, ws = run_moe(tq, ex, x, idx, w)
+    check_moe(tq, oracle, ex, lambda e: logical[e], x, idx, w, out, ws, list(range(T)))
+    assert_debug_flag_neutral(tq, ex, x, idx, w, out)
+
+
 @pytest.mark.parametrize("E,H,I,T,topk", [(5, 512, 768, 150, 3), (4, 1280, 256, 70, 2)])
 def test_moe_mfma_forced_small(tq, oracle, E, H, I, T, topk):
     """The int8 MFMA expert path on host-packed experts: one expert spans several
