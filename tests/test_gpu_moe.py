@@ -250,6 +250,41 @@ def test_moe_mixed_all_rank_ranges(tq, oracle):
     assert_debug_flag_neutral(tq, ex, x, idx, w, out)
 
 
+@pytest.mark.parametrize("T,flags", [(1, 0), (24, 1), (40, 0), (40, 2)])
+def test_moe_timed_matches_untimed(tq, oracle, T, flags):
+    """tq_moe_grouped_timed on every path (single token, forced VALU, mixed, forced MFMA
+    with its two launches on two streams): the output is bitwise that of tq_moe_grouped,
+    every kernel stage of the path takes a positive time, the empty ones none below zero,
+    and the stages follow one another."""
+    E, H, I, topk = 16, 1024, 512, 4
+    ex, _ = host_experts(tq, oracle, E, H, I, seed=95)
+    rng = np.random.default_rng(96)
+    x = torch.from_numpy(rng.standard_normal((T, H)).astype(np.float32)).cuda()
+    idx = torch.from_numpy(np.stack([rng.choice(E, topk, replace=False) for _ in range(T)]).astype(np.int32)).cuda()
+    w = torch.from_numpy(rng.uniform(0.1, 1.0, (T, topk)).astype(np.float32)).cuda()
+    path = tq.tq_moe_path(ex, T, topk, flags)
+    assert path == {(1, 0): tq.TQ_MOE_PATH_T1, (24, 1): tq.TQ_MOE_PATH_VALU, (40, 0): tq.TQ_MOE_PATH_MIXED,
+                    (40, 2): tq.TQ_MOE_PATH_MFMA}[(T, flags)]
+    ws = tq.moe_workspace(ex, T, topk)
+    announce(f"moe timed entry point T={T} flags={flags}")
+    ref = torch.empty((T, H), dtype=torch.float32, device="cuda")
+    tq.tq_moe_grouped(ex, x, idx, w, ref, ws, flags)
+    n = tq.tq_moe_stage_count()
+    names = [tq.tq_moe_stage_name(i) for i in range(n)]
+    for rep in range(2):  # (the second call reuses the events)
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(2 * n)]
+        out = torch.full((T, H), float("nan"), device="cuda")
+        tq.tq_moe_grouped_timed(ex, x, idx, w, out, ws, evs, flags)
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref), f"call {rep}"
+        kernel_stages = {"gate_up", "down"} if path == tq.TQ_MOE_PATH_T1 else set(names)
+        for i, name in enumerate(names):
+            ms = evs[2 * i].elapsed_time(evs[2 * i + 1])
+            assert (ms > 0) if name in kernel_stages else (ms >= 0), (name, ms)
+            if i > 0:
+                assert evs[2 * (i - 1) + 1].elapsed_time(evs[2 * i]) >= 0, f"stage {name} starts before its predecessor ends"
+
+
 def test_moe_mixed_boundary_counts(tq, oracle):
     """The mixed path's rank ranges at their bounds: experts of exactly 33 slots (VALU),
     32, 28 and 3 (MFMA role), 2 and 1 (VALU); ragged rows (3 and 5 blocks). Every token
