@@ -316,7 +316,7 @@ tq_status tq_gemv_mx_timed(const tq_mat_mx* w, const int8_t* q, const float* d, 
  * workspace must be ordered on one stream.
  * flags: 0 (automatic path choice), or TQ_MOE_FORCE_VALU / TQ_MOE_FORCE_MFMA to pin
  * the per-expert path (VALU dot4 for few tokens per expert, int8 MFMA for many; the
- * automatic choice mixes the two below 1024 slots, see tq_moe_path).
+ * automatic choice mixes the two below 2048 slots, see tq_moe_path).
  * Single-token steps (t == 1, topk <= 8, topk * inter <= 16384) take a path of their
  * own unless TQ_MOE_FORCE_MFMA is given (tq_moe_path). The grouped paths address the
  * quantized activations with 32-bit offsets: TQ_ERR_INVALID if t * topk * max(hidden,
@@ -367,10 +367,10 @@ tq_status tq_moe_grouped_noalloc(const tq_experts* ex, const float* x, int64_t t
  * gate/up kernel, then a down kernel with the requantization and the weighted combine
  * fused), TQ_MOE_PATH_VALU (dispatch + grouped VALU dot4 kernels), TQ_MOE_PATH_MFMA
  * (dispatch + grouped int8 MFMA kernels), TQ_MOE_PATH_MIXED (the automatic choice for
- * fewer than 1024 slots and more than 2 tokens: dispatch + one launch per projection
- * whose first workgroups run the 32-token MFMA tiles of the experts of 3 to 32 slots and
- * the others the grouped VALU tasks of the remaining experts); -1 if the arguments are
- * invalid. Host only, no device work. */
+ * fewer than 2048 slots and more than 2 tokens: dispatch + one launch per projection
+ * whose first workgroups run the 32-token MFMA tiles of the experts of more than 2 slots
+ * and the others the grouped VALU tasks of the remaining experts); -1 if the arguments
+ * are invalid. Host only, no device work. */
 #define TQ_MOE_PATH_T1 0
 #define TQ_MOE_PATH_VALU 1
 #define TQ_MOE_PATH_MFMA 2

@@ -38,7 +38,7 @@ static const char* const kStageNames[kNumStages] = {"prologue", "gate_up", "requ
 // Control words at the start of the workspace.
 enum Ctrl {
   kFlags = 0, kNActive = 1, kTasksGU = 2, kTasksDn = 3, kNValid = 4, kTasksMGU = 5, kTasksMDn = 6,
-  kTSmall = 7, kTasksMGUs = 8, kTasksMDns = 9, kTSingle = 10, kR32 = 11, kRSkip = 12, kCtrlWords = 64
+  kTSmall = 7, kTasksMGUs = 8, kTasksMDns = 9, kTSingle = 10, kRSkip = 11, kCtrlWords = 64
 };
 
 constexpr int kMT = 128;     // tokens per MFMA task tile (eight 16-row MFMA tiles)
@@ -51,7 +51,7 @@ constexpr int kMStages = 3;  // token-tile blocks in flight in LDS per MFMA work
 constexpr int kMTs = 32;
 constexpr int kMWavesS = 4;
 constexpr int kMNs = 16 * kMWavesS;
-constexpr int64_t kMfmaMinSlots = 1024;  // automatic path choice: MFMA from this many slots
+constexpr int64_t kMfmaMinSlots = 2048;  // automatic path choice: MFMA from this many slots
 // Mixed path (automatic choice below kMfmaMinSlots slots, more than kHybMin tokens): the
 // experts of more than kHybMin and at most kMTs slots run on the kMTs-token MFMA kernel
 // beside the grouped VALU kernel, which takes the others. On the VALU kernel such an
@@ -62,7 +62,7 @@ constexpr int kHybMin = 2;  // (measured on MI355X: 2 and 3 best at 8 and 32 tok
 constexpr int kTbWaves = 4;  // waves per grouped VALU workgroup
 
 struct Layout {
-  size_t ctrl, active, act_off, tt_off, tile_exp, slot_list, xq, xd, xb, h, hq, hd, hb, yd, total;
+  size_t ctrl, active, act_off, tt_off, tile_exp, tt32_off, tile32_exp, slot_list, xq, xd, xb, h, hq, hd, hb, yd, total;
   // debug stage dump (TQ_MOE_DEBUG_STAGES), past `total`: g and u per slot, and the exact
   // block sums of gate, up (per slot, row, hidden block) and down (per slot, row, inter block)
   size_t dg, du, dgs, dus, dds, total_dbg;
@@ -84,6 +84,8 @@ static Layout make_layout(int n_experts, int hidden, int inter, int64_t t, int t
   L.act_off = take(((size_t)n_experts + 1) * 4);
   L.tt_off = take(((size_t)n_experts + 1) * 4);
   L.tile_exp = take((S / kMT + (size_t)n_experts + 1) * 4);
+  L.tt32_off = take(((size_t)n_experts + 1) * 4);
+  L.tile32_exp = take((S / kMTs + (size_t)n_experts + 1) * 4);
   L.slot_list = take(S * 4);
   L.xq = take((size_t)t * hidden);
   L.xd = take((size_t)t * (hidden / 256) * 4);
@@ -161,6 +163,8 @@ struct MoeArgs {
   int32_t* act_off;
   int32_t* tt_off;  // per active expert: first token tile (kMT tokens) of the MFMA path
   int32_t* tile_exp;  // per token tile of the MFMA path: its active expert's rank
+  int32_t* tt32_off;    // mixed path: per active expert, its first kMTs-token tile
+  int32_t* tile32_exp;  // mixed path: per kMTs-token tile (experts of more than hyb slots), the rank
   int32_t* slot_list;
   int8_t* xq;
   float* xd;
@@ -198,7 +202,7 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
   __shared__ __attribute__((aligned(16))) int s_base[kMaxExperts];  // rank key, then the slot cursor
   __shared__ int s_ebr[kMaxExperts];   // expert of each rank
   __shared__ int s_scan[256], s_scan2[256];
-  __shared__ int s_nact, s_bad, s_tsmall, s_tsingle, s_r32, s_rhot, s_thot;
+  __shared__ int s_nact, s_bad, s_tsmall, s_tsingle, s_rhot;
   const int tid = threadIdx.x, E = A.n_experts;
   const int64_t S = A.t * A.topk;
   for (int e = tid; e < E; e += 256) s_cnt[e] = 0;
@@ -207,9 +211,7 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
     s_nact = 0;
     s_tsmall = 0x7fffffff;
     s_tsingle = 0x7fffffff;
-    s_r32 = 0x7fffffff;
     s_rhot = 0x7fffffff;
-    s_thot = 0x7fffffff;
   }
   __syncthreads();
   // The slots' expert ids, kSB per thread at a time, all requested before any is used
@@ -286,11 +288,15 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
   // exclusive scan of the slot counts in rank order, contiguous ranks per thread
   const int per = (n_active + 255) / 256;
   const int r0 = min(n_active, tid * per), r1 = min(n_active, r0 + per);
-  // (and of the kMT-token tiles of the MFMA path)
+  // (and of the token tiles: kMT-token tiles of every expert for the MFMA path; on the
+  // mixed path (t32) instead the kMTs-token tiles of the experts of more than hyb slots,
+  // which its MFMA role takes, in the lists tile32_exp / tt32_off)
+  const bool t32 = by_count && A.hyb > 0;
+  const auto ntiles = [&](int c) { return t32 ? (c > A.hyb ? (c + kMTs - 1) / kMTs : 0) : (c + kMT - 1) / kMT; };
   int ns = 0, nt = 0;
   for (int r = r0; r < r1; ++r) {
     ns += s_cnt[s_ebr[r]];
-    nt += (s_cnt[s_ebr[r]] + kMT - 1) / kMT;
+    nt += ntiles(s_cnt[s_ebr[r]]);
   }
   s_scan[tid] = ns;
   s_scan2[tid] = nt;
@@ -313,29 +319,26 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
     // store each, where an atomic minimum over the tail would queue on one LDS word).
     if (by_count) {
       const int c = s_cnt[e], cprev = r > 0 ? s_cnt[s_ebr[r - 1]] : 0x7fffffff;
-      if (c <= kMTs && cprev > kMTs) {
-        s_tsmall = tpos;
-        s_r32 = r;
-      }
+      if (c <= kMTs && cprev > kMTs) s_tsmall = tpos;
       if (c <= kMT && cprev > kMT) s_tsingle = tpos;
-      if (c <= A.hyb && cprev > A.hyb) {
-        s_rhot = r;
-        s_thot = tpos;
-      }
+      if (c <= A.hyb && cprev > A.hyb) s_rhot = r;
     }
     A.active[r] = e;
     A.act_off[r] = pos;
-    A.tt_off[r] = tpos;
     s_base[e] = pos;  // key no longer needed: becomes the expert's slot cursor
     pos += s_cnt[e];
-    for (const int t1 = tpos + (s_cnt[e] + kMT - 1) / kMT; tpos < t1; ++tpos) A.tile_exp[tpos] = r;
+    const int n_t = ntiles(s_cnt[e]);
+    int32_t* const tt = t32 ? A.tt32_off : A.tt_off;
+    int32_t* const te = t32 ? A.tile32_exp : A.tile_exp;
+    if (n_t > 0 || !t32) tt[r] = tpos;
+    for (const int t1 = tpos + n_t; tpos < t1; ++tpos) te[tpos] = r;
   }
   __syncthreads();
   if (tid == 255) {
     const int n_valid = s_scan[255], n_tiles = s_scan2[255];
     const int t_small = min(s_tsmall, n_tiles);
     A.act_off[n_active] = n_valid;
-    A.tt_off[n_active] = n_tiles;
+    (t32 ? A.tt32_off : A.tt_off)[n_active] = n_tiles;
     A.ctrl[kNActive] = n_active;
     A.ctrl[kNValid] = n_valid;
     A.ctrl[kTasksGU] = n_active * A.tiles_gu;
@@ -346,20 +349,17 @@ __global__ __launch_bounds__(256) void k_moe_prologue(const float* __restrict__ 
     A.ctrl[kTSingle] = min(s_tsingle, t_small);
     A.ctrl[kTasksMGUs] = (n_tiles - t_small) * A.tiles_mgus;
     A.ctrl[kTasksMDns] = (n_tiles - t_small) * A.tiles_mdns;
-    A.ctrl[kR32] = 0;
     A.ctrl[kRSkip] = 0;
     if (A.hyb > 0) {
-      // ranks r32 .. rhot - 1 (more than hyb, at most kMTs slots: one tile each, tiles
-      // t_small .. t_hot - 1) go to the small-tile MFMA launch; the VALU kernel takes
-      // ranks 0 .. r32 - 1 and rhot .. n_active - 1
-      const int r32 = min(s_r32, n_active), rhot = max(r32, min(s_rhot, n_active));
-      const int t_hot = max(t_small, min(s_thot, n_tiles));
-      A.ctrl[kR32] = r32;
-      A.ctrl[kRSkip] = rhot - r32;
-      A.ctrl[kTasksGU] = (n_active - (rhot - r32)) * A.tiles_gu;
-      A.ctrl[kTasksDn] = (n_active - (rhot - r32)) * A.tiles_dn;
-      A.ctrl[kTasksMGUs] = (t_hot - t_small) * A.tiles_mgus;
-      A.ctrl[kTasksMDns] = (t_hot - t_small) * A.tiles_mdns;
+      // ranks 0 .. rhot - 1 (more than hyb slots) go to the MFMA role in kMTs-token tiles
+      // (the list tile32_exp, n_tiles of them); the VALU role takes ranks rhot on. (Not
+      // by count: no MFMA tiles, every rank on the VALU role.)
+      const int rhot = t32 ? min(s_rhot, n_active) : 0;
+      A.ctrl[kRSkip] = rhot;
+      A.ctrl[kTasksGU] = (n_active - rhot) * A.tiles_gu;
+      A.ctrl[kTasksDn] = (n_active - rhot) * A.tiles_dn;
+      A.ctrl[kTasksMGUs] = t32 ? n_tiles * A.tiles_mgus : 0;
+      A.ctrl[kTasksMDns] = t32 ? n_tiles * A.tiles_mdns : 0;
     }
     A.ctrl[kFlags] = s_bad ? 1 : 0;
   }
@@ -523,10 +523,9 @@ __device__ __forceinline__ void tb_acts_compute(const MoeArgs& A, const int (&wc
 // lane 0 gets the range's start, lane 1 its end, lane 2 the expert id. Kept in a vector
 // register and read out lane by lane only where used, so that a fetch issued one task
 // ahead is not waited for at once.
-// (on the mixed path the VALU kernel's task ranks skip the rskip ranks from r32 on)
-__device__ __forceinline__ int tb_task_fetch(const MoeArgs& A, int task, int tiles, int lane, int r32, int rskip) {
-  int a = task / tiles;
-  a += a >= r32 ? rskip : 0;
+// (on the mixed path the VALU role's task ranks start at rskip, past the MFMA role's)
+__device__ __forceinline__ int tb_task_fetch(const MoeArgs& A, int task, int tiles, int lane, int rskip) {
+  const int a = task / tiles + rskip;
   return *(lane == 2 ? A.active + a : A.act_off + a + (lane & 1));
 }
 struct TbTask {
@@ -557,7 +556,7 @@ __device__ __forceinline__ void tb_run(const MoeArgs& A, int bid, int nblk) {
   const int kb = K / 256;
   const int tiles = NMAT == 2 ? A.tiles_gu : A.tiles_dn;
   const int n_tasks = A.ctrl[NMAT == 2 ? kTasksGU : kTasksDn];
-  const int r32 = A.ctrl[kR32], rskip = A.ctrl[kRSkip];
+  const int rskip = A.ctrl[kRSkip];
   const uint32_t arows = (uint32_t)(NMAT == 2 ? A.t : A.t * A.topk);
   const __amdgpu_buffer_rsrc_t qr = make_rsrc(NMAT == 2 ? A.xq : A.hq, arows * (uint32_t)K);
   const __amdgpu_buffer_rsrc_t dr = make_rsrc(NMAT == 2 ? A.xd : A.hd, arows * (uint32_t)kb * 4u);
@@ -566,7 +565,7 @@ __device__ __forceinline__ void tb_run(const MoeArgs& A, int bid, int nblk) {
   if (task >= n_tasks) return;
   // A task's scalars and slot list are fetched while the task before it runs (at its own
   // start each would be another round trip ahead of the weight loads).
-  int tv = tb_task_fetch(A, task, tiles, lane, r32, rskip);
+  int tv = tb_task_fetch(A, task, tiles, lane, rskip);
   int sv;
   {
     const TbTask t0 = tb_task(tv, task, tiles);
@@ -575,7 +574,7 @@ __device__ __forceinline__ void tb_run(const MoeArgs& A, int bid, int nblk) {
   for (; task < n_tasks; task += nblk) {
     const TbTask cur = tb_task(tv, task, tiles);
     const int task_next = min(task + nblk, n_tasks - 1);
-    const int tv_next = tb_task_fetch(A, task_next, tiles, lane, r32, rskip);
+    const int tv_next = tb_task_fetch(A, task_next, tiles, lane, rskip);
     const int64_t e = cur.e;
     const int off = cur.off, cnt = cur.cnt;
     // rows past N (a ragged last tile) load the last row and write nothing
@@ -787,11 +786,14 @@ constexpr int kMfmaLoadsPerBlock = PW + 3 * NMAT;
 // DN2: the down projection with two 16-row tiles of the matrix per wave, run as the two
 // "matrices" of the NMAT = 2 path (the second's resource starts 16 rows on), so that each
 // token operand read from LDS feeds two MFMAs, as in gate/up.
+// T32: the mixed path's MFMA role, whose tasks walk the kMTs-token tile list (tile32_exp,
+// every tile of the experts of more than hyb slots) instead of the kMT-token one.
 // `bid` of `nblk` as in tb_run (the whole grid for k_moe_mfma, the first workgroups of
 // k_mixed).
-template <int NMAT, int MT, int WAVES, bool SMALL, bool DBG, bool DN2>
+template <int NMAT, int MT, int WAVES, bool SMALL, bool DBG, bool DN2, bool T32>
 __device__ __forceinline__ void mfma_run(const MoeArgs& A, int bid, int nblk) {
   static_assert(!DN2 || NMAT == 2, "DN2 runs two row tiles as two matrices");
+  static_assert(!T32 || (SMALL && MT == kMTs), "the kMTs-token tile list feeds the small-tile instance");
   constexpr bool GU = NMAT == 2 && !DN2;  // the gate/up projection
   constexpr int RW = DN2 ? 32 : 16;       // weight rows per wave
   constexpr int MN = RW * WAVES;          // weight rows per task
@@ -817,7 +819,7 @@ __device__ __forceinline__ void mfma_run(const MoeArgs& A, int bid, int nblk) {
   const int kb = K / 256;
   const int RT = SMALL ? (GU ? A.tiles_mgus : A.tiles_mdns) : (GU ? A.tiles_mgu : A.tiles_mdn);
   const int n_tasks = ld_uniform(A.ctrl + (SMALL ? (GU ? kTasksMGUs : kTasksMDns) : (GU ? kTasksMGU : kTasksMDn)));
-  const int tile0 = SMALL ? ld_uniform(A.ctrl + kTSmall) : 0;
+  const int tile0 = SMALL && !T32 ? ld_uniform(A.ctrl + kTSmall) : 0;
   const int8_t* qsrc = GU ? A.xq : A.hq;
   const float* dsrc = GU ? A.xd : A.hd;
   // Tiles before t1 (experts of several tiles): task = tile * RT + rtile, so one row tile
@@ -841,11 +843,12 @@ __device__ __forceinline__ void mfma_run(const MoeArgs& A, int bid, int nblk) {
       tile = t1 + x + 8 * (i / RT);
       rtile = i - (i / RT) * RT;
     }
-    const int a = ld_uniform(A.tile_exp + tile);
-    const int ttile = tile - ld_uniform(A.tt_off + a);
+    const int a = ld_uniform((T32 ? A.tile32_exp : A.tile_exp) + tile);
+    const int ttile = tile - ld_uniform((T32 ? A.tt32_off : A.tt_off) + a);
     const int64_t e = ld_uniform(A.active + a);
     const int off = ld_uniform(A.act_off + a), cnt = ld_uniform(A.act_off + a + 1) - off;
-    const int m0 = ttile * kMT, nvalid = min(MT, cnt - m0);  // (SMALL: one tile, ttile 0)
+    // (SMALL: one tile, ttile 0, except on the T32 list)
+    const int m0 = ttile * (T32 ? MT : kMT), nvalid = min(MT, cnt - m0);
     const int nsub = (nvalid + 15) / 16;  // 16-token sub-tiles holding valid tokens
     const int ncomp = 2 * ((nsub + 1) / 2);  // sub-tiles computed (in pairs)
     const int row0 = rtile * MN + wv * RW;  // N is a multiple of 256: all the wave's rows exist
@@ -1091,11 +1094,11 @@ __device__ __forceinline__ void mfma_run(const MoeArgs& A, int bid, int nblk) {
   }
 }
 
-template <int NMAT, int MT, int WAVES, bool SMALL, bool DBG, bool DN2 = false>
+template <int NMAT, int MT, int WAVES, bool SMALL, bool DBG, bool DN2 = false, bool T32 = false>
 // (the small-tile gate/up instance is held to the registers of three waves per SIMD)
 __global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(SMALL && NMAT == 2 ? 3 : 1))) void k_moe_mfma(
     MoeArgs A) {
-  mfma_run<NMAT, MT, WAVES, SMALL, DBG, DN2>(A, blockIdx.x, gridDim.x);
+  mfma_run<NMAT, MT, WAVES, SMALL, DBG, DN2, T32>(A, blockIdx.x, gridDim.x);
 }
 
 // The mixed path's projection in one launch: workgroups 0 .. n_mfma - 1 run the kMTs-token
@@ -1111,7 +1114,7 @@ __global__ __launch_bounds__(kTbWaves * 64) __attribute__((amdgpu_waves_per_eu(N
 k_mixed(MoeArgs A, int n_mfma) {
   static_assert(kTbWaves == kMWavesS, "both roles run four-wave workgroups");
   if ((int)blockIdx.x < n_mfma)
-    mfma_run<2, kMTs, kMWavesS, true, false, NMAT == 1>(A, blockIdx.x, n_mfma);
+    mfma_run<2, kMTs, kMWavesS, true, false, NMAT == 1, true>(A, blockIdx.x, n_mfma);
   else
     tb_run<NMAT, NL, RPW, NT, NTL, kTbWaves, RAGGED>(A, blockIdx.x - n_mfma, gridDim.x - n_mfma);
 }
@@ -1833,6 +1836,8 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
   A.act_off = reinterpret_cast<int32_t*>(base + L.act_off);
   A.tt_off = reinterpret_cast<int32_t*>(base + L.tt_off);
   A.tile_exp = reinterpret_cast<int32_t*>(base + L.tile_exp);
+  A.tt32_off = reinterpret_cast<int32_t*>(base + L.tt32_off);
+  A.tile32_exp = reinterpret_cast<int32_t*>(base + L.tile32_exp);
   A.slot_list = reinterpret_cast<int32_t*>(base + L.slot_list);
   A.xq = reinterpret_cast<int8_t*>(base + L.xq);
   A.xd = reinterpret_cast<float*>(base + L.xd);
@@ -1926,7 +1931,7 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
                       A, n_mgus);
   else if (mixed)  // (debug: the VALU kernel on the caller's stream, the MFMA tiles beside it)
     st = launch_pair(events, 1, ss, pick_tb<2>(ex->hidden / 256), dim3(g_gu), kTbWaves * 64,
-                     k_moe_mfma<2, kMTs, kMWavesS, true, true>, dim3(g_mgus), kMWavesS * 64, stm, fn, A);
+                     k_moe_mfma<2, kMTs, kMWavesS, true, true, false, true>, dim3(g_mgus), kMWavesS * 64, stm, fn, A);
   else st = launch_stage(events, 1, pick_tb<2>(ex->hidden / 256), dim3(g_gu), kTbWaves * 64, stm, fn, A);
   if (st != TQ_OK) return st;
   if ((st = launch_stage(events, 2, k_moe_requant, dim3((unsigned)((hblocks + 31) / 32)), 256, stm, fn, A, hblocks)) !=
@@ -1943,7 +1948,7 @@ static tq_status moe_run(const tq_experts* ex, const float* x, int64_t t, const 
                       A, n_mdns);
   else if (mixed)
     st = launch_pair(events, 3, ss, pick_tb<1>(ex->inter / 256), dim3(g_dn), kTbWaves * 64,
-                     k_moe_mfma<2, kMTs, kMWavesS, true, true, true>, dim3(g_mdns), kMWavesS * 64, stm, fn, A);
+                     k_moe_mfma<2, kMTs, kMWavesS, true, true, true, true>, dim3(g_mdns), kMWavesS * 64, stm, fn, A);
   else st = launch_stage(events, 3, pick_tb<1>(ex->inter / 256), dim3(g_dn), kTbWaves * 64, stm, fn, A);
   if (st != TQ_OK) return st;
   const int64_t nout = t * (ex->hidden / 4);

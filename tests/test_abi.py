@@ -388,8 +388,8 @@ def test_moe_path_choice():
     assert path(d, 32, 8, tq.TQ_MOE_FORCE_VALU) == tq.TQ_MOE_PATH_VALU
     assert path(d, 32, 8, tq.TQ_MOE_FORCE_MFMA) == tq.TQ_MOE_PATH_MFMA
     assert path(d, 2, 8) == tq.TQ_MOE_PATH_VALU  # (2 tokens: no expert has more than 2 slots)
-    assert path(d, 3, 8) == tq.TQ_MOE_PATH_MIXED and path(d, 127, 8) == tq.TQ_MOE_PATH_MIXED
-    assert path(d, 128, 8) == tq.TQ_MOE_PATH_MFMA  # 1024 slots
+    assert path(d, 3, 8) == tq.TQ_MOE_PATH_MIXED and path(d, 255, 8) == tq.TQ_MOE_PATH_MIXED
+    assert path(d, 256, 8) == tq.TQ_MOE_PATH_MFMA  # 2048 slots
     assert path(d, 2048, 8) == tq.TQ_MOE_PATH_MFMA
     assert path(d, 2048, 8, tq.TQ_MOE_FORCE_VALU) == tq.TQ_MOE_PATH_VALU
     deep = _experts_desc(E=256, H=7168, I=2048)

@@ -230,11 +230,12 @@ def test_moe_prefill_2048_paths_agree(tq, experts_h4096):
 
 
 def test_moe_mixed_all_rank_ranges(tq, oracle):
-    """The mixed path with every rank range populated: expert 0 in all 40 tokens (more than
-    32 slots: VALU), experts 1-5 with 16 slots each (MFMA role), experts 6 and 7 with one
-    slot each (VALU, past the MFMA ranks); hidden 17 blocks (loads per lane rounded up from
-    3 to 4, ragged) and inter 9 blocks (ragged). Every token staged against the oracle
-    (debug run), and the one-launch production kernels bitwise equal to it."""
+    """The mixed path with both roles populated: expert 0 in all 40 tokens (more than 32
+    slots: two 32-token tiles of the MFMA role), experts 1-5 with 16 slots each (one tile
+    each), experts 6 and 7 with one slot each (VALU role); hidden 17 blocks (loads per lane
+    rounded up from 3 to 4, ragged) and inter 9 blocks (ragged). Every token staged
+    against the oracle (debug run), and the one-launch production kernels bitwise equal
+    to it."""
     E, H, I, T, topk = 8, 256 * 17, 256 * 9, 40, 3
     ex, logical = host_experts(tq, oracle, E, H, I, seed=71)
     rng = np.random.default_rng(72)
@@ -286,9 +287,10 @@ def test_moe_timed_matches_untimed(tq, oracle, T, flags):
 
 
 def test_moe_mixed_boundary_counts(tq, oracle):
-    """The mixed path's rank ranges at their bounds: experts of exactly 33 slots (VALU),
-    32, 28 and 3 (MFMA role), 2 and 1 (VALU); ragged rows (3 and 5 blocks). Every token
-    staged against the oracle, and the production kernels bitwise equal to the debug run."""
+    """The mixed path's roles at their bounds: experts of exactly 33 slots (two 32-token
+    tiles, the second with one token), 32, 28 and 3 (one tile) on the MFMA role, 2 and 1
+    on the VALU role; ragged rows (3 and 5 blocks). Every token staged against the oracle,
+    and the production kernels bitwise equal to the debug run."""
     E, H, I, T, topk = 8, 256 * 3, 256 * 5, 33, 3
     ex, logical = host_experts(tq, oracle, E, H, I, seed=81)
     rng = np.random.default_rng(82)

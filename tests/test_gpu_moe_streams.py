@@ -126,8 +126,8 @@ def test_two_host_threads_own_streams(tq):
     ex = synth_experts(tq, 41, 0, E, H, I)
     n = 3
     data = [make_inputs(42 + k, n) for k in range(2)]
-    assert tq.tq_moe_path(ex, T, TOPK, 0) == tq.TQ_MOE_PATH_MFMA
     F = tq.TQ_MOE_FORCE_MFMA
+    assert tq.tq_moe_path(ex, T, TOPK, F) == tq.TQ_MOE_PATH_MFMA
     ws0 = tq.moe_workspace(ex, T, TOPK)
     ref = []
     for k in range(2):
