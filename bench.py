@@ -803,7 +803,7 @@ def run_moe(args, wl, cfg):
         rpw = 8 if nl_gu == 1 else (4 if nl_gu == 2 else (2 if nl_gu <= 4 else 1))
         nt = 2 if nl_gu <= 2 else 1  # tokens per group of the grouped VALU kernel (first, later)
         # the MFMA stage is two launches: 128-token tiles, then the experts of at most 32 slots
-        gu_kernel = ("k_moe_mfma<2, 128, 8, false, false, false> + k_moe_mfma<2, 32, 4, true, false, false>" if mfma
+        gu_kernel = ("k_moe_mfma<2, 128, 8, false, false, false, false> + k_moe_mfma<2, 32, 4, true, false, false, false>" if mfma
                      else f"k_tb<2, {nl_gu}, {rpw}, {nt}, {nt}, 4, {ragged}>")
         if path == tq.TQ_MOE_PATH_MIXED:  # one launch: the VALU tasks and the 32-token MFMA tiles
             gu_kernel = mixed_kernel(2, H // 256)
@@ -836,7 +836,7 @@ def run_moe(args, wl, cfg):
     else:
         dn_bytes = n_distinct * matrix_bytes(H, I) + T * topk * (I + (I // 256) * 4) + T * topk * H * 4
         # (down: two 16-row tiles per wave, run as the kernel's two-matrix path)
-        dn_kernel = ("k_moe_mfma<2, 128, 8, false, false, true> + k_moe_mfma<2, 32, 4, true, false, true>" if mfma
+        dn_kernel = ("k_moe_mfma<2, 128, 8, false, false, true, false> + k_moe_mfma<2, 32, 4, true, false, true, false>" if mfma
                      else "k_tb<1, ...>")
         if path == tq.TQ_MOE_PATH_MIXED:
             dn_kernel = mixed_kernel(1, I // 256)
